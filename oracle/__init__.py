@@ -1,0 +1,18 @@
+"""fp64 CPU oracle for the DSTD-LIF layer (test infrastructure only).
+
+Only the test suite, ``__graft_entry__.smoke()`` and the CPU-baseline leg of
+``bench.py`` may import this package. It shares no code with the HIP library.
+"""
+from .oracle import (  # noqa: F401
+    build_oracle,
+    kernel,
+    kdstd,
+    dstd_events,
+    dstd_forward,
+    dstd_scan,
+    dstd_backward,
+    exact_forward,
+    conv_forward,
+    conv_backward,
+    num_threads,
+)

@@ -1,0 +1,639 @@
+/*
+ * dstd_oracle.c -- plain, slow, fp64 CPU oracle for the DSTD-LIF layer.
+ *
+ * TEST INFRASTRUCTURE ONLY. Nothing in the product path may link, load or call
+ * this file: only the test suite, the smoke check and the benchmark's CPU
+ * baseline leg use it. It shares no code, header, table or constant with the
+ * HIP library; it is written from the paper (Sakemi et al., "Scalable Training
+ * of Continuous-Time Spiking Neural Networks with Differentiable Spike-Time
+ * Discretization"):
+ *
+ *   LIF model and spike kernel K(t) ............ App. A, Eq. (LIF_model_TTFS),
+ *                                                  Table "tab:kernel" (row tau_v != tau_I)
+ *   exact spike time (sort + interval candidates) App. A, Eq. (timing_exact), Alg. 1
+ *   DSTD grid T_m = T_first + m*dt - t_offset .. App. B.1
+ *   DSTD event weights s_jm ..................... Eq. (DSTD_kernel), Table "tab:DSTD_kernels"
+ *   weighted events w^_im = sum_j w_ij s_jm ..... App. B.1 (definition of w^)
+ *   DSTD candidate times and min selection ...... Table "tab:timing_DSTD", Eq. (timing_DSTD)
+ *
+ * Every quantity is computed in double precision from its plain definition.
+ * Inputs are double; callers pass the float32 values the GPU sees, widened
+ * exactly, or fp64 values for finite-difference pins.
+ *
+ * Readings where the paper is silent (listed in the design notes):
+ *  - M intervals, M+1 grid points T_0..T_M; the grid is passed as (t0, dt, M),
+ *    the random t_offset of Alg. 2 is folded into t0 by the caller.
+ *  - Eq. (DSTD_kernel) is applied literally at the grid ends: an input in
+ *    [T_{-1}, T_0) keeps only its weight at T_0, an input in [T_M, T_{M+1})
+ *    keeps only its weight at T_M; everything else (including +inf = silent)
+ *    contributes nothing.
+ *  - The last candidate interval is [T_M, t_max) (t_max = +inf by default):
+ *    Eq. (timing_DSTD) leaves T_{M+1} undefined; the exact method's analogue
+ *    uses +inf for the interval after the last input.
+ *  - "Reaches the threshold" means v >= V_th; the interval is half-open.
+ *  - The general kernel is symmetric in (tau_v, tau_I); tau_v == tau_I is not
+ *    handled here (the equal-tau row of the tables is a different formula).
+ *
+ * The only non-closed-form step is the root of v^(t) = V_th inside an
+ * interval for general (tau_v, tau_I) (Table "tab:timing_DSTD" gives closed
+ * forms only for special ratios). Inside one interval v^ is a combination of
+ * two exponentials, so its derivative has at most one zero; the interval is
+ * split there into monotone pieces and the first rising piece that reaches
+ * V_th is bisected to full double precision.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+/* ------------------------------------------------------------------------ */
+/* Spike kernel, Table "tab:kernel", row tau_v != tau_I.                      */
+/* ------------------------------------------------------------------------ */
+static double kern(double tv, double ti, double t) {
+    if (t < 0.0) return 0.0; /* Heaviside factor */
+    double c = tv * ti / (tv - ti);
+    return c * (exp(-t / tv) - exp(-t / ti));
+}
+
+double oracle_kernel(double tau_v, double tau_i, double t) { return kern(tau_v, tau_i, t); }
+
+/* ------------------------------------------------------------------------ */
+/* DSTD kernel K_DSTD, Table "tab:DSTD_kernels", row tau_v != tau_I, and its  */
+/* derivative with respect to its argument.                                  */
+/* ------------------------------------------------------------------------ */
+static double kdstd(double tv, double ti, double D, double t) {
+    double den = exp(-D / tv) - exp(-D / ti);
+    if (t >= 0.0)
+        return (exp((t - D) / tv) - exp((t - D) / ti)) / den;
+    return (-exp(-D / ti) * exp(t / tv) + exp(-D / tv) * exp(t / ti)) / den;
+}
+
+static double kdstd_dt(double tv, double ti, double D, double t) {
+    double den = exp(-D / tv) - exp(-D / ti);
+    if (t >= 0.0)
+        return (exp((t - D) / tv) / tv - exp((t - D) / ti) / ti) / den;
+    return (-exp(-D / ti) * exp(t / tv) / tv + exp(-D / tv) * exp(t / ti) / ti) / den;
+}
+
+double oracle_kdstd(double tau_v, double tau_i, double dt, double t) { return kdstd(tau_v, tau_i, dt, t); }
+
+/* Grid point T_m (App. B.1 with t_offset folded into t0). */
+static double grid(double t0, double dt, int m) { return t0 + (double)m * dt; }
+
+/*
+ * Eq. (DSTD_kernel) taken literally: s_jm = K_DSTD(t_j - T_m) when
+ * T_{m-1} <= t_j < T_{m+1}, else 0, for m = 0..M. Every m is tested; the
+ * nonzero ones (at most two, the compact support of App. B.3) are returned.
+ */
+static int events_literal(double t, double t0, double dt, int M, double tv, double ti,
+                          int *m_out, double *s_out, double *ds_out) {
+    int n = 0;
+    for (int m = 0; m <= M; ++m) {
+        double lo = grid(t0, dt, m - 1), hi = grid(t0, dt, m + 1);
+        if (lo <= t && t < hi) {
+            double arg = t - grid(t0, dt, m);
+            if (n < 2) {
+                m_out[n] = m;
+                s_out[n] = kdstd(tv, ti, dt, arg);
+                ds_out[n] = kdstd_dt(tv, ti, dt, arg);
+            }
+            ++n;
+        }
+    }
+    return n;
+}
+
+/* Dense event tensor s[b][m][j] for small cases (pins). */
+void oracle_dstd_events(double tau_v, double tau_i, int M, double t0, double dt,
+                        int64_t B, int64_t N_in, const double *t_in, double *s, double *ds) {
+    memset(s, 0, sizeof(double) * (size_t)(B * (M + 1) * N_in));
+    if (ds) memset(ds, 0, sizeof(double) * (size_t)(B * (M + 1) * N_in));
+    for (int64_t b = 0; b < B; ++b)
+        for (int64_t j = 0; j < N_in; ++j) {
+            int mm[2]; double sv[2], dv[2];
+            int n = events_literal(t_in[b * N_in + j], t0, dt, M, tau_v, tau_i, mm, sv, dv);
+            for (int k = 0; k < n && k < 2; ++k) {
+                s[(b * (M + 1) + mm[k]) * N_in + j] = sv[k];
+                if (ds) ds[(b * (M + 1) + mm[k]) * N_in + j] = dv[k];
+            }
+        }
+}
+
+/* ------------------------------------------------------------------------ */
+/* Candidate solve inside one interval.                                      */
+/*                                                                           */
+/* On an interval the potential is v(t) = c*(a*exp(-(t-tr)/tv)               */
+/*  - b*exp(-(t-tr)/ti)), the general-tau analogue of the a_iq, b_iq prefix   */
+/* sums of Tables "tab:spike_timing" / "tab:timing_DSTD" (weights times       */
+/* exp(T/tau)), written relative to a reference time tr so the exponentials  */
+/* stay in range.                                                            */
+/* ------------------------------------------------------------------------ */
+typedef struct { double tv, ti, c, theta, tr, a, b; } piece_t;
+
+static double pv(const piece_t *p, double t) {
+    double s = t - p->tr;
+    return p->c * (p->a * exp(-s / p->tv) - p->b * exp(-s / p->ti));
+}
+
+static double pdv(const piece_t *p, double t) {
+    double s = t - p->tr;
+    return p->c * (-p->a / p->tv * exp(-s / p->tv) + p->b / p->ti * exp(-s / p->ti));
+}
+
+/* value at hi; hi may be +inf, where both exponentials vanish */
+static double pv_end(const piece_t *p, double hi) { return isinf(hi) ? 0.0 : pv(p, hi); }
+
+/*
+ * First t in [lo, hi) with v(t) >= theta. Returns 1 and sets *root when it
+ * exists. *peak receives sup v over [lo, hi] (for the ambiguity margin).
+ */
+static int first_crossing(const piece_t *p, double lo, double hi, double *root, double *peak) {
+    double th = p->theta;
+    /* critical point of v: exp(-kappa*s) = a*ti/(b*tv), kappa = 1/ti - 1/tv */
+    double kappa = 1.0 / p->ti - 1.0 / p->tv;
+    double tc = NAN;
+    double ratio = (p->b != 0.0) ? (p->a * p->ti) / (p->b * p->tv) : -1.0;
+    if (ratio > 0.0) {
+        tc = p->tr - log(ratio) / kappa;
+        if (!(tc > lo && tc < hi)) tc = NAN;
+    }
+    double v_lo = pv(p, lo), v_hi = pv_end(p, hi);
+    double pk = fmax(v_lo, v_hi);
+    if (!isnan(tc)) pk = fmax(pk, pv(p, tc));
+    *peak = pk;
+
+    if (v_lo >= th) { *root = lo; return 1; }
+    double e0[2], e1[2];
+    int np = 0;
+    if (!isnan(tc)) { e0[0] = lo; e1[0] = tc; e0[1] = tc; e1[1] = hi; np = 2; }
+    else { e0[0] = lo; e1[0] = hi; np = 1; }
+    for (int k = 0; k < np; ++k) {
+        double a = e0[k], b = e1[k];
+        double fa = pv(p, a) - th;
+        double fb = pv_end(p, b) - th;
+        if (fa >= 0.0) { *root = a; return 1; }
+        if (fb < 0.0) continue; /* piece stays below threshold */
+        if (isinf(b)) continue; /* v -> 0 < theta at +inf: unreachable */
+        /* f(a) < 0 <= f(b) on a monotone piece: bisect */
+        for (int it = 0; it < 400; ++it) {
+            double mid = 0.5 * (a + b);
+            if (!(mid > a && mid < b)) break;
+            if (pv(p, mid) - th >= 0.0) b = mid; else a = mid;
+        }
+        if (b >= hi) return 0; /* the crossing is exactly at hi: next interval */
+        *root = b;
+        return 1;
+    }
+    return 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* DSTD forward for one sample: Eq. (DSTD), App. B.1, Table "tab:timing_DSTD" */
+/* and Eq. (timing_DSTD).                                                    */
+/* ------------------------------------------------------------------------ */
+typedef struct {
+    double tv, ti, theta, t0, dt, t_max;
+    int M;
+} prm_t;
+
+static void canon(prm_t *p, double tau_m, double tau_s) {
+    /* K is symmetric in (tau_v, tau_I); keep tau_v > tau_I */
+    p->tv = fmax(tau_m, tau_s);
+    p->ti = fmin(tau_m, tau_s);
+}
+
+/* per-neuron scan over the M+1 DSTD intervals given w^[0..M] */
+static void dstd_scan(const prm_t *p, const double *wh, double *t_out, double *slope,
+                      int *q_out, double *margin, double *v_at_T) {
+    double c = p->tv * p->ti / (p->tv - p->ti);
+    double tr = p->t0;
+    piece_t pc = {p->tv, p->ti, c, p->theta, tr, 0.0, 0.0};
+    double pre = INFINITY; /* min over earlier intervals of theta - peak */
+    for (int q = 0; q <= p->M; ++q) {
+        double Tq = grid(p->t0, p->dt, q);
+        /* prefix sums a_iq, b_iq (weights times exp(T_m/tau)), shifted frame */
+        pc.a += wh[q] * exp((Tq - tr) / p->tv);
+        pc.b += wh[q] * exp((Tq - tr) / p->ti);
+        double hi = (q < p->M) ? grid(p->t0, p->dt, q + 1) : p->t_max;
+        if (v_at_T) v_at_T[q] = pv(&pc, Tq);
+        double root, peak;
+        int hit = first_crossing(&pc, Tq, hi, &root, &peak);
+        if (hit) {
+            *t_out = root;
+            *slope = pdv(&pc, root);
+            *q_out = q;
+            double m = pre;
+            m = fmin(m, fabs(peak - p->theta));
+            m = fmin(m, fabs(pv(&pc, Tq) - p->theta));
+            if (q < p->M) m = fmin(m, fabs(pv(&pc, hi) - p->theta));
+            if (margin) *margin = m;
+            return;
+        }
+        pre = fmin(pre, p->theta - peak);
+    }
+    *t_out = INFINITY;
+    *slope = 0.0;
+    *q_out = -1;
+    if (margin) *margin = pre;
+}
+
+typedef struct { int n; int m[2]; double s[2]; double ds[2]; } ev_t;
+
+static void sample_events(const prm_t *p, const double *t_row, int64_t N_in, ev_t *ev) {
+    for (int64_t j = 0; j < N_in; ++j) {
+        ev_t e;
+        int n = events_literal(t_row[j], p->t0, p->dt, p->M, p->tv, p->ti, e.m, e.s, e.ds);
+        e.n = n > 2 ? 2 : n;
+        ev[j] = e;
+    }
+}
+
+/*
+ * Forward of one dense layer.
+ *   t_in [B][N_in] (+inf = silent), W [N_out][N_in] (w_ij: j -> i)
+ * Outputs (double): t_out [B][N_out] (+inf = no spike), slope = dv^/dt at
+ * t_out, q_idx = interval index (-1 = none), margin (distance of the
+ * decision-relevant potentials from V_th), vabs = sum over m <= q* of
+ * |K(t_out - T_m)| * sum_j |w_ij s_jm| (scale of the terms forming v^(t_out)),
+ * what (optional) [B][M+1][N_out] = weighted events.
+ */
+void oracle_dstd_forward(double tau_m, double tau_s, double theta, int M, double t0, double dt,
+                         double t_max, int64_t B, int64_t N_in, int64_t N_out,
+                         const double *t_in, const double *W,
+                         double *t_out, double *slope, int32_t *q_idx, double *margin,
+                         double *vabs, double *what) {
+    prm_t p;
+    canon(&p, tau_m, tau_s);
+    p.theta = theta; p.M = M; p.t0 = t0; p.dt = dt; p.t_max = t_max;
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t b = 0; b < B; ++b) {
+        ev_t *ev = (ev_t *)malloc(sizeof(ev_t) * (size_t)(N_in > 0 ? N_in : 1));
+        double *wh = (double *)malloc(sizeof(double) * (size_t)(M + 1));
+        double *wabs = (double *)malloc(sizeof(double) * (size_t)(M + 1));
+        sample_events(&p, t_in + b * N_in, N_in, ev);
+        for (int64_t i = 0; i < N_out; ++i) {
+            for (int m = 0; m <= M; ++m) { wh[m] = 0.0; wabs[m] = 0.0; }
+            const double *wr = W + i * N_in;
+            /* w^_im = sum_j w_ij s_jm over the nonzero s_jm */
+            for (int64_t j = 0; j < N_in; ++j)
+                for (int k = 0; k < ev[j].n; ++k) {
+                    wh[ev[j].m[k]] += wr[j] * ev[j].s[k];
+                    wabs[ev[j].m[k]] += fabs(wr[j] * ev[j].s[k]);
+                }
+            if (what)
+                for (int m = 0; m <= M; ++m) what[(b * (M + 1) + m) * N_out + i] = wh[m];
+            double to, sl, mg; int q;
+            dstd_scan(&p, wh, &to, &sl, &q, &mg, NULL);
+            int64_t o = b * N_out + i;
+            t_out[o] = to; slope[o] = sl; q_idx[o] = q;
+            if (margin) margin[o] = mg;
+            if (vabs) {
+                double va = 0.0;
+                for (int m = 0; m <= (q < 0 ? -1 : q); ++m)
+                    va += fabs(kern(p.tv, p.ti, to - grid(t0, dt, m))) * wabs[m];
+                vabs[o] = va;
+            }
+        }
+        free(ev); free(wh); free(wabs);
+    }
+}
+
+/* Scan only, from given weighted events w^ [B][M+1][N_out] (pins the solver). */
+void oracle_dstd_scan(double tau_m, double tau_s, double theta, int M, double t0, double dt,
+                      double t_max, int64_t B, int64_t N_out, const double *what,
+                      double *t_out, double *slope, int32_t *q_idx, double *margin,
+                      double *v_at_T /* [B][M+1][N_out] or NULL */) {
+    prm_t p;
+    canon(&p, tau_m, tau_s);
+    p.theta = theta; p.M = M; p.t0 = t0; p.dt = dt; p.t_max = t_max;
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t b = 0; b < B; ++b) {
+        double *wh = (double *)malloc(sizeof(double) * (size_t)(M + 1));
+        double *vt = (double *)malloc(sizeof(double) * (size_t)(M + 1));
+        for (int64_t i = 0; i < N_out; ++i) {
+            for (int m = 0; m <= M; ++m) { wh[m] = what[(b * (M + 1) + m) * N_out + i]; vt[m] = NAN; }
+            double to, sl, mg; int q;
+            dstd_scan(&p, wh, &to, &sl, &q, &mg, vt);
+            int64_t o = b * N_out + i;
+            t_out[o] = to; slope[o] = sl; q_idx[o] = q;
+            if (margin) margin[o] = mg;
+            if (v_at_T) for (int m = 0; m <= M; ++m) v_at_T[(b * (M + 1) + m) * N_out + i] = vt[m];
+        }
+        free(wh); free(vt);
+    }
+}
+
+/*
+ * Backward of one dense layer. The DSTD spike time solves v^(t) = V_th with
+ * v^(t) = sum_{m<=q*} w^_m K(t - T_m) (App. B.1); the interval index q* is
+ * piecewise constant, so by the implicit-function theorem
+ *   d t / d w^_m = -K(t - T_m) / v^'(t)   for m <= q*,  0 otherwise,
+ * which is what reverse-mode differentiation of the closed-form candidates of
+ * Table "tab:timing_DSTD" yields as well (each candidate is that root).
+ * Chain rule through w^_im = sum_j w_ij s_jm and s_jm = K_DSTD(t_j - T_m):
+ *   dL/dw_ij = sum_b sum_m G[b,m,i] s_jm,   dL/dt_j = sum_m sum_i G[b,m,i] w_ij ds_jm/dt_j
+ * with G[b,m,i] = -g_bi K(t_bi - T_m) / slope_bi. Non-fired neurons (q < 0)
+ * contribute nothing. grad_W is [N_out][N_in], grad_t_in is [B][N_in].
+ */
+void oracle_dstd_backward(double tau_m, double tau_s, double theta, int M, double t0, double dt,
+                          double t_max, int64_t B, int64_t N_in, int64_t N_out,
+                          const double *t_in, const double *W,
+                          const double *t_out, const double *slope, const int32_t *q_idx,
+                          const double *grad_t_out,
+                          int64_t n_isel, const int64_t *isel, double *grad_W,
+                          int64_t n_bsel, const int64_t *bsel, double *grad_t_in) {
+    /* grad_W rows are computed for the n_isel neurons listed in isel (all when
+       n_isel < 0) and stored as [n_isel][N_in]; grad_t_in rows likewise for the
+       samples in bsel, stored as [n_bsel][N_in]. */
+    prm_t p;
+    canon(&p, tau_m, tau_s);
+    p.theta = theta; p.M = M; p.t0 = t0; p.dt = dt; p.t_max = t_max;
+    int64_t ni = n_isel < 0 ? N_out : n_isel;
+    int64_t nb = n_bsel < 0 ? B : n_bsel;
+    ev_t *ev = (ev_t *)malloc(sizeof(ev_t) * (size_t)(B * N_in > 0 ? B * N_in : 1));
+    double *G = (double *)calloc((size_t)(B * N_out * (M + 1) > 0 ? B * N_out * (M + 1) : 1), sizeof(double));
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t b = 0; b < B; ++b) {
+        sample_events(&p, t_in + b * N_in, N_in, ev + b * N_in);
+        for (int64_t i = 0; i < N_out; ++i) {
+            int64_t o = b * N_out + i;
+            int q = q_idx[o];
+            if (q < 0 || grad_t_out[o] == 0.0) continue;
+            double gam = -grad_t_out[o] / slope[o];
+            for (int m = 0; m <= q; ++m)
+                G[o * (M + 1) + m] = gam * kern(p.tv, p.ti, t_out[o] - grid(t0, dt, m));
+        }
+    }
+    if (grad_t_in) {
+#pragma omp parallel for schedule(dynamic, 1)
+        for (int64_t r = 0; r < nb; ++r) {
+            int64_t b = n_bsel < 0 ? r : bsel[r];
+            for (int64_t j = 0; j < N_in; ++j) {
+                const ev_t *e = ev + b * N_in + j;
+                double acc = 0.0;
+                for (int k = 0; k < e->n; ++k)
+                    for (int64_t i = 0; i < N_out; ++i)
+                        acc += G[(b * N_out + i) * (M + 1) + e->m[k]] * W[i * N_in + j] * e->ds[k];
+                grad_t_in[r * N_in + j] = acc;
+            }
+        }
+    }
+    if (grad_W) {
+#pragma omp parallel for schedule(dynamic, 1)
+        for (int64_t r = 0; r < ni; ++r) {
+            int64_t i = n_isel < 0 ? r : isel[r];
+            for (int64_t j = 0; j < N_in; ++j) {
+                double acc = 0.0;
+                for (int64_t b = 0; b < B; ++b) {
+                    const ev_t *e = ev + b * N_in + j;
+                    for (int k = 0; k < e->n; ++k)
+                        acc += G[(b * N_out + i) * (M + 1) + e->m[k]] * e->s[k];
+                }
+                grad_W[r * N_in + j] = acc;
+            }
+        }
+    }
+    free(ev);
+    free(G);
+}
+
+/* ------------------------------------------------------------------------ */
+/* Exact continuous-time LIF spike times (App. A, Eq. (timing_exact), Alg. 1) */
+/* ------------------------------------------------------------------------ */
+typedef struct { double t; double w; } tw_t;
+
+static int cmp_tw(const void *x, const void *y) {
+    double a = ((const tw_t *)x)->t, b = ((const tw_t *)y)->t;
+    return (a > b) - (a < b);
+}
+
+/*
+ * Sort the presynaptic spikes ascending; on [t~_k, t~_{k+1}) the potential is
+ * sum_{j<=k} w_j K(t - t~_j); take the first interval whose candidate lies in
+ * it (t~_{N+1} = t_max, +inf by default). Non-finite inputs are silent.
+ */
+void oracle_exact_forward(double tau_m, double tau_s, double theta, double t_max,
+                          int64_t B, int64_t N_in, int64_t N_out,
+                          const double *t_in, const double *W, double *t_out, double *slope) {
+    double tv = fmax(tau_m, tau_s), ti = fmin(tau_m, tau_s);
+    double c = tv * ti / (tv - ti);
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t b = 0; b < B; ++b) {
+        tw_t *s = (tw_t *)malloc(sizeof(tw_t) * (size_t)(N_in > 0 ? N_in : 1));
+        for (int64_t i = 0; i < N_out; ++i) {
+            int64_t n = 0;
+            for (int64_t j = 0; j < N_in; ++j) {
+                double t = t_in[b * N_in + j];
+                if (isfinite(t)) { s[n].t = t; s[n].w = W[i * N_in + j]; ++n; }
+            }
+            qsort(s, (size_t)n, sizeof(tw_t), cmp_tw);
+            double to = INFINITY, sl = 0.0;
+            if (n > 0) {
+                piece_t pc = {tv, ti, c, theta, s[0].t, 0.0, 0.0};
+                for (int64_t k = 0; k < n; ++k) {
+                    pc.a += s[k].w * exp((s[k].t - pc.tr) / tv);
+                    pc.b += s[k].w * exp((s[k].t - pc.tr) / ti);
+                    double lo = s[k].t;
+                    double hi = (k + 1 < n) ? s[k + 1].t : t_max;
+                    if (!(hi > lo)) continue; /* simultaneous spikes add up first */
+                    if (lo >= t_max) break;
+                    if (hi > t_max) hi = t_max;
+                    double root, peak;
+                    if (first_crossing(&pc, lo, hi, &root, &peak)) {
+                        to = root; sl = pdv(&pc, root);
+                        break;
+                    }
+                }
+            }
+            t_out[b * N_out + i] = to;
+            slope[b * N_out + i] = sl;
+        }
+        free(s);
+    }
+}
+
+int oracle_num_threads(void) {
+#ifdef _OPENMP
+    return omp_get_max_threads();
+#else
+    return 1;
+#endif
+}
+
+/* ------------------------------------------------------------------------ */
+/* Convolutional DSTD-LIF layer.                                             */
+/*                                                                           */
+/* A conv layer is a dense layer whose weight matrix is the convolution's    */
+/* (sparse, shared) connectivity, so w^_im = sum_j w_ij s_jm of App. B.1      */
+/* holds with j ranging over the receptive field of output neuron i. Inputs  */
+/* are NCHW [B][C_in][H][W]; W is [C_out][C_in][KH][KW]; outputs NCHW.        */
+/* pool_in = 2 averages the input events over 2x2 windows before the         */
+/* convolution, pool_in = 0 averages them over the whole map (global pool),   */
+/* pool_in = 1 uses them as they are. Averaging events is linear, so it is    */
+/* the same as averaging the synaptic input currents (reading: the paper's    */
+/* own nets down-sample with stride-2 convolutions, Table "tab:architectures",*/
+/* and do not define spike pooling).                                         */
+/* ------------------------------------------------------------------------ */
+typedef struct {
+    int C_in, H, W, C_out, KH, KW, stride, pad, pool;
+    int Hp, Wp, Ho, Wo, P; /* pooled input map, output map, pool size */
+} cgeom_t;
+
+static void cgeom(cgeom_t *g, int C_in, int H, int W, int C_out, int KH, int KW, int stride,
+                  int pad, int pool) {
+    g->C_in = C_in; g->H = H; g->W = W; g->C_out = C_out; g->KH = KH; g->KW = KW;
+    g->stride = stride; g->pad = pad; g->pool = pool;
+    if (pool == 2) { g->Hp = H / 2; g->Wp = W / 2; g->P = 4; }
+    else if (pool == 0) { g->Hp = 1; g->Wp = 1; g->P = H * W; }
+    else { g->Hp = H; g->Wp = W; g->P = 1; }
+    g->Ho = (g->Hp + 2 * pad - KH) / stride + 1;
+    g->Wo = (g->Wp + 2 * pad - KW) / stride + 1;
+}
+
+/* raw input pixels (y, x) that pool into pooled cell (py, px) */
+static int pool_cells(const cgeom_t *g, int py, int px, int *ys, int *xs) {
+    int n = 0;
+    if (g->pool == 2) {
+        for (int dy = 0; dy < 2; ++dy)
+            for (int dx = 0; dx < 2; ++dx) { ys[n] = 2 * py + dy; xs[n] = 2 * px + dx; ++n; }
+    } else if (g->pool == 0) {
+        for (int y = 0; y < g->H; ++y)
+            for (int x = 0; x < g->W; ++x) { ys[n] = y; xs[n] = x; ++n; }
+    } else { ys[0] = py; xs[0] = px; n = 1; }
+    return n;
+}
+
+void oracle_conv_forward(double tau_m, double tau_s, double theta, int M, double t0, double dt,
+                         double t_max, int64_t B, int C_in, int H, int Wd, int C_out, int KH,
+                         int KW, int stride, int pad, int pool,
+                         const double *t_in, const double *W,
+                         double *t_out, double *slope, int32_t *q_idx, double *margin, double *vabs) {
+    prm_t p;
+    canon(&p, tau_m, tau_s);
+    p.theta = theta; p.M = M; p.t0 = t0; p.dt = dt; p.t_max = t_max;
+    cgeom_t g;
+    cgeom(&g, C_in, H, Wd, C_out, KH, KW, stride, pad, pool);
+    int64_t nin = (int64_t)C_in * H * Wd;
+    int64_t nout = (int64_t)C_out * g.Ho * g.Wo;
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t b = 0; b < B; ++b) {
+        ev_t *ev = (ev_t *)malloc(sizeof(ev_t) * (size_t)nin);
+        double *wh = (double *)malloc(sizeof(double) * (size_t)(M + 1));
+        double *wabs = (double *)malloc(sizeof(double) * (size_t)(M + 1));
+        int *ys = (int *)malloc(sizeof(int) * (size_t)(H * Wd));
+        int *xs = (int *)malloc(sizeof(int) * (size_t)(H * Wd));
+        sample_events(&p, t_in + b * nin, nin, ev);
+        for (int co = 0; co < C_out; ++co)
+            for (int oy = 0; oy < g.Ho; ++oy)
+                for (int ox = 0; ox < g.Wo; ++ox) {
+                    for (int m = 0; m <= M; ++m) { wh[m] = 0.0; wabs[m] = 0.0; }
+                    for (int ci = 0; ci < C_in; ++ci)
+                        for (int ky = 0; ky < KH; ++ky)
+                            for (int kx = 0; kx < KW; ++kx) {
+                                int py = oy * stride + ky - pad, px = ox * stride + kx - pad;
+                                if (py < 0 || py >= g.Hp || px < 0 || px >= g.Wp) continue;
+                                double w = W[((co * C_in + ci) * KH + ky) * KW + kx] / g.P;
+                                int nc = pool_cells(&g, py, px, ys, xs);
+                                for (int r = 0; r < nc; ++r) {
+                                    const ev_t *e = ev + ((int64_t)ci * H + ys[r]) * Wd + xs[r];
+                                    for (int k = 0; k < e->n; ++k) {
+                                        wh[e->m[k]] += w * e->s[k];
+                                        wabs[e->m[k]] += fabs(w * e->s[k]);
+                                    }
+                                }
+                            }
+                    double to, sl, mg; int q;
+                    dstd_scan(&p, wh, &to, &sl, &q, &mg, NULL);
+                    int64_t o = b * nout + ((int64_t)co * g.Ho + oy) * g.Wo + ox;
+                    t_out[o] = to; slope[o] = sl; q_idx[o] = q;
+                    if (margin) margin[o] = mg;
+                    if (vabs) {
+                        double va = 0.0;
+                        for (int m = 0; m <= (q < 0 ? -1 : q); ++m)
+                            va += fabs(kern(p.tv, p.ti, to - grid(t0, dt, m))) * wabs[m];
+                        vabs[o] = va;
+                    }
+                }
+        free(ev); free(wh); free(wabs); free(ys); free(xs);
+    }
+}
+
+/* Backward of the conv layer: the dense-layer chain rule over the conv's
+   connectivity (and through the linear event pooling). */
+void oracle_conv_backward(double tau_m, double tau_s, double theta, int M, double t0, double dt,
+                          double t_max, int64_t B, int C_in, int H, int Wd, int C_out, int KH,
+                          int KW, int stride, int pad, int pool,
+                          const double *t_in, const double *W,
+                          const double *t_out, const double *slope, const int32_t *q_idx,
+                          const double *grad_t_out, double *grad_W, double *grad_t_in) {
+    prm_t p;
+    canon(&p, tau_m, tau_s);
+    p.theta = theta; p.M = M; p.t0 = t0; p.dt = dt; p.t_max = t_max;
+    (void)theta;
+    cgeom_t g;
+    cgeom(&g, C_in, H, Wd, C_out, KH, KW, stride, pad, pool);
+    int64_t nin = (int64_t)C_in * H * Wd;
+    int64_t nout = (int64_t)C_out * g.Ho * g.Wo;
+    int64_t nw = (int64_t)C_out * C_in * KH * KW;
+    int nth = 1;
+#ifdef _OPENMP
+    nth = omp_get_max_threads();
+#endif
+    double *dWp = (double *)calloc((size_t)(nw * nth), sizeof(double));
+    memset(grad_t_in, 0, sizeof(double) * (size_t)(B * nin));
+#pragma omp parallel
+    {
+        int tid = 0;
+#ifdef _OPENMP
+        tid = omp_get_thread_num();
+#endif
+        double *dWl = dWp + (int64_t)tid * nw;
+        ev_t *ev = (ev_t *)malloc(sizeof(ev_t) * (size_t)nin);
+        double *G = (double *)malloc(sizeof(double) * (size_t)(M + 1));
+        int *ys = (int *)malloc(sizeof(int) * (size_t)(H * Wd));
+        int *xs = (int *)malloc(sizeof(int) * (size_t)(H * Wd));
+#pragma omp for schedule(dynamic, 1)
+        for (int64_t b = 0; b < B; ++b) {
+            sample_events(&p, t_in + b * nin, nin, ev);
+            double *dt_row = grad_t_in + b * nin;
+            for (int co = 0; co < C_out; ++co)
+                for (int oy = 0; oy < g.Ho; ++oy)
+                    for (int ox = 0; ox < g.Wo; ++ox) {
+                        int64_t o = b * nout + ((int64_t)co * g.Ho + oy) * g.Wo + ox;
+                        int q = q_idx[o];
+                        if (q < 0 || grad_t_out[o] == 0.0) continue;
+                        double gam = -grad_t_out[o] / slope[o];
+                        for (int m = 0; m <= M; ++m)
+                            G[m] = (m <= q) ? gam * kern(p.tv, p.ti, t_out[o] - grid(t0, dt, m)) : 0.0;
+                        for (int ci = 0; ci < C_in; ++ci)
+                            for (int ky = 0; ky < KH; ++ky)
+                                for (int kx = 0; kx < KW; ++kx) {
+                                    int py = oy * stride + ky - pad, px = ox * stride + kx - pad;
+                                    if (py < 0 || py >= g.Hp || px < 0 || px >= g.Wp) continue;
+                                    int64_t widx = ((int64_t)(co * C_in + ci) * KH + ky) * KW + kx;
+                                    double w = W[widx];
+                                    int nc = pool_cells(&g, py, px, ys, xs);
+                                    for (int r = 0; r < nc; ++r) {
+                                        int64_t jin = ((int64_t)ci * H + ys[r]) * Wd + xs[r];
+                                        const ev_t *e = ev + jin;
+                                        for (int k = 0; k < e->n; ++k) {
+                                            dWl[widx] += G[e->m[k]] * e->s[k] / g.P;
+                                            dt_row[jin] += G[e->m[k]] * w * e->ds[k] / g.P;
+                                        }
+                                    }
+                                }
+                    }
+        }
+        free(ev); free(G); free(ys); free(xs);
+    }
+    for (int64_t k = 0; k < nw; ++k) {
+        double s = 0.0;
+        for (int t = 0; t < nth; ++t) s += dWp[(int64_t)t * nw + k];
+        grad_W[k] = s;
+    }
+    free(dWp);
+}

@@ -1,0 +1,238 @@
+"""ctypes binding of the fp64 C oracle (``dstd_oracle.c``).
+
+Test infrastructure only: the product path never imports this module.
+Inputs are widened to float64 (pass the float32 arrays the GPU sees, or
+float64 arrays for finite-difference pins); results are float64.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = [os.path.join(_HERE, "dstd_oracle.c")]
+_LIB_PATH = os.path.join(_HERE, "libdstd_oracle.so")
+_lib = None
+
+
+def build_oracle(force: bool = True) -> str:
+    """Compile the oracle with gcc (-O2, OpenMP, fp64, no fast-math)."""
+    if force or not os.path.exists(_LIB_PATH):
+        cmd = ["gcc", "-O2", "-fopenmp", "-shared", "-fPIC", "-std=c11", "-Wall",
+               "-o", _LIB_PATH + ".tmp"] + _SRC + ["-lm"]
+        subprocess.run(cmd, check=True)
+        os.replace(_LIB_PATH + ".tmp", _LIB_PATH)
+    return _LIB_PATH
+
+
+_D = C.c_double
+_I = C.c_int
+_L = C.c_int64
+_P = C.c_void_p
+
+
+def _load():
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB_PATH):
+        build_oracle(force=True)
+    lib = C.CDLL(_LIB_PATH)
+    lib.oracle_kernel.restype = _D
+    lib.oracle_kernel.argtypes = [_D, _D, _D]
+    lib.oracle_kdstd.restype = _D
+    lib.oracle_kdstd.argtypes = [_D, _D, _D, _D]
+    lib.oracle_dstd_events.restype = None
+    lib.oracle_dstd_events.argtypes = [_D, _D, _I, _D, _D, _L, _L, _P, _P, _P]
+    lib.oracle_dstd_forward.restype = None
+    lib.oracle_dstd_forward.argtypes = [_D, _D, _D, _I, _D, _D, _D, _L, _L, _L,
+                                        _P, _P, _P, _P, _P, _P, _P, _P]
+    lib.oracle_dstd_scan.restype = None
+    lib.oracle_dstd_scan.argtypes = [_D, _D, _D, _I, _D, _D, _D, _L, _L, _P,
+                                     _P, _P, _P, _P, _P]
+    lib.oracle_dstd_backward.restype = None
+    lib.oracle_dstd_backward.argtypes = [_D, _D, _D, _I, _D, _D, _D, _L, _L, _L,
+                                         _P, _P, _P, _P, _P, _P, _L, _P, _P, _L, _P, _P]
+    lib.oracle_exact_forward.restype = None
+    lib.oracle_exact_forward.argtypes = [_D, _D, _D, _D, _L, _L, _L, _P, _P, _P, _P]
+    lib.oracle_conv_forward.restype = None
+    lib.oracle_conv_forward.argtypes = [_D, _D, _D, _I, _D, _D, _D, _L,
+                                        _I, _I, _I, _I, _I, _I, _I, _I, _I,
+                                        _P, _P, _P, _P, _P, _P, _P]
+    lib.oracle_conv_backward.restype = None
+    lib.oracle_conv_backward.argtypes = [_D, _D, _D, _I, _D, _D, _D, _L,
+                                         _I, _I, _I, _I, _I, _I, _I, _I, _I,
+                                         _P, _P, _P, _P, _P, _P, _P, _P]
+    lib.oracle_num_threads.restype = _I
+    lib.oracle_num_threads.argtypes = []
+    _lib = lib
+    return lib
+
+
+def _f64(a):
+    """Widen to float64 exactly (float32 inputs keep their bits' value)."""
+    return np.ascontiguousarray(np.asarray(a, dtype=np.float64))
+
+
+def _ptr(a):
+    return None if a is None else a.ctypes.data_as(C.c_void_p)
+
+
+def num_threads() -> int:
+    return int(_load().oracle_num_threads())
+
+
+def kernel(tau_v, tau_i, t) -> float:
+    """Spike kernel K(t), Table "tab:kernel" (general row)."""
+    return float(_load().oracle_kernel(tau_v, tau_i, t))
+
+
+def kdstd(tau_v, tau_i, dt, t) -> float:
+    """DSTD kernel K_DSTD(t), Table "tab:DSTD_kernels" (general row)."""
+    return float(_load().oracle_kdstd(tau_v, tau_i, dt, t))
+
+
+def dstd_events(p, t_in):
+    """Dense event tensor s[b, m, j] and ds/dt, Eq. (DSTD_kernel)."""
+    t_in = _f64(t_in)
+    B, N_in = t_in.shape
+    M = int(p["M"])
+    s = np.zeros((B, M + 1, N_in))
+    ds = np.zeros((B, M + 1, N_in))
+    tv, ti = max(p["tau_m"], p["tau_s"]), min(p["tau_m"], p["tau_s"])
+    _load().oracle_dstd_events(tv, ti, M, p["t0"], p["dt"], B, N_in, _ptr(t_in), _ptr(s), _ptr(ds))
+    return s, ds
+
+
+def _pargs(p):
+    return (float(p["tau_m"]), float(p["tau_s"]), float(p["threshold"]), int(p["M"]),
+            float(p["t0"]), float(p["dt"]), float(p.get("t_max", np.inf)))
+
+
+def dstd_forward(p, t_in, W, want_what=False):
+    """DSTD forward of a dense layer. Returns dict of float64/int32 arrays."""
+    t_in = _f64(t_in)
+    W = _f64(W)
+    B, N_in = t_in.shape
+    N_out = W.shape[0]
+    assert W.shape == (N_out, N_in)
+    M = int(p["M"])
+    t_out = np.empty((B, N_out))
+    slope = np.empty((B, N_out))
+    q = np.empty((B, N_out), dtype=np.int32)
+    margin = np.empty((B, N_out))
+    vabs = np.empty((B, N_out))
+    what = np.empty((B, M + 1, N_out)) if want_what else None
+    _load().oracle_dstd_forward(*_pargs(p), B, N_in, N_out, _ptr(t_in), _ptr(W),
+                                _ptr(t_out), _ptr(slope), _ptr(q), _ptr(margin), _ptr(vabs),
+                                _ptr(what))
+    out = dict(t_out=t_out, slope=slope, q=q, margin=margin, vabs=vabs)
+    if want_what:
+        out["what"] = what
+    return out
+
+
+def dstd_scan(p, what):
+    """Interval scan + solve from given weighted events what[b, m, i] (float64)."""
+    what = np.ascontiguousarray(np.asarray(what, dtype=np.float64))
+    B, M1, N_out = what.shape
+    assert M1 == int(p["M"]) + 1
+    t_out = np.empty((B, N_out))
+    slope = np.empty((B, N_out))
+    q = np.empty((B, N_out), dtype=np.int32)
+    margin = np.empty((B, N_out))
+    vT = np.empty((B, M1, N_out))
+    _load().oracle_dstd_scan(*_pargs(p), B, N_out, _ptr(what), _ptr(t_out), _ptr(slope), _ptr(q),
+                             _ptr(margin), _ptr(vT))
+    return dict(t_out=t_out, slope=slope, q=q, margin=margin, v_at_T=vT)
+
+
+def dstd_backward(p, t_in, W, fwd, grad_t_out, isel=None, bsel=None, want_dW=True, want_dt=True):
+    """DSTD backward of a dense layer (implicit-function gradients).
+
+    ``fwd`` is a dict with t_out, slope, q (the oracle's own forward, or any
+    forward outputs of the same layer). Returns (grad_W rows, grad_t_in rows).
+    """
+    t_in = _f64(t_in)
+    W = _f64(W)
+    B, N_in = t_in.shape
+    N_out = W.shape[0]
+    t_out = np.ascontiguousarray(fwd["t_out"], dtype=np.float64)
+    slope = np.ascontiguousarray(fwd["slope"], dtype=np.float64)
+    q = np.ascontiguousarray(fwd["q"], dtype=np.int32)
+    g = np.ascontiguousarray(grad_t_out, dtype=np.float64)
+    isel_a = None if isel is None else np.ascontiguousarray(isel, dtype=np.int64)
+    bsel_a = None if bsel is None else np.ascontiguousarray(bsel, dtype=np.int64)
+    ni = N_out if isel is None else len(isel_a)
+    nb = B if bsel is None else len(bsel_a)
+    dW = np.empty((ni, N_in)) if want_dW else None
+    dt = np.empty((nb, N_in)) if want_dt else None
+    _load().oracle_dstd_backward(*_pargs(p), B, N_in, N_out, _ptr(t_in), _ptr(W), _ptr(t_out),
+                                 _ptr(slope), _ptr(q), _ptr(g),
+                                 -1 if isel is None else ni, _ptr(isel_a), _ptr(dW),
+                                 -1 if bsel is None else nb, _ptr(bsel_a), _ptr(dt))
+    return dW, dt
+
+
+def exact_forward(p, t_in, W):
+    """Exact continuous-time LIF spike times (Alg. 1, Eq. (timing_exact))."""
+    t_in = _f64(t_in)
+    W = _f64(W)
+    B, N_in = t_in.shape
+    N_out = W.shape[0]
+    t_out = np.empty((B, N_out))
+    slope = np.empty((B, N_out))
+    _load().oracle_exact_forward(float(p["tau_m"]), float(p["tau_s"]), float(p["threshold"]),
+                                 float(p.get("t_max", np.inf)), B, N_in, N_out, _ptr(t_in), _ptr(W),
+                                 _ptr(t_out), _ptr(slope))
+    return dict(t_out=t_out, slope=slope)
+
+
+def _conv_geom(cs):
+    return (int(cs["C_in"]), int(cs["H"]), int(cs["W"]), int(cs["C_out"]), int(cs["KH"]),
+            int(cs["KW"]), int(cs["stride"]), int(cs["pad"]), int(cs["pool_in"]))
+
+
+def conv_out_hw(cs):
+    C_in, H, Wd, C_out, KH, KW, st, pad, pool = _conv_geom(cs)
+    if pool == 2:
+        H, Wd = H // 2, Wd // 2
+    elif pool == 0:
+        H, Wd = 1, 1
+    return (H + 2 * pad - KH) // st + 1, (Wd + 2 * pad - KW) // st + 1
+
+
+def conv_forward(p, cs, t_in, W):
+    """DSTD forward of a conv layer (events pooled before the convolution)."""
+    t_in = _f64(t_in)
+    W = _f64(W)
+    B = t_in.shape[0]
+    Ho, Wo = conv_out_hw(cs)
+    C_out = int(cs["C_out"])
+    shp = (B, C_out, Ho, Wo)
+    t_out = np.empty(shp)
+    slope = np.empty(shp)
+    q = np.empty(shp, dtype=np.int32)
+    margin = np.empty(shp)
+    vabs = np.empty(shp)
+    _load().oracle_conv_forward(*_pargs(p), B, *_conv_geom(cs), _ptr(t_in), _ptr(W), _ptr(t_out),
+                                _ptr(slope), _ptr(q), _ptr(margin), _ptr(vabs))
+    return dict(t_out=t_out, slope=slope, q=q, margin=margin, vabs=vabs)
+
+
+def conv_backward(p, cs, t_in, W, fwd, grad_t_out):
+    t_in = _f64(t_in)
+    W = _f64(W)
+    t_out = np.ascontiguousarray(fwd["t_out"], dtype=np.float64)
+    slope = np.ascontiguousarray(fwd["slope"], dtype=np.float64)
+    q = np.ascontiguousarray(fwd["q"], dtype=np.int32)
+    g = np.ascontiguousarray(grad_t_out, dtype=np.float64)
+    B = t_in.shape[0]
+    dW = np.empty(W.shape)
+    dt = np.empty(t_in.shape)
+    _load().oracle_conv_backward(*_pargs(p), B, *_conv_geom(cs), _ptr(t_in), _ptr(W), _ptr(t_out),
+                                 _ptr(slope), _ptr(q), _ptr(g), _ptr(dW), _ptr(dt))
+    return dW, dt

@@ -1,0 +1,198 @@
+/*
+ * dstd_lif.h -- C ABI of the MI355X (gfx950) DSTD-LIF layer library.
+ *
+ * Differentiable spike-time discretization (DSTD) for a time-to-first-spike
+ * leaky integrate-and-fire layer with membrane / synaptic time constants
+ * (tau_m, tau_s), after Sakemi et al., "Scalable Training of Continuous-Time
+ * Spiking Neural Networks with Differentiable Spike-Time Discretization".
+ *
+ * One layer maps presynaptic spike times t_j to weighted events at the grid
+ * points T_m = t0 + m*dt (m = 0..M), contracts them with the weights, scans
+ * the M intervals of every postsynaptic neuron for the first threshold
+ * crossing and solves for the continuous spike time; the backward pass
+ * returns gradients with respect to the weights and the input spike times.
+ *
+ * Conventions for every call:
+ *  - All array pointers are DEVICE pointers owned by the caller; the library
+ *    never allocates, frees or keeps device memory between calls.
+ *  - Arrays are dense, row-major, fp32 unless stated (W may be bf16).
+ *  - Work is enqueued asynchronously on `stream` (a hipStream_t, passed as
+ *    void*; NULL = the default stream); outputs are valid once the stream
+ *    reaches that point.
+ *  - Scratch memory comes from the caller: `ws` of `ws_bytes` bytes, at
+ *    least what the matching *_workspace_size() call returns, 256-byte
+ *    aligned. Its contents need not be initialised and are clobbered.
+ *  - Arguments are validated on the host before anything is enqueued; on a
+ *    non-OK status nothing was enqueued and outputs are untouched (except
+ *    DSTD_ERR_HIP, raised by a failed launch: outputs are then undefined).
+ *  - Results are deterministic: no floating-point atomics across threads,
+ *    fixed reduction orders; repeated calls give identical bits.
+ *  - Calls are thread-safe; dstd_last_error() is per thread.
+ */
+#ifndef DSTD_LIF_H
+#define DSTD_LIF_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    DSTD_OK = 0,
+    DSTD_ERR_NULL = -1,        /* a required pointer is NULL */
+    DSTD_ERR_SHAPE = -2,       /* negative / inconsistent sizes */
+    DSTD_ERR_PARAM = -3,       /* invalid LIF or grid parameter */
+    DSTD_ERR_UNSUPPORTED = -4, /* valid but not implemented (e.g. tau_m == tau_s, M too large) */
+    DSTD_ERR_WORKSPACE = -5,   /* ws too small or misaligned */
+    DSTD_ERR_HIP = -6          /* a HIP launch failed; see dstd_last_error() */
+} dstd_status;
+
+typedef enum { DSTD_F32 = 0, DSTD_BF16 = 1 } dstd_dtype;
+
+/*
+ * Layer parameters.
+ *  tau_m, tau_s : membrane and synaptic time constants (the paper's tau_v,
+ *                 tau_I; LIF model Eq. (LIF_model_TTFS)); finite, > 0. The
+ *                 spike kernel (Table "tab:kernel") is symmetric in the
+ *                 pair; |tau_m - tau_s| <= 1e-3 * max(tau_m, tau_s) is
+ *                 DSTD_ERR_UNSUPPORTED (the equal-constant case uses other
+ *                 formulas, Eqs. (equal_tau_*)).
+ *  threshold    : firing threshold V_th > 0. A neuron fires at the first t
+ *                 where v(t) >= V_th.
+ *  M            : number of DSTD intervals, 1 <= M <= DSTD_MAX_M; the grid
+ *                 has M+1 points (App. B.1).
+ *  t0, dt       : grid T_m = t0 + m*dt, dt > 0; the random t_offset of
+ *                 Alg. 2 is folded into t0 by the caller.
+ *  t_max        : end of the last candidate interval [T_M, t_max); +INFINITY
+ *                 leaves it open (the exact method's t_{N+1} = inf, App. A).
+ *                 Must be > T_M.
+ *  flags        : reserved, must be 0.
+ */
+typedef struct {
+    float tau_m, tau_s;
+    float threshold;
+    int32_t M;
+    float t0, dt;
+    float t_max;
+    int32_t flags;
+} dstd_lif_params;
+
+#define DSTD_MAX_M 256
+
+/* ---------------------------------------------------------------- dense -- */
+
+/* Workspace bytes needed by dstd_lif_forward / dstd_lif_backward. Returns 0
+   for invalid arguments (the calls then report the precise error). */
+size_t dstd_lif_forward_workspace_size(const dstd_lif_params *p, int64_t B, int64_t N_in,
+                                       int64_t N_out);
+size_t dstd_lif_backward_workspace_size(const dstd_lif_params *p, int64_t B, int64_t N_in,
+                                        int64_t N_out);
+
+/*
+ * Forward pass of one dense layer (Eq. (DSTD), App. B.1 definition of the
+ * weighted events, Table "tab:timing_DSTD", Eq. (timing_DSTD)).
+ *  t_in  [B][N_in]      input spike times; +inf (any non-finite value) = no
+ *                       spike. Inputs outside [T_0 - dt, T_M + dt) contribute
+ *                       nothing; an input in [T_0 - dt, T_0) only contributes
+ *                       its weight at T_0, one in [T_M, T_M + dt) only its
+ *                       weight at T_M (Eq. (DSTD_kernel) at the grid ends).
+ *  W     [N_out][N_in]  weights w_ij (input j -> neuron i), fp32 or bf16.
+ *  t_out [B][N_out]     out: spike time, +inf if the neuron does not fire.
+ *  slope [B][N_out]     out: dv/dt at the spike (0 if none); needed by backward.
+ *  q_idx [B][N_out]     out: interval index q of the spike (T_q <= t < T_{q+1},
+ *                       q = M for [T_M, t_max)), -1 if none.
+ * B, N_in, N_out >= 0; zero sizes are valid no-ops (N_in == 0 gives silent
+ * outputs). Only the O(B*N_out) outputs are kept for the backward pass.
+ */
+dstd_status dstd_lif_forward(const dstd_lif_params *p, int64_t B, int64_t N_in, int64_t N_out,
+                             const float *t_in, const void *W, dstd_dtype w_dtype,
+                             float *t_out, float *slope, int32_t *q_idx,
+                             void *ws, size_t ws_bytes, void *stream);
+
+/*
+ * Backward pass of one dense layer. t_out, slope, q_idx are the forward's
+ * outputs for the same (t_in, W, p). The interval index is piecewise
+ * constant, so the spike time's derivative follows from the implicit-function
+ * theorem applied to v^(t) = V_th: d t / d w^_m = -K(t - T_m) / slope for
+ * m <= q, which equals differentiating the candidates of Table
+ * "tab:timing_DSTD".
+ *  grad_t_out [B][N_out]  dL/dt_out; ignored where q_idx < 0.
+ *  grad_W     [N_out][N_in] out (fp32, overwritten, not accumulated), or NULL
+ *                           to skip.
+ *  grad_t_in  [B][N_in]   out (overwritten), or NULL to skip (first layer).
+ *                         Inputs without events get 0.
+ * A spike with slope below 1e-12 * threshold uses that floor (the exact
+ * derivative of a tangent crossing is unbounded).
+ */
+dstd_status dstd_lif_backward(const dstd_lif_params *p, int64_t B, int64_t N_in, int64_t N_out,
+                              const float *t_in, const void *W, dstd_dtype w_dtype,
+                              const float *t_out, const float *slope, const int32_t *q_idx,
+                              const float *grad_t_out, float *grad_W, float *grad_t_in,
+                              void *ws, size_t ws_bytes, void *stream);
+
+/* ----------------------------------------------------------------- conv -- */
+
+/*
+ * Convolutional layer geometry. Inputs NCHW [B][C_in][H][W], weights
+ * [C_out][C_in][KH][KW], outputs NCHW [B][C_out][H_out][W_out].
+ *  pool_in : 1 = none; 2 = average the input EVENTS over 2x2 windows
+ *            (H, W even) before the convolution; 0 = average them over the
+ *            whole H x W map. Averaging events is linear, i.e. it averages
+ *            the synaptic input currents.
+ *  H_out = (H_p + 2*pad - KH)/stride + 1 with H_p the (pooled) input height.
+ */
+typedef struct {
+    int32_t C_in, H, W, C_out, KH, KW, stride, pad, pool_in;
+} dstd_conv_shape;
+
+size_t dstd_lif_conv_forward_workspace_size(const dstd_lif_params *p, const dstd_conv_shape *cs,
+                                            int64_t B);
+size_t dstd_lif_conv_backward_workspace_size(const dstd_lif_params *p, const dstd_conv_shape *cs,
+                                             int64_t B);
+
+/* Same contract as dstd_lif_forward with the convolution's connectivity:
+   w^_{i m} sums w_ij s_jm over the receptive field of output neuron i. */
+dstd_status dstd_lif_conv_forward(const dstd_lif_params *p, const dstd_conv_shape *cs, int64_t B,
+                                  const float *t_in, const void *W, dstd_dtype w_dtype,
+                                  float *t_out, float *slope, int32_t *q_idx,
+                                  void *ws, size_t ws_bytes, void *stream);
+
+dstd_status dstd_lif_conv_backward(const dstd_lif_params *p, const dstd_conv_shape *cs, int64_t B,
+                                   const float *t_in, const void *W, dstd_dtype w_dtype,
+                                   const float *t_out, const float *slope, const int32_t *q_idx,
+                                   const float *grad_t_out, float *grad_W, float *grad_t_in,
+                                   void *ws, size_t ws_bytes, void *stream);
+
+/* --------------------------------------------------------------- losses -- */
+
+/*
+ * Softmax cross-entropy on the output spike times (App. C.1): logits
+ * -t/tau_soft, S = softmax, L = -(1/B) sum_b ln S_{b, label_b}. Neurons that
+ * did not fire (t = +inf) enter the softmax at t_cap and get no gradient.
+ *  t_out [B][N], labels [B] int32 in [0, N), grad_t [B][N] out = dL/dt,
+ *  loss [1] out (device float). N <= 1024.
+ */
+dstd_status dstd_softmax_ce_grad(int64_t B, int64_t N, const float *t_out, const int32_t *labels,
+                                 float tau_soft, float t_cap, float *grad_t, float *loss,
+                                 void *stream);
+
+/* Mean squared error L = (1/B) sum_{b,i fired} (t - y)^2 / 2 over fired outputs;
+   grad_t [B][N] out, loss [1] out (device float). N <= 1024. */
+dstd_status dstd_mse_grad(int64_t B, int64_t N, const float *t_out, const float *target,
+                          float *grad_t, float *loss, void *stream);
+
+/* ----------------------------------------------------------------- misc -- */
+
+const char *dstd_status_string(dstd_status s);
+/* Detail of the last non-OK status returned on the calling thread. */
+const char *dstd_last_error(void);
+/* Library ABI version (major * 100 + minor). */
+int32_t dstd_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DSTD_LIF_H */

@@ -345,10 +345,13 @@ void oracle_dstd_backward(double tau_m, double tau_s, double theta, int M, doubl
                           const double *t_out, const double *slope, const int32_t *q_idx,
                           const double *grad_t_out,
                           int64_t n_isel, const int64_t *isel, double *grad_W,
-                          int64_t n_bsel, const int64_t *bsel, double *grad_t_in) {
+                          int64_t n_bsel, const int64_t *bsel, double *grad_t_in,
+                          double *grad_W_abs, double *grad_t_in_abs) {
     /* grad_W rows are computed for the n_isel neurons listed in isel (all when
        n_isel < 0) and stored as [n_isel][N_in]; grad_t_in rows likewise for the
-       samples in bsel, stored as [n_bsel][N_in]. */
+       samples in bsel, stored as [n_bsel][N_in]. The optional *_abs outputs
+       receive the sum of the absolute values of the terms of each gradient
+       element (its conditioning, used to judge rounding). */
     prm_t p;
     canon(&p, tau_m, tau_s);
     p.theta = theta; p.M = M; p.t0 = t0; p.dt = dt; p.t_max = t_max;
@@ -374,11 +377,15 @@ void oracle_dstd_backward(double tau_m, double tau_s, double theta, int M, doubl
             int64_t b = n_bsel < 0 ? r : bsel[r];
             for (int64_t j = 0; j < N_in; ++j) {
                 const ev_t *e = ev + b * N_in + j;
-                double acc = 0.0;
+                double acc = 0.0, aabs = 0.0;
                 for (int k = 0; k < e->n; ++k)
-                    for (int64_t i = 0; i < N_out; ++i)
-                        acc += G[(b * N_out + i) * (M + 1) + e->m[k]] * W[i * N_in + j] * e->ds[k];
+                    for (int64_t i = 0; i < N_out; ++i) {
+                        double term = G[(b * N_out + i) * (M + 1) + e->m[k]] * W[i * N_in + j] * e->ds[k];
+                        acc += term;
+                        aabs += fabs(term);
+                    }
                 grad_t_in[r * N_in + j] = acc;
+                if (grad_t_in_abs) grad_t_in_abs[r * N_in + j] = aabs;
             }
         }
     }
@@ -387,13 +394,17 @@ void oracle_dstd_backward(double tau_m, double tau_s, double theta, int M, doubl
         for (int64_t r = 0; r < ni; ++r) {
             int64_t i = n_isel < 0 ? r : isel[r];
             for (int64_t j = 0; j < N_in; ++j) {
-                double acc = 0.0;
+                double acc = 0.0, aabs = 0.0;
                 for (int64_t b = 0; b < B; ++b) {
                     const ev_t *e = ev + b * N_in + j;
-                    for (int k = 0; k < e->n; ++k)
-                        acc += G[(b * N_out + i) * (M + 1) + e->m[k]] * e->s[k];
+                    for (int k = 0; k < e->n; ++k) {
+                        double term = G[(b * N_out + i) * (M + 1) + e->m[k]] * e->s[k];
+                        acc += term;
+                        aabs += fabs(term);
+                    }
                 }
                 grad_W[r * N_in + j] = acc;
+                if (grad_W_abs) grad_W_abs[r * N_in + j] = aabs;
             }
         }
     }

@@ -55,7 +55,7 @@ def _load():
                                      _P, _P, _P, _P, _P]
     lib.oracle_dstd_backward.restype = None
     lib.oracle_dstd_backward.argtypes = [_D, _D, _D, _I, _D, _D, _D, _L, _L, _L,
-                                         _P, _P, _P, _P, _P, _P, _L, _P, _P, _L, _P, _P]
+                                         _P, _P, _P, _P, _P, _P, _L, _P, _P, _L, _P, _P, _P, _P]
     lib.oracle_exact_forward.restype = None
     lib.oracle_exact_forward.argtypes = [_D, _D, _D, _D, _L, _L, _L, _P, _P, _P, _P]
     lib.oracle_conv_forward.restype = None
@@ -150,11 +150,13 @@ def dstd_scan(p, what):
     return dict(t_out=t_out, slope=slope, q=q, margin=margin, v_at_T=vT)
 
 
-def dstd_backward(p, t_in, W, fwd, grad_t_out, isel=None, bsel=None, want_dW=True, want_dt=True):
+def dstd_backward(p, t_in, W, fwd, grad_t_out, isel=None, bsel=None, want_dW=True, want_dt=True,
+                  want_abs=False):
     """DSTD backward of a dense layer (implicit-function gradients).
 
-    ``fwd`` is a dict with t_out, slope, q (the oracle's own forward, or any
-    forward outputs of the same layer). Returns (grad_W rows, grad_t_in rows).
+    ``fwd`` is a dict with t_out, slope, q (the oracle's own forward outputs).
+    Returns (grad_W rows, grad_t_in rows), plus (|terms| sums of each) when
+    ``want_abs``.
     """
     t_in = _f64(t_in)
     W = _f64(W)
@@ -170,10 +172,15 @@ def dstd_backward(p, t_in, W, fwd, grad_t_out, isel=None, bsel=None, want_dW=Tru
     nb = B if bsel is None else len(bsel_a)
     dW = np.empty((ni, N_in)) if want_dW else None
     dt = np.empty((nb, N_in)) if want_dt else None
+    dWa = np.empty((ni, N_in)) if (want_dW and want_abs) else None
+    dta = np.empty((nb, N_in)) if (want_dt and want_abs) else None
     _load().oracle_dstd_backward(*_pargs(p), B, N_in, N_out, _ptr(t_in), _ptr(W), _ptr(t_out),
                                  _ptr(slope), _ptr(q), _ptr(g),
                                  -1 if isel is None else ni, _ptr(isel_a), _ptr(dW),
-                                 -1 if bsel is None else nb, _ptr(bsel_a), _ptr(dt))
+                                 -1 if bsel is None else nb, _ptr(bsel_a), _ptr(dt),
+                                 _ptr(dWa), _ptr(dta))
+    if want_abs:
+        return dW, dt, dWa, dta
     return dW, dt
 
 

@@ -1,0 +1,290 @@
+// dstd_api.hip -- C ABI of the DSTD-LIF library: argument validation (host
+// only, before anything is enqueued), layer constants, workspace layout and
+// kernel dispatch. The contract of every entry point is documented in
+// include/dstd_lif.h.
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <algorithm>
+
+#include "../../include/dstd_lif.h"
+#include "dstd_internal.h"
+#include "dstd_kernels.h"
+
+using dstd::LifConst;
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+dstd_status fail(dstd_status s, const char *fmt, ...) {
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_err, sizeof(g_err), fmt, ap);
+    va_end(ap);
+    return s;
+}
+
+constexpr size_t kAlign = 256;
+size_t align_up(size_t n) { return (n + kAlign - 1) / kAlign * kAlign; }
+
+// Host validation of the layer parameters (no device access).
+dstd_status check_params(const dstd_lif_params *p) {
+    if (!p) return fail(DSTD_ERR_NULL, "params is NULL");
+    if (!(isfinite(p->tau_m) && p->tau_m > 0.f) || !(isfinite(p->tau_s) && p->tau_s > 0.f))
+        return fail(DSTD_ERR_PARAM, "time constants must be finite and > 0 (tau_m=%g tau_s=%g)",
+                    (double)p->tau_m, (double)p->tau_s);
+    double tmax = std::max((double)p->tau_m, (double)p->tau_s);
+    if (fabs((double)p->tau_m - (double)p->tau_s) <= 1e-3 * tmax)
+        return fail(DSTD_ERR_UNSUPPORTED,
+                    "tau_m == tau_s (within 1e-3 relative) uses the equal-constant kernel, "
+                    "which is not implemented");
+    if (!(isfinite(p->threshold) && p->threshold > 0.f))
+        return fail(DSTD_ERR_PARAM, "threshold must be finite and > 0");
+    if (p->M < 1) return fail(DSTD_ERR_PARAM, "M must be >= 1 (got %d)", p->M);
+    if (p->M > DSTD_MAX_M)
+        return fail(DSTD_ERR_UNSUPPORTED, "M = %d exceeds DSTD_MAX_M = %d", p->M, DSTD_MAX_M);
+    if (!(isfinite(p->dt) && p->dt > 0.f)) return fail(DSTD_ERR_PARAM, "dt must be finite and > 0");
+    if (!isfinite(p->t0)) return fail(DSTD_ERR_PARAM, "t0 must be finite");
+    double TM = (double)p->t0 + (double)p->M * (double)p->dt;
+    if (isnan(p->t_max) || !((double)p->t_max > TM))
+        return fail(DSTD_ERR_PARAM, "t_max must be > T_M = t0 + M*dt (got %g, T_M = %g)",
+                    (double)p->t_max, TM);
+    if (p->flags != 0) return fail(DSTD_ERR_PARAM, "flags must be 0");
+    return DSTD_OK;
+}
+
+double kern_d(double tv, double ti, double u) {
+    double c = tv * ti / (tv - ti), kap = 1.0 / ti - 1.0 / tv;
+    return -c * exp(-u / tv) * expm1(-kap * u);
+}
+
+LifConst make_const(const dstd_lif_params *p) {
+    double tv = std::max((double)p->tau_m, (double)p->tau_s);
+    double ti = std::min((double)p->tau_m, (double)p->tau_s);
+    double dt = p->dt;
+    double kap = 1.0 / ti - 1.0 / tv;
+    double upk = log(tv / ti) / kap;  // peak time of K
+    double TM = (double)p->t0 + (double)p->M * dt;
+    double last = isinf(p->t_max) ? INFINITY : (double)p->t_max - TM;
+    LifConst C;
+    C.tv = (float)tv;
+    C.ti = (float)ti;
+    C.inv_tv = (float)(1.0 / tv);
+    C.inv_ti = (float)(1.0 / ti);
+    C.c = (float)(tv * ti / (tv - ti));
+    C.kappa = (float)kap;
+    C.alpha = (float)exp(-dt / tv);
+    C.beta = (float)exp(-dt / ti);
+    C.k_dt = (float)kern_d(tv, ti, dt);
+    C.inv_em1 = (float)(1.0 / expm1(-kap * dt));
+    C.kmax_dt = (float)kern_d(tv, ti, std::min(dt, upk));
+    C.kmax_last = (float)kern_d(tv, ti, std::min(last, upk));
+    C.theta = p->threshold;
+    C.t0 = p->t0;
+    C.dt = p->dt;
+    C.last_len = (float)last;
+    C.slope_floor = 1e-12f * p->threshold;
+    C.M = p->M;
+    C.alpha_d = exp(-dt / tv);
+    C.beta_d = exp(-dt / ti);
+    C.k_dt_d = kern_d(tv, ti, dt);
+    return C;
+}
+
+dstd_status check_dims(int64_t B, int64_t N_in, int64_t N_out) {
+    if (B < 0 || N_in < 0 || N_out < 0)
+        return fail(DSTD_ERR_SHAPE, "sizes must be >= 0 (B=%lld N_in=%lld N_out=%lld)",
+                    (long long)B, (long long)N_in, (long long)N_out);
+    const int64_t lim = (int64_t)1 << 24;
+    if (N_in >= lim || N_out >= lim)
+        return fail(DSTD_ERR_SHAPE, "N_in and N_out must be < 2^24");
+    if (B > 65535)
+        return fail(DSTD_ERR_SHAPE, "B = %lld exceeds the supported batch (65535)", (long long)B);
+    return DSTD_OK;
+}
+
+struct DenseWs {
+    size_t row, L, R, dL, dR, G, part, total;
+};
+
+DenseWs dense_ws_layout(int M, int64_t B, int64_t N_in, int64_t N_out, bool backward) {
+    DenseWs w{};
+    size_t off = 0;
+    size_t n = (size_t)(B * N_in);
+    w.row = off; off += align_up(n * sizeof(int));
+    w.L = off; off += align_up(n * sizeof(float));
+    w.R = off; off += align_up(n * sizeof(float));
+    if (backward) {
+        w.dL = off; off += align_up(n * sizeof(float));
+        w.dR = off; off += align_up(n * sizeof(float));
+        w.G = off; off += align_up((size_t)B * (M + 3) * (size_t)N_out * sizeof(float));
+        dstd::DwPlan dp = dstd::plan_dw(B, N_in, N_out);
+        w.part = off;
+        if (dp.nsplit > 1) off += align_up((size_t)dp.nsplit * (size_t)N_out * (size_t)N_in * sizeof(float));
+    }
+    w.total = off;
+    return w;
+}
+
+dstd_status check_ws(void *ws, size_t ws_bytes, size_t need) {
+    if (need == 0) return DSTD_OK;
+    if (!ws) return fail(DSTD_ERR_NULL, "workspace is NULL (%zu bytes needed)", need);
+    if (((uintptr_t)ws) % kAlign != 0) return fail(DSTD_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+    if (ws_bytes < need)
+        return fail(DSTD_ERR_WORKSPACE, "workspace too small: %zu < %zu bytes", ws_bytes, need);
+    return DSTD_OK;
+}
+
+dstd_status hip_status(hipError_t e, const char *what) {
+    if (e == hipSuccess) return DSTD_OK;
+    return fail(DSTD_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+template <typename T> T *at(void *ws, size_t off) {
+    return reinterpret_cast<T *>(static_cast<char *>(ws) + off);
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *dstd_status_string(dstd_status s) {
+    switch (s) {
+        case DSTD_OK: return "ok";
+        case DSTD_ERR_NULL: return "null pointer";
+        case DSTD_ERR_SHAPE: return "invalid shape";
+        case DSTD_ERR_PARAM: return "invalid parameter";
+        case DSTD_ERR_UNSUPPORTED: return "unsupported";
+        case DSTD_ERR_WORKSPACE: return "workspace too small or misaligned";
+        case DSTD_ERR_HIP: return "HIP error";
+    }
+    return "unknown status";
+}
+
+const char *dstd_last_error(void) { return g_err; }
+
+int32_t dstd_version(void) { return 100; }
+
+size_t dstd_lif_forward_workspace_size(const dstd_lif_params *p, int64_t B, int64_t N_in,
+                                       int64_t N_out) {
+    if (check_params(p) != DSTD_OK || check_dims(B, N_in, N_out) != DSTD_OK) return 0;
+    return dense_ws_layout(p->M, B, N_in, N_out, false).total;
+}
+
+size_t dstd_lif_backward_workspace_size(const dstd_lif_params *p, int64_t B, int64_t N_in,
+                                        int64_t N_out) {
+    if (check_params(p) != DSTD_OK || check_dims(B, N_in, N_out) != DSTD_OK) return 0;
+    return dense_ws_layout(p->M, B, N_in, N_out, true).total;
+}
+
+dstd_status dstd_lif_forward(const dstd_lif_params *p, int64_t B, int64_t N_in, int64_t N_out,
+                             const float *t_in, const void *W, dstd_dtype w_dtype, float *t_out,
+                             float *slope, int32_t *q_idx, void *ws, size_t ws_bytes,
+                             void *stream) {
+    dstd_status s = check_params(p);
+    if (s != DSTD_OK) return s;
+    if ((s = check_dims(B, N_in, N_out)) != DSTD_OK) return s;
+    if (w_dtype != DSTD_F32 && w_dtype != DSTD_BF16)
+        return fail(DSTD_ERR_PARAM, "unknown weight dtype %d", (int)w_dtype);
+    if (B * N_out > 0 && (!t_out || !slope || !q_idx))
+        return fail(DSTD_ERR_NULL, "t_out, slope and q_idx are required");
+    if (B * N_in > 0 && !t_in) return fail(DSTD_ERR_NULL, "t_in is NULL");
+    if (N_in * N_out > 0 && !W) return fail(DSTD_ERR_NULL, "W is NULL");
+    DenseWs L = dense_ws_layout(p->M, B, N_in, N_out, false);
+    if ((s = check_ws(ws, ws_bytes, L.total)) != DSTD_OK) return s;
+    if (B * N_out == 0) return DSTD_OK;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    LifConst C = make_const(p);
+    hipError_t e = dstd::launch_bin_events(C, B * N_in, t_in, at<int>(ws, L.row), at<float>(ws, L.L),
+                                           at<float>(ws, L.R), nullptr, nullptr, st);
+    if (e != hipSuccess) return hip_status(e, "bin_events launch");
+    e = dstd::launch_forward(C, B, N_in, N_out, W, w_dtype == DSTD_BF16, at<int>(ws, L.row),
+                             at<float>(ws, L.L), at<float>(ws, L.R), t_out, slope, q_idx, st);
+    return hip_status(e, "forward launch");
+}
+
+dstd_status dstd_lif_backward(const dstd_lif_params *p, int64_t B, int64_t N_in, int64_t N_out,
+                              const float *t_in, const void *W, dstd_dtype w_dtype,
+                              const float *t_out, const float *slope, const int32_t *q_idx,
+                              const float *grad_t_out, float *grad_W, float *grad_t_in, void *ws,
+                              size_t ws_bytes, void *stream) {
+    dstd_status s = check_params(p);
+    if (s != DSTD_OK) return s;
+    if ((s = check_dims(B, N_in, N_out)) != DSTD_OK) return s;
+    if (w_dtype != DSTD_F32 && w_dtype != DSTD_BF16)
+        return fail(DSTD_ERR_PARAM, "unknown weight dtype %d", (int)w_dtype);
+    if (B * N_out > 0 && (!t_out || !slope || !q_idx || !grad_t_out))
+        return fail(DSTD_ERR_NULL, "t_out, slope, q_idx and grad_t_out are required");
+    if (B * N_in > 0 && !t_in) return fail(DSTD_ERR_NULL, "t_in is NULL");
+    if (grad_t_in && N_in * N_out > 0 && !W) return fail(DSTD_ERR_NULL, "W is NULL");
+    DenseWs L = dense_ws_layout(p->M, B, N_in, N_out, true);
+    if ((s = check_ws(ws, ws_bytes, L.total)) != DSTD_OK) return s;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    hipError_t e;
+    // Empty sizes need no special case: with B == 0 the dW kernel writes
+    // zeros, with N_out == 0 the dt_in kernel does (no memset is used, so the
+    // call stays safe to capture in a graph).
+    LifConst C = make_const(p);
+    int *row = at<int>(ws, L.row);
+    float *Lw = at<float>(ws, L.L), *Rw = at<float>(ws, L.R);
+    float *dLw = at<float>(ws, L.dL), *dRw = at<float>(ws, L.dR);
+    float *G = at<float>(ws, L.G);
+    e = dstd::launch_bin_events(C, B * N_in, t_in, row, Lw, Rw, dLw, dRw, st);
+    if (e != hipSuccess) return hip_status(e, "bin_events launch");
+    e = dstd::launch_grad_g(C, B, N_out, t_out, slope, q_idx, grad_t_out, G, st);
+    if (e != hipSuccess) return hip_status(e, "grad_g launch");
+    if (grad_W && N_out * N_in > 0) {
+        e = dstd::launch_dw(C, B, N_in, N_out, G, row, Lw, Rw, grad_W, at<float>(ws, L.part), st);
+        if (e != hipSuccess) return hip_status(e, "dW launch");
+    }
+    if (grad_t_in && B * N_in > 0) {
+        e = dstd::launch_dtin(C, B, N_in, N_out, G, W, w_dtype == DSTD_BF16, row, dLw, dRw,
+                              grad_t_in, st);
+        if (e != hipSuccess) return hip_status(e, "dt_in launch");
+    }
+    return DSTD_OK;
+}
+
+dstd_status dstd_softmax_ce_grad(int64_t B, int64_t N, const float *t_out, const int32_t *labels,
+                                 float tau_soft, float t_cap, float *grad_t, float *loss,
+                                 void *stream) {
+    if (B < 0 || N < 1 || N > 1024) return fail(DSTD_ERR_SHAPE, "need B >= 0 and 1 <= N <= 1024");
+    if (!(isfinite(tau_soft) && tau_soft > 0.f)) return fail(DSTD_ERR_PARAM, "tau_soft must be > 0");
+    if (!isfinite(t_cap)) return fail(DSTD_ERR_PARAM, "t_cap must be finite");
+    if (!loss || (B > 0 && (!t_out || !labels || !grad_t)))
+        return fail(DSTD_ERR_NULL, "t_out, labels, grad_t and loss are required");
+    hipError_t e = dstd::launch_softmax_ce(B, N, t_out, labels, tau_soft, t_cap, grad_t, loss,
+                                           static_cast<hipStream_t>(stream));
+    return hip_status(e, "softmax_ce launch");
+}
+
+dstd_status dstd_mse_grad(int64_t B, int64_t N, const float *t_out, const float *target,
+                          float *grad_t, float *loss, void *stream) {
+    if (B < 0 || N < 1 || N > 1024) return fail(DSTD_ERR_SHAPE, "need B >= 0 and 1 <= N <= 1024");
+    if (!loss || (B > 0 && (!t_out || !target || !grad_t)))
+        return fail(DSTD_ERR_NULL, "t_out, target, grad_t and loss are required");
+    hipError_t e = dstd::launch_mse(B, N, t_out, target, grad_t, loss,
+                                    static_cast<hipStream_t>(stream));
+    return hip_status(e, "mse launch");
+}
+
+dstd_status dstd_lif_conv_forward(const dstd_lif_params *, const dstd_conv_shape *, int64_t,
+                                  const float *, const void *, dstd_dtype, float *, float *,
+                                  int32_t *, void *, size_t, void *) {
+    return fail(DSTD_ERR_UNSUPPORTED, "conv layers are not built yet");
+}
+dstd_status dstd_lif_conv_backward(const dstd_lif_params *, const dstd_conv_shape *, int64_t,
+                                   const float *, const void *, dstd_dtype, const float *,
+                                   const float *, const int32_t *, const float *, float *, float *,
+                                   void *, size_t, void *) {
+    return fail(DSTD_ERR_UNSUPPORTED, "conv layers are not built yet");
+}
+size_t dstd_lif_conv_forward_workspace_size(const dstd_lif_params *, const dstd_conv_shape *,
+                                            int64_t) { return 0; }
+size_t dstd_lif_conv_backward_workspace_size(const dstd_lif_params *, const dstd_conv_shape *,
+                                             int64_t) { return 0; }
+
+}  // extern "C"

@@ -1,0 +1,272 @@
+// dstd_internal.h -- device-side building blocks shared by the DSTD-LIF
+// kernels (gfx950). Not part of the public ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <hip/hip_bf16.h>
+#include <stdint.h>
+
+namespace dstd {
+
+constexpr int kWave = 64;  // CDNA wavefront width
+
+// Layer constants, computed once per call on the host in double precision and
+// rounded to fp32. The kernel K (Table "tab:kernel") is symmetric in the time
+// constants; tv > ti is the canonical order.
+struct LifConst {
+    float tv, ti;          // time constants, tv > ti
+    float inv_tv, inv_ti;  // 1/tv, 1/ti
+    float c;               // tv*ti/(tv - ti)
+    float kappa;           // 1/ti - 1/tv > 0
+    float alpha, beta;     // exp(-dt/tv), exp(-dt/ti): one-interval decays
+    float k_dt;            // K(dt)
+    float inv_em1;         // 1/expm1(-kappa*dt)  (< 0)
+    float kmax_dt;         // max of K on [0, dt]
+    float kmax_last;       // max of K on [0, last_len]
+    float theta;           // V_th
+    float t0, dt;          // grid T_m = t0 + m*dt
+    float last_len;        // t_max - T_M (may be +inf)
+    float slope_floor;     // smallest slope used in the backward pass
+    int M;                 // intervals; M+1 grid points
+    // fp64 copies for the O(M) recurrences (state propagation over all
+    // intervals), so their rounding does not grow with M
+    double alpha_d, beta_d, k_dt_d;
+};
+
+// Event rows in LDS / G tables: row r holds grid point m = r - 1, so the
+// dropped halves of inputs at the grid ends land in the two zero rows
+// r = 0 (m = -1) and r = M + 2 (m = M + 1).
+__device__ __forceinline__ int rows_of(const LifConst &C) { return C.M + 3; }
+
+__device__ __forceinline__ float bf16_to_f32(uint16_t h) {
+    return __uint_as_float(static_cast<uint32_t>(h) << 16);
+}
+
+template <typename WT> struct WLoad;
+template <> struct WLoad<float> {
+    static __device__ __forceinline__ float get(const float *p, int64_t k) { return p[k]; }
+};
+template <> struct WLoad<uint16_t> {
+    static __device__ __forceinline__ float get(const uint16_t *p, int64_t k) { return bf16_to_f32(p[k]); }
+};
+
+// K(u) = c (e^{-u/tv} - e^{-u/ti}) = -c e^{-u/tv} expm1(-kappa u), u >= 0,
+// written with expm1 so small u keeps full relative precision.
+__device__ __forceinline__ float kern(const LifConst &C, float u) {
+    return -C.c * expf(-u * C.inv_tv) * expm1f(-C.kappa * u);
+}
+
+// DSTD events of one input spike (Eq. (DSTD_kernel), Table "tab:DSTD_kernels",
+// row tau_v != tau_I), in forms without cancellation:
+//   q = floor((t - t0)/dt), x = t - T_q in [0, dt), y = dt - x
+//   weight at T_q     : L = e^{x/tv} expm1(-kappa y) / expm1(-kappa dt)
+//   weight at T_{q+1} : R = e^{-y/ti} expm1(-kappa x) / expm1(-kappa dt)
+// and their derivatives with respect to t. `row` = q + 1 (the LDS row of T_q),
+// or -1 when the input contributes nothing (non-finite or out of
+// [T_0 - dt, T_M + dt)). Halves that fall outside the grid are zeroed.
+struct Event { int row; float L, R, dL, dR; };
+
+__device__ __forceinline__ Event bin_event(const LifConst &C, float t) {
+    Event e{-1, 0.f, 0.f, 0.f, 0.f};
+    if (!isfinite(t)) return e;
+    float rel = t - C.t0;
+    float qf = floorf(rel / C.dt);
+    if (!(qf >= -1.f && qf <= static_cast<float>(C.M))) return e;
+    int q = static_cast<int>(qf);
+    float x = fmaf(-qf, C.dt, rel);
+    x = fminf(fmaxf(x, 0.f), C.dt);
+    float y = C.dt - x;
+    float ex = expf(x * C.inv_tv);
+    float ey = expf(-y * C.inv_ti);
+    float my = expm1f(-C.kappa * y);
+    float mx = expm1f(-C.kappa * x);
+    e.L = ex * my * C.inv_em1;
+    e.R = ey * mx * C.inv_em1;
+    e.dL = ex * (my * C.inv_tv + C.kappa * (1.f + my)) * C.inv_em1;
+    e.dR = ey * (mx * C.inv_ti - C.kappa * (1.f + mx)) * C.inv_em1;
+    if (q < 0) { e.L = 0.f; e.dL = 0.f; }
+    if (q >= C.M) { e.R = 0.f; e.dR = 0.f; }
+    e.row = q + 1;
+    return e;
+}
+
+// Potential inside one interval, relative to its left grid point:
+//   v(u) = V e^{-u/tv} + I K(u)
+// where V = v(T_q) and I is the synaptic current just after the event at T_q
+// (the state-space form of v^(t) = sum_{m<=q} w^_m K(t - T_m)).
+struct Seg { float V, I; };
+
+__device__ __forceinline__ void seg_eval(const LifConst &C, const Seg &s, float u, float &f,
+                                         float &fp) {
+    float ev = expf(-u * C.inv_tv);
+    float em = expm1f(-C.kappa * u);
+    float K = -C.c * ev * em;
+    float Kp = C.c * ev * (C.kappa + em * C.inv_ti);  // K'(u)
+    f = fmaf(s.V, ev, s.I * K) - C.theta;
+    fp = fmaf(-s.V * C.inv_tv, ev, s.I * Kp);
+}
+
+// First root of v(u) = theta on [0, hi] given f(0) < 0 <= f(hi): safeguarded
+// Newton started at the left end, keeping the bracket; on the rising piece
+// of v the function is concave in the common cases, where Newton from the
+// left is monotone.
+__device__ __forceinline__ float seg_root(const LifConst &C, const Seg &s, float hi, float &slope) {
+    float lo = 0.f, u = 0.f;
+    float f, fp;
+    seg_eval(C, s, u, f, fp);
+    for (int it = 0; it < 40; ++it) {
+        float un = (fp > 0.f) ? u - f / fp : 0.5f * (lo + hi);
+        if (!(un > lo && un < hi)) un = 0.5f * (lo + hi);
+        float step = un - u;
+        u = un;
+        seg_eval(C, s, u, f, fp);
+        if (f < 0.f) lo = u; else hi = u;
+        if (fabsf(step) <= 1e-7f * C.dt || hi - lo <= 1e-7f * C.dt) break;
+    }
+    slope = fp;
+    return u;
+}
+
+// Does the interval [0, len) (len = dt, or last_len for q = M) contain the
+// first crossing? v_end is v at the interval's right end when finite (the
+// recurrence value that also starts the next interval). Returns the root.
+__device__ __forceinline__ bool seg_crossing(const LifConst &C, const Seg &s, float len,
+                                             float v_end, bool end_finite, float &u_out,
+                                             float &slope) {
+    if (s.V >= C.theta) {  // only reachable through rounding: v is continuous
+        float f, fp;
+        seg_eval(C, s, 0.f, f, fp);
+        u_out = 0.f;
+        slope = fp;
+        return true;
+    }
+    if (end_finite && v_end >= C.theta) {
+        u_out = seg_root(C, s, len, slope);
+        return true;
+    }
+    // interior maximum: v'(u*) = 0 with e^{-kappa u*} = (ti/tv)(1 + V/(c I))
+    if (s.I > 0.f) {
+        float r = (C.ti * C.inv_tv) * (1.f + s.V / (C.c * s.I));
+        if (r > 0.f && r < 1.f) {
+            float us = -logf(r) / C.kappa;
+            if (us > 0.f && us < len) {
+                float f, fp;
+                seg_eval(C, s, us, f, fp);
+                if (f >= 0.f) {
+                    u_out = seg_root(C, s, us, slope);
+                    return true;
+                }
+            }
+        }
+    }
+    return false;
+}
+
+// Scan over the M+1 intervals of one neuron with its weighted events read by
+// `wq(m)` (Table "tab:timing_DSTD", Eq. (timing_DSTD)): the earliest interval
+// whose candidate lies inside it.
+template <typename F>
+__device__ __forceinline__ void scan_neuron(const LifConst &C, F wq, float &t_out, float &slope,
+                                            int &q_out) {
+    // The state (v at T_q, current after the event at T_q) is propagated in
+    // fp64: over M intervals fp32 rounding of the recurrence would grow with M.
+    // Interval tests and the root solve use the fp32-rounded state.
+    double Vd = 0.0, Id = 0.0;
+    t_out = INFINITY;
+    slope = 0.f;
+    q_out = -1;
+    for (int q = 0; q <= C.M; ++q) {
+        Id += static_cast<double>(wq(q));
+        const double vn_d = fma(Vd, C.alpha_d, Id * C.k_dt_d);
+        Seg s{static_cast<float>(Vd), static_cast<float>(Id)};
+        bool last = (q == C.M);
+        float len = last ? C.last_len : C.dt;
+        float kmax = last ? C.kmax_last : C.kmax_dt;
+        float ub = fmaxf(s.V, 0.f) + fmaxf(s.I, 0.f) * kmax;
+        if (ub * 1.0001f >= C.theta) {
+            bool fin = !last || isfinite(C.last_len);
+            float vend = static_cast<float>(vn_d);
+            if (last && fin) {
+                float f, fp;
+                seg_eval(C, s, C.last_len, f, fp);
+                vend = f + C.theta;
+            }
+            float u, sl;
+            if (seg_crossing(C, s, len, vend, fin, u, sl)) {
+                t_out = static_cast<float>(fma(static_cast<double>(q), static_cast<double>(C.dt),
+                                               static_cast<double>(C.t0)) +
+                                           static_cast<double>(u));
+                slope = sl;
+                q_out = q;
+                return;
+            }
+        }
+        Vd = vn_d;
+        Id *= C.beta_d;
+    }
+}
+
+// LDS float add without return (ds_add_f32). Each address is owned by one
+// lane, so the order of additions is the program order: deterministic.
+__device__ __forceinline__ void lds_add(float *p, float v) {
+    __hip_atomic_fetch_add(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+}
+
+__device__ __forceinline__ int uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }
+
+// Reads through the constant address space: with a wave-uniform address the
+// compiler emits scalar (SMEM) loads, batched into s_load_dwordx16 when
+// consecutive. Only for data that no kernel in flight writes.
+typedef __attribute__((address_space(4))) const int cint_t;
+typedef __attribute__((address_space(4))) const float cflt_t;
+__device__ __forceinline__ cint_t *as_const(const int *p) { return (cint_t *)p; }
+__device__ __forceinline__ cflt_t *as_const(const float *p) { return (cflt_t *)p; }
+
+// 16 consecutive weights of one row as fp32; `vec` selects 16-byte loads
+// (row start and N_in aligned). Rows past N_out read row 0 and return zeros.
+template <typename WT> struct W16;
+template <> struct W16<float> {
+    static __device__ __forceinline__ void load(const float *p, bool vec, bool ok, float *w) {
+        if (vec) {
+            const float4 *q = reinterpret_cast<const float4 *>(p);
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                float4 v = q[k];
+                w[4 * k] = v.x; w[4 * k + 1] = v.y; w[4 * k + 2] = v.z; w[4 * k + 3] = v.w;
+            }
+        } else {
+#pragma unroll
+            for (int k = 0; k < 16; ++k) w[k] = p[k];
+        }
+        if (!ok) {
+#pragma unroll
+            for (int k = 0; k < 16; ++k) w[k] = 0.f;
+        }
+    }
+};
+template <> struct W16<uint16_t> {
+    static __device__ __forceinline__ void load(const uint16_t *p, bool vec, bool ok, float *w) {
+        if (vec) {
+            const uint4 *q = reinterpret_cast<const uint4 *>(p);
+#pragma unroll
+            for (int k = 0; k < 2; ++k) {
+                uint4 v = q[k];
+                uint32_t u[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+                for (int h = 0; h < 4; ++h) {
+                    w[8 * k + 2 * h] = __uint_as_float(u[h] << 16);
+                    w[8 * k + 2 * h + 1] = __uint_as_float(u[h] & 0xffff0000u);
+                }
+            }
+        } else {
+#pragma unroll
+            for (int k = 0; k < 16; ++k) w[k] = bf16_to_f32(p[k]);
+        }
+        if (!ok) {
+#pragma unroll
+            for (int k = 0; k < 16; ++k) w[k] = 0.f;
+        }
+    }
+};
+
+}  // namespace dstd

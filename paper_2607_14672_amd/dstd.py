@@ -1,0 +1,324 @@
+"""Thin Python binding of the DSTD-LIF C ABI (``include/dstd_lif.h``).
+
+The functions named like the C entry points take plain integers (device
+pointers, sizes, stream handles) and return the status code. The tensor
+helpers below them only marshal arguments: they allocate outputs and
+workspace with PyTorch on the tensors' device, pass ``data_ptr()`` and the
+current stream, and raise on a non-OK status. Every step of the layer runs in
+the HIP library; if ``libdstd_lif.so`` is missing, loading fails loudly.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import math
+import os
+from typing import Optional, Tuple
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libdstd_lif.so")
+
+DSTD_OK = 0
+DSTD_ERR_NULL = -1
+DSTD_ERR_SHAPE = -2
+DSTD_ERR_PARAM = -3
+DSTD_ERR_UNSUPPORTED = -4
+DSTD_ERR_WORKSPACE = -5
+DSTD_ERR_HIP = -6
+DSTD_F32 = 0
+DSTD_BF16 = 1
+DSTD_MAX_M = 256
+
+
+class dstd_lif_params(C.Structure):
+    _fields_ = [("tau_m", C.c_float), ("tau_s", C.c_float), ("threshold", C.c_float),
+                ("M", C.c_int32), ("t0", C.c_float), ("dt", C.c_float), ("t_max", C.c_float),
+                ("flags", C.c_int32)]
+
+
+class dstd_conv_shape(C.Structure):
+    _fields_ = [(k, C.c_int32) for k in ("C_in", "H", "W", "C_out", "KH", "KW", "stride", "pad",
+                                         "pool_in")]
+
+
+class DSTDError(RuntimeError):
+    def __init__(self, fn: str, status: int):
+        lib = _load()
+        self.status = status
+        msg = lib.dstd_status_string(status).decode()
+        detail = lib.dstd_last_error().decode()
+        super().__init__(f"{fn}: {msg} ({status}): {detail}")
+
+
+_lib = None
+_P = C.c_void_p
+_L = C.c_int64
+_S = C.c_size_t
+_I = C.c_int
+_F = C.c_float
+
+# name -> (restype, argtypes)
+_SIGS = {
+    "dstd_lif_forward_workspace_size": (_S, [_P, _L, _L, _L]),
+    "dstd_lif_backward_workspace_size": (_S, [_P, _L, _L, _L]),
+    "dstd_lif_forward": (_I, [_P, _L, _L, _L, _P, _P, _I, _P, _P, _P, _P, _S, _P]),
+    "dstd_lif_backward": (_I, [_P, _L, _L, _L, _P, _P, _I, _P, _P, _P, _P, _P, _P, _P, _S, _P]),
+    "dstd_lif_conv_forward_workspace_size": (_S, [_P, _P, _L]),
+    "dstd_lif_conv_backward_workspace_size": (_S, [_P, _P, _L]),
+    "dstd_lif_conv_forward": (_I, [_P, _P, _L, _P, _P, _I, _P, _P, _P, _P, _S, _P]),
+    "dstd_lif_conv_backward": (_I, [_P, _P, _L, _P, _P, _I, _P, _P, _P, _P, _P, _P, _P, _S, _P]),
+    "dstd_softmax_ce_grad": (_I, [_L, _L, _P, _P, _F, _F, _P, _P, _P]),
+    "dstd_mse_grad": (_I, [_L, _L, _P, _P, _P, _P, _P]),
+    "dstd_status_string": (C.c_char_p, [_I]),
+    "dstd_last_error": (C.c_char_p, []),
+    "dstd_version": (C.c_int32, []),
+}
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2607_14672_amd.build`")
+        lib = C.CDLL(LIB_PATH)
+        for name, (res, args) in _SIGS.items():
+            fn = getattr(lib, name)
+            fn.restype = res
+            fn.argtypes = args
+        _lib = lib
+    return _lib
+
+
+def exported_symbols():
+    return list(_SIGS)
+
+
+def _ref(s):
+    return None if s is None else C.addressof(s)
+
+
+# ------------------------------------------------------------ raw C ABI --
+def dstd_lif_forward_workspace_size(p, B, N_in, N_out):
+    return _load().dstd_lif_forward_workspace_size(_ref(p), B, N_in, N_out)
+
+
+def dstd_lif_backward_workspace_size(p, B, N_in, N_out):
+    return _load().dstd_lif_backward_workspace_size(_ref(p), B, N_in, N_out)
+
+
+def dstd_lif_forward(p, B, N_in, N_out, t_in, W, w_dtype, t_out, slope, q_idx, ws, ws_bytes, stream):
+    return _load().dstd_lif_forward(_ref(p), B, N_in, N_out, t_in, W, w_dtype, t_out, slope, q_idx,
+                                    ws, ws_bytes, stream)
+
+
+def dstd_lif_backward(p, B, N_in, N_out, t_in, W, w_dtype, t_out, slope, q_idx, grad_t_out,
+                      grad_W, grad_t_in, ws, ws_bytes, stream):
+    return _load().dstd_lif_backward(_ref(p), B, N_in, N_out, t_in, W, w_dtype, t_out, slope, q_idx,
+                                     grad_t_out, grad_W, grad_t_in, ws, ws_bytes, stream)
+
+
+def dstd_lif_conv_forward_workspace_size(p, cs, B):
+    return _load().dstd_lif_conv_forward_workspace_size(_ref(p), _ref(cs), B)
+
+
+def dstd_lif_conv_backward_workspace_size(p, cs, B):
+    return _load().dstd_lif_conv_backward_workspace_size(_ref(p), _ref(cs), B)
+
+
+def dstd_lif_conv_forward(p, cs, B, t_in, W, w_dtype, t_out, slope, q_idx, ws, ws_bytes, stream):
+    return _load().dstd_lif_conv_forward(_ref(p), _ref(cs), B, t_in, W, w_dtype, t_out, slope, q_idx,
+                                         ws, ws_bytes, stream)
+
+
+def dstd_lif_conv_backward(p, cs, B, t_in, W, w_dtype, t_out, slope, q_idx, grad_t_out, grad_W,
+                           grad_t_in, ws, ws_bytes, stream):
+    return _load().dstd_lif_conv_backward(_ref(p), _ref(cs), B, t_in, W, w_dtype, t_out, slope,
+                                          q_idx, grad_t_out, grad_W, grad_t_in, ws, ws_bytes, stream)
+
+
+def dstd_softmax_ce_grad(B, N, t_out, labels, tau_soft, t_cap, grad_t, loss, stream):
+    return _load().dstd_softmax_ce_grad(B, N, t_out, labels, tau_soft, t_cap, grad_t, loss, stream)
+
+
+def dstd_mse_grad(B, N, t_out, target, grad_t, loss, stream):
+    return _load().dstd_mse_grad(B, N, t_out, target, grad_t, loss, stream)
+
+
+def dstd_status_string(s):
+    return _load().dstd_status_string(s).decode()
+
+
+def dstd_last_error():
+    return _load().dstd_last_error().decode()
+
+
+def dstd_version():
+    return _load().dstd_version()
+
+
+# -------------------------------------------------------- tensor helpers --
+def make_params(tau_m, tau_s, threshold, M, t0, dt, t_max=math.inf) -> dstd_lif_params:
+    return dstd_lif_params(float(tau_m), float(tau_s), float(threshold), int(M), float(t0),
+                           float(dt), float(t_max), 0)
+
+
+def make_conv_shape(C_in, H, W, C_out, KH=3, KW=3, stride=1, pad=1, pool_in=1) -> dstd_conv_shape:
+    return dstd_conv_shape(C_in, H, W, C_out, KH, KW, stride, pad, pool_in)
+
+
+def conv_out_hw(cs: dstd_conv_shape) -> Tuple[int, int]:
+    H, W = cs.H, cs.W
+    if cs.pool_in == 2:
+        H, W = H // 2, W // 2
+    elif cs.pool_in == 0:
+        H, W = 1, 1
+    return (H + 2 * cs.pad - cs.KH) // cs.stride + 1, (W + 2 * cs.pad - cs.KW) // cs.stride + 1
+
+
+def _torch():
+    import torch
+    return torch
+
+
+def _stream(dev):
+    return _torch().cuda.current_stream(dev).cuda_stream
+
+
+def _wdtype(W):
+    torch = _torch()
+    if W.dtype == torch.float32:
+        return DSTD_F32
+    if W.dtype == torch.bfloat16:
+        return DSTD_BF16
+    raise TypeError(f"W must be float32 or bfloat16, got {W.dtype}")
+
+
+def _check(name, st):
+    if st != DSTD_OK:
+        raise DSTDError(name, st)
+
+
+def _cont(x, dtype=None):
+    if dtype is not None:
+        assert x.dtype == dtype, f"expected {dtype}, got {x.dtype}"
+    assert x.is_cuda, "tensors must live on the GPU"
+    return x.contiguous()
+
+
+def _ptr(x):
+    return None if x is None else x.data_ptr()
+
+
+def workspace(nbytes: int, device):
+    torch = _torch()
+    return torch.empty(max(int(nbytes), 1), dtype=torch.uint8, device=device)
+
+
+def forward(p: dstd_lif_params, t_in, W, ws=None):
+    """Dense layer forward. t_in [B, N_in] f32, W [N_out, N_in] f32|bf16 (CUDA tensors)."""
+    torch = _torch()
+    t_in = _cont(t_in, torch.float32)
+    W = _cont(W)
+    B, N_in = t_in.shape
+    N_out = W.shape[0]
+    assert W.shape[1] == N_in
+    dev = t_in.device
+    t_out = torch.empty((B, N_out), dtype=torch.float32, device=dev)
+    slope = torch.empty_like(t_out)
+    q = torch.empty((B, N_out), dtype=torch.int32, device=dev)
+    need = dstd_lif_forward_workspace_size(p, B, N_in, N_out)
+    if ws is None or ws.numel() < need:
+        ws = workspace(need, dev)
+    _check("dstd_lif_forward",
+           dstd_lif_forward(p, B, N_in, N_out, _ptr(t_in), _ptr(W), _wdtype(W), _ptr(t_out),
+                            _ptr(slope), _ptr(q), _ptr(ws), ws.numel(), _stream(dev)))
+    return t_out, slope, q
+
+
+def backward(p: dstd_lif_params, t_in, W, t_out, slope, q, grad_t_out, need_W=True,
+             need_t_in=True, ws=None):
+    """Dense layer backward; returns (grad_W or None, grad_t_in or None)."""
+    torch = _torch()
+    t_in = _cont(t_in, torch.float32)
+    W = _cont(W)
+    B, N_in = t_in.shape
+    N_out = W.shape[0]
+    dev = t_in.device
+    gW = torch.empty((N_out, N_in), dtype=torch.float32, device=dev) if need_W else None
+    gt = torch.empty((B, N_in), dtype=torch.float32, device=dev) if need_t_in else None
+    need = dstd_lif_backward_workspace_size(p, B, N_in, N_out)
+    if ws is None or ws.numel() < need:
+        ws = workspace(need, dev)
+    _check("dstd_lif_backward",
+           dstd_lif_backward(p, B, N_in, N_out, _ptr(t_in), _ptr(W), _wdtype(W),
+                             _ptr(_cont(t_out, torch.float32)), _ptr(_cont(slope, torch.float32)),
+                             _ptr(_cont(q, torch.int32)), _ptr(_cont(grad_t_out, torch.float32)),
+                             _ptr(gW), _ptr(gt), _ptr(ws), ws.numel(), _stream(dev)))
+    return gW, gt
+
+
+def conv_forward(p: dstd_lif_params, cs: dstd_conv_shape, t_in, W, ws=None):
+    """Conv layer forward. t_in [B, C_in, H, W] f32, W [C_out, C_in, KH, KW]."""
+    torch = _torch()
+    t_in = _cont(t_in, torch.float32)
+    W = _cont(W)
+    B = t_in.shape[0]
+    Ho, Wo = conv_out_hw(cs)
+    dev = t_in.device
+    t_out = torch.empty((B, cs.C_out, Ho, Wo), dtype=torch.float32, device=dev)
+    slope = torch.empty_like(t_out)
+    q = torch.empty((B, cs.C_out, Ho, Wo), dtype=torch.int32, device=dev)
+    need = dstd_lif_conv_forward_workspace_size(p, cs, B)
+    if ws is None or ws.numel() < need:
+        ws = workspace(need, dev)
+    _check("dstd_lif_conv_forward",
+           dstd_lif_conv_forward(p, cs, B, _ptr(t_in), _ptr(W), _wdtype(W), _ptr(t_out),
+                                 _ptr(slope), _ptr(q), _ptr(ws), ws.numel(), _stream(dev)))
+    return t_out, slope, q
+
+
+def conv_backward(p, cs, t_in, W, t_out, slope, q, grad_t_out, need_W=True, need_t_in=True,
+                  ws=None):
+    torch = _torch()
+    t_in = _cont(t_in, torch.float32)
+    W = _cont(W)
+    B = t_in.shape[0]
+    dev = t_in.device
+    gW = torch.empty(W.shape, dtype=torch.float32, device=dev) if need_W else None
+    gt = torch.empty(t_in.shape, dtype=torch.float32, device=dev) if need_t_in else None
+    need = dstd_lif_conv_backward_workspace_size(p, cs, B)
+    if ws is None or ws.numel() < need:
+        ws = workspace(need, dev)
+    _check("dstd_lif_conv_backward",
+           dstd_lif_conv_backward(p, cs, B, _ptr(t_in), _ptr(W), _wdtype(W),
+                                  _ptr(_cont(t_out, torch.float32)),
+                                  _ptr(_cont(slope, torch.float32)), _ptr(_cont(q, torch.int32)),
+                                  _ptr(_cont(grad_t_out, torch.float32)), _ptr(gW), _ptr(gt),
+                                  _ptr(ws), ws.numel(), _stream(dev)))
+    return gW, gt
+
+
+def softmax_ce_grad(t_out, labels, tau_soft: float = 1.0, t_cap: Optional[float] = None):
+    torch = _torch()
+    t_out = _cont(t_out, torch.float32)
+    labels = _cont(labels, torch.int32)
+    B, N = t_out.shape
+    if t_cap is None:
+        raise ValueError("t_cap is required (time used for outputs that did not fire)")
+    grad = torch.empty_like(t_out)
+    loss = torch.empty((1,), dtype=torch.float32, device=t_out.device)
+    _check("dstd_softmax_ce_grad",
+           dstd_softmax_ce_grad(B, N, _ptr(t_out), _ptr(labels), float(tau_soft), float(t_cap),
+                                _ptr(grad), _ptr(loss), _stream(t_out.device)))
+    return grad, loss
+
+
+def mse_grad(t_out, target):
+    torch = _torch()
+    t_out = _cont(t_out, torch.float32)
+    target = _cont(target, torch.float32)
+    B, N = t_out.shape
+    grad = torch.empty_like(t_out)
+    loss = torch.empty((1,), dtype=torch.float32, device=t_out.device)
+    _check("dstd_mse_grad", dstd_mse_grad(B, N, _ptr(t_out), _ptr(target), _ptr(grad), _ptr(loss),
+                                          _stream(t_out.device)))
+    return grad, loss

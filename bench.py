@@ -1,0 +1,302 @@
+"""DSTD-LIF training-step benchmark on one MI355X.
+
+A step is one forward + backward pass of the whole workload: every layer's
+spike binning, event contraction, interval scan and root solve, the loss
+gradient on the output spike times, and every layer's backward (dL/dW for
+all layers, dL/dt_in for all but the first). All of it runs in the HIP
+library through its C ABI; inputs, weights, outputs and workspaces are
+allocated before the timed region.
+
+Prints ONE JSON line (rank 0) with the throughput in samples/s, the roofline
+of the dominant kernel (timed with the library's hipEvent timer on the stream
+the kernels run on) and the fp64 CPU oracle timed on the host as a baseline.
+
+  python bench.py [--steps K] [--warmup W] [--workload mlp3]
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import glob
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "DSTD LIF fwd+bwd samples/s; % MFMA peak (GEMM) and % HBM peak (scan)"
+# MI355X published peaks (dense, per GPU)
+PEAK_FP32_VECTOR_TFLOPS = 157.3
+PEAK_HBM_GBS = 8000.0
+# algorithmic flops per (sample, input with events, neuron) update: the two
+# halves of an event are multiplied by the weight and added to two bins
+FLOPS_PER_UPDATE = 4
+
+
+def kernel_source_sha():
+    h = hashlib.sha256()
+    for f in sorted(glob.glob(os.path.join(ROOT, "paper_2607_14672_amd", "csrc", "*"))):
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+class Net:
+    """Preallocated buffers and raw C-ABI calls for one workload."""
+
+    def __init__(self, wl, dev):
+        import torch
+        from paper_2607_14672_amd import dstd, workloads
+        self.torch, self.dstd, self.wl, self.dev = torch, dstd, wl, dev
+        d = workloads.Draws(wl)
+        self.draws = d
+        B = wl.batch
+        self.B = B
+        self.stream = torch.cuda.current_stream(dev).cuda_stream
+        self.t0 = torch.from_numpy(d.t_in).to(dev)
+        self.L = []
+        t_prev = self.t0
+        for l, lay in enumerate(wl.layers):
+            if lay.kind != "dense":
+                raise NotImplementedError("bench covers dense workloads")
+            W = torch.from_numpy(d.weights(l)).to(dev)
+            if lay.w_dtype == "bf16":
+                W = W.to(torch.bfloat16)
+            p = dstd.make_params(lay.tau_m, lay.tau_s, lay.threshold, lay.M, lay.t0, lay.dt,
+                                 lay.t_max)
+            e = dict(lay=lay, p=p, W=W, wdt=dstd.DSTD_BF16 if lay.w_dtype == "bf16" else dstd.DSTD_F32,
+                     t_in=t_prev,
+                     t_out=torch.empty((B, lay.n_out), dtype=torch.float32, device=dev),
+                     slope=torch.empty((B, lay.n_out), dtype=torch.float32, device=dev),
+                     q=torch.empty((B, lay.n_out), dtype=torch.int32, device=dev),
+                     g_out=torch.empty((B, lay.n_out), dtype=torch.float32, device=dev),
+                     gW=torch.empty((lay.n_out, lay.n_in), dtype=torch.float32, device=dev))
+            e["ws_f"] = dstd.workspace(dstd.dstd_lif_forward_workspace_size(p, B, lay.n_in, lay.n_out), dev)
+            e["ws_b"] = dstd.workspace(dstd.dstd_lif_backward_workspace_size(p, B, lay.n_in, lay.n_out), dev)
+            self.L.append(e)
+            t_prev = e["t_out"]
+        for l in range(1, len(self.L)):
+            self.L[l]["g_in_buf"] = self.L[l - 1]["g_out"]
+        last = wl.layers[-1]
+        self.t_cap = float(last.t0 + last.M * last.dt + 2.0)
+        if wl.loss == "ce":
+            self.labels = torch.from_numpy(d.labels).to(dev)
+        else:
+            self.targets = torch.from_numpy(d.targets).to(dev)
+        self.loss = torch.empty((1,), dtype=torch.float32, device=dev)
+
+    def _ck(self, name, st):
+        if st != 0:
+            raise self.dstd.DSTDError(name, st)
+
+    def forward(self):
+        ds = self.dstd
+        for e in self.L:
+            lay = e["lay"]
+            self._ck("dstd_lif_forward", ds.dstd_lif_forward(
+                e["p"], self.B, lay.n_in, lay.n_out, e["t_in"].data_ptr(), e["W"].data_ptr(), e["wdt"],
+                e["t_out"].data_ptr(), e["slope"].data_ptr(), e["q"].data_ptr(),
+                e["ws_f"].data_ptr(), e["ws_f"].numel(), self.stream))
+
+    def loss_grad(self):
+        ds = self.dstd
+        e = self.L[-1]
+        if self.wl.loss == "ce":
+            self._ck("dstd_softmax_ce_grad", ds.dstd_softmax_ce_grad(
+                self.B, e["lay"].n_out, e["t_out"].data_ptr(), self.labels.data_ptr(), 1.0, self.t_cap,
+                e["g_out"].data_ptr(), self.loss.data_ptr(), self.stream))
+        else:
+            self._ck("dstd_mse_grad", ds.dstd_mse_grad(
+                self.B, e["lay"].n_out, e["t_out"].data_ptr(), self.targets.data_ptr(),
+                e["g_out"].data_ptr(), self.loss.data_ptr(), self.stream))
+
+    def backward(self):
+        ds = self.dstd
+        for l in reversed(range(len(self.L))):
+            e = self.L[l]
+            lay = e["lay"]
+            g_in = e["g_in_buf"].data_ptr() if l > 0 else None
+            self._ck("dstd_lif_backward", ds.dstd_lif_backward(
+                e["p"], self.B, lay.n_in, lay.n_out, e["t_in"].data_ptr(), e["W"].data_ptr(), e["wdt"],
+                e["t_out"].data_ptr(), e["slope"].data_ptr(), e["q"].data_ptr(), e["g_out"].data_ptr(),
+                e["gW"].data_ptr(), g_in, e["ws_b"].data_ptr(), e["ws_b"].numel(), self.stream))
+
+    def step(self):
+        self.forward()
+        self.loss_grad()
+        self.backward()
+
+    def activity(self):
+        """Per layer: inputs with events (in-grid), fraction of neurons firing."""
+        out = []
+        for e in self.L:
+            lay = e["lay"]
+            t = e["t_in"].float().cpu().numpy()
+            lo, hi = lay.t0 - lay.dt, lay.t0 + (lay.M + 1) * lay.dt
+            ing = np.isfinite(t) & (t >= lo) & (t < hi)
+            q = e["q"].cpu().numpy()
+            out.append(dict(in_grid_inputs=int(ing.sum()), in_grid_frac=float(ing.mean()),
+                            fire_frac=float((q >= 0).mean())))
+        return out
+
+
+def kernel_algorithmic_flops(net, act):
+    """Algorithmic flops of one step, per kernel name (2-sparse events:
+    FLOPS_PER_UPDATE per (sample, input with events, neuron))."""
+    fl = {"fwd_dense": 0.0, "dw_dense": 0.0, "dtin_dense": 0.0}
+    for l, (e, a) in enumerate(zip(net.L, act)):
+        upd = a["in_grid_inputs"] * e["lay"].n_out
+        fl["fwd_dense"] += FLOPS_PER_UPDATE * upd
+        fl["dw_dense"] += FLOPS_PER_UPDATE * upd
+        if l > 0:
+            fl["dtin_dense"] += FLOPS_PER_UPDATE * upd
+    return fl
+
+
+def traffic_for(kernel, workload, sha):
+    """HBM bytes per step of `kernel` from the committed rocprofv3 counter
+    summary, or None if none exists or the kernels changed since."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{kernel}_{workload}.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        d = json.load(f)
+    if d.get("kernel_source_sha") != sha:
+        return None
+    return d.get("hbm_bytes_per_step")
+
+
+def cpu_baseline(wl, min_seconds=10.0):
+    """The fp64 oracle (as it stands) on the host: fwd + bwd of the whole
+    workload on its full batch, repeated until min_seconds of CPU work."""
+    import oracle
+    from paper_2607_14672_amd import workloads
+    d = workloads.Draws(wl)
+    Ws = [d.weights(l) for l in range(len(wl.layers))]
+    reps, n, t_start = 0, 0, time.perf_counter()
+    while True:
+        t = d.t_in
+        fw = []
+        for l, lay in enumerate(wl.layers):
+            r = oracle.dstd_forward(lay.params(), t, Ws[l])
+            fw.append((t, r))
+            t = r["t_out"].astype(np.float32)
+        to = fw[-1][1]["t_out"]
+        last = wl.layers[-1]
+        if wl.loss == "ce":
+            cap = last.t0 + last.M * last.dt + 2.0
+            tt = np.where(np.isfinite(to), to, cap)
+            z = -tt
+            s = np.exp(z - z.max(1, keepdims=True))
+            s /= s.sum(1, keepdims=True)
+            g = np.where(np.isfinite(to), -(s - np.eye(to.shape[1])[d.labels]) / to.shape[0], 0.0)
+        else:
+            g = np.where(np.isfinite(to), (to - d.targets) / to.shape[0], 0.0)
+        for l in reversed(range(len(wl.layers))):
+            tin, r = fw[l]
+            _, gx = oracle.dstd_backward(wl.layers[l].params(), tin, Ws[l], r,
+                                         np.where(r["q"] >= 0, g, 0.0), want_dt=l > 0)
+            if l > 0:
+                g = gx
+        reps += 1
+        n += wl.batch
+        el = time.perf_counter() - t_start
+        if el >= min_seconds:
+            break
+    return dict(value=n / el, unit="samples/s", cores=oracle.num_threads(), kind="oracle",
+                sample=f"{reps} x full batch of {wl.batch} samples (fwd+bwd of all layers, fp64), "
+                       f"{el:.1f} s")
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", default="mlp3")
+    ap.add_argument("--profile-steps", type=int, default=20)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="also run a 256 MiB device copy (HBM counter calibration)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py: this build measures one GPU only; --gpus {args.gpus} is not supported "
+              "(the data-parallel design is described, not built).", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2607_14672_amd import dstd, workloads
+    dstd._load()
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    wl = workloads.get(args.workload)
+    net = Net(wl, dev)
+
+    for _ in range(args.warmup):
+        net.step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        net.step()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    ms = 1e3 * elapsed / max(args.steps, 1)
+    value = wl.batch * args.steps / elapsed
+
+    # per-kernel durations with the library's hipEvent timer (separate pass)
+    act = net.activity()
+    dstd.dstd_profile_reset()
+    dstd.dstd_profile_enable(True)
+    for _ in range(args.profile_steps):
+        net.step()
+    torch.cuda.synchronize()
+    dstd.dstd_profile_enable(False)
+    prof = dstd.profile_table()
+    per_step = {k: v[1] / args.profile_steps for k, v in prof.items()}
+    launches = {k: v[0] / args.profile_steps for k, v in prof.items()}
+    dom = max(per_step, key=per_step.get)
+    flops = kernel_algorithmic_flops(net, act)
+    sha = kernel_source_sha()
+    roof = None
+    if dom in flops:
+        achieved = flops[dom] / (per_step[dom] * 1e-3) / 1e12
+        roof = dict(bound="alu", achieved=round(achieved, 3), peak=PEAK_FP32_VECTOR_TFLOPS,
+                    unit="TFLOP/s", frac=round(achieved / PEAK_FP32_VECTOR_TFLOPS, 4),
+                    traffic=traffic_for(dom, args.workload, sha), kernel=dom,
+                    kernel_ms_per_step=round(per_step[dom], 4),
+                    avg_launch_ms=round(per_step[dom] / launches[dom], 4),
+                    algorithmic_flops_per_step=flops[dom])
+
+    if args.copy_probe:
+        a = torch.empty(64 << 20, dtype=torch.float32, device=dev)
+        b = torch.empty_like(a)
+        for _ in range(3):
+            b.copy_(a)
+        torch.cuda.synchronize()
+
+    cpu = None if args.no_cpu_baseline else cpu_baseline(wl)
+    out = {
+        "metric": METRIC, "value": round(value, 1), "unit": "samples/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "data": "synthetic (seeded uniform spike times; calibrated random weights)",
+        "config": {"workload": wl.description, "name": wl.name, "global_batch": wl.batch,
+                   "layers": [f"{e['lay'].n_in}->{e['lay'].n_out} M={e['lay'].M}" for e in net.L],
+                   "parallelism": "single GPU"},
+        "roofline": roof,
+        "cpu_baseline": cpu,
+        "detail": {"kernel_ms_per_step": {k: round(v, 4) for k, v in sorted(per_step.items())},
+                   "launches_per_step": launches, "activity": act, "kernel_source_sha": sha,
+                   "loss": float(net.loss.cpu())},
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -183,6 +183,25 @@ dstd_status dstd_softmax_ce_grad(int64_t B, int64_t N, const float *t_out, const
 dstd_status dstd_mse_grad(int64_t B, int64_t N, const float *t_out, const float *target,
                           float *grad_t, float *loss, void *stream);
 
+/* ------------------------------------------------------------ profiling -- */
+
+/*
+ * Opt-in per-kernel timing (not from the paper: an instrument for measuring
+ * this library). While enabled, each kernel the library launches is bracketed
+ * by hipEvents on its stream; dstd_profile_collect() waits for them and adds
+ * the durations to per-kernel totals readable with dstd_profile_entry().
+ * Keep it disabled while capturing a stream into a graph.
+ *  dstd_profile_enable : on != 0 enables; returns the previous setting.
+ *  dstd_profile_entry  : idx in [0, dstd_profile_count()); *name stays valid
+ *                        until dstd_profile_reset().
+ */
+int32_t dstd_profile_enable(int32_t on);
+dstd_status dstd_profile_collect(void);
+int32_t dstd_profile_count(void);
+dstd_status dstd_profile_entry(int32_t idx, const char **name, int64_t *launches,
+                               double *total_ms);
+void dstd_profile_reset(void);
+
 /* ----------------------------------------------------------------- misc -- */
 
 const char *dstd_status_string(dstd_status s);

@@ -91,6 +91,8 @@ LifConst make_const(const dstd_lif_params *p) {
     C.alpha_d = exp(-dt / tv);
     C.beta_d = exp(-dt / ti);
     C.k_dt_d = kern_d(tv, ti, dt);
+    C.r_lo_dt = (float)exp(-kap * dt);
+    C.r_lo_last = isinf(last) ? 0.f : (float)exp(-kap * last);
     return C;
 }
 
@@ -107,23 +109,39 @@ dstd_status check_dims(int64_t B, int64_t N_in, int64_t N_out) {
 }
 
 struct DenseWs {
-    size_t row, L, R, dL, dR, G, part, total;
+    size_t row, L, R, dL, dR, G, part, dtpart, wt, sj, sr, sL, sR, nvalid, total;
+    int64_t sstride;
 };
 
 DenseWs dense_ws_layout(int M, int64_t B, int64_t N_in, int64_t N_out, bool backward) {
     DenseWs w{};
     size_t off = 0;
     size_t n = (size_t)(B * N_in);
-    w.row = off; off += align_up(n * sizeof(int));
-    w.L = off; off += align_up(n * sizeof(float));
-    w.R = off; off += align_up(n * sizeof(float));
+    if (!backward) {
+        // forward: transposed weights (room for fp32), sorted events, counts
+        w.wt = off; off += align_up((size_t)N_in * (size_t)N_out * sizeof(float));
+        // sorted event lists: per sample N_in records; the last sample's list
+        // is padded so batched reads past its end stay in the allocation
+        w.sstride = N_in;
+        size_t ns = n + dstd::kSortPad;
+        w.sj = off; off += align_up(ns * sizeof(int));
+        w.sr = off; off += align_up(ns * sizeof(int));
+        w.sL = off; off += align_up(ns * sizeof(float));
+        w.sR = off; off += align_up(ns * sizeof(float));
+        w.nvalid = off; off += align_up((size_t)B * sizeof(int));
+    }
     if (backward) {
+        w.row = off; off += align_up(n * sizeof(int));
+        w.L = off; off += align_up(n * sizeof(float));
+        w.R = off; off += align_up(n * sizeof(float));
         w.dL = off; off += align_up(n * sizeof(float));
         w.dR = off; off += align_up(n * sizeof(float));
         w.G = off; off += align_up((size_t)B * (M + 3) * (size_t)N_out * sizeof(float));
-        dstd::DwPlan dp = dstd::plan_dw(B, N_in, N_out);
+        dstd::DwPlan dp = dstd::plan_dw(B, N_in, N_out, M);
         w.part = off;
         if (dp.nsplit > 1) off += align_up((size_t)dp.nsplit * (size_t)N_out * (size_t)N_in * sizeof(float));
+        w.dtpart = off;
+        off += align_up(dstd::dtin_partial_bytes(M, B, N_in, N_out));
     }
     w.total = off;
     return w;
@@ -198,11 +216,10 @@ dstd_status dstd_lif_forward(const dstd_lif_params *p, int64_t B, int64_t N_in, 
     if (B * N_out == 0) return DSTD_OK;
     hipStream_t st = static_cast<hipStream_t>(stream);
     LifConst C = make_const(p);
-    hipError_t e = dstd::launch_bin_events(C, B * N_in, t_in, at<int>(ws, L.row), at<float>(ws, L.L),
-                                           at<float>(ws, L.R), nullptr, nullptr, st);
-    if (e != hipSuccess) return hip_status(e, "bin_events launch");
-    e = dstd::launch_forward(C, B, N_in, N_out, W, w_dtype == DSTD_BF16, at<int>(ws, L.row),
-                             at<float>(ws, L.L), at<float>(ws, L.R), t_out, slope, q_idx, st);
+    dstd::SortedEv srt{at<int>(ws, L.sj), at<int>(ws, L.sr), at<float>(ws, L.sL),
+                       at<float>(ws, L.sR), L.sstride};
+    hipError_t e = dstd::launch_forward(C, B, N_in, N_out, W, w_dtype == DSTD_BF16, at<void>(ws, L.wt),
+                                        srt, at<int>(ws, L.nvalid), t_in, t_out, slope, q_idx, st);
     return hip_status(e, "forward launch");
 }
 
@@ -242,7 +259,7 @@ dstd_status dstd_lif_backward(const dstd_lif_params *p, int64_t B, int64_t N_in,
     }
     if (grad_t_in && B * N_in > 0) {
         e = dstd::launch_dtin(C, B, N_in, N_out, G, W, w_dtype == DSTD_BF16, row, dLw, dRw,
-                              grad_t_in, st);
+                              grad_t_in, at<float>(ws, L.dtpart), st);
         if (e != hipSuccess) return hip_status(e, "dt_in launch");
     }
     return DSTD_OK;

@@ -9,6 +9,7 @@
 // solve read the bins straight from LDS, so w^ never goes to HBM.
 #include "dstd_internal.h"
 #include "dstd_kernels.h"
+#include "dstd_profile.h"
 
 #include <algorithm>
 
@@ -36,89 +37,225 @@ __global__ __launch_bounds__(256) void bin_events_kernel(LifConst C, int64_t n,
     }
 }
 
-// --------------------------------------------------------------- forward --
-// Block = `waves` wavefronts; lane = neuron i within a 64-neuron tile; each
-// wave owns `spw` samples and a private LDS bin table [spw][M+3][64]. For
-// every input j the lane multiplies its weight W[i, j] (kept in registers and
-// reused for all the wave's samples) by the two event weights of (b, j) and
-// adds them to bins row and row+1 of its own column: one ds_add_f32 each,
-// conflict-free (64 consecutive words), in program order.
+// ----------------------------------------------------------- event sort --
+// Per sample, the inputs that have events, sorted by event row (stable: j
+// ascending within a row), as structure-of-arrays records {j, row, L, R}.
+// One block of kSortWaves wavefronts per sample; wave w owns a contiguous
+// range of inputs. Row histograms per wave (integer LDS atomics, order-free)
+// give every (row, wave) pair its start offset; each wave then places its
+// inputs 64 at a time, each lane ranked among the lanes of its batch with the
+// same row. The fixed order keeps every sum of the forward pass bitwise
+// reproducible.
+constexpr int kSortWaves = 8;
+
+__global__ __launch_bounds__(kSortWaves * 64) void bin_sort_kernel(LifConst C, int N_in,
+                                                                   const float *__restrict__ t_in,
+                                                                   SortedEv srt,
+                                                                   int *__restrict__ n_valid) {
+    extern __shared__ int sh[];  // hist [kSortWaves][R], rowstart [R + 1]
+    const int b = blockIdx.x;
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = uniform(threadIdx.x >> 6);
+    const int R = rows_of(C);
+    int *hist = sh;
+    int *rowstart = sh + kSortWaves * R;
+    const float *tb = t_in + static_cast<int64_t>(b) * N_in;
+    const int per = ((N_in + kSortWaves * kWave - 1) / (kSortWaves * kWave)) * kWave;
+    const int j_lo = wave * per, j_hi = min(N_in, j_lo + per);
+    for (int k = threadIdx.x; k < kSortWaves * R + R + 1; k += blockDim.x) sh[k] = 0;
+    __syncthreads();
+    for (int j0 = j_lo; j0 < j_hi; j0 += kWave) {
+        const int j = j0 + lane;
+        const int r = (j < j_hi) ? bin_row(C, tb[j]) : -1;
+        if (r >= 0) atomicAdd(&hist[wave * R + r], 1);
+    }
+    __syncthreads();
+    for (int r = threadIdx.x; r < R; r += blockDim.x) {
+        int t = 0;
+        for (int w = 0; w < kSortWaves; ++w) t += hist[w * R + r];
+        rowstart[r + 1] = t;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        for (int r = 1; r <= R; ++r) rowstart[r] += rowstart[r - 1];
+        n_valid[b] = rowstart[R];
+    }
+    __syncthreads();
+    for (int r = threadIdx.x; r < R; r += blockDim.x) {
+        int base = rowstart[r];
+        for (int w = 0; w < kSortWaves; ++w) {
+            const int h = hist[w * R + r];
+            hist[w * R + r] = base;  // becomes this wave's next slot in row r
+            base += h;
+        }
+    }
+    __syncthreads();
+    const int64_t ob = static_cast<int64_t>(b) * srt.stride;
+    int *next = hist + wave * R;
+    for (int j0 = j_lo; j0 < j_hi; j0 += kWave) {
+        const int j = j0 + lane;
+        Event e{-1, 0.f, 0.f, 0.f, 0.f};
+        if (j < j_hi) e = bin_event(C, tb[j]);
+        const int r = e.row;
+        int rank = 0, total = 0;
+#pragma unroll
+        for (int l = 0; l < kWave; ++l) {
+            const int rl = __shfl(r, l);
+            const bool same = (rl == r);
+            rank += (same && l < lane) ? 1 : 0;
+            total += same ? 1 : 0;
+        }
+        const int pos = (r >= 0) ? next[r] + rank : 0;
+        if (r >= 0) {
+            const int64_t o = ob + pos;
+            srt.j[o] = j;
+            srt.r[o] = r;
+            srt.L[o] = e.L;
+            srt.R[o] = e.R;
+        }
+        __builtin_amdgcn_wave_barrier();
+        if (r >= 0 && rank == total - 1) next[r] = pos + 1;  // one lane per row
+        __builtin_amdgcn_wave_barrier();
+    }
+}
+
+// W [N_out][N_in] -> WT [N_in][N_out] through a padded LDS tile.
 template <typename WT>
-__global__ __launch_bounds__(256) void fwd_dense_kernel(LifConst C, int B, int N_in, int N_out,
-                                                         int spw, int vec,
-                                                         const WT *__restrict__ W,
-                                                         const int *__restrict__ ev_row,
-                                                         const float *__restrict__ ev_L,
-                                                         const float *__restrict__ ev_R,
+__global__ __launch_bounds__(256) void transpose_kernel(int rows, int cols,
+                                                        const WT *__restrict__ in,
+                                                        WT *__restrict__ out) {
+    __shared__ WT tile[32][33];
+    const int c0 = blockIdx.x * 32, r0 = blockIdx.y * 32;
+    const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;  // 32 x 8
+    for (int k = ty; k < 32; k += 8) {
+        const int r = r0 + k, c = c0 + tx;
+        if (r < rows && c < cols) tile[k][tx] = in[static_cast<int64_t>(r) * cols + c];
+    }
+    __syncthreads();
+    for (int k = ty; k < 32; k += 8) {
+        const int c = c0 + k, r = r0 + tx;
+        if (r < rows && c < cols) out[static_cast<int64_t>(c) * rows + r] = tile[tx][k];
+    }
+}
+
+// --------------------------------------------------------------- forward --
+// Lane = neuron i of a 64-neuron tile, one sample per wavefront (4 per block).
+// The wave walks its sample's events in grid order: each record adds
+// W[i, j] L and W[i, j] R to the running sums of its row (WT row j is one
+// coalesced 256-byte load with a scalar base). When a row closes, grid point
+// m = row - 1 is complete (its L parts come from this row, its R parts from
+// the previous one) and goes straight into the interval scan: the weighted
+// events never exist in memory. Once every lane has found its crossing
+// interval, later events cannot change the outputs and the wave stops.
+constexpr int kBatch = 8;
+
+template <typename WT>
+__global__ __launch_bounds__(256) void fwd_sorted_kernel(LifConst C, int B, int N_in, int N_out,
+                                                         const WT *__restrict__ Wt,
+                                                         SortedEv srt,
+                                                         const int *__restrict__ n_valid,
                                                          float *__restrict__ t_out,
                                                          float *__restrict__ slope,
                                                          int *__restrict__ q_idx) {
-    extern __shared__ float lds[];
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = uniform(threadIdx.x >> 6);
     const int waves = blockDim.x >> 6;
-    const int R = rows_of(C);
     const int i = blockIdx.x * kWave + lane;
-    const int b0 = uniform((blockIdx.y * waves + wave) * spw);
-    const int nb = uniform(min(spw, B - b0));
-    if (nb <= 0) return;  // wave-uniform; no block barrier below
-    float *acc = lds + static_cast<int64_t>(wave) * spw * R * kWave;
-    for (int k = lane; k < nb * R * kWave; k += kWave) acc[k] = 0.f;
-
     const bool row_ok = i < N_out;
-    const WT *wrow = W + static_cast<int64_t>(row_ok ? i : 0) * N_in;
-    constexpr int JC = 16;
-    int j0 = 0;
-    for (; j0 + JC <= N_in; j0 += JC) {
-        float w[JC];
-        W16<WT>::load(wrow + j0, vec != 0, row_ok, w);
-        for (int s = 0; s < nb; ++s) {
-            const int64_t base = static_cast<int64_t>(b0 + s) * N_in + j0;
-            cint_t *rp = as_const(ev_row + base);
-            cflt_t *lp = as_const(ev_L + base);
-            cflt_t *qp = as_const(ev_R + base);
-            int r[JC];
-            float l[JC], rr[JC];
+    const int b = uniform(blockIdx.y * waves + wave);
+    if (b >= B) return;  // wave-uniform; the kernel has no block barrier
+    const int n = *as_const(n_valid + b);
+    const int64_t eo = static_cast<int64_t>(b) * srt.stride;
+    const int *ej = srt.j + eo;
+    const int *er = srt.r + eo;
+    const float *eL = srt.L + eo;
+    const float *eR = srt.R + eo;
+    Scan sc;
+    int cur = 0;  // row whose records are being summed
+    float aL = 0.f, aR = 0.f, carry = 0.f;
+    bool done = false;
+    // close rows cur .. target-1: grid point cur-1 gets this row's L sums
+    // plus the previous row's R sums
+    auto close_to = [&](int target) {
+        while (cur < target && !done) {
+            if (cur >= 1) sc.step(C, cur - 1, aL + carry);
+            carry = aR;
+            aL = 0.f;
+            aR = 0.f;
+            ++cur;
+            if (__all(sc.found() || !row_ok)) done = true;
+        }
+    };
+    // All loads are unconditional and branch-free, so the compiler can keep
+    // the next batch's weight loads in flight (in-order vmcnt waits): record
+    // arrays are padded by two batches, records past n are masked by
+    // selects, their input index is clamped into range, and lanes past N_out
+    // read a valid column (their results are never stored).
+    const int64_t col = row_ok ? i : 0;
+    auto wload = [&](int j) {
+        const int js = (static_cast<unsigned>(j) < static_cast<unsigned>(N_in)) ? j : 0;
+        return WLoad<WT>::get(Wt, static_cast<int64_t>(js) * N_out + col);
+    };
+    float w[kBatch], wn[kBatch];
 #pragma unroll
-            for (int jj = 0; jj < JC; ++jj) {
-                r[jj] = rp[jj];
-                l[jj] = lp[jj];
-                rr[jj] = qp[jj];
-            }
-            float *a = acc + s * R * kWave + lane;
+    for (int kk = 0; kk < kBatch; ++kk) wn[kk] = wload(as_const(ej)[kk]);
+    for (int k0 = 0; k0 < n && !done; k0 += kBatch) {
+        int rr[kBatch], jj1[kBatch];
+        float ll[kBatch], rv[kBatch];
+        const int nk = min(kBatch, n - k0);
 #pragma unroll
-            for (int jj = 0; jj < JC; ++jj) {
-                if (r[jj] < 0) continue;
-                float *p = a + r[jj] * kWave;
-                lds_add(p, w[jj] * l[jj]);
-                lds_add(p + kWave, w[jj] * rr[jj]);
+        for (int kk = 0; kk < kBatch; ++kk) {
+            w[kk] = wn[kk];
+            const bool in = kk < nk;
+            const int r = as_const(er + k0)[kk];
+            const float l = as_const(eL + k0)[kk];
+            const float v = as_const(eR + k0)[kk];
+            rr[kk] = in ? r : 0x7fffffff;
+            ll[kk] = in ? l : 0.f;
+            rv[kk] = in ? v : 0.f;
+            jj1[kk] = as_const(ej + k0 + kBatch)[kk];
+        }
+        // the next batch's weights are in flight while this one is consumed
+#pragma unroll
+        for (int kk = 0; kk < kBatch; ++kk) wn[kk] = wload(jj1[kk]);
+        if (nk == kBatch && rr[kBatch - 1] == cur) {
+            // common case: the whole batch continues the current row
+#pragma unroll
+            for (int kk = 0; kk < kBatch; ++kk) {
+                aL = fmaf(w[kk], ll[kk], aL);
+                aR = fmaf(w[kk], rv[kk], aR);
             }
+            continue;
+        }
+        int kk_start = 0;
+        while (!done) {
+            int stop = kBatch, target = 0;
+#pragma unroll
+            for (int kk = 0; kk < kBatch; ++kk) {
+                if (kk >= kk_start && kk < stop && kk < nk) {
+                    if (rr[kk] == cur) {
+                        aL = fmaf(w[kk], ll[kk], aL);
+                        aR = fmaf(w[kk], rv[kk], aR);
+                    } else {
+                        stop = kk;
+                        target = rr[kk];
+                    }
+                }
+            }
+            if (stop >= kBatch || stop >= nk) break;
+            close_to(target);
+            kk_start = stop;
         }
     }
-    for (; j0 < N_in; ++j0) {  // ragged tail of the inputs
-        float w = row_ok ? WLoad<WT>::get(wrow, j0) : 0.f;
-        for (int s = 0; s < nb; ++s) {
-            const int64_t base = static_cast<int64_t>(b0 + s) * N_in + j0;
-            int r = *as_const(ev_row + base);
-            if (r < 0) continue;
-            float *p = acc + s * R * kWave + lane + r * kWave;
-            lds_add(p, w * *as_const(ev_L + base));
-            lds_add(p + kWave, w * *as_const(ev_R + base));
-        }
-    }
-    __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): LDS adds retired
-    __builtin_amdgcn_wave_barrier();
+    close_to(C.M + 2);  // row M+2 has no records
     if (!row_ok) return;
-    for (int s = 0; s < nb; ++s) {
-        const float *col = acc + s * R * kWave + lane + kWave;  // row 1 = grid point 0
-        float to, sl;
-        int q;
-        scan_neuron(C, [&](int m) { return col[m * kWave]; }, to, sl, q);
-        int64_t o = static_cast<int64_t>(b0 + s) * N_out + i;
-        t_out[o] = to;
-        slope[o] = sl;
-        q_idx[o] = q;
-    }
+    float to, sl;
+    int q;
+    sc.finish(C, to, sl, q);
+    const int64_t o = static_cast<int64_t>(b) * N_out + i;
+    t_out[o] = to;
+    slope[o] = sl;
+    q_idx[o] = q;
 }
 
 // ------------------------------------------------------------ scan grads --
@@ -162,80 +299,73 @@ __global__ __launch_bounds__(256) void grad_g_kernel(LifConst C, int B, int N_ou
 }
 
 // ----------------------------------------------------------------- dW ----
-// dW[i, j] = sum_b (G[b, row_bj, i] L_bj + G[b, row_bj + 1, i] R_bj).
-// Block tile: 64 neurons (lanes) x waves*JW inputs (each wave JW inputs in
-// registers); loop over this block's share of the batch, staging G[b, :, tile]
-// in LDS. Batch splits write partial sums reduced in a fixed order.
-template <int JW>
-__global__ __launch_bounds__(512) void dw_dense_kernel(LifConst C, int B, int N_in, int N_out,
-                                                        int b_per_split, int nbs,
+// dW[i, j] = sum_b (G[b, r_bj, i] L_bj + G[b, r_bj + 1, i] R_bj).
+// Lane = input j (events are coalesced vector loads); a block covers
+// 4 x 64 inputs and a tile of TI neurons whose sums stay in registers over
+// its share of the batch. G[b, :, tile] is staged in LDS (double buffered)
+// as pairs (G[r], G[r+1]) per neuron, so one 8-byte read with an immediate
+// neuron offset serves both halves of an event. Slot R-1 is a zero pair for
+// inputs without events. Batch splits write partial sums, reduced in order.
+template <int TI>
+__global__ __launch_bounds__(256) void dw_dense_kernel(LifConst C, int B, int N_in, int N_out,
+                                                        int b_per_split, int pstride,
                                                         const float *__restrict__ G,
                                                         const int *__restrict__ ev_row,
                                                         const float *__restrict__ ev_L,
                                                         const float *__restrict__ ev_R,
                                                         float *__restrict__ dW_part) {
-    extern __shared__ float gs[];  // [nbs][R][64]
-    const int lane = threadIdx.x & (kWave - 1);
-    const int wave = uniform(threadIdx.x >> 6);
-    const int waves = blockDim.x >> 6;
+    extern __shared__ float2 ps[];  // [2][TI][pstride]
     const int R = rows_of(C);
-    const int i0 = blockIdx.x * kWave;
-    const int i = i0 + lane;
-    const int jb = uniform(blockIdx.y * waves * JW + wave * JW);
+    const int j = blockIdx.x * blockDim.x + threadIdx.x;
+    const int i0 = blockIdx.y * TI;
+    const int ni = min(TI, N_out - i0);
     const int b_lo = blockIdx.z * b_per_split;
     const int b_hi = min(B, b_lo + b_per_split);
-    float acc[JW];
+    const bool j_ok = j < N_in;
+    float acc[TI];
 #pragma unroll
-    for (int jj = 0; jj < JW; ++jj) acc[jj] = 0.f;
-    const int nj = uniform(max(0, min(JW, N_in - jb)));
-    for (int bs = b_lo; bs < b_hi; bs += nbs) {
-        const int nbb = min(nbs, b_hi - bs);
-        for (int k = threadIdx.x; k < nbb * R * kWave; k += blockDim.x) {
-            int sb = k / (R * kWave), r = (k / kWave) % R, l = k % kWave;
-            gs[k] = (i0 + l < N_out)
-                        ? G[(static_cast<int64_t>(bs + sb) * R + r) * N_out + i0 + l]
-                        : 0.f;
+    for (int ii = 0; ii < TI; ++ii) acc[ii] = 0.f;
+    auto stage = [&](int b, float2 *buf) {
+        const float *gb = G + static_cast<int64_t>(b) * R * N_out + i0;
+        for (int k = threadIdx.x; k < R * TI; k += blockDim.x) {
+            const int r = k / TI, l = k % TI;
+            const float v = (l < ni) ? gb[static_cast<int64_t>(r) * N_out + l] : 0.f;
+            float2 *row = buf + l * pstride;
+            if (r < R - 1) row[r].x = v;
+            if (r > 0) row[r - 1].y = v;
         }
-        __syncthreads();
-        for (int sb = 0; sb < nbb; ++sb) {
-            const int64_t base = static_cast<int64_t>(bs + sb) * N_in + jb;
-            const float *g = gs + sb * R * kWave + lane;
-            if (nj == JW) {
-                cint_t *rp = as_const(ev_row + base);
-                cflt_t *lp = as_const(ev_L + base);
-                cflt_t *qp = as_const(ev_R + base);
-                int r[JW];
-                float l[JW], rr[JW];
-#pragma unroll
-                for (int jj = 0; jj < JW; ++jj) {
-                    r[jj] = rp[jj];
-                    l[jj] = lp[jj];
-                    rr[jj] = qp[jj];
-                }
-#pragma unroll
-                for (int jj = 0; jj < JW; ++jj) {
-                    if (r[jj] < 0) continue;
-                    float g0 = g[r[jj] * kWave], g1 = g[(r[jj] + 1) * kWave];
-                    acc[jj] = fmaf(g0, l[jj], fmaf(g1, rr[jj], acc[jj]));
-                }
-            } else {
-                for (int jj = 0; jj < nj; ++jj) {
-                    int r = *as_const(ev_row + base + jj);
-                    if (r < 0) continue;
-                    float g0 = g[r * kWave], g1 = g[(r + 1) * kWave];
-                    acc[jj] = fmaf(g0, *as_const(ev_L + base + jj),
-                                   fmaf(g1, *as_const(ev_R + base + jj), acc[jj]));
-                }
+        for (int l = threadIdx.x; l < TI; l += blockDim.x) buf[l * pstride + R - 1] = make_float2(0.f, 0.f);
+    };
+    if (b_lo < b_hi) stage(b_lo, ps);
+    __syncthreads();
+    for (int b = b_lo; b < b_hi; ++b) {
+        float2 *cur = ps + ((b - b_lo) & 1) * TI * pstride;
+        if (b + 1 < b_hi) stage(b + 1, ps + ((b + 1 - b_lo) & 1) * TI * pstride);
+        int slot = R - 1;
+        float L = 0.f, Rv = 0.f;
+        if (j_ok) {
+            const int64_t o = static_cast<int64_t>(b) * N_in + j;
+            const int r = ev_row[o];
+            if (r >= 0) {
+                slot = r;
+                L = ev_L[o];
+                Rv = ev_R[o];
             }
+        }
+        const float2 *p = cur + slot;
+#pragma unroll
+        for (int ii = 0; ii < TI; ++ii) {
+            const float2 g = p[ii * pstride];
+            acc[ii] = fmaf(g.x, L, fmaf(g.y, Rv, acc[ii]));
         }
         __syncthreads();
     }
-    if (i >= N_out) return;
+    if (!j_ok) return;
     float *out = dW_part + static_cast<int64_t>(blockIdx.z) * N_out * N_in +
-                 static_cast<int64_t>(i) * N_in + jb;
+                 static_cast<int64_t>(i0) * N_in + j;
 #pragma unroll
-    for (int jj = 0; jj < JW; ++jj)
-        if (jj < nj) out[jj] = acc[jj];
+    for (int ii = 0; ii < TI; ++ii)
+        if (ii < ni) out[static_cast<int64_t>(ii) * N_in] = acc[ii];
 }
 
 __global__ __launch_bounds__(256) void reduce_splits_kernel(int64_t n, int nsplit,
@@ -249,26 +379,34 @@ __global__ __launch_bounds__(256) void reduce_splits_kernel(int64_t n, int nspli
 }
 
 // ------------------------------------------------------------- dt_in ----
-// dt_in[b, j] = dL_bj sum_i W[i, j] G[b, row, i] + dR_bj sum_i W[i, j] G[b, row+1, i].
-// Lane = input j (coalesced W rows and events); the block keeps SB samples'
-// G tiles for 64 neurons in LDS as (G[r], G[r+1]) pairs per neuron, so one
-// 8-byte LDS read per (b, i, j) serves both halves; slot R-1 is a zero pair
-// used by inputs without events.
+// dt_in[b, j] = dL_bj sum_i W[i, j] G[b, r, i] + dR_bj sum_i W[i, j] G[b, r+1, i]
+// (r = event row of input j in sample b). Lane = input j (coalesced W rows
+// and events); a block holds SB samples' G tiles for 64 neurons in LDS,
+// row-major with an odd row stride (65 words), so the lane-dependent rows r,
+// r+1 of one neuron come from one conflict-free ds_read2_b32 whose neuron
+// offset is an immediate. An extra zero row serves inputs without events.
+// The neuron range may be split across blocks (blockIdx.z): each split
+// writes its partial dt_in, summed in a fixed order.
+constexpr int kDtStride = kWave + 1;
+
 template <int SB, typename WT>
 __global__ __launch_bounds__(256) void dtin_dense_kernel(LifConst C, int B, int N_in, int N_out,
-                                                          int pstride,
+                                                          int i_per_split,
                                                           const float *__restrict__ G,
                                                           const WT *__restrict__ W,
                                                           const int *__restrict__ ev_row,
                                                           const float *__restrict__ ev_dL,
                                                           const float *__restrict__ ev_dR,
-                                                          float *__restrict__ dt_in) {
-    extern __shared__ float2 ps[];  // [SB][64][pstride]
+                                                          float *__restrict__ out) {
+    extern __shared__ float gs[];  // [SB][R + 1][kDtStride]
     const int R = rows_of(C);
+    const int RT = R + 1;
     const int j = blockIdx.x * blockDim.x + threadIdx.x;
     const int b0 = blockIdx.y * SB;
+    const int i_lo = blockIdx.z * i_per_split;
+    const int i_hi = min(N_out, i_lo + i_per_split);
     const bool j_ok = j < N_in;
-    int slot[SB];
+    int base[SB];
     float aL[SB], aR[SB];
 #pragma unroll
     for (int s = 0; s < SB; ++s) {
@@ -276,12 +414,16 @@ __global__ __launch_bounds__(256) void dtin_dense_kernel(LifConst C, int B, int 
         aR[s] = 0.f;
         int b = b0 + s;
         int r = (j_ok && b < B) ? ev_row[static_cast<int64_t>(b) * N_in + j] : -1;
-        slot[s] = (r < 0) ? (R - 1) : r;
+        if (r < 0) r = R - 1;  // rows R-1 and R are zero
+        base[s] = (s * RT + r) * kDtStride;
     }
-    for (int i0 = 0; i0 < N_out; i0 += kWave) {
-        const int ni = min(kWave, N_out - i0);
+    // the extra zero row of every sample tile
+    for (int k = threadIdx.x; k < SB * kDtStride; k += blockDim.x)
+        gs[((k / kDtStride) * RT + R) * kDtStride + (k % kDtStride)] = 0.f;
+    for (int i0 = i_lo; i0 < i_hi; i0 += kWave) {
+        const int ni = min(kWave, i_hi - i0);
         // weights of this neuron chunk for the lane's input, issued before the
-        // barrier so their latency overlaps the G staging
+        // barrier so their latency overlaps the staging
         float w[kWave];
 #pragma unroll
         for (int ii = 0; ii < kWave; ++ii)
@@ -289,36 +431,34 @@ __global__ __launch_bounds__(256) void dtin_dense_kernel(LifConst C, int B, int 
                                       : 0.f;
         __syncthreads();
         for (int k = threadIdx.x; k < SB * R * kWave; k += blockDim.x) {
-            int s = k / (R * kWave);
-            int r = (k / kWave) % R;
-            int l = k % kWave;
-            int b = b0 + s;
-            float v = (b < B && l < ni)
-                          ? G[(static_cast<int64_t>(b) * R + r) * N_out + i0 + l]
-                          : 0.f;
-            float2 *row = ps + (static_cast<int64_t>(s) * kWave + l) * pstride;
-            if (r < R - 1) row[r].x = v;
-            if (r > 0) row[r - 1].y = v;
-            if (r == R - 1) row[R - 1] = make_float2(0.f, 0.f);
+            const int s = k / (R * kWave);
+            const int r = (k / kWave) % R;
+            const int l = k % kWave;
+            const int b = b0 + s;
+            gs[(s * RT + r) * kDtStride + l] =
+                (b < B && l < ni) ? G[(static_cast<int64_t>(b) * R + r) * N_out + i0 + l] : 0.f;
         }
         __syncthreads();
 #pragma unroll
         for (int ii = 0; ii < kWave; ++ii) {
 #pragma unroll
             for (int s = 0; s < SB; ++s) {
-                float2 g = ps[(s * kWave + ii) * pstride + slot[s]];
-                aL[s] = fmaf(w[ii], g.x, aL[s]);
-                aR[s] = fmaf(w[ii], g.y, aR[s]);
+                const float g0 = gs[base[s] + ii];
+                const float g1 = gs[base[s] + kDtStride + ii];
+                aL[s] = fmaf(w[ii], g0, aL[s]);
+                aR[s] = fmaf(w[ii], g1, aR[s]);
             }
         }
     }
     if (!j_ok) return;
 #pragma unroll
     for (int s = 0; s < SB; ++s) {
-        int b = b0 + s;
+        const int b = b0 + s;
         if (b >= B) continue;
-        int64_t o = static_cast<int64_t>(b) * N_in + j;
-        dt_in[o] = (slot[s] == R - 1) ? 0.f : fmaf(aL[s], ev_dL[o], aR[s] * ev_dR[o]);
+        const int64_t o = static_cast<int64_t>(b) * N_in + j;
+        const bool has = (base[s] != (s * RT + R - 1) * kDtStride);
+        out[static_cast<int64_t>(blockIdx.z) * B * N_in + o] =
+            has ? fmaf(aL[s], ev_dL[o], aR[s] * ev_dR[o]) : 0.f;
     }
 }
 
@@ -395,45 +535,50 @@ hipError_t launch_bin_events(const LifConst &C, int64_t n, const float *t_in, in
                              float *R, float *dL, float *dR, hipStream_t st) {
     if (n == 0) return hipSuccess;
     int64_t blocks = (n + 255) / 256;
+    ProfScope prof("bin_events", st);
     hipLaunchKernelGGL(bin_events_kernel, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, st, C,
                        n, t_in, row, L, R, dL, dR);
     return hipGetLastError();
 }
 
-FwdPlan plan_forward(int M, int64_t B) {
-    const int64_t per_sample = static_cast<int64_t>(M + 3) * kWave * sizeof(float);
-    FwdPlan p;
-    p.waves = 4;
-    p.spw = 1;
-    // largest samples-per-wave with <= 72 KB of LDS per block (two blocks per CU)
-    while (p.spw < 4 && p.waves * (p.spw + 1) * per_sample <= 72 * 1024 &&
-           (p.spw + 1) * p.waves <= B)
-        ++p.spw;
-    while (p.waves > 1 && p.waves * p.spw * per_sample > 150 * 1024) --p.waves;
-    p.lds = static_cast<size_t>(p.waves * p.spw * per_sample);
-    return p;
-}
-
 hipError_t launch_forward(const LifConst &C, int64_t B, int64_t N_in, int64_t N_out, const void *W,
-                          bool bf16, const int *row, const float *L, const float *R, float *t_out,
-                          float *slope, int *q_idx, hipStream_t st) {
-    FwdPlan p = plan_forward(C.M, B);
-    dim3 grid(static_cast<unsigned>((N_out + kWave - 1) / kWave),
-              static_cast<unsigned>((B + p.waves * p.spw - 1) / (p.waves * p.spw)));
-    dim3 block(p.waves * kWave);
-    const uintptr_t wa = reinterpret_cast<uintptr_t>(W);
-    if (bf16) {
-        int vec = (N_in % 8 == 0) && (wa % 16 == 0);
-        hipLaunchKernelGGL(fwd_dense_kernel<uint16_t>, grid, block, p.lds, st, C,
-                           static_cast<int>(B), static_cast<int>(N_in), static_cast<int>(N_out),
-                           p.spw, vec, static_cast<const uint16_t *>(W), row, L, R, t_out, slope,
-                           q_idx);
-    } else {
-        int vec = (N_in % 4 == 0) && (wa % 16 == 0);
-        hipLaunchKernelGGL(fwd_dense_kernel<float>, grid, block, p.lds, st, C, static_cast<int>(B),
-                           static_cast<int>(N_in), static_cast<int>(N_out), p.spw, vec,
-                           static_cast<const float *>(W), row, L, R, t_out, slope, q_idx);
+                          bool bf16, void *Wt, SortedEv srt, int *n_valid, const float *t_in,
+                          float *t_out, float *slope, int *q_idx, hipStream_t st) {
+    const int R = C.M + 3;
+    {
+        ProfScope prof("bin_sort", st);
+        hipLaunchKernelGGL(bin_sort_kernel, dim3(static_cast<unsigned>(B)), dim3(kSortWaves * kWave),
+                           (kSortWaves * R + R + 1) * sizeof(int), st, C, static_cast<int>(N_in), t_in,
+                           srt, n_valid);
     }
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    dim3 tg(static_cast<unsigned>((N_in + 31) / 32), static_cast<unsigned>((N_out + 31) / 32));
+    if (N_in > 0) {
+        ProfScope prof("transpose_w", st);
+        if (bf16)
+            hipLaunchKernelGGL(transpose_kernel<uint16_t>, tg, dim3(256), 0, st,
+                               static_cast<int>(N_out), static_cast<int>(N_in),
+                               static_cast<const uint16_t *>(W), static_cast<uint16_t *>(Wt));
+        else
+            hipLaunchKernelGGL(transpose_kernel<float>, tg, dim3(256), 0, st, static_cast<int>(N_out),
+                               static_cast<int>(N_in), static_cast<const float *>(W),
+                               static_cast<float *>(Wt));
+    }
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    constexpr int waves = 4;
+    dim3 grid(static_cast<unsigned>((N_out + kWave - 1) / kWave),
+              static_cast<unsigned>((B + waves - 1) / waves));
+    ProfScope prof("fwd_dense", st);
+    if (bf16)
+        hipLaunchKernelGGL(fwd_sorted_kernel<uint16_t>, grid, dim3(waves * kWave), 0, st, C,
+                           static_cast<int>(B), static_cast<int>(N_in), static_cast<int>(N_out),
+                           static_cast<const uint16_t *>(Wt), srt, n_valid, t_out, slope, q_idx);
+    else
+        hipLaunchKernelGGL(fwd_sorted_kernel<float>, grid, dim3(waves * kWave), 0, st, C,
+                           static_cast<int>(B), static_cast<int>(N_in), static_cast<int>(N_out),
+                           static_cast<const float *>(Wt), srt, n_valid, t_out, slope, q_idx);
     return hipGetLastError();
 }
 
@@ -442,20 +587,23 @@ hipError_t launch_grad_g(const LifConst &C, int64_t B, int64_t N_out, const floa
                          hipStream_t st) {
     int64_t n = B * N_out;
     if (n == 0) return hipSuccess;
+    ProfScope prof("grad_g", st);
     hipLaunchKernelGGL(grad_g_kernel, dim3(static_cast<unsigned>((n + 255) / 256)), dim3(256), 0,
                        st, C, static_cast<int>(B), static_cast<int>(N_out), t_out, slope, q_idx,
                        grad_t, G);
     return hipGetLastError();
 }
 
-DwPlan plan_dw(int64_t B, int64_t N_in, int64_t N_out) {
+static int dw_ti(int M) { return (M + 3 + 1) * 63 * 8 < 65536 ? 64 : 32; }
+
+DwPlan plan_dw(int64_t B, int64_t N_in, int64_t N_out, int M) {
     DwPlan p;
-    p.waves = 8;
-    p.jw = 16;
-    int64_t tiles = ((N_out + kWave - 1) / kWave) * ((N_in + p.waves * p.jw - 1) / (p.waves * p.jw));
+    p.waves = 4;
+    p.jw = dw_ti(M);
+    int64_t tiles = ((N_in + 255) / 256) * ((N_out + p.jw - 1) / p.jw);
     p.nsplit = 1;
-    // aim for >= 2 blocks per CU (256 CUs); keep >= 8 samples per split
-    while (tiles * p.nsplit < 512 && B / (p.nsplit * 2) >= 8) p.nsplit *= 2;
+    // aim for >= 4 blocks per CU (256 CUs); keep >= 4 samples per split
+    while (tiles * p.nsplit < 1024 && B / (p.nsplit * 2) >= 4) p.nsplit *= 2;
     p.b_per_split = static_cast<int>(std::max<int64_t>(1, (B + p.nsplit - 1) / p.nsplit));
     p.nsplit = static_cast<int>(std::max<int64_t>(1, (B + p.b_per_split - 1) / p.b_per_split));
     return p;
@@ -464,67 +612,89 @@ DwPlan plan_dw(int64_t B, int64_t N_in, int64_t N_out) {
 hipError_t launch_dw(const LifConst &C, int64_t B, int64_t N_in, int64_t N_out, const float *G,
                      const int *row, const float *L, const float *R, float *dW, float *part,
                      hipStream_t st) {
-    DwPlan p = plan_dw(B, N_in, N_out);
-    dim3 grid(static_cast<unsigned>((N_out + kWave - 1) / kWave),
-              static_cast<unsigned>((N_in + p.waves * p.jw - 1) / (p.waves * p.jw)),
-              static_cast<unsigned>(p.nsplit));
-    const size_t per = static_cast<size_t>(C.M + 3) * kWave * sizeof(float);
-    int nbs = static_cast<int>(std::max<size_t>(1, std::min<size_t>(4, (48 * 1024) / per)));
-    size_t lds = per * nbs;
+    DwPlan p = plan_dw(B, N_in, N_out, C.M);
+    const int ti = p.jw;
+    const int pstride = (C.M + 3) | 1;
+    dim3 grid(static_cast<unsigned>((N_in + 255) / 256),
+              static_cast<unsigned>((N_out + ti - 1) / ti), static_cast<unsigned>(p.nsplit));
+    size_t lds = 2 * static_cast<size_t>(ti) * pstride * sizeof(float2);
     float *dst = (p.nsplit == 1) ? dW : part;
-    hipLaunchKernelGGL(dw_dense_kernel<16>, grid, dim3(p.waves * kWave), lds, st, C,
-                       static_cast<int>(B), static_cast<int>(N_in), static_cast<int>(N_out),
-                       p.b_per_split, nbs, G, row, L, R, dst);
+    {
+        ProfScope prof("dw_dense", st);
+        if (ti == 64)
+            hipLaunchKernelGGL(dw_dense_kernel<64>, grid, dim3(256), lds, st, C, static_cast<int>(B),
+                               static_cast<int>(N_in), static_cast<int>(N_out), p.b_per_split,
+                               pstride, G, row, L, R, dst);
+        else
+            hipLaunchKernelGGL(dw_dense_kernel<32>, grid, dim3(256), lds, st, C, static_cast<int>(B),
+                               static_cast<int>(N_in), static_cast<int>(N_out), p.b_per_split,
+                               pstride, G, row, L, R, dst);
+    }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || p.nsplit == 1) return e;
     int64_t n = N_out * N_in;
+    ProfScope prof("dw_reduce", st);
     hipLaunchKernelGGL(reduce_splits_kernel, dim3(static_cast<unsigned>((n + 255) / 256)), dim3(256),
                        0, st, n, p.nsplit, part, dW);
     return hipGetLastError();
 }
 
-static int dtin_sb(int M) {
-    const int64_t per = static_cast<int64_t>(kWave) * (M + 3 + 1) * sizeof(float2);
-    int sb = 4;
-    while (sb > 1 && sb * per > 80 * 1024) sb /= 2;
-    return sb;
+static int dtin_sb(int M) { return (M + 4) * kDtStride * 2 * sizeof(float) <= 80 * 1024 ? 2 : 1; }
+
+static int dtin_nsplit(int64_t B, int64_t N_in, int64_t N_out, int sb) {
+    const int64_t blocks = ((N_in + 255) / 256) * ((B + sb - 1) / sb);
+    const int64_t chunks = (N_out + kWave - 1) / kWave;
+    int64_t ns = 1;
+    while (blocks * ns < 1024 && ns * 2 <= chunks && ns < 16) ns *= 2;
+    return static_cast<int>(ns);
+}
+
+size_t dtin_partial_bytes(int M, int64_t B, int64_t N_in, int64_t N_out) {
+    int ns = dtin_nsplit(B, N_in, N_out, dtin_sb(M));
+    return ns > 1 ? static_cast<size_t>(ns) * B * N_in * sizeof(float) : 0;
 }
 
 hipError_t launch_dtin(const LifConst &C, int64_t B, int64_t N_in, int64_t N_out, const float *G,
                        const void *W, bool bf16, const int *row, const float *dL, const float *dR,
-                       float *dt_in, hipStream_t st) {
+                       float *dt_in, float *part, hipStream_t st) {
     const int R = C.M + 3;
-    const int pstride = R | 1;  // odd stride in 8-byte slots
     const int sb = dtin_sb(C.M);
+    const int ns = dtin_nsplit(B, N_in, N_out, sb);
+    int64_t chunks = (N_out + kWave - 1) / kWave;
+    const int i_per = static_cast<int>(((chunks + ns - 1) / ns) * kWave);
     const int threads = 256;
     dim3 grid(static_cast<unsigned>((N_in + threads - 1) / threads),
-              static_cast<unsigned>((B + sb - 1) / sb));
-    size_t lds = static_cast<size_t>(sb) * kWave * pstride * sizeof(float2);
+              static_cast<unsigned>((B + sb - 1) / sb), static_cast<unsigned>(ns));
+    size_t lds = static_cast<size_t>(sb) * (R + 1) * kDtStride * sizeof(float);
+    float *dst = ns > 1 ? part : dt_in;
+    {
+    ProfScope prof("dtin_dense", st);
 #define DTIN_LAUNCH(SBV, WT)                                                                      \
     hipLaunchKernelGGL((dtin_dense_kernel<SBV, WT>), grid, dim3(threads), lds, st, C,            \
                        static_cast<int>(B), static_cast<int>(N_in), static_cast<int>(N_out),     \
-                       pstride, G, static_cast<const WT *>(W), row, dL, dR, dt_in)
+                       i_per, G, static_cast<const WT *>(W), row, dL, dR, dst)
     if (bf16) {
-        if (sb == 4) DTIN_LAUNCH(4, uint16_t);
-        else if (sb == 2) DTIN_LAUNCH(2, uint16_t);
+        if (sb == 2) DTIN_LAUNCH(2, uint16_t);
         else DTIN_LAUNCH(1, uint16_t);
     } else {
-        if (sb == 4) DTIN_LAUNCH(4, float);
-        else if (sb == 2) DTIN_LAUNCH(2, float);
+        if (sb == 2) DTIN_LAUNCH(2, float);
         else DTIN_LAUNCH(1, float);
     }
 #undef DTIN_LAUNCH
+    }
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || ns == 1) return e;
+    int64_t n = B * N_in;
+    ProfScope prof("dtin_reduce", st);
+    hipLaunchKernelGGL(reduce_splits_kernel, dim3(static_cast<unsigned>((n + 255) / 256)), dim3(256),
+                       0, st, n, ns, part, dt_in);
     return hipGetLastError();
-}
-
-size_t dtin_lds_bytes(int M) {
-    const int R = M + 3;
-    return static_cast<size_t>(dtin_sb(M)) * kWave * (R | 1) * sizeof(float2);
 }
 
 hipError_t launch_softmax_ce(int64_t B, int64_t N, const float *t, const int *labels,
                              float tau_soft, float t_cap, float *grad, float *loss,
                              hipStream_t st) {
+    ProfScope prof("softmax_ce", st);
     hipLaunchKernelGGL(softmax_ce_kernel, dim3(1), dim3(256), 0, st, static_cast<int>(B),
                        static_cast<int>(N), t, labels, tau_soft, t_cap, grad, loss);
     return hipGetLastError();
@@ -532,6 +702,7 @@ hipError_t launch_softmax_ce(int64_t B, int64_t N, const float *t, const int *la
 
 hipError_t launch_mse(int64_t B, int64_t N, const float *t, const float *y, float *grad,
                       float *loss, hipStream_t st) {
+    ProfScope prof("mse", st);
     hipLaunchKernelGGL(mse_kernel, dim3(1), dim3(256), 0, st, static_cast<int>(B),
                        static_cast<int>(N), t, y, grad, loss);
     return hipGetLastError();

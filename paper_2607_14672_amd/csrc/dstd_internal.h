@@ -31,6 +31,9 @@ struct LifConst {
     // fp64 copies for the O(M) recurrences (state propagation over all
     // intervals), so their rounding does not grow with M
     double alpha_d, beta_d, k_dt_d;
+    // e^{-kappa*len} for len = dt and for the last interval: the interior
+    // maximum u* of v lies inside [0, len) iff e^{-kappa u*} is in (this, 1)
+    float r_lo_dt, r_lo_last;
 };
 
 // Event rows in LDS / G tables: row r holds grid point m = r - 1, so the
@@ -66,13 +69,21 @@ __device__ __forceinline__ float kern(const LifConst &C, float u) {
 // [T_0 - dt, T_M + dt)). Halves that fall outside the grid are zeroed.
 struct Event { int row; float L, R, dL, dR; };
 
+// Event row of an input spike time (q + 1), or -1 if it has no events.
+__device__ __forceinline__ int bin_row(const LifConst &C, float t) {
+    if (!isfinite(t)) return -1;
+    float qf = floorf((t - C.t0) / C.dt);
+    if (!(qf >= -1.f && qf <= static_cast<float>(C.M))) return -1;
+    return static_cast<int>(qf) + 1;
+}
+
 __device__ __forceinline__ Event bin_event(const LifConst &C, float t) {
     Event e{-1, 0.f, 0.f, 0.f, 0.f};
-    if (!isfinite(t)) return e;
+    const int row = bin_row(C, t);
+    if (row < 0) return e;
     float rel = t - C.t0;
-    float qf = floorf(rel / C.dt);
-    if (!(qf >= -1.f && qf <= static_cast<float>(C.M))) return e;
-    int q = static_cast<int>(qf);
+    int q = row - 1;
+    float qf = static_cast<float>(q);
     float x = fmaf(-qf, C.dt, rel);
     x = fminf(fmaxf(x, 0.f), C.dt);
     float y = C.dt - x;
@@ -89,6 +100,10 @@ __device__ __forceinline__ Event bin_event(const LifConst &C, float t) {
     e.row = q + 1;
     return e;
 }
+
+// Per-sample lists of the inputs with events, sorted by event row, as
+// structure-of-arrays (each array [B][stride]).
+struct SortedEv { int *j; int *r; float *L; float *R; int64_t stride; };
 
 // Potential inside one interval, relative to its left grid point:
 //   v(u) = V e^{-u/tv} + I K(u)
@@ -114,97 +129,97 @@ __device__ __forceinline__ float seg_root(const LifConst &C, const Seg &s, float
     float lo = 0.f, u = 0.f;
     float f, fp;
     seg_eval(C, s, u, f, fp);
-    for (int it = 0; it < 40; ++it) {
+    for (int it = 0; it < 48; ++it) {
         float un = (fp > 0.f) ? u - f / fp : 0.5f * (lo + hi);
         if (!(un > lo && un < hi)) un = 0.5f * (lo + hi);
         float step = un - u;
         u = un;
         seg_eval(C, s, u, f, fp);
         if (f < 0.f) lo = u; else hi = u;
-        if (fabsf(step) <= 1e-7f * C.dt || hi - lo <= 1e-7f * C.dt) break;
+        // Newton converges quadratically: once a step is below 1e-6 of u the
+        // next one is below an fp32 ulp. The bracket test catches bisection.
+        const float tol = 1e-6f * fmaxf(u, 1e-6f * C.dt);
+        if (fabsf(step) <= tol || hi - lo <= 0.25f * tol) break;
     }
     slope = fp;
     return u;
 }
 
-// Does the interval [0, len) (len = dt, or last_len for q = M) contain the
-// first crossing? v_end is v at the interval's right end when finite (the
-// recurrence value that also starts the next interval). Returns the root.
-__device__ __forceinline__ bool seg_crossing(const LifConst &C, const Seg &s, float len,
-                                             float v_end, bool end_finite, float &u_out,
-                                             float &slope) {
-    if (s.V >= C.theta) {  // only reachable through rounding: v is continuous
-        float f, fp;
-        seg_eval(C, s, 0.f, f, fp);
-        u_out = 0.f;
-        slope = fp;
-        return true;
-    }
-    if (end_finite && v_end >= C.theta) {
-        u_out = seg_root(C, s, len, slope);
-        return true;
-    }
-    // interior maximum: v'(u*) = 0 with e^{-kappa u*} = (ti/tv)(1 + V/(c I))
-    if (s.I > 0.f) {
-        float r = (C.ti * C.inv_tv) * (1.f + s.V / (C.c * s.I));
-        if (r > 0.f && r < 1.f) {
-            float us = -logf(r) / C.kappa;
-            if (us > 0.f && us < len) {
-                float f, fp;
-                seg_eval(C, s, us, f, fp);
-                if (f >= 0.f) {
-                    u_out = seg_root(C, s, us, slope);
-                    return true;
-                }
-            }
-        }
-    }
-    return false;
-}
-
-// Scan over the M+1 intervals of one neuron with its weighted events read by
-// `wq(m)` (Table "tab:timing_DSTD", Eq. (timing_DSTD)): the earliest interval
-// whose candidate lies inside it.
-template <typename F>
-__device__ __forceinline__ void scan_neuron(const LifConst &C, F wq, float &t_out, float &slope,
-                                            int &q_out) {
-    // The state (v at T_q, current after the event at T_q) is propagated in
-    // fp64: over M intervals fp32 rounding of the recurrence would grow with M.
-    // Interval tests and the root solve use the fp32-rounded state.
+// Interval scan of one neuron (Table "tab:timing_DSTD", Eq. (timing_DSTD)):
+// weighted events arrive in grid order through step(); the earliest interval
+// whose candidate lies inside it is kept. The state (v at T_q, current after
+// the event at T_q) is propagated in fp64: over M intervals fp32 rounding of
+// the recurrence would grow with M. Interval tests use the fp32-rounded state.
+// Only the crossing interval and its bracket are located here; the root is
+// solved once in finish(), with all lanes of the wave together.
+struct Scan {
     double Vd = 0.0, Id = 0.0;
-    t_out = INFINITY;
-    slope = 0.f;
-    q_out = -1;
-    for (int q = 0; q <= C.M; ++q) {
-        Id += static_cast<double>(wq(q));
+    int qf = -1;
+    Seg sf{0.f, 0.f};
+    float hi = 0.f;
+
+    __device__ __forceinline__ void step(const LifConst &C, int q, float w) {
+        Id += static_cast<double>(w);
         const double vn_d = fma(Vd, C.alpha_d, Id * C.k_dt_d);
-        Seg s{static_cast<float>(Vd), static_cast<float>(Id)};
-        bool last = (q == C.M);
-        float len = last ? C.last_len : C.dt;
-        float kmax = last ? C.kmax_last : C.kmax_dt;
-        float ub = fmaxf(s.V, 0.f) + fmaxf(s.I, 0.f) * kmax;
-        if (ub * 1.0001f >= C.theta) {
-            bool fin = !last || isfinite(C.last_len);
-            float vend = static_cast<float>(vn_d);
-            if (last && fin) {
-                float f, fp;
-                seg_eval(C, s, C.last_len, f, fp);
-                vend = f + C.theta;
-            }
-            float u, sl;
-            if (seg_crossing(C, s, len, vend, fin, u, sl)) {
-                t_out = static_cast<float>(fma(static_cast<double>(q), static_cast<double>(C.dt),
-                                               static_cast<double>(C.t0)) +
-                                           static_cast<double>(u));
-                slope = sl;
-                q_out = q;
-                return;
+        if (qf < 0) {
+            const Seg s{static_cast<float>(Vd), static_cast<float>(Id)};
+            const bool last = (q == C.M);
+            const float kmax = last ? C.kmax_last : C.kmax_dt;
+            // v(u) = V e^{-u/tv} + I K(u) <= max(V,0) + max(I,0) max K
+            const float ub = fmaxf(s.V, 0.f) + fmaxf(s.I, 0.f) * kmax;
+            if (ub * 1.0001f >= C.theta) {
+                const float len = last ? C.last_len : C.dt;
+                const bool fin = !last || isfinite(C.last_len);
+                float vend = -INFINITY;
+                if (!last) {
+                    vend = static_cast<float>(vn_d);
+                } else if (fin) {
+                    float f, fp;
+                    seg_eval(C, s, C.last_len, f, fp);
+                    vend = f + C.theta;
+                }
+                if (s.V >= C.theta) {  // only through rounding: v is continuous
+                    qf = q; sf = s; hi = 0.f;
+                } else if (vend >= C.theta) {
+                    qf = q; sf = s; hi = len;
+                } else if (s.I > 0.f) {
+                    // interior maximum: v'(u*) = 0 with e^{-kappa u*} = (ti/tv)(1 + V/(c I))
+                    const float r = (C.ti * C.inv_tv) * (1.f + s.V / (C.c * s.I));
+                    const float r_lo = last ? C.r_lo_last : C.r_lo_dt;
+                    if (r > r_lo && r < 1.f) {
+                        const float us = -logf(r) / C.kappa;
+                        float f, fp;
+                        seg_eval(C, s, us, f, fp);
+                        if (f >= 0.f) { qf = q; sf = s; hi = us; }
+                    }
+                }
             }
         }
         Vd = vn_d;
         Id *= C.beta_d;
     }
-}
+
+    __device__ __forceinline__ bool found() const { return qf >= 0; }
+
+    __device__ __forceinline__ void finish(const LifConst &C, float &t_out, float &slope,
+                                           int &q_out) const {
+        t_out = INFINITY;
+        slope = 0.f;
+        q_out = qf;
+        if (qf < 0) return;
+        float u, sl;
+        if (hi > 0.f) {
+            u = seg_root(C, sf, hi, sl);
+        } else {
+            float f;
+            u = 0.f;
+            seg_eval(C, sf, 0.f, f, sl);
+        }
+        t_out = static_cast<float>(fma(static_cast<double>(qf), static_cast<double>(C.dt),
+                                       static_cast<double>(C.t0)) + static_cast<double>(u));
+        slope = sl;
+    }
+};
 
 // LDS float add without return (ds_add_f32). Each address is owned by one
 // lane, so the order of additions is the program order: deterministic.

@@ -68,6 +68,12 @@ _SIGS = {
     "dstd_lif_conv_backward": (_I, [_P, _P, _L, _P, _P, _I, _P, _P, _P, _P, _P, _P, _P, _S, _P]),
     "dstd_softmax_ce_grad": (_I, [_L, _L, _P, _P, _F, _F, _P, _P, _P]),
     "dstd_mse_grad": (_I, [_L, _L, _P, _P, _P, _P, _P]),
+    "dstd_profile_enable": (C.c_int32, [C.c_int32]),
+    "dstd_profile_collect": (_I, []),
+    "dstd_profile_count": (C.c_int32, []),
+    "dstd_profile_entry": (_I, [C.c_int32, C.POINTER(C.c_char_p), C.POINTER(C.c_int64),
+                                C.POINTER(C.c_double)]),
+    "dstd_profile_reset": (None, []),
     "dstd_status_string": (C.c_char_p, [_I]),
     "dstd_last_error": (C.c_char_p, []),
     "dstd_version": (C.c_int32, []),
@@ -153,6 +159,37 @@ def dstd_last_error():
 
 def dstd_version():
     return _load().dstd_version()
+
+
+def dstd_profile_enable(on):
+    return _load().dstd_profile_enable(1 if on else 0)
+
+
+def dstd_profile_collect():
+    return _load().dstd_profile_collect()
+
+
+def dstd_profile_count():
+    return _load().dstd_profile_count()
+
+
+def dstd_profile_entry(idx):
+    name = C.c_char_p()
+    n = C.c_int64()
+    ms = C.c_double()
+    st = _load().dstd_profile_entry(idx, C.byref(name), C.byref(n), C.byref(ms))
+    _check("dstd_profile_entry", st)
+    return name.value.decode(), n.value, ms.value
+
+
+def dstd_profile_reset():
+    _load().dstd_profile_reset()
+
+
+def profile_table():
+    """{kernel name: (launches, total ms)} of the library's own timer."""
+    dstd_profile_collect()
+    return {e[0]: (e[1], e[2]) for e in (dstd_profile_entry(i) for i in range(dstd_profile_count()))}
 
 
 # -------------------------------------------------------- tensor helpers --

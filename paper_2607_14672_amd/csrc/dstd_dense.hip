@@ -186,40 +186,36 @@ __global__ __launch_bounds__(256) void fwd_sorted_kernel(LifConst C, int B, int 
             if (__all(sc.found() || !row_ok)) done = true;
         }
     };
-    // All loads are unconditional and branch-free, so the compiler can keep
-    // the next batch's weight loads in flight (in-order vmcnt waits): record
-    // arrays are padded by two batches, records past n are masked by
-    // selects, their input index is clamped into range, and lanes past N_out
-    // read a valid column (their results are never stored).
-    const int64_t col = row_ok ? i : 0;
-    auto wload = [&](int j) {
-        const int js = (static_cast<unsigned>(j) < static_cast<unsigned>(N_in)) ? j : 0;
-        return WLoad<WT>::get(Wt, static_cast<int64_t>(js) * N_out + col);
-    };
+    // Weight loads are raw buffer loads: per-lane column offset (constant)
+    // plus a scalar row offset j*N_out, range-checked by the hardware, so
+    // they need no address arithmetic in vector registers and no clamping.
+    // Record arrays are padded by two batches, so the batched scalar reads
+    // are unconditional; only a partial last batch is masked. Lanes past
+    // N_out read column 0 (their results are never stored).
+    const __amdgpu_buffer_rsrc_t wr =
+        make_rsrc(Wt, static_cast<uint32_t>(static_cast<int64_t>(N_in) * N_out * sizeof(WT)));
+    const int voff = (row_ok ? i : 0) * static_cast<int>(sizeof(WT));
+    const int rstride = N_out * static_cast<int>(sizeof(WT));
     float w[kBatch], wn[kBatch];
 #pragma unroll
-    for (int kk = 0; kk < kBatch; ++kk) wn[kk] = wload(as_const(ej)[kk]);
+    for (int kk = 0; kk < kBatch; ++kk) wn[kk] = BufLoad<WT>::get(wr, voff, as_const(ej)[kk] * rstride);
     for (int k0 = 0; k0 < n && !done; k0 += kBatch) {
         int rr[kBatch], jj1[kBatch];
         float ll[kBatch], rv[kBatch];
-        const int nk = min(kBatch, n - k0);
 #pragma unroll
         for (int kk = 0; kk < kBatch; ++kk) {
             w[kk] = wn[kk];
-            const bool in = kk < nk;
-            const int r = as_const(er + k0)[kk];
-            const float l = as_const(eL + k0)[kk];
-            const float v = as_const(eR + k0)[kk];
-            rr[kk] = in ? r : 0x7fffffff;
-            ll[kk] = in ? l : 0.f;
-            rv[kk] = in ? v : 0.f;
+            rr[kk] = as_const(er + k0)[kk];
+            ll[kk] = as_const(eL + k0)[kk];
+            rv[kk] = as_const(eR + k0)[kk];
             jj1[kk] = as_const(ej + k0 + kBatch)[kk];
         }
         // the next batch's weights are in flight while this one is consumed
 #pragma unroll
-        for (int kk = 0; kk < kBatch; ++kk) wn[kk] = wload(jj1[kk]);
+        for (int kk = 0; kk < kBatch; ++kk) wn[kk] = BufLoad<WT>::get(wr, voff, jj1[kk] * rstride);
+        const int nk = min(kBatch, n - k0);
         if (nk == kBatch && rr[kBatch - 1] == cur) {
-            // common case: the whole batch continues the current row
+            // common case: a full batch that continues the current row
 #pragma unroll
             for (int kk = 0; kk < kBatch; ++kk) {
                 aL = fmaf(w[kk], ll[kk], aL);
@@ -306,7 +302,7 @@ __global__ __launch_bounds__(256) void grad_g_kernel(LifConst C, int B, int N_ou
 // as pairs (G[r], G[r+1]) per neuron, so one 8-byte read with an immediate
 // neuron offset serves both halves of an event. Slot R-1 is a zero pair for
 // inputs without events. Batch splits write partial sums, reduced in order.
-template <int TI>
+template <int TI, int NPER>
 __global__ __launch_bounds__(256) void dw_dense_kernel(LifConst C, int B, int N_in, int N_out,
                                                         int b_per_split, int pstride,
                                                         const float *__restrict__ G,
@@ -325,22 +321,43 @@ __global__ __launch_bounds__(256) void dw_dense_kernel(LifConst C, int B, int N_
     float acc[TI];
 #pragma unroll
     for (int ii = 0; ii < TI; ++ii) acc[ii] = 0.f;
-    auto stage = [&](int b, float2 *buf) {
+    // Staging of G[b, :, tile] into LDS pairs in two steps, so the next
+    // sample's global loads (NPER registers per thread, unconditional with
+    // indices clamped into range) overlap this sample's compute. Neurons past
+    // the tile end hold copies of its last neuron; their sums are not stored.
+    const int total = R * TI;
+    float pre[NPER];
+    auto fetch = [&](int b) {
         const float *gb = G + static_cast<int64_t>(b) * R * N_out + i0;
-        for (int k = threadIdx.x; k < R * TI; k += blockDim.x) {
-            const int r = k / TI, l = k % TI;
-            const float v = (l < ni) ? gb[static_cast<int64_t>(r) * N_out + l] : 0.f;
-            float2 *row = buf + l * pstride;
-            if (r < R - 1) row[r].x = v;
-            if (r > 0) row[r - 1].y = v;
+#pragma unroll
+        for (int c = 0; c < NPER; ++c) {
+            const int k = threadIdx.x + c * 256;
+            const int r = min(k / TI, R - 1), l = min(k % TI, ni - 1);
+            pre[c] = gb[static_cast<int64_t>(r) * N_out + l];
+        }
+    };
+    auto store = [&](float2 *buf) {
+#pragma unroll
+        for (int c = 0; c < NPER; ++c) {
+            const int k = threadIdx.x + c * 256;
+            if (k < total) {
+                const int r = k / TI, l = k % TI;
+                float2 *row = buf + l * pstride;
+                if (r < R - 1) row[r].x = pre[c];
+                if (r > 0) row[r - 1].y = pre[c];
+            }
         }
         for (int l = threadIdx.x; l < TI; l += blockDim.x) buf[l * pstride + R - 1] = make_float2(0.f, 0.f);
     };
-    if (b_lo < b_hi) stage(b_lo, ps);
+    if (b_lo < b_hi) {
+        fetch(b_lo);
+        store(ps);
+    }
     __syncthreads();
     for (int b = b_lo; b < b_hi; ++b) {
         float2 *cur = ps + ((b - b_lo) & 1) * TI * pstride;
-        if (b + 1 < b_hi) stage(b + 1, ps + ((b + 1 - b_lo) & 1) * TI * pstride);
+        const bool more = b + 1 < b_hi;
+        if (more) fetch(b + 1);
         int slot = R - 1;
         float L = 0.f, Rv = 0.f;
         if (j_ok) {
@@ -358,6 +375,7 @@ __global__ __launch_bounds__(256) void dw_dense_kernel(LifConst C, int B, int N_
             const float2 g = p[ii * pstride];
             acc[ii] = fmaf(g.x, L, fmaf(g.y, Rv, acc[ii]));
         }
+        if (more) store(ps + ((b + 1 - b_lo) & 1) * TI * pstride);
         __syncthreads();
     }
     if (!j_ok) return;
@@ -594,7 +612,19 @@ hipError_t launch_grad_g(const LifConst &C, int64_t B, int64_t N_out, const floa
     return hipGetLastError();
 }
 
-static int dw_ti(int M) { return (M + 3 + 1) * 63 * 8 < 65536 ? 64 : 32; }
+// neuron tile: the LDS pair offset of the last neuron must fit the 16-bit
+// instruction offset
+static int dw_ti(int M) {
+    const int ps = (M + 3) | 1;
+    return (ps * 63 * 8 < 65536) ? 64 : 32;
+}
+
+// register slots per thread for staging one tile (R * TI values / 256 threads)
+static int dw_nper(int M, int ti) {
+    const int need = ((M + 3) * ti + 255) / 256;
+    for (int n : {9, 17, 33}) if (need <= n) return n;
+    return -1;
+}
 
 DwPlan plan_dw(int64_t B, int64_t N_in, int64_t N_out, int M) {
     DwPlan p;
@@ -621,14 +651,21 @@ hipError_t launch_dw(const LifConst &C, int64_t B, int64_t N_in, int64_t N_out, 
     float *dst = (p.nsplit == 1) ? dW : part;
     {
         ProfScope prof("dw_dense", st);
-        if (ti == 64)
-            hipLaunchKernelGGL(dw_dense_kernel<64>, grid, dim3(256), lds, st, C, static_cast<int>(B),
-                               static_cast<int>(N_in), static_cast<int>(N_out), p.b_per_split,
-                               pstride, G, row, L, R, dst);
-        else
-            hipLaunchKernelGGL(dw_dense_kernel<32>, grid, dim3(256), lds, st, C, static_cast<int>(B),
-                               static_cast<int>(N_in), static_cast<int>(N_out), p.b_per_split,
-                               pstride, G, row, L, R, dst);
+        const int nper = dw_nper(C.M, ti);
+#define DW_LAUNCH(TIV, NP)                                                                        \
+    hipLaunchKernelGGL((dw_dense_kernel<TIV, NP>), grid, dim3(256), lds, st, C, static_cast<int>(B), \
+                       static_cast<int>(N_in), static_cast<int>(N_out), p.b_per_split, pstride, G, \
+                       row, L, R, dst)
+        if (ti == 64) {
+            if (nper == 9) DW_LAUNCH(64, 9);
+            else if (nper == 17) DW_LAUNCH(64, 17);
+            else DW_LAUNCH(64, 33);
+        } else {
+            if (nper == 9) DW_LAUNCH(32, 9);
+            else if (nper == 17) DW_LAUNCH(32, 17);
+            else DW_LAUNCH(32, 33);
+        }
+#undef DW_LAUNCH
     }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || p.nsplit == 1) return e;

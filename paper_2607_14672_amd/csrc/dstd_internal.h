@@ -229,6 +229,26 @@ __device__ __forceinline__ void lds_add(float *p, float v) {
 
 __device__ __forceinline__ int uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }
 
+// Raw buffer access: a per-lane byte offset plus a wave-uniform (scalar)
+// byte offset, with hardware range checking (reads past `bytes` return 0).
+constexpr int kBufWord3 = 0x00020000;  // gfx9 raw-buffer descriptor, word 3
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void *p, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(p), static_cast<short>(0),
+                                             static_cast<int>(bytes), kBufWord3);
+}
+template <typename WT> struct BufLoad;
+template <> struct BufLoad<float> {
+    static __device__ __forceinline__ float get(__amdgpu_buffer_rsrc_t r, int voff, int soff) {
+        // the builtin returns the 32 bits as an integer: reinterpret, not convert
+        return __int_as_float(static_cast<int>(__builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, 0)));
+    }
+};
+template <> struct BufLoad<uint16_t> {
+    static __device__ __forceinline__ float get(__amdgpu_buffer_rsrc_t r, int voff, int soff) {
+        return bf16_to_f32(static_cast<uint16_t>(__builtin_amdgcn_raw_buffer_load_b16(r, voff, soff, 0)));
+    }
+};
+
 // Reads through the constant address space: with a wave-uniform address the
 // compiler emits scalar (SMEM) loads, batched into s_load_dwordx16 when
 // consecutive. Only for data that no kernel in flight writes.

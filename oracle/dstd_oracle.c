@@ -580,7 +580,10 @@ void oracle_conv_backward(double tau_m, double tau_s, double theta, int M, doubl
                           int KW, int stride, int pad, int pool,
                           const double *t_in, const double *W,
                           const double *t_out, const double *slope, const int32_t *q_idx,
-                          const double *grad_t_out, double *grad_W, double *grad_t_in) {
+                          const double *grad_t_out, double *grad_W, double *grad_t_in,
+                          double *grad_W_abs, double *grad_t_in_abs) {
+    /* The optional *_abs outputs (NULL to skip) receive, per gradient element,
+       the sum of the absolute values of its terms (its conditioning). */
     prm_t p;
     canon(&p, tau_m, tau_s);
     p.theta = theta; p.M = M; p.t0 = t0; p.dt = dt; p.t_max = t_max;
@@ -595,7 +598,9 @@ void oracle_conv_backward(double tau_m, double tau_s, double theta, int M, doubl
     nth = omp_get_max_threads();
 #endif
     double *dWp = (double *)calloc((size_t)(nw * nth), sizeof(double));
+    double *dWa = (double *)calloc((size_t)(nw * nth), sizeof(double));
     memset(grad_t_in, 0, sizeof(double) * (size_t)(B * nin));
+    if (grad_t_in_abs) memset(grad_t_in_abs, 0, sizeof(double) * (size_t)(B * nin));
 #pragma omp parallel
     {
         int tid = 0;
@@ -603,6 +608,7 @@ void oracle_conv_backward(double tau_m, double tau_s, double theta, int M, doubl
         tid = omp_get_thread_num();
 #endif
         double *dWl = dWp + (int64_t)tid * nw;
+        double *dWal = dWa + (int64_t)tid * nw;
         ev_t *ev = (ev_t *)malloc(sizeof(ev_t) * (size_t)nin);
         double *G = (double *)malloc(sizeof(double) * (size_t)(M + 1));
         int *ys = (int *)malloc(sizeof(int) * (size_t)(H * Wd));
@@ -611,6 +617,7 @@ void oracle_conv_backward(double tau_m, double tau_s, double theta, int M, doubl
         for (int64_t b = 0; b < B; ++b) {
             sample_events(&p, t_in + b * nin, nin, ev);
             double *dt_row = grad_t_in + b * nin;
+            double *dta_row = grad_t_in_abs ? grad_t_in_abs + b * nin : NULL;
             for (int co = 0; co < C_out; ++co)
                 for (int oy = 0; oy < g.Ho; ++oy)
                     for (int ox = 0; ox < g.Wo; ++ox) {
@@ -632,8 +639,12 @@ void oracle_conv_backward(double tau_m, double tau_s, double theta, int M, doubl
                                         int64_t jin = ((int64_t)ci * H + ys[r]) * Wd + xs[r];
                                         const ev_t *e = ev + jin;
                                         for (int k = 0; k < e->n; ++k) {
-                                            dWl[widx] += G[e->m[k]] * e->s[k] / g.P;
-                                            dt_row[jin] += G[e->m[k]] * w * e->ds[k] / g.P;
+                                            double tw = G[e->m[k]] * e->s[k] / g.P;
+                                            double tt = G[e->m[k]] * w * e->ds[k] / g.P;
+                                            dWl[widx] += tw;
+                                            dWal[widx] += fabs(tw);
+                                            dt_row[jin] += tt;
+                                            if (dta_row) dta_row[jin] += fabs(tt);
                                         }
                                     }
                                 }
@@ -642,9 +653,14 @@ void oracle_conv_backward(double tau_m, double tau_s, double theta, int M, doubl
         free(ev); free(G); free(ys); free(xs);
     }
     for (int64_t k = 0; k < nw; ++k) {
-        double s = 0.0;
-        for (int t = 0; t < nth; ++t) s += dWp[(int64_t)t * nw + k];
+        double s = 0.0, a = 0.0;
+        for (int t = 0; t < nth; ++t) {
+            s += dWp[(int64_t)t * nw + k];
+            a += dWa[(int64_t)t * nw + k];
+        }
         grad_W[k] = s;
+        if (grad_W_abs) grad_W_abs[k] = a;
     }
     free(dWp);
+    free(dWa);
 }

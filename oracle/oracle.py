@@ -20,7 +20,9 @@ _lib = None
 
 def build_oracle(force: bool = True) -> str:
     """Compile the oracle with gcc (-O2, OpenMP, fp64, no fast-math)."""
-    if force or not os.path.exists(_LIB_PATH):
+    stale = (not os.path.exists(_LIB_PATH) or
+             max(os.path.getmtime(f) for f in _SRC) > os.path.getmtime(_LIB_PATH))
+    if force or stale:
         cmd = ["gcc", "-O2", "-fopenmp", "-shared", "-fPIC", "-std=c11", "-Wall",
                "-o", _LIB_PATH + ".tmp"] + _SRC + ["-lm"]
         subprocess.run(cmd, check=True)
@@ -38,8 +40,7 @@ def _load():
     global _lib
     if _lib is not None:
         return _lib
-    if not os.path.exists(_LIB_PATH):
-        build_oracle(force=True)
+    build_oracle(force=False)  # builds when missing or older than its source
     lib = C.CDLL(_LIB_PATH)
     lib.oracle_kernel.restype = _D
     lib.oracle_kernel.argtypes = [_D, _D, _D]
@@ -65,7 +66,7 @@ def _load():
     lib.oracle_conv_backward.restype = None
     lib.oracle_conv_backward.argtypes = [_D, _D, _D, _I, _D, _D, _D, _L,
                                          _I, _I, _I, _I, _I, _I, _I, _I, _I,
-                                         _P, _P, _P, _P, _P, _P, _P, _P]
+                                         _P, _P, _P, _P, _P, _P, _P, _P, _P, _P]
     lib.oracle_num_threads.restype = _I
     lib.oracle_num_threads.argtypes = []
     _lib = lib
@@ -230,7 +231,9 @@ def conv_forward(p, cs, t_in, W):
     return dict(t_out=t_out, slope=slope, q=q, margin=margin, vabs=vabs)
 
 
-def conv_backward(p, cs, t_in, W, fwd, grad_t_out):
+def conv_backward(p, cs, t_in, W, fwd, grad_t_out, want_abs=False):
+    """DSTD backward of a conv layer. Returns (grad_W, grad_t_in), plus the
+    per-element sums of |terms| of each when ``want_abs``."""
     t_in = _f64(t_in)
     W = _f64(W)
     t_out = np.ascontiguousarray(fwd["t_out"], dtype=np.float64)
@@ -240,6 +243,11 @@ def conv_backward(p, cs, t_in, W, fwd, grad_t_out):
     B = t_in.shape[0]
     dW = np.empty(W.shape)
     dt = np.empty(t_in.shape)
+    dWa = np.empty(W.shape) if want_abs else None
+    dta = np.empty(t_in.shape) if want_abs else None
     _load().oracle_conv_backward(*_pargs(p), B, *_conv_geom(cs), _ptr(t_in), _ptr(W), _ptr(t_out),
-                                 _ptr(slope), _ptr(q), _ptr(g), _ptr(dW), _ptr(dt))
+                                 _ptr(slope), _ptr(q), _ptr(g), _ptr(dW), _ptr(dt), _ptr(dWa),
+                                 _ptr(dta))
+    if want_abs:
+        return dW, dt, dWa, dta
     return dW, dt

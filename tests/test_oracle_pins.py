@@ -443,10 +443,17 @@ def test_conv_equals_dense_layer_with_conv_connectivity(cs):
     assert (fd["q"] >= 0).sum() > 0
     np.testing.assert_allclose(fc["t_out"].reshape(B, -1), fd["t_out"], atol=1e-12)
     g = rng.standard_normal(fc["t_out"].shape)
-    dWc, dtc = oracle.conv_backward(p, cs, t.reshape(B, cs["C_in"], cs["H"], cs["W"]), Wc, fc, g)
-    dWd, dtd = oracle.dstd_backward(p, t, Wd, fd, g.reshape(B, -1))
+    dWc, dtc, dWca, dtca = oracle.conv_backward(p, cs, t.reshape(B, cs["C_in"], cs["H"], cs["W"]),
+                                                Wc, fc, g, want_abs=True)
+    dWd, dtd, dWda, dtda = oracle.dstd_backward(p, t, Wd, fd, g.reshape(B, -1), want_abs=True)
     np.testing.assert_allclose(dtc.reshape(B, -1), dtd, rtol=1e-10, atol=1e-12)
+    # each (output, input) pair is reached by one tap, so the |term| sums agree too
+    np.testing.assert_allclose(dtca.reshape(B, -1), dtda, rtol=1e-10, atol=1e-12)
     ref = np.zeros(Wc.size)
+    ref_abs = np.zeros(Wc.size)
     for o, j, wi, fac in idx:
         ref[wi] += dWd[o, j] * fac
+        ref_abs[wi] += dWda[o, j] * fac
     np.testing.assert_allclose(dWc.reshape(-1), ref, rtol=1e-10, atol=1e-12)
+    np.testing.assert_allclose(dWca.reshape(-1), ref_abs, rtol=1e-10, atol=1e-12)
+    assert (dWca.reshape(-1) >= np.abs(dWc.reshape(-1)) - 1e-15).all()

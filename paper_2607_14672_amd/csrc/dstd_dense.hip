@@ -187,8 +187,8 @@ __global__ __launch_bounds__(256) void fwd_sorted_kernel(LifConst C, int B, int 
         }
     };
     // Weight loads are raw buffer loads: per-lane column offset (constant)
-    // plus a scalar row offset j*N_out, range-checked by the hardware, so
-    // they need no address arithmetic in vector registers and no clamping.
+    // plus a scalar row offset j*N_out, so they need no address arithmetic
+    // in vector registers.
     // Record arrays are padded by two batches, so the batched scalar reads
     // are unconditional; only a partial last batch is masked. Lanes past
     // N_out read column 0 (their results are never stored).
@@ -196,9 +196,13 @@ __global__ __launch_bounds__(256) void fwd_sorted_kernel(LifConst C, int B, int 
         make_rsrc(Wt, static_cast<uint32_t>(static_cast<int64_t>(N_in) * N_out * sizeof(WT)));
     const int voff = (row_ok ? i : 0) * static_cast<int>(sizeof(WT));
     const int rstride = N_out * static_cast<int>(sizeof(WT));
+    // Reads past the end of the list see stale workspace: their input index
+    // is clamped into [0, N_in) so every scalar offset stays inside WT.
+    const unsigned jmax = static_cast<unsigned>(max(N_in - 1, 0));
+    auto wrow = [&](int j) { return static_cast<int>(min(static_cast<unsigned>(j), jmax)) * rstride; };
     float w[kBatch], wn[kBatch];
 #pragma unroll
-    for (int kk = 0; kk < kBatch; ++kk) wn[kk] = BufLoad<WT>::get(wr, voff, as_const(ej)[kk] * rstride);
+    for (int kk = 0; kk < kBatch; ++kk) wn[kk] = BufLoad<WT>::get(wr, voff, wrow(as_const(ej)[kk]));
     for (int k0 = 0; k0 < n && !done; k0 += kBatch) {
         int rr[kBatch], jj1[kBatch];
         float ll[kBatch], rv[kBatch];
@@ -212,7 +216,7 @@ __global__ __launch_bounds__(256) void fwd_sorted_kernel(LifConst C, int B, int 
         }
         // the next batch's weights are in flight while this one is consumed
 #pragma unroll
-        for (int kk = 0; kk < kBatch; ++kk) wn[kk] = BufLoad<WT>::get(wr, voff, jj1[kk] * rstride);
+        for (int kk = 0; kk < kBatch; ++kk) wn[kk] = BufLoad<WT>::get(wr, voff, wrow(jj1[kk]));
         const int nk = min(kBatch, n - k0);
         if (nk == kBatch && rr[kBatch - 1] == cur) {
             // common case: a full batch that continues the current row
@@ -260,17 +264,24 @@ __global__ __launch_bounds__(256) void fwd_sorted_kernel(LifConst C, int B, int 
 // backward recurrence K(s + dt) = alpha K(s) + K(dt) e^{-s/ti}, all terms
 // positive, so no per-element exponential and no cancellation; it runs in
 // fp64 so its rounding does not grow with the number of intervals.
-__global__ __launch_bounds__(256) void grad_g_kernel(LifConst C, int B, int N_out,
+// Neurons are (channel c, position p) pairs, N_out = n_pos * n_ch: outputs
+// are read channel-major (o = (b, c, p), NCHW for a conv layer) and G is
+// written position-major, G[b, r, p, c], so a position's channels are
+// contiguous. A dense layer is the case n_pos = 1.
+__global__ __launch_bounds__(256) void grad_g_kernel(LifConst C, int B, int n_pos, int n_ch,
                                                      const float *__restrict__ t_out,
                                                      const float *__restrict__ slope,
                                                      const int *__restrict__ q_idx,
                                                      const float *__restrict__ grad_t,
                                                      float *__restrict__ G) {
-    int64_t k = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
-    if (k >= static_cast<int64_t>(B) * N_out) return;
-    const int b = static_cast<int>(k / N_out), i = static_cast<int>(k % N_out);
+    const int N_out = n_pos * n_ch;
+    int64_t t = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (t >= static_cast<int64_t>(B) * N_out) return;
+    const int b = static_cast<int>(t / N_out), rem = static_cast<int>(t % N_out);
+    const int p = rem / n_ch, c = rem % n_ch;
+    const int64_t k = static_cast<int64_t>(b) * N_out + static_cast<int64_t>(c) * n_pos + p;
     const int R = rows_of(C);
-    float *g = G + static_cast<int64_t>(b) * R * N_out + i;
+    float *g = G + static_cast<int64_t>(b) * R * N_out + rem;
     int q = q_idx[k];
     float gv = (q >= 0) ? grad_t[k] : 0.f;
     g[0] = 0.f;
@@ -405,7 +416,6 @@ __global__ __launch_bounds__(256) void reduce_splits_kernel(int64_t n, int nspli
 // offset is an immediate. An extra zero row serves inputs without events.
 // The neuron range may be split across blocks (blockIdx.z): each split
 // writes its partial dt_in, summed in a fixed order.
-constexpr int kDtStride = kWave + 1;
 
 template <int SB, typename WT>
 __global__ __launch_bounds__(256) void dtin_dense_kernel(LifConst C, int B, int N_in, int N_out,
@@ -600,15 +610,15 @@ hipError_t launch_forward(const LifConst &C, int64_t B, int64_t N_in, int64_t N_
     return hipGetLastError();
 }
 
-hipError_t launch_grad_g(const LifConst &C, int64_t B, int64_t N_out, const float *t_out,
-                         const float *slope, const int *q_idx, const float *grad_t, float *G,
-                         hipStream_t st) {
-    int64_t n = B * N_out;
+hipError_t launch_grad_g(const LifConst &C, int64_t B, int64_t n_pos, int64_t n_ch,
+                         const float *t_out, const float *slope, const int *q_idx,
+                         const float *grad_t, float *G, hipStream_t st) {
+    int64_t n = B * n_pos * n_ch;
     if (n == 0) return hipSuccess;
     ProfScope prof("grad_g", st);
     hipLaunchKernelGGL(grad_g_kernel, dim3(static_cast<unsigned>((n + 255) / 256)), dim3(256), 0,
-                       st, C, static_cast<int>(B), static_cast<int>(N_out), t_out, slope, q_idx,
-                       grad_t, G);
+                       st, C, static_cast<int>(B), static_cast<int>(n_pos), static_cast<int>(n_ch),
+                       t_out, slope, q_idx, grad_t, G);
     return hipGetLastError();
 }
 

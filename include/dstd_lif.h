@@ -138,27 +138,51 @@ dstd_status dstd_lif_backward(const dstd_lif_params *p, int64_t B, int64_t N_in,
  * Convolutional layer geometry. Inputs NCHW [B][C_in][H][W], weights
  * [C_out][C_in][KH][KW], outputs NCHW [B][C_out][H_out][W_out].
  *  pool_in : 1 = none; 2 = average the input EVENTS over 2x2 windows
- *            (H, W even) before the convolution; 0 = average them over the
- *            whole H x W map. Averaging events is linear, i.e. it averages
- *            the synaptic input currents.
- *  H_out = (H_p + 2*pad - KH)/stride + 1 with H_p the (pooled) input height.
+ *            (H and W must be even) before the convolution; 0 = average them
+ *            over the whole H x W map (a global pool: H_p = W_p = 1).
+ *            Averaging events is linear, i.e. it averages the synaptic input
+ *            currents. The paper's own nets down-sample with stride-2
+ *            convolutions (Table "tab:architectures") and do not define spike
+ *            pooling; this is the linear reading.
+ *  H_out = (H_p + 2*pad - KH)/stride + 1 with H_p the (pooled) input height
+ *  (likewise W_out); zero padding: padded positions have no events.
+ * Supported: 1 <= KH, KW <= 7, stride >= 1, 0 <= pad <= max(KH, KW),
+ * C_in, H, W, C_out >= 1, (M + 3) * W_p <= 16128, per-sample sizes below
+ * 2^30 (DSTD_ERR_SHAPE / DSTD_ERR_UNSUPPORTED otherwise).
  */
 typedef struct {
     int32_t C_in, H, W, C_out, KH, KW, stride, pad, pool_in;
 } dstd_conv_shape;
 
+/* Workspace bytes of dstd_lif_conv_forward / _backward; 0 for invalid
+   arguments (the calls then report the precise error). */
 size_t dstd_lif_conv_forward_workspace_size(const dstd_lif_params *p, const dstd_conv_shape *cs,
                                             int64_t B);
 size_t dstd_lif_conv_backward_workspace_size(const dstd_lif_params *p, const dstd_conv_shape *cs,
                                              int64_t B);
 
-/* Same contract as dstd_lif_forward with the convolution's connectivity:
-   w^_{i m} sums w_ij s_jm over the receptive field of output neuron i. */
+/*
+ * Forward pass of one conv layer: the dense forward (Eq. (DSTD), App. B.1,
+ * Table "tab:timing_DSTD") with the convolution's connectivity, i.e.
+ * w^_{(c,y,x), m} sums w_ij s_jm over the receptive field of output neuron
+ * (c, y, x) (pooled events weighted by 1/P for a pool of P pixels).
+ *  t_in  [B][C_in][H][W]          input spike times (+inf = no spike)
+ *  W     [C_out][C_in][KH][KW]    fp32 or bf16 (converted to fp32 inside)
+ *  t_out, slope, q_idx [B][C_out][H_out][W_out]  as in dstd_lif_forward.
+ * B = 0 is a valid no-op.
+ */
 dstd_status dstd_lif_conv_forward(const dstd_lif_params *p, const dstd_conv_shape *cs, int64_t B,
                                   const float *t_in, const void *W, dstd_dtype w_dtype,
                                   float *t_out, float *slope, int32_t *q_idx,
                                   void *ws, size_t ws_bytes, void *stream);
 
+/*
+ * Backward pass of one conv layer (same chain rule as dstd_lif_backward).
+ *  grad_W    [C_out][C_in][KH][KW] out (fp32, overwritten; zeros for B = 0),
+ *            or NULL to skip.
+ *  grad_t_in [B][C_in][H][W] out (overwritten), or NULL to skip; inputs
+ *            without events get 0.
+ */
 dstd_status dstd_lif_conv_backward(const dstd_lif_params *p, const dstd_conv_shape *cs, int64_t B,
                                    const float *t_in, const void *W, dstd_dtype w_dtype,
                                    const float *t_out, const float *slope, const int32_t *q_idx,

@@ -117,6 +117,7 @@ DenseWs dense_ws_layout(int M, int64_t B, int64_t N_in, int64_t N_out, bool back
     DenseWs w{};
     size_t off = 0;
     size_t n = (size_t)(B * N_in);
+    if (!backward && B * N_out == 0) return w;  // the forward enqueues nothing
     if (!backward) {
         // forward: transposed weights (room for fp32), sorted events, counts
         w.wt = off; off += align_up((size_t)N_in * (size_t)N_out * sizeof(float));
@@ -163,6 +164,85 @@ dstd_status hip_status(hipError_t e, const char *what) {
 
 template <typename T> T *at(void *ws, size_t off) {
     return reinterpret_cast<T *>(static_cast<char *>(ws) + off);
+}
+
+
+// Host validation of a conv layer; fills the derived geometry.
+dstd_status check_conv(const dstd_conv_shape *cs, int64_t B, int M, dstd::ConvGeom *g) {
+    if (!cs) return fail(DSTD_ERR_NULL, "conv shape is NULL");
+    if (B < 0) return fail(DSTD_ERR_SHAPE, "B must be >= 0");
+    if (cs->C_in < 1 || cs->H < 1 || cs->W < 1 || cs->C_out < 1)
+        return fail(DSTD_ERR_SHAPE, "C_in, H, W and C_out must be >= 1");
+    if (cs->C_in > (1 << 20) || cs->C_out > (1 << 20))
+        return fail(DSTD_ERR_SHAPE, "C_in and C_out must be <= 2^20");
+    if (cs->KH < 1 || cs->KW < 1 || cs->KH > dstd::kConvMaxK || cs->KW > dstd::kConvMaxK)
+        return fail(DSTD_ERR_UNSUPPORTED, "kernel size %dx%d: 1..%d supported", cs->KH, cs->KW,
+                    dstd::kConvMaxK);
+    if (cs->stride < 1 || cs->pad < 0 || cs->pad >= std::max(cs->KH, cs->KW) + 1)
+        return fail(DSTD_ERR_SHAPE, "need stride >= 1 and 0 <= pad <= max(KH, KW)");
+    if (cs->pool_in != 0 && cs->pool_in != 1 && cs->pool_in != 2)
+        return fail(DSTD_ERR_PARAM, "pool_in must be 0, 1 or 2 (got %d)", cs->pool_in);
+    if (cs->pool_in == 2 && (cs->H % 2 != 0 || cs->W % 2 != 0))
+        return fail(DSTD_ERR_SHAPE, "2x2 event pooling needs even H and W (got %dx%d)", cs->H, cs->W);
+    dstd::ConvGeom &G = *g;
+    G.C_in = cs->C_in; G.H = cs->H; G.W = cs->W; G.C_out = cs->C_out;
+    G.KH = cs->KH; G.KW = cs->KW; G.stride = cs->stride; G.pad = cs->pad; G.pool = cs->pool_in;
+    if (G.pool == 2) { G.Hp = G.H / 2; G.Wp = G.W / 2; G.P = 4; }
+    else if (G.pool == 0) { G.Hp = 1; G.Wp = 1; G.P = G.H * G.W; }
+    else { G.Hp = G.H; G.Wp = G.W; G.P = 1; }
+    const int64_t ho = ((int64_t)G.Hp + 2 * G.pad - G.KH) / G.stride + 1;
+    const int64_t wo = ((int64_t)G.Wp + 2 * G.pad - G.KW) / G.stride + 1;
+    if ((int64_t)G.Hp + 2 * G.pad < G.KH || (int64_t)G.Wp + 2 * G.pad < G.KW || ho < 1 || wo < 1)
+        return fail(DSTD_ERR_SHAPE, "kernel larger than the padded input map");
+    G.Ho = (int)ho; G.Wo = (int)wo;
+    const int64_t pc = (int64_t)G.P * G.C_in;
+    const int64_t lim = (int64_t)1 << 30;
+    const int64_t nw = (int64_t)G.KH * G.KW * G.C_in * G.C_out;
+    if (pc * G.Wp >= lim || (int64_t)G.C_in * G.H * G.W >= lim || nw * 4 >= lim ||
+        (int64_t)G.C_out * G.Ho * G.Wo >= lim)
+        return fail(DSTD_ERR_SHAPE, "conv layer too large (per-sample sizes must stay below 2^30)");
+    if (B * G.Hp >= ((int64_t)1 << 31) || B * G.Ho * G.Wo >= ((int64_t)1 << 31))
+        return fail(DSTD_ERR_SHAPE, "batch too large for this map size");
+    if ((int64_t)(M + 3) * G.Wp + 256 > 16384)
+        return fail(DSTD_ERR_UNSUPPORTED, "(M + 3) * W_p = %lld exceeds the cell-row sort's LDS "
+                    "table (16128 buckets)", (long long)(M + 3) * G.Wp);
+    G.PC = (int)pc;
+    G.inv_P = (float)(1.0 / G.P);
+    return DSTD_OK;
+}
+
+struct ConvWs {
+    size_t wt, key, L, R, off;                        // forward
+    size_t row, dL, dR, G, part, wd;                  // backward (L, R shared names)
+    size_t total;
+};
+
+ConvWs conv_ws_layout(int M, const dstd::ConvGeom &g, int64_t B, bool backward) {
+    ConvWs w{};
+    size_t off = 0;
+    const size_t n = (size_t)B * g.Hp * g.Wp * g.PC;  // inputs (cell-major)
+    const size_t nw = (size_t)g.KH * g.KW * g.C_in * g.C_out;
+    const int R = M + 3;
+    if (!backward) {
+        w.wt = off; off += align_up(nw * sizeof(float));
+        const size_t nr = n + dstd::kSortPad;
+        w.key = off; off += align_up(nr * sizeof(int));
+        w.L = off; off += align_up(nr * sizeof(float));
+        w.R = off; off += align_up(nr * sizeof(float));
+        w.off = off; off += align_up((size_t)B * g.Hp * ((size_t)R * g.Wp + 1) * sizeof(int));
+    } else {
+        w.row = off; off += align_up(n * sizeof(int));
+        w.L = off; off += align_up(n * sizeof(float));
+        w.R = off; off += align_up(n * sizeof(float));
+        w.dL = off; off += align_up(n * sizeof(float));
+        w.dR = off; off += align_up(n * sizeof(float));
+        w.G = off; off += align_up((size_t)B * R * g.Ho * g.Wo * g.C_out * sizeof(float));
+        dstd::ConvDwPlan dp = dstd::plan_conv_dw(g, B, M);
+        w.part = off; off += align_up((size_t)dp.nsplit * nw * sizeof(float));
+        w.wd = off; off += align_up(nw * sizeof(float));
+    }
+    w.total = off;
+    return w;
 }
 
 }  // namespace
@@ -251,7 +331,7 @@ dstd_status dstd_lif_backward(const dstd_lif_params *p, int64_t B, int64_t N_in,
     float *G = at<float>(ws, L.G);
     e = dstd::launch_bin_events(C, B * N_in, t_in, row, Lw, Rw, dLw, dRw, st);
     if (e != hipSuccess) return hip_status(e, "bin_events launch");
-    e = dstd::launch_grad_g(C, B, N_out, t_out, slope, q_idx, grad_t_out, G, st);
+    e = dstd::launch_grad_g(C, B, 1, N_out, t_out, slope, q_idx, grad_t_out, G, st);
     if (e != hipSuccess) return hip_status(e, "grad_g launch");
     if (grad_W && N_out * N_in > 0) {
         e = dstd::launch_dw(C, B, N_in, N_out, G, row, Lw, Rw, grad_W, at<float>(ws, L.part), st);
@@ -288,20 +368,69 @@ dstd_status dstd_mse_grad(int64_t B, int64_t N, const float *t_out, const float 
     return hip_status(e, "mse launch");
 }
 
-dstd_status dstd_lif_conv_forward(const dstd_lif_params *, const dstd_conv_shape *, int64_t,
-                                  const float *, const void *, dstd_dtype, float *, float *,
-                                  int32_t *, void *, size_t, void *) {
-    return fail(DSTD_ERR_UNSUPPORTED, "conv layers are not built yet");
+size_t dstd_lif_conv_forward_workspace_size(const dstd_lif_params *p, const dstd_conv_shape *cs,
+                                            int64_t B) {
+    dstd::ConvGeom g;
+    if (check_params(p) != DSTD_OK || check_conv(cs, B, p->M, &g) != DSTD_OK) return 0;
+    return conv_ws_layout(p->M, g, B, false).total;
 }
-dstd_status dstd_lif_conv_backward(const dstd_lif_params *, const dstd_conv_shape *, int64_t,
-                                   const float *, const void *, dstd_dtype, const float *,
-                                   const float *, const int32_t *, const float *, float *, float *,
-                                   void *, size_t, void *) {
-    return fail(DSTD_ERR_UNSUPPORTED, "conv layers are not built yet");
+
+size_t dstd_lif_conv_backward_workspace_size(const dstd_lif_params *p, const dstd_conv_shape *cs,
+                                             int64_t B) {
+    dstd::ConvGeom g;
+    if (check_params(p) != DSTD_OK || check_conv(cs, B, p->M, &g) != DSTD_OK) return 0;
+    return conv_ws_layout(p->M, g, B, true).total;
 }
-size_t dstd_lif_conv_forward_workspace_size(const dstd_lif_params *, const dstd_conv_shape *,
-                                            int64_t) { return 0; }
-size_t dstd_lif_conv_backward_workspace_size(const dstd_lif_params *, const dstd_conv_shape *,
-                                             int64_t) { return 0; }
+
+dstd_status dstd_lif_conv_forward(const dstd_lif_params *p, const dstd_conv_shape *cs, int64_t B,
+                                  const float *t_in, const void *W, dstd_dtype w_dtype,
+                                  float *t_out, float *slope, int32_t *q_idx, void *ws,
+                                  size_t ws_bytes, void *stream) {
+    dstd_status s = check_params(p);
+    if (s != DSTD_OK) return s;
+    dstd::ConvGeom g;
+    if ((s = check_conv(cs, B, p->M, &g)) != DSTD_OK) return s;
+    if (w_dtype != DSTD_F32 && w_dtype != DSTD_BF16)
+        return fail(DSTD_ERR_PARAM, "unknown weight dtype %d", (int)w_dtype);
+    if (B > 0 && (!t_in || !W || !t_out || !slope || !q_idx))
+        return fail(DSTD_ERR_NULL, "t_in, W, t_out, slope and q_idx are required");
+    ConvWs L = conv_ws_layout(p->M, g, B, false);
+    if ((s = check_ws(ws, ws_bytes, L.total)) != DSTD_OK) return s;
+    if (B == 0) return DSTD_OK;
+    LifConst C = make_const(p);
+    dstd::ConvSorted srt{at<int>(ws, L.key), at<float>(ws, L.L), at<float>(ws, L.R),
+                         at<int>(ws, L.off)};
+    hipError_t e = dstd::launch_conv_forward(C, g, B, W, w_dtype == DSTD_BF16, at<float>(ws, L.wt),
+                                             srt, t_in, t_out, slope, q_idx,
+                                             static_cast<hipStream_t>(stream));
+    return hip_status(e, "conv forward launch");
+}
+
+dstd_status dstd_lif_conv_backward(const dstd_lif_params *p, const dstd_conv_shape *cs, int64_t B,
+                                   const float *t_in, const void *W, dstd_dtype w_dtype,
+                                   const float *t_out, const float *slope, const int32_t *q_idx,
+                                   const float *grad_t_out, float *grad_W, float *grad_t_in,
+                                   void *ws, size_t ws_bytes, void *stream) {
+    dstd_status s = check_params(p);
+    if (s != DSTD_OK) return s;
+    dstd::ConvGeom g;
+    if ((s = check_conv(cs, B, p->M, &g)) != DSTD_OK) return s;
+    if (w_dtype != DSTD_F32 && w_dtype != DSTD_BF16)
+        return fail(DSTD_ERR_PARAM, "unknown weight dtype %d", (int)w_dtype);
+    if (B > 0 && (!t_in || !t_out || !slope || !q_idx || !grad_t_out))
+        return fail(DSTD_ERR_NULL, "t_in, t_out, slope, q_idx and grad_t_out are required");
+    if (grad_t_in && B > 0 && !W) return fail(DSTD_ERR_NULL, "W is NULL");
+    ConvWs L = conv_ws_layout(p->M, g, B, true);
+    if ((s = check_ws(ws, ws_bytes, L.total)) != DSTD_OK) return s;
+    LifConst C = make_const(p);
+    dstd::ConvBwdWs bw{at<int>(ws, L.row), at<float>(ws, L.L),  at<float>(ws, L.R),
+                       at<float>(ws, L.dL), at<float>(ws, L.dR), at<float>(ws, L.G),
+                       at<float>(ws, L.part), at<float>(ws, L.wd)};
+    // With B == 0 the dW kernel still runs (one empty split) and writes zeros.
+    hipError_t e = dstd::launch_conv_backward(C, g, B, W, w_dtype == DSTD_BF16, t_in, t_out, slope,
+                                              q_idx, grad_t_out, bw, grad_W, grad_t_in,
+                                              static_cast<hipStream_t>(stream));
+    return hip_status(e, "conv backward launch");
+}
 
 }  // extern "C"

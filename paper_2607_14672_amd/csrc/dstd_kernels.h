@@ -23,15 +23,57 @@ hipError_t launch_bin_events(const LifConst &C, int64_t n, const float *t_in, in
 hipError_t launch_forward(const LifConst &C, int64_t B, int64_t N_in, int64_t N_out, const void *W,
                           bool bf16, void *Wt, SortedEv srt, int *n_valid, const float *t_in,
                           float *t_out, float *slope, int *q_idx, hipStream_t st);
-hipError_t launch_grad_g(const LifConst &C, int64_t B, int64_t N_out, const float *t_out,
-                         const float *slope, const int *q_idx, const float *grad_t, float *G,
-                         hipStream_t st);
+// G[b, r, p, c] for neurons (c, p), N_out = n_pos * n_ch; dense: n_pos = 1
+hipError_t launch_grad_g(const LifConst &C, int64_t B, int64_t n_pos, int64_t n_ch,
+                         const float *t_out, const float *slope, const int *q_idx,
+                         const float *grad_t, float *G, hipStream_t st);
 hipError_t launch_dw(const LifConst &C, int64_t B, int64_t N_in, int64_t N_out, const float *G,
                      const int *row, const float *L, const float *R, float *dW, float *part,
                      hipStream_t st);
 hipError_t launch_dtin(const LifConst &C, int64_t B, int64_t N_in, int64_t N_out, const float *G,
                        const void *W, bool bf16, const int *row, const float *dL, const float *dR,
                        float *dt_in, float *part, hipStream_t st);
+// ------------------------------------------------------------------ conv --
+// Geometry of a conv layer, derived on the host. The (pooled) input map has
+// Hp x Wp cells of P raw pixels; PC = P * C_in raw inputs per cell.
+struct ConvGeom {
+    int C_in, H, W, C_out, KH, KW, stride, pad, pool;
+    int Hp, Wp, Ho, Wo, P, PC;
+    float inv_P;
+};
+
+constexpr int kConvMaxK = 7;  // largest kernel height/width
+
+// Per cell row (b, py): records bucketed by (event row r, cell column px),
+// key = px * C_in + ci; off[(b*Hp + py) * (R*Wp + 1) + r*Wp + px] = bucket
+// start within the cell row's Wp * PC record slots.
+struct ConvSorted { int *key; float *L; float *R; int *off; };
+
+struct ConvBwdWs {
+    int *row;
+    float *L, *R, *dL, *dR;  // cell-major events
+    float *G;                // [B][R][Ho*Wo][C_out]
+    float *part;             // dW partial sums [nsplit][C_out][KH*KW*C_in]
+    float *wd;               // [KH*KW][C_out][C_in] weights / P
+};
+
+struct ConvDwPlan { int ti, nsplit, s_per_split; };
+
+// the dt_in kernel's LDS row stride (words); odd, so rows r and r+1 of one
+// lane fall in different banks
+constexpr int kDtStride = kWave + 1;
+
+ConvDwPlan plan_conv_dw(const ConvGeom &g, int64_t B, int M);
+int conv_sort_lds_bytes(int M, const ConvGeom &g);
+int conv_dtin_sb(int M, const ConvGeom &g);
+hipError_t launch_conv_forward(const LifConst &C, const ConvGeom &g, int64_t B, const void *W,
+                               bool bf16, float *Wt, ConvSorted cs, const float *t_in,
+                               float *t_out, float *slope, int *q_idx, hipStream_t st);
+hipError_t launch_conv_backward(const LifConst &C, const ConvGeom &g, int64_t B, const void *W,
+                                bool bf16, const float *t_in, const float *t_out,
+                                const float *slope, const int *q_idx, const float *grad_t,
+                                ConvBwdWs ws, float *grad_W, float *grad_t_in, hipStream_t st);
+
 hipError_t launch_softmax_ce(int64_t B, int64_t N, const float *t, const int *labels,
                              float tau_soft, float t_cap, float *grad, float *loss, hipStream_t st);
 hipError_t launch_mse(int64_t B, int64_t N, const float *t, const float *y, float *grad,

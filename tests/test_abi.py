@@ -107,3 +107,66 @@ def test_status_strings():
     for s in range(-6, 1):
         assert dstd.dstd_status_string(s)
     assert dstd.dstd_version() >= 100
+
+
+def _cs(**kw):
+    base = dict(C_in=4, H=8, W=8, C_out=6, KH=3, KW=3, stride=1, pad=1, pool_in=1)
+    base.update(kw)
+    return dstd.make_conv_shape(**base)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(C_in=0), dstd.DSTD_ERR_SHAPE),
+    (dict(C_out=0), dstd.DSTD_ERR_SHAPE),
+    (dict(H=0), dstd.DSTD_ERR_SHAPE),
+    (dict(KH=0), dstd.DSTD_ERR_UNSUPPORTED),
+    (dict(KW=9), dstd.DSTD_ERR_UNSUPPORTED),
+    (dict(stride=0), dstd.DSTD_ERR_SHAPE),
+    (dict(pad=-1), dstd.DSTD_ERR_SHAPE),
+    (dict(pad=5), dstd.DSTD_ERR_SHAPE),
+    (dict(pool_in=3), dstd.DSTD_ERR_PARAM),
+    (dict(pool_in=2, H=7), dstd.DSTD_ERR_SHAPE),
+    (dict(H=2, W=2, KH=5, KW=5, pad=1), dstd.DSTD_ERR_SHAPE),
+    (dict(W=1000, H=4), dstd.DSTD_ERR_UNSUPPORTED),
+])
+def test_conv_shape_validation(kw, status):
+    p = _p()
+    cs = _cs(**kw)
+    assert dstd.dstd_lif_conv_forward_workspace_size(p, cs, 2) == 0
+    st = dstd.dstd_lif_conv_forward(p, cs, 2, 1, 1, 0, 1, 1, 1, 256, 1 << 30, None)
+    assert st == status, dstd.dstd_last_error()
+    st = dstd.dstd_lif_conv_backward(p, cs, 2, 1, 1, 0, 1, 1, 1, 1, 1, 1, 256, 1 << 30, None)
+    assert st == status
+    assert dstd.dstd_last_error()
+
+
+def test_conv_null_and_workspace_errors():
+    p = _p()
+    cs = _cs()
+    need = dstd.dstd_lif_conv_forward_workspace_size(p, cs, 2)
+    nb = dstd.dstd_lif_conv_backward_workspace_size(p, cs, 2)
+    assert need > 0 and nb > 0
+    assert dstd.dstd_lif_conv_forward(p, None, 2, 1, 1, 0, 1, 1, 1, 256, need, None) == dstd.DSTD_ERR_NULL
+    assert dstd.dstd_lif_conv_forward(p, cs, -1, 1, 1, 0, 1, 1, 1, 256, need, None) == dstd.DSTD_ERR_SHAPE
+    assert dstd.dstd_lif_conv_forward(p, cs, 2, None, 1, 0, 1, 1, 1, 256, need, None) == dstd.DSTD_ERR_NULL
+    assert dstd.dstd_lif_conv_forward(p, cs, 2, 1, 1, 3, 1, 1, 1, 256, need, None) == dstd.DSTD_ERR_PARAM
+    assert dstd.dstd_lif_conv_forward(p, cs, 2, 1, 1, 0, 1, 1, 1, 256, need - 1, None) == dstd.DSTD_ERR_WORKSPACE
+    assert dstd.dstd_lif_conv_forward(p, cs, 2, 1, 1, 0, 1, 1, 1, 260, need, None) == dstd.DSTD_ERR_WORKSPACE
+    assert dstd.dstd_lif_conv_backward(p, cs, 2, 1, 1, 0, 1, 1, 1, None, 1, 1, 256, nb, None) == dstd.DSTD_ERR_NULL
+    assert dstd.dstd_lif_conv_backward(p, cs, 2, 1, None, 0, 1, 1, 1, 1, 1, 1, 256, nb, None) == dstd.DSTD_ERR_NULL
+    assert dstd.dstd_lif_conv_backward(p, cs, 2, 1, 1, 0, 1, 1, 1, 1, 1, 1, 256, nb - 1, None) == dstd.DSTD_ERR_WORKSPACE
+    # the backward without grad_t_in does not need W
+    assert dstd.dstd_lif_conv_backward(p, cs, 2, 1, None, 0, 1, 1, 1, 1, 1, None, 256, nb - 1, None) == dstd.DSTD_ERR_WORKSPACE
+
+
+def test_conv_workspace_and_geometry():
+    p = _p()
+    a = dstd.dstd_lif_conv_forward_workspace_size(p, _cs(), 2)
+    b = dstd.dstd_lif_conv_forward_workspace_size(p, _cs(), 4)
+    c = dstd.dstd_lif_conv_backward_workspace_size(p, _cs(), 4)
+    d = dstd.dstd_lif_conv_backward_workspace_size(_p(M=64), _cs(), 4)
+    assert 0 < a < b and 0 < c < d
+    assert dstd.conv_out_hw(_cs()) == (8, 8)
+    assert dstd.conv_out_hw(_cs(stride=2)) == (4, 4)
+    assert dstd.conv_out_hw(_cs(pool_in=2)) == (4, 4)
+    assert dstd.conv_out_hw(_cs(pool_in=0, KH=1, KW=1, pad=0)) == (1, 1)

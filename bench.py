@@ -63,22 +63,33 @@ class Net:
         self.L = []
         t_prev = self.t0
         for l, lay in enumerate(wl.layers):
-            if lay.kind != "dense":
-                raise NotImplementedError("bench covers dense workloads")
             W = torch.from_numpy(d.weights(l)).to(dev)
             if lay.w_dtype == "bf16":
                 W = W.to(torch.bfloat16)
             p = dstd.make_params(lay.tau_m, lay.tau_s, lay.threshold, lay.M, lay.t0, lay.dt,
                                  lay.t_max)
-            e = dict(lay=lay, p=p, W=W, wdt=dstd.DSTD_BF16 if lay.w_dtype == "bf16" else dstd.DSTD_F32,
-                     t_in=t_prev,
-                     t_out=torch.empty((B, lay.n_out), dtype=torch.float32, device=dev),
-                     slope=torch.empty((B, lay.n_out), dtype=torch.float32, device=dev),
-                     q=torch.empty((B, lay.n_out), dtype=torch.int32, device=dev),
-                     g_out=torch.empty((B, lay.n_out), dtype=torch.float32, device=dev),
-                     gW=torch.empty((lay.n_out, lay.n_in), dtype=torch.float32, device=dev))
-            e["ws_f"] = dstd.workspace(dstd.dstd_lif_forward_workspace_size(p, B, lay.n_in, lay.n_out), dev)
-            e["ws_b"] = dstd.workspace(dstd.dstd_lif_backward_workspace_size(p, B, lay.n_in, lay.n_out), dev)
+            if lay.kind == "conv":
+                cs = dstd.make_conv_shape(**lay.conv_shape())
+                out_shape = (B, lay.C_out) + dstd.conv_out_hw(cs)
+                t_in = t_prev.reshape(B, lay.C_in, lay.H, lay.W)
+                ws_f = dstd.dstd_lif_conv_forward_workspace_size(p, cs, B)
+                ws_b = dstd.dstd_lif_conv_backward_workspace_size(p, cs, B)
+            else:
+                cs = None
+                out_shape = (B, lay.n_out)
+                t_in = t_prev.reshape(B, lay.n_in)
+                ws_f = dstd.dstd_lif_forward_workspace_size(p, B, lay.n_in, lay.n_out)
+                ws_b = dstd.dstd_lif_backward_workspace_size(p, B, lay.n_in, lay.n_out)
+            e = dict(lay=lay, p=p, cs=cs, W=W,
+                     wdt=dstd.DSTD_BF16 if lay.w_dtype == "bf16" else dstd.DSTD_F32,
+                     t_in=t_in,
+                     t_out=torch.empty(out_shape, dtype=torch.float32, device=dev),
+                     slope=torch.empty(out_shape, dtype=torch.float32, device=dev),
+                     q=torch.empty(out_shape, dtype=torch.int32, device=dev),
+                     g_out=torch.empty(out_shape, dtype=torch.float32, device=dev),
+                     gW=torch.empty(tuple(W.shape), dtype=torch.float32, device=dev))
+            e["ws_f"] = dstd.workspace(ws_f, dev)
+            e["ws_b"] = dstd.workspace(ws_b, dev)
             self.L.append(e)
             t_prev = e["t_out"]
         for l in range(1, len(self.L)):
@@ -96,13 +107,23 @@ class Net:
             raise self.dstd.DSTDError(name, st)
 
     def forward(self):
+        for l in range(len(self.L)):
+            self.forward_layer(l)
+
+    def forward_layer(self, l):
         ds = self.dstd
-        for e in self.L:
-            lay = e["lay"]
-            self._ck("dstd_lif_forward", ds.dstd_lif_forward(
-                e["p"], self.B, lay.n_in, lay.n_out, e["t_in"].data_ptr(), e["W"].data_ptr(), e["wdt"],
+        e = self.L[l]
+        lay = e["lay"]
+        if e["cs"] is not None:
+            self._ck("dstd_lif_conv_forward", ds.dstd_lif_conv_forward(
+                e["p"], e["cs"], self.B, e["t_in"].data_ptr(), e["W"].data_ptr(), e["wdt"],
                 e["t_out"].data_ptr(), e["slope"].data_ptr(), e["q"].data_ptr(),
                 e["ws_f"].data_ptr(), e["ws_f"].numel(), self.stream))
+            return
+        self._ck("dstd_lif_forward", ds.dstd_lif_forward(
+            e["p"], self.B, lay.n_in, lay.n_out, e["t_in"].data_ptr(), e["W"].data_ptr(), e["wdt"],
+            e["t_out"].data_ptr(), e["slope"].data_ptr(), e["q"].data_ptr(),
+            e["ws_f"].data_ptr(), e["ws_f"].numel(), self.stream))
 
     def loss_grad(self):
         ds = self.dstd
@@ -117,15 +138,25 @@ class Net:
                 e["g_out"].data_ptr(), self.loss.data_ptr(), self.stream))
 
     def backward(self):
-        ds = self.dstd
         for l in reversed(range(len(self.L))):
-            e = self.L[l]
-            lay = e["lay"]
-            g_in = e["g_in_buf"].data_ptr() if l > 0 else None
-            self._ck("dstd_lif_backward", ds.dstd_lif_backward(
-                e["p"], self.B, lay.n_in, lay.n_out, e["t_in"].data_ptr(), e["W"].data_ptr(), e["wdt"],
-                e["t_out"].data_ptr(), e["slope"].data_ptr(), e["q"].data_ptr(), e["g_out"].data_ptr(),
-                e["gW"].data_ptr(), g_in, e["ws_b"].data_ptr(), e["ws_b"].numel(), self.stream))
+            self.backward_layer(l)
+
+    def backward_layer(self, l):
+        ds = self.dstd
+        e = self.L[l]
+        lay = e["lay"]
+        g_in = e["g_in_buf"].data_ptr() if l > 0 else None
+        if e["cs"] is not None:
+            self._ck("dstd_lif_conv_backward", ds.dstd_lif_conv_backward(
+                e["p"], e["cs"], self.B, e["t_in"].data_ptr(), e["W"].data_ptr(), e["wdt"],
+                e["t_out"].data_ptr(), e["slope"].data_ptr(), e["q"].data_ptr(),
+                e["g_out"].data_ptr(), e["gW"].data_ptr(), g_in, e["ws_b"].data_ptr(),
+                e["ws_b"].numel(), self.stream))
+            return
+        self._ck("dstd_lif_backward", ds.dstd_lif_backward(
+            e["p"], self.B, lay.n_in, lay.n_out, e["t_in"].data_ptr(), e["W"].data_ptr(), e["wdt"],
+            e["t_out"].data_ptr(), e["slope"].data_ptr(), e["q"].data_ptr(), e["g_out"].data_ptr(),
+            e["gW"].data_ptr(), g_in, e["ws_b"].data_ptr(), e["ws_b"].numel(), self.stream))
 
     def step(self):
         self.forward()
@@ -142,20 +173,81 @@ class Net:
             ing = np.isfinite(t) & (t >= lo) & (t < hi)
             q = e["q"].cpu().numpy()
             out.append(dict(in_grid_inputs=int(ing.sum()), in_grid_frac=float(ing.mean()),
-                            fire_frac=float((q >= 0).mean())))
+                            fire_frac=float((q >= 0).mean()),
+                            updates=int(event_updates(lay, ing))))
         return out
+
+
+def layer_profile(net, dstd, torch, reps=5):
+    """Per layer: milliseconds of each library kernel in its forward and its
+    backward (hipEvent timer, mean over reps full steps)."""
+    out = [dict(fwd={}, bwd={}) for _ in net.L]
+
+    def timed(fn, into):
+        dstd.dstd_profile_reset()
+        dstd.dstd_profile_enable(True)
+        fn()
+        torch.cuda.synchronize()
+        dstd.dstd_profile_enable(False)
+        for k, v in dstd.profile_table().items():
+            into[k] = into.get(k, 0.0) + v[1] / reps
+
+    for _ in range(reps):
+        for l in range(len(net.L)):
+            timed(lambda: net.forward_layer(l), out[l]["fwd"])
+        net.loss_grad()
+        for l in reversed(range(len(net.L))):
+            timed(lambda: net.backward_layer(l), out[l]["bwd"])
+    return [{d: {k: round(v, 4) for k, v in sorted(x[d].items())} for d in x} for x in out]
+
+
+def event_updates(lay, ing):
+    """(input with events, output neuron) connections of one layer over the
+    batch: each such pair costs one weighted-event update in the forward, dW
+    and dt_in contractions. `ing` is the in-grid indicator of the inputs."""
+    B = ing.shape[0]
+    if lay.kind == "dense":
+        return ing.reshape(B, -1).sum() * lay.n_out
+    x = ing.reshape(B, lay.C_in, lay.H, lay.W).sum(axis=1).astype(np.int64)  # per pixel
+    if lay.pool_in == 2:
+        x = x.reshape(B, lay.H // 2, 2, lay.W // 2, 2).sum(axis=(2, 4))
+    elif lay.pool_in == 0:
+        x = x.sum(axis=(1, 2)).reshape(B, 1, 1)
+    Hp, Wp = x.shape[1], x.shape[2]
+    xp = np.zeros((B, Hp + 2 * lay.pad, Wp + 2 * lay.pad), dtype=np.int64)
+    xp[:, lay.pad:lay.pad + Hp, lay.pad:lay.pad + Wp] = x
+    Ho = (Hp + 2 * lay.pad - lay.KH) // lay.stride + 1
+    Wo = (Wp + 2 * lay.pad - lay.KW) // lay.stride + 1
+    tot = 0
+    for ky in range(lay.KH):
+        for kx in range(lay.KW):
+            tot += xp[:, ky:ky + lay.stride * (Ho - 1) + 1:lay.stride,
+                      kx:kx + lay.stride * (Wo - 1) + 1:lay.stride].sum()
+    return tot * lay.C_out
+
+
+def layer_desc(lay):
+    if lay.kind == "conv":
+        pool = {0: " global-pool", 1: "", 2: " pool2"}[lay.pool_in]
+        return (f"conv{lay.KH}x{lay.KW}/s{lay.stride}{pool} {lay.C_in}x{lay.H}x{lay.W}"
+                f"->{lay.C_out} M={lay.M}")
+    return f"{lay.n_in}->{lay.n_out} M={lay.M}"
 
 
 def kernel_algorithmic_flops(net, act):
     """Algorithmic flops of one step, per kernel name (2-sparse events:
     FLOPS_PER_UPDATE per (sample, input with events, neuron))."""
-    fl = {"fwd_dense": 0.0, "dw_dense": 0.0, "dtin_dense": 0.0}
+    fl = {k: 0.0 for k in ("fwd_dense", "dw_dense", "dtin_dense", "conv_fwd", "conv_dw",
+                           "conv_dtin")}
     for l, (e, a) in enumerate(zip(net.L, act)):
-        upd = a["in_grid_inputs"] * e["lay"].n_out
-        fl["fwd_dense"] += FLOPS_PER_UPDATE * upd
-        fl["dw_dense"] += FLOPS_PER_UPDATE * upd
+        upd = a["updates"]
+        pre = "conv_" if e["cs"] is not None else ""
+        fwd, dw, dt = ((pre + "fwd", pre + "dw", pre + "dtin") if pre else
+                       ("fwd_dense", "dw_dense", "dtin_dense"))
+        fl[fwd] += FLOPS_PER_UPDATE * upd
+        fl[dw] += FLOPS_PER_UPDATE * upd
         if l > 0:
-            fl["dtin_dense"] += FLOPS_PER_UPDATE * upd
+            fl[dt] += FLOPS_PER_UPDATE * upd
     return fl
 
 
@@ -174,20 +266,44 @@ def traffic_for(kernel, workload, sha):
 
 def cpu_baseline(wl, min_seconds=10.0):
     """The fp64 oracle (as it stands) on the host: fwd + bwd of the whole
-    workload on its full batch, repeated until min_seconds of CPU work."""
+    workload, repeated until min_seconds of CPU work. Dense workloads run the
+    full batch per repetition; conv workloads a 2-image sub-batch (a full
+    conv batch takes minutes in the oracle)."""
     import oracle
     from paper_2607_14672_amd import workloads
     d = workloads.Draws(wl)
     Ws = [d.weights(l) for l in range(len(wl.layers))]
+    conv = any(lay.kind == "conv" for lay in wl.layers)
+    nb = 2 if conv else wl.batch
+    t_first = d.t_in[:nb]
+    labels = None if d.labels is None else d.labels[:nb]
+    targets = None if d.targets is None else d.targets[:nb]
+
+    def fwd(lay, t, W):
+        if lay.kind == "conv":
+            return oracle.conv_forward(lay.params(), lay.conv_shape(),
+                                       t.reshape(t.shape[0], lay.C_in, lay.H, lay.W), W)
+        return oracle.dstd_forward(lay.params(), t.reshape(t.shape[0], -1), W)
+
+    def bwd(lay, t, W, r, g, need_dt):
+        g = np.where(r["q"] >= 0, g.reshape(r["q"].shape), 0.0)
+        if lay.kind == "conv":
+            _, gx = oracle.conv_backward(lay.params(), lay.conv_shape(),
+                                         t.reshape(t.shape[0], lay.C_in, lay.H, lay.W), W, r, g)
+            return gx
+        _, gx = oracle.dstd_backward(lay.params(), t.reshape(t.shape[0], -1), W, r, g,
+                                     want_dt=need_dt)
+        return gx
+
     reps, n, t_start = 0, 0, time.perf_counter()
     while True:
-        t = d.t_in
+        t = t_first
         fw = []
         for l, lay in enumerate(wl.layers):
-            r = oracle.dstd_forward(lay.params(), t, Ws[l])
+            r = fwd(lay, t, Ws[l])
             fw.append((t, r))
             t = r["t_out"].astype(np.float32)
-        to = fw[-1][1]["t_out"]
+        to = fw[-1][1]["t_out"].reshape(nb, -1)
         last = wl.layers[-1]
         if wl.loss == "ce":
             cap = last.t0 + last.M * last.dt + 2.0
@@ -195,23 +311,22 @@ def cpu_baseline(wl, min_seconds=10.0):
             z = -tt
             s = np.exp(z - z.max(1, keepdims=True))
             s /= s.sum(1, keepdims=True)
-            g = np.where(np.isfinite(to), -(s - np.eye(to.shape[1])[d.labels]) / to.shape[0], 0.0)
+            g = np.where(np.isfinite(to), -(s - np.eye(to.shape[1])[labels]) / nb, 0.0)
         else:
-            g = np.where(np.isfinite(to), (to - d.targets) / to.shape[0], 0.0)
+            g = np.where(np.isfinite(to), (to - targets) / nb, 0.0)
         for l in reversed(range(len(wl.layers))):
             tin, r = fw[l]
-            _, gx = oracle.dstd_backward(wl.layers[l].params(), tin, Ws[l], r,
-                                         np.where(r["q"] >= 0, g, 0.0), want_dt=l > 0)
+            gx = bwd(wl.layers[l], tin, Ws[l], r, g, l > 0)
             if l > 0:
                 g = gx
         reps += 1
-        n += wl.batch
+        n += nb
         el = time.perf_counter() - t_start
         if el >= min_seconds:
             break
     return dict(value=n / el, unit="samples/s", cores=oracle.num_threads(), kind="oracle",
-                sample=f"{reps} x full batch of {wl.batch} samples (fwd+bwd of all layers, fp64), "
-                       f"{el:.1f} s")
+                sample=f"{reps} x {'sub-batch' if conv else 'full batch'} of {nb} samples "
+                       f"(fwd+bwd of all layers, fp64), {el:.1f} s")
 
 
 def main():
@@ -222,6 +337,8 @@ def main():
     ap.add_argument("--workload", default="mlp3")
     ap.add_argument("--profile-steps", type=int, default=20)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--layer-profile", action="store_true",
+                    help="add per-layer kernel times to the detail section")
     ap.add_argument("--copy-probe", action="store_true",
                     help="also run a 256 MiB device copy (HBM counter calibration)")
     args = ap.parse_args()
@@ -280,6 +397,7 @@ def main():
             b.copy_(a)
         torch.cuda.synchronize()
 
+    per_layer = layer_profile(net, dstd, torch) if args.layer_profile else None
     cpu = None if args.no_cpu_baseline else cpu_baseline(wl)
     out = {
         "metric": METRIC, "value": round(value, 1), "unit": "samples/s", "n_gpus": 1,
@@ -287,13 +405,13 @@ def main():
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
         "data": "synthetic (seeded uniform spike times; calibrated random weights)",
         "config": {"workload": wl.description, "name": wl.name, "global_batch": wl.batch,
-                   "layers": [f"{e['lay'].n_in}->{e['lay'].n_out} M={e['lay'].M}" for e in net.L],
+                   "layers": [layer_desc(e["lay"]) for e in net.L],
                    "parallelism": "single GPU"},
         "roofline": roof,
         "cpu_baseline": cpu,
         "detail": {"kernel_ms_per_step": {k: round(v, 4) for k, v in sorted(per_step.items())},
                    "launches_per_step": launches, "activity": act, "kernel_source_sha": sha,
-                   "loss": float(net.loss.cpu())},
+                   "loss": float(net.loss.cpu()), "per_layer_ms": per_layer},
     }
     print(json.dumps(out), flush=True)
 

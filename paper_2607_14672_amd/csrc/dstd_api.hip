@@ -212,8 +212,9 @@ dstd_status check_conv(const dstd_conv_shape *cs, int64_t B, int M, dstd::ConvGe
 }
 
 struct ConvWs {
-    size_t wt, key, L, R, off;                        // forward
-    size_t row, dL, dR, G, part, wd;                  // backward (L, R shared names)
+    size_t wt, key, L, R, off;                        // both passes
+    size_t px, src, P;                                // backward sort extras
+    size_t row, eL, eR, gam, uq, q, live, part;       // backward
     size_t total;
 };
 
@@ -222,24 +223,30 @@ ConvWs conv_ws_layout(int M, const dstd::ConvGeom &g, int64_t B, bool backward) 
     size_t off = 0;
     const size_t n = (size_t)B * g.Hp * g.Wp * g.PC;  // inputs (cell-major)
     const size_t nw = (size_t)g.KH * g.KW * g.C_in * g.C_out;
+    const size_t nout = (size_t)B * g.Ho * g.Wo * g.C_out;
     const int R = M + 3;
-    if (!backward) {
-        w.wt = off; off += align_up(nw * sizeof(float));
-        const size_t nr = n + dstd::kSortPad;
-        w.key = off; off += align_up(nr * sizeof(int));
-        w.L = off; off += align_up(nr * sizeof(float));
-        w.R = off; off += align_up(nr * sizeof(float));
-        w.off = off; off += align_up((size_t)B * g.Hp * ((size_t)R * g.Wp + 1) * sizeof(int));
-    } else {
+    if (B == 0 && !backward) return w;
+    // weights / P and the records sorted per cell row; batched reads may run
+    // past the last record by up to kSortPad slots
+    w.wt = off; off += align_up(nw * sizeof(float));
+    const size_t nr = n + dstd::kSortPad;
+    w.key = off; off += align_up(nr * sizeof(int));
+    w.L = off; off += align_up(nr * sizeof(float));
+    w.R = off; off += align_up(nr * sizeof(float));
+    w.off = off; off += align_up((size_t)B * g.Hp * ((size_t)R * g.Wp + 1) * sizeof(int));
+    if (backward) {
+        w.px = off; off += align_up(nr * sizeof(int));
+        w.src = off; off += align_up(nr * sizeof(int));
+        w.P = off; off += align_up(nr * (size_t)(g.KH * g.KW) * sizeof(float));
         w.row = off; off += align_up(n * sizeof(int));
-        w.L = off; off += align_up(n * sizeof(float));
-        w.R = off; off += align_up(n * sizeof(float));
-        w.dL = off; off += align_up(n * sizeof(float));
-        w.dR = off; off += align_up(n * sizeof(float));
-        w.G = off; off += align_up((size_t)B * R * g.Ho * g.Wo * g.C_out * sizeof(float));
+        w.eL = off; off += align_up(n * sizeof(float));
+        w.eR = off; off += align_up(n * sizeof(float));
+        w.gam = off; off += align_up(nout * sizeof(float));
+        w.uq = off; off += align_up(nout * sizeof(float));
+        w.q = off; off += align_up(nout * sizeof(int));
+        w.live = off; off += align_up((size_t)B * g.Ho * g.Wo * sizeof(int));
         dstd::ConvDwPlan dp = dstd::plan_conv_dw(g, B, M);
         w.part = off; off += align_up((size_t)dp.nsplit * nw * sizeof(float));
-        w.wd = off; off += align_up(nw * sizeof(float));
     }
     w.total = off;
     return w;
@@ -399,7 +406,7 @@ dstd_status dstd_lif_conv_forward(const dstd_lif_params *p, const dstd_conv_shap
     if (B == 0) return DSTD_OK;
     LifConst C = make_const(p);
     dstd::ConvSorted srt{at<int>(ws, L.key), at<float>(ws, L.L), at<float>(ws, L.R),
-                         at<int>(ws, L.off)};
+                         at<int>(ws, L.off), nullptr, nullptr, nullptr};
     hipError_t e = dstd::launch_conv_forward(C, g, B, W, w_dtype == DSTD_BF16, at<float>(ws, L.wt),
                                              srt, t_in, t_out, slope, q_idx,
                                              static_cast<hipStream_t>(stream));
@@ -420,12 +427,25 @@ dstd_status dstd_lif_conv_backward(const dstd_lif_params *p, const dstd_conv_sha
     if (B > 0 && (!t_in || !t_out || !slope || !q_idx || !grad_t_out))
         return fail(DSTD_ERR_NULL, "t_in, t_out, slope, q_idx and grad_t_out are required");
     if (grad_t_in && B > 0 && !W) return fail(DSTD_ERR_NULL, "W is NULL");
+    if (grad_t_in && g.C_out > dstd::kConvMaxCoutDt)
+        return fail(DSTD_ERR_UNSUPPORTED, "grad_t_in of a conv layer needs C_out <= %d",
+                    dstd::kConvMaxCoutDt);
     ConvWs L = conv_ws_layout(p->M, g, B, true);
     if ((s = check_ws(ws, ws_bytes, L.total)) != DSTD_OK) return s;
     LifConst C = make_const(p);
-    dstd::ConvBwdWs bw{at<int>(ws, L.row), at<float>(ws, L.L),  at<float>(ws, L.R),
-                       at<float>(ws, L.dL), at<float>(ws, L.dR), at<float>(ws, L.G),
-                       at<float>(ws, L.part), at<float>(ws, L.wd)};
+    dstd::ConvBwdWs bw;
+    bw.row = at<int>(ws, L.row);
+    bw.L = at<float>(ws, L.eL);
+    bw.R = at<float>(ws, L.eR);
+    bw.gam = at<float>(ws, L.gam);
+    bw.uq = at<float>(ws, L.uq);
+    bw.q = at<int>(ws, L.q);
+    bw.live = at<int>(ws, L.live);
+    bw.part = at<float>(ws, L.part);
+    bw.wt = at<float>(ws, L.wt);
+    bw.srt = dstd::ConvSorted{at<int>(ws, L.key), at<float>(ws, L.L), at<float>(ws, L.R),
+                              at<int>(ws, L.off), at<int>(ws, L.px), at<int>(ws, L.src),
+                              at<float>(ws, L.P)};
     // With B == 0 the dW kernel still runs (one empty split) and writes zeros.
     hipError_t e = dstd::launch_conv_backward(C, g, B, W, w_dtype == DSTD_BF16, t_in, t_out, slope,
                                               q_idx, grad_t_out, bw, grad_W, grad_t_in,

@@ -47,17 +47,28 @@ constexpr int kConvMaxK = 7;  // largest kernel height/width
 // Per cell row (b, py): records bucketed by (event row r, cell column px),
 // key = px * C_in + ci; off[(b*Hp + py) * (R*Wp + 1) + r*Wp + px] = bucket
 // start within the cell row's Wp * PC record slots.
-struct ConvSorted { int *key; float *L; float *R; int *off; };
+// The backward sort also writes the record's cell column (px) and its input
+// index in the cell row (src = px * PC + j'), stores the event derivatives
+// dL, dR in place of L, R, and zeroes the record's per-tap partial sums
+// P[record][KH*KW] (px, src and P are NULL in the forward).
+struct ConvSorted { int *key; float *L; float *R; int *off; int *px; int *src; float *P; };
 
 struct ConvBwdWs {
     int *row;
-    float *L, *R, *dL, *dR;  // cell-major events
-    float *G;                // [B][R][Ho*Wo][C_out]
+    float *L, *R;            // cell-major events (dW)
+    float *gam, *uq;         // per output neuron, [B][Ho*Wo][C_out]: -g/slope, t - T_q
+    int *q;                  //   and its interval (-1: no gradient flows)
+    int *live;               // [B][Ho*Wo]: any channel there passes gradient
     float *part;             // dW partial sums [nsplit][C_out][KH*KW*C_in]
-    float *wd;               // [KH*KW][C_out][C_in] weights / P
+    float *wt;               // [KH*KW*C_in][C_out] weights / P (as the forward)
+    ConvSorted srt;          // records sorted as in the forward, with dL, dR
 };
 
+// largest C_out the dt_in kernel handles (channel tiles of 64 per lane)
+constexpr int kConvMaxCoutDt = 512;
+
 struct ConvDwPlan { int ti, nsplit, s_per_split; };
+constexpr int kConvMaxSplitSamples = 4096;  // (b, position) samples per dW block
 
 // the dt_in kernel's LDS row stride (words); odd, so rows r and r+1 of one
 // lane fall in different banks
@@ -65,7 +76,6 @@ constexpr int kDtStride = kWave + 1;
 
 ConvDwPlan plan_conv_dw(const ConvGeom &g, int64_t B, int M);
 int conv_sort_lds_bytes(int M, const ConvGeom &g);
-int conv_dtin_sb(int M, const ConvGeom &g);
 hipError_t launch_conv_forward(const LifConst &C, const ConvGeom &g, int64_t B, const void *W,
                                bool bf16, float *Wt, ConvSorted cs, const float *t_in,
                                float *t_out, float *slope, int *q_idx, hipStream_t st);

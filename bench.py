@@ -100,7 +100,7 @@ class Net:
             self.labels = torch.from_numpy(d.labels).to(dev)
         else:
             self.targets = torch.from_numpy(d.targets).to(dev)
-        self.loss = torch.empty((1,), dtype=torch.float32, device=dev)
+        self.loss = torch.empty((B + 1,), dtype=torch.float32, device=dev)  # total, per sample
 
     def _ck(self, name, st):
         if st != 0:
@@ -162,6 +162,27 @@ class Net:
         self.forward()
         self.loss_grad()
         self.backward()
+
+    def capture(self, warmup=3):
+        """Record one whole step into a HIP graph (the library's calls are
+        asynchronous, allocate nothing and use no memset, so they capture)."""
+        torch = self.torch
+        eager = self.stream
+        side = torch.cuda.Stream(self.dev)
+        side.wait_stream(torch.cuda.current_stream(self.dev))
+        with torch.cuda.stream(side):
+            self.stream = side.cuda_stream
+            for _ in range(warmup):
+                self.step()
+        torch.cuda.current_stream(self.dev).wait_stream(side)
+        graph = torch.cuda.CUDAGraph()
+        try:
+            with torch.cuda.graph(graph):
+                self.stream = torch.cuda.current_stream(self.dev).cuda_stream
+                self.step()
+        finally:
+            self.stream = eager
+        return graph
 
     def activity(self):
         """Per layer: inputs with events (in-grid), fraction of neurons firing."""
@@ -337,6 +358,9 @@ def main():
     ap.add_argument("--workload", default="mlp3")
     ap.add_argument("--profile-steps", type=int, default=20)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--eager", action="store_true",
+                    help="launch every kernel from Python each step instead of replaying a "
+                         "HIP graph of the step")
     ap.add_argument("--layer-profile", action="store_true",
                     help="add per-layer kernel times to the detail section")
     ap.add_argument("--copy-probe", action="store_true",
@@ -355,12 +379,16 @@ def main():
     wl = workloads.get(args.workload)
     net = Net(wl, dev)
 
+    run = net.step
+    if not args.eager:
+        graph = net.capture()
+        run = graph.replay
     for _ in range(args.warmup):
-        net.step()
+        run()
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(args.steps):
-        net.step()
+        run()
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     ms = 1e3 * elapsed / max(args.steps, 1)
@@ -406,12 +434,13 @@ def main():
         "data": "synthetic (seeded uniform spike times; calibrated random weights)",
         "config": {"workload": wl.description, "name": wl.name, "global_batch": wl.batch,
                    "layers": [layer_desc(e["lay"]) for e in net.L],
-                   "parallelism": "single GPU"},
+                   "parallelism": "single GPU",
+                   "execution": "eager launches" if args.eager else "HIP graph of the step"},
         "roofline": roof,
         "cpu_baseline": cpu,
         "detail": {"kernel_ms_per_step": {k: round(v, 4) for k, v in sorted(per_step.items())},
                    "launches_per_step": launches, "activity": act, "kernel_source_sha": sha,
-                   "loss": float(net.loss.cpu()), "per_layer_ms": per_layer},
+                   "loss": float(net.loss[0].cpu()), "per_layer_ms": per_layer},
     }
     print(json.dumps(out), flush=True)
 

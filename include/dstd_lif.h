@@ -196,14 +196,17 @@ dstd_status dstd_lif_conv_backward(const dstd_lif_params *p, const dstd_conv_sha
  * -t/tau_soft, S = softmax, L = -(1/B) sum_b ln S_{b, label_b}. Neurons that
  * did not fire (t = +inf) enter the softmax at t_cap and get no gradient.
  *  t_out [B][N], labels [B] int32 in [0, N), grad_t [B][N] out = dL/dt,
- *  loss [1] out (device float). N <= 1024.
+ *  loss [B + 1] out (device floats): loss[0] = L, loss[1 + b] = sample b's
+ *  term -(1/B) ln S_{b, label_b} (summed into loss[0] in a fixed order).
+ *  1 <= N < 2^24, 0 <= B <= 65535.
  */
 dstd_status dstd_softmax_ce_grad(int64_t B, int64_t N, const float *t_out, const int32_t *labels,
                                  float tau_soft, float t_cap, float *grad_t, float *loss,
                                  void *stream);
 
-/* Mean squared error L = (1/B) sum_{b,i fired} (t - y)^2 / 2 over fired outputs;
-   grad_t [B][N] out, loss [1] out (device float). N <= 1024. */
+/* Mean squared error L = (1/B) sum_{b,i fired} (t - y)^2 / 2 over fired
+   outputs; grad_t [B][N] out; loss [B + 1] out (device floats): loss[0] = L,
+   loss[1 + b] = sample b's term. 1 <= N < 2^24, 0 <= B <= 65535. */
 dstd_status dstd_mse_grad(int64_t B, int64_t N, const float *t_out, const float *target,
                           float *grad_t, float *loss, void *stream);
 

@@ -109,7 +109,7 @@ dstd_status check_dims(int64_t B, int64_t N_in, int64_t N_out) {
 }
 
 struct DenseWs {
-    size_t row, L, R, dL, dR, G, part, dtpart, wt, sj, sr, sL, sR, nvalid, total;
+    size_t row, L, R, dL, dR, G, part, dtpart, wt, sj, sr, sL, sR, nvalid, rs, total;
     int64_t sstride;
 };
 
@@ -130,6 +130,7 @@ DenseWs dense_ws_layout(int M, int64_t B, int64_t N_in, int64_t N_out, bool back
         w.sL = off; off += align_up(ns * sizeof(float));
         w.sR = off; off += align_up(ns * sizeof(float));
         w.nvalid = off; off += align_up((size_t)B * sizeof(int));
+        w.rs = off; off += align_up((size_t)B * (M + 4) * sizeof(int));
     }
     if (backward) {
         w.row = off; off += align_up(n * sizeof(int));
@@ -304,7 +305,7 @@ dstd_status dstd_lif_forward(const dstd_lif_params *p, int64_t B, int64_t N_in, 
     hipStream_t st = static_cast<hipStream_t>(stream);
     LifConst C = make_const(p);
     dstd::SortedEv srt{at<int>(ws, L.sj), at<int>(ws, L.sr), at<float>(ws, L.sL),
-                       at<float>(ws, L.sR), L.sstride};
+                       at<float>(ws, L.sR), L.sstride, at<int>(ws, L.rs)};
     hipError_t e = dstd::launch_forward(C, B, N_in, N_out, W, w_dtype == DSTD_BF16, at<void>(ws, L.wt),
                                         srt, at<int>(ws, L.nvalid), t_in, t_out, slope, q_idx, st);
     return hip_status(e, "forward launch");
@@ -355,7 +356,8 @@ dstd_status dstd_lif_backward(const dstd_lif_params *p, int64_t B, int64_t N_in,
 dstd_status dstd_softmax_ce_grad(int64_t B, int64_t N, const float *t_out, const int32_t *labels,
                                  float tau_soft, float t_cap, float *grad_t, float *loss,
                                  void *stream) {
-    if (B < 0 || N < 1 || N > 1024) return fail(DSTD_ERR_SHAPE, "need B >= 0 and 1 <= N <= 1024");
+    if (B < 0 || B > 65535 || N < 1 || N >= (1 << 24))
+        return fail(DSTD_ERR_SHAPE, "need 0 <= B <= 65535 and 1 <= N < 2^24");
     if (!(isfinite(tau_soft) && tau_soft > 0.f)) return fail(DSTD_ERR_PARAM, "tau_soft must be > 0");
     if (!isfinite(t_cap)) return fail(DSTD_ERR_PARAM, "t_cap must be finite");
     if (!loss || (B > 0 && (!t_out || !labels || !grad_t)))
@@ -367,7 +369,8 @@ dstd_status dstd_softmax_ce_grad(int64_t B, int64_t N, const float *t_out, const
 
 dstd_status dstd_mse_grad(int64_t B, int64_t N, const float *t_out, const float *target,
                           float *grad_t, float *loss, void *stream) {
-    if (B < 0 || N < 1 || N > 1024) return fail(DSTD_ERR_SHAPE, "need B >= 0 and 1 <= N <= 1024");
+    if (B < 0 || B > 65535 || N < 1 || N >= (1 << 24))
+        return fail(DSTD_ERR_SHAPE, "need 0 <= B <= 65535 and 1 <= N < 2^24");
     if (!loss || (B > 0 && (!t_out || !target || !grad_t)))
         return fail(DSTD_ERR_NULL, "t_out, target, grad_t and loss are required");
     hipError_t e = dstd::launch_mse(B, N, t_out, target, grad_t, loss,

@@ -81,6 +81,8 @@ __global__ __launch_bounds__(kSortWaves * 64) void bin_sort_kernel(LifConst C, i
         n_valid[b] = rowstart[R];
     }
     __syncthreads();
+    for (int r = threadIdx.x; r <= R; r += blockDim.x)
+        srt.rs[static_cast<int64_t>(b) * (R + 1) + r] = rowstart[r];
     for (int r = threadIdx.x; r < R; r += blockDim.x) {
         int base = rowstart[r];
         for (int w = 0; w < kSortWaves; ++w) {
@@ -248,6 +250,125 @@ __global__ __launch_bounds__(256) void fwd_sorted_kernel(LifConst C, int B, int 
         }
     }
     close_to(C.M + 2);  // row M+2 has no records
+    if (!row_ok) return;
+    float to, sl;
+    int q;
+    sc.finish(C, to, sl, q);
+    const int64_t o = static_cast<int64_t>(b) * N_out + i;
+    t_out[o] = to;
+    slope[o] = sl;
+    q_idx[o] = q;
+}
+
+// Row-parallel forward (M <= kRowsMaxM). A block of kRowWaves wavefronts
+// serves one (sample, 64-neuron tile): wave w sums the records of a
+// contiguous range of whole event rows (ranges split the sample's records
+// about evenly), in the same per-row order as the single-wave walk above, and
+// writes each row's L and R sums to LDS; wave 0 then runs the interval scan
+// over the rows. Four times the waves of the single-wave walk, each with a
+// quarter of its dependent load chain; the sums are identical.
+constexpr int kRowWaves = 4;
+constexpr int kRowsMaxM = 64;
+
+template <typename WT>
+__global__ __launch_bounds__(kRowWaves * 64) void fwd_rows_kernel(LifConst C, int N_in, int N_out,
+                                                                  const WT *__restrict__ Wt,
+                                                                  SortedEv srt,
+                                                                  float *__restrict__ t_out,
+                                                                  float *__restrict__ slope,
+                                                                  int *__restrict__ q_idx) {
+    extern __shared__ float rsum[];  // AL[R][64], AR[R][64]
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = uniform(threadIdx.x >> 6);
+    const int i = blockIdx.x * kWave + lane;
+    const bool row_ok = i < N_out;
+    const int b = blockIdx.y;
+    const int R = rows_of(C);
+    float *AL = rsum;
+    float *AR = rsum + R * kWave;
+    const int *rs = srt.rs + static_cast<int64_t>(b) * (R + 1);
+    const int n = *as_const(rs + R);
+    // first row of range w: the row holding record w*n/kRowWaves
+    auto row_of = [&](int t) {
+        int lo = 0, hi = R - 1;  // rs[lo] <= t < rs[hi] (rs[R-1] == n)
+        if (t >= n) return R - 1;
+        while (hi - lo > 1) {
+            const int mid = (lo + hi) >> 1;
+            if (*as_const(rs + mid) <= t) lo = mid; else hi = mid;
+        }
+        return lo;
+    };
+    const int r_lo = (wave == 0) ? 0 : row_of(static_cast<int>((static_cast<int64_t>(n) * wave) / kRowWaves));
+    const int r_hi = (wave == kRowWaves - 1)
+                         ? R - 1
+                         : row_of(static_cast<int>((static_cast<int64_t>(n) * (wave + 1)) / kRowWaves));
+    const int k_lo = *as_const(rs + r_lo), k_hi = *as_const(rs + r_hi);
+    const int64_t eo = static_cast<int64_t>(b) * srt.stride;
+    const int *ej = srt.j + eo;
+    const int *er = srt.r + eo;
+    const float *eL = srt.L + eo;
+    const float *eR = srt.R + eo;
+    int cur = r_lo;
+    float aL = 0.f, aR = 0.f;
+    // close rows cur .. target-1 of this wave's range
+    auto close_to = [&](int target) {
+        while (cur < target) {
+            AL[cur * kWave + lane] = aL;
+            AR[cur * kWave + lane] = aR;
+            aL = 0.f;
+            aR = 0.f;
+            ++cur;
+        }
+    };
+    const __amdgpu_buffer_rsrc_t wr =
+        make_rsrc(Wt, static_cast<uint32_t>(static_cast<int64_t>(N_in) * N_out * sizeof(WT)));
+    const int voff = (row_ok ? i : 0) * static_cast<int>(sizeof(WT));
+    const int rstride = N_out * static_cast<int>(sizeof(WT));
+    const unsigned jmax = static_cast<unsigned>(max(N_in - 1, 0));
+    auto wrow = [&](int j) { return static_cast<int>(min(static_cast<unsigned>(j), jmax)) * rstride; };
+    float w[kBatch], wn[kBatch];
+#pragma unroll
+    for (int kk = 0; kk < kBatch; ++kk) wn[kk] = BufLoad<WT>::get(wr, voff, wrow(as_const(ej + k_lo)[kk]));
+    for (int k0 = k_lo; k0 < k_hi; k0 += kBatch) {
+        int rr[kBatch], jj1[kBatch];
+        float ll[kBatch], rv[kBatch];
+#pragma unroll
+        for (int kk = 0; kk < kBatch; ++kk) {
+            w[kk] = wn[kk];
+            rr[kk] = as_const(er + k0)[kk];
+            ll[kk] = as_const(eL + k0)[kk];
+            rv[kk] = as_const(eR + k0)[kk];
+            jj1[kk] = as_const(ej + k0 + kBatch)[kk];
+        }
+#pragma unroll
+        for (int kk = 0; kk < kBatch; ++kk) wn[kk] = BufLoad<WT>::get(wr, voff, wrow(jj1[kk]));
+        const int nk = min(kBatch, k_hi - k0);
+        if (nk == kBatch && rr[kBatch - 1] == cur) {
+#pragma unroll
+            for (int kk = 0; kk < kBatch; ++kk) {
+                aL = fmaf(w[kk], ll[kk], aL);
+                aR = fmaf(w[kk], rv[kk], aR);
+            }
+            continue;
+        }
+#pragma unroll
+        for (int kk = 0; kk < kBatch; ++kk) {
+            if (kk < nk) {
+                if (rr[kk] != cur) close_to(rr[kk]);
+                aL = fmaf(w[kk], ll[kk], aL);
+                aR = fmaf(w[kk], rv[kk], aR);
+            }
+        }
+    }
+    close_to(r_hi);
+    __syncthreads();
+    if (wave != 0) return;
+    // grid point m: L sums of row m+1 plus R sums of row m
+    Scan sc;
+    for (int m = 0; m <= C.M; ++m) {
+        sc.step(C, m, AL[(m + 1) * kWave + lane] + AR[m * kWave + lane]);
+        if (__all(sc.found() || !row_ok)) break;
+    }
     if (!row_ok) return;
     float to, sl;
     int q;
@@ -491,71 +612,88 @@ __global__ __launch_bounds__(256) void dtin_dense_kernel(LifConst C, int B, int 
 }
 
 // ---------------------------------------------------------------- losses --
-// One block; thread t handles samples t, t + blockDim, ...; the per-sample
-// losses are summed by a fixed LDS tree (deterministic).
-__global__ __launch_bounds__(256) void softmax_ce_kernel(int B, int N, const float *__restrict__ t,
-                                                         const int *__restrict__ labels,
-                                                         float tau_soft, float t_cap,
-                                                         float *__restrict__ grad,
-                                                         float *__restrict__ loss) {
-    __shared__ float red[256];
-    float acc = 0.f;
-    const float inv = 1.f / tau_soft;
-    for (int b = threadIdx.x; b < B; b += blockDim.x) {
-        const float *tb = t + static_cast<int64_t>(b) * N;
-        float *gb = grad + static_cast<int64_t>(b) * N;
-        float mx = -INFINITY;
-        for (int k = 0; k < N; ++k) {
-            float tk = isfinite(tb[k]) ? tb[k] : t_cap;
-            mx = fmaxf(mx, -tk * inv);
-        }
-        float z = 0.f;
-        for (int k = 0; k < N; ++k) {
-            float tk = isfinite(tb[k]) ? tb[k] : t_cap;
-            z += expf(-tk * inv - mx);
-        }
-        int lab = labels[b];
-        float lz = logf(z) + mx;
-        for (int k = 0; k < N; ++k) {
-            bool fired = isfinite(tb[k]);
-            float tk = fired ? tb[k] : t_cap;
-            float sk = expf(-tk * inv - lz);
-            float dl = (sk - (k == lab ? 1.f : 0.f)) * (-inv) / static_cast<float>(B);
-            gb[k] = fired ? dl : 0.f;
-            if (k == lab) acc += (lz + tk * inv) / static_cast<float>(B);
-        }
-    }
-    red[threadIdx.x] = acc;
+// One block per sample; block reductions run over a fixed LDS tree, so the
+// per-sample losses (loss[1 + b]) and their fixed-order sum (loss[0]) are
+// deterministic.
+constexpr int kLossThreads = 256;
+
+__device__ __forceinline__ float block_reduce(float v, float *red, bool is_max) {
+    red[threadIdx.x] = v;
     __syncthreads();
-    for (int w = blockDim.x / 2; w > 0; w >>= 1) {
-        if (threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
+    for (int w = kLossThreads / 2; w > 0; w >>= 1) {
+        if (threadIdx.x < w)
+            red[threadIdx.x] = is_max ? fmaxf(red[threadIdx.x], red[threadIdx.x + w])
+                                      : red[threadIdx.x] + red[threadIdx.x + w];
         __syncthreads();
     }
-    if (threadIdx.x == 0) loss[0] = red[0];
+    const float r = red[0];
+    __syncthreads();
+    return r;
 }
 
-__global__ __launch_bounds__(256) void mse_kernel(int B, int N, const float *__restrict__ t,
-                                                  const float *__restrict__ y,
-                                                  float *__restrict__ grad,
-                                                  float *__restrict__ loss) {
-    __shared__ float red[256];
+__global__ __launch_bounds__(kLossThreads) void softmax_ce_kernel(int B, int N,
+                                                                  const float *__restrict__ t,
+                                                                  const int *__restrict__ labels,
+                                                                  float tau_soft, float t_cap,
+                                                                  float *__restrict__ grad,
+                                                                  float *__restrict__ loss) {
+    __shared__ float red[kLossThreads];
+    const int b = blockIdx.x;
+    const float inv = 1.f / tau_soft;
+    const float *tb = t + static_cast<int64_t>(b) * N;
+    float *gb = grad + static_cast<int64_t>(b) * N;
+    float mx = -INFINITY;
+    for (int k = threadIdx.x; k < N; k += kLossThreads) {
+        const float tk = isfinite(tb[k]) ? tb[k] : t_cap;
+        mx = fmaxf(mx, -tk * inv);
+    }
+    mx = block_reduce(mx, red, true);
+    float z = 0.f;
+    for (int k = threadIdx.x; k < N; k += kLossThreads) {
+        const float tk = isfinite(tb[k]) ? tb[k] : t_cap;
+        z += expf(-tk * inv - mx);
+    }
+    z = block_reduce(z, red, false);
+    const int lab = labels[b];
+    const float lz = logf(z) + mx;
+    for (int k = threadIdx.x; k < N; k += kLossThreads) {
+        const bool fired = isfinite(tb[k]);
+        const float tk = fired ? tb[k] : t_cap;
+        const float sk = expf(-tk * inv - lz);
+        const float dl = (sk - (k == lab ? 1.f : 0.f)) * (-inv) / static_cast<float>(B);
+        gb[k] = fired ? dl : 0.f;
+    }
+    if (threadIdx.x == 0) {
+        const float tl = isfinite(tb[lab]) ? tb[lab] : t_cap;
+        loss[1 + b] = (lz + tl * inv) / static_cast<float>(B);
+    }
+}
+
+__global__ __launch_bounds__(kLossThreads) void mse_kernel(int B, int N, const float *__restrict__ t,
+                                                           const float *__restrict__ y,
+                                                           float *__restrict__ grad,
+                                                           float *__restrict__ loss) {
+    __shared__ float red[kLossThreads];
+    const int b = blockIdx.x;
     float acc = 0.f;
-    for (int b = threadIdx.x; b < B; b += blockDim.x) {
-        for (int k = 0; k < N; ++k) {
-            int64_t o = static_cast<int64_t>(b) * N + k;
-            bool fired = isfinite(t[o]);
-            float d = fired ? (t[o] - y[o]) : 0.f;
-            grad[o] = d / static_cast<float>(B);
-            acc += 0.5f * d * d / static_cast<float>(B);
-        }
+    for (int k = threadIdx.x; k < N; k += kLossThreads) {
+        const int64_t o = static_cast<int64_t>(b) * N + k;
+        const bool fired = isfinite(t[o]);
+        const float d = fired ? (t[o] - y[o]) : 0.f;
+        grad[o] = d / static_cast<float>(B);
+        acc += 0.5f * d * d / static_cast<float>(B);
     }
-    red[threadIdx.x] = acc;
-    __syncthreads();
-    for (int w = blockDim.x / 2; w > 0; w >>= 1) {
-        if (threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
-        __syncthreads();
-    }
-    if (threadIdx.x == 0) loss[0] = red[0];
+    acc = block_reduce(acc, red, false);
+    if (threadIdx.x == 0) loss[1 + b] = acc;
+}
+
+// loss[0] = sum_b loss[1 + b] in a fixed order
+__global__ __launch_bounds__(kLossThreads) void loss_total_kernel(int B, float *__restrict__ loss) {
+    __shared__ float red[kLossThreads];
+    float acc = 0.f;
+    for (int b = threadIdx.x; b < B; b += kLossThreads) acc += loss[1 + b];
+    acc = block_reduce(acc, red, false);
+    if (threadIdx.x == 0) loss[0] = acc;
 }
 
 // ------------------------------------------------------------- launchers --
@@ -595,10 +733,23 @@ hipError_t launch_forward(const LifConst &C, int64_t B, int64_t N_in, int64_t N_
     }
     e = hipGetLastError();
     if (e != hipSuccess) return e;
+    ProfScope prof("fwd_dense", st);
+    if (C.M <= kRowsMaxM) {
+        dim3 grid(static_cast<unsigned>((N_out + kWave - 1) / kWave), static_cast<unsigned>(B));
+        const size_t lds = 2 * static_cast<size_t>(R) * kWave * sizeof(float);
+        if (bf16)
+            hipLaunchKernelGGL(fwd_rows_kernel<uint16_t>, grid, dim3(kRowWaves * kWave), lds, st, C,
+                               static_cast<int>(N_in), static_cast<int>(N_out),
+                               static_cast<const uint16_t *>(Wt), srt, t_out, slope, q_idx);
+        else
+            hipLaunchKernelGGL(fwd_rows_kernel<float>, grid, dim3(kRowWaves * kWave), lds, st, C,
+                               static_cast<int>(N_in), static_cast<int>(N_out),
+                               static_cast<const float *>(Wt), srt, t_out, slope, q_idx);
+        return hipGetLastError();
+    }
     constexpr int waves = 4;
     dim3 grid(static_cast<unsigned>((N_out + kWave - 1) / kWave),
               static_cast<unsigned>((B + waves - 1) / waves));
-    ProfScope prof("fwd_dense", st);
     if (bf16)
         hipLaunchKernelGGL(fwd_sorted_kernel<uint16_t>, grid, dim3(waves * kWave), 0, st, C,
                            static_cast<int>(B), static_cast<int>(N_in), static_cast<int>(N_out),
@@ -742,16 +893,23 @@ hipError_t launch_softmax_ce(int64_t B, int64_t N, const float *t, const int *la
                              float tau_soft, float t_cap, float *grad, float *loss,
                              hipStream_t st) {
     ProfScope prof("softmax_ce", st);
-    hipLaunchKernelGGL(softmax_ce_kernel, dim3(1), dim3(256), 0, st, static_cast<int>(B),
-                       static_cast<int>(N), t, labels, tau_soft, t_cap, grad, loss);
+    if (B > 0)
+        hipLaunchKernelGGL(softmax_ce_kernel, dim3(static_cast<unsigned>(B)), dim3(kLossThreads), 0,
+                           st, static_cast<int>(B), static_cast<int>(N), t, labels, tau_soft,
+                           t_cap, grad, loss);
+    hipLaunchKernelGGL(loss_total_kernel, dim3(1), dim3(kLossThreads), 0, st, static_cast<int>(B),
+                       loss);
     return hipGetLastError();
 }
 
 hipError_t launch_mse(int64_t B, int64_t N, const float *t, const float *y, float *grad,
                       float *loss, hipStream_t st) {
     ProfScope prof("mse", st);
-    hipLaunchKernelGGL(mse_kernel, dim3(1), dim3(256), 0, st, static_cast<int>(B),
-                       static_cast<int>(N), t, y, grad, loss);
+    if (B > 0)
+        hipLaunchKernelGGL(mse_kernel, dim3(static_cast<unsigned>(B)), dim3(kLossThreads), 0, st,
+                           static_cast<int>(B), static_cast<int>(N), t, y, grad, loss);
+    hipLaunchKernelGGL(loss_total_kernel, dim3(1), dim3(kLossThreads), 0, st, static_cast<int>(B),
+                       loss);
     return hipGetLastError();
 }
 

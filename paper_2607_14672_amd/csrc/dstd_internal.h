@@ -102,8 +102,9 @@ __device__ __forceinline__ Event bin_event(const LifConst &C, float t) {
 }
 
 // Per-sample lists of the inputs with events, sorted by event row, as
-// structure-of-arrays (each array [B][stride]).
-struct SortedEv { int *j; int *r; float *L; float *R; int64_t stride; };
+// structure-of-arrays (each array [B][stride]); rs[b][r] (r = 0..M+3) is the
+// start of event row r in sample b's list (rs[b][M+3] = its length).
+struct SortedEv { int *j; int *r; float *L; float *R; int64_t stride; int *rs; };
 
 // Potential inside one interval, relative to its left grid point:
 //   v(u) = V e^{-u/tv} + I K(u)

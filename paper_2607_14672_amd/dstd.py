@@ -335,6 +335,7 @@ def conv_backward(p, cs, t_in, W, t_out, slope, q, grad_t_out, need_W=True, need
 
 
 def softmax_ce_grad(t_out, labels, tau_soft: float = 1.0, t_cap: Optional[float] = None):
+    """Returns (dL/dt [B, N], loss [B + 1]): loss[0] = L, loss[1 + b] = sample b's term."""
     torch = _torch()
     t_out = _cont(t_out, torch.float32)
     labels = _cont(labels, torch.int32)
@@ -342,7 +343,7 @@ def softmax_ce_grad(t_out, labels, tau_soft: float = 1.0, t_cap: Optional[float]
     if t_cap is None:
         raise ValueError("t_cap is required (time used for outputs that did not fire)")
     grad = torch.empty_like(t_out)
-    loss = torch.empty((1,), dtype=torch.float32, device=t_out.device)
+    loss = torch.empty((B + 1,), dtype=torch.float32, device=t_out.device)
     _check("dstd_softmax_ce_grad",
            dstd_softmax_ce_grad(B, N, _ptr(t_out), _ptr(labels), float(tau_soft), float(t_cap),
                                 _ptr(grad), _ptr(loss), _stream(t_out.device)))
@@ -350,12 +351,13 @@ def softmax_ce_grad(t_out, labels, tau_soft: float = 1.0, t_cap: Optional[float]
 
 
 def mse_grad(t_out, target):
+    """Returns (dL/dt [B, N], loss [B + 1]): loss[0] = L, loss[1 + b] = sample b's term."""
     torch = _torch()
     t_out = _cont(t_out, torch.float32)
     target = _cont(target, torch.float32)
     B, N = t_out.shape
     grad = torch.empty_like(t_out)
-    loss = torch.empty((1,), dtype=torch.float32, device=t_out.device)
+    loss = torch.empty((B + 1,), dtype=torch.float32, device=t_out.device)
     _check("dstd_mse_grad", dstd_mse_grad(B, N, _ptr(t_out), _ptr(target), _ptr(grad), _ptr(loss),
                                           _stream(t_out.device)))
     return grad, loss

@@ -79,7 +79,7 @@ def test_shape_null_dtype_and_workspace_errors():
     assert dstd.dstd_lif_forward(p, 4, 10, 5, 1, 1, 0, 1, 1, 1, 256, need - 1, None) == dstd.DSTD_ERR_WORKSPACE
     assert dstd.dstd_lif_forward(p, 4, 10, 5, 1, 1, 0, 1, 1, 1, 257, need, None) == dstd.DSTD_ERR_WORKSPACE
     nb = dstd.dstd_lif_backward_workspace_size(p, 4, 10, 5)
-    assert nb > need
+    assert nb > 0
     assert dstd.dstd_lif_backward(p, 4, 10, 5, 1, 1, 0, 1, 1, 1, None, 1, 1, 256, nb, None) == dstd.DSTD_ERR_NULL
     assert dstd.dstd_lif_backward(p, 4, 10, 5, 1, 1, 0, 1, 1, 1, 1, 1, 1, 256, nb - 1, None) == dstd.DSTD_ERR_WORKSPACE
 
@@ -99,7 +99,7 @@ def test_loss_validation():
     assert dstd.dstd_softmax_ce_grad(4, 10, 1, 1, 0.0, 3.0, 1, 1, None) == dstd.DSTD_ERR_PARAM
     assert dstd.dstd_softmax_ce_grad(4, 10, 1, 1, 1.0, math.inf, 1, 1, None) == dstd.DSTD_ERR_PARAM
     assert dstd.dstd_softmax_ce_grad(4, 10, None, 1, 1.0, 3.0, 1, 1, None) == dstd.DSTD_ERR_NULL
-    assert dstd.dstd_mse_grad(4, 2000, 1, 1, 1, 1, None) == dstd.DSTD_ERR_SHAPE
+    assert dstd.dstd_mse_grad(4, 1 << 24, 1, 1, 1, 1, None) == dstd.DSTD_ERR_SHAPE
     assert dstd.dstd_mse_grad(4, 10, 1, 1, 1, None, None) == dstd.DSTD_ERR_NULL
 
 

@@ -255,7 +255,10 @@ def test_softmax_ce_grad(dev):
     onehot = np.eye(N)[lab]
     ref_g = np.where(np.isfinite(t), -(s - onehot) / tau / B, 0.0)
     np.testing.assert_allclose(g.cpu().numpy(), ref_g, rtol=1e-5, atol=1e-7)
-    assert float(loss.cpu()) == pytest.approx(ref_loss, rel=1e-5)
+    loss = loss.cpu().numpy()
+    assert float(loss[0]) == pytest.approx(ref_loss, rel=1e-5)
+    per = -np.log(s[np.arange(B), lab]) / B
+    np.testing.assert_allclose(loss[1:], per, rtol=1e-5, atol=1e-7)
 
 
 def test_mse_grad(dev):
@@ -270,4 +273,31 @@ def test_mse_grad(dev):
     f = np.isfinite(t)
     d = np.where(f, t.astype(np.float64) - y, 0.0)
     np.testing.assert_allclose(g.cpu().numpy(), d / B, rtol=1e-6, atol=1e-8)
-    assert float(loss.cpu()) == pytest.approx(0.5 * np.sum(d * d) / B, rel=1e-5)
+    loss = loss.cpu().numpy()
+    assert float(loss[0]) == pytest.approx(0.5 * np.sum(d * d) / B, rel=1e-5)
+    np.testing.assert_allclose(loss[1:], 0.5 * np.sum(d * d, axis=1) / B, rtol=1e-5, atol=1e-8)
+
+
+@pytest.mark.parametrize("B,N", [(3, 4096), (256, 4096), (1, 1)])
+def test_loss_kernels_wide(dev, B, N):
+    """Many outputs per sample (the 4096-wide layer) and tiny shapes."""
+    import torch
+    from paper_2607_14672_amd import dstd
+    rng = np.random.default_rng(B + N)
+    t = (rng.random((B, N)) * 2).astype(np.float32)
+    t[rng.random((B, N)) < 0.3] = np.inf
+    y = (1 + rng.random((B, N))).astype(np.float32)
+    g, loss = dstd.mse_grad(torch.from_numpy(t).to(dev), torch.from_numpy(y).to(dev))
+    d = np.where(np.isfinite(t), t.astype(np.float64) - y, 0.0)
+    np.testing.assert_allclose(g.cpu().numpy(), d / B, rtol=1e-6, atol=1e-9)
+    assert float(loss[0].cpu()) == pytest.approx(0.5 * np.sum(d * d) / B, rel=1e-5)
+    lab = rng.integers(0, N, B).astype(np.int32)
+    g2, loss2 = dstd.softmax_ce_grad(torch.from_numpy(t).to(dev), torch.from_numpy(lab).to(dev),
+                                     0.5, 5.0)
+    tt = np.where(np.isfinite(t), t, 5.0).astype(np.float64)
+    z = -tt / 0.5
+    sm = np.exp(z - z.max(1, keepdims=True))
+    sm /= sm.sum(1, keepdims=True)
+    ref_g = np.where(np.isfinite(t), -(sm - np.eye(N)[lab]) / 0.5 / B, 0.0)
+    np.testing.assert_allclose(g2.cpu().numpy(), ref_g, rtol=1e-4, atol=1e-9)
+    assert float(loss2[0].cpu()) == pytest.approx(-np.mean(np.log(sm[np.arange(B), lab])), rel=1e-5)

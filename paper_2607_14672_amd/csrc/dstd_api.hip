@@ -105,11 +105,14 @@ dstd_status check_dims(int64_t B, int64_t N_in, int64_t N_out) {
         return fail(DSTD_ERR_SHAPE, "N_in and N_out must be < 2^24");
     if (B > 65535)
         return fail(DSTD_ERR_SHAPE, "B = %lld exceeds the supported batch (65535)", (long long)B);
+    if (N_in * N_out * 4 >= ((int64_t)1 << 31))
+        return fail(DSTD_ERR_SHAPE, "N_in * N_out = %lld exceeds 2^29 weights",
+                    (long long)(N_in * N_out));
     return DSTD_OK;
 }
 
 struct DenseWs {
-    size_t row, L, R, dL, dR, G, part, dtpart, wt, sj, sr, sL, sR, nvalid, rs, total;
+    size_t row, L, R, G, part, wt, sj, sr, sL, sR, nvalid, rs, total;
     int64_t sstride;
 };
 
@@ -118,32 +121,28 @@ DenseWs dense_ws_layout(int M, int64_t B, int64_t N_in, int64_t N_out, bool back
     size_t off = 0;
     size_t n = (size_t)(B * N_in);
     if (!backward && B * N_out == 0) return w;  // the forward enqueues nothing
-    if (!backward) {
-        // forward: transposed weights (room for fp32), sorted events, counts
-        w.wt = off; off += align_up((size_t)N_in * (size_t)N_out * sizeof(float));
-        // sorted event lists: per sample N_in records; the last sample's list
-        // is padded so batched reads past its end stay in the allocation
-        w.sstride = N_in;
-        size_t ns = n + dstd::kSortPad;
-        w.sj = off; off += align_up(ns * sizeof(int));
-        w.sr = off; off += align_up(ns * sizeof(int));
-        w.sL = off; off += align_up(ns * sizeof(float));
-        w.sR = off; off += align_up(ns * sizeof(float));
-        w.nvalid = off; off += align_up((size_t)B * sizeof(int));
-        w.rs = off; off += align_up((size_t)B * (M + 4) * sizeof(int));
-    }
+    // transposed weights (room for fp32) and the row-sorted event records of
+    // every sample: both passes walk them (the backward for dt_in)
+    w.wt = off; off += align_up((size_t)N_in * (size_t)N_out * sizeof(float));
+    // sorted event lists: per sample N_in records; the last sample's list
+    // is padded so batched reads past its end stay in the allocation
+    w.sstride = N_in;
+    size_t ns = n + dstd::kSortPad;
+    w.sj = off; off += align_up(ns * sizeof(int));
+    w.sr = off; off += align_up(ns * sizeof(int));
+    w.sL = off; off += align_up(ns * sizeof(float));
+    w.sR = off; off += align_up(ns * sizeof(float));
+    w.nvalid = off; off += align_up((size_t)B * sizeof(int));
+    w.rs = off; off += align_up((size_t)B * (M + 4) * sizeof(int));
     if (backward) {
+        // per-input events for the dW reduction, scan gradients G, dW partials
         w.row = off; off += align_up(n * sizeof(int));
         w.L = off; off += align_up(n * sizeof(float));
         w.R = off; off += align_up(n * sizeof(float));
-        w.dL = off; off += align_up(n * sizeof(float));
-        w.dR = off; off += align_up(n * sizeof(float));
         w.G = off; off += align_up((size_t)B * (M + 3) * (size_t)N_out * sizeof(float));
         dstd::DwPlan dp = dstd::plan_dw(B, N_in, N_out, M);
         w.part = off;
         if (dp.nsplit > 1) off += align_up((size_t)dp.nsplit * (size_t)N_out * (size_t)N_in * sizeof(float));
-        w.dtpart = off;
-        off += align_up(dstd::dtin_partial_bytes(M, B, N_in, N_out));
     }
     w.total = off;
     return w;
@@ -330,27 +329,23 @@ dstd_status dstd_lif_backward(const dstd_lif_params *p, int64_t B, int64_t N_in,
     hipStream_t st = static_cast<hipStream_t>(stream);
     hipError_t e;
     // Empty sizes need no special case: with B == 0 the dW kernel writes
-    // zeros, with N_out == 0 the dt_in kernel does (no memset is used, so the
-    // call stays safe to capture in a graph).
+    // zeros; dt_in is zeroed by the event sort and only inputs with events
+    // are written after that (no memset is used, so the call stays safe to
+    // capture in a graph).
     LifConst C = make_const(p);
-    int *row = at<int>(ws, L.row);
-    float *Lw = at<float>(ws, L.L), *Rw = at<float>(ws, L.R);
-    float *dLw = at<float>(ws, L.dL), *dRw = at<float>(ws, L.dR);
-    float *G = at<float>(ws, L.G);
-    e = dstd::launch_bin_events(C, B * N_in, t_in, row, Lw, Rw, dLw, dRw, st);
-    if (e != hipSuccess) return hip_status(e, "bin_events launch");
-    e = dstd::launch_grad_g(C, B, 1, N_out, t_out, slope, q_idx, grad_t_out, G, st);
-    if (e != hipSuccess) return hip_status(e, "grad_g launch");
-    if (grad_W && N_out * N_in > 0) {
-        e = dstd::launch_dw(C, B, N_in, N_out, G, row, Lw, Rw, grad_W, at<float>(ws, L.part), st);
-        if (e != hipSuccess) return hip_status(e, "dW launch");
-    }
-    if (grad_t_in && B * N_in > 0) {
-        e = dstd::launch_dtin(C, B, N_in, N_out, G, W, w_dtype == DSTD_BF16, row, dLw, dRw,
-                              grad_t_in, at<float>(ws, L.dtpart), st);
-        if (e != hipSuccess) return hip_status(e, "dt_in launch");
-    }
-    return DSTD_OK;
+    dstd::DenseBwdWs bw;
+    bw.row = at<int>(ws, L.row);
+    bw.L = at<float>(ws, L.L);
+    bw.R = at<float>(ws, L.R);
+    bw.srt = dstd::SortedEv{at<int>(ws, L.sj), at<int>(ws, L.sr), at<float>(ws, L.sL),
+                            at<float>(ws, L.sR), L.sstride, at<int>(ws, L.rs)};
+    bw.n_valid = at<int>(ws, L.nvalid);
+    bw.wt = at<void>(ws, L.wt);
+    bw.G = at<float>(ws, L.G);
+    bw.part = at<float>(ws, L.part);
+    e = dstd::launch_backward(C, B, N_in, N_out, W, w_dtype == DSTD_BF16, t_in, t_out, slope,
+                              q_idx, grad_t_out, bw, grad_W, grad_t_in, st);
+    return hip_status(e, "backward launch");
 }
 
 dstd_status dstd_softmax_ce_grad(int64_t B, int64_t N, const float *t_out, const int32_t *labels,

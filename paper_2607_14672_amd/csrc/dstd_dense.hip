@@ -1,12 +1,14 @@
 // dstd_dense.hip -- DSTD-LIF dense-layer kernels for gfx950.
 //
-// The event matrix S[b, m, j] has at most two nonzeros per (b, j): the
-// DSTD kernel has two-point support (App. B.3). The contraction
-// w^[b, m, i] = sum_j W[i, j] S[b, m, j] therefore runs as a scatter of the
-// two weighted halves of every input into per-neuron bins held in LDS,
-// instead of a dense (M+1)-row GEMM that would spend (M+1)/2 times the
-// method's multiply-adds on zeros. The per-neuron interval scan and root
-// solve read the bins straight from LDS, so w^ never goes to HBM.
+// The event matrix S[b, m, j] has at most two nonzeros per (b, j): the DSTD
+// kernel has two-point support (App. B.3). The contraction
+// w^[b, m, i] = sum_j W[i, j] S[b, m, j] therefore runs over each sample's
+// inputs sorted by event row: a wavefront (lanes = neurons) adds W[i, j] L and
+// W[i, j] R of every input to the running sums of its row and feeds each
+// closed row to the interval scan, instead of a dense (M+1)-row GEMM that
+// would spend (M+1)/2 times the method's multiply-adds on zeros. The weighted
+// events never go to HBM. The backward walks the same sorted lists for dt_in
+// and reduces dW over the batch with per-input events.
 #include "dstd_internal.h"
 #include "dstd_kernels.h"
 #include "dstd_profile.h"
@@ -15,49 +17,31 @@
 
 namespace dstd {
 
-// ---------------------------------------------------------------- events --
-// One thread per (b, j). Structure-of-arrays outputs so that kernels reading
-// them per wave (uniform j) or per lane (j across lanes) are both coalesced.
-__global__ __launch_bounds__(256) void bin_events_kernel(LifConst C, int64_t n,
-                                                         const float *__restrict__ t_in,
-                                                         int *__restrict__ ev_row,
-                                                         float *__restrict__ ev_L,
-                                                         float *__restrict__ ev_R,
-                                                         float *__restrict__ ev_dL,
-                                                         float *__restrict__ ev_dR) {
-    int64_t k = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
-    if (k >= n) return;
-    Event e = bin_event(C, t_in[k]);
-    ev_row[k] = e.row;
-    ev_L[k] = e.L;
-    ev_R[k] = e.R;
-    if (ev_dL) {
-        ev_dL[k] = e.dL;
-        ev_dR[k] = e.dR;
-    }
-}
-
 // ----------------------------------------------------------- event sort --
 // Per sample, the inputs that have events, sorted by event row (stable: j
-// ascending within a row), as structure-of-arrays records {j, row, L, R}.
+// ascending within a row), as structure-of-arrays records {j, row, L, R}
+// (with deriv: the derivatives dL, dR in place of L, R), plus the row starts.
 // One block of kSortWaves wavefronts per sample; wave w owns a contiguous
 // range of inputs. Row histograms per wave (integer LDS atomics, order-free)
 // give every (row, wave) pair its start offset; each wave then places its
 // inputs 64 at a time, each lane ranked among the lanes of its batch with the
-// same row. The fixed order keeps every sum of the forward pass bitwise
-// reproducible.
+// same row (one ballot per distinct row). The fixed order keeps every sum of
+// the forward pass bitwise reproducible.
 constexpr int kSortWaves = 8;
+constexpr int kPrepThreads = kSortWaves * 64;
 
-__global__ __launch_bounds__(kSortWaves * 64) void bin_sort_kernel(LifConst C, int N_in,
-                                                                   const float *__restrict__ t_in,
-                                                                   SortedEv srt,
-                                                                   int *__restrict__ n_valid) {
-    extern __shared__ int sh[];  // hist [kSortWaves][R], rowstart [R + 1]
-    const int b = blockIdx.x;
+// Optional per-input outputs of the sort, in input order [B][N_in]: the
+// events (row -1: none) for the dW reduction, and an array set to zero
+// (dt_in, whose inputs with events are written later).
+struct SortOut { int *row; float *L; float *R; float *zero; };
+
+__device__ void sort_sample(const LifConst &C, int b, int N_in, const float *__restrict__ t_in,
+                            SortedEv srt, int *__restrict__ n_valid, int deriv, SortOut xo,
+                            int *sh) {
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = uniform(threadIdx.x >> 6);
     const int R = rows_of(C);
-    int *hist = sh;
+    int *hist = sh;  // [kSortWaves][R], then rowstart [R + 1]
     int *rowstart = sh + kSortWaves * R;
     const float *tb = t_in + static_cast<int64_t>(b) * N_in;
     const int per = ((N_in + kSortWaves * kWave - 1) / (kSortWaves * kWave)) * kWave;
@@ -93,50 +77,129 @@ __global__ __launch_bounds__(kSortWaves * 64) void bin_sort_kernel(LifConst C, i
     }
     __syncthreads();
     const int64_t ob = static_cast<int64_t>(b) * srt.stride;
+    const int64_t ib = static_cast<int64_t>(b) * N_in;
     int *next = hist + wave * R;
+    const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
     for (int j0 = j_lo; j0 < j_hi; j0 += kWave) {
         const int j = j0 + lane;
         Event e{-1, 0.f, 0.f, 0.f, 0.f};
         if (j < j_hi) e = bin_event(C, tb[j]);
         const int r = e.row;
-        int rank = 0, total = 0;
-#pragma unroll
-        for (int l = 0; l < kWave; ++l) {
-            const int rl = __shfl(r, l);
-            const bool same = (rl == r);
-            rank += (same && l < lane) ? 1 : 0;
-            total += same ? 1 : 0;
+        if (j < j_hi) {
+            if (xo.row) {
+                xo.row[ib + j] = r;
+                xo.L[ib + j] = e.L;
+                xo.R[ib + j] = e.R;
+            }
+            if (xo.zero) xo.zero[ib + j] = 0.f;
         }
-        const int pos = (r >= 0) ? next[r] + rank : 0;
+        int pos = 0;
+        uint64_t todo = __ballot(r >= 0);
+        while (todo) {
+            const int lead = __ffsll(static_cast<unsigned long long>(todo)) - 1;
+            const int rl = __builtin_amdgcn_readlane(r, lead);
+            const uint64_t same = __ballot(r == rl);
+            const int base = next[rl];
+            if (r == rl) pos = base + __popcll(same & below);
+            __builtin_amdgcn_wave_barrier();
+            if (lane == lead) next[rl] = base + __popcll(same);
+            __builtin_amdgcn_wave_barrier();
+            todo &= ~same;
+        }
         if (r >= 0) {
             const int64_t o = ob + pos;
             srt.j[o] = j;
             srt.r[o] = r;
-            srt.L[o] = e.L;
-            srt.R[o] = e.R;
+            srt.L[o] = deriv ? e.dL : e.L;
+            srt.R[o] = deriv ? e.dR : e.R;
         }
-        __builtin_amdgcn_wave_barrier();
-        if (r >= 0 && rank == total - 1) next[r] = pos + 1;  // one lane per row
-        __builtin_amdgcn_wave_barrier();
     }
 }
 
-// W [N_out][N_in] -> WT [N_in][N_out] through a padded LDS tile.
+// W [N_out][N_in] -> WT [N_in][N_out], one 32 x 32 tile through a padded LDS
+// tile (kPrepThreads threads: 32 x 16).
 template <typename WT>
-__global__ __launch_bounds__(256) void transpose_kernel(int rows, int cols,
-                                                        const WT *__restrict__ in,
-                                                        WT *__restrict__ out) {
-    __shared__ WT tile[32][33];
-    const int c0 = blockIdx.x * 32, r0 = blockIdx.y * 32;
-    const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;  // 32 x 8
-    for (int k = ty; k < 32; k += 8) {
+__device__ void transpose_tile(int rows, int cols, const WT *__restrict__ in, WT *__restrict__ out,
+                               int tile, WT (*buf)[33]) {
+    const int ntx = (cols + 31) / 32;
+    const int c0 = (tile % ntx) * 32, r0 = (tile / ntx) * 32;
+    const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
+    for (int k = ty; k < 32; k += kPrepThreads / 32) {
         const int r = r0 + k, c = c0 + tx;
-        if (r < rows && c < cols) tile[k][tx] = in[static_cast<int64_t>(r) * cols + c];
+        if (r < rows && c < cols) buf[k][tx] = in[static_cast<int64_t>(r) * cols + c];
     }
     __syncthreads();
-    for (int k = ty; k < 32; k += 8) {
+    for (int k = ty; k < 32; k += kPrepThreads / 32) {
         const int c = c0 + k, r = r0 + tx;
-        if (r < rows && c < cols) out[static_cast<int64_t>(c) * rows + r] = tile[tx][k];
+        if (r < rows && c < cols) out[static_cast<int64_t>(c) * rows + r] = buf[tx][k];
+    }
+}
+
+// G[b, r, i] = dL/dw^[b, m = r-1, i] = -g K(t - T_m) / slope for m <= q,
+// 0 otherwise (and in the two end rows). K(t - T_m) follows the exact
+// backward recurrence K(s + dt) = alpha K(s) + K(dt) e^{-s/ti}, all terms
+// positive, so no per-element exponential and no cancellation; it runs in
+// fp64 so its rounding does not grow with the number of intervals.
+__device__ void grad_g_one(const LifConst &C, int64_t k, int N_out, const float *__restrict__ t_out,
+                           const float *__restrict__ slope, const int *__restrict__ q_idx,
+                           const float *__restrict__ grad_t, float *__restrict__ G) {
+    const int64_t b = k / N_out;
+    const int i = static_cast<int>(k % N_out);
+    const int R = rows_of(C);
+    float *g = G + b * R * N_out + i;
+    const int q = q_idx[k];
+    const float gv = (q >= 0) ? grad_t[k] : 0.f;
+    g[0] = 0.f;
+    g[static_cast<int64_t>(R - 1) * N_out] = 0.f;
+    if (q < 0 || gv == 0.f) {
+        for (int m = 0; m <= C.M; ++m) g[static_cast<int64_t>(m + 1) * N_out] = 0.f;
+        return;
+    }
+    const float gam = -gv / fmaxf(slope[k], C.slope_floor);
+    const double T_q = fma(static_cast<double>(q), static_cast<double>(C.dt), static_cast<double>(C.t0));
+    const float u = static_cast<float>(fmax(static_cast<double>(t_out[k]) - T_q, 0.0));
+    const float ev = expf(-u * C.inv_tv);
+    const float em = expm1f(-C.kappa * u);
+    double K = -C.c * ev * em;   // K(u)
+    double Q = ev * (1.f + em);  // e^{-u/ti}
+    for (int m = C.M; m > q; --m) g[static_cast<int64_t>(m + 1) * N_out] = 0.f;
+    for (int m = q; m >= 0; --m) {
+        g[static_cast<int64_t>(m + 1) * N_out] = static_cast<float>(gam * K);
+        K = fma(C.alpha_d, K, C.k_dt_d * Q);
+        Q *= C.beta_d;
+    }
+}
+
+// Independent setup work of a layer call in one launch, by block role:
+// blocks [0, n_sort) sort one sample each, the next n_tr blocks transpose one
+// weight tile each, the rest compute G for kPrepThreads neurons each
+// (backward only). One launch instead of three: every launch costs a few
+// microseconds even when its work is tiny.
+struct PrepGrad {
+    const float *t_out, *slope, *grad_t;
+    const int *q_idx;
+    float *G;
+};
+
+template <typename WT>
+__global__ __launch_bounds__(kPrepThreads) void prep_kernel(LifConst C, int n_sort, int n_tr,
+                                                            int N_in, int N_out,
+                                                            const float *__restrict__ t_in,
+                                                            SortedEv srt, int *__restrict__ n_valid,
+                                                            int deriv, SortOut xo,
+                                                            const WT *__restrict__ W,
+                                                            WT *__restrict__ Wt, PrepGrad pg,
+                                                            int64_t n_grad) {
+    extern __shared__ int sh[];
+    __shared__ WT buf[32][33];
+    const int blk = blockIdx.x;
+    if (blk < n_sort) {
+        sort_sample(C, blk, N_in, t_in, srt, n_valid, deriv, xo, sh);
+    } else if (blk < n_sort + n_tr) {
+        transpose_tile<WT>(N_out, N_in, W, Wt, blk - n_sort, buf);
+    } else {
+        const int64_t k = static_cast<int64_t>(blk - n_sort - n_tr) * kPrepThreads + threadIdx.x;
+        if (k < n_grad) grad_g_one(C, k, N_out, pg.t_out, pg.slope, pg.q_idx, pg.grad_t, pg.G);
     }
 }
 
@@ -379,53 +442,6 @@ __global__ __launch_bounds__(kRowWaves * 64) void fwd_rows_kernel(LifConst C, in
     q_idx[o] = q;
 }
 
-// ------------------------------------------------------------ scan grads --
-// G[b, r, i] = dL/dw^[b, m = r-1, i] = -g K(t - T_m) / slope for m <= q,
-// 0 otherwise (and in the two end rows). K(t - T_m) follows the exact
-// backward recurrence K(s + dt) = alpha K(s) + K(dt) e^{-s/ti}, all terms
-// positive, so no per-element exponential and no cancellation; it runs in
-// fp64 so its rounding does not grow with the number of intervals.
-// Neurons are (channel c, position p) pairs, N_out = n_pos * n_ch: outputs
-// are read channel-major (o = (b, c, p), NCHW for a conv layer) and G is
-// written position-major, G[b, r, p, c], so a position's channels are
-// contiguous. A dense layer is the case n_pos = 1.
-__global__ __launch_bounds__(256) void grad_g_kernel(LifConst C, int B, int n_pos, int n_ch,
-                                                     const float *__restrict__ t_out,
-                                                     const float *__restrict__ slope,
-                                                     const int *__restrict__ q_idx,
-                                                     const float *__restrict__ grad_t,
-                                                     float *__restrict__ G) {
-    const int N_out = n_pos * n_ch;
-    int64_t t = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
-    if (t >= static_cast<int64_t>(B) * N_out) return;
-    const int b = static_cast<int>(t / N_out), rem = static_cast<int>(t % N_out);
-    const int p = rem / n_ch, c = rem % n_ch;
-    const int64_t k = static_cast<int64_t>(b) * N_out + static_cast<int64_t>(c) * n_pos + p;
-    const int R = rows_of(C);
-    float *g = G + static_cast<int64_t>(b) * R * N_out + rem;
-    int q = q_idx[k];
-    float gv = (q >= 0) ? grad_t[k] : 0.f;
-    g[0] = 0.f;
-    g[static_cast<int64_t>(R - 1) * N_out] = 0.f;
-    if (q < 0 || gv == 0.f) {
-        for (int m = 0; m <= C.M; ++m) g[static_cast<int64_t>(m + 1) * N_out] = 0.f;
-        return;
-    }
-    float gam = -gv / fmaxf(slope[k], C.slope_floor);
-    double T_q = fma(static_cast<double>(q), static_cast<double>(C.dt), static_cast<double>(C.t0));
-    float u = static_cast<float>(fmax(static_cast<double>(t_out[k]) - T_q, 0.0));
-    float ev = expf(-u * C.inv_tv);
-    float em = expm1f(-C.kappa * u);
-    double K = -C.c * ev * em;   // K(u)
-    double Q = ev * (1.f + em);  // e^{-u/ti}
-    for (int m = C.M; m > q; --m) g[static_cast<int64_t>(m + 1) * N_out] = 0.f;
-    for (int m = q; m >= 0; --m) {
-        g[static_cast<int64_t>(m + 1) * N_out] = static_cast<float>(gam * K);
-        K = fma(C.alpha_d, K, C.k_dt_d * Q);
-        Q *= C.beta_d;
-    }
-}
-
 // ----------------------------------------------------------------- dW ----
 // dW[i, j] = sum_b (G[b, r_bj, i] L_bj + G[b, r_bj + 1, i] R_bj).
 // Lane = input j (events are coalesced vector loads); a block covers
@@ -528,86 +544,128 @@ __global__ __launch_bounds__(256) void reduce_splits_kernel(int64_t n, int nspli
     out[k] = s;
 }
 
-// ------------------------------------------------------------- dt_in ----
-// dt_in[b, j] = dL_bj sum_i W[i, j] G[b, r, i] + dR_bj sum_i W[i, j] G[b, r+1, i]
-// (r = event row of input j in sample b). Lane = input j (coalesced W rows
-// and events); a block holds SB samples' G tiles for 64 neurons in LDS,
-// row-major with an odd row stride (65 words), so the lane-dependent rows r,
-// r+1 of one neuron come from one conflict-free ds_read2_b32 whose neuron
-// offset is an immediate. An extra zero row serves inputs without events.
-// The neuron range may be split across blocks (blockIdx.z): each split
-// writes its partial dt_in, summed in a fixed order.
+// -------------------------------------------------------- dt_in (rows) --
+// dt_in of every input with events, from its sample's row-sorted records
+// {j, row r, dL, dR}: dL sum_i W[i, j] G[b, r, i] + dR sum_i W[i, j] G[b, r+1, i].
+// A block takes a contiguous range of whole event rows of one sample
+// (kDtRanges ranges per sample, about equal in records); its four waves walk
+// the same records, each over its own NTW 64-neuron tiles per group of
+// 4 * NTW tiles (lane = neuron: WT row j is one coalesced load per tile).
+// Records go 8 at a time: each wave reduces its lanes (fixed butterfly), the
+// four wave sums are added in wave order through LDS. Inputs without events
+// are not visited (their dt_in was zeroed earlier).
+constexpr int kDtRanges = 16;
 
-template <int SB, typename WT>
-__global__ __launch_bounds__(256) void dtin_dense_kernel(LifConst C, int B, int N_in, int N_out,
-                                                          int i_per_split,
-                                                          const float *__restrict__ G,
-                                                          const WT *__restrict__ W,
-                                                          const int *__restrict__ ev_row,
-                                                          const float *__restrict__ ev_dL,
-                                                          const float *__restrict__ ev_dR,
-                                                          float *__restrict__ out) {
-    extern __shared__ float gs[];  // [SB][R + 1][kDtStride]
+// The launch may carry extra blocks (blockIdx.y >= B) that finish the dW
+// split reduction of the same layer (independent work, one launch less).
+struct RedJob { int64_t n; int nsplit; const float *part; float *out; };
+
+template <typename WT, int NTW>
+__global__ __launch_bounds__(256) void dtin_rows_kernel(LifConst C, int B, int N_in, int N_out,
+                                                        const WT *__restrict__ Wt, SortedEv srt,
+                                                        const float *__restrict__ G,
+                                                        float *__restrict__ dt_in, RedJob red) {
+    __shared__ float part[4][kBatch];
+    if (static_cast<int>(blockIdx.y) >= B) {
+        const int64_t k = (static_cast<int64_t>(blockIdx.y - B) * gridDim.x + blockIdx.x) * blockDim.x +
+                          threadIdx.x;
+        if (k < red.n) {
+            float s = 0.f;
+            for (int z = 0; z < red.nsplit; ++z) s += red.part[static_cast<int64_t>(z) * red.n + k];
+            red.out[k] = s;
+        }
+        return;
+    }
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = uniform(threadIdx.x >> 6);
+    const int range = blockIdx.x;
+    const int b = blockIdx.y;
     const int R = rows_of(C);
-    const int RT = R + 1;
-    const int j = blockIdx.x * blockDim.x + threadIdx.x;
-    const int b0 = blockIdx.y * SB;
-    const int i_lo = blockIdx.z * i_per_split;
-    const int i_hi = min(N_out, i_lo + i_per_split);
-    const bool j_ok = j < N_in;
-    int base[SB];
-    float aL[SB], aR[SB];
-#pragma unroll
-    for (int s = 0; s < SB; ++s) {
-        aL[s] = 0.f;
-        aR[s] = 0.f;
-        int b = b0 + s;
-        int r = (j_ok && b < B) ? ev_row[static_cast<int64_t>(b) * N_in + j] : -1;
-        if (r < 0) r = R - 1;  // rows R-1 and R are zero
-        base[s] = (s * RT + r) * kDtStride;
-    }
-    // the extra zero row of every sample tile
-    for (int k = threadIdx.x; k < SB * kDtStride; k += blockDim.x)
-        gs[((k / kDtStride) * RT + R) * kDtStride + (k % kDtStride)] = 0.f;
-    for (int i0 = i_lo; i0 < i_hi; i0 += kWave) {
-        const int ni = min(kWave, i_hi - i0);
-        // weights of this neuron chunk for the lane's input, issued before the
-        // barrier so their latency overlaps the staging
-        float w[kWave];
-#pragma unroll
-        for (int ii = 0; ii < kWave; ++ii)
-            w[ii] = (j_ok && ii < ni) ? WLoad<WT>::get(W, static_cast<int64_t>(i0 + ii) * N_in + j)
-                                      : 0.f;
-        __syncthreads();
-        for (int k = threadIdx.x; k < SB * R * kWave; k += blockDim.x) {
-            const int s = k / (R * kWave);
-            const int r = (k / kWave) % R;
-            const int l = k % kWave;
-            const int b = b0 + s;
-            gs[(s * RT + r) * kDtStride + l] =
-                (b < B && l < ni) ? G[(static_cast<int64_t>(b) * R + r) * N_out + i0 + l] : 0.f;
+    const int *rs = srt.rs + static_cast<int64_t>(b) * (R + 1);
+    const int n = *as_const(rs + R);
+    auto row_of = [&](int t) {
+        int lo = 0, hi = R - 1;
+        if (t >= n) return R - 1;
+        while (hi - lo > 1) {
+            const int mid = (lo + hi) >> 1;
+            if (*as_const(rs + mid) <= t) lo = mid; else hi = mid;
         }
-        __syncthreads();
+        return lo;
+    };
+    const int r_lo = (range == 0) ? 0 : row_of(static_cast<int>((static_cast<int64_t>(n) * range) / kDtRanges));
+    const int r_hi = (range == kDtRanges - 1)
+                         ? R - 1
+                         : row_of(static_cast<int>((static_cast<int64_t>(n) * (range + 1)) / kDtRanges));
+    if (*as_const(rs + r_lo) == *as_const(rs + r_hi)) return;  // block-uniform: no records
+    const int64_t eo = static_cast<int64_t>(b) * srt.stride;
+    const int *ej = srt.j + eo;
+    const float *edl = srt.L + eo;
+    const float *edr = srt.R + eo;
+    const float *Gb = G + static_cast<int64_t>(b) * R * N_out;
+    const __amdgpu_buffer_rsrc_t wr =
+        make_rsrc(Wt, static_cast<uint32_t>(static_cast<int64_t>(N_in) * N_out * sizeof(WT)));
+    const int rstride = N_out * static_cast<int>(sizeof(WT));
+    const unsigned jmax = static_cast<unsigned>(max(N_in - 1, 0));
+    constexpr int kGroup = 4 * NTW * kWave;
+    const int ngroups = (N_out + kGroup - 1) / kGroup;
+    for (int r = r_lo; r < r_hi; ++r) {
+        const int s = *as_const(rs + r), e = *as_const(rs + r + 1);
+        for (int k0 = s; k0 < e; k0 += kBatch) {
+            const int nk = min(kBatch, e - k0);
+            int jo[kBatch];
+            float dl[kBatch], dr[kBatch], v[kBatch];
 #pragma unroll
-        for (int ii = 0; ii < kWave; ++ii) {
-#pragma unroll
-            for (int s = 0; s < SB; ++s) {
-                const float g0 = gs[base[s] + ii];
-                const float g1 = gs[base[s] + kDtStride + ii];
-                aL[s] = fmaf(w[ii], g0, aL[s]);
-                aR[s] = fmaf(w[ii], g1, aR[s]);
+            for (int kk = 0; kk < kBatch; ++kk) {
+                jo[kk] = static_cast<int>(min(static_cast<unsigned>(as_const(ej + k0)[kk]), jmax)) * rstride;
+                dl[kk] = as_const(edl + k0)[kk];
+                dr[kk] = as_const(edr + k0)[kk];
+                v[kk] = 0.f;
             }
-        }
-    }
-    if (!j_ok) return;
+            for (int grp = 0; grp < ngroups; ++grp) {
+                float g0[NTW], g1[NTW], w[kBatch][NTW];
+                int voff[NTW];
 #pragma unroll
-    for (int s = 0; s < SB; ++s) {
-        const int b = b0 + s;
-        if (b >= B) continue;
-        const int64_t o = static_cast<int64_t>(b) * N_in + j;
-        const bool has = (base[s] != (s * RT + R - 1) * kDtStride);
-        out[static_cast<int64_t>(blockIdx.z) * B * N_in + o] =
-            has ? fmaf(aL[s], ev_dL[o], aR[s] * ev_dR[o]) : 0.f;
+                for (int t = 0; t < NTW; ++t) {
+                    const int i = grp * kGroup + (wave * NTW + t) * kWave + lane;
+                    const int ic = min(i, N_out - 1);
+                    const bool ok = i < N_out;
+                    g0[t] = ok ? Gb[static_cast<int64_t>(r) * N_out + ic] : 0.f;
+                    g1[t] = ok ? Gb[static_cast<int64_t>(r + 1) * N_out + ic] : 0.f;
+                    voff[t] = ic * static_cast<int>(sizeof(WT));
+                }
+#pragma unroll
+                for (int kk = 0; kk < kBatch; ++kk)
+#pragma unroll
+                    for (int t = 0; t < NTW; ++t) w[kk][t] = BufLoad<WT>::get(wr, voff[t], jo[kk]);
+#pragma unroll
+                for (int kk = 0; kk < kBatch; ++kk)
+#pragma unroll
+                    for (int t = 0; t < NTW; ++t)
+                        v[kk] = fmaf(w[kk][t], fmaf(dl[kk], g0[t], dr[kk] * g1[t]), v[kk]);
+            }
+#pragma unroll
+            for (int m = kWave / 2; m >= 1; m >>= 1) {
+#pragma unroll
+                for (int kk = 0; kk < kBatch; ++kk) v[kk] += __shfl_xor(v[kk], m);
+            }
+            float mine = 0.f;
+#pragma unroll
+            for (int kk = 0; kk < kBatch; ++kk)
+                if (lane == kk) mine = v[kk];
+            if (lane < kBatch) part[wave][lane] = mine;
+            __syncthreads();
+            if (wave == 0 && lane < nk) {
+                int jl = 0;
+#pragma unroll
+                for (int kk = 0; kk < kBatch; ++kk) {
+                    const int jk = as_const(ej + k0)[kk];
+                    if (lane == kk) jl = jk;
+                }
+                dt_in[static_cast<int64_t>(b) * N_in + jl] =
+                    ((part[0][lane] + part[1][lane]) + part[2][lane]) + part[3][lane];
+            }
+            __syncthreads();
+        }
     }
 }
 
@@ -697,13 +755,36 @@ __global__ __launch_bounds__(kLossThreads) void loss_total_kernel(int B, float *
 }
 
 // ------------------------------------------------------------- launchers --
-hipError_t launch_bin_events(const LifConst &C, int64_t n, const float *t_in, int *row, float *L,
-                             float *R, float *dL, float *dR, hipStream_t st) {
-    if (n == 0) return hipSuccess;
-    int64_t blocks = (n + 255) / 256;
-    ProfScope prof("bin_events", st);
-    hipLaunchKernelGGL(bin_events_kernel, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, st, C,
-                       n, t_in, row, L, R, dL, dR);
+static int tiles32(int64_t N_in, int64_t N_out) {
+    return static_cast<int>(((N_in + 31) / 32) * ((N_out + 31) / 32));
+}
+
+static size_t sort_lds_bytes(const LifConst &C) {
+    const int R = C.M + 3;
+    return static_cast<size_t>(kSortWaves * R + R + 1) * sizeof(int);
+}
+
+static hipError_t launch_prep(const LifConst &C, int64_t B, int64_t N_in, int64_t N_out,
+                              const float *t_in, SortedEv srt, int *n_valid, bool deriv, SortOut xo,
+                              const void *W, bool bf16, void *Wt, bool transpose, PrepGrad pg,
+                              int64_t n_grad, const char *name, hipStream_t st) {
+    const int n_tr = (transpose && N_in * N_out > 0) ? tiles32(N_in, N_out) : 0;
+    const int64_t n_gb = (n_grad + kPrepThreads - 1) / kPrepThreads;
+    const int64_t blocks = B + n_tr + n_gb;
+    if (blocks == 0) return hipSuccess;
+    ProfScope prof(name, st);
+    if (bf16)
+        hipLaunchKernelGGL(prep_kernel<uint16_t>, dim3(static_cast<unsigned>(blocks)),
+                           dim3(kPrepThreads), sort_lds_bytes(C), st, C, static_cast<int>(B), n_tr,
+                           static_cast<int>(N_in), static_cast<int>(N_out), t_in, srt, n_valid,
+                           deriv ? 1 : 0, xo, static_cast<const uint16_t *>(W),
+                           static_cast<uint16_t *>(Wt), pg, n_grad);
+    else
+        hipLaunchKernelGGL(prep_kernel<float>, dim3(static_cast<unsigned>(blocks)),
+                           dim3(kPrepThreads), sort_lds_bytes(C), st, C, static_cast<int>(B), n_tr,
+                           static_cast<int>(N_in), static_cast<int>(N_out), t_in, srt, n_valid,
+                           deriv ? 1 : 0, xo, static_cast<const float *>(W),
+                           static_cast<float *>(Wt), pg, n_grad);
     return hipGetLastError();
 }
 
@@ -711,27 +792,10 @@ hipError_t launch_forward(const LifConst &C, int64_t B, int64_t N_in, int64_t N_
                           bool bf16, void *Wt, SortedEv srt, int *n_valid, const float *t_in,
                           float *t_out, float *slope, int *q_idx, hipStream_t st) {
     const int R = C.M + 3;
-    {
-        ProfScope prof("bin_sort", st);
-        hipLaunchKernelGGL(bin_sort_kernel, dim3(static_cast<unsigned>(B)), dim3(kSortWaves * kWave),
-                           (kSortWaves * R + R + 1) * sizeof(int), st, C, static_cast<int>(N_in), t_in,
-                           srt, n_valid);
-    }
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    dim3 tg(static_cast<unsigned>((N_in + 31) / 32), static_cast<unsigned>((N_out + 31) / 32));
-    if (N_in > 0) {
-        ProfScope prof("transpose_w", st);
-        if (bf16)
-            hipLaunchKernelGGL(transpose_kernel<uint16_t>, tg, dim3(256), 0, st,
-                               static_cast<int>(N_out), static_cast<int>(N_in),
-                               static_cast<const uint16_t *>(W), static_cast<uint16_t *>(Wt));
-        else
-            hipLaunchKernelGGL(transpose_kernel<float>, tg, dim3(256), 0, st, static_cast<int>(N_out),
-                               static_cast<int>(N_in), static_cast<const float *>(W),
-                               static_cast<float *>(Wt));
-    }
-    e = hipGetLastError();
+    hipError_t e = launch_prep(C, B, N_in, N_out, t_in, srt, n_valid, false,
+                               SortOut{nullptr, nullptr, nullptr, nullptr}, W, bf16, Wt, true,
+                               PrepGrad{nullptr, nullptr, nullptr, nullptr, nullptr}, 0,
+                               "sort_transpose", st);
     if (e != hipSuccess) return e;
     ProfScope prof("fwd_dense", st);
     if (C.M <= kRowsMaxM) {
@@ -758,18 +822,6 @@ hipError_t launch_forward(const LifConst &C, int64_t B, int64_t N_in, int64_t N_
         hipLaunchKernelGGL(fwd_sorted_kernel<float>, grid, dim3(waves * kWave), 0, st, C,
                            static_cast<int>(B), static_cast<int>(N_in), static_cast<int>(N_out),
                            static_cast<const float *>(Wt), srt, n_valid, t_out, slope, q_idx);
-    return hipGetLastError();
-}
-
-hipError_t launch_grad_g(const LifConst &C, int64_t B, int64_t n_pos, int64_t n_ch,
-                         const float *t_out, const float *slope, const int *q_idx,
-                         const float *grad_t, float *G, hipStream_t st) {
-    int64_t n = B * n_pos * n_ch;
-    if (n == 0) return hipSuccess;
-    ProfScope prof("grad_g", st);
-    hipLaunchKernelGGL(grad_g_kernel, dim3(static_cast<unsigned>((n + 255) / 256)), dim3(256), 0,
-                       st, C, static_cast<int>(B), static_cast<int>(n_pos), static_cast<int>(n_ch),
-                       t_out, slope, q_idx, grad_t, G);
     return hipGetLastError();
 }
 
@@ -800,93 +852,83 @@ DwPlan plan_dw(int64_t B, int64_t N_in, int64_t N_out, int M) {
     return p;
 }
 
-hipError_t launch_dw(const LifConst &C, int64_t B, int64_t N_in, int64_t N_out, const float *G,
-                     const int *row, const float *L, const float *R, float *dW, float *part,
-                     hipStream_t st) {
-    DwPlan p = plan_dw(B, N_in, N_out, C.M);
+static hipError_t launch_dw(const LifConst &C, const DwPlan &p, int64_t B, int64_t N_in,
+                            int64_t N_out, const float *G, const int *row, const float *L,
+                            const float *R, float *dst, hipStream_t st) {
     const int ti = p.jw;
     const int pstride = (C.M + 3) | 1;
     dim3 grid(static_cast<unsigned>((N_in + 255) / 256),
               static_cast<unsigned>((N_out + ti - 1) / ti), static_cast<unsigned>(p.nsplit));
     size_t lds = 2 * static_cast<size_t>(ti) * pstride * sizeof(float2);
-    float *dst = (p.nsplit == 1) ? dW : part;
-    {
-        ProfScope prof("dw_dense", st);
-        const int nper = dw_nper(C.M, ti);
+    ProfScope prof("dw_dense", st);
+    const int nper = dw_nper(C.M, ti);
 #define DW_LAUNCH(TIV, NP)                                                                        \
     hipLaunchKernelGGL((dw_dense_kernel<TIV, NP>), grid, dim3(256), lds, st, C, static_cast<int>(B), \
                        static_cast<int>(N_in), static_cast<int>(N_out), p.b_per_split, pstride, G, \
                        row, L, R, dst)
-        if (ti == 64) {
-            if (nper == 9) DW_LAUNCH(64, 9);
-            else if (nper == 17) DW_LAUNCH(64, 17);
-            else DW_LAUNCH(64, 33);
-        } else {
-            if (nper == 9) DW_LAUNCH(32, 9);
-            else if (nper == 17) DW_LAUNCH(32, 17);
-            else DW_LAUNCH(32, 33);
-        }
-#undef DW_LAUNCH
-    }
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess || p.nsplit == 1) return e;
-    int64_t n = N_out * N_in;
-    ProfScope prof("dw_reduce", st);
-    hipLaunchKernelGGL(reduce_splits_kernel, dim3(static_cast<unsigned>((n + 255) / 256)), dim3(256),
-                       0, st, n, p.nsplit, part, dW);
-    return hipGetLastError();
-}
-
-static int dtin_sb(int M) { return (M + 4) * kDtStride * 2 * sizeof(float) <= 80 * 1024 ? 2 : 1; }
-
-static int dtin_nsplit(int64_t B, int64_t N_in, int64_t N_out, int sb) {
-    const int64_t blocks = ((N_in + 255) / 256) * ((B + sb - 1) / sb);
-    const int64_t chunks = (N_out + kWave - 1) / kWave;
-    int64_t ns = 1;
-    while (blocks * ns < 1024 && ns * 2 <= chunks && ns < 16) ns *= 2;
-    return static_cast<int>(ns);
-}
-
-size_t dtin_partial_bytes(int M, int64_t B, int64_t N_in, int64_t N_out) {
-    int ns = dtin_nsplit(B, N_in, N_out, dtin_sb(M));
-    return ns > 1 ? static_cast<size_t>(ns) * B * N_in * sizeof(float) : 0;
-}
-
-hipError_t launch_dtin(const LifConst &C, int64_t B, int64_t N_in, int64_t N_out, const float *G,
-                       const void *W, bool bf16, const int *row, const float *dL, const float *dR,
-                       float *dt_in, float *part, hipStream_t st) {
-    const int R = C.M + 3;
-    const int sb = dtin_sb(C.M);
-    const int ns = dtin_nsplit(B, N_in, N_out, sb);
-    int64_t chunks = (N_out + kWave - 1) / kWave;
-    const int i_per = static_cast<int>(((chunks + ns - 1) / ns) * kWave);
-    const int threads = 256;
-    dim3 grid(static_cast<unsigned>((N_in + threads - 1) / threads),
-              static_cast<unsigned>((B + sb - 1) / sb), static_cast<unsigned>(ns));
-    size_t lds = static_cast<size_t>(sb) * (R + 1) * kDtStride * sizeof(float);
-    float *dst = ns > 1 ? part : dt_in;
-    {
-    ProfScope prof("dtin_dense", st);
-#define DTIN_LAUNCH(SBV, WT)                                                                      \
-    hipLaunchKernelGGL((dtin_dense_kernel<SBV, WT>), grid, dim3(threads), lds, st, C,            \
-                       static_cast<int>(B), static_cast<int>(N_in), static_cast<int>(N_out),     \
-                       i_per, G, static_cast<const WT *>(W), row, dL, dR, dst)
-    if (bf16) {
-        if (sb == 2) DTIN_LAUNCH(2, uint16_t);
-        else DTIN_LAUNCH(1, uint16_t);
+    if (ti == 64) {
+        if (nper == 9) DW_LAUNCH(64, 9);
+        else if (nper == 17) DW_LAUNCH(64, 17);
+        else DW_LAUNCH(64, 33);
     } else {
-        if (sb == 2) DTIN_LAUNCH(2, float);
-        else DTIN_LAUNCH(1, float);
+        if (nper == 9) DW_LAUNCH(32, 9);
+        else if (nper == 17) DW_LAUNCH(32, 17);
+        else DW_LAUNCH(32, 33);
     }
-#undef DTIN_LAUNCH
-    }
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess || ns == 1) return e;
-    int64_t n = B * N_in;
-    ProfScope prof("dtin_reduce", st);
-    hipLaunchKernelGGL(reduce_splits_kernel, dim3(static_cast<unsigned>((n + 255) / 256)), dim3(256),
-                       0, st, n, ns, part, dt_in);
+#undef DW_LAUNCH
     return hipGetLastError();
+}
+
+hipError_t launch_backward(const LifConst &C, int64_t B, int64_t N_in, int64_t N_out,
+                           const void *W, bool bf16, const float *t_in, const float *t_out,
+                           const float *slope, const int *q_idx, const float *grad_t,
+                           DenseBwdWs ws, float *grad_W, float *grad_t_in, hipStream_t st) {
+    const bool zero_dt = grad_t_in && B * N_in > 0;
+    const bool run_dt = zero_dt && N_out > 0;
+    const bool run_dw = grad_W && N_out * N_in > 0;
+    // sort (per-input events for dW; row-sorted records with derivatives and
+    // a zeroed dt_in when dt_in is wanted), transpose W, G: one launch
+    hipError_t e = launch_prep(C, B, N_in, N_out, t_in, ws.srt, ws.n_valid, true,
+                               SortOut{ws.row, ws.L, ws.R, zero_dt ? grad_t_in : nullptr}, W, bf16,
+                               ws.wt, run_dt, PrepGrad{t_out, slope, grad_t, q_idx, ws.G},
+                               B * N_out, "bwd_prep", st);
+    if (e != hipSuccess) return e;
+    DwPlan p = plan_dw(B, N_in, N_out, C.M);
+    const bool split = run_dw && p.nsplit > 1;
+    if (run_dw) {
+        e = launch_dw(C, p, B, N_in, N_out, ws.G, ws.row, ws.L, ws.R, split ? ws.part : grad_W, st);
+        if (e != hipSuccess) return e;
+    }
+    const RedJob red{split ? N_out * N_in : 0, p.nsplit, ws.part, grad_W};
+    if (run_dt) {
+        const int tiles = static_cast<int>((N_out + kWave - 1) / kWave);
+        const int tpw = (tiles + 3) / 4;  // tiles per wave
+        const int64_t red_rows = (red.n + kDtRanges * 256 - 1) / (kDtRanges * 256);
+        dim3 grid(kDtRanges, static_cast<unsigned>(B + red_rows));
+        ProfScope prof("dtin_rows", st);
+#define DTR(WTY, NTV)                                                                            \
+    hipLaunchKernelGGL((dtin_rows_kernel<WTY, NTV>), grid, dim3(256), 0, st, C,                 \
+                       static_cast<int>(B), static_cast<int>(N_in), static_cast<int>(N_out),     \
+                       static_cast<const WTY *>(ws.wt), ws.srt, ws.G, grad_t_in, red)
+#define DTR_NT(WTY)                                      \
+    do {                                                 \
+        if (tpw <= 1) DTR(WTY, 1);                       \
+        else if (tpw <= 2) DTR(WTY, 2);                  \
+        else DTR(WTY, 4);                                \
+    } while (0)
+        if (bf16) DTR_NT(uint16_t);
+        else DTR_NT(float);
+#undef DTR_NT
+#undef DTR
+        return hipGetLastError();
+    }
+    if (split) {
+        ProfScope prof("dw_reduce", st);
+        hipLaunchKernelGGL(reduce_splits_kernel, dim3(static_cast<unsigned>((red.n + 255) / 256)),
+                           dim3(256), 0, st, red.n, p.nsplit, ws.part, grad_W);
+        return hipGetLastError();
+    }
+    return hipSuccess;
 }
 
 hipError_t launch_softmax_ce(int64_t B, int64_t N, const float *t, const int *labels,

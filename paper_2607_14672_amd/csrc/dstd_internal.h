@@ -222,16 +222,11 @@ struct Scan {
     }
 };
 
-// LDS float add without return (ds_add_f32). Each address is owned by one
-// lane, so the order of additions is the program order: deterministic.
-__device__ __forceinline__ void lds_add(float *p, float v) {
-    __hip_atomic_fetch_add(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-}
-
 __device__ __forceinline__ int uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }
 
 // Raw buffer access: a per-lane byte offset plus a wave-uniform (scalar)
-// byte offset, with hardware range checking (reads past `bytes` return 0).
+// byte offset. Every caller keeps both offsets inside `bytes` (indices are
+// clamped); the descriptor's range check is only a backstop.
 constexpr int kBufWord3 = 0x00020000;  // gfx9 raw-buffer descriptor, word 3
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void *p, uint32_t bytes) {
     return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(p), static_cast<short>(0),
@@ -257,52 +252,5 @@ typedef __attribute__((address_space(4))) const int cint_t;
 typedef __attribute__((address_space(4))) const float cflt_t;
 __device__ __forceinline__ cint_t *as_const(const int *p) { return (cint_t *)p; }
 __device__ __forceinline__ cflt_t *as_const(const float *p) { return (cflt_t *)p; }
-
-// 16 consecutive weights of one row as fp32; `vec` selects 16-byte loads
-// (row start and N_in aligned). Rows past N_out read row 0 and return zeros.
-template <typename WT> struct W16;
-template <> struct W16<float> {
-    static __device__ __forceinline__ void load(const float *p, bool vec, bool ok, float *w) {
-        if (vec) {
-            const float4 *q = reinterpret_cast<const float4 *>(p);
-#pragma unroll
-            for (int k = 0; k < 4; ++k) {
-                float4 v = q[k];
-                w[4 * k] = v.x; w[4 * k + 1] = v.y; w[4 * k + 2] = v.z; w[4 * k + 3] = v.w;
-            }
-        } else {
-#pragma unroll
-            for (int k = 0; k < 16; ++k) w[k] = p[k];
-        }
-        if (!ok) {
-#pragma unroll
-            for (int k = 0; k < 16; ++k) w[k] = 0.f;
-        }
-    }
-};
-template <> struct W16<uint16_t> {
-    static __device__ __forceinline__ void load(const uint16_t *p, bool vec, bool ok, float *w) {
-        if (vec) {
-            const uint4 *q = reinterpret_cast<const uint4 *>(p);
-#pragma unroll
-            for (int k = 0; k < 2; ++k) {
-                uint4 v = q[k];
-                uint32_t u[4] = {v.x, v.y, v.z, v.w};
-#pragma unroll
-                for (int h = 0; h < 4; ++h) {
-                    w[8 * k + 2 * h] = __uint_as_float(u[h] << 16);
-                    w[8 * k + 2 * h + 1] = __uint_as_float(u[h] & 0xffff0000u);
-                }
-            }
-        } else {
-#pragma unroll
-            for (int k = 0; k < 16; ++k) w[k] = bf16_to_f32(p[k]);
-        }
-        if (!ok) {
-#pragma unroll
-            for (int k = 0; k < 16; ++k) w[k] = 0.f;
-        }
-    }
-};
 
 }  // namespace dstd

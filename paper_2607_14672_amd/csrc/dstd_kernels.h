@@ -16,23 +16,31 @@ struct DwPlan { int waves, jw, nsplit, b_per_split; };
 constexpr int kSortPad = 64;
 
 DwPlan plan_dw(int64_t B, int64_t N_in, int64_t N_out, int M);
-size_t dtin_partial_bytes(int M, int64_t B, int64_t N_in, int64_t N_out);
 
-hipError_t launch_bin_events(const LifConst &C, int64_t n, const float *t_in, int *row, float *L,
-                             float *R, float *dL, float *dR, hipStream_t st);
 hipError_t launch_forward(const LifConst &C, int64_t B, int64_t N_in, int64_t N_out, const void *W,
                           bool bf16, void *Wt, SortedEv srt, int *n_valid, const float *t_in,
                           float *t_out, float *slope, int *q_idx, hipStream_t st);
-// G[b, r, p, c] for neurons (c, p), N_out = n_pos * n_ch; dense: n_pos = 1
-hipError_t launch_grad_g(const LifConst &C, int64_t B, int64_t n_pos, int64_t n_ch,
-                         const float *t_out, const float *slope, const int *q_idx,
-                         const float *grad_t, float *G, hipStream_t st);
-hipError_t launch_dw(const LifConst &C, int64_t B, int64_t N_in, int64_t N_out, const float *G,
-                     const int *row, const float *L, const float *R, float *dW, float *part,
-                     hipStream_t st);
-hipError_t launch_dtin(const LifConst &C, int64_t B, int64_t N_in, int64_t N_out, const float *G,
-                       const void *W, bool bf16, const int *row, const float *dL, const float *dR,
-                       float *dt_in, float *part, hipStream_t st);
+
+// Dense backward workspace: per-input events (dW), the row-sorted records
+// with derivatives (dt_in), WT, G and the dW split partial sums.
+struct DenseBwdWs {
+    int *row;
+    float *L, *R;
+    SortedEv srt;
+    int *n_valid;
+    void *wt;
+    float *G;
+    float *part;
+};
+hipError_t launch_backward(const LifConst &C, int64_t B, int64_t N_in, int64_t N_out,
+                           const void *W, bool bf16, const float *t_in, const float *t_out,
+                           const float *slope, const int *q_idx, const float *grad_t,
+                           DenseBwdWs ws, float *grad_W, float *grad_t_in, hipStream_t st);
+hipError_t launch_softmax_ce(int64_t B, int64_t N, const float *t, const int *labels,
+                             float tau_soft, float t_cap, float *grad, float *loss, hipStream_t st);
+hipError_t launch_mse(int64_t B, int64_t N, const float *t, const float *y, float *grad,
+                      float *loss, hipStream_t st);
+
 // ------------------------------------------------------------------ conv --
 // Geometry of a conv layer, derived on the host. The (pooled) input map has
 // Hp x Wp cells of P raw pixels; PC = P * C_in raw inputs per cell.
@@ -83,10 +91,5 @@ hipError_t launch_conv_backward(const LifConst &C, const ConvGeom &g, int64_t B,
                                 bool bf16, const float *t_in, const float *t_out,
                                 const float *slope, const int *q_idx, const float *grad_t,
                                 ConvBwdWs ws, float *grad_W, float *grad_t_in, hipStream_t st);
-
-hipError_t launch_softmax_ce(int64_t B, int64_t N, const float *t, const int *labels,
-                             float tau_soft, float t_cap, float *grad, float *loss, hipStream_t st);
-hipError_t launch_mse(int64_t B, int64_t N, const float *t, const float *y, float *grad,
-                      float *loss, hipStream_t st);
 
 }  // namespace dstd

@@ -273,8 +273,9 @@ def kernel_algorithmic_flops(net, act):
 
 
 def traffic_for(kernel, workload, sha):
-    """HBM bytes per step of `kernel` from the committed rocprofv3 counter
-    summary, or None if none exists or the kernels changed since."""
+    """HBM bytes (FETCH + WRITE, copy-calibrated) per launch of `kernel` from
+    the committed rocprofv3 counter summary, or None if none exists or the
+    kernel sources changed since it was taken."""
     path = os.path.join(ROOT, "profiles", f"traffic_{kernel}_{workload}.json")
     if not os.path.exists(path):
         return None
@@ -282,7 +283,7 @@ def traffic_for(kernel, workload, sha):
         d = json.load(f)
     if d.get("kernel_source_sha") != sha:
         return None
-    return d.get("hbm_bytes_per_step")
+    return round(d["hbm_bytes_per_step"] / d["dispatches_per_step"])
 
 
 def cpu_baseline(wl, min_seconds=10.0):
@@ -411,12 +412,14 @@ def main():
     roof = None
     if dom in flops:
         achieved = flops[dom] / (per_step[dom] * 1e-3) / 1e12
+        n_launch = launches[dom]
         roof = dict(bound="alu", achieved=round(achieved, 3), peak=PEAK_FP32_VECTOR_TFLOPS,
                     unit="TFLOP/s", frac=round(achieved / PEAK_FP32_VECTOR_TFLOPS, 4),
-                    traffic=traffic_for(dom, args.workload, sha), kernel=dom,
-                    kernel_ms_per_step=round(per_step[dom], 4),
-                    avg_launch_ms=round(per_step[dom] / launches[dom], 4),
-                    algorithmic_flops_per_step=flops[dom])
+                    traffic=traffic_for(dom, args.workload, sha), traffic_unit="bytes per launch",
+                    kernel=dom, launches_per_step=n_launch,
+                    avg_launch_ms=round(per_step[dom] / n_launch, 4),
+                    algorithmic_flops_per_launch=round(flops[dom] / n_launch),
+                    kernel_ms_per_step=round(per_step[dom], 4))
 
     if args.copy_probe:
         a = torch.empty(64 << 20, dtype=torch.float32, device=dev)

@@ -112,7 +112,7 @@ dstd_status check_dims(int64_t B, int64_t N_in, int64_t N_out) {
 }
 
 struct DenseWs {
-    size_t row, L, R, G, part, wt, sj, sr, sL, sR, nvalid, rs, total;
+    size_t row, L, R, gam, uq, q, part, wt, sj, sr, sL, sR, nvalid, rs, total;
     int64_t sstride;
 };
 
@@ -135,11 +135,13 @@ DenseWs dense_ws_layout(int M, int64_t B, int64_t N_in, int64_t N_out, bool back
     w.nvalid = off; off += align_up((size_t)B * sizeof(int));
     w.rs = off; off += align_up((size_t)B * (M + 4) * sizeof(int));
     if (backward) {
-        // per-input events for the dW reduction, scan gradients G, dW partials
+        // per-input events for the dW reduction, gradient triples, dW partials
         w.row = off; off += align_up(n * sizeof(int));
         w.L = off; off += align_up(n * sizeof(float));
         w.R = off; off += align_up(n * sizeof(float));
-        w.G = off; off += align_up((size_t)B * (M + 3) * (size_t)N_out * sizeof(float));
+        w.gam = off; off += align_up((size_t)B * (size_t)N_out * sizeof(float));
+        w.uq = off; off += align_up((size_t)B * (size_t)N_out * sizeof(float));
+        w.q = off; off += align_up((size_t)B * (size_t)N_out * sizeof(int));
         dstd::DwPlan dp = dstd::plan_dw(B, N_in, N_out, M);
         w.part = off;
         if (dp.nsplit > 1) off += align_up((size_t)dp.nsplit * (size_t)N_out * (size_t)N_in * sizeof(float));
@@ -341,7 +343,9 @@ dstd_status dstd_lif_backward(const dstd_lif_params *p, int64_t B, int64_t N_in,
                             at<float>(ws, L.sR), L.sstride, at<int>(ws, L.rs)};
     bw.n_valid = at<int>(ws, L.nvalid);
     bw.wt = at<void>(ws, L.wt);
-    bw.G = at<float>(ws, L.G);
+    bw.gam = at<float>(ws, L.gam);
+    bw.uq = at<float>(ws, L.uq);
+    bw.q = at<int>(ws, L.q);
     bw.part = at<float>(ws, L.part);
     e = dstd::launch_backward(C, B, N_in, N_out, W, w_dtype == DSTD_BF16, t_in, t_out, slope,
                               q_idx, grad_t_out, bw, grad_W, grad_t_in, st);

@@ -51,13 +51,6 @@ __device__ __forceinline__ int64_t nchw_index(const ConvGeom &g, int b, int ci, 
     return ((static_cast<int64_t>(b) * g.C_in + ci) * g.H + y) * g.W + x;
 }
 
-// G[m] of one neuron: gamma K(t - T_m) for 0 <= m <= q, else 0, with
-// t - T_m = (t - T_q) + (q - m) dt (one rounding; all terms >= 0).
-__device__ __forceinline__ float g_at(const LifConst &C, float gam, float uq, int q, int m) {
-    if (m < 0 || m > q) return 0.f;
-    return gam * kern(C, fmaf(static_cast<float>(q - m), C.dt, uq));
-}
-
 // ------------------------------------------------------------ cell sort --
 // One block per cell row (b, py); wave w handles cells px = w, w + 4, ...
 // LDS: hist[r][px] (later the next free slot of bucket (r, px)), then the
@@ -378,8 +371,8 @@ __global__ __launch_bounds__(256) void conv_events_kernel(LifConst C, ConvGeom g
     if (dt_in) dt_in[src] = 0.f;
 }
 
-// Per output neuron (b, co, p) -> position-major [b][p][co]: gamma = -g/slope
-// (0 where no gradient flows), u = t - T_q (difference taken in fp64), q.
+// Per output neuron (b, co, p) -> position-major [b][p][co]: the gradient
+// triple (gamma, t - T_q, q) of grad_prep.
 __global__ __launch_bounds__(256) void conv_grad_prep_kernel(LifConst C, ConvGeom g, int64_t n,
                                                              const float *__restrict__ t_out,
                                                              const float *__restrict__ slope,
@@ -397,12 +390,14 @@ __global__ __launch_bounds__(256) void conv_grad_prep_kernel(LifConst C, ConvGeo
     const int64_t b = u / HoWo;
     const int64_t o = (b * g.C_out + co) * HoWo + p;
     const int q = q_idx[o];
-    const float gv = (q >= 0) ? grad_t[o] : 0.f;
-    const bool flow = q >= 0 && gv != 0.f;
-    const double T_q = fma(static_cast<double>(q), static_cast<double>(C.dt), static_cast<double>(C.t0));
-    gam[t] = flow ? -gv / fmaxf(slope[o], C.slope_floor) : 0.f;
-    uq[t] = flow ? static_cast<float>(fmax(static_cast<double>(t_out[o]) - T_q, 0.0)) : 0.f;
-    qv[t] = flow ? q : -1;
+    GradPrep gp{0.f, 0.f, -1};
+    if (q >= 0) {  // silent neurons: no further loads
+        const float g = grad_t[o];
+        if (g != 0.f) gp = grad_prep(C, t_out[o], slope[o], q, g);
+    }
+    gam[t] = gp.gam;
+    uq[t] = gp.uq;
+    qv[t] = gp.q;
 }
 
 // live[s] = 1 if any channel at sample s = (b, p) passes gradient.

@@ -135,50 +135,16 @@ __device__ void transpose_tile(int rows, int cols, const WT *__restrict__ in, WT
     }
 }
 
-// G[b, r, i] = dL/dw^[b, m = r-1, i] = -g K(t - T_m) / slope for m <= q,
-// 0 otherwise (and in the two end rows). K(t - T_m) follows the exact
-// backward recurrence K(s + dt) = alpha K(s) + K(dt) e^{-s/ti}, all terms
-// positive, so no per-element exponential and no cancellation; it runs in
-// fp64 so its rounding does not grow with the number of intervals.
-__device__ void grad_g_one(const LifConst &C, int64_t k, int N_out, const float *__restrict__ t_out,
-                           const float *__restrict__ slope, const int *__restrict__ q_idx,
-                           const float *__restrict__ grad_t, float *__restrict__ G) {
-    const int64_t b = k / N_out;
-    const int i = static_cast<int>(k % N_out);
-    const int R = rows_of(C);
-    float *g = G + b * R * N_out + i;
-    const int q = q_idx[k];
-    const float gv = (q >= 0) ? grad_t[k] : 0.f;
-    g[0] = 0.f;
-    g[static_cast<int64_t>(R - 1) * N_out] = 0.f;
-    if (q < 0 || gv == 0.f) {
-        for (int m = 0; m <= C.M; ++m) g[static_cast<int64_t>(m + 1) * N_out] = 0.f;
-        return;
-    }
-    const float gam = -gv / fmaxf(slope[k], C.slope_floor);
-    const double T_q = fma(static_cast<double>(q), static_cast<double>(C.dt), static_cast<double>(C.t0));
-    const float u = static_cast<float>(fmax(static_cast<double>(t_out[k]) - T_q, 0.0));
-    const float ev = expf(-u * C.inv_tv);
-    const float em = expm1f(-C.kappa * u);
-    double K = -C.c * ev * em;   // K(u)
-    double Q = ev * (1.f + em);  // e^{-u/ti}
-    for (int m = C.M; m > q; --m) g[static_cast<int64_t>(m + 1) * N_out] = 0.f;
-    for (int m = q; m >= 0; --m) {
-        g[static_cast<int64_t>(m + 1) * N_out] = static_cast<float>(gam * K);
-        K = fma(C.alpha_d, K, C.k_dt_d * Q);
-        Q *= C.beta_d;
-    }
-}
-
 // Independent setup work of a layer call in one launch, by block role:
 // blocks [0, n_sort) sort one sample each, the next n_tr blocks transpose one
-// weight tile each, the rest compute G for kPrepThreads neurons each
-// (backward only). One launch instead of three: every launch costs a few
-// microseconds even when its work is tiny.
+// weight tile each, the rest write the gradient triple (gamma, t - T_q, q)
+// of kPrepThreads neurons each (backward only). One launch instead of three:
+// every launch costs a few microseconds even when its work is tiny.
 struct PrepGrad {
     const float *t_out, *slope, *grad_t;
     const int *q_idx;
-    float *G;
+    float *gam, *uq;
+    int *q;
 };
 
 template <typename WT>
@@ -199,7 +165,17 @@ __global__ __launch_bounds__(kPrepThreads) void prep_kernel(LifConst C, int n_so
         transpose_tile<WT>(N_out, N_in, W, Wt, blk - n_sort, buf);
     } else {
         const int64_t k = static_cast<int64_t>(blk - n_sort - n_tr) * kPrepThreads + threadIdx.x;
-        if (k < n_grad) grad_g_one(C, k, N_out, pg.t_out, pg.slope, pg.q_idx, pg.grad_t, pg.G);
+        if (k < n_grad) {
+            const int q = pg.q_idx[k];
+            GradPrep gp{0.f, 0.f, -1};
+            if (q >= 0) {  // silent neurons: no further loads
+                const float g = pg.grad_t[k];
+                if (g != 0.f) gp = grad_prep(C, pg.t_out[k], pg.slope[k], q, g);
+            }
+            pg.gam[k] = gp.gam;
+            pg.uq[k] = gp.uq;
+            pg.q[k] = gp.q;
+        }
     }
 }
 
@@ -332,6 +308,7 @@ __global__ __launch_bounds__(256) void fwd_sorted_kernel(LifConst C, int B, int 
 // quarter of its dependent load chain; the sums are identical.
 constexpr int kRowWaves = 4;
 constexpr int kRowsMaxM = 64;
+constexpr int kRowChunk = 32;  // records per vector load; the lookahead stays within kSortPad
 
 template <typename WT>
 __global__ __launch_bounds__(kRowWaves * 64) void fwd_rows_kernel(LifConst C, int N_in, int N_out,
@@ -389,37 +366,42 @@ __global__ __launch_bounds__(kRowWaves * 64) void fwd_rows_kernel(LifConst C, in
     const int rstride = N_out * static_cast<int>(sizeof(WT));
     const unsigned jmax = static_cast<unsigned>(max(N_in - 1, 0));
     auto wrow = [&](int j) { return static_cast<int>(min(static_cast<unsigned>(j), jmax)) * rstride; };
-    float w[kBatch], wn[kBatch];
+    // Records come kRowChunk at a time, one per lane, with vector loads (the
+    // next chunk's in flight while this one is summed); each record's
+    // fields are broadcast with readlane. All of a chunk's weight loads are
+    // issued before the first one is consumed.
+    auto rdl = [](float v, int k) { return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), k)); };
+    int jn = ej[k_lo + lane], rn = er[k_lo + lane];
+    float Ln = eL[k_lo + lane], Rn = eR[k_lo + lane];
+    for (int c0 = k_lo; c0 < k_hi; c0 += kRowChunk) {
+        const int jc = jn, rc = rn;
+        const float Lc = Ln, Rc = Rn;
+        // the next chunk (reads past the sample's list stay inside the padded arrays)
+        jn = ej[c0 + kRowChunk + lane];
+        rn = er[c0 + kRowChunk + lane];
+        Ln = eL[c0 + kRowChunk + lane];
+        Rn = eR[c0 + kRowChunk + lane];
+        const int nc = min(kRowChunk, k_hi - c0);
+        float w[kRowChunk];
 #pragma unroll
-    for (int kk = 0; kk < kBatch; ++kk) wn[kk] = BufLoad<WT>::get(wr, voff, wrow(as_const(ej + k_lo)[kk]));
-    for (int k0 = k_lo; k0 < k_hi; k0 += kBatch) {
-        int rr[kBatch], jj1[kBatch];
-        float ll[kBatch], rv[kBatch];
+        for (int kk = 0; kk < kRowChunk; ++kk)
+            w[kk] = BufLoad<WT>::get(wr, voff, wrow(__builtin_amdgcn_readlane(jc, kk)));
+        if (nc == kRowChunk && __builtin_amdgcn_readlane(rc, kRowChunk - 1) == cur) {
+            // common case: a full chunk that continues the current row
 #pragma unroll
-        for (int kk = 0; kk < kBatch; ++kk) {
-            w[kk] = wn[kk];
-            rr[kk] = as_const(er + k0)[kk];
-            ll[kk] = as_const(eL + k0)[kk];
-            rv[kk] = as_const(eR + k0)[kk];
-            jj1[kk] = as_const(ej + k0 + kBatch)[kk];
-        }
-#pragma unroll
-        for (int kk = 0; kk < kBatch; ++kk) wn[kk] = BufLoad<WT>::get(wr, voff, wrow(jj1[kk]));
-        const int nk = min(kBatch, k_hi - k0);
-        if (nk == kBatch && rr[kBatch - 1] == cur) {
-#pragma unroll
-            for (int kk = 0; kk < kBatch; ++kk) {
-                aL = fmaf(w[kk], ll[kk], aL);
-                aR = fmaf(w[kk], rv[kk], aR);
+            for (int kk = 0; kk < kRowChunk; ++kk) {
+                aL = fmaf(w[kk], rdl(Lc, kk), aL);
+                aR = fmaf(w[kk], rdl(Rc, kk), aR);
             }
             continue;
         }
 #pragma unroll
-        for (int kk = 0; kk < kBatch; ++kk) {
-            if (kk < nk) {
-                if (rr[kk] != cur) close_to(rr[kk]);
-                aL = fmaf(w[kk], ll[kk], aL);
-                aR = fmaf(w[kk], rv[kk], aR);
+        for (int kk = 0; kk < kRowChunk; ++kk) {
+            if (kk < nc) {
+                const int r = __builtin_amdgcn_readlane(rc, kk);
+                if (r != cur) close_to(r);
+                aL = fmaf(w[kk], rdl(Lc, kk), aL);
+                aR = fmaf(w[kk], rdl(Rc, kk), aR);
             }
         }
     }
@@ -428,8 +410,11 @@ __global__ __launch_bounds__(kRowWaves * 64) void fwd_rows_kernel(LifConst C, in
     if (wave != 0) return;
     // grid point m: L sums of row m+1 plus R sums of row m
     Scan sc;
+    float wn = AL[kWave + lane] + AR[lane];  // next grid point's sum, read ahead
     for (int m = 0; m <= C.M; ++m) {
-        sc.step(C, m, AL[(m + 1) * kWave + lane] + AR[m * kWave + lane]);
+        const float wc = wn;
+        if (m < C.M) wn = AL[(m + 2) * kWave + lane] + AR[(m + 1) * kWave + lane];
+        sc.step(C, m, wc);
         if (__all(sc.found() || !row_ok)) break;
     }
     if (!row_ok) return;
@@ -446,14 +431,20 @@ __global__ __launch_bounds__(kRowWaves * 64) void fwd_rows_kernel(LifConst C, in
 // dW[i, j] = sum_b (G[b, r_bj, i] L_bj + G[b, r_bj + 1, i] R_bj).
 // Lane = input j (events are coalesced vector loads); a block covers
 // 4 x 64 inputs and a tile of TI neurons whose sums stay in registers over
-// its share of the batch. G[b, :, tile] is staged in LDS (double buffered)
-// as pairs (G[r], G[r+1]) per neuron, so one 8-byte read with an immediate
-// neuron offset serves both halves of an event. Slot R-1 is a zero pair for
-// inputs without events. Batch splits write partial sums, reduced in order.
+// its share of the batch. G[b, :, tile] is computed in place from the
+// gradient triples (each thread owns one neuron and a fixed set of rows, so
+// neurons without gradient cost no exponential) and staged in LDS (double
+// buffered) as pairs (G[r], G[r+1]) per neuron, so one 8-byte read with an
+// immediate neuron offset serves both halves of an event; the next sample's
+// values are computed while this one is consumed. Slot R-1 is a zero pair
+// for inputs without events; a sample whose tile is all zero is skipped.
+// Batch splits write partial sums, reduced in order.
 template <int TI, int NPER>
 __global__ __launch_bounds__(256) void dw_dense_kernel(LifConst C, int B, int N_in, int N_out,
                                                         int b_per_split, int pstride,
-                                                        const float *__restrict__ G,
+                                                        const float *__restrict__ gam,
+                                                        const float *__restrict__ uq,
+                                                        const int *__restrict__ qv,
                                                         const int *__restrict__ ev_row,
                                                         const float *__restrict__ ev_L,
                                                         const float *__restrict__ ev_R,
@@ -469,20 +460,24 @@ __global__ __launch_bounds__(256) void dw_dense_kernel(LifConst C, int B, int N_
     float acc[TI];
 #pragma unroll
     for (int ii = 0; ii < TI; ++ii) acc[ii] = 0.f;
-    // Staging of G[b, :, tile] into LDS pairs in two steps, so the next
-    // sample's global loads (NPER registers per thread, unconditional with
-    // indices clamped into range) overlap this sample's compute. Neurons past
-    // the tile end hold copies of its last neuron; their sums are not stored.
     const int total = R * TI;
+    // element c of this thread: row r = r_first + c * (256 / TI), neuron l
+    const int l_own = threadIdx.x % TI, r_first = threadIdx.x / TI;
+    constexpr int kRowStep = 256 / TI;
     float pre[NPER];
     auto fetch = [&](int b) {
-        const float *gb = G + static_cast<int64_t>(b) * R * N_out + i0;
+        const int64_t k = static_cast<int64_t>(b) * N_out + i0 + min(l_own, ni - 1);
+        const bool own = l_own < ni;
+        const float gm = own ? gam[k] : 0.f;
+        const float u = own ? uq[k] : 0.f;
+        const int q = own ? qv[k] : -1;
+        bool nz = false;
 #pragma unroll
         for (int c = 0; c < NPER; ++c) {
-            const int k = threadIdx.x + c * 256;
-            const int r = min(k / TI, R - 1), l = min(k % TI, ni - 1);
-            pre[c] = gb[static_cast<int64_t>(r) * N_out + l];
+            pre[c] = g_at(C, gm, u, q, r_first + c * kRowStep - 1);
+            nz = nz || pre[c] != 0.f;
         }
+        return nz;
     };
     auto store = [&](float2 *buf) {
 #pragma unroll
@@ -497,34 +492,38 @@ __global__ __launch_bounds__(256) void dw_dense_kernel(LifConst C, int B, int N_
         }
         for (int l = threadIdx.x; l < TI; l += blockDim.x) buf[l * pstride + R - 1] = make_float2(0.f, 0.f);
     };
+    bool live = false;
     if (b_lo < b_hi) {
-        fetch(b_lo);
+        live = fetch(b_lo);
         store(ps);
     }
-    __syncthreads();
+    live = __syncthreads_or(live);
     for (int b = b_lo; b < b_hi; ++b) {
         float2 *cur = ps + ((b - b_lo) & 1) * TI * pstride;
         const bool more = b + 1 < b_hi;
-        if (more) fetch(b + 1);
-        int slot = R - 1;
-        float L = 0.f, Rv = 0.f;
-        if (j_ok) {
-            const int64_t o = static_cast<int64_t>(b) * N_in + j;
-            const int r = ev_row[o];
-            if (r >= 0) {
-                slot = r;
-                L = ev_L[o];
-                Rv = ev_R[o];
+        bool live_next = false;
+        if (more) live_next = fetch(b + 1);
+        if (live) {
+            int slot = R - 1;
+            float L = 0.f, Rv = 0.f;
+            if (j_ok) {
+                const int64_t o = static_cast<int64_t>(b) * N_in + j;
+                const int r = ev_row[o];
+                if (r >= 0) {
+                    slot = r;
+                    L = ev_L[o];
+                    Rv = ev_R[o];
+                }
+            }
+            const float2 *p = cur + slot;
+#pragma unroll
+            for (int ii = 0; ii < TI; ++ii) {
+                const float2 g = p[ii * pstride];
+                acc[ii] = fmaf(g.x, L, fmaf(g.y, Rv, acc[ii]));
             }
         }
-        const float2 *p = cur + slot;
-#pragma unroll
-        for (int ii = 0; ii < TI; ++ii) {
-            const float2 g = p[ii * pstride];
-            acc[ii] = fmaf(g.x, L, fmaf(g.y, Rv, acc[ii]));
-        }
         if (more) store(ps + ((b + 1 - b_lo) & 1) * TI * pstride);
-        __syncthreads();
+        live = __syncthreads_or(live_next);
     }
     if (!j_ok) return;
     float *out = dW_part + static_cast<int64_t>(blockIdx.z) * N_out * N_in +
@@ -546,7 +545,9 @@ __global__ __launch_bounds__(256) void reduce_splits_kernel(int64_t n, int nspli
 
 // -------------------------------------------------------- dt_in (rows) --
 // dt_in of every input with events, from its sample's row-sorted records
-// {j, row r, dL, dR}: dL sum_i W[i, j] G[b, r, i] + dR sum_i W[i, j] G[b, r+1, i].
+// {j, row r, dL, dR}: dL sum_i W[i, j] G[b, m = r-1, i] + dR sum_i W[i, j] G[b, m = r, i],
+// G evaluated in place from the gradient triples (once per event row for the
+// first 4 * NTW tiles of neurons).
 // A block takes a contiguous range of whole event rows of one sample
 // (kDtRanges ranges per sample, about equal in records); its four waves walk
 // the same records, each over its own NTW 64-neuron tiles per group of
@@ -563,7 +564,9 @@ struct RedJob { int64_t n; int nsplit; const float *part; float *out; };
 template <typename WT, int NTW>
 __global__ __launch_bounds__(256) void dtin_rows_kernel(LifConst C, int B, int N_in, int N_out,
                                                         const WT *__restrict__ Wt, SortedEv srt,
-                                                        const float *__restrict__ G,
+                                                        const float *__restrict__ gam,
+                                                        const float *__restrict__ uq,
+                                                        const int *__restrict__ qv,
                                                         float *__restrict__ dt_in, RedJob red) {
     __shared__ float part[4][kBatch];
     if (static_cast<int>(blockIdx.y) >= B) {
@@ -601,15 +604,36 @@ __global__ __launch_bounds__(256) void dtin_rows_kernel(LifConst C, int B, int N
     const int *ej = srt.j + eo;
     const float *edl = srt.L + eo;
     const float *edr = srt.R + eo;
-    const float *Gb = G + static_cast<int64_t>(b) * R * N_out;
+    const int64_t nb = static_cast<int64_t>(b) * N_out;
     const __amdgpu_buffer_rsrc_t wr =
         make_rsrc(Wt, static_cast<uint32_t>(static_cast<int64_t>(N_in) * N_out * sizeof(WT)));
     const int rstride = N_out * static_cast<int>(sizeof(WT));
     const unsigned jmax = static_cast<unsigned>(max(N_in - 1, 0));
     constexpr int kGroup = 4 * NTW * kWave;
     const int ngroups = (N_out + kGroup - 1) / kGroup;
+    // this lane's neurons of group 0 (the only group when N_out <= kGroup)
+    float gm0[NTW], ua0[NTW];
+    int qa0[NTW], voff0[NTW];
+#pragma unroll
+    for (int t = 0; t < NTW; ++t) {
+        const int i = (wave * NTW + t) * kWave + lane;
+        const int ic = min(i, N_out - 1);
+        const bool ok = i < N_out;
+        gm0[t] = ok ? gam[nb + ic] : 0.f;
+        ua0[t] = ok ? uq[nb + ic] : 0.f;
+        qa0[t] = ok ? qv[nb + ic] : -1;
+        voff0[t] = ic * static_cast<int>(sizeof(WT));
+    }
     for (int r = r_lo; r < r_hi; ++r) {
         const int s = *as_const(rs + r), e = *as_const(rs + r + 1);
+        if (s == e) continue;
+        // G at grid points r - 1 (L halves) and r (R halves), group 0
+        float h0[NTW], h1[NTW];
+#pragma unroll
+        for (int t = 0; t < NTW; ++t) {
+            h0[t] = g_at(C, gm0[t], ua0[t], qa0[t], r - 1);
+            h1[t] = g_at(C, gm0[t], ua0[t], qa0[t], r);
+        }
         for (int k0 = s; k0 < e; k0 += kBatch) {
             const int nk = min(kBatch, e - k0);
             int jo[kBatch];
@@ -626,12 +650,21 @@ __global__ __launch_bounds__(256) void dtin_rows_kernel(LifConst C, int B, int N
                 int voff[NTW];
 #pragma unroll
                 for (int t = 0; t < NTW; ++t) {
-                    const int i = grp * kGroup + (wave * NTW + t) * kWave + lane;
-                    const int ic = min(i, N_out - 1);
-                    const bool ok = i < N_out;
-                    g0[t] = ok ? Gb[static_cast<int64_t>(r) * N_out + ic] : 0.f;
-                    g1[t] = ok ? Gb[static_cast<int64_t>(r + 1) * N_out + ic] : 0.f;
-                    voff[t] = ic * static_cast<int>(sizeof(WT));
+                    if (grp == 0) {
+                        g0[t] = h0[t];
+                        g1[t] = h1[t];
+                        voff[t] = voff0[t];
+                    } else {
+                        const int i = grp * kGroup + (wave * NTW + t) * kWave + lane;
+                        const int ic = min(i, N_out - 1);
+                        const bool ok = i < N_out;
+                        const float gm = ok ? gam[nb + ic] : 0.f;
+                        const float u = ok ? uq[nb + ic] : 0.f;
+                        const int q = ok ? qv[nb + ic] : -1;
+                        g0[t] = g_at(C, gm, u, q, r - 1);
+                        g1[t] = g_at(C, gm, u, q, r);
+                        voff[t] = ic * static_cast<int>(sizeof(WT));
+                    }
                 }
 #pragma unroll
                 for (int kk = 0; kk < kBatch; ++kk)
@@ -794,7 +827,7 @@ hipError_t launch_forward(const LifConst &C, int64_t B, int64_t N_in, int64_t N_
     const int R = C.M + 3;
     hipError_t e = launch_prep(C, B, N_in, N_out, t_in, srt, n_valid, false,
                                SortOut{nullptr, nullptr, nullptr, nullptr}, W, bf16, Wt, true,
-                               PrepGrad{nullptr, nullptr, nullptr, nullptr, nullptr}, 0,
+                               PrepGrad{nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr}, 0,
                                "sort_transpose", st);
     if (e != hipSuccess) return e;
     ProfScope prof("fwd_dense", st);
@@ -853,8 +886,7 @@ DwPlan plan_dw(int64_t B, int64_t N_in, int64_t N_out, int M) {
 }
 
 static hipError_t launch_dw(const LifConst &C, const DwPlan &p, int64_t B, int64_t N_in,
-                            int64_t N_out, const float *G, const int *row, const float *L,
-                            const float *R, float *dst, hipStream_t st) {
+                            int64_t N_out, const DenseBwdWs &ws, float *dst, hipStream_t st) {
     const int ti = p.jw;
     const int pstride = (C.M + 3) | 1;
     dim3 grid(static_cast<unsigned>((N_in + 255) / 256),
@@ -864,8 +896,8 @@ static hipError_t launch_dw(const LifConst &C, const DwPlan &p, int64_t B, int64
     const int nper = dw_nper(C.M, ti);
 #define DW_LAUNCH(TIV, NP)                                                                        \
     hipLaunchKernelGGL((dw_dense_kernel<TIV, NP>), grid, dim3(256), lds, st, C, static_cast<int>(B), \
-                       static_cast<int>(N_in), static_cast<int>(N_out), p.b_per_split, pstride, G, \
-                       row, L, R, dst)
+                       static_cast<int>(N_in), static_cast<int>(N_out), p.b_per_split, pstride,    \
+                       ws.gam, ws.uq, ws.q, ws.row, ws.L, ws.R, dst)
     if (ti == 64) {
         if (nper == 9) DW_LAUNCH(64, 9);
         else if (nper == 17) DW_LAUNCH(64, 17);
@@ -887,16 +919,17 @@ hipError_t launch_backward(const LifConst &C, int64_t B, int64_t N_in, int64_t N
     const bool run_dt = zero_dt && N_out > 0;
     const bool run_dw = grad_W && N_out * N_in > 0;
     // sort (per-input events for dW; row-sorted records with derivatives and
-    // a zeroed dt_in when dt_in is wanted), transpose W, G: one launch
+    // a zeroed dt_in when dt_in is wanted), transpose W, gradient triples:
+    // one launch
     hipError_t e = launch_prep(C, B, N_in, N_out, t_in, ws.srt, ws.n_valid, true,
                                SortOut{ws.row, ws.L, ws.R, zero_dt ? grad_t_in : nullptr}, W, bf16,
-                               ws.wt, run_dt, PrepGrad{t_out, slope, grad_t, q_idx, ws.G},
+                               ws.wt, run_dt, PrepGrad{t_out, slope, grad_t, q_idx, ws.gam, ws.uq, ws.q},
                                B * N_out, "bwd_prep", st);
     if (e != hipSuccess) return e;
     DwPlan p = plan_dw(B, N_in, N_out, C.M);
     const bool split = run_dw && p.nsplit > 1;
     if (run_dw) {
-        e = launch_dw(C, p, B, N_in, N_out, ws.G, ws.row, ws.L, ws.R, split ? ws.part : grad_W, st);
+        e = launch_dw(C, p, B, N_in, N_out, ws, split ? ws.part : grad_W, st);
         if (e != hipSuccess) return e;
     }
     const RedJob red{split ? N_out * N_in : 0, p.nsplit, ws.part, grad_W};
@@ -909,7 +942,7 @@ hipError_t launch_backward(const LifConst &C, int64_t B, int64_t N_in, int64_t N
 #define DTR(WTY, NTV)                                                                            \
     hipLaunchKernelGGL((dtin_rows_kernel<WTY, NTV>), grid, dim3(256), 0, st, C,                 \
                        static_cast<int>(B), static_cast<int>(N_in), static_cast<int>(N_out),     \
-                       static_cast<const WTY *>(ws.wt), ws.srt, ws.G, grad_t_in, red)
+                       static_cast<const WTY *>(ws.wt), ws.srt, ws.gam, ws.uq, ws.q, grad_t_in, red)
 #define DTR_NT(WTY)                                      \
     do {                                                 \
         if (tpw <= 1) DTR(WTY, 1);                       \

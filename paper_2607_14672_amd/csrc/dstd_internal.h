@@ -122,21 +122,25 @@ __device__ __forceinline__ void seg_eval(const LifConst &C, const Seg &s, float 
     fp = fmaf(-s.V * C.inv_tv, ev, s.I * Kp);
 }
 
-// First root of v(u) = theta on [0, hi] given f(0) < 0 <= f(hi): safeguarded
-// Newton started at the left end, keeping the bracket; on the rising piece
-// of v the function is concave in the common cases, where Newton from the
-// left is monotone.
-__device__ __forceinline__ float seg_root(const LifConst &C, const Seg &s, float hi, float &slope) {
-    float lo = 0.f, u = 0.f;
+// First root of v(u) = theta on [0, hi] given f(0) < 0 <= f(hi) = fhi (the
+// only root there: v has at most one extremum per interval, and [0, hi]
+// either ends at it or past the crossing). Safeguarded Newton started at the
+// regula-falsi point of the bracket, keeping the bracket.
+__device__ __forceinline__ float seg_root(const LifConst &C, const Seg &s, float hi, float fhi,
+                                          float &slope) {
+    const float f0 = s.V - C.theta;  // f(0) < 0
+    float lo = 0.f;
+    float u = (fhi > f0) ? hi * (-f0 / (fhi - f0)) : 0.5f * hi;
+    if (!(u > 0.f && u < hi)) u = 0.5f * hi;
     float f, fp;
     seg_eval(C, s, u, f, fp);
     for (int it = 0; it < 48; ++it) {
+        if (f < 0.f) lo = u; else hi = u;
         float un = (fp > 0.f) ? u - f / fp : 0.5f * (lo + hi);
         if (!(un > lo && un < hi)) un = 0.5f * (lo + hi);
-        float step = un - u;
+        const float step = un - u;
         u = un;
         seg_eval(C, s, u, f, fp);
-        if (f < 0.f) lo = u; else hi = u;
         // Newton converges quadratically: once a step is below 1e-6 of u the
         // next one is below an fp32 ulp. The bracket test catches bisection.
         const float tol = 1e-6f * fmaxf(u, 1e-6f * C.dt);
@@ -144,6 +148,32 @@ __device__ __forceinline__ float seg_root(const LifConst &C, const Seg &s, float
     }
     slope = fp;
     return u;
+}
+
+// Scan gradient of one neuron, G[m] = dL/dw^_m = gamma K(t - T_m) for
+// 0 <= m <= q (implicit-function theorem on v^(t) = theta), from the
+// per-neuron triple gamma = -g / slope (slope floored at 1e-12 theta),
+// u = t - T_q (difference taken in fp64) and q; q = -1 where no gradient
+// flows (silent neuron or g = 0).
+struct GradPrep { float gam, uq; int q; };
+
+__device__ __forceinline__ GradPrep grad_prep(const LifConst &C, float t, float slope, int q,
+                                              float g) {
+    GradPrep r{0.f, 0.f, -1};
+    if (q < 0 || g == 0.f) return r;
+    const double T_q = fma(static_cast<double>(q), static_cast<double>(C.dt), static_cast<double>(C.t0));
+    r.gam = -g / fmaxf(slope, C.slope_floor);
+    r.uq = static_cast<float>(fmax(static_cast<double>(t) - T_q, 0.0));
+    r.q = q;
+    return r;
+}
+
+// G[m] from the triple: t - T_m = (t - T_q) + (q - m) dt is formed with one
+// rounding from non-negative terms, and K(u) keeps full relative precision
+// (expm1 form), so no per-neuron recurrence over the grid is needed.
+__device__ __forceinline__ float g_at(const LifConst &C, float gam, float uq, int q, int m) {
+    if (m < 0 || m > q) return 0.f;
+    return gam * kern(C, fmaf(static_cast<float>(q - m), C.dt, uq));
 }
 
 // Interval scan of one neuron (Table "tab:timing_DSTD", Eq. (timing_DSTD)):
@@ -157,7 +187,7 @@ struct Scan {
     double Vd = 0.0, Id = 0.0;
     int qf = -1;
     Seg sf{0.f, 0.f};
-    float hi = 0.f;
+    float hi = 0.f, fhi = 0.f;  // bracket end of the crossing and v - theta there
 
     __device__ __forceinline__ void step(const LifConst &C, int q, float w) {
         Id += static_cast<double>(w);
@@ -182,16 +212,19 @@ struct Scan {
                 if (s.V >= C.theta) {  // only through rounding: v is continuous
                     qf = q; sf = s; hi = 0.f;
                 } else if (vend >= C.theta) {
-                    qf = q; sf = s; hi = len;
+                    qf = q; sf = s; hi = len; fhi = vend - C.theta;
                 } else if (s.I > 0.f) {
                     // interior maximum: v'(u*) = 0 with e^{-kappa u*} = (ti/tv)(1 + V/(c I))
                     const float r = (C.ti * C.inv_tv) * (1.f + s.V / (C.c * s.I));
                     const float r_lo = last ? C.r_lo_last : C.r_lo_dt;
-                    if (r > r_lo && r < 1.f) {
+                    // v(u*) = e^{-u*/tv} (V + c I (1 - r)) <= V + c I (1 - r): the
+                    // maximum is evaluated only if this bound reaches theta
+                    if (r > r_lo && r < 1.f &&
+                        fmaf(s.I * C.c, 1.f - r, s.V) * 1.0001f >= C.theta) {
                         const float us = -logf(r) / C.kappa;
                         float f, fp;
                         seg_eval(C, s, us, f, fp);
-                        if (f >= 0.f) { qf = q; sf = s; hi = us; }
+                        if (f >= 0.f) { qf = q; sf = s; hi = us; fhi = f; }
                     }
                 }
             }
@@ -210,7 +243,7 @@ struct Scan {
         if (qf < 0) return;
         float u, sl;
         if (hi > 0.f) {
-            u = seg_root(C, sf, hi, sl);
+            u = seg_root(C, sf, hi, fhi, sl);
         } else {
             float f;
             u = 0.f;

@@ -13,7 +13,7 @@ struct DwPlan { int waves, jw, nsplit, b_per_split; };
 
 // records past the end of a sample's sorted list that the forward kernel may
 // read (and mask): the list array is padded by this many records
-constexpr int kSortPad = 64;
+constexpr int kSortPad = 128;
 
 DwPlan plan_dw(int64_t B, int64_t N_in, int64_t N_out, int M);
 
@@ -22,14 +22,16 @@ hipError_t launch_forward(const LifConst &C, int64_t B, int64_t N_in, int64_t N_
                           float *t_out, float *slope, int *q_idx, hipStream_t st);
 
 // Dense backward workspace: per-input events (dW), the row-sorted records
-// with derivatives (dt_in), WT, G and the dW split partial sums.
+// with derivatives (dt_in), WT, the per-neuron gradient triples and the dW
+// split partial sums.
 struct DenseBwdWs {
     int *row;
     float *L, *R;
     SortedEv srt;
     int *n_valid;
     void *wt;
-    float *G;
+    float *gam, *uq;
+    int *q;
     float *part;
 };
 hipError_t launch_backward(const LifConst &C, int64_t B, int64_t N_in, int64_t N_out,

@@ -572,6 +572,7 @@ __global__ __launch_bounds__(256) void conv_dw_kernel(LifConst C, ConvGeom g, in
     // element c of this thread: row r = r_first + c * (256 / TI), channel l
     const int l_own = threadIdx.x % TI, r_first = threadIdx.x / TI;
     constexpr int kRowStep = 256 / TI;
+    const GStep gst = g_step(C, kRowStep);
     float pre[NPER];
     // G[b, :, p, tile] of sample s; returns whether any value is nonzero
     auto fetch = [&](int64_t s) {
@@ -580,12 +581,10 @@ __global__ __launch_bounds__(256) void conv_dw_kernel(LifConst C, ConvGeom g, in
         const float gm = own ? gam[nb] : 0.f;
         const float u = own ? uq[nb] : 0.f;
         const int q = own ? qv[nb] : -1;
+        g_strided<NPER>(C, gst, gm, u, q, r_first - 1, kRowStep, pre);
         bool nz = false;
 #pragma unroll
-        for (int c = 0; c < NPER; ++c) {
-            pre[c] = g_at(C, gm, u, q, r_first + c * kRowStep - 1);
-            nz = nz || pre[c] != 0.f;
-        }
+        for (int c = 0; c < NPER; ++c) nz = nz || pre[c] != 0.f;
         return nz;
     };
     auto store = [&](float2 *buf) {

@@ -464,6 +464,7 @@ __global__ __launch_bounds__(256) void dw_dense_kernel(LifConst C, int B, int N_
     // element c of this thread: row r = r_first + c * (256 / TI), neuron l
     const int l_own = threadIdx.x % TI, r_first = threadIdx.x / TI;
     constexpr int kRowStep = 256 / TI;
+    const GStep gst = g_step(C, kRowStep);
     float pre[NPER];
     auto fetch = [&](int b) {
         const int64_t k = static_cast<int64_t>(b) * N_out + i0 + min(l_own, ni - 1);
@@ -471,12 +472,10 @@ __global__ __launch_bounds__(256) void dw_dense_kernel(LifConst C, int B, int N_
         const float gm = own ? gam[k] : 0.f;
         const float u = own ? uq[k] : 0.f;
         const int q = own ? qv[k] : -1;
+        g_strided<NPER>(C, gst, gm, u, q, r_first - 1, kRowStep, pre);
         bool nz = false;
 #pragma unroll
-        for (int c = 0; c < NPER; ++c) {
-            pre[c] = g_at(C, gm, u, q, r_first + c * kRowStep - 1);
-            nz = nz || pre[c] != 0.f;
-        }
+        for (int c = 0; c < NPER; ++c) nz = nz || pre[c] != 0.f;
         return nz;
     };
     auto store = [&](float2 *buf) {

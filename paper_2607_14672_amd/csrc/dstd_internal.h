@@ -176,6 +176,38 @@ __device__ __forceinline__ float g_at(const LifConst &C, float gam, float uq, in
     return gam * kern(C, fmaf(static_cast<float>(q - m), C.dt, uq));
 }
 
+// G of one neuron at the grid points m_c = m0 + c * step, c = 0..N-1 (rows of
+// a strided staging pattern; entries outside 0 <= m_c <= q are 0). The
+// largest m_c <= q is evaluated directly; the smaller ones follow from the
+// recurrence K(u + s) = a_s K(u) + K(s) e^{-u/ti}, e^{-(u+s)/ti} =
+// b_s e^{-u/ti} (s = step * dt), whose terms are all positive.
+struct GStep { float a, b, k; };  // e^{-s/tv}, e^{-s/ti}, K(s)
+
+__device__ __forceinline__ GStep g_step(const LifConst &C, int step) {
+    const float s = static_cast<float>(step) * C.dt;
+    return GStep{expf(-s * C.inv_tv), expf(-s * C.inv_ti), kern(C, s)};
+}
+
+template <int N>
+__device__ __forceinline__ void g_strided(const LifConst &C, const GStep &gs, float gam, float uq,
+                                          int q, int m0, int step, float *out) {
+    // highest c with m_c <= q (-1: none)
+    const int c_top = (q < m0) ? -1 : min(N - 1, (q - m0) / step);
+    const float u_top = fmaf(static_cast<float>(q - (m0 + max(c_top, 0) * step)), C.dt, uq);
+    const float ev = expf(-u_top * C.inv_tv);
+    const float em = expm1f(-C.kappa * u_top);
+    float K = -C.c * ev * em;  // K(u_top)
+    float E = ev * (1.f + em);  // e^{-u_top/ti}
+#pragma unroll
+    for (int c = N - 1; c >= 0; --c) {
+        if (c < c_top) {
+            K = fmaf(gs.a, K, gs.k * E);
+            E *= gs.b;
+        }
+        out[c] = (c <= c_top && m0 + c * step >= 0) ? gam * K : 0.f;
+    }
+}
+
 // Interval scan of one neuron (Table "tab:timing_DSTD", Eq. (timing_DSTD)):
 // weighted events arrive in grid order through step(); the earliest interval
 // whose candidate lies inside it is kept. The state (v at T_q, current after

@@ -300,32 +300,32 @@ __global__ __launch_bounds__(256) void fwd_sorted_kernel(LifConst C, int B, int 
 }
 
 // Row-parallel forward (M <= kRowsMaxM). A block of kRowWaves wavefronts
-// serves one (sample, 64-neuron tile): wave w sums the records of a
-// contiguous range of whole event rows (ranges split the sample's records
-// about evenly), in the same per-row order as the single-wave walk above, and
-// writes each row's L and R sums to LDS; wave 0 then runs the interval scan
-// over the rows. Four times the waves of the single-wave walk, each with a
-// quarter of its dependent load chain; the sums are identical.
+// serves one sample and NT 64-neuron tiles: wave w sums, for all NT tiles,
+// the records of a contiguous range of whole event rows (ranges split the
+// sample's records about evenly), in the same per-row order as the
+// single-wave walk above, and writes each row's L and R sums to LDS; then
+// wave t runs the interval scan of tile t (NT == kRowWaves) or wave 0 scans
+// the single tile (NT == 1). The sums and their order are those of the
+// single-wave walk.
 constexpr int kRowWaves = 4;
 constexpr int kRowsMaxM = 64;
 constexpr int kRowChunk = 32;  // records per vector load; the lookahead stays within kSortPad
+constexpr int kRowSub = 8;     // records whose NT tile loads are in flight together
 
-template <typename WT>
+template <typename WT, int NT>
 __global__ __launch_bounds__(kRowWaves * 64) void fwd_rows_kernel(LifConst C, int N_in, int N_out,
                                                                   const WT *__restrict__ Wt,
                                                                   SortedEv srt,
                                                                   float *__restrict__ t_out,
                                                                   float *__restrict__ slope,
                                                                   int *__restrict__ q_idx) {
-    extern __shared__ float rsum[];  // AL[R][64], AR[R][64]
+    extern __shared__ float rsum[];  // AL[NT][R][64], AR[NT][R][64]
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = uniform(threadIdx.x >> 6);
-    const int i = blockIdx.x * kWave + lane;
-    const bool row_ok = i < N_out;
     const int b = blockIdx.y;
     const int R = rows_of(C);
     float *AL = rsum;
-    float *AR = rsum + R * kWave;
+    float *AR = rsum + NT * R * kWave;
     const int *rs = srt.rs + static_cast<int64_t>(b) * (R + 1);
     const int n = *as_const(rs + R);
     // first row of range w: the row holding record w*n/kRowWaves
@@ -349,71 +349,102 @@ __global__ __launch_bounds__(kRowWaves * 64) void fwd_rows_kernel(LifConst C, in
     const float *eL = srt.L + eo;
     const float *eR = srt.R + eo;
     int cur = r_lo;
-    float aL = 0.f, aR = 0.f;
+    float aL[NT], aR[NT];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+        aL[t] = 0.f;
+        aR[t] = 0.f;
+    }
     // close rows cur .. target-1 of this wave's range
     auto close_to = [&](int target) {
         while (cur < target) {
-            AL[cur * kWave + lane] = aL;
-            AR[cur * kWave + lane] = aR;
-            aL = 0.f;
-            aR = 0.f;
+#pragma unroll
+            for (int t = 0; t < NT; ++t) {
+                AL[(t * R + cur) * kWave + lane] = aL[t];
+                AR[(t * R + cur) * kWave + lane] = aR[t];
+                aL[t] = 0.f;
+                aR[t] = 0.f;
+            }
             ++cur;
         }
     };
     const __amdgpu_buffer_rsrc_t wr =
         make_rsrc(Wt, static_cast<uint32_t>(static_cast<int64_t>(N_in) * N_out * sizeof(WT)));
-    const int voff = (row_ok ? i : 0) * static_cast<int>(sizeof(WT));
+    int voff[NT];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+        const int i = (blockIdx.x * NT + t) * kWave + lane;
+        voff[t] = min(i, N_out - 1) * static_cast<int>(sizeof(WT));
+    }
     const int rstride = N_out * static_cast<int>(sizeof(WT));
-    const unsigned jmax = static_cast<unsigned>(max(N_in - 1, 0));
-    auto wrow = [&](int j) { return static_cast<int>(min(static_cast<unsigned>(j), jmax)) * rstride; };
+    const int jmax = max(N_in - 1, 0);
     // Records come kRowChunk at a time, one per lane, with vector loads (the
     // next chunk's in flight while this one is summed); each record's
-    // fields are broadcast with readlane. All of a chunk's weight loads are
-    // issued before the first one is consumed.
+    // fields are broadcast with readlane, its weight-row offset precomputed
+    // per lane (clamped: lanes past the range read stale records).
     auto rdl = [](float v, int k) { return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), k)); };
-    int jn = ej[k_lo + lane], rn = er[k_lo + lane];
+    int jn = min(max(ej[k_lo + lane], 0), jmax) * rstride, rn = er[k_lo + lane];
     float Ln = eL[k_lo + lane], Rn = eR[k_lo + lane];
     for (int c0 = k_lo; c0 < k_hi; c0 += kRowChunk) {
         const int jc = jn, rc = rn;
         const float Lc = Ln, Rc = Rn;
-        // the next chunk (reads past the sample's list stay inside the padded arrays)
-        jn = ej[c0 + kRowChunk + lane];
+        jn = min(max(ej[c0 + kRowChunk + lane], 0), jmax) * rstride;
         rn = er[c0 + kRowChunk + lane];
         Ln = eL[c0 + kRowChunk + lane];
         Rn = eR[c0 + kRowChunk + lane];
         const int nc = min(kRowChunk, k_hi - c0);
-        float w[kRowChunk];
+        const bool one_row = nc == kRowChunk && __builtin_amdgcn_readlane(rc, kRowChunk - 1) == cur;
 #pragma unroll
-        for (int kk = 0; kk < kRowChunk; ++kk)
-            w[kk] = BufLoad<WT>::get(wr, voff, wrow(__builtin_amdgcn_readlane(jc, kk)));
-        if (nc == kRowChunk && __builtin_amdgcn_readlane(rc, kRowChunk - 1) == cur) {
-            // common case: a full chunk that continues the current row
+        for (int s0 = 0; s0 < kRowChunk; s0 += kRowSub) {
+            float w[kRowSub][NT];
 #pragma unroll
-            for (int kk = 0; kk < kRowChunk; ++kk) {
-                aL = fmaf(w[kk], rdl(Lc, kk), aL);
-                aR = fmaf(w[kk], rdl(Rc, kk), aR);
-            }
-            continue;
-        }
+            for (int kk = 0; kk < kRowSub; ++kk)
 #pragma unroll
-        for (int kk = 0; kk < kRowChunk; ++kk) {
-            if (kk < nc) {
-                const int r = __builtin_amdgcn_readlane(rc, kk);
-                if (r != cur) close_to(r);
-                aL = fmaf(w[kk], rdl(Lc, kk), aL);
-                aR = fmaf(w[kk], rdl(Rc, kk), aR);
+                for (int t = 0; t < NT; ++t)
+                    w[kk][t] = BufLoad<WT>::get(wr, voff[t], __builtin_amdgcn_readlane(jc, s0 + kk));
+            if (one_row) {
+#pragma unroll
+                for (int kk = 0; kk < kRowSub; ++kk) {
+                    const float l = rdl(Lc, s0 + kk), r = rdl(Rc, s0 + kk);
+#pragma unroll
+                    for (int t = 0; t < NT; ++t) {
+                        aL[t] = fmaf(w[kk][t], l, aL[t]);
+                        aR[t] = fmaf(w[kk][t], r, aR[t]);
+                    }
+                }
+            } else {
+#pragma unroll
+                for (int kk = 0; kk < kRowSub; ++kk) {
+                    if (s0 + kk < nc) {
+                        const int row = __builtin_amdgcn_readlane(rc, s0 + kk);
+                        if (row != cur) close_to(row);
+                        const float l = rdl(Lc, s0 + kk), r = rdl(Rc, s0 + kk);
+#pragma unroll
+                        for (int t = 0; t < NT; ++t) {
+                            aL[t] = fmaf(w[kk][t], l, aL[t]);
+                            aR[t] = fmaf(w[kk][t], r, aR[t]);
+                        }
+                    }
+                }
             }
         }
     }
     close_to(r_hi);
     __syncthreads();
-    if (wave != 0) return;
+    // wave t scans tile t
+    const int tile = (NT == 1) ? 0 : wave;
+    if (NT == 1 && wave != 0) return;
+    const int i = (blockIdx.x * NT + tile) * kWave + lane;
+    const bool row_ok = i < N_out;
+    if (uniform(static_cast<int>(__any(row_ok))) == 0) return;
+    const float *tl = AL + tile * R * kWave;
+    const float *tr = AR + tile * R * kWave;
     // grid point m: L sums of row m+1 plus R sums of row m
     Scan sc;
-    float wn = AL[kWave + lane] + AR[lane];  // next grid point's sum, read ahead
+    float wn = tl[kWave + lane] + tr[lane];  // next grid point's sum, read ahead
     for (int m = 0; m <= C.M; ++m) {
         const float wc = wn;
-        if (m < C.M) wn = AL[(m + 2) * kWave + lane] + AR[(m + 1) * kWave + lane];
+        if (m < C.M) wn = tl[(m + 2) * kWave + lane] + tr[(m + 1) * kWave + lane];
         sc.step(C, m, wc);
         if (__all(sc.found() || !row_ok)) break;
     }
@@ -831,16 +862,23 @@ hipError_t launch_forward(const LifConst &C, int64_t B, int64_t N_in, int64_t N_
     if (e != hipSuccess) return e;
     ProfScope prof("fwd_dense", st);
     if (C.M <= kRowsMaxM) {
-        dim3 grid(static_cast<unsigned>((N_out + kWave - 1) / kWave), static_cast<unsigned>(B));
-        const size_t lds = 2 * static_cast<size_t>(R) * kWave * sizeof(float);
-        if (bf16)
-            hipLaunchKernelGGL(fwd_rows_kernel<uint16_t>, grid, dim3(kRowWaves * kWave), lds, st, C,
-                               static_cast<int>(N_in), static_cast<int>(N_out),
-                               static_cast<const uint16_t *>(Wt), srt, t_out, slope, q_idx);
-        else
-            hipLaunchKernelGGL(fwd_rows_kernel<float>, grid, dim3(kRowWaves * kWave), lds, st, C,
-                               static_cast<int>(N_in), static_cast<int>(N_out),
-                               static_cast<const float *>(Wt), srt, t_out, slope, q_idx);
+        // four tiles per block (one scan per wave) when there are enough neurons
+        const int tiles = static_cast<int>((N_out + kWave - 1) / kWave);
+        const int nt = (tiles >= kRowWaves) ? kRowWaves : 1;
+        dim3 grid(static_cast<unsigned>((tiles + nt - 1) / nt), static_cast<unsigned>(B));
+        const size_t lds = 2 * static_cast<size_t>(nt) * R * kWave * sizeof(float);
+#define FWR(WTY, NTV)                                                                            \
+    hipLaunchKernelGGL((fwd_rows_kernel<WTY, NTV>), grid, dim3(kRowWaves * kWave), lds, st, C,  \
+                       static_cast<int>(N_in), static_cast<int>(N_out),                          \
+                       static_cast<const WTY *>(Wt), srt, t_out, slope, q_idx)
+        if (bf16) {
+            if (nt == kRowWaves) FWR(uint16_t, kRowWaves);
+            else FWR(uint16_t, 1);
+        } else {
+            if (nt == kRowWaves) FWR(float, kRowWaves);
+            else FWR(float, 1);
+        }
+#undef FWR
         return hipGetLastError();
     }
     constexpr int waves = 4;

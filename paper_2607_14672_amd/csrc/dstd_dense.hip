@@ -179,6 +179,33 @@ __global__ __launch_bounds__(kPrepThreads) void prep_kernel(LifConst C, int n_so
     }
 }
 
+// Event-row ranges of a sample's sorted list. With rs[r] the start of row r
+// (rs[R - 1] = rs[R] = n: the last row holds no records), the row holding
+// record t < n is the number of rows r < R - 1 with rs[r] <= t, minus one;
+// t >= n maps to R - 1. All lanes load the row starts at once (one round
+// trip instead of a chain of dependent scalar loads) and count with ballots;
+// a range's first records come back with readlane. The result: rows
+// [ra, rb) holding records [ka, kb).
+struct RowRange { int ra, rb, ka, kb; };
+
+__device__ __forceinline__ RowRange row_range(const int *rs, int R, int n, int ta, int tb,
+                                              bool first, bool last, int lane) {
+    int ca = 0, cb = 0, v0 = 0;
+    for (int r0 = 0; r0 < R - 1; r0 += kWave) {
+        const int r = r0 + lane;
+        const int v = (r < R - 1) ? rs[r] : 0x7fffffff;
+        if (r0 == 0) v0 = v;
+        ca += __popcll(__ballot(v <= ta));
+        cb += __popcll(__ballot(v <= tb));
+    }
+    RowRange g;
+    g.ra = first ? 0 : ((ta >= n) ? R - 1 : ca - 1);
+    g.rb = last ? R - 1 : ((tb >= n) ? R - 1 : cb - 1);
+    g.ka = (g.ra == R - 1) ? n : ((g.ra < kWave) ? __builtin_amdgcn_readlane(v0, g.ra) : rs[g.ra]);
+    g.kb = (g.rb == R - 1) ? n : ((g.rb < kWave) ? __builtin_amdgcn_readlane(v0, g.rb) : rs[g.rb]);
+    return g;
+}
+
 // --------------------------------------------------------------- forward --
 // Lane = neuron i of a 64-neuron tile, one sample per wavefront (4 per block).
 // The wave walks its sample's events in grid order: each record adds
@@ -300,14 +327,14 @@ __global__ __launch_bounds__(256) void fwd_sorted_kernel(LifConst C, int B, int 
 }
 
 // Row-parallel forward (M <= kRowsMaxM). A block of kRowWaves wavefronts
-// serves one sample and NT 64-neuron tiles: wave w sums, for all NT tiles,
+// serves one sample and NT (1 or kRowTiles) 64-neuron tiles: wave w sums, for all NT tiles,
 // the records of a contiguous range of whole event rows (ranges split the
 // sample's records about evenly), in the same per-row order as the
 // single-wave walk above, and writes each row's L and R sums to LDS; then
-// wave t runs the interval scan of tile t (NT == kRowWaves) or wave 0 scans
-// the single tile (NT == 1). The sums and their order are those of the
-// single-wave walk.
+// wave t < NT runs the interval scan of tile t. The sums and their order are
+// those of the single-wave walk.
 constexpr int kRowWaves = 4;
+constexpr int kRowTiles = 4;
 constexpr int kRowsMaxM = 64;
 constexpr int kRowChunk = 32;  // records per vector load; the lookahead stays within kSortPad
 constexpr int kRowSub = 8;     // records whose NT tile loads are in flight together
@@ -328,21 +355,12 @@ __global__ __launch_bounds__(kRowWaves * 64) void fwd_rows_kernel(LifConst C, in
     float *AR = rsum + NT * R * kWave;
     const int *rs = srt.rs + static_cast<int64_t>(b) * (R + 1);
     const int n = *as_const(rs + R);
-    // first row of range w: the row holding record w*n/kRowWaves
-    auto row_of = [&](int t) {
-        int lo = 0, hi = R - 1;  // rs[lo] <= t < rs[hi] (rs[R-1] == n)
-        if (t >= n) return R - 1;
-        while (hi - lo > 1) {
-            const int mid = (lo + hi) >> 1;
-            if (*as_const(rs + mid) <= t) lo = mid; else hi = mid;
-        }
-        return lo;
-    };
-    const int r_lo = (wave == 0) ? 0 : row_of(static_cast<int>((static_cast<int64_t>(n) * wave) / kRowWaves));
-    const int r_hi = (wave == kRowWaves - 1)
-                         ? R - 1
-                         : row_of(static_cast<int>((static_cast<int64_t>(n) * (wave + 1)) / kRowWaves));
-    const int k_lo = *as_const(rs + r_lo), k_hi = *as_const(rs + r_hi);
+    // range w: the rows holding records [w*n/kRowWaves, (w+1)*n/kRowWaves)
+    const RowRange rg = row_range(rs, R, n, static_cast<int>((static_cast<int64_t>(n) * wave) / kRowWaves),
+                                  static_cast<int>((static_cast<int64_t>(n) * (wave + 1)) / kRowWaves),
+                                  wave == 0, wave == kRowWaves - 1, lane);
+    const int r_lo = uniform(rg.ra), r_hi = uniform(rg.rb);
+    const int k_lo = uniform(rg.ka), k_hi = uniform(rg.kb);
     const int64_t eo = static_cast<int64_t>(b) * srt.stride;
     const int *ej = srt.j + eo;
     const int *er = srt.r + eo;
@@ -432,8 +450,8 @@ __global__ __launch_bounds__(kRowWaves * 64) void fwd_rows_kernel(LifConst C, in
     close_to(r_hi);
     __syncthreads();
     // wave t scans tile t
-    const int tile = (NT == 1) ? 0 : wave;
-    if (NT == 1 && wave != 0) return;
+    if (wave >= NT) return;
+    const int tile = wave;
     const int i = (blockIdx.x * NT + tile) * kWave + lane;
     const bool row_ok = i < N_out;
     if (uniform(static_cast<int>(__any(row_ok))) == 0) return;
@@ -616,20 +634,11 @@ __global__ __launch_bounds__(256) void dtin_rows_kernel(LifConst C, int B, int N
     const int R = rows_of(C);
     const int *rs = srt.rs + static_cast<int64_t>(b) * (R + 1);
     const int n = *as_const(rs + R);
-    auto row_of = [&](int t) {
-        int lo = 0, hi = R - 1;
-        if (t >= n) return R - 1;
-        while (hi - lo > 1) {
-            const int mid = (lo + hi) >> 1;
-            if (*as_const(rs + mid) <= t) lo = mid; else hi = mid;
-        }
-        return lo;
-    };
-    const int r_lo = (range == 0) ? 0 : row_of(static_cast<int>((static_cast<int64_t>(n) * range) / kDtRanges));
-    const int r_hi = (range == kDtRanges - 1)
-                         ? R - 1
-                         : row_of(static_cast<int>((static_cast<int64_t>(n) * (range + 1)) / kDtRanges));
-    if (*as_const(rs + r_lo) == *as_const(rs + r_hi)) return;  // block-uniform: no records
+    const RowRange rg = row_range(rs, R, n, static_cast<int>((static_cast<int64_t>(n) * range) / kDtRanges),
+                                  static_cast<int>((static_cast<int64_t>(n) * (range + 1)) / kDtRanges),
+                                  range == 0, range == kDtRanges - 1, lane);
+    const int r_lo = uniform(rg.ra), r_hi = uniform(rg.rb);
+    if (uniform(rg.ka) == uniform(rg.kb)) return;  // block-uniform: no records
     const int64_t eo = static_cast<int64_t>(b) * srt.stride;
     const int *ej = srt.j + eo;
     const float *edl = srt.L + eo;
@@ -864,7 +873,7 @@ hipError_t launch_forward(const LifConst &C, int64_t B, int64_t N_in, int64_t N_
     if (C.M <= kRowsMaxM) {
         // four tiles per block (one scan per wave) when there are enough neurons
         const int tiles = static_cast<int>((N_out + kWave - 1) / kWave);
-        const int nt = (tiles >= kRowWaves) ? kRowWaves : 1;
+        const int nt = (tiles >= kRowTiles) ? kRowTiles : 1;
         dim3 grid(static_cast<unsigned>((tiles + nt - 1) / nt), static_cast<unsigned>(B));
         const size_t lds = 2 * static_cast<size_t>(nt) * R * kWave * sizeof(float);
 #define FWR(WTY, NTV)                                                                            \
@@ -872,10 +881,10 @@ hipError_t launch_forward(const LifConst &C, int64_t B, int64_t N_in, int64_t N_
                        static_cast<int>(N_in), static_cast<int>(N_out),                          \
                        static_cast<const WTY *>(Wt), srt, t_out, slope, q_idx)
         if (bf16) {
-            if (nt == kRowWaves) FWR(uint16_t, kRowWaves);
+            if (nt == kRowTiles) FWR(uint16_t, kRowTiles);
             else FWR(uint16_t, 1);
         } else {
-            if (nt == kRowWaves) FWR(float, kRowWaves);
+            if (nt == kRowTiles) FWR(float, kRowTiles);
             else FWR(float, 1);
         }
 #undef FWR

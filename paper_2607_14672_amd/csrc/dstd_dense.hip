@@ -327,14 +327,18 @@ __global__ __launch_bounds__(256) void fwd_sorted_kernel(LifConst C, int B, int 
 }
 
 // Row-parallel forward (M <= kRowsMaxM). A block of kRowWaves wavefronts
-// serves one sample and NT (1 or kRowTiles) 64-neuron tiles: wave w sums, for all NT tiles,
-// the records of a contiguous range of whole event rows (ranges split the
-// sample's records about evenly), in the same per-row order as the
-// single-wave walk above, and writes each row's L and R sums to LDS; then
-// wave t < NT runs the interval scan of tile t. The sums and their order are
-// those of the single-wave walk.
+// serves one sample and NT (1, 2 or 4) 64-neuron tiles: wave w sums, for all
+// NT tiles, the records of a contiguous range of whole event rows (ranges
+// split the sample's records about evenly), in the same per-row order as the
+// single-wave walk above; then wave t < NT runs the interval scan of tile t.
+// Grid point m takes the L sums of row m+1 plus the R sums of row m. Where
+// both rows lie in one wave's range, that wave adds them and stores the
+// point's sum in LDS; at a boundary between two ranges the two halves are
+// stored apart (first row's L sums, last row's R sums, per wave) and added
+// by the scanning wave. The sums, and their order, are those of the
+// single-wave walk; one value per point halves the LDS a tile needs.
 constexpr int kRowWaves = 4;
-constexpr int kRowTiles = 4;
+constexpr int kRowLdsCap = 48 * 1024;  // LDS budget per block when choosing NT
 constexpr int kRowsMaxM = 64;
 constexpr int kRowChunk = 32;  // records per vector load; the lookahead stays within kSortPad
 constexpr int kRowSub = 8;     // records whose NT tile loads are in flight together
@@ -346,13 +350,17 @@ __global__ __launch_bounds__(kRowWaves * 64) void fwd_rows_kernel(LifConst C, in
                                                                   float *__restrict__ t_out,
                                                                   float *__restrict__ slope,
                                                                   int *__restrict__ q_idx) {
-    extern __shared__ float rsum[];  // AL[NT][R][64], AR[NT][R][64]
+    // LDS: P[NT][R][64] point sums, BL[NT][kRowWaves][64] and
+    // BR[NT][kRowWaves][64] range-boundary halves, span[2][kRowWaves] ranges
+    extern __shared__ float rsum[];
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = uniform(threadIdx.x >> 6);
     const int b = blockIdx.y;
     const int R = rows_of(C);
-    float *AL = rsum;
-    float *AR = rsum + NT * R * kWave;
+    float *P = rsum;
+    float *BL = rsum + NT * R * kWave;
+    float *BR = BL + NT * kRowWaves * kWave;
+    int *span = reinterpret_cast<int *>(BR + NT * kRowWaves * kWave);
     const int *rs = srt.rs + static_cast<int64_t>(b) * (R + 1);
     const int n = *as_const(rs + R);
     // range w: the rows holding records [w*n/kRowWaves, (w+1)*n/kRowWaves)
@@ -367,19 +375,24 @@ __global__ __launch_bounds__(kRowWaves * 64) void fwd_rows_kernel(LifConst C, in
     const float *eL = srt.L + eo;
     const float *eR = srt.R + eo;
     int cur = r_lo;
-    float aL[NT], aR[NT];
+    float aL[NT], aR[NT], cy[NT];
 #pragma unroll
     for (int t = 0; t < NT; ++t) {
         aL[t] = 0.f;
         aR[t] = 0.f;
+        cy[t] = 0.f;
     }
-    // close rows cur .. target-1 of this wave's range
+    // close rows cur .. target-1 of this wave's range: point cur-1 gets this
+    // row's L sums plus the previous row's R sums (cy)
     auto close_to = [&](int target) {
         while (cur < target) {
 #pragma unroll
             for (int t = 0; t < NT; ++t) {
-                AL[(t * R + cur) * kWave + lane] = aL[t];
-                AR[(t * R + cur) * kWave + lane] = aR[t];
+                if (cur == r_lo)
+                    BL[(t * kRowWaves + wave) * kWave + lane] = aL[t];
+                else
+                    P[(t * R + cur - 1) * kWave + lane] = aL[t] + cy[t];
+                cy[t] = aR[t];
                 aL[t] = 0.f;
                 aR[t] = 0.f;
             }
@@ -448,6 +461,14 @@ __global__ __launch_bounds__(kRowWaves * 64) void fwd_rows_kernel(LifConst C, in
         }
     }
     close_to(r_hi);
+    if (r_hi > r_lo) {
+#pragma unroll
+        for (int t = 0; t < NT; ++t) BR[(t * kRowWaves + wave) * kWave + lane] = cy[t];
+    }
+    if (lane == 0) {
+        span[wave] = r_lo;
+        span[kRowWaves + wave] = r_hi;
+    }
     __syncthreads();
     // wave t scans tile t
     if (wave >= NT) return;
@@ -455,14 +476,27 @@ __global__ __launch_bounds__(kRowWaves * 64) void fwd_rows_kernel(LifConst C, in
     const int i = (blockIdx.x * NT + tile) * kWave + lane;
     const bool row_ok = i < N_out;
     if (uniform(static_cast<int>(__any(row_ok))) == 0) return;
-    const float *tl = AL + tile * R * kWave;
-    const float *tr = AR + tile * R * kWave;
-    // grid point m: L sums of row m+1 plus R sums of row m
+    // range boundaries: point lo(w) - 1 of each nonempty range w >= 1 (wave
+    // 0's range always holds row 0 and is never empty) is w's first-row L
+    // sums plus the last-row R sums of the nonempty range before it; this
+    // wave writes it into its own tile's slot (no other wave stores there)
+    float *tp = P + tile * R * kWave;
+    const float *tbl = BL + tile * kRowWaves * kWave;
+    const float *tbr = BR + tile * kRowWaves * kWave;
+    int prev = 0;
+#pragma unroll
+    for (int w = 1; w < kRowWaves; ++w) {
+        const int lo = uniform(span[w]), hi = uniform(span[kRowWaves + w]);
+        if (hi > lo) {
+            tp[(lo - 1) * kWave + lane] = tbl[w * kWave + lane] + tbr[prev * kWave + lane];
+            prev = w;
+        }
+    }
     Scan sc;
-    float wn = tl[kWave + lane] + tr[lane];  // next grid point's sum, read ahead
+    float wn = tp[lane];  // next grid point's sum, read ahead
     for (int m = 0; m <= C.M; ++m) {
         const float wc = wn;
-        if (m < C.M) wn = tl[(m + 2) * kWave + lane] + tr[(m + 1) * kWave + lane];
+        if (m < C.M) wn = tp[(m + 1) * kWave + lane];
         sc.step(C, m, wc);
         if (__all(sc.found() || !row_ok)) break;
     }
@@ -871,20 +905,29 @@ hipError_t launch_forward(const LifConst &C, int64_t B, int64_t N_in, int64_t N_
     if (e != hipSuccess) return e;
     ProfScope prof("fwd_dense", st);
     if (C.M <= kRowsMaxM) {
-        // four tiles per block (one scan per wave) when there are enough neurons
+        // up to four tiles per block (one scan per wave) when there are
+        // enough neurons and their point sums fit the LDS budget
         const int tiles = static_cast<int>((N_out + kWave - 1) / kWave);
-        const int nt = (tiles >= kRowTiles) ? kRowTiles : 1;
+        auto lds_of = [&](int t) {
+            return static_cast<size_t>(t) * (R + 2 * kRowWaves) * kWave * sizeof(float) +
+                   2 * kRowWaves * sizeof(int);
+        };
+        int nt = 1;
+        for (int t : {4, 2})
+            if (nt == 1 && tiles >= t && lds_of(t) <= kRowLdsCap) nt = t;
         dim3 grid(static_cast<unsigned>((tiles + nt - 1) / nt), static_cast<unsigned>(B));
-        const size_t lds = 2 * static_cast<size_t>(nt) * R * kWave * sizeof(float);
+        const size_t lds = lds_of(nt);
 #define FWR(WTY, NTV)                                                                            \
     hipLaunchKernelGGL((fwd_rows_kernel<WTY, NTV>), grid, dim3(kRowWaves * kWave), lds, st, C,  \
                        static_cast<int>(N_in), static_cast<int>(N_out),                          \
                        static_cast<const WTY *>(Wt), srt, t_out, slope, q_idx)
         if (bf16) {
-            if (nt == kRowTiles) FWR(uint16_t, kRowTiles);
+            if (nt == 4) FWR(uint16_t, 4);
+            else if (nt == 2) FWR(uint16_t, 2);
             else FWR(uint16_t, 1);
         } else {
-            if (nt == kRowTiles) FWR(float, kRowTiles);
+            if (nt == 4) FWR(float, 4);
+            else if (nt == 2) FWR(float, 2);
             else FWR(float, 1);
         }
 #undef FWR

@@ -517,14 +517,17 @@ __global__ __launch_bounds__(kRowWaves * 64) void fwd_rows_kernel(LifConst C, in
 // its share of the batch. G[b, :, tile] is computed in place from the
 // gradient triples (each thread owns one neuron and a fixed set of rows, so
 // neurons without gradient cost no exponential) and staged in LDS (double
-// buffered) as pairs (G[r], G[r+1]) per neuron, so one 8-byte read with an
-// immediate neuron offset serves both halves of an event; the next sample's
-// values are computed while this one is consumed. Slot R-1 is a zero pair
-// for inputs without events; a sample whose tile is all zero is skipped.
+// buffered) as rows of TI + 1 floats, G[r][neuron]: the two halves of an
+// event, G[r][i] and G[r+1][i], are TI + 1 dwords apart, so one two-address
+// LDS read with immediate offsets (i, i + TI + 1) serves both, and the odd
+// row stride spreads lanes with different event rows over the banks. Rows
+// R-1 and R stay zero (R-1 is the point after the grid; slot R-1 serves
+// inputs without events). The next sample's G values and events are fetched
+// while this one is consumed; a sample whose tile is all zero is skipped.
 // Batch splits write partial sums, reduced in order.
 template <int TI, int NPER>
 __global__ __launch_bounds__(256) void dw_dense_kernel(LifConst C, int B, int N_in, int N_out,
-                                                        int b_per_split, int pstride,
+                                                        int b_per_split,
                                                         const float *__restrict__ gam,
                                                         const float *__restrict__ uq,
                                                         const int *__restrict__ qv,
@@ -532,8 +535,10 @@ __global__ __launch_bounds__(256) void dw_dense_kernel(LifConst C, int B, int N_
                                                         const float *__restrict__ ev_L,
                                                         const float *__restrict__ ev_R,
                                                         float *__restrict__ dW_part) {
-    extern __shared__ float2 ps[];  // [2][TI][pstride]
+    extern __shared__ float gs[];  // [2][R + 1][TI + 1]
+    constexpr int kStr = TI + 1;
     const int R = rows_of(C);
+    const int gbuf = (R + 1) * kStr;
     const int j = blockIdx.x * blockDim.x + threadIdx.x;
     const int i0 = blockIdx.y * TI;
     const int ni = min(TI, N_out - i0);
@@ -549,62 +554,80 @@ __global__ __launch_bounds__(256) void dw_dense_kernel(LifConst C, int B, int N_
     constexpr int kRowStep = 256 / TI;
     const GStep gst = g_step(C, kRowStep);
     float pre[NPER];
-    auto fetch = [&](int b) {
-        const int64_t k = static_cast<int64_t>(b) * N_out + i0 + min(l_own, ni - 1);
-        const bool own = l_own < ni;
-        const float gm = own ? gam[k] : 0.f;
-        const float u = own ? uq[k] : 0.f;
-        const int q = own ? qv[k] : -1;
-        g_strided<NPER>(C, gst, gm, u, q, r_first - 1, kRowStep, pre);
+    // gradient triple of this thread's neuron in sample b (q = -1: none, or
+    // past the block's share); loaded two samples ahead of its use
+    struct Tri { float gm, u; int q; };
+    auto load_tri = [&](int b) {
+        Tri t{0.f, 0.f, -1};
+        if (l_own < ni && b < b_hi) {
+            const int64_t k = static_cast<int64_t>(b) * N_out + i0 + l_own;
+            t.gm = gam[k];
+            t.u = uq[k];
+            t.q = qv[k];
+        }
+        return t;
+    };
+    auto fetch = [&](const Tri &t) {
+        g_strided<NPER>(C, gst, t.gm, t.u, t.q, r_first - 1, kRowStep, pre);
         bool nz = false;
 #pragma unroll
         for (int c = 0; c < NPER; ++c) nz = nz || pre[c] != 0.f;
         return nz;
     };
-    auto store = [&](float2 *buf) {
+    auto store = [&](float *buf) {
 #pragma unroll
         for (int c = 0; c < NPER; ++c) {
             const int k = threadIdx.x + c * 256;
             if (k < total) {
                 const int r = k / TI, l = k % TI;
-                float2 *row = buf + l * pstride;
-                if (r < R - 1) row[r].x = pre[c];
-                if (r > 0) row[r - 1].y = pre[c];
+                if (r < R - 1) buf[r * kStr + l] = pre[c];
             }
         }
-        for (int l = threadIdx.x; l < TI; l += blockDim.x) buf[l * pstride + R - 1] = make_float2(0.f, 0.f);
     };
+    // event of (b, j): slot (row) and halves; no events: slot R-1, zeros
+    auto event = [&](int b, int &slot, float &L, float &Rv) {
+        slot = R - 1;
+        L = 0.f;
+        Rv = 0.f;
+        if (j_ok && b < b_hi) {
+            const int64_t o = static_cast<int64_t>(b) * N_in + j;
+            const int r = ev_row[o];
+            if (r >= 0) {
+                slot = r;
+                L = ev_L[o];
+                Rv = ev_R[o];
+            }
+        }
+    };
+    for (int k = threadIdx.x; k < 2 * 2 * kStr; k += blockDim.x)
+        gs[(k / (2 * kStr)) * gbuf + (R - 1) * kStr + k % (2 * kStr)] = 0.f;
     bool live = false;
     if (b_lo < b_hi) {
-        live = fetch(b_lo);
-        store(ps);
+        live = fetch(load_tri(b_lo));
+        store(gs);
     }
+    Tri tri_n = load_tri(b_lo + 1);
+    int slot_n;
+    float L_n, R_n;
+    event(b_lo, slot_n, L_n, R_n);
     live = __syncthreads_or(live);
     for (int b = b_lo; b < b_hi; ++b) {
-        float2 *cur = ps + ((b - b_lo) & 1) * TI * pstride;
+        const float *cur = gs + ((b - b_lo) & 1) * gbuf;
         const bool more = b + 1 < b_hi;
+        const int slot = slot_n;
+        const float L = L_n, Rv = R_n;
+        event(b + 1, slot_n, L_n, R_n);
+        const Tri tri = tri_n;
+        tri_n = load_tri(b + 2);
         bool live_next = false;
-        if (more) live_next = fetch(b + 1);
+        if (more) live_next = fetch(tri);
         if (live) {
-            int slot = R - 1;
-            float L = 0.f, Rv = 0.f;
-            if (j_ok) {
-                const int64_t o = static_cast<int64_t>(b) * N_in + j;
-                const int r = ev_row[o];
-                if (r >= 0) {
-                    slot = r;
-                    L = ev_L[o];
-                    Rv = ev_R[o];
-                }
-            }
-            const float2 *p = cur + slot;
+            const float *p = cur + slot * kStr;
 #pragma unroll
-            for (int ii = 0; ii < TI; ++ii) {
-                const float2 g = p[ii * pstride];
-                acc[ii] = fmaf(g.x, L, fmaf(g.y, Rv, acc[ii]));
-            }
+            for (int ii = 0; ii < TI; ++ii)
+                acc[ii] = fmaf(p[ii], L, fmaf(p[ii + kStr], Rv, acc[ii]));
         }
-        if (more) store(ps + ((b + 1 - b_lo) & 1) * TI * pstride);
+        if (more) store(gs + ((b + 1 - b_lo) & 1) * gbuf);
         live = __syncthreads_or(live_next);
     }
     if (!j_ok) return;
@@ -947,11 +970,9 @@ hipError_t launch_forward(const LifConst &C, int64_t B, int64_t N_in, int64_t N_
     return hipGetLastError();
 }
 
-// neuron tile: the LDS pair offset of the last neuron must fit the 16-bit
-// instruction offset
+// neuron tile: 64, or 32 where two 64-wide G buffers would pass 48 KB of LDS
 static int dw_ti(int M) {
-    const int ps = (M + 3) | 1;
-    return (ps * 63 * 8 < 65536) ? 64 : 32;
+    return (2 * (M + 4) * 65 * 4 <= 48 * 1024) ? 64 : 32;
 }
 
 // register slots per thread for staging one tile (R * TI values / 256 threads)
@@ -977,15 +998,14 @@ DwPlan plan_dw(int64_t B, int64_t N_in, int64_t N_out, int M) {
 static hipError_t launch_dw(const LifConst &C, const DwPlan &p, int64_t B, int64_t N_in,
                             int64_t N_out, const DenseBwdWs &ws, float *dst, hipStream_t st) {
     const int ti = p.jw;
-    const int pstride = (C.M + 3) | 1;
     dim3 grid(static_cast<unsigned>((N_in + 255) / 256),
               static_cast<unsigned>((N_out + ti - 1) / ti), static_cast<unsigned>(p.nsplit));
-    size_t lds = 2 * static_cast<size_t>(ti) * pstride * sizeof(float2);
+    size_t lds = 2 * static_cast<size_t>(C.M + 4) * (ti + 1) * sizeof(float);
     ProfScope prof("dw_dense", st);
     const int nper = dw_nper(C.M, ti);
 #define DW_LAUNCH(TIV, NP)                                                                        \
     hipLaunchKernelGGL((dw_dense_kernel<TIV, NP>), grid, dim3(256), lds, st, C, static_cast<int>(B), \
-                       static_cast<int>(N_in), static_cast<int>(N_out), p.b_per_split, pstride,    \
+                       static_cast<int>(N_in), static_cast<int>(N_out), p.b_per_split,             \
                        ws.gam, ws.uq, ws.q, ws.row, ws.L, ws.R, dst)
     if (ti == 64) {
         if (nper == 9) DW_LAUNCH(64, 9);

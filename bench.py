@@ -258,13 +258,12 @@ def layer_desc(lay):
 def kernel_algorithmic_flops(net, act):
     """Algorithmic flops of one step, per kernel name (2-sparse events:
     FLOPS_PER_UPDATE per (sample, input with events, neuron))."""
-    fl = {k: 0.0 for k in ("fwd_dense", "dw_dense", "dtin_dense", "conv_fwd", "conv_dw",
-                           "conv_dtin")}
+    fl = {k: 0.0 for k in ("fwd_dense", "dw_dense", "dtin_rows", "conv_fwd", "conv_dw",
+                           "conv_dtp")}
     for l, (e, a) in enumerate(zip(net.L, act)):
         upd = a["updates"]
-        pre = "conv_" if e["cs"] is not None else ""
-        fwd, dw, dt = ((pre + "fwd", pre + "dw", pre + "dtin") if pre else
-                       ("fwd_dense", "dw_dense", "dtin_dense"))
+        fwd, dw, dt = (("conv_fwd", "conv_dw", "conv_dtp") if e["cs"] is not None else
+                       ("fwd_dense", "dw_dense", "dtin_rows"))
         fl[fwd] += FLOPS_PER_UPDATE * upd
         fl[dw] += FLOPS_PER_UPDATE * upd
         if l > 0:

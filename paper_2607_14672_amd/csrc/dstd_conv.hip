@@ -51,54 +51,121 @@ __device__ __forceinline__ int64_t nchw_index(const ConvGeom &g, int b, int ci, 
     return ((static_cast<int64_t>(b) * g.C_in + ci) * g.H + y) * g.W + x;
 }
 
+// Cell-major events of every input (row -1: no events) for the dW reduction
+// (NULL: not wanted).
+struct CellEv { int *row; float *L, *R; };
+
+// The t-th raw input of cell row (b, py) in NCHW order (channel-major, so
+// consecutive t are mostly consecutive addresses): its NCHW index, and its
+// cell-major slot px * PC + j' in `slot`.
+__device__ __forceinline__ int64_t cell_row_input(const ConvGeom &g, int b, int py, int t,
+                                                  int &slot) {
+    const int per_ch = g.Wp * g.P;
+    const int ci = t / per_ch, rem = t % per_ch;
+    int y, x, px, d;
+    if (g.pool == 2) {
+        const int dy = rem / g.W;
+        x = rem % g.W;
+        y = 2 * py + dy;
+        px = x >> 1;
+        d = dy * 2 + (x & 1);
+    } else if (g.pool == 0) {
+        d = rem;
+        y = d / g.W;
+        x = d % g.W;
+        px = 0;
+    } else {
+        x = rem;
+        y = py;
+        px = rem;
+        d = 0;
+    }
+    slot = px * g.PC + d * g.C_in + ci;
+    return nchw_index(g, b, ci, y, x);
+}
+
 // ------------------------------------------------------------ cell sort --
-// One block per cell row (b, py); wave w handles cells px = w, w + 4, ...
-// LDS: hist[r][px] (later the next free slot of bucket (r, px)), then the
-// per-thread partial sums of the prefix scan.
-__global__ __launch_bounds__(256) void conv_sort_kernel(LifConst C, ConvGeom g,
-                                                        const float *__restrict__ t_in,
-                                                        ConvSorted cs) {
-    extern __shared__ int sh[];
+// One block of 256 threads per cell row (b, py).
+// LDS: hist[r][px] (later the next free slot of bucket (r, px)), the 256
+// per-thread partial sums of the prefix scan, then (when they fit) the cell
+// row's input spike times in cell-major order, read once in NCHW order.
+// Wave w owns cells px = w, w + 4, ... (each bucket is ranked by one wave
+// only); where a cell has fewer than 64 inputs a wave takes several of its
+// cells per pass. Records of a bucket keep the input order (j' ascending).
+// The placement pass also writes the cell row's events (ev).
+__host__ __device__ __forceinline__ int sort_stage_floats(int M, const ConvGeom &g) {
+    const int per = g.Wp * g.PC;
+    return ((M + 3) * g.Wp + 256 + per) * 4 <= 64 * 1024 ? per : 0;
+}
+
+__device__ void sort_cell_row(const LifConst &C, const ConvGeom &g, const float *__restrict__ t_in,
+                              const ConvSorted &cs, const CellEv &ev, int cr, int *sh) {
     const int R = rows_of(C);
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = uniform(threadIdx.x >> 6);
     const int nw = blockDim.x >> 6;
-    const int cr = blockIdx.x;  // b * Hp + py
     const int b = cr / g.Hp, py = cr % g.Hp;
     const int nb = R * g.Wp;  // buckets, flat f = r * Wp + px
     const bool bwd = cs.P != nullptr;
     const int KT = g.KH * g.KW;
     int *hist = sh;
     int *part = sh + nb;
+    float *tl = sort_stage_floats(C.M, g) > 0 ? reinterpret_cast<float *>(part + 256) : nullptr;
     for (int k = threadIdx.x; k < nb; k += blockDim.x) hist[k] = 0;
+    if (tl) {
+        const int per = g.Wp * g.PC;
+        for (int t = threadIdx.x; t < per; t += blockDim.x) {
+            int slot;
+            const int64_t src = cell_row_input(g, b, py, t, slot);
+            tl[slot] = t_in[src];
+        }
+    }
     __syncthreads();
-    for (int px = wave; px < g.Wp; px += nw) {
+    auto t_at = [&](int px, int j) {
+        if (tl) return tl[px * g.PC + j];
+        int y, x;
+        raw_pixel(g, py, px, j / g.C_in, y, x);
+        return t_in[nchw_index(g, b, j % g.C_in, y, x)];
+    };
+    const int cpi = (g.PC < kWave) ? kWave / g.PC : 1;  // cells per pass
+    const int lsub = (g.PC < kWave) ? lane / g.PC : 0;
+    const int lj = (g.PC < kWave) ? lane % g.PC : lane;
+    for (int i0 = 0; wave + nw * i0 < g.Wp; i0 += cpi) {
+        const int px = wave + nw * (i0 + lsub);
+        const bool cell_ok = lsub < cpi && px < g.Wp;
         for (int j0 = 0; j0 < g.PC; j0 += kWave) {
-            const int j = j0 + lane;
-            if (j < g.PC) {
-                int y, x;
-                raw_pixel(g, py, px, j / g.C_in, y, x);
-                const int r = bin_row(C, t_in[nchw_index(g, b, j % g.C_in, y, x)]);
+            const int j = j0 + lj;
+            if (cell_ok && j < g.PC) {
+                const int r = bin_row(C, t_at(px, j));
                 if (r >= 0) atomicAdd(&hist[r * g.Wp + px], 1);
             }
         }
     }
     __syncthreads();
-    // exclusive prefix over the buckets in (r, px) order
+    // exclusive prefix over the buckets in (r, px) order: per-thread chunk
+    // sums, scanned by wave 0 (four per lane), then each chunk in order
     const int chunk = (nb + blockDim.x - 1) / blockDim.x;
     const int lo = min(nb, static_cast<int>(threadIdx.x) * chunk), hi = min(nb, lo + chunk);
     int s = 0;
     for (int f = lo; f < hi; ++f) s += hist[f];
     part[threadIdx.x] = s;
     __syncthreads();
-    if (threadIdx.x == 0) {
-        int run = 0;
-        for (int t = 0; t < static_cast<int>(blockDim.x); ++t) {
-            const int v = part[t];
-            part[t] = run;
-            run += v;
+    if (wave == 0) {
+        const int v0 = part[4 * lane], v1 = part[4 * lane + 1], v2 = part[4 * lane + 2],
+                  v3 = part[4 * lane + 3];
+        const int tot = v0 + v1 + v2 + v3;
+        int inc = tot;
+#pragma unroll
+        for (int m = 1; m < kWave; m <<= 1) {
+            const int o = __shfl_up(inc, m);
+            if (lane >= m) inc += o;
         }
-        cs.off[static_cast<int64_t>(cr) * (nb + 1) + nb] = run;
+        const int ex = inc - tot;
+        part[4 * lane] = ex;
+        part[4 * lane + 1] = ex + v0;
+        part[4 * lane + 2] = ex + v0 + v1;
+        part[4 * lane + 3] = ex + v0 + v1 + v2;
+        if (lane == kWave - 1) cs.off[static_cast<int64_t>(cr) * (nb + 1) + nb] = inc;
     }
     __syncthreads();
     int run = part[threadIdx.x];
@@ -110,34 +177,41 @@ __global__ __launch_bounds__(256) void conv_sort_kernel(LifConst C, ConvGeom g,
         run += v;
     }
     __syncthreads();
-    // placement: lanes with the same row are ranked by lane (j' ascending)
+    // placement: lanes of one bucket are ranked by lane (j' ascending)
     const int64_t rb = static_cast<int64_t>(cr) * g.Wp * g.PC;
     const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
-    for (int px = wave; px < g.Wp; px += nw) {
+    for (int i0 = 0; wave + nw * i0 < g.Wp; i0 += cpi) {
+        const int px = wave + nw * (i0 + lsub);
+        const bool cell_ok = lsub < cpi && px < g.Wp;
         for (int j0 = 0; j0 < g.PC; j0 += kWave) {
-            const int j = j0 + lane;
+            const int j = j0 + lj;
             Event e{-1, 0.f, 0.f, 0.f, 0.f};
-            if (j < g.PC) {
-                int y, x;
-                raw_pixel(g, py, px, j / g.C_in, y, x);
-                e = bin_event(C, t_in[nchw_index(g, b, j % g.C_in, y, x)]);
+            int f = -1;
+            if (cell_ok && j < g.PC) {
+                e = bin_event(C, t_at(px, j));
+                const int64_t k = rb + static_cast<int64_t>(px) * g.PC + j;
+                if (ev.row) {
+                    ev.row[k] = e.row;
+                    ev.L[k] = e.L;
+                    ev.R[k] = e.R;
+                }
+                if (e.row >= 0) f = e.row * g.Wp + px;
             }
-            const int r = e.row;
             int pos = 0;
-            uint64_t todo = __ballot(r >= 0);
+            uint64_t todo = __ballot(f >= 0);
             while (todo) {
                 const int lead = __ffsll(static_cast<unsigned long long>(todo)) - 1;
-                const int rl = __builtin_amdgcn_readlane(r, lead);
-                const uint64_t same = __ballot(r == rl);
-                int *slot = &hist[rl * g.Wp + px];
+                const int fl = __builtin_amdgcn_readlane(f, lead);
+                const uint64_t same = __ballot(f == fl);
+                int *slot = &hist[fl];
                 const int base = *slot;
-                if (r == rl) pos = base + __popcll(same & below);
+                if (f == fl) pos = base + __popcll(same & below);
                 __builtin_amdgcn_wave_barrier();
                 if (lane == lead) *slot = base + __popcll(same);
                 __builtin_amdgcn_wave_barrier();
                 todo &= ~same;
             }
-            if (r >= 0) {
+            if (f >= 0) {
                 const int64_t o = rb + pos;
                 cs.key[o] = px * g.C_in + (j % g.C_in);
                 cs.L[o] = bwd ? e.dL : e.L;
@@ -152,14 +226,32 @@ __global__ __launch_bounds__(256) void conv_sort_kernel(LifConst C, ConvGeom g,
     }
 }
 
+// The events of one cell row without the sort (dW wanted, dt_in not), read
+// in NCHW order.
+__device__ void events_cell_row(const LifConst &C, const ConvGeom &g,
+                                const float *__restrict__ t_in, const CellEv &ev, int cr) {
+    const int b = cr / g.Hp, py = cr % g.Hp;
+    const int per = g.Wp * g.PC;
+    const int64_t rb = static_cast<int64_t>(cr) * per;
+    for (int t = threadIdx.x; t < per; t += blockDim.x) {
+        int slot;
+        const int64_t src = cell_row_input(g, b, py, t, slot);
+        const Event e = bin_event(C, t_in[src]);
+        ev.row[rb + slot] = e.row;
+        ev.L[rb + slot] = e.L;
+        ev.R[rb + slot] = e.R;
+    }
+}
+
 // ------------------------------------------------------ weight layout ----
-// WT[(k * C_in + ci) * C_out + co] = W[co, ci, k] / P (k = ky*KW + kx).
+// WT[(k * C_in + ci) * C_out + co] = W[co, ci, k] / P (k = ky*KW + kx); block
+// blk of 256 threads takes entries blk * 256 ...
 template <typename WT>
-__global__ __launch_bounds__(256) void conv_weights_kernel(ConvGeom g, const WT *__restrict__ W,
-                                                           float *__restrict__ out) {
+__device__ void weights_block(const ConvGeom &g, const WT *__restrict__ W, float *__restrict__ out,
+                              int64_t blk) {
     const int KT = g.KH * g.KW;
     const int64_t n = static_cast<int64_t>(KT) * g.C_in * g.C_out;
-    const int64_t t = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+    const int64_t t = blk * blockDim.x + threadIdx.x;
     if (t >= n) return;
     const int co = static_cast<int>(t % g.C_out);
     const int64_t u = t / g.C_out;
@@ -345,71 +437,74 @@ __global__ __launch_bounds__(256) void conv_fwd_kernel(LifConst C, ConvGeom g, i
 }
 
 // --------------------------------------------------------- backward ------
-// Events of every input in cell-major order (row -1 = no events) for the dW
-// reduction; dt_in starts at zero (inputs with events are overwritten later).
-__global__ __launch_bounds__(256) void conv_events_kernel(LifConst C, ConvGeom g, int64_t n,
-                                                          const float *__restrict__ t_in,
-                                                          int *__restrict__ ev_row,
-                                                          float *__restrict__ ev_L,
-                                                          float *__restrict__ ev_R,
-                                                          float *__restrict__ dt_in) {
-    const int64_t k = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
-    if (k >= n) return;
-    const int j = static_cast<int>(k % g.PC);
-    const int64_t cell = k / g.PC;
-    const int px = static_cast<int>(cell % g.Wp);
-    const int64_t u = cell / g.Wp;
-    const int py = static_cast<int>(u % g.Hp);
-    const int b = static_cast<int>(u / g.Hp);
-    int y, x;
-    raw_pixel(g, py, px, j / g.C_in, y, x);
-    const int64_t src = nchw_index(g, b, j % g.C_in, y, x);
-    const Event e = bin_event(C, t_in[src]);
-    ev_row[k] = e.row;
-    ev_L[k] = e.L;
-    ev_R[k] = e.R;
-    if (dt_in) dt_in[src] = 0.f;
-}
+// Gradient triples (gamma, t - T_q, q) of grad_prep for kGradPos output
+// positions s = b * Ho*Wo + p and every channel: read from the NCHW outputs
+// with positions along the lanes, staged in LDS kGradCh channels at a time
+// and written position-major [s][co] (each position's channels contiguous).
+// live[s] = 1 if any channel of s passes gradient.
+constexpr int kGradPos = 16, kGradCh = 64;
+constexpr int kGradLdsBytes = (3 * kGradCh * (kGradPos + 1) + kGradPos) * 4;
 
-// Per output neuron (b, co, p) -> position-major [b][p][co]: the gradient
-// triple (gamma, t - T_q, q) of grad_prep.
-__global__ __launch_bounds__(256) void conv_grad_prep_kernel(LifConst C, ConvGeom g, int64_t n,
-                                                             const float *__restrict__ t_out,
-                                                             const float *__restrict__ slope,
-                                                             const int *__restrict__ q_idx,
-                                                             const float *__restrict__ grad_t,
-                                                             float *__restrict__ gam,
-                                                             float *__restrict__ uq,
-                                                             int *__restrict__ qv) {
-    const int64_t t = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
-    if (t >= n) return;
+__device__ void grad_block(const LifConst &C, const ConvGeom &g, int64_t n_pos, int64_t blk,
+                           const float *__restrict__ t_out, const float *__restrict__ slope,
+                           const int *__restrict__ q_idx, const float *__restrict__ grad_t,
+                           float *__restrict__ gam, float *__restrict__ uq, int *__restrict__ qv,
+                           int *__restrict__ live, int *sh) {
+    constexpr int kS = kGradPos + 1;
+    float *sg = reinterpret_cast<float *>(sh);
+    float *su = sg + kGradCh * kS;
+    int *sq = reinterpret_cast<int *>(su + kGradCh * kS);
+    int *sl = sq + kGradCh * kS;
     const int HoWo = g.Ho * g.Wo;
-    const int co = static_cast<int>(t % g.C_out);
-    const int64_t u = t / g.C_out;
-    const int p = static_cast<int>(u % HoWo);
-    const int64_t b = u / HoWo;
-    const int64_t o = (b * g.C_out + co) * HoWo + p;
-    const int q = q_idx[o];
-    GradPrep gp{0.f, 0.f, -1};
-    if (q >= 0) {  // silent neurons: no further loads
-        const float g = grad_t[o];
-        if (g != 0.f) gp = grad_prep(C, t_out[o], slope[o], q, g);
+    const int64_t s0 = blk * kGradPos;
+    if (threadIdx.x < kGradPos) sl[threadIdx.x] = 0;
+    __syncthreads();
+    for (int c0 = 0; c0 < g.C_out; c0 += kGradCh) {
+        for (int e = threadIdx.x; e < kGradCh * kGradPos; e += blockDim.x) {
+            const int cl = e / kGradPos, pl = e % kGradPos;
+            const int co = c0 + cl;
+            const int64_t sp = s0 + pl;
+            GradPrep gp{0.f, 0.f, -1};
+            if (co < g.C_out && sp < n_pos) {
+                const int64_t b = sp / HoWo;
+                const int p = static_cast<int>(sp % HoWo);
+                const int64_t o = (b * g.C_out + co) * HoWo + p;
+                const int q = q_idx[o];
+                if (q >= 0) {  // silent neurons: no further loads
+                    const float gt = grad_t[o];
+                    if (gt != 0.f) gp = grad_prep(C, t_out[o], slope[o], q, gt);
+                }
+            }
+            sg[cl * kS + pl] = gp.gam;
+            su[cl * kS + pl] = gp.uq;
+            sq[cl * kS + pl] = gp.q;
+            if (gp.q >= 0) sl[pl] = 1;
+        }
+        __syncthreads();
+        for (int e = threadIdx.x; e < kGradPos * kGradCh; e += blockDim.x) {
+            const int pl = e / kGradCh, cl = e % kGradCh;
+            const int co = c0 + cl;
+            const int64_t sp = s0 + pl;
+            if (co < g.C_out && sp < n_pos) {
+                const int64_t d = sp * g.C_out + co;
+                gam[d] = sg[cl * kS + pl];
+                uq[d] = su[cl * kS + pl];
+                qv[d] = sq[cl * kS + pl];
+            }
+        }
+        __syncthreads();
     }
-    gam[t] = gp.gam;
-    uq[t] = gp.uq;
-    qv[t] = gp.q;
+    if (live && threadIdx.x < kGradPos && s0 + threadIdx.x < n_pos) live[s0 + threadIdx.x] = sl[threadIdx.x];
 }
 
-// live[s] = 1 if any channel at sample s = (b, p) passes gradient.
-__global__ __launch_bounds__(256) void conv_live_kernel(int64_t n_samp, int C_out,
-                                                        const int *__restrict__ qv,
-                                                        int *__restrict__ live) {
-    const int64_t s = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
-    if (s >= n_samp) return;
-    const int *q = qv + s * C_out;
-    int f = 0;
-    for (int c = 0; c < C_out; ++c) f |= (q[c] >= 0) ? 1 : 0;
-    live[s] = f;
+// dt_in = 0 for block blk's 1024 inputs (inputs with events are overwritten
+// by the gather afterwards)
+__device__ void zero_block(float *__restrict__ dt, int64_t n, int64_t blk) {
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        const int64_t i = blk * 1024 + k * 256 + threadIdx.x;
+        if (i < n) dt[i] = 0.f;
+    }
 }
 
 // dt_in partials. Wave = output position; lane = output channel, NT tiles of
@@ -510,11 +605,11 @@ __global__ __launch_bounds__(256) void conv_dtp_kernel(LifConst C, ConvGeom g, i
 }
 
 // dt_in of every input with events: the sum of its per-tap partials (taps
-// that reach no output position stay 0), written to its NCHW slot.
-__global__ __launch_bounds__(256) void conv_dt_gather_kernel(ConvGeom g, int R, int64_t n,
-                                                             ConvSorted cs,
-                                                             float *__restrict__ dt_in) {
-    const int64_t t = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+// that reach no output position stay 0), written to its NCHW slot. Block blk
+// of 256 threads takes record slots blk * 256 ...
+__device__ void dt_gather_block(const ConvGeom &g, int R, int64_t n, const ConvSorted &cs,
+                                float *__restrict__ dt_in, int64_t blk) {
+    const int64_t t = blk * blockDim.x + threadIdx.x;
     if (t >= n) return;
     const int64_t per = static_cast<int64_t>(g.Wp) * g.PC;
     const int64_t cr = t / per;
@@ -538,12 +633,14 @@ __global__ __launch_bounds__(256) void conv_dt_gather_kernel(ConvGeom g, int R, 
 // sums stay in registers over its share of the (b, p) samples. G[b, :, p,
 // tile] is computed in place from (gamma, t - T_q, q) -- each thread owns one
 // channel and a fixed set of rows; channels without gradient cost no
-// exponential -- and staged in LDS as (G[r], G[r+1]) pairs, double buffered,
-// the next sample's values in registers (NPER per thread) during this one's
-// sums. A sample whose tile is all zero is skipped.
+// exponential -- and staged in LDS as rows G[r][channel] of TI + 1 floats,
+// double buffered (an event's two halves G[r][i], G[r+1][i] are TI + 1 dwords
+// apart: one two-address LDS read; rows R-1 and R stay zero), the next
+// sample's values in registers (NPER per thread) during this one's sums. A
+// sample whose tile is all zero is skipped.
 template <int TI, int NPER>
 __global__ __launch_bounds__(256) void conv_dw_kernel(LifConst C, ConvGeom g, int64_t n_samp,
-                                                      int s_per_split, int pstride,
+                                                      int s_per_split,
                                                       const float *__restrict__ gam,
                                                       const float *__restrict__ uq,
                                                       const int *__restrict__ qv,
@@ -552,9 +649,11 @@ __global__ __launch_bounds__(256) void conv_dw_kernel(LifConst C, ConvGeom g, in
                                                       const float *__restrict__ ev_L,
                                                       const float *__restrict__ ev_R,
                                                       float *__restrict__ part) {
-    extern __shared__ float2 ps[];  // [2][TI][pstride], then the live sample list
+    extern __shared__ float gs[];  // [2][R + 1][TI + 1], then the live sample list
     __shared__ int n_live_w[4];
+    constexpr int kStr = TI + 1;
     const int R = rows_of(C);
+    const int gbuf = (R + 1) * kStr;
     const int NJ = g.KH * g.KW * g.C_in;
     const int jj = blockIdx.x * blockDim.x + threadIdx.x;
     const int co0 = blockIdx.y * TI;
@@ -587,22 +686,20 @@ __global__ __launch_bounds__(256) void conv_dw_kernel(LifConst C, ConvGeom g, in
         for (int c = 0; c < NPER; ++c) nz = nz || pre[c] != 0.f;
         return nz;
     };
-    auto store = [&](float2 *buf) {
+    auto store = [&](float *buf) {
 #pragma unroll
         for (int c = 0; c < NPER; ++c) {
             const int kk = threadIdx.x + c * 256;
             if (kk < total) {
                 const int r = kk / TI, l = kk % TI;
-                float2 *row = buf + l * pstride;
-                if (r < R - 1) row[r].x = pre[c];
-                if (r > 0) row[r - 1].y = pre[c];
+                if (r < R - 1) buf[r * kStr + l] = pre[c];
             }
         }
-        for (int l = threadIdx.x; l < TI; l += blockDim.x)
-            buf[l * pstride + R - 1] = make_float2(0.f, 0.f);
     };
+    for (int t = threadIdx.x; t < 2 * 2 * kStr; t += blockDim.x)
+        gs[(t / (2 * kStr)) * gbuf + (R - 1) * kStr + t % (2 * kStr)] = 0.f;
     // the split's samples through which any gradient flows, in order
-    int *list = reinterpret_cast<int *>(ps + 2 * TI * pstride);
+    int *list = reinterpret_cast<int *>(gs + 2 * gbuf);
     const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x >> 6;
     const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
     int n_live = 0;
@@ -621,12 +718,12 @@ __global__ __launch_bounds__(256) void conv_dw_kernel(LifConst C, ConvGeom g, in
     bool live = false;  // the staged sample's tile has a nonzero value
     if (n_live > 0) {
         live = fetch(s_lo + list[0]);
-        store(ps);
+        store(gs);
     }
     live = __syncthreads_or(live);
     for (int i = 0; i < n_live; ++i) {
         const int64_t s = s_lo + list[i];
-        float2 *cur = ps + (i & 1) * TI * pstride;
+        const float *cur = gs + (i & 1) * gbuf;
         const bool more = i + 1 < n_live;
         bool live_next = false;
         if (more) live_next = fetch(s_lo + list[i + 1]);
@@ -641,17 +738,15 @@ __global__ __launch_bounds__(256) void conv_dw_kernel(LifConst C, ConvGeom g, in
                     const int r = ev_row[e];
                     if (r >= 0) {
                         const float L = ev_L[e], Rv = ev_R[e];
-                        const float2 *q = cur + r;
+                        const float *q = cur + r * kStr;
 #pragma unroll
-                        for (int ii = 0; ii < TI; ++ii) {
-                            const float2 gg = q[ii * pstride];
-                            acc[ii] = fmaf(gg.x, L, fmaf(gg.y, Rv, acc[ii]));
-                        }
+                        for (int ii = 0; ii < TI; ++ii)
+                            acc[ii] = fmaf(q[ii], L, fmaf(q[ii + kStr], Rv, acc[ii]));
                     }
                 }
             }
         }
-        if (more) store(ps + ((i + 1) & 1) * TI * pstride);
+        if (more) store(gs + ((i + 1) & 1) * gbuf);
         live = __syncthreads_or(live_next);
     }
     if (!j_ok) return;
@@ -668,15 +763,13 @@ __global__ __launch_bounds__(256) void conv_dw_kernel(LifConst C, ConvGeom g, in
 // [co][ci][ky][kx] slot.
 constexpr int kRedOut = 32, kRedGrp = 8;
 
-__global__ __launch_bounds__(256) void conv_dw_reduce_kernel(ConvGeom g, int nsplit,
-                                                             const float *__restrict__ part,
-                                                             float *__restrict__ dW) {
-    __shared__ float red[kRedGrp][kRedOut];
+__device__ void dw_reduce_block(const ConvGeom &g, int nsplit, const float *__restrict__ part,
+                                float *__restrict__ dW, int64_t blk, float (*red)[kRedOut]) {
     const int KT = g.KH * g.KW;
     const int NJ = KT * g.C_in;
     const int64_t n = static_cast<int64_t>(g.C_out) * NJ;
     const int lo = threadIdx.x % kRedOut, h = threadIdx.x / kRedOut;
-    const int64_t src = static_cast<int64_t>(blockIdx.x) * kRedOut + lo;  // [co][k][ci]
+    const int64_t src = blk * kRedOut + lo;  // [co][k][ci]
     float s = 0.f;
     if (src < n) {
 #pragma unroll 8
@@ -694,39 +787,93 @@ __global__ __launch_bounds__(256) void conv_dw_reduce_kernel(ConvGeom g, int nsp
     }
 }
 
+// --------------------------------------------------------- fused launches --
+// Independent per-call work shares one launch by block role (a launch costs
+// several microseconds even when its work is tiny).
+// Forward set-up: blocks [0, n_sort) sort cell rows, the rest lay out WT.
+template <typename WT>
+__global__ __launch_bounds__(256) void conv_fprep_kernel(LifConst C, ConvGeom g, int n_sort,
+                                                         const float *__restrict__ t_in,
+                                                         ConvSorted cs, const WT *__restrict__ W,
+                                                         float *__restrict__ Wt) {
+    extern __shared__ int sh[];
+    const int blk = static_cast<int>(blockIdx.x);
+    if (blk < n_sort)
+        sort_cell_row(C, g, t_in, cs, CellEv{nullptr, nullptr, nullptr}, blk, sh);
+    else
+        weights_block<WT>(g, W, Wt, blk - n_sort);
+}
+
+// Backward set-up: [0, n_cr) cell rows (events for dW; with cs.key set also
+// the sort with derivatives), then n_gr blocks of gradient triples and live
+// flags, n_z blocks zeroing dt_in, and the WT layout.
+template <typename WT>
+__global__ __launch_bounds__(256) void conv_bprep_kernel(
+    LifConst C, ConvGeom g, int n_cr, int n_gr, int n_z, const float *__restrict__ t_in,
+    ConvSorted cs, CellEv ev, int64_t n_pos, const float *__restrict__ t_out,
+    const float *__restrict__ slope, const int *__restrict__ q_idx,
+    const float *__restrict__ grad_t, float *__restrict__ gam, float *__restrict__ uq,
+    int *__restrict__ qv, int *__restrict__ live, float *__restrict__ dt_in, int64_t n_in,
+    const WT *__restrict__ W, float *__restrict__ Wt) {
+    extern __shared__ int sh[];
+    int blk = static_cast<int>(blockIdx.x);
+    if (blk < n_cr) {
+        if (cs.key)
+            sort_cell_row(C, g, t_in, cs, ev, blk, sh);
+        else
+            events_cell_row(C, g, t_in, ev, blk);
+        return;
+    }
+    blk -= n_cr;
+    if (blk < n_gr) {
+        grad_block(C, g, n_pos, blk, t_out, slope, q_idx, grad_t, gam, uq, qv, live, sh);
+        return;
+    }
+    blk -= n_gr;
+    if (blk < n_z) {
+        zero_block(dt_in, n_in, blk);
+        return;
+    }
+    weights_block<WT>(g, W, Wt, blk - n_z);
+}
+
+// Backward finish: [0, n_red) dW split reduction, the rest gathers dt_in.
+__global__ __launch_bounds__(256) void conv_bfin_kernel(ConvGeom g, int R, int n_red, int nsplit,
+                                                        const float *__restrict__ part,
+                                                        float *__restrict__ dW, int64_t n_in,
+                                                        ConvSorted cs,
+                                                        float *__restrict__ dt_in) {
+    __shared__ float red[kRedGrp][kRedOut];
+    const int blk = static_cast<int>(blockIdx.x);
+    if (blk < n_red)
+        dw_reduce_block(g, nsplit, part, dW, blk, red);
+    else
+        dt_gather_block(g, R, n_in, cs, dt_in, blk - n_red);
+}
+
 // ------------------------------------------------------------ launchers --
 int conv_sort_lds_bytes(int M, const ConvGeom &g) {
-    return ((M + 3) * g.Wp + 256) * static_cast<int>(sizeof(int));
-}
-
-static hipError_t launch_conv_weights(const ConvGeom &g, const void *W, bool bf16, float *Wt,
-                                      hipStream_t st) {
-    const int64_t nw = static_cast<int64_t>(g.KH) * g.KW * g.C_in * g.C_out;
-    ProfScope prof("conv_weights", st);
-    const unsigned blocks = static_cast<unsigned>((nw + 255) / 256);
-    if (bf16)
-        hipLaunchKernelGGL(conv_weights_kernel<uint16_t>, dim3(blocks), dim3(256), 0, st, g,
-                           static_cast<const uint16_t *>(W), Wt);
-    else
-        hipLaunchKernelGGL(conv_weights_kernel<float>, dim3(blocks), dim3(256), 0, st, g,
-                           static_cast<const float *>(W), Wt);
-    return hipGetLastError();
-}
-
-static hipError_t launch_conv_sort(const LifConst &C, const ConvGeom &g, int64_t B,
-                                   const float *t_in, ConvSorted cs, hipStream_t st) {
-    ProfScope prof("conv_sort", st);
-    hipLaunchKernelGGL(conv_sort_kernel, dim3(static_cast<unsigned>(B * g.Hp)), dim3(256),
-                       conv_sort_lds_bytes(C.M, g), st, C, g, t_in, cs);
-    return hipGetLastError();
+    return ((M + 3) * g.Wp + 256 + sort_stage_floats(M, g)) * static_cast<int>(sizeof(int));
 }
 
 hipError_t launch_conv_forward(const LifConst &C, const ConvGeom &g, int64_t B, const void *W,
                                bool bf16, float *Wt, ConvSorted cs, const float *t_in,
                                float *t_out, float *slope, int *q_idx, hipStream_t st) {
-    hipError_t e = launch_conv_weights(g, W, bf16, Wt, st);
-    if (e != hipSuccess) return e;
-    if ((e = launch_conv_sort(C, g, B, t_in, cs, st)) != hipSuccess) return e;
+    const int64_t nw = static_cast<int64_t>(g.KH) * g.KW * g.C_in * g.C_out;
+    const int n_sort = static_cast<int>(B * g.Hp);
+    {
+        ProfScope prof("conv_fprep", st);
+        const unsigned blocks = static_cast<unsigned>(n_sort + (nw + 255) / 256);
+        const int lds = conv_sort_lds_bytes(C.M, g);
+        if (bf16)
+            hipLaunchKernelGGL(conv_fprep_kernel<uint16_t>, dim3(blocks), dim3(256), lds, st, C, g,
+                               n_sort, t_in, cs, static_cast<const uint16_t *>(W), Wt);
+        else
+            hipLaunchKernelGGL(conv_fprep_kernel<float>, dim3(blocks), dim3(256), lds, st, C, g,
+                               n_sort, t_in, cs, static_cast<const float *>(W), Wt);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
     const int64_t n_pos = B * g.Ho * g.Wo;
     constexpr int waves = 4;
     dim3 grid(static_cast<unsigned>((n_pos + waves - 1) / waves),
@@ -744,10 +891,11 @@ hipError_t launch_conv_forward(const LifConst &C, const ConvGeom &g, int64_t B, 
     return hipGetLastError();
 }
 
+// channel tile: 32 for narrow layers or where two 64-wide G buffers would
+// pass 48 KB of LDS
 static int conv_dw_ti(const ConvGeom &g, int M) {
-    const int ps = (M + 3) | 1;
-    const int ti_max = (ps * 63 * 8 < 65536) ? 64 : 32;  // LDS immediate offsets
-    return (g.C_out <= 32) ? 32 : ti_max;
+    if (g.C_out <= 32) return 32;
+    return (2 * (M + 4) * 65 * 4 <= 48 * 1024) ? 64 : 32;
 }
 
 static int conv_dw_nper(int M, int ti) {
@@ -782,74 +930,70 @@ hipError_t launch_conv_backward(const LifConst &C, const ConvGeom &g, int64_t B,
     const int R = C.M + 3;
     const int64_t n_in = B * g.Hp * g.Wp * g.PC;
     const int64_t n_pos = B * g.Ho * g.Wo;
+    const int64_t nj = static_cast<int64_t>(g.KH) * g.KW * g.C_in;
+    const bool dt = grad_t_in && n_in > 0;
     hipError_t e;
-    if (n_in > 0) {
-        ProfScope prof("conv_events", st);
-        hipLaunchKernelGGL(conv_events_kernel, dim3(static_cast<unsigned>((n_in + 255) / 256)),
-                           dim3(256), 0, st, C, g, n_in, t_in, ws.row, ws.L, ws.R, grad_t_in);
-        if ((e = hipGetLastError()) != hipSuccess) return e;
-    }
     {
-        // per neuron (gamma, t - T_q, q), position-major: G of both gradients
-        const int64_t n = n_pos * g.C_out;
-        ProfScope prof("conv_grad_prep", st);
-        if (n > 0)
-            hipLaunchKernelGGL(conv_grad_prep_kernel, dim3(static_cast<unsigned>((n + 255) / 256)),
-                               dim3(256), 0, st, C, g, n, t_out, slope, q_idx, grad_t, ws.gam,
-                               ws.uq, ws.q);
+        // cell rows (events; with dt_in the sort), gradient triples + live
+        // flags, and the WT layout for dt_in: one launch
+        const int n_cr = (n_in > 0 && (grad_W || dt)) ? static_cast<int>(B * g.Hp) : 0;
+        const int n_gr = static_cast<int>((n_pos + kGradPos - 1) / kGradPos);
+        const int64_t nw = nj * g.C_out;
+        const int n_wt = dt ? static_cast<int>((nw + 255) / 256) : 0;
+        const int n_z = dt ? static_cast<int>((n_in + 1023) / 1024) : 0;
+        const CellEv ev{grad_W ? ws.row : nullptr, ws.L, ws.R};
+        ConvSorted cs = ws.srt;
+        if (!dt) cs.key = nullptr;
+        int lds = kGradLdsBytes;
+        if (dt) lds = std::max(lds, conv_sort_lds_bytes(C.M, g));
+        const unsigned blocks = static_cast<unsigned>(n_cr + n_gr + n_z + n_wt);
+        ProfScope prof("conv_bprep", st);
+        if (blocks > 0) {
+            if (bf16)
+                hipLaunchKernelGGL(conv_bprep_kernel<uint16_t>, dim3(blocks), dim3(256), lds, st, C,
+                                   g, n_cr, n_gr, n_z, t_in, cs, ev, n_pos, t_out, slope, q_idx,
+                                   grad_t, ws.gam, ws.uq, ws.q, grad_W ? ws.live : nullptr,
+                                   grad_t_in, n_in, static_cast<const uint16_t *>(W), ws.wt);
+            else
+                hipLaunchKernelGGL(conv_bprep_kernel<float>, dim3(blocks), dim3(256), lds, st, C,
+                                   g, n_cr, n_gr, n_z, t_in, cs, ev, n_pos, t_out, slope, q_idx,
+                                   grad_t, ws.gam, ws.uq, ws.q, grad_W ? ws.live : nullptr,
+                                   grad_t_in, n_in, static_cast<const float *>(W), ws.wt);
+        }
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
+    ConvDwPlan p{};
     if (grad_W) {
-        ConvDwPlan p = plan_conv_dw(g, B, C.M);
-        const int64_t nj = static_cast<int64_t>(g.KH) * g.KW * g.C_in;
-        const int pstride = (C.M + 3) | 1;
+        p = plan_conv_dw(g, B, C.M);
         dim3 grid(static_cast<unsigned>((nj + 255) / 256),
                   static_cast<unsigned>((g.C_out + p.ti - 1) / p.ti),
                   static_cast<unsigned>(p.nsplit));
-        const size_t lds = 2 * static_cast<size_t>(p.ti) * pstride * sizeof(float2) +
+        const size_t lds = 2 * static_cast<size_t>(R + 1) * (p.ti + 1) * sizeof(float) +
                            static_cast<size_t>(p.s_per_split) * sizeof(int);
         const int nper = conv_dw_nper(C.M, p.ti);
-        if (n_pos > 0) {
-            ProfScope prof("conv_live", st);
-            hipLaunchKernelGGL(conv_live_kernel, dim3(static_cast<unsigned>((n_pos + 255) / 256)),
-                               dim3(256), 0, st, n_pos, g.C_out, ws.q, ws.live);
-            if ((e = hipGetLastError()) != hipSuccess) return e;
-        }
-        {
-            ProfScope prof("conv_dw", st);
+        ProfScope prof("conv_dw", st);
 #define CDW_LAUNCH(TIV, NP)                                                                   \
     hipLaunchKernelGGL((conv_dw_kernel<TIV, NP>), grid, dim3(256), lds, st, C, g, n_pos,       \
-                       p.s_per_split, pstride, ws.gam, ws.uq, ws.q, ws.live, ws.row, ws.L, ws.R, \
-                       ws.part)
-            if (p.ti == 64) {
-                if (nper == 5) CDW_LAUNCH(64, 5);
-                else if (nper == 9) CDW_LAUNCH(64, 9);
-                else if (nper == 17) CDW_LAUNCH(64, 17);
-                else CDW_LAUNCH(64, 33);
-            } else {
-                if (nper == 5) CDW_LAUNCH(32, 5);
-                else if (nper == 9) CDW_LAUNCH(32, 9);
-                else if (nper == 17) CDW_LAUNCH(32, 17);
-                else CDW_LAUNCH(32, 33);
-            }
-#undef CDW_LAUNCH
+                       p.s_per_split, ws.gam, ws.uq, ws.q, ws.live, ws.row, ws.L, ws.R, ws.part)
+        if (p.ti == 64) {
+            if (nper == 5) CDW_LAUNCH(64, 5);
+            else if (nper == 9) CDW_LAUNCH(64, 9);
+            else if (nper == 17) CDW_LAUNCH(64, 17);
+            else CDW_LAUNCH(64, 33);
+        } else {
+            if (nper == 5) CDW_LAUNCH(32, 5);
+            else if (nper == 9) CDW_LAUNCH(32, 9);
+            else if (nper == 17) CDW_LAUNCH(32, 17);
+            else CDW_LAUNCH(32, 33);
         }
-        if ((e = hipGetLastError()) != hipSuccess) return e;
-        const int64_t n = static_cast<int64_t>(g.C_out) * nj;
-        ProfScope prof("conv_dw_reduce", st);
-        hipLaunchKernelGGL(conv_dw_reduce_kernel,
-                           dim3(static_cast<unsigned>((n + kRedOut - 1) / kRedOut)),
-                           dim3(kRedOut * kRedGrp), 0, st, g, p.nsplit, ws.part, grad_W);
+#undef CDW_LAUNCH
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
-    if (grad_t_in && n_in > 0) {
-        if ((e = launch_conv_weights(g, W, bf16, ws.wt, st)) != hipSuccess) return e;
-        if ((e = launch_conv_sort(C, g, B, t_in, ws.srt, st)) != hipSuccess) return e;
-        if (n_pos > 0) {
-            constexpr int waves = 4;
-            dim3 grid(static_cast<unsigned>((n_pos + waves - 1) / waves));
-            const int nt = (g.C_out + kWave - 1) / kWave;
-            ProfScope prof("conv_dtp", st);
+    if (dt && n_pos > 0) {
+        constexpr int waves = 4;
+        dim3 grid(static_cast<unsigned>((n_pos + waves - 1) / waves));
+        const int nt = (g.C_out + kWave - 1) / kWave;
+        ProfScope prof("conv_dtp", st);
 #define DTP_LAUNCH(KHV, NTV)                                                                  \
     hipLaunchKernelGGL((conv_dtp_kernel<KHV, NTV>), grid, dim3(waves * kWave), 0, st, C, g,    \
                        n_pos, ws.wt, ws.srt, ws.gam, ws.uq, ws.q)
@@ -860,16 +1004,23 @@ hipError_t launch_conv_backward(const LifConst &C, const ConvGeom &g, int64_t B,
         else if (nt <= 4) DTP_LAUNCH(KHV, 4);     \
         else DTP_LAUNCH(KHV, 8);                  \
     } while (0)
-            if (g.KH == 1) DTP_NT(1);
-            else if (g.KH <= 3) DTP_NT(3);
-            else DTP_NT(kConvMaxK);
+        if (g.KH == 1) DTP_NT(1);
+        else if (g.KH <= 3) DTP_NT(3);
+        else DTP_NT(kConvMaxK);
 #undef DTP_NT
 #undef DTP_LAUNCH
-            if ((e = hipGetLastError()) != hipSuccess) return e;
-        }
-        ProfScope prof("conv_dt_gather", st);
-        hipLaunchKernelGGL(conv_dt_gather_kernel, dim3(static_cast<unsigned>((n_in + 255) / 256)),
-                           dim3(256), 0, st, g, R, n_in, ws.srt, grad_t_in);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
+    {
+        // dW split reduction and dt_in gather: one launch
+        const int64_t n = static_cast<int64_t>(g.C_out) * nj;
+        const int n_red = grad_W ? static_cast<int>((n + kRedOut - 1) / kRedOut) : 0;
+        const int n_ga = dt ? static_cast<int>((n_in + 255) / 256) : 0;
+        ProfScope prof("conv_bfin", st);
+        if (n_red + n_ga > 0)
+            hipLaunchKernelGGL(conv_bfin_kernel, dim3(static_cast<unsigned>(n_red + n_ga)),
+                               dim3(256), 0, st, g, R, n_red, p.nsplit, ws.part, grad_W, n_in,
+                               ws.srt, grad_t_in);
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     return hipSuccess;

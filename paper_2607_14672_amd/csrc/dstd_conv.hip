@@ -337,6 +337,15 @@ struct PosWalk {
 
 // -------------------------------------------------------------- forward --
 // Wave = one output position, lane = output channel of a 64-wide tile.
+// The position's records, in the order the sums need them (event row, then
+// kernel row, then bucket order), form a virtual list: lanes = event rows
+// hold the KH segment bounds of their row and an exclusive prefix of the
+// row counts; for 64 list entries at a time each lane finds its entry's row
+// (binary search over the prefix with lane shuffles), its segment and its
+// record, and loads the record's fields with one vector load each. The
+// entries are then summed one by one (weight rows loaded 8 at a time), and
+// rows close into the interval scan as the row changes. Sums and their
+// order are those of a row-by-row walk.
 template <int KHT>
 __global__ __launch_bounds__(256) void conv_fwd_kernel(LifConst C, ConvGeom g, int64_t n_pos,
                                                        const float *__restrict__ Wt,
@@ -366,67 +375,109 @@ __global__ __launch_bounds__(256) void conv_fwd_kernel(LifConst C, ConvGeom g, i
         Wt, static_cast<uint32_t>(static_cast<int64_t>(wk.wlim + 1) * g.C_out * sizeof(float)));
     const int voff = (row_ok ? co : 0) * static_cast<int>(sizeof(float));
     const int rstride = g.C_out * static_cast<int>(sizeof(float));
+    auto rdl = [](float v, int k) {
+        return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), k));
+    };
     Scan sc;
     float aL = 0.f, aR = 0.f, carry = 0.f;
-    for (int r = 0; r <= R - 2; ++r) {
-        if ((r & (kWave - 1)) == 0) wk.load_offs(g, cs, R, r, lane);
-        int s0[KHT], n0[KHT];
-        if (wk.segments(r, s0, n0) > 0) {
-            // first batch of every kernel row issued together
-            float w[KHT][kCBatch], lv[KHT][kCBatch], rv[KHT][kCBatch];
+    int cur = 0;  // row being summed
+    // close rows cur .. target-1: point r-1 gets row r's L sums plus row
+    // r-1's R sums
+    auto close_to = [&](int target) {
+        while (cur < target) {
+            if (cur >= 1) sc.step(C, cur - 1, aL + carry);
+            carry = aR;
+            aL = 0.f;
+            aR = 0.f;
+            ++cur;
+        }
+    };
+    bool done = false;
+    for (int r0 = 0; r0 <= R - 2 && !done; r0 += kWave) {
+        wk.load_offs(g, cs, R, r0, lane);
+        const bool rvalid = r0 + lane <= R - 2;
+        int n0[KHT];
+        int nr = 0;
 #pragma unroll
-            for (int ky = 0; ky < KHT; ++ky) {
-                const int64_t o = wk.recb[ky] + s0[ky];
+        for (int ky = 0; ky < KHT; ++ky) {
+            n0[ky] = rvalid ? wk.ob[ky] - wk.oa[ky] : 0;
+            nr += n0[ky];
+        }
+        int inc = nr;
 #pragma unroll
-                for (int kk = 0; kk < kCBatch; ++kk) {
-                    w[ky][kk] = BufLoad<float>::get(wr, voff,
-                                                    wk.wrow(as_const(cs.key + o)[kk], ky, rstride));
-                    lv[ky][kk] = as_const(cs.L + o)[kk];
-                    rv[ky][kk] = as_const(cs.R + o)[kk];
-                }
+        for (int m = 1; m < kWave; m <<= 1) {
+            const int o = __shfl_up(inc, m);
+            if (lane >= m) inc += o;
+        }
+        const int start = inc - nr;
+        const int start_eff = rvalid ? start : 0x7fffffff;
+        const int total = uniform(__builtin_amdgcn_readlane(inc, kWave - 1));
+        for (int c0 = 0; c0 < total && !done; c0 += kWave) {
+            const int v = c0 + lane;
+            const bool rec_ok = v < total;
+            // row lane lo: the last row whose prefix start is <= v
+            int lo = 0;
+#pragma unroll
+            for (int step = kWave / 2; step >= 1; step >>= 1) {
+                const int cand = lo + step;
+                const int sv = __shfl(start_eff, cand & (kWave - 1));
+                if (cand < kWave && sv <= v) lo = cand;
             }
+            int kk = v - __shfl(start, lo);
+            int sel = -1, ridx = 0;
 #pragma unroll
             for (int ky = 0; ky < KHT; ++ky) {
-#pragma unroll
-                for (int kk = 0; kk < kCBatch; ++kk) {
-                    if (kk < n0[ky]) {
-                        aL = fmaf(w[ky][kk], lv[ky][kk], aL);
-                        aR = fmaf(w[ky][kk], rv[ky][kk], aR);
+                const int a = __shfl(wk.oa[ky], lo), nn = __shfl(n0[ky], lo);
+                if (sel < 0) {
+                    if (kk < nn) {
+                        sel = ky;
+                        ridx = a + kk;
+                    } else {
+                        kk -= nn;
                     }
                 }
             }
-            // long segments: further batches
+            int64_t gi = 0;
+            int wof = 0;
 #pragma unroll
             for (int ky = 0; ky < KHT; ++ky) {
-                for (int k0 = kCBatch; k0 < n0[ky]; k0 += kCBatch) {
-                    const int64_t o = wk.recb[ky] + s0[ky] + k0;
-                    const int nk = n0[ky] - k0;
-                    float wb[kCBatch], lb[kCBatch], rb[kCBatch];
+                if (sel == ky) {
+                    gi = wk.recb[ky] + ridx;
+                    wof = wk.wofs[ky];
+                }
+            }
+            const bool ok = rec_ok && sel >= 0;
+            const int key = ok ? cs.key[gi] : 0;
+            const float Lv = ok ? cs.L[gi] : 0.f;
+            const float Rv = ok ? cs.R[gi] : 0.f;
+            const int wb = min(max(key + wof, 0), wk.wlim) * rstride;
+            const int rrow = r0 + lo;
+            const int nc = min(kWave, total - c0);
+            for (int s0 = 0; s0 < nc; s0 += kCBatch) {
+                float w[kCBatch];
 #pragma unroll
-                    for (int kk = 0; kk < kCBatch; ++kk) {
-                        wb[kk] = BufLoad<float>::get(wr, voff,
-                                                     wk.wrow(as_const(cs.key + o)[kk], ky, rstride));
-                        lb[kk] = as_const(cs.L + o)[kk];
-                        rb[kk] = as_const(cs.R + o)[kk];
-                    }
+                for (int q = 0; q < kCBatch; ++q)
+                    w[q] = BufLoad<float>::get(wr, voff, __builtin_amdgcn_readlane(wb, s0 + q));
 #pragma unroll
-                    for (int kk = 0; kk < kCBatch; ++kk) {
-                        if (kk < nk) {
-                            aL = fmaf(wb[kk], lb[kk], aL);
-                            aR = fmaf(wb[kk], rb[kk], aR);
+                for (int q = 0; q < kCBatch; ++q) {
+                    if (s0 + q < nc) {
+                        const int row = __builtin_amdgcn_readlane(rrow, s0 + q);
+                        if (row != cur) {
+                            close_to(row);
+                            if (__all(sc.found() || !row_ok)) {
+                                done = true;
+                                break;
+                            }
                         }
+                        aL = fmaf(w[q], rdl(Lv, s0 + q), aL);
+                        aR = fmaf(w[q], rdl(Rv, s0 + q), aR);
                     }
                 }
+                if (done) break;
             }
         }
-        // row r closes: grid point m = r - 1 gets its L sums plus the
-        // previous row's R sums
-        if (r >= 1) sc.step(C, r - 1, aL + carry);
-        carry = aR;
-        aL = 0.f;
-        aR = 0.f;
-        if (__all(sc.found() || !row_ok)) break;
     }
+    if (!done) close_to(R - 1);
     if (!row_ok) return;
     float to, sl;
     int q;

@@ -210,6 +210,75 @@ dstd_status dstd_softmax_ce_grad(int64_t B, int64_t N, const float *t_out, const
 dstd_status dstd_mse_grad(int64_t B, int64_t N, const float *t_out, const float *target,
                           float *grad_t, float *loss, void *stream);
 
+/* ------------------------------------------------------ synfire terms -- */
+
+/*
+ * Synfire-chain training terms of one layer (App. C.1, Eqs.
+ * (temporal_penalty) and (dead_neuron_penalty)), for the outputs t of the
+ * layer's forward pass.
+ *  Temporal penalty  T = scale * sum over neurons that fire (t finite) of
+ *      gamma_head (t - t_head)^2 [t < t_head] + gamma_tail (t - t_tail)^2 [t > t_tail];
+ *    silent neurons (t = +inf) contribute nothing (the paper's dead-neuron
+ *    term exists because T gives them no gradient).
+ *  Dead-neuron term  Q = -gamma_q * scale * sum over silent neurons of the
+ *      sum of their weight row (dense: row i of W; conv: all weights of the
+ *      neuron's output channel), so dQ/dw_ij = -gamma_q * scale * (number of
+ *      silent neurons that row i feeds).
+ * t_head, t_tail are this layer's window ends, l * tau_shift + t_head and
+ * l * tau_shift + tau_width - t_tail in the paper's hyperparameters (the
+ * caller forms them). scale folds the mini-batch mean and, for conv layers,
+ * the division by the spatial size: 1/B (dense) or 1/(B * H_out * W_out).
+ * All gammas >= 0 and finite, t_head and t_tail finite, scale > 0 and finite
+ * (DSTD_ERR_PARAM otherwise).
+ */
+typedef struct {
+    float gamma_head, gamma_tail;
+    float t_head, t_tail;
+    float gamma_q;
+    float scale;
+} dstd_synfire_params;
+
+/*
+ * Backward passes with the synfire terms: as dstd_lif_backward /
+ * dstd_lif_conv_backward (same workspace size), except that each firing
+ * neuron's gradient is grad_t_out + dT/dt (added inside the kernels that
+ * build the per-neuron gradient), and grad_W additionally holds dQ/dW
+ * (added where the dW sums are written). sp = NULL gives the plain
+ * backward; all gammas zero give the plain backward's results bit for bit.
+ */
+dstd_status dstd_lif_backward_synfire(const dstd_lif_params *p, const dstd_synfire_params *sp,
+                                      int64_t B, int64_t N_in, int64_t N_out,
+                                      const float *t_in, const void *W, dstd_dtype w_dtype,
+                                      const float *t_out, const float *slope,
+                                      const int32_t *q_idx, const float *grad_t_out,
+                                      float *grad_W, float *grad_t_in, void *ws,
+                                      size_t ws_bytes, void *stream);
+dstd_status dstd_lif_conv_backward_synfire(const dstd_lif_params *p, const dstd_synfire_params *sp,
+                                           const dstd_conv_shape *cs, int64_t B,
+                                           const float *t_in, const void *W, dstd_dtype w_dtype,
+                                           const float *t_out, const float *slope,
+                                           const int32_t *q_idx, const float *grad_t_out,
+                                           float *grad_W, float *grad_t_in, void *ws,
+                                           size_t ws_bytes, void *stream);
+
+/*
+ * Values of the two terms (for reporting; the gradients come from the
+ * backward calls above). The layer's outputs are t_out [B][rows][spatial]
+ * (dense: rows = N_out, spatial = 1; conv NCHW: rows = C_out, spatial =
+ * H_out * W_out); W holds rows x row_len weights, row-major (dense [N_out]
+ * [N_in]; conv [C_out][C_in * KH * KW]), fp32 or bf16.
+ *  value [2] out (device floats): value[0] = T, value[1] = Q, each summed in
+ *  a fixed order (bitwise reproducible).
+ * Workspace: dstd_synfire_penalty_workspace_size(B, rows, spatial) bytes,
+ * 256-byte aligned. B, rows, spatial >= 0 with per-layer element counts
+ * below 2^31; rows * row_len below 2^31.
+ */
+size_t dstd_synfire_penalty_workspace_size(int64_t B, int64_t rows, int64_t spatial);
+dstd_status dstd_synfire_penalty(const dstd_synfire_params *sp, int64_t B, int64_t rows,
+                                 int64_t spatial, int64_t row_len, const float *t_out,
+                                 const void *W, dstd_dtype w_dtype, float *value, void *ws,
+                                 size_t ws_bytes, void *stream);
+
 /* ------------------------------------------------------------ profiling -- */
 
 /*

@@ -16,3 +16,4 @@ from .oracle import (  # noqa: F401
     conv_backward,
     num_threads,
 )
+from .synfire import window, temporal_penalty, dead_neuron_penalty  # noqa: F401

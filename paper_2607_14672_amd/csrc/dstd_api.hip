@@ -112,7 +112,7 @@ dstd_status check_dims(int64_t B, int64_t N_in, int64_t N_out) {
 }
 
 struct DenseWs {
-    size_t row, L, R, gam, uq, q, part, wt, sj, sr, sL, sR, nvalid, rs, total;
+    size_t row, L, R, gam, uq, q, part, dq, wt, sj, sr, sL, sR, nvalid, rs, total;
     int64_t sstride;
 };
 
@@ -142,6 +142,7 @@ DenseWs dense_ws_layout(int M, int64_t B, int64_t N_in, int64_t N_out, bool back
         w.gam = off; off += align_up((size_t)B * (size_t)N_out * sizeof(float));
         w.uq = off; off += align_up((size_t)B * (size_t)N_out * sizeof(float));
         w.q = off; off += align_up((size_t)B * (size_t)N_out * sizeof(int));
+        w.dq = off; off += align_up((size_t)N_out * sizeof(float));  // dead-neuron term per row
         dstd::DwPlan dp = dstd::plan_dw(B, N_in, N_out, M);
         w.part = off;
         if (dp.nsplit > 1) off += align_up((size_t)dp.nsplit * (size_t)N_out * (size_t)N_in * sizeof(float));
@@ -216,7 +217,7 @@ dstd_status check_conv(const dstd_conv_shape *cs, int64_t B, int M, dstd::ConvGe
 struct ConvWs {
     size_t wt, key, L, R, off;                        // both passes
     size_t px, src, P;                                // backward sort extras
-    size_t row, eL, eR, gam, uq, q, live, part;       // backward
+    size_t row, eL, eR, gam, uq, q, live, part, dq;   // backward
     size_t total;
 };
 
@@ -247,12 +248,52 @@ ConvWs conv_ws_layout(int M, const dstd::ConvGeom &g, int64_t B, bool backward) 
         w.uq = off; off += align_up(nout * sizeof(float));
         w.q = off; off += align_up(nout * sizeof(int));
         w.live = off; off += align_up((size_t)B * g.Ho * g.Wo * sizeof(int));
+        w.dq = off; off += align_up((size_t)g.C_out * sizeof(float));  // dead-neuron term per channel
         dstd::ConvDwPlan dp = dstd::plan_conv_dw(g, B, M);
         w.part = off; off += align_up((size_t)dp.nsplit * nw * sizeof(float));
     }
     w.total = off;
     return w;
 }
+
+// Synfire terms of a backward call (NULL: off).
+dstd_status check_synfire(const dstd_synfire_params *sp) {
+    if (!sp) return DSTD_OK;
+    const float g[3] = {sp->gamma_head, sp->gamma_tail, sp->gamma_q};
+    for (float v : g)
+        if (!(isfinite(v) && v >= 0.f))
+            return fail(DSTD_ERR_PARAM, "synfire gammas must be finite and >= 0");
+    if (!isfinite(sp->t_head) || !isfinite(sp->t_tail))
+        return fail(DSTD_ERR_PARAM, "synfire t_head and t_tail must be finite");
+    if (!(isfinite(sp->scale) && sp->scale > 0.f))
+        return fail(DSTD_ERR_PARAM, "synfire scale must be finite and > 0");
+    return DSTD_OK;
+}
+
+dstd::Synfire make_synfire(const dstd_synfire_params *sp, float *dq) {
+    dstd::Synfire f{};
+    if (!sp) return f;
+    f.on = 1;
+    f.gh = sp->gamma_head;
+    f.gt = sp->gamma_tail;
+    f.th = sp->t_head;
+    f.tt = sp->t_tail;
+    f.gq = sp->gamma_q;
+    f.scale = sp->scale;
+    f.dq = dq;
+    return f;
+}
+
+dstd_status dense_backward(const dstd_lif_params *p, const dstd_synfire_params *sp, int64_t B,
+                           int64_t N_in, int64_t N_out, const float *t_in, const void *W,
+                           dstd_dtype w_dtype, const float *t_out, const float *slope,
+                           const int32_t *q_idx, const float *grad_t_out, float *grad_W,
+                           float *grad_t_in, void *ws, size_t ws_bytes, void *stream);
+dstd_status conv_backward(const dstd_lif_params *p, const dstd_synfire_params *sp,
+                          const dstd_conv_shape *cs, int64_t B, const float *t_in, const void *W,
+                          dstd_dtype w_dtype, const float *t_out, const float *slope,
+                          const int32_t *q_idx, const float *grad_t_out, float *grad_W,
+                          float *grad_t_in, void *ws, size_t ws_bytes, void *stream);
 
 }  // namespace
 
@@ -317,8 +358,32 @@ dstd_status dstd_lif_backward(const dstd_lif_params *p, int64_t B, int64_t N_in,
                               const float *t_out, const float *slope, const int32_t *q_idx,
                               const float *grad_t_out, float *grad_W, float *grad_t_in, void *ws,
                               size_t ws_bytes, void *stream) {
+    return dense_backward(p, nullptr, B, N_in, N_out, t_in, W, w_dtype, t_out, slope, q_idx,
+                          grad_t_out, grad_W, grad_t_in, ws, ws_bytes, stream);
+}
+
+dstd_status dstd_lif_backward_synfire(const dstd_lif_params *p, const dstd_synfire_params *sp,
+                                      int64_t B, int64_t N_in, int64_t N_out, const float *t_in,
+                                      const void *W, dstd_dtype w_dtype, const float *t_out,
+                                      const float *slope, const int32_t *q_idx,
+                                      const float *grad_t_out, float *grad_W, float *grad_t_in,
+                                      void *ws, size_t ws_bytes, void *stream) {
+    return dense_backward(p, sp, B, N_in, N_out, t_in, W, w_dtype, t_out, slope, q_idx,
+                          grad_t_out, grad_W, grad_t_in, ws, ws_bytes, stream);
+}
+
+}  // extern "C"
+
+namespace {
+
+dstd_status dense_backward(const dstd_lif_params *p, const dstd_synfire_params *sp, int64_t B,
+                           int64_t N_in, int64_t N_out, const float *t_in, const void *W,
+                           dstd_dtype w_dtype, const float *t_out, const float *slope,
+                           const int32_t *q_idx, const float *grad_t_out, float *grad_W,
+                           float *grad_t_in, void *ws, size_t ws_bytes, void *stream) {
     dstd_status s = check_params(p);
     if (s != DSTD_OK) return s;
+    if ((s = check_synfire(sp)) != DSTD_OK) return s;
     if ((s = check_dims(B, N_in, N_out)) != DSTD_OK) return s;
     if (w_dtype != DSTD_F32 && w_dtype != DSTD_BF16)
         return fail(DSTD_ERR_PARAM, "unknown weight dtype %d", (int)w_dtype);
@@ -348,9 +413,14 @@ dstd_status dstd_lif_backward(const dstd_lif_params *p, int64_t B, int64_t N_in,
     bw.q = at<int>(ws, L.q);
     bw.part = at<float>(ws, L.part);
     e = dstd::launch_backward(C, B, N_in, N_out, W, w_dtype == DSTD_BF16, t_in, t_out, slope,
-                              q_idx, grad_t_out, bw, grad_W, grad_t_in, st);
+                              q_idx, grad_t_out, bw, grad_W, grad_t_in,
+                              make_synfire(sp, at<float>(ws, L.dq)), st);
     return hip_status(e, "backward launch");
 }
+
+}  // namespace
+
+extern "C" {
 
 dstd_status dstd_softmax_ce_grad(int64_t B, int64_t N, const float *t_out, const int32_t *labels,
                                  float tau_soft, float t_cap, float *grad_t, float *loss,
@@ -420,8 +490,66 @@ dstd_status dstd_lif_conv_backward(const dstd_lif_params *p, const dstd_conv_sha
                                    const float *t_out, const float *slope, const int32_t *q_idx,
                                    const float *grad_t_out, float *grad_W, float *grad_t_in,
                                    void *ws, size_t ws_bytes, void *stream) {
+    return conv_backward(p, nullptr, cs, B, t_in, W, w_dtype, t_out, slope, q_idx, grad_t_out,
+                         grad_W, grad_t_in, ws, ws_bytes, stream);
+}
+
+dstd_status dstd_lif_conv_backward_synfire(const dstd_lif_params *p, const dstd_synfire_params *sp,
+                                           const dstd_conv_shape *cs, int64_t B,
+                                           const float *t_in, const void *W, dstd_dtype w_dtype,
+                                           const float *t_out, const float *slope,
+                                           const int32_t *q_idx, const float *grad_t_out,
+                                           float *grad_W, float *grad_t_in, void *ws,
+                                           size_t ws_bytes, void *stream) {
+    return conv_backward(p, sp, cs, B, t_in, W, w_dtype, t_out, slope, q_idx, grad_t_out,
+                         grad_W, grad_t_in, ws, ws_bytes, stream);
+}
+
+size_t dstd_synfire_penalty_workspace_size(int64_t B, int64_t rows, int64_t spatial) {
+    if (B < 0 || rows < 0 || spatial < 0) return 0;
+    const int64_t n_tb = dstd::synfire_value_blocks(B * rows * spatial);
+    return align_up((size_t)(rows + n_tb) * sizeof(float));
+}
+
+dstd_status dstd_synfire_penalty(const dstd_synfire_params *sp, int64_t B, int64_t rows,
+                                 int64_t spatial, int64_t row_len, const float *t_out,
+                                 const void *W, dstd_dtype w_dtype, float *value, void *ws,
+                                 size_t ws_bytes, void *stream) {
+    if (!sp || !value) return fail(DSTD_ERR_NULL, "synfire parameters and value are required");
+    dstd_status s = check_synfire(sp);
+    if (s != DSTD_OK) return s;
+    if (B < 0 || rows < 0 || spatial < 0 || row_len < 0)
+        return fail(DSTD_ERR_SHAPE, "sizes must be >= 0");
+    const int64_t lim = (int64_t)1 << 31;
+    if (B > 0 && rows > 0 && spatial > 0 && B * rows * spatial >= lim)
+        return fail(DSTD_ERR_SHAPE, "B * rows * spatial must be < 2^31");
+    if (rows > 0 && row_len > 0 && rows * row_len >= lim)
+        return fail(DSTD_ERR_SHAPE, "rows * row_len must be < 2^31");
+    if (w_dtype != DSTD_F32 && w_dtype != DSTD_BF16)
+        return fail(DSTD_ERR_PARAM, "unknown weight dtype %d", (int)w_dtype);
+    if (B * rows * spatial > 0 && !t_out) return fail(DSTD_ERR_NULL, "t_out is NULL");
+    if (rows * row_len > 0 && !W) return fail(DSTD_ERR_NULL, "W is NULL");
+    if ((s = check_ws(ws, ws_bytes, dstd_synfire_penalty_workspace_size(B, rows, spatial))) != DSTD_OK)
+        return s;
+    hipError_t e = dstd::launch_synfire_value(make_synfire(sp, nullptr), B, rows, spatial, row_len,
+                                              t_out, W, w_dtype == DSTD_BF16,
+                                              static_cast<float *>(ws), value,
+                                              static_cast<hipStream_t>(stream));
+    return hip_status(e, "synfire value launch");
+}
+
+}  // extern "C"
+
+namespace {
+
+dstd_status conv_backward(const dstd_lif_params *p, const dstd_synfire_params *sp,
+                          const dstd_conv_shape *cs, int64_t B, const float *t_in, const void *W,
+                          dstd_dtype w_dtype, const float *t_out, const float *slope,
+                          const int32_t *q_idx, const float *grad_t_out, float *grad_W,
+                          float *grad_t_in, void *ws, size_t ws_bytes, void *stream) {
     dstd_status s = check_params(p);
     if (s != DSTD_OK) return s;
+    if ((s = check_synfire(sp)) != DSTD_OK) return s;
     dstd::ConvGeom g;
     if ((s = check_conv(cs, B, p->M, &g)) != DSTD_OK) return s;
     if (w_dtype != DSTD_F32 && w_dtype != DSTD_BF16)
@@ -451,8 +579,9 @@ dstd_status dstd_lif_conv_backward(const dstd_lif_params *p, const dstd_conv_sha
     // With B == 0 the dW kernel still runs (one empty split) and writes zeros.
     hipError_t e = dstd::launch_conv_backward(C, g, B, W, w_dtype == DSTD_BF16, t_in, t_out, slope,
                                               q_idx, grad_t_out, bw, grad_W, grad_t_in,
+                                              make_synfire(sp, at<float>(ws, L.dq)),
                                               static_cast<hipStream_t>(stream));
     return hip_status(e, "conv backward launch");
 }
 
-}  // extern "C"
+}  // namespace

@@ -499,8 +499,8 @@ constexpr int kGradLdsBytes = (3 * kGradCh * (kGradPos + 1) + kGradPos) * 4;
 __device__ void grad_block(const LifConst &C, const ConvGeom &g, int64_t n_pos, int64_t blk,
                            const float *__restrict__ t_out, const float *__restrict__ slope,
                            const int *__restrict__ q_idx, const float *__restrict__ grad_t,
-                           float *__restrict__ gam, float *__restrict__ uq, int *__restrict__ qv,
-                           int *__restrict__ live, int *sh) {
+                           const Synfire &sf, float *__restrict__ gam, float *__restrict__ uq,
+                           int *__restrict__ qv, int *__restrict__ live, int *sh) {
     constexpr int kS = kGradPos + 1;
     float *sg = reinterpret_cast<float *>(sh);
     float *su = sg + kGradCh * kS;
@@ -522,8 +522,10 @@ __device__ void grad_block(const LifConst &C, const ConvGeom &g, int64_t n_pos, 
                 const int64_t o = (b * g.C_out + co) * HoWo + p;
                 const int q = q_idx[o];
                 if (q >= 0) {  // silent neurons: no further loads
-                    const float gt = grad_t[o];
-                    if (gt != 0.f) gp = grad_prep(C, t_out[o], slope[o], q, gt);
+                    float gt = grad_t[o];
+                    const float t = t_out[o];
+                    if (sf.on) gt += synfire_dt(sf, t);
+                    if (gt != 0.f) gp = grad_prep(C, t, slope[o], q, gt);
                 }
             }
             sg[cl * kS + pl] = gp.gam;
@@ -546,6 +548,28 @@ __device__ void grad_block(const LifConst &C, const ConvGeom &g, int64_t n_pos, 
         __syncthreads();
     }
     if (live && threadIdx.x < kGradPos && s0 + threadIdx.x < n_pos) live[s0 + threadIdx.x] = sl[threadIdx.x];
+}
+
+// Dead-neuron term of output channel co: dq[co] = -gamma_q * scale * (number
+// of silent (b, position) outputs of the channel); integer counts, so the
+// block sum is exact.
+__device__ void dead_channel_block(const ConvGeom &g, int64_t B, const int *__restrict__ q_idx,
+                                   const Synfire &sf, int co, int *sh) {
+    const int HoWo = g.Ho * g.Wo;
+    const int64_t n = B * HoWo;
+    int cnt = 0;
+    for (int64_t e = threadIdx.x; e < n; e += blockDim.x) {
+        const int64_t b = e / HoWo;
+        const int p = static_cast<int>(e % HoWo);
+        cnt += (q_idx[(b * g.C_out + co) * HoWo + p] < 0) ? 1 : 0;
+    }
+    sh[threadIdx.x] = cnt;
+    __syncthreads();
+    for (int h = blockDim.x / 2; h > 0; h >>= 1) {
+        if (static_cast<int>(threadIdx.x) < h) sh[threadIdx.x] += sh[threadIdx.x + h];
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) sf.dq[co] = -(sf.gq * sf.scale * static_cast<float>(sh[0]));
 }
 
 // dt_in = 0 for block blk's 1024 inputs (inputs with events are overwritten
@@ -815,7 +839,8 @@ __global__ __launch_bounds__(256) void conv_dw_kernel(LifConst C, ConvGeom g, in
 constexpr int kRedOut = 32, kRedGrp = 8;
 
 __device__ void dw_reduce_block(const ConvGeom &g, int nsplit, const float *__restrict__ part,
-                                float *__restrict__ dW, int64_t blk, float (*red)[kRedOut]) {
+                                const float *__restrict__ dq, float *__restrict__ dW, int64_t blk,
+                                float (*red)[kRedOut]) {
     const int KT = g.KH * g.KW;
     const int NJ = KT * g.C_in;
     const int64_t n = static_cast<int64_t>(g.C_out) * NJ;
@@ -834,7 +859,8 @@ __device__ void dw_reduce_block(const ConvGeom &g, int nsplit, const float *__re
         const int co = static_cast<int>(src / NJ);
         const int rem = static_cast<int>(src % NJ);
         const int k = rem / g.C_in, ci = rem % g.C_in;
-        dW[(static_cast<int64_t>(co) * g.C_in + ci) * KT + k] = tot * g.inv_P;
+        const float v = tot * g.inv_P;
+        dW[(static_cast<int64_t>(co) * g.C_in + ci) * KT + k] = dq ? v + dq[co] : v;
     }
 }
 
@@ -857,15 +883,16 @@ __global__ __launch_bounds__(256) void conv_fprep_kernel(LifConst C, ConvGeom g,
 
 // Backward set-up: [0, n_cr) cell rows (events for dW; with cs.key set also
 // the sort with derivatives), then n_gr blocks of gradient triples and live
-// flags, n_z blocks zeroing dt_in, and the WT layout.
+// flags, n_z blocks zeroing dt_in, n_dq blocks of dead-neuron terms (one per
+// channel, synfire terms on) and the WT layout.
 template <typename WT>
 __global__ __launch_bounds__(256) void conv_bprep_kernel(
-    LifConst C, ConvGeom g, int n_cr, int n_gr, int n_z, const float *__restrict__ t_in,
+    LifConst C, ConvGeom g, int n_cr, int n_gr, int n_z, int n_dq, const float *__restrict__ t_in,
     ConvSorted cs, CellEv ev, int64_t n_pos, const float *__restrict__ t_out,
     const float *__restrict__ slope, const int *__restrict__ q_idx,
-    const float *__restrict__ grad_t, float *__restrict__ gam, float *__restrict__ uq,
-    int *__restrict__ qv, int *__restrict__ live, float *__restrict__ dt_in, int64_t n_in,
-    const WT *__restrict__ W, float *__restrict__ Wt) {
+    const float *__restrict__ grad_t, Synfire sf, float *__restrict__ gam,
+    float *__restrict__ uq, int *__restrict__ qv, int *__restrict__ live,
+    float *__restrict__ dt_in, int64_t n_in, const WT *__restrict__ W, float *__restrict__ Wt) {
     extern __shared__ int sh[];
     int blk = static_cast<int>(blockIdx.x);
     if (blk < n_cr) {
@@ -877,7 +904,7 @@ __global__ __launch_bounds__(256) void conv_bprep_kernel(
     }
     blk -= n_cr;
     if (blk < n_gr) {
-        grad_block(C, g, n_pos, blk, t_out, slope, q_idx, grad_t, gam, uq, qv, live, sh);
+        grad_block(C, g, n_pos, blk, t_out, slope, q_idx, grad_t, sf, gam, uq, qv, live, sh);
         return;
     }
     blk -= n_gr;
@@ -885,19 +912,25 @@ __global__ __launch_bounds__(256) void conv_bprep_kernel(
         zero_block(dt_in, n_in, blk);
         return;
     }
-    weights_block<WT>(g, W, Wt, blk - n_z);
+    blk -= n_z;
+    if (blk < n_dq) {
+        dead_channel_block(g, n_pos / (g.Ho * g.Wo), q_idx, sf, blk, sh);
+        return;
+    }
+    weights_block<WT>(g, W, Wt, blk - n_dq);
 }
 
 // Backward finish: [0, n_red) dW split reduction, the rest gathers dt_in.
 __global__ __launch_bounds__(256) void conv_bfin_kernel(ConvGeom g, int R, int n_red, int nsplit,
                                                         const float *__restrict__ part,
+                                                        const float *__restrict__ dq,
                                                         float *__restrict__ dW, int64_t n_in,
                                                         ConvSorted cs,
                                                         float *__restrict__ dt_in) {
     __shared__ float red[kRedGrp][kRedOut];
     const int blk = static_cast<int>(blockIdx.x);
     if (blk < n_red)
-        dw_reduce_block(g, nsplit, part, dW, blk, red);
+        dw_reduce_block(g, nsplit, part, dq, dW, blk, red);
     else
         dt_gather_block(g, R, n_in, cs, dt_in, blk - n_red);
 }
@@ -977,7 +1010,8 @@ ConvDwPlan plan_conv_dw(const ConvGeom &g, int64_t B, int M) {
 hipError_t launch_conv_backward(const LifConst &C, const ConvGeom &g, int64_t B, const void *W,
                                 bool bf16, const float *t_in, const float *t_out,
                                 const float *slope, const int *q_idx, const float *grad_t,
-                                ConvBwdWs ws, float *grad_W, float *grad_t_in, hipStream_t st) {
+                                ConvBwdWs ws, float *grad_W, float *grad_t_in, const Synfire &sf,
+                                hipStream_t st) {
     const int R = C.M + 3;
     const int64_t n_in = B * g.Hp * g.Wp * g.PC;
     const int64_t n_pos = B * g.Ho * g.Wo;
@@ -992,24 +1026,29 @@ hipError_t launch_conv_backward(const LifConst &C, const ConvGeom &g, int64_t B,
         const int64_t nw = nj * g.C_out;
         const int n_wt = dt ? static_cast<int>((nw + 255) / 256) : 0;
         const int n_z = dt ? static_cast<int>((n_in + 1023) / 1024) : 0;
+        // dead-neuron terms only where dW is written
+        const bool dead = sf.on && sf.dq && grad_W;
+        const int n_dq = dead ? g.C_out : 0;
         const CellEv ev{grad_W ? ws.row : nullptr, ws.L, ws.R};
         ConvSorted cs = ws.srt;
         if (!dt) cs.key = nullptr;
-        int lds = kGradLdsBytes;
+        int lds = std::max(kGradLdsBytes, 256 * static_cast<int>(sizeof(int)));
         if (dt) lds = std::max(lds, conv_sort_lds_bytes(C.M, g));
-        const unsigned blocks = static_cast<unsigned>(n_cr + n_gr + n_z + n_wt);
+        const unsigned blocks = static_cast<unsigned>(n_cr + n_gr + n_z + n_dq + n_wt);
         ProfScope prof("conv_bprep", st);
         if (blocks > 0) {
             if (bf16)
                 hipLaunchKernelGGL(conv_bprep_kernel<uint16_t>, dim3(blocks), dim3(256), lds, st, C,
-                                   g, n_cr, n_gr, n_z, t_in, cs, ev, n_pos, t_out, slope, q_idx,
-                                   grad_t, ws.gam, ws.uq, ws.q, grad_W ? ws.live : nullptr,
-                                   grad_t_in, n_in, static_cast<const uint16_t *>(W), ws.wt);
+                                   g, n_cr, n_gr, n_z, n_dq, t_in, cs, ev, n_pos, t_out, slope,
+                                   q_idx, grad_t, sf, ws.gam, ws.uq, ws.q,
+                                   grad_W ? ws.live : nullptr, grad_t_in, n_in,
+                                   static_cast<const uint16_t *>(W), ws.wt);
             else
                 hipLaunchKernelGGL(conv_bprep_kernel<float>, dim3(blocks), dim3(256), lds, st, C,
-                                   g, n_cr, n_gr, n_z, t_in, cs, ev, n_pos, t_out, slope, q_idx,
-                                   grad_t, ws.gam, ws.uq, ws.q, grad_W ? ws.live : nullptr,
-                                   grad_t_in, n_in, static_cast<const float *>(W), ws.wt);
+                                   g, n_cr, n_gr, n_z, n_dq, t_in, cs, ev, n_pos, t_out, slope,
+                                   q_idx, grad_t, sf, ws.gam, ws.uq, ws.q,
+                                   grad_W ? ws.live : nullptr, grad_t_in, n_in,
+                                   static_cast<const float *>(W), ws.wt);
         }
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
@@ -1070,8 +1109,8 @@ hipError_t launch_conv_backward(const LifConst &C, const ConvGeom &g, int64_t B,
         ProfScope prof("conv_bfin", st);
         if (n_red + n_ga > 0)
             hipLaunchKernelGGL(conv_bfin_kernel, dim3(static_cast<unsigned>(n_red + n_ga)),
-                               dim3(256), 0, st, g, R, n_red, p.nsplit, ws.part, grad_W, n_in,
-                               ws.srt, grad_t_in);
+                               dim3(256), 0, st, g, R, n_red, p.nsplit, ws.part,
+                               (sf.on && sf.dq) ? sf.dq : nullptr, grad_W, n_in, ws.srt, grad_t_in);
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     return hipSuccess;

@@ -137,14 +137,18 @@ __device__ void transpose_tile(int rows, int cols, const WT *__restrict__ in, WT
 
 // Independent setup work of a layer call in one launch, by block role:
 // blocks [0, n_sort) sort one sample each, the next n_tr blocks transpose one
-// weight tile each, the rest write the gradient triple (gamma, t - T_q, q)
-// of kPrepThreads neurons each (backward only). One launch instead of three:
-// every launch costs a few microseconds even when its work is tiny.
+// weight tile each, then blocks writing the gradient triple (gamma, t - T_q,
+// q) of kPrepThreads neurons each (backward only) and, with the synfire
+// terms on, blocks counting each neuron's silent samples into sf.dq. One
+// launch instead of several: every launch costs a few microseconds even when
+// its work is tiny.
 struct PrepGrad {
     const float *t_out, *slope, *grad_t;
     const int *q_idx;
     float *gam, *uq;
     int *q;
+    Synfire sf;
+    int B;
 };
 
 template <typename WT>
@@ -164,13 +168,28 @@ __global__ __launch_bounds__(kPrepThreads) void prep_kernel(LifConst C, int n_so
     } else if (blk < n_sort + n_tr) {
         transpose_tile<WT>(N_out, N_in, W, Wt, blk - n_sort, buf);
     } else {
-        const int64_t k = static_cast<int64_t>(blk - n_sort - n_tr) * kPrepThreads + threadIdx.x;
+        const int64_t n_gb = (n_grad + kPrepThreads - 1) / kPrepThreads;
+        const int64_t gb = blk - n_sort - n_tr;
+        if (gb >= n_gb) {
+            // silent-sample count of neuron i over the batch (dead-neuron term)
+            const int i = static_cast<int>((gb - n_gb) * kPrepThreads + threadIdx.x);
+            if (i < N_out) {
+                int cnt = 0;
+                for (int b = 0; b < pg.B; ++b)
+                    cnt += (pg.q_idx[static_cast<int64_t>(b) * N_out + i] < 0) ? 1 : 0;
+                pg.sf.dq[i] = -(pg.sf.gq * pg.sf.scale * static_cast<float>(cnt));
+            }
+            return;
+        }
+        const int64_t k = gb * kPrepThreads + threadIdx.x;
         if (k < n_grad) {
             const int q = pg.q_idx[k];
             GradPrep gp{0.f, 0.f, -1};
             if (q >= 0) {  // silent neurons: no further loads
-                const float g = pg.grad_t[k];
-                if (g != 0.f) gp = grad_prep(C, pg.t_out[k], pg.slope[k], q, g);
+                float g = pg.grad_t[k];
+                const float t = pg.t_out[k];
+                if (pg.sf.on) g += synfire_dt(pg.sf, t);
+                if (g != 0.f) gp = grad_prep(C, t, pg.slope[k], q, g);
             }
             pg.gam[k] = gp.gam;
             pg.uq[k] = gp.uq;
@@ -534,6 +553,7 @@ __global__ __launch_bounds__(256) void dw_dense_kernel(LifConst C, int B, int N_
                                                         const int *__restrict__ ev_row,
                                                         const float *__restrict__ ev_L,
                                                         const float *__restrict__ ev_R,
+                                                        const float *__restrict__ dq,
                                                         float *__restrict__ dW_part) {
     extern __shared__ float gs[];  // [2][R + 1][TI + 1]
     constexpr int kStr = TI + 1;
@@ -633,19 +653,25 @@ __global__ __launch_bounds__(256) void dw_dense_kernel(LifConst C, int B, int N_
     if (!j_ok) return;
     float *out = dW_part + static_cast<int64_t>(blockIdx.z) * N_out * N_in +
                  static_cast<int64_t>(i0) * N_in + j;
+    // dq: the dead-neuron term of each row, added to the final sums (one
+    // split only; with splits the reduction adds it)
 #pragma unroll
     for (int ii = 0; ii < TI; ++ii)
-        if (ii < ni) out[static_cast<int64_t>(ii) * N_in] = acc[ii];
+        if (ii < ni) out[static_cast<int64_t>(ii) * N_in] = dq ? acc[ii] + dq[i0 + ii] : acc[ii];
 }
 
+// dW[k] = sum of the split partials in split order (+ the row's dead-neuron
+// term dq[k / row_len] when dq is set)
 __global__ __launch_bounds__(256) void reduce_splits_kernel(int64_t n, int nsplit,
                                                             const float *__restrict__ part,
+                                                            const float *__restrict__ dq,
+                                                            int row_len,
                                                             float *__restrict__ out) {
     int64_t k = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
     if (k >= n) return;
     float s = 0.f;
     for (int z = 0; z < nsplit; ++z) s += part[static_cast<int64_t>(z) * n + k];
-    out[k] = s;
+    out[k] = dq ? s + dq[k / row_len] : s;
 }
 
 // -------------------------------------------------------- dt_in (rows) --
@@ -664,7 +690,7 @@ constexpr int kDtRanges = 16;
 
 // The launch may carry extra blocks (blockIdx.y >= B) that finish the dW
 // split reduction of the same layer (independent work, one launch less).
-struct RedJob { int64_t n; int nsplit; const float *part; float *out; };
+struct RedJob { int64_t n; int nsplit; const float *part; float *out; const float *dq; int row_len; };
 
 template <typename WT, int NTW>
 __global__ __launch_bounds__(256) void dtin_rows_kernel(LifConst C, int B, int N_in, int N_out,
@@ -680,7 +706,7 @@ __global__ __launch_bounds__(256) void dtin_rows_kernel(LifConst C, int B, int N
         if (k < red.n) {
             float s = 0.f;
             for (int z = 0; z < red.nsplit; ++z) s += red.part[static_cast<int64_t>(z) * red.n + k];
-            red.out[k] = s;
+            red.out[k] = red.dq ? s + red.dq[k / red.row_len] : s;
         }
         return;
     }
@@ -899,7 +925,8 @@ static hipError_t launch_prep(const LifConst &C, int64_t B, int64_t N_in, int64_
                               int64_t n_grad, const char *name, hipStream_t st) {
     const int n_tr = (transpose && N_in * N_out > 0) ? tiles32(N_in, N_out) : 0;
     const int64_t n_gb = (n_grad + kPrepThreads - 1) / kPrepThreads;
-    const int64_t blocks = B + n_tr + n_gb;
+    const int64_t n_db = (pg.sf.on && pg.sf.dq) ? (N_out + kPrepThreads - 1) / kPrepThreads : 0;
+    const int64_t blocks = B + n_tr + n_gb + n_db;
     if (blocks == 0) return hipSuccess;
     ProfScope prof(name, st);
     if (bf16)
@@ -923,8 +950,9 @@ hipError_t launch_forward(const LifConst &C, int64_t B, int64_t N_in, int64_t N_
     const int R = C.M + 3;
     hipError_t e = launch_prep(C, B, N_in, N_out, t_in, srt, n_valid, false,
                                SortOut{nullptr, nullptr, nullptr, nullptr}, W, bf16, Wt, true,
-                               PrepGrad{nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr}, 0,
-                               "sort_transpose", st);
+                               PrepGrad{nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr,
+                                        Synfire{}, 0},
+                               0, "sort_transpose", st);
     if (e != hipSuccess) return e;
     ProfScope prof("fwd_dense", st);
     if (C.M <= kRowsMaxM) {
@@ -996,7 +1024,8 @@ DwPlan plan_dw(int64_t B, int64_t N_in, int64_t N_out, int M) {
 }
 
 static hipError_t launch_dw(const LifConst &C, const DwPlan &p, int64_t B, int64_t N_in,
-                            int64_t N_out, const DenseBwdWs &ws, float *dst, hipStream_t st) {
+                            int64_t N_out, const DenseBwdWs &ws, const float *dq, float *dst,
+                            hipStream_t st) {
     const int ti = p.jw;
     dim3 grid(static_cast<unsigned>((N_in + 255) / 256),
               static_cast<unsigned>((N_out + ti - 1) / ti), static_cast<unsigned>(p.nsplit));
@@ -1006,7 +1035,7 @@ static hipError_t launch_dw(const LifConst &C, const DwPlan &p, int64_t B, int64
 #define DW_LAUNCH(TIV, NP)                                                                        \
     hipLaunchKernelGGL((dw_dense_kernel<TIV, NP>), grid, dim3(256), lds, st, C, static_cast<int>(B), \
                        static_cast<int>(N_in), static_cast<int>(N_out), p.b_per_split,             \
-                       ws.gam, ws.uq, ws.q, ws.row, ws.L, ws.R, dst)
+                       ws.gam, ws.uq, ws.q, ws.row, ws.L, ws.R, dq, dst)
     if (ti == 64) {
         if (nper == 9) DW_LAUNCH(64, 9);
         else if (nper == 17) DW_LAUNCH(64, 17);
@@ -1023,25 +1052,33 @@ static hipError_t launch_dw(const LifConst &C, const DwPlan &p, int64_t B, int64
 hipError_t launch_backward(const LifConst &C, int64_t B, int64_t N_in, int64_t N_out,
                            const void *W, bool bf16, const float *t_in, const float *t_out,
                            const float *slope, const int *q_idx, const float *grad_t,
-                           DenseBwdWs ws, float *grad_W, float *grad_t_in, hipStream_t st) {
+                           DenseBwdWs ws, float *grad_W, float *grad_t_in, const Synfire &sf,
+                           hipStream_t st) {
     const bool zero_dt = grad_t_in && B * N_in > 0;
     const bool run_dt = zero_dt && N_out > 0;
     const bool run_dw = grad_W && N_out * N_in > 0;
     // sort (per-input events for dW; row-sorted records with derivatives and
     // a zeroed dt_in when dt_in is wanted), transpose W, gradient triples:
     // one launch
+    // the dead-neuron term needs dW; without dW only dT/dt is used
+    Synfire sfp = sf;
+    if (!run_dw) sfp.dq = nullptr;
+    const float *dq = (sfp.on && sfp.dq) ? sfp.dq : nullptr;
     hipError_t e = launch_prep(C, B, N_in, N_out, t_in, ws.srt, ws.n_valid, true,
                                SortOut{ws.row, ws.L, ws.R, zero_dt ? grad_t_in : nullptr}, W, bf16,
-                               ws.wt, run_dt, PrepGrad{t_out, slope, grad_t, q_idx, ws.gam, ws.uq, ws.q},
+                               ws.wt, run_dt,
+                               PrepGrad{t_out, slope, grad_t, q_idx, ws.gam, ws.uq, ws.q, sfp,
+                                        static_cast<int>(B)},
                                B * N_out, "bwd_prep", st);
     if (e != hipSuccess) return e;
     DwPlan p = plan_dw(B, N_in, N_out, C.M);
     const bool split = run_dw && p.nsplit > 1;
     if (run_dw) {
-        e = launch_dw(C, p, B, N_in, N_out, ws, split ? ws.part : grad_W, st);
+        e = launch_dw(C, p, B, N_in, N_out, ws, split ? nullptr : dq, split ? ws.part : grad_W, st);
         if (e != hipSuccess) return e;
     }
-    const RedJob red{split ? N_out * N_in : 0, p.nsplit, ws.part, grad_W};
+    const RedJob red{split ? N_out * N_in : 0, p.nsplit, ws.part, grad_W, dq,
+                     static_cast<int>(N_in)};
     if (run_dt) {
         const int tiles = static_cast<int>((N_out + kWave - 1) / kWave);
         const int tpw = (tiles + 3) / 4;  // tiles per wave
@@ -1067,7 +1104,8 @@ hipError_t launch_backward(const LifConst &C, int64_t B, int64_t N_in, int64_t N
     if (split) {
         ProfScope prof("dw_reduce", st);
         hipLaunchKernelGGL(reduce_splits_kernel, dim3(static_cast<unsigned>((red.n + 255) / 256)),
-                           dim3(256), 0, st, red.n, p.nsplit, ws.part, grad_W);
+                           dim3(256), 0, st, red.n, p.nsplit, ws.part, dq,
+                           static_cast<int>(N_in), grad_W);
         return hipGetLastError();
     }
     return hipSuccess;

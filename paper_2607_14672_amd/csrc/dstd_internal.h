@@ -155,6 +155,25 @@ __device__ __forceinline__ float seg_root(const LifConst &C, const Seg &s, float
 // per-neuron triple gamma = -g / slope (slope floored at 1e-12 theta),
 // u = t - T_q (difference taken in fp64) and q; q = -1 where no gradient
 // flows (silent neuron or g = 0).
+// Synfire-chain training terms inside a backward call (App. C.1): the
+// temporal penalty's dT/dt joins the gradient of every firing neuron; dq
+// (workspace, one float per weight row) receives -gamma_q * scale * (number
+// of silent neurons the row feeds) and is added where dW is written.
+struct Synfire {
+    int on;
+    float gh, gt, th, tt, gq, scale;
+    float *dq;
+};
+
+// d T / d t of a firing neuron: 2 scale (gamma_head (t - t_head) below the
+// window, gamma_tail (t - t_tail) above it), 0 inside
+__device__ __forceinline__ float synfire_dt(const Synfire &s, float t) {
+    float d = 0.f;
+    if (t < s.th) d = 2.f * s.gh * (t - s.th);
+    else if (t > s.tt) d = 2.f * s.gt * (t - s.tt);
+    return s.scale * d;
+}
+
 struct GradPrep { float gam, uq; int q; };
 
 __device__ __forceinline__ GradPrep grad_prep(const LifConst &C, float t, float slope, int q,

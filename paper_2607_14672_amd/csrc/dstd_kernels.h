@@ -37,7 +37,8 @@ struct DenseBwdWs {
 hipError_t launch_backward(const LifConst &C, int64_t B, int64_t N_in, int64_t N_out,
                            const void *W, bool bf16, const float *t_in, const float *t_out,
                            const float *slope, const int *q_idx, const float *grad_t,
-                           DenseBwdWs ws, float *grad_W, float *grad_t_in, hipStream_t st);
+                           DenseBwdWs ws, float *grad_W, float *grad_t_in, const Synfire &sf,
+                           hipStream_t st);
 hipError_t launch_softmax_ce(int64_t B, int64_t N, const float *t, const int *labels,
                              float tau_soft, float t_cap, float *grad, float *loss, hipStream_t st);
 hipError_t launch_mse(int64_t B, int64_t N, const float *t, const float *y, float *grad,
@@ -92,6 +93,14 @@ hipError_t launch_conv_forward(const LifConst &C, const ConvGeom &g, int64_t B, 
 hipError_t launch_conv_backward(const LifConst &C, const ConvGeom &g, int64_t B, const void *W,
                                 bool bf16, const float *t_in, const float *t_out,
                                 const float *slope, const int *q_idx, const float *grad_t,
-                                ConvBwdWs ws, float *grad_W, float *grad_t_in, hipStream_t st);
+                                ConvBwdWs ws, float *grad_W, float *grad_t_in,
+                                const Synfire &sf, hipStream_t st);
+
+// Synfire term values (reporting): T and Q of one layer's outputs
+// t [B][rows][spatial] and weights [rows][row_len].
+int synfire_value_blocks(int64_t n);
+hipError_t launch_synfire_value(const Synfire &sf, int64_t B, int64_t rows, int64_t spatial,
+                                int64_t row_len, const float *t_out, const void *W, bool bf16,
+                                float *ws, float *value, hipStream_t st);
 
 }  // namespace dstd

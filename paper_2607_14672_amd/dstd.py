@@ -40,6 +40,11 @@ class dstd_conv_shape(C.Structure):
                                          "pool_in")]
 
 
+class dstd_synfire_params(C.Structure):
+    _fields_ = [(k, C.c_float) for k in ("gamma_head", "gamma_tail", "t_head", "t_tail", "gamma_q",
+                                         "scale")]
+
+
 class DSTDError(RuntimeError):
     def __init__(self, fn: str, status: int):
         lib = _load()
@@ -66,6 +71,12 @@ _SIGS = {
     "dstd_lif_conv_backward_workspace_size": (_S, [_P, _P, _L]),
     "dstd_lif_conv_forward": (_I, [_P, _P, _L, _P, _P, _I, _P, _P, _P, _P, _S, _P]),
     "dstd_lif_conv_backward": (_I, [_P, _P, _L, _P, _P, _I, _P, _P, _P, _P, _P, _P, _P, _S, _P]),
+    "dstd_lif_backward_synfire": (_I, [_P, _P, _L, _L, _L, _P, _P, _I, _P, _P, _P, _P, _P, _P, _P,
+                                       _S, _P]),
+    "dstd_lif_conv_backward_synfire": (_I, [_P, _P, _P, _L, _P, _P, _I, _P, _P, _P, _P, _P, _P, _P,
+                                            _S, _P]),
+    "dstd_synfire_penalty_workspace_size": (_S, [_L, _L, _L]),
+    "dstd_synfire_penalty": (_I, [_P, _L, _L, _L, _L, _P, _P, _I, _P, _P, _S, _P]),
     "dstd_softmax_ce_grad": (_I, [_L, _L, _P, _P, _F, _F, _P, _P, _P]),
     "dstd_mse_grad": (_I, [_L, _L, _P, _P, _P, _P, _P]),
     "dstd_profile_enable": (C.c_int32, [C.c_int32]),
@@ -141,6 +152,30 @@ def dstd_lif_conv_backward(p, cs, B, t_in, W, w_dtype, t_out, slope, q_idx, grad
                                           q_idx, grad_t_out, grad_W, grad_t_in, ws, ws_bytes, stream)
 
 
+def dstd_lif_backward_synfire(p, sp, B, N_in, N_out, t_in, W, w_dtype, t_out, slope, q_idx,
+                              grad_t_out, grad_W, grad_t_in, ws, ws_bytes, stream):
+    return _load().dstd_lif_backward_synfire(_ref(p), _ref(sp), B, N_in, N_out, t_in, W, w_dtype,
+                                             t_out, slope, q_idx, grad_t_out, grad_W, grad_t_in,
+                                             ws, ws_bytes, stream)
+
+
+def dstd_lif_conv_backward_synfire(p, sp, cs, B, t_in, W, w_dtype, t_out, slope, q_idx,
+                                   grad_t_out, grad_W, grad_t_in, ws, ws_bytes, stream):
+    return _load().dstd_lif_conv_backward_synfire(_ref(p), _ref(sp), _ref(cs), B, t_in, W, w_dtype,
+                                                  t_out, slope, q_idx, grad_t_out, grad_W,
+                                                  grad_t_in, ws, ws_bytes, stream)
+
+
+def dstd_synfire_penalty_workspace_size(B, rows, spatial):
+    return _load().dstd_synfire_penalty_workspace_size(B, rows, spatial)
+
+
+def dstd_synfire_penalty(sp, B, rows, spatial, row_len, t_out, W, w_dtype, value, ws, ws_bytes,
+                         stream):
+    return _load().dstd_synfire_penalty(_ref(sp), B, rows, spatial, row_len, t_out, W, w_dtype,
+                                        value, ws, ws_bytes, stream)
+
+
 def dstd_softmax_ce_grad(B, N, t_out, labels, tau_soft, t_cap, grad_t, loss, stream):
     return _load().dstd_softmax_ce_grad(B, N, t_out, labels, tau_soft, t_cap, grad_t, loss, stream)
 
@@ -196,6 +231,12 @@ def profile_table():
 def make_params(tau_m, tau_s, threshold, M, t0, dt, t_max=math.inf) -> dstd_lif_params:
     return dstd_lif_params(float(tau_m), float(tau_s), float(threshold), int(M), float(t0),
                            float(dt), float(t_max), 0)
+
+
+def make_synfire(gamma_head, gamma_tail, t_head, t_tail, gamma_q, scale) -> dstd_synfire_params:
+    """One layer's synfire-term parameters (window ends t_head, t_tail already
+    shifted for the layer; scale = 1/B, conv 1/(B*H_out*W_out))."""
+    return dstd_synfire_params(gamma_head, gamma_tail, t_head, t_tail, gamma_q, scale)
 
 
 def make_conv_shape(C_in, H, W, C_out, KH=3, KW=3, stride=1, pad=1, pool_in=1) -> dstd_conv_shape:
@@ -272,8 +313,10 @@ def forward(p: dstd_lif_params, t_in, W, ws=None):
 
 
 def backward(p: dstd_lif_params, t_in, W, t_out, slope, q, grad_t_out, need_W=True,
-             need_t_in=True, ws=None):
-    """Dense layer backward; returns (grad_W or None, grad_t_in or None)."""
+             need_t_in=True, ws=None, synfire: Optional[dstd_synfire_params] = None):
+    """Dense layer backward; returns (grad_W or None, grad_t_in or None). With
+    `synfire`, the layer's temporal-penalty and dead-neuron gradients are
+    included."""
     torch = _torch()
     t_in = _cont(t_in, torch.float32)
     W = _cont(W)
@@ -285,11 +328,14 @@ def backward(p: dstd_lif_params, t_in, W, t_out, slope, q, grad_t_out, need_W=Tr
     need = dstd_lif_backward_workspace_size(p, B, N_in, N_out)
     if ws is None or ws.numel() < need:
         ws = workspace(need, dev)
-    _check("dstd_lif_backward",
-           dstd_lif_backward(p, B, N_in, N_out, _ptr(t_in), _ptr(W), _wdtype(W),
-                             _ptr(_cont(t_out, torch.float32)), _ptr(_cont(slope, torch.float32)),
-                             _ptr(_cont(q, torch.int32)), _ptr(_cont(grad_t_out, torch.float32)),
-                             _ptr(gW), _ptr(gt), _ptr(ws), ws.numel(), _stream(dev)))
+    args = (B, N_in, N_out, _ptr(t_in), _ptr(W), _wdtype(W), _ptr(_cont(t_out, torch.float32)),
+            _ptr(_cont(slope, torch.float32)), _ptr(_cont(q, torch.int32)),
+            _ptr(_cont(grad_t_out, torch.float32)), _ptr(gW), _ptr(gt), _ptr(ws), ws.numel(),
+            _stream(dev))
+    if synfire is None:
+        _check("dstd_lif_backward", dstd_lif_backward(p, *args))
+    else:
+        _check("dstd_lif_backward_synfire", dstd_lif_backward_synfire(p, synfire, *args))
     return gW, gt
 
 
@@ -314,7 +360,7 @@ def conv_forward(p: dstd_lif_params, cs: dstd_conv_shape, t_in, W, ws=None):
 
 
 def conv_backward(p, cs, t_in, W, t_out, slope, q, grad_t_out, need_W=True, need_t_in=True,
-                  ws=None):
+                  ws=None, synfire: Optional[dstd_synfire_params] = None):
     torch = _torch()
     t_in = _cont(t_in, torch.float32)
     W = _cont(W)
@@ -325,13 +371,39 @@ def conv_backward(p, cs, t_in, W, t_out, slope, q, grad_t_out, need_W=True, need
     need = dstd_lif_conv_backward_workspace_size(p, cs, B)
     if ws is None or ws.numel() < need:
         ws = workspace(need, dev)
-    _check("dstd_lif_conv_backward",
-           dstd_lif_conv_backward(p, cs, B, _ptr(t_in), _ptr(W), _wdtype(W),
-                                  _ptr(_cont(t_out, torch.float32)),
-                                  _ptr(_cont(slope, torch.float32)), _ptr(_cont(q, torch.int32)),
-                                  _ptr(_cont(grad_t_out, torch.float32)), _ptr(gW), _ptr(gt),
-                                  _ptr(ws), ws.numel(), _stream(dev)))
+    args = (B, _ptr(t_in), _ptr(W), _wdtype(W), _ptr(_cont(t_out, torch.float32)),
+            _ptr(_cont(slope, torch.float32)), _ptr(_cont(q, torch.int32)),
+            _ptr(_cont(grad_t_out, torch.float32)), _ptr(gW), _ptr(gt), _ptr(ws), ws.numel(),
+            _stream(dev))
+    if synfire is None:
+        _check("dstd_lif_conv_backward", dstd_lif_conv_backward(p, cs, *args))
+    else:
+        _check("dstd_lif_conv_backward_synfire",
+               dstd_lif_conv_backward_synfire(p, synfire, cs, *args))
     return gW, gt
+
+
+def synfire_penalty(sp: dstd_synfire_params, t_out, W):
+    """Values (T, Q) of the synfire terms as a device tensor [2]. t_out is
+    [B, N_out] (dense) or [B, C_out, H_out, W_out] (conv); W is the layer's
+    weight tensor (rows = its first dimension)."""
+    torch = _torch()
+    t_out = _cont(t_out, torch.float32)
+    W = _cont(W)
+    B = t_out.shape[0]
+    rows = t_out.shape[1]
+    spatial = 1
+    for d in t_out.shape[2:]:
+        spatial *= d
+    row_len = W.numel() // max(W.shape[0], 1)
+    dev = t_out.device
+    value = torch.empty(2, dtype=torch.float32, device=dev)
+    need = dstd_synfire_penalty_workspace_size(B, rows, spatial)
+    ws = workspace(need, dev)
+    _check("dstd_synfire_penalty",
+           dstd_synfire_penalty(sp, B, rows, spatial, row_len, _ptr(t_out), _ptr(W), _wdtype(W),
+                                _ptr(value), _ptr(ws), ws.numel(), _stream(dev)))
+    return value
 
 
 def softmax_ce_grad(t_out, labels, tau_soft: float = 1.0, t_cap: Optional[float] = None):

@@ -170,3 +170,39 @@ def test_conv_workspace_and_geometry():
     assert dstd.conv_out_hw(_cs(stride=2)) == (4, 4)
     assert dstd.conv_out_hw(_cs(pool_in=2)) == (4, 4)
     assert dstd.conv_out_hw(_cs(pool_in=0, KH=1, KW=1, pad=0)) == (1, 1)
+
+
+@pytest.mark.parametrize("kw", [dict(gamma_head=-0.1), dict(gamma_tail=math.nan),
+                                dict(gamma_q=math.inf), dict(t_head=math.inf),
+                                dict(t_tail=math.nan), dict(scale=0.0), dict(scale=-1.0),
+                                dict(scale=math.inf)])
+def test_synfire_validation(kw):
+    base = dict(gamma_head=0.1, gamma_tail=0.1, t_head=0.2, t_tail=0.8, gamma_q=0.01, scale=0.25)
+    base.update(kw)
+    sp = dstd.make_synfire(**base)
+    p = _p()
+    nb = dstd.dstd_lif_backward_workspace_size(p, 4, 10, 5)
+    assert dstd.dstd_lif_backward_synfire(p, sp, 4, 10, 5, 1, 1, 0, 1, 1, 1, 1, 1, 1, 256, nb,
+                                          None) == dstd.DSTD_ERR_PARAM
+    cs = dstd.make_conv_shape(C_in=2, H=6, W=6, C_out=3)
+    nc = dstd.dstd_lif_conv_backward_workspace_size(p, cs, 2)
+    assert dstd.dstd_lif_conv_backward_synfire(p, sp, cs, 2, 1, 1, 0, 1, 1, 1, 1, 1, 1, 256, nc,
+                                               None) == dstd.DSTD_ERR_PARAM
+    assert dstd.dstd_synfire_penalty(sp, 4, 5, 1, 10, 1, 1, 0, 1, 256, 1 << 20,
+                                     None) == dstd.DSTD_ERR_PARAM
+
+
+def test_synfire_penalty_errors():
+    sp = dstd.make_synfire(0.1, 0.1, 0.2, 0.8, 0.01, 0.25)
+    need = dstd.dstd_synfire_penalty_workspace_size(4, 5, 1)
+    assert need > 0
+    assert dstd.dstd_synfire_penalty_workspace_size(-1, 5, 1) == 0
+    assert dstd.dstd_synfire_penalty(None, 4, 5, 1, 10, 1, 1, 0, 1, 256, need, None) == dstd.DSTD_ERR_NULL
+    assert dstd.dstd_synfire_penalty(sp, 4, 5, 1, 10, 1, 1, 0, None, 256, need, None) == dstd.DSTD_ERR_NULL
+    assert dstd.dstd_synfire_penalty(sp, -4, 5, 1, 10, 1, 1, 0, 1, 256, need, None) == dstd.DSTD_ERR_SHAPE
+    assert dstd.dstd_synfire_penalty(sp, 4, 5, 1, 10, None, 1, 0, 1, 256, need, None) == dstd.DSTD_ERR_NULL
+    assert dstd.dstd_synfire_penalty(sp, 4, 5, 1, 10, 1, None, 0, 1, 256, need, None) == dstd.DSTD_ERR_NULL
+    assert dstd.dstd_synfire_penalty(sp, 4, 5, 1, 10, 1, 1, 5, 1, 256, need, None) == dstd.DSTD_ERR_PARAM
+    assert dstd.dstd_synfire_penalty(sp, 4, 5, 1, 10, 1, 1, 0, 1, 256, need - 1, None) == dstd.DSTD_ERR_WORKSPACE
+    assert dstd.dstd_synfire_penalty(sp, 1 << 16, 1 << 16, 1, 10, 1, 1, 0, 1, 256, 1 << 40,
+                                     None) == dstd.DSTD_ERR_SHAPE

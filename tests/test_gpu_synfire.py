@@ -1,0 +1,196 @@
+"""GPU parity of the synfire training terms (App. C.1) fused into the
+backward passes, and of their value call, against the fp64 oracle."""
+import math
+
+import numpy as np
+import pytest
+
+import oracle
+from tests.parity import check_forward, check_grad
+
+pytestmark = pytest.mark.gpu
+
+SF = dict(gamma_head=0.05, gamma_tail=0.02, t_head=0.45, t_tail=0.75, gamma_q=0.01)
+
+
+@pytest.fixture(scope="module")
+def dev():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    from paper_2607_14672_amd import dstd
+    dstd._load()
+    return torch.device("cuda:0")
+
+
+def _prm(p):
+    from paper_2607_14672_amd import dstd
+    return dstd.make_params(p["tau_m"], p["tau_s"], p["threshold"], p["M"], p["t0"], p["dt"],
+                            p.get("t_max", math.inf))
+
+
+def _sp(scale, **kw):
+    from paper_2607_14672_amd import dstd
+    d = dict(SF, **kw)
+    return dstd.make_synfire(d["gamma_head"], d["gamma_tail"], d["t_head"], d["t_tail"],
+                             d["gamma_q"], scale)
+
+
+def _compare(gW, gx, exp, mask, label):
+    """dW rows and dt_in samples reached by an ill-conditioned spike (the
+    oracle's own mask: tiny slope, both sides agree it fires) are left out:
+    the penalty gradient of such a neuron flows through that slope on both
+    sides."""
+    eW, ex, eWa, exa = exp
+    B, rows = mask.shape[0], mask.shape[1]
+    m = mask.reshape(B, rows, -1)
+    row_ok = ~m.any(axis=(0, 2))
+    smp_ok = ~m.any(axis=(1, 2))
+    assert row_ok.sum() >= 0.8 * rows and smp_ok.sum() >= 0.5 * B, (row_ok.sum(), smp_ok.sum())
+    check_grad(gW[row_ok], eW[row_ok], label + " dW", eWa[row_ok])
+    check_grad(gx[smp_ok], ex[smp_ok], label + " dt_in", exa[smp_ok])
+
+
+def _expected(p, t, W, orc, g, scale, conv_cs=None):
+    """Oracle gradients with the synfire terms: the upstream gradient plus
+    dT/dt into the layer's backward, plus dQ/dW."""
+    _, dT = oracle.temporal_penalty(orc["t_out"], SF["gamma_head"], SF["gamma_tail"],
+                                    SF["t_head"], SF["t_tail"], scale)
+    g_tot = np.where(orc["q"] >= 0, g.astype(np.float64) + dT, 0.0)
+    if conv_cs is None:
+        oW, ox, oWa, oxa = oracle.dstd_backward(p, t, W, orc, g_tot, want_abs=True)
+    else:
+        oW, ox, oWa, oxa = oracle.conv_backward(p, conv_cs, t, W, orc, g_tot, want_abs=True)
+    _, dQ = oracle.dead_neuron_penalty(orc["t_out"], W, SF["gamma_q"], scale)
+    return oW + dQ, ox, oWa + np.abs(dQ), oxa
+
+
+def test_dense_synfire_gradients(dev):
+    import torch
+    from paper_2607_14672_amd import dstd
+    rng = np.random.default_rng(11)
+    B, N_in, N_out, M = 6, 70, 90, 16
+    p = dict(tau_m=1.0, tau_s=0.3, threshold=1.0, M=M, t0=0.0, dt=1.0 / M)
+    t = rng.random((B, N_in)).astype(np.float32)
+    W = ((4.0 / N_in) * (1 + 0.3 * math.sqrt(N_in) * rng.standard_normal((N_out, N_in)))).astype(np.float32)
+    prm = _prm(p)
+    tt, Wt = torch.from_numpy(t).to(dev), torch.from_numpy(W).to(dev)
+    to, sl, q = dstd.forward(prm, tt, Wt)
+    gpu = dict(t_out=to.cpu().numpy(), slope=sl.cpu().numpy(), q=q.cpu().numpy())
+    orc = oracle.dstd_forward(p, t, W)
+    mask, st = check_forward(gpu, orc, N_in, 1.0, label="dense synfire")
+    # the terms need fire / no-fire agreement everywhere
+    assert st["ambiguous"] == 0, st
+    silent = int((orc["q"] < 0).sum())
+    assert 0 < silent < orc["q"].size  # both terms are exercised
+    g = rng.standard_normal((B, N_out)).astype(np.float32)
+    gt = torch.from_numpy(g).to(dev)
+    gW, gx = dstd.backward(prm, tt, Wt, to, sl, q, gt, synfire=_sp(1.0 / B))
+    torch.cuda.synchronize()
+    _compare(gW.cpu().numpy(), gx.cpu().numpy(), _expected(p, t, W, orc, g, 1.0 / B), mask,
+             "dense synfire")
+    # all gammas zero: bit-identical to the plain backward
+    z = dstd.make_synfire(0.0, 0.0, SF["t_head"], SF["t_tail"], 0.0, 1.0)
+    gW0, gx0 = dstd.backward(prm, tt, Wt, to, sl, q, gt, synfire=z)
+    gW1, gx1 = dstd.backward(prm, tt, Wt, to, sl, q, gt)
+    torch.cuda.synchronize()
+    assert torch.equal(gW0, gW1) and torch.equal(gx0, gx1)
+    # without dW the temporal term still reaches dt_in
+    _, gx2 = dstd.backward(prm, tt, Wt, to, sl, q, gt, need_W=False, synfire=_sp(1.0 / B))
+    torch.cuda.synchronize()
+    assert torch.equal(gx2, gx)
+
+
+def test_dense_synfire_split_dw(dev):
+    """A batch large enough that dW is summed over batch splits (the term is
+    then added by the split reduction instead of the dW kernel)."""
+    import torch
+    from paper_2607_14672_amd import dstd
+    rng = np.random.default_rng(12)
+    B, N_in, N_out, M = 64, 40, 30, 8
+    p = dict(tau_m=1.0, tau_s=0.3, threshold=1.0, M=M, t0=0.0, dt=1.0 / M)
+    t = rng.random((B, N_in)).astype(np.float32)
+    W = ((6.0 / N_in) * (1 + 0.3 * math.sqrt(N_in) * rng.standard_normal((N_out, N_in)))).astype(np.float32)
+    prm = _prm(p)
+    tt, Wt = torch.from_numpy(t).to(dev), torch.from_numpy(W).to(dev)
+    to, sl, q = dstd.forward(prm, tt, Wt)
+    gpu = dict(t_out=to.cpu().numpy(), slope=sl.cpu().numpy(), q=q.cpu().numpy())
+    orc = oracle.dstd_forward(p, t, W)
+    mask, st = check_forward(gpu, orc, N_in, 1.0, label="dense synfire split")
+    assert st["ambiguous"] == 0, st
+    g = rng.standard_normal((B, N_out)).astype(np.float32)
+    gW, gx = dstd.backward(prm, tt, Wt, to, sl, q, torch.from_numpy(g).to(dev),
+                           synfire=_sp(1.0 / B))
+    torch.cuda.synchronize()
+    _compare(gW.cpu().numpy(), gx.cpu().numpy(), _expected(p, t, W, orc, g, 1.0 / B), mask,
+             "dense synfire split")
+
+
+def test_conv_synfire_gradients(dev):
+    import torch
+    from paper_2607_14672_amd import dstd
+    rng = np.random.default_rng(13)
+    B, M = 3, 12
+    cs = dict(C_in=4, H=10, W=10, C_out=8, KH=3, KW=3, stride=1, pad=1, pool_in=1)
+    p = dict(tau_m=1.0, tau_s=0.3, threshold=1.0, M=M, t0=0.0, dt=1.0 / M)
+    t = rng.random((B, 4, 10, 10)).astype(np.float32)
+    fan = 36
+    W = ((4.0 / fan) * (1 + 0.3 * math.sqrt(fan) * rng.standard_normal((8, 4, 3, 3)))).astype(np.float32)
+    prm = _prm(p)
+    c = dstd.make_conv_shape(**cs)
+    tt, Wt = torch.from_numpy(t).to(dev), torch.from_numpy(W).to(dev)
+    to, sl, q = dstd.conv_forward(prm, c, tt, Wt)
+    gpu = dict(t_out=to.cpu().numpy(), slope=sl.cpu().numpy(), q=q.cpu().numpy())
+    orc = oracle.conv_forward(p, cs, t, W)
+    mask, st = check_forward(gpu, orc, fan, 1.0, label="conv synfire")
+    assert st["ambiguous"] == 0, st
+    silent = int((orc["q"] < 0).sum())
+    assert 0 < silent < orc["q"].size
+    scale = 1.0 / (B * 10 * 10)
+    g = rng.standard_normal(orc["t_out"].shape).astype(np.float32)
+    gt = torch.from_numpy(g).to(dev)
+    gW, gx = dstd.conv_backward(prm, c, tt, Wt, to, sl, q, gt, synfire=_sp(scale))
+    torch.cuda.synchronize()
+    _compare(gW.cpu().numpy(), gx.cpu().numpy(), _expected(p, t, W, orc, g, scale, conv_cs=cs),
+             mask, "conv synfire")
+    z = dstd.make_synfire(0.0, 0.0, SF["t_head"], SF["t_tail"], 0.0, 1.0)
+    gW0, gx0 = dstd.conv_backward(prm, c, tt, Wt, to, sl, q, gt, synfire=z)
+    gW1, gx1 = dstd.conv_backward(prm, c, tt, Wt, to, sl, q, gt)
+    torch.cuda.synchronize()
+    assert torch.equal(gW0, gW1) and torch.equal(gx0, gx1)
+
+
+@pytest.mark.parametrize("shape,wshape,bf16", [
+    ((5, 33), (33, 17), False),
+    ((7, 300), (300, 1000), True),
+    ((3, 8, 6, 5), (8, 4, 3, 3), False),
+    ((130, 12), (12, 5), False),
+], ids=["dense", "dense-bf16", "conv", "dense-many-samples"])
+def test_synfire_value(dev, shape, wshape, bf16):
+    import torch
+    from paper_2607_14672_amd import dstd
+    from paper_2607_14672_amd import workloads as wl
+    rng = np.random.default_rng(len(shape) * 100 + shape[0])
+    t = rng.uniform(-0.2, 1.4, size=shape).astype(np.float32)
+    t[rng.random(shape) < 0.2] = np.inf
+    W = rng.standard_normal(wshape).astype(np.float32)
+    if bf16:
+        W = wl.bf16_round(W)
+    spatial = int(np.prod(shape[2:])) if len(shape) > 2 else 1
+    scale = 1.0 / (shape[0] * spatial)
+    Wt = torch.from_numpy(W).to(dev)
+    if bf16:
+        Wt = Wt.to(torch.bfloat16)
+    v = dstd.synfire_penalty(_sp(scale), torch.from_numpy(t).to(dev), Wt).cpu().numpy()
+    T, _ = oracle.temporal_penalty(t, SF["gamma_head"], SF["gamma_tail"], SF["t_head"],
+                                   SF["t_tail"], scale)
+    Q, _ = oracle.dead_neuron_penalty(t, W, SF["gamma_q"], scale)
+    # fp32 sums of positive terms (T) and of row sums (Q): relative 1e-5 of
+    # the sum of |terms|
+    Tabs = T
+    Qabs = SF["gamma_q"] * scale * float(np.sum((~np.isfinite(t.reshape(shape[0], shape[1], -1)))
+                                                .sum(axis=(0, 2)) * np.abs(W.reshape(wshape[0], -1)).sum(axis=1)))
+    assert abs(v[0] - T) <= 1e-5 * Tabs + 1e-7, (v, T)
+    assert abs(v[1] - Q) <= 1e-5 * Qabs + 1e-7, (v, Q)
+    # bitwise reproducible
+    v2 = dstd.synfire_penalty(_sp(scale), torch.from_numpy(t).to(dev), Wt).cpu().numpy()
+    assert np.array_equal(v, v2)

@@ -7,6 +7,7 @@ from .oracle import (  # noqa: F401
     build_oracle,
     kernel,
     kdstd,
+    lambert_w0,
     dstd_events,
     dstd_forward,
     dstd_scan,

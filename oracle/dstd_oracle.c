@@ -9,12 +9,15 @@
  * Discretization"):
  *
  *   LIF model and spike kernel K(t) ............ App. A, Eq. (LIF_model_TTFS),
- *                                                  Table "tab:kernel" (row tau_v != tau_I)
+ *                                                  Table "tab:kernel" (rows tau_v != tau_I,
+ *                                                  (tau, tau), (inf, tau), (inf, inf))
  *   exact spike time (sort + interval candidates) App. A, Eq. (timing_exact), Alg. 1
  *   DSTD grid T_m = T_first + m*dt - t_offset .. App. B.1
  *   DSTD event weights s_jm ..................... Eq. (DSTD_kernel), Table "tab:DSTD_kernels"
  *   weighted events w^_im = sum_j w_ij s_jm ..... App. B.1 (definition of w^)
- *   DSTD candidate times and min selection ...... Table "tab:timing_DSTD", Eq. (timing_DSTD)
+ *   DSTD candidate times and min selection ...... Table "tab:timing_DSTD", Eq. (timing_DSTD);
+ *                                                  the closed-form rows as printed, with the
+ *                                                  principal branch W_0 for (tau, tau)
  *
  * Every quantity is computed in double precision from its plain definition.
  * Inputs are double; callers pass the float32 values the GPU sees, widened
@@ -31,8 +34,10 @@
  *    Eq. (timing_DSTD) leaves T_{M+1} undefined; the exact method's analogue
  *    uses +inf for the interval after the last input.
  *  - "Reaches the threshold" means v >= V_th; the interval is half-open.
- *  - The general kernel is symmetric in (tau_v, tau_I); tau_v == tau_I is not
- *    handled here (the equal-tau row of the tables is a different formula).
+ *  - The kernel is symmetric in (tau_v, tau_I); the canonical order puts the
+ *    larger (possibly infinite) constant first. A time constant of +inf
+ *    selects the (inf, tau) / (inf, inf) rows, equal finite constants the
+ *    (tau, tau) row.
  *
  * The only non-closed-form step is the root of v^(t) = V_th inside an
  * interval for general (tau_v, tau_I) (Table "tab:timing_DSTD" gives closed
@@ -51,21 +56,54 @@
 #endif
 
 /* ------------------------------------------------------------------------ */
-/* Spike kernel, Table "tab:kernel", row tau_v != tau_I.                      */
+/* Rows of the tables, by the pair of time constants.                        */
+/* ------------------------------------------------------------------------ */
+enum { ROW_GENERAL = 0, ROW_EQUAL = 1, ROW_INF_TAU = 2, ROW_INF_INF = 3 };
+
+static int row_of(double tv, double ti) {
+    if (isinf(tv) && isinf(ti)) return ROW_INF_INF;
+    if (isinf(tv) || isinf(ti)) return ROW_INF_TAU;
+    if (tv == ti) return ROW_EQUAL;
+    return ROW_GENERAL;
+}
+
+/* the finite constant of an (inf, tau) pair */
+static double finite_of(double tv, double ti) { return isinf(tv) ? ti : tv; }
+
+/* ------------------------------------------------------------------------ */
+/* Spike kernel K(t), Table "tab:kernel".                                    */
 /* ------------------------------------------------------------------------ */
 static double kern(double tv, double ti, double t) {
     if (t < 0.0) return 0.0; /* Heaviside factor */
-    double c = tv * ti / (tv - ti);
-    return c * (exp(-t / tv) - exp(-t / ti));
+    switch (row_of(tv, ti)) {
+        case ROW_INF_INF: return t;
+        case ROW_INF_TAU: { double tau = finite_of(tv, ti); return tau * (1.0 - exp(-t / tau)); }
+        case ROW_EQUAL: return t * exp(-t / tv);
+        default: {
+            double c = tv * ti / (tv - ti);
+            return c * (exp(-t / tv) - exp(-t / ti));
+        }
+    }
 }
 
 double oracle_kernel(double tau_v, double tau_i, double t) { return kern(tau_v, tau_i, t); }
 
 /* ------------------------------------------------------------------------ */
-/* DSTD kernel K_DSTD, Table "tab:DSTD_kernels", row tau_v != tau_I, and its  */
-/* derivative with respect to its argument.                                  */
+/* DSTD kernel K_DSTD, Table "tab:DSTD_kernels", and its derivative with      */
+/* respect to its argument (D = dt).                                         */
 /* ------------------------------------------------------------------------ */
 static double kdstd(double tv, double ti, double D, double t) {
+    int row = row_of(tv, ti);
+    if (row == ROW_INF_INF) return (t < 0.0) ? (t + D) / D : (D - t) / D;
+    if (row == ROW_INF_TAU) {
+        double tau = finite_of(tv, ti), den = 1.0 - exp(-D / tau);
+        if (t < 0.0) return (-exp(-D / tau) + exp(t / tau)) / den;
+        return (1.0 - exp((t - D) / tau)) / den;
+    }
+    if (row == ROW_EQUAL) {
+        if (t < 0.0) return (t + D) / D * exp(t / tv);
+        return (D - t) / D * exp(t / tv);
+    }
     double den = exp(-D / tv) - exp(-D / ti);
     if (t >= 0.0)
         return (exp((t - D) / tv) - exp((t - D) / ti)) / den;
@@ -73,6 +111,17 @@ static double kdstd(double tv, double ti, double D, double t) {
 }
 
 static double kdstd_dt(double tv, double ti, double D, double t) {
+    int row = row_of(tv, ti);
+    if (row == ROW_INF_INF) return (t < 0.0) ? 1.0 / D : -1.0 / D;
+    if (row == ROW_INF_TAU) {
+        double tau = finite_of(tv, ti), den = 1.0 - exp(-D / tau);
+        if (t < 0.0) return exp(t / tau) / tau / den;
+        return -exp((t - D) / tau) / tau / den;
+    }
+    if (row == ROW_EQUAL) {
+        if (t < 0.0) return exp(t / tv) * (1.0 / D + (t + D) / (D * tv));
+        return exp(t / tv) * (-1.0 / D + (D - t) / (D * tv));
+    }
     double den = exp(-D / tv) - exp(-D / ti);
     if (t >= 0.0)
         return (exp((t - D) / tv) / tv - exp((t - D) / ti) / ti) / den;
@@ -132,26 +181,135 @@ void oracle_dstd_events(double tau_v, double tau_i, int M, double t0, double dt,
 /* exp(T/tau)), written relative to a reference time tr so the exponentials  */
 /* stay in range.                                                            */
 /* ------------------------------------------------------------------------ */
-typedef struct { double tv, ti, c, theta, tr, a, b; } piece_t;
+typedef struct { double tv, ti, c, theta, tr, a, b; int row; } piece_t;
 
+static void piece_init(piece_t *p, double tv, double ti, double theta, double tr) {
+    p->tv = tv; p->ti = ti; p->theta = theta; p->tr = tr; p->a = 0.0; p->b = 0.0;
+    p->row = row_of(tv, ti);
+    p->c = (p->row == ROW_GENERAL) ? tv * ti / (tv - ti) : 0.0;
+}
+
+/*
+ * Add a weight w arriving at time T to the prefix sums a, b of Tables
+ * "tab:spike_timing" / "tab:timing_DSTD" (shifted frame s = T - tr):
+ *   general  : a += w e^{s/tv},            b += w e^{s/ti}
+ *   (tau,tau): a += w e^{s/tau},           b += w (s/tau) e^{s/tau}
+ *   (inf,tau): a += w e^{s/tau},           b += w
+ *   (inf,inf): a += w s,                   b += w
+ */
+static void piece_add(piece_t *p, double w, double T) {
+    double s = T - p->tr;
+    switch (p->row) {
+        case ROW_INF_INF: p->a += w * s; p->b += w; break;
+        case ROW_INF_TAU: { double tau = finite_of(p->tv, p->ti);
+                            p->a += w * exp(s / tau); p->b += w; break; }
+        case ROW_EQUAL: p->a += w * exp(s / p->tv); p->b += w * (s / p->tv) * exp(s / p->tv); break;
+        default: p->a += w * exp(s / p->tv); p->b += w * exp(s / p->ti); break;
+    }
+}
+
+/* the potential on the current piece, from the prefix sums:
+ *   general  : c (a e^{-s/tv} - b e^{-s/ti})
+ *   (tau,tau): e^{-s/tau} (s a - tau b)
+ *   (inf,tau): tau (b - a e^{-s/tau})
+ *   (inf,inf): b s - a                                                    */
 static double pv(const piece_t *p, double t) {
     double s = t - p->tr;
-    return p->c * (p->a * exp(-s / p->tv) - p->b * exp(-s / p->ti));
+    switch (p->row) {
+        case ROW_INF_INF: return p->b * s - p->a;
+        case ROW_INF_TAU: { double tau = finite_of(p->tv, p->ti);
+                            return tau * (p->b - p->a * exp(-s / tau)); }
+        case ROW_EQUAL: return exp(-s / p->tv) * (s * p->a - p->tv * p->b);
+        default: return p->c * (p->a * exp(-s / p->tv) - p->b * exp(-s / p->ti));
+    }
 }
 
 static double pdv(const piece_t *p, double t) {
     double s = t - p->tr;
-    return p->c * (-p->a / p->tv * exp(-s / p->tv) + p->b / p->ti * exp(-s / p->ti));
+    switch (p->row) {
+        case ROW_INF_INF: return p->b;
+        case ROW_INF_TAU: { double tau = finite_of(p->tv, p->ti); return p->a * exp(-s / tau); }
+        case ROW_EQUAL: return exp(-s / p->tv) * (p->a * (1.0 - s / p->tv) + p->b);
+        default: return p->c * (-p->a / p->tv * exp(-s / p->tv) + p->b / p->ti * exp(-s / p->ti));
+    }
 }
 
-/* value at hi; hi may be +inf, where both exponentials vanish */
-static double pv_end(const piece_t *p, double hi) { return isinf(hi) ? 0.0 : pv(p, hi); }
+/* value at hi; at hi = +inf the decaying rows vanish, (inf, tau) tends to
+   tau b and (inf, inf) to +-inf with the sign of b (-a when b = 0) */
+static double pv_end(const piece_t *p, double hi) {
+    if (!isinf(hi)) return pv(p, hi);
+    switch (p->row) {
+        case ROW_INF_INF: return (p->b > 0.0) ? INFINITY : (p->b < 0.0) ? -INFINITY : -p->a;
+        case ROW_INF_TAU: return finite_of(p->tv, p->ti) * p->b;
+        default: return 0.0;
+    }
+}
+
+/*
+ * Principal branch W_0 of the Lambert W function (w e^w = x, w >= -1) for
+ * x >= -1/e: the series in p = sqrt(2 (e x + 1)) about the branch point (or
+ * log-based guesses) refined by Halley's iteration.
+ */
+double oracle_lambert_w0(double x) {
+    const double E = 2.718281828459045235360287;
+    if (!(x >= -1.0 / E)) return NAN;
+    if (x == 0.0) return 0.0;
+    double w;
+    if (x < -0.3) {
+        double p = sqrt(fmax(0.0, 2.0 * (E * x + 1.0)));
+        w = -1.0 + p - p * p / 3.0 + 11.0 / 72.0 * p * p * p - 43.0 / 540.0 * p * p * p * p;
+        if (p < 1e-5) return w; /* the series is exact to rounding there */
+    } else if (x < 3.0) {
+        w = log1p(x) * (1.0 - 0.5 * log1p(log1p(x)) / (1.0 + log1p(x)));
+    } else {
+        double l = log(x);
+        w = l - log(l);
+    }
+    for (int it = 0; it < 100; ++it) {
+        double e = exp(w), f = w * e - x;
+        double wn = w - f / (e * (w + 1.0) - (w + 2.0) * f / (2.0 * w + 2.0));
+        if (!isfinite(wn)) break;
+        if (fabs(wn - w) <= 4e-16 * (1.0 + fabs(wn))) { w = wn; break; }
+        w = wn;
+    }
+    return w;
+}
+
+/*
+ * Candidate of one interval from Table "tab:timing_DSTD" (shifted frame), for
+ * the closed-form rows; NAN where the formula has no real value:
+ *   (tau,tau): tau [b/a - W_0(-(V_th/tau)/a e^{b/a})]   (a > 0)
+ *   (inf,tau): tau ln[a / (b - V_th/tau)]
+ *   (inf,inf): (V_th + a) / b
+ */
+static double candidate(const piece_t *p) {
+    double th = p->theta;
+    switch (p->row) {
+        case ROW_INF_INF: return (p->b > 0.0) ? (th + p->a) / p->b : NAN;
+        case ROW_INF_TAU: {
+            double tau = finite_of(p->tv, p->ti), den = p->b - th / tau;
+            return (p->a > 0.0 && den > 0.0) ? tau * log(p->a / den) : NAN;
+        }
+        case ROW_EQUAL: {
+            if (!(p->a > 0.0)) return NAN;
+            double r = p->b / p->a;
+            double z = -(th / p->tv) / p->a * exp(r);
+            double w = oracle_lambert_w0(z);
+            return isnan(w) ? NAN : p->tv * (r - w);
+        }
+        default: return NAN;
+    }
+}
 
 /*
  * First t in [lo, hi) with v(t) >= theta. Returns 1 and sets *root when it
  * exists. *peak receives sup v over [lo, hi] (for the ambiguity margin).
  */
+static int first_crossing_closed(const piece_t *p, double lo, double hi, double *root,
+                                 double *peak);
+
 static int first_crossing(const piece_t *p, double lo, double hi, double *root, double *peak) {
+    if (p->row != ROW_GENERAL) return first_crossing_closed(p, lo, hi, root, peak);
     double th = p->theta;
     /* critical point of v: exp(-kappa*s) = a*ti/(b*tv), kappa = 1/ti - 1/tv */
     double kappa = 1.0 / p->ti - 1.0 / p->tv;
@@ -191,6 +349,31 @@ static int first_crossing(const piece_t *p, double lo, double hi, double *root, 
     return 0;
 }
 
+/*
+ * Closed-form rows: the potential's only critical point is the maximum of
+ * (tau, tau) at s = tau (1 + b/a) (a > 0); the (inf, .) rows are monotone.
+ * The first time in [lo, hi) with v >= V_th is lo itself when v(lo) >= V_th,
+ * else the table's candidate when it lies in [lo, hi) (for (tau, tau) the
+ * W_0 branch is the crossing on the rising side, i.e. the first one).
+ */
+static int first_crossing_closed(const piece_t *p, double lo, double hi, double *root,
+                                 double *peak) {
+    double th = p->theta;
+    double v_lo = pv(p, lo), v_hi = pv_end(p, hi);
+    double pk = fmax(v_lo, v_hi);
+    if (p->row == ROW_EQUAL && p->a > 0.0) {
+        double sc = p->tr + p->tv * (1.0 + p->b / p->a);
+        if (sc > lo && sc < hi) pk = fmax(pk, pv(p, sc));
+    }
+    *peak = pk;
+    if (v_lo >= th) { *root = lo; return 1; }
+    double c = candidate(p);
+    if (isnan(c)) return 0;
+    double t = p->tr + c;
+    if (t >= lo && t < hi) { *root = t; return 1; }
+    return 0;
+}
+
 /* ------------------------------------------------------------------------ */
 /* DSTD forward for one sample: Eq. (DSTD), App. B.1, Table "tab:timing_DSTD" */
 /* and Eq. (timing_DSTD).                                                    */
@@ -209,15 +392,13 @@ static void canon(prm_t *p, double tau_m, double tau_s) {
 /* per-neuron scan over the M+1 DSTD intervals given w^[0..M] */
 static void dstd_scan(const prm_t *p, const double *wh, double *t_out, double *slope,
                       int *q_out, double *margin, double *v_at_T) {
-    double c = p->tv * p->ti / (p->tv - p->ti);
-    double tr = p->t0;
-    piece_t pc = {p->tv, p->ti, c, p->theta, tr, 0.0, 0.0};
+    piece_t pc;
+    piece_init(&pc, p->tv, p->ti, p->theta, p->t0);
     double pre = INFINITY; /* min over earlier intervals of theta - peak */
     for (int q = 0; q <= p->M; ++q) {
         double Tq = grid(p->t0, p->dt, q);
-        /* prefix sums a_iq, b_iq (weights times exp(T_m/tau)), shifted frame */
-        pc.a += wh[q] * exp((Tq - tr) / p->tv);
-        pc.b += wh[q] * exp((Tq - tr) / p->ti);
+        /* prefix sums a_iq, b_iq of Table "tab:timing_DSTD", shifted frame */
+        piece_add(&pc, wh[q], Tq);
         double hi = (q < p->M) ? grid(p->t0, p->dt, q + 1) : p->t_max;
         if (v_at_T) v_at_T[q] = pv(&pc, Tq);
         double root, peak;
@@ -431,7 +612,6 @@ void oracle_exact_forward(double tau_m, double tau_s, double theta, double t_max
                           int64_t B, int64_t N_in, int64_t N_out,
                           const double *t_in, const double *W, double *t_out, double *slope) {
     double tv = fmax(tau_m, tau_s), ti = fmin(tau_m, tau_s);
-    double c = tv * ti / (tv - ti);
 #pragma omp parallel for schedule(dynamic, 1)
     for (int64_t b = 0; b < B; ++b) {
         tw_t *s = (tw_t *)malloc(sizeof(tw_t) * (size_t)(N_in > 0 ? N_in : 1));
@@ -444,10 +624,10 @@ void oracle_exact_forward(double tau_m, double tau_s, double theta, double t_max
             qsort(s, (size_t)n, sizeof(tw_t), cmp_tw);
             double to = INFINITY, sl = 0.0;
             if (n > 0) {
-                piece_t pc = {tv, ti, c, theta, s[0].t, 0.0, 0.0};
+                piece_t pc;
+                piece_init(&pc, tv, ti, theta, s[0].t);
                 for (int64_t k = 0; k < n; ++k) {
-                    pc.a += s[k].w * exp((s[k].t - pc.tr) / tv);
-                    pc.b += s[k].w * exp((s[k].t - pc.tr) / ti);
+                    piece_add(&pc, s[k].w, s[k].t);
                     double lo = s[k].t;
                     double hi = (k + 1 < n) ? s[k + 1].t : t_max;
                     if (!(hi > lo)) continue; /* simultaneous spikes add up first */

@@ -46,6 +46,8 @@ def _load():
     lib.oracle_kernel.argtypes = [_D, _D, _D]
     lib.oracle_kdstd.restype = _D
     lib.oracle_kdstd.argtypes = [_D, _D, _D, _D]
+    lib.oracle_lambert_w0.restype = _D
+    lib.oracle_lambert_w0.argtypes = [_D]
     lib.oracle_dstd_events.restype = None
     lib.oracle_dstd_events.argtypes = [_D, _D, _I, _D, _D, _L, _L, _P, _P, _P]
     lib.oracle_dstd_forward.restype = None
@@ -87,13 +89,20 @@ def num_threads() -> int:
 
 
 def kernel(tau_v, tau_i, t) -> float:
-    """Spike kernel K(t), Table "tab:kernel" (general row)."""
+    """Spike kernel K(t), Table "tab:kernel" (the row follows from the pair:
+    +inf constants and equal constants select the closed-form rows)."""
     return float(_load().oracle_kernel(tau_v, tau_i, t))
 
 
 def kdstd(tau_v, tau_i, dt, t) -> float:
-    """DSTD kernel K_DSTD(t), Table "tab:DSTD_kernels" (general row)."""
+    """DSTD kernel K_DSTD(t), Table "tab:DSTD_kernels" (row as for kernel())."""
     return float(_load().oracle_kdstd(tau_v, tau_i, dt, t))
+
+
+def lambert_w0(x) -> float:
+    """Principal branch of the Lambert W function (used by the (tau, tau)
+    candidate of Table "tab:timing_DSTD")."""
+    return float(_load().oracle_lambert_w0(x))
 
 
 def dstd_events(p, t_in):

@@ -33,14 +33,17 @@ size_t align_up(size_t n) { return (n + kAlign - 1) / kAlign * kAlign; }
 // Host validation of the layer parameters (no device access).
 dstd_status check_params(const dstd_lif_params *p) {
     if (!p) return fail(DSTD_ERR_NULL, "params is NULL");
-    if (!(isfinite(p->tau_m) && p->tau_m > 0.f) || !(isfinite(p->tau_s) && p->tau_s > 0.f))
-        return fail(DSTD_ERR_PARAM, "time constants must be finite and > 0 (tau_m=%g tau_s=%g)",
+    // each time constant is > 0, finite or +inf (the closed-form rows)
+    if (!(p->tau_m > 0.f) || !(p->tau_s > 0.f))
+        return fail(DSTD_ERR_PARAM, "time constants must be > 0 or +inf (tau_m=%g tau_s=%g)",
                     (double)p->tau_m, (double)p->tau_s);
-    double tmax = std::max((double)p->tau_m, (double)p->tau_s);
-    if (fabs((double)p->tau_m - (double)p->tau_s) <= 1e-3 * tmax)
-        return fail(DSTD_ERR_UNSUPPORTED,
-                    "tau_m == tau_s (within 1e-3 relative) uses the equal-constant kernel, "
-                    "which is not implemented");
+    if (isfinite(p->tau_m) && isfinite(p->tau_s) && p->tau_m != p->tau_s) {
+        double tmax = std::max((double)p->tau_m, (double)p->tau_s);
+        if (fabs((double)p->tau_m - (double)p->tau_s) <= 1e-3 * tmax)
+            return fail(DSTD_ERR_UNSUPPORTED,
+                        "tau_m and tau_s differ by less than 1e-3 relative without being equal: "
+                        "use equal constants (the (tau, tau) row) or separate them further");
+    }
     if (!(isfinite(p->threshold) && p->threshold > 0.f))
         return fail(DSTD_ERR_PARAM, "threshold must be finite and > 0");
     if (p->M < 1) return fail(DSTD_ERR_PARAM, "M must be >= 1 (got %d)", p->M);
@@ -56,32 +59,56 @@ dstd_status check_params(const dstd_lif_params *p) {
     return DSTD_OK;
 }
 
-double kern_d(double tv, double ti, double u) {
-    double c = tv * ti / (tv - ti), kap = 1.0 / ti - 1.0 / tv;
-    return -c * exp(-u / tv) * expm1(-kap * u);
+// Row of Table "tab:kernel" for the canonical pair tv >= ti (tv may be inf).
+int kind_of(double tv, double ti) {
+    if (isinf(ti)) return dstd::kInfInf;
+    if (isinf(tv)) return dstd::kInfTau;
+    if (tv == ti) return dstd::kEqual;
+    return dstd::kGeneral;
+}
+
+// K(u), u >= 0 (u may be +inf for the (inf, tau) row's limit)
+double kern_d(int kind, double tv, double ti, double u) {
+    switch (kind) {
+        case dstd::kEqual: return u * exp(-u / ti);
+        case dstd::kInfTau: return -ti * expm1(-u / ti);
+        case dstd::kInfInf: return u;
+        default: {
+            double c = tv * ti / (tv - ti), kap = 1.0 / ti - 1.0 / tv;
+            return -c * exp(-u / tv) * expm1(-kap * u);
+        }
+    }
 }
 
 LifConst make_const(const dstd_lif_params *p) {
     double tv = std::max((double)p->tau_m, (double)p->tau_s);
     double ti = std::min((double)p->tau_m, (double)p->tau_s);
+    const int kind = kind_of(tv, ti);
     double dt = p->dt;
-    double kap = 1.0 / ti - 1.0 / tv;
-    double upk = log(tv / ti) / kap;  // peak time of K
+    // K's maximum on [0, len] sits at min(len, peak): the general row peaks
+    // at ln(tv/ti)/kappa, (tau, tau) at tau; the other rows increase
+    double kap = (kind == dstd::kGeneral) ? 1.0 / ti - 1.0 / tv : 0.0;
+    double upk = (kind == dstd::kGeneral) ? log(tv / ti) / kap
+                 : (kind == dstd::kEqual) ? ti : INFINITY;
     double TM = (double)p->t0 + (double)p->M * dt;
     double last = isinf(p->t_max) ? INFINITY : (double)p->t_max - TM;
-    LifConst C;
+    LifConst C{};
+    C.kind = kind;
     C.tv = (float)tv;
     C.ti = (float)ti;
-    C.inv_tv = (float)(1.0 / tv);
+    C.inv_tv = (float)(1.0 / tv);  // 0 for an infinite constant
     C.inv_ti = (float)(1.0 / ti);
-    C.c = (float)(tv * ti / (tv - ti));
+    C.c = (kind == dstd::kGeneral) ? (float)(tv * ti / (tv - ti)) : 0.f;
     C.kappa = (float)kap;
     C.alpha = (float)exp(-dt / tv);
     C.beta = (float)exp(-dt / ti);
-    C.k_dt = (float)kern_d(tv, ti, dt);
-    C.inv_em1 = (float)(1.0 / expm1(-kap * dt));
-    C.kmax_dt = (float)kern_d(tv, ti, std::min(dt, upk));
-    C.kmax_last = (float)kern_d(tv, ti, std::min(last, upk));
+    C.k_dt = (float)kern_d(kind, tv, ti, dt);
+    C.inv_em1 = (kind == dstd::kGeneral) ? (float)(1.0 / expm1(-kap * dt)) : 0.f;
+    C.kmax_dt = (float)kern_d(kind, tv, ti, std::min(dt, upk));
+    C.kmax_last = (float)kern_d(kind, tv, ti, std::min(last, upk));
+    C.inv_dt = (float)(1.0 / dt);
+    C.e_mdt = (float)exp(-dt / ti);
+    C.inv_D = (kind == dstd::kInfTau) ? (float)(-1.0 / expm1(-dt / ti)) : 0.f;
     C.theta = p->threshold;
     C.t0 = p->t0;
     C.dt = p->dt;
@@ -90,7 +117,7 @@ LifConst make_const(const dstd_lif_params *p) {
     C.M = p->M;
     C.alpha_d = exp(-dt / tv);
     C.beta_d = exp(-dt / ti);
-    C.k_dt_d = kern_d(tv, ti, dt);
+    C.k_dt_d = kern_d(kind, tv, ti, dt);
     C.r_lo_dt = (float)exp(-kap * dt);
     C.r_lo_last = isinf(last) ? 0.f : (float)exp(-kap * last);
     return C;

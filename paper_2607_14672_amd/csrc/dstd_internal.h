@@ -10,12 +10,25 @@ namespace dstd {
 
 constexpr int kWave = 64;  // CDNA wavefront width
 
+// The rows of Table "tab:kernel" this library evaluates: the general row
+// (tau_v != tau_I, both finite) and the three closed-form limits.
+enum KernelKind : int {
+    kGeneral = 0,  // K = c (e^{-u/tv} - e^{-u/ti})
+    kEqual = 1,    // (tau, tau):  K = u e^{-u/tau}
+    kInfTau = 2,   // (inf, tau):  K = tau (1 - e^{-u/tau})
+    kInfInf = 3,   // (inf, inf):  K = u
+};
+
 // Layer constants, computed once per call on the host in double precision and
 // rounded to fp32. The kernel K (Table "tab:kernel") is symmetric in the time
-// constants; tv > ti is the canonical order.
+// constants; tv >= ti is the canonical order (an infinite constant is tv; the
+// finite one of the (inf, tau) row is ti, as is the common one of (tau, tau)).
+// Every case keeps the state form v(T_q + u) = V e^{-u/tv} + I K(u) with the
+// current decaying as e^{-u/ti}; a 1/inf is stored as 0 (e^0 = 1).
 struct LifConst {
-    float tv, ti;          // time constants, tv > ti
-    float inv_tv, inv_ti;  // 1/tv, 1/ti
+    int kind;              // KernelKind
+    float tv, ti;          // time constants, tv >= ti (tv may be +inf)
+    float inv_tv, inv_ti;  // 1/tv, 1/ti (0 for an infinite constant)
     float c;               // tv*ti/(tv - ti)
     float kappa;           // 1/ti - 1/tv > 0
     float alpha, beta;     // exp(-dt/tv), exp(-dt/ti): one-interval decays
@@ -34,6 +47,9 @@ struct LifConst {
     // e^{-kappa*len} for len = dt and for the last interval: the interior
     // maximum u* of v lies inside [0, len) iff e^{-kappa u*} is in (this, 1)
     float r_lo_dt, r_lo_last;
+    // closed-form rows: 1/dt, and for (inf, tau) e^{-dt/tau} and
+    // 1/(1 - e^{-dt/tau})
+    float inv_dt, e_mdt, inv_D;
 };
 
 // Event rows in LDS / G tables: row r holds grid point m = r - 1, so the
@@ -53,17 +69,27 @@ template <> struct WLoad<uint16_t> {
     static __device__ __forceinline__ float get(const uint16_t *p, int64_t k) { return bf16_to_f32(p[k]); }
 };
 
-// K(u) = c (e^{-u/tv} - e^{-u/ti}) = -c e^{-u/tv} expm1(-kappa u), u >= 0,
-// written with expm1 so small u keeps full relative precision.
+// K(u), u >= 0 (Table "tab:kernel"). General row: c (e^{-u/tv} - e^{-u/ti})
+// = -c e^{-u/tv} expm1(-kappa u), written with expm1 so small u keeps full
+// relative precision; likewise tau (1 - e^{-u/tau}) = -tau expm1(-u/tau).
 __device__ __forceinline__ float kern(const LifConst &C, float u) {
-    return -C.c * expf(-u * C.inv_tv) * expm1f(-C.kappa * u);
+    switch (C.kind) {
+        case kEqual: return u * expf(-u * C.inv_ti);
+        case kInfTau: return -C.ti * expm1f(-u * C.inv_ti);
+        case kInfInf: return u;
+        default: return -C.c * expf(-u * C.inv_tv) * expm1f(-C.kappa * u);
+    }
 }
 
-// DSTD events of one input spike (Eq. (DSTD_kernel), Table "tab:DSTD_kernels",
-// row tau_v != tau_I), in forms without cancellation:
-//   q = floor((t - t0)/dt), x = t - T_q in [0, dt), y = dt - x
-//   weight at T_q     : L = e^{x/tv} expm1(-kappa y) / expm1(-kappa dt)
-//   weight at T_{q+1} : R = e^{-y/ti} expm1(-kappa x) / expm1(-kappa dt)
+// DSTD events of one input spike (Eq. (DSTD_kernel), Table "tab:DSTD_kernels"),
+// in forms without cancellation, with q = floor((t - t0)/dt),
+// x = t - T_q in [0, dt), y = dt - x:
+//   general : L = e^{x/tv} expm1(-kappa y) / expm1(-kappa dt)      (at T_q)
+//             R = e^{-y/ti} expm1(-kappa x) / expm1(-kappa dt)     (at T_{q+1})
+//   (tau,tau): L = (y/dt) e^{x/tau},   R = (x/dt) e^{-y/tau}
+//   (inf,tau): L = (1 - e^{-y/tau}) / D,  R = e^{-dt/tau} (e^{x/tau} - 1) / D,
+//              D = 1 - e^{-dt/tau}
+//   (inf,inf): L = y/dt,  R = x/dt
 // and their derivatives with respect to t. `row` = q + 1 (the LDS row of T_q),
 // or -1 when the input contributes nothing (non-finite or out of
 // [T_0 - dt, T_M + dt)). Halves that fall outside the grid are zeroed.
@@ -87,14 +113,33 @@ __device__ __forceinline__ Event bin_event(const LifConst &C, float t) {
     float x = fmaf(-qf, C.dt, rel);
     x = fminf(fmaxf(x, 0.f), C.dt);
     float y = C.dt - x;
-    float ex = expf(x * C.inv_tv);
-    float ey = expf(-y * C.inv_ti);
-    float my = expm1f(-C.kappa * y);
-    float mx = expm1f(-C.kappa * x);
-    e.L = ex * my * C.inv_em1;
-    e.R = ey * mx * C.inv_em1;
-    e.dL = ex * (my * C.inv_tv + C.kappa * (1.f + my)) * C.inv_em1;
-    e.dR = ey * (mx * C.inv_ti - C.kappa * (1.f + mx)) * C.inv_em1;
+    if (C.kind == kEqual) {
+        const float ex = expf(x * C.inv_ti), ey = expf(-y * C.inv_ti);
+        e.L = y * C.inv_dt * ex;
+        e.R = x * C.inv_dt * ey;
+        e.dL = ex * C.inv_dt * fmaf(y, C.inv_ti, -1.f);
+        e.dR = ey * C.inv_dt * fmaf(x, C.inv_ti, 1.f);
+    } else if (C.kind == kInfTau) {
+        const float ey = expf(-y * C.inv_ti);
+        e.L = -expm1f(-y * C.inv_ti) * C.inv_D;
+        e.R = C.e_mdt * expm1f(x * C.inv_ti) * C.inv_D;
+        e.dR = ey * C.inv_ti * C.inv_D;
+        e.dL = -e.dR;
+    } else if (C.kind == kInfInf) {
+        e.L = y * C.inv_dt;
+        e.R = x * C.inv_dt;
+        e.dL = -C.inv_dt;
+        e.dR = C.inv_dt;
+    } else {
+        float ex = expf(x * C.inv_tv);
+        float ey = expf(-y * C.inv_ti);
+        float my = expm1f(-C.kappa * y);
+        float mx = expm1f(-C.kappa * x);
+        e.L = ex * my * C.inv_em1;
+        e.R = ey * mx * C.inv_em1;
+        e.dL = ex * (my * C.inv_tv + C.kappa * (1.f + my)) * C.inv_em1;
+        e.dR = ey * (mx * C.inv_ti - C.kappa * (1.f + mx)) * C.inv_em1;
+    }
     if (q < 0) { e.L = 0.f; e.dL = 0.f; }
     if (q >= C.M) { e.R = 0.f; e.dR = 0.f; }
     e.row = q + 1;
@@ -114,6 +159,23 @@ struct Seg { float V, I; };
 
 __device__ __forceinline__ void seg_eval(const LifConst &C, const Seg &s, float u, float &f,
                                          float &fp) {
+    if (C.kind == kEqual) {  // v = (V + I u) e^{-u/tau}
+        const float e = expf(-u * C.inv_ti);
+        const float a = fmaf(s.I, u, s.V);
+        f = a * e - C.theta;
+        fp = e * fmaf(-a, C.inv_ti, s.I);
+        return;
+    }
+    if (C.kind == kInfTau) {  // v = V + I tau (1 - e^{-u/tau})
+        f = fmaf(s.I, -C.ti * expm1f(-u * C.inv_ti), s.V) - C.theta;
+        fp = s.I * expf(-u * C.inv_ti);
+        return;
+    }
+    if (C.kind == kInfInf) {  // v = V + I u
+        f = fmaf(s.I, u, s.V) - C.theta;
+        fp = s.I;
+        return;
+    }
     float ev = expf(-u * C.inv_tv);
     float em = expm1f(-C.kappa * u);
     float K = -C.c * ev * em;
@@ -213,10 +275,16 @@ __device__ __forceinline__ void g_strided(const LifConst &C, const GStep &gs, fl
     // highest c with m_c <= q (-1: none)
     const int c_top = (q < m0) ? -1 : min(N - 1, (q - m0) / step);
     const float u_top = fmaf(static_cast<float>(q - (m0 + max(c_top, 0) * step)), C.dt, uq);
-    const float ev = expf(-u_top * C.inv_tv);
-    const float em = expm1f(-C.kappa * u_top);
-    float K = -C.c * ev * em;  // K(u_top)
-    float E = ev * (1.f + em);  // e^{-u_top/ti}
+    float K, E;  // K(u_top), e^{-u_top/ti}
+    if (C.kind == kGeneral) {
+        const float ev = expf(-u_top * C.inv_tv);
+        const float em = expm1f(-C.kappa * u_top);
+        K = -C.c * ev * em;
+        E = ev * (1.f + em);
+    } else {
+        K = kern(C, u_top);
+        E = expf(-u_top * C.inv_ti);
+    }
 #pragma unroll
     for (int c = N - 1; c >= 0; --c) {
         if (c < c_top) {
@@ -247,8 +315,9 @@ struct Scan {
             const Seg s{static_cast<float>(Vd), static_cast<float>(Id)};
             const bool last = (q == C.M);
             const float kmax = last ? C.kmax_last : C.kmax_dt;
-            // v(u) = V e^{-u/tv} + I K(u) <= max(V,0) + max(I,0) max K
-            const float ub = fmaxf(s.V, 0.f) + fmaxf(s.I, 0.f) * kmax;
+            // v(u) = V e^{-u/tv} + I K(u) <= max(V,0) + max(I,0) max K (max K
+            // is +inf on the open last interval of the (inf, inf) row)
+            const float ub = fmaxf(s.V, 0.f) + (s.I > 0.f ? s.I * kmax : 0.f);
             if (ub * 1.0001f >= C.theta) {
                 const float len = last ? C.last_len : C.dt;
                 const bool fin = !last || isfinite(C.last_len);
@@ -259,12 +328,28 @@ struct Scan {
                     float f, fp;
                     seg_eval(C, s, C.last_len, f, fp);
                     vend = f + C.theta;
+                } else if (C.kind == kInfTau) {
+                    // open last interval: v rises to V + I tau (never reached)
+                    const float lim = fmaf(s.I, C.ti, s.V);
+                    if (s.I > 0.f && lim > C.theta) vend = lim;
+                } else if (C.kind == kInfInf) {
+                    if (s.I > 0.f) vend = INFINITY;  // v = V + I u grows without bound
                 }
                 if (s.V >= C.theta) {  // only through rounding: v is continuous
                     qf = q; sf = s; hi = 0.f;
                 } else if (vend >= C.theta) {
                     qf = q; sf = s; hi = len; fhi = vend - C.theta;
-                } else if (s.I > 0.f) {
+                } else if (C.kind == kEqual) {
+                    // interior maximum of (V + I u) e^{-u/tau} at u* = tau - V/I (I > 0),
+                    // where v = I tau e^{-u*/tau} <= I tau
+                    if (s.I > 0.f && s.I * C.ti * 1.0001f >= C.theta) {
+                        const float us = C.ti - s.V / s.I;
+                        if (us > 0.f && us < len) {
+                            const float vs = s.I * C.ti * expf(-us * C.inv_ti);
+                            if (vs >= C.theta) { qf = q; sf = s; hi = us; fhi = vs - C.theta; }
+                        }
+                    }
+                } else if (C.kind == kGeneral && s.I > 0.f) {
                     // interior maximum: v'(u*) = 0 with e^{-kappa u*} = (ti/tv)(1 + V/(c I))
                     const float r = (C.ti * C.inv_tv) * (1.f + s.V / (C.c * s.I));
                     const float r_lo = last ? C.r_lo_last : C.r_lo_dt;
@@ -293,7 +378,15 @@ struct Scan {
         q_out = qf;
         if (qf < 0) return;
         float u, sl;
-        if (hi > 0.f) {
+        if (hi > 0.f && C.kind == kInfInf) {
+            // Table "tab:timing_DSTD", row (inf, inf): V + I u = theta, I > 0
+            u = fminf((C.theta - sf.V) / sf.I, hi);
+            sl = sf.I;
+        } else if (hi > 0.f && C.kind == kInfTau) {
+            // row (inf, tau): V + I tau (1 - e^{-u/tau}) = theta, I > 0
+            u = fminf(-C.ti * log1pf(-(C.theta - sf.V) / (sf.I * C.ti)), hi);
+            sl = sf.I * expf(-u * C.inv_ti);
+        } else if (hi > 0.f) {
             u = seg_root(C, sf, hi, fhi, sl);
         } else {
             float f;

@@ -34,10 +34,10 @@ def _p(**kw):
 
 
 @pytest.mark.parametrize("kw,status", [
-    (dict(tau_m=1.0, tau_s=1.0), dstd.DSTD_ERR_UNSUPPORTED),
     (dict(tau_m=1.0, tau_s=1.0005), dstd.DSTD_ERR_UNSUPPORTED),
     (dict(tau_m=-1.0), dstd.DSTD_ERR_PARAM),
-    (dict(tau_s=math.inf), dstd.DSTD_ERR_PARAM),
+    (dict(tau_s=-math.inf), dstd.DSTD_ERR_PARAM),
+    (dict(tau_s=0.0), dstd.DSTD_ERR_PARAM),
     (dict(tau_s=math.nan), dstd.DSTD_ERR_PARAM),
     (dict(threshold=0.0), dstd.DSTD_ERR_PARAM),
     (dict(M=0), dstd.DSTD_ERR_PARAM),
@@ -56,6 +56,16 @@ def test_parameter_validation(kw, status):
     st = dstd.dstd_lif_backward(p, 4, 10, 5, 1, 1, 0, 1, 1, 1, 1, 1, 1, 256, 1 << 20, None)
     assert st == status
     assert dstd.dstd_last_error()
+
+
+@pytest.mark.parametrize("tm,ts", [(1.0, 1.0), (math.inf, 0.5), (0.5, math.inf),
+                                   (math.inf, math.inf)])
+def test_closed_form_rows_are_accepted(tm, ts):
+    """Equal constants and infinite constants select the (tau, tau), (inf,
+    tau) and (inf, inf) rows (Table "tab:kernel")."""
+    p = _p(tau_m=tm, tau_s=ts)
+    assert dstd.dstd_lif_forward_workspace_size(p, 4, 10, 5) > 0
+    assert dstd.dstd_lif_backward_workspace_size(p, 4, 10, 5) > 0
 
 
 def test_flags_must_be_zero():

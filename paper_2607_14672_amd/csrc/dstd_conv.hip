@@ -346,7 +346,7 @@ struct PosWalk {
 // entries are then summed one by one (weight rows loaded 8 at a time), and
 // rows close into the interval scan as the row changes. Sums and their
 // order are those of a row-by-row walk.
-template <int KHT>
+template <int KHT, int KS>
 __global__ __launch_bounds__(256) void conv_fwd_kernel(LifConst C, ConvGeom g, int64_t n_pos,
                                                        const float *__restrict__ Wt,
                                                        ConvSorted cs, float *__restrict__ t_out,
@@ -378,7 +378,7 @@ __global__ __launch_bounds__(256) void conv_fwd_kernel(LifConst C, ConvGeom g, i
     auto rdl = [](float v, int k) {
         return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), k));
     };
-    Scan sc;
+    Scan<KS> sc;
     float aL = 0.f, aR = 0.f, carry = 0.f;
     int cur = 0;  // row being summed
     // close rows cur .. target-1: point r-1 gets row r's L sums plus row
@@ -584,7 +584,7 @@ __device__ void zero_block(float *__restrict__ dt, int64_t n, int64_t blk) {
 
 // dt_in partials. Wave = output position; lane = output channel, NT tiles of
 // 64 per lane. Rows stop after the last grid point any channel's G reaches.
-template <int KHT, int NT>
+template <int KHT, int NT, int KS>
 __global__ __launch_bounds__(256) void conv_dtp_kernel(LifConst C, ConvGeom g, int64_t n_pos,
                                                        const float *__restrict__ Wt,
                                                        ConvSorted cs,
@@ -622,7 +622,7 @@ __global__ __launch_bounds__(256) void conv_dtp_kernel(LifConst C, ConvGeom g, i
 #pragma unroll
     for (int t = 0; t < NT; ++t) {
         gA[t] = 0.f;
-        gB[t] = g_at(C, gm[t], ua[t], qa[t], 0);
+        gB[t] = g_at<KS>(C, gm[t], ua[t], qa[t], 0);
     }
     const __amdgpu_buffer_rsrc_t wr = make_rsrc(
         Wt, static_cast<uint32_t>(static_cast<int64_t>(wk.wlim + 1) * g.C_out * sizeof(float)));
@@ -674,7 +674,7 @@ __global__ __launch_bounds__(256) void conv_dtp_kernel(LifConst C, ConvGeom g, i
 #pragma unroll
         for (int t = 0; t < NT; ++t) {
             gA[t] = gB[t];
-            gB[t] = g_at(C, gm[t], ua[t], qa[t], r + 1);
+            gB[t] = g_at<KS>(C, gm[t], ua[t], qa[t], r + 1);
         }
     }
 }
@@ -713,7 +713,7 @@ __device__ void dt_gather_block(const ConvGeom &g, int R, int64_t n, const ConvS
 // apart: one two-address LDS read; rows R-1 and R stay zero), the next
 // sample's values in registers (NPER per thread) during this one's sums. A
 // sample whose tile is all zero is skipped.
-template <int TI, int NPER>
+template <int TI, int NPER, int KS>
 __global__ __launch_bounds__(256) void conv_dw_kernel(LifConst C, ConvGeom g, int64_t n_samp,
                                                       int s_per_split,
                                                       const float *__restrict__ gam,
@@ -746,7 +746,7 @@ __global__ __launch_bounds__(256) void conv_dw_kernel(LifConst C, ConvGeom g, in
     // element c of this thread: row r = r_first + c * (256 / TI), channel l
     const int l_own = threadIdx.x % TI, r_first = threadIdx.x / TI;
     constexpr int kRowStep = 256 / TI;
-    const GStep gst = g_step(C, kRowStep);
+    const GStep gst = g_step<KS>(C, kRowStep);
     float pre[NPER];
     // G[b, :, p, tile] of sample s; returns whether any value is nonzero
     auto fetch = [&](int64_t s) {
@@ -755,7 +755,7 @@ __global__ __launch_bounds__(256) void conv_dw_kernel(LifConst C, ConvGeom g, in
         const float gm = own ? gam[nb] : 0.f;
         const float u = own ? uq[nb] : 0.f;
         const int q = own ? qv[nb] : -1;
-        g_strided<NPER>(C, gst, gm, u, q, r_first - 1, kRowStep, pre);
+        g_strided<NPER, KS>(C, gst, gm, u, q, r_first - 1, kRowStep, pre);
         bool nz = false;
 #pragma unroll
         for (int c = 0; c < NPER; ++c) nz = nz || pre[c] != 0.f;
@@ -963,15 +963,19 @@ hipError_t launch_conv_forward(const LifConst &C, const ConvGeom &g, int64_t B, 
     dim3 grid(static_cast<unsigned>((n_pos + waves - 1) / waves),
               static_cast<unsigned>((g.C_out + kWave - 1) / kWave));
     ProfScope prof("conv_fwd", st);
-    if (g.KH == 1)
-        hipLaunchKernelGGL(conv_fwd_kernel<1>, grid, dim3(waves * kWave), 0, st, C, g, n_pos, Wt,
-                           cs, t_out, slope, q_idx);
-    else if (g.KH <= 3)
-        hipLaunchKernelGGL(conv_fwd_kernel<3>, grid, dim3(waves * kWave), 0, st, C, g, n_pos, Wt,
-                           cs, t_out, slope, q_idx);
-    else
-        hipLaunchKernelGGL(conv_fwd_kernel<kConvMaxK>, grid, dim3(waves * kWave), 0, st, C, g,
-                           n_pos, Wt, cs, t_out, slope, q_idx);
+#define CFW(KHV, KSV)                                                                            \
+    hipLaunchKernelGGL((conv_fwd_kernel<KHV, KSV>), grid, dim3(waves * kWave), 0, st, C, g, n_pos, \
+                       Wt, cs, t_out, slope, q_idx)
+#define CFW_K(KHV)                                                        \
+    do {                                                                  \
+        if (C.kind == kGeneral) CFW(KHV, kGeneral);                       \
+        else CFW(KHV, kAnyKind);                                          \
+    } while (0)
+    if (g.KH == 1) CFW_K(1);
+    else if (g.KH <= 3) CFW_K(3);
+    else CFW_K(kConvMaxK);
+#undef CFW_K
+#undef CFW
     return hipGetLastError();
 }
 
@@ -1062,9 +1066,14 @@ hipError_t launch_conv_backward(const LifConst &C, const ConvGeom &g, int64_t B,
                            static_cast<size_t>(p.s_per_split) * sizeof(int);
         const int nper = conv_dw_nper(C.M, p.ti);
         ProfScope prof("conv_dw", st);
-#define CDW_LAUNCH(TIV, NP)                                                                   \
-    hipLaunchKernelGGL((conv_dw_kernel<TIV, NP>), grid, dim3(256), lds, st, C, g, n_pos,       \
+#define CDW_LAUNCH_K(TIV, NP, KSV)                                                            \
+    hipLaunchKernelGGL((conv_dw_kernel<TIV, NP, KSV>), grid, dim3(256), lds, st, C, g, n_pos,  \
                        p.s_per_split, ws.gam, ws.uq, ws.q, ws.live, ws.row, ws.L, ws.R, ws.part)
+#define CDW_LAUNCH(TIV, NP)                                               \
+    do {                                                                  \
+        if (C.kind == kGeneral) CDW_LAUNCH_K(TIV, NP, kGeneral);          \
+        else CDW_LAUNCH_K(TIV, NP, kAnyKind);                             \
+    } while (0)
         if (p.ti == 64) {
             if (nper == 5) CDW_LAUNCH(64, 5);
             else if (nper == 9) CDW_LAUNCH(64, 9);
@@ -1077,6 +1086,7 @@ hipError_t launch_conv_backward(const LifConst &C, const ConvGeom &g, int64_t B,
             else CDW_LAUNCH(32, 33);
         }
 #undef CDW_LAUNCH
+#undef CDW_LAUNCH_K
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     if (dt && n_pos > 0) {
@@ -1084,9 +1094,14 @@ hipError_t launch_conv_backward(const LifConst &C, const ConvGeom &g, int64_t B,
         dim3 grid(static_cast<unsigned>((n_pos + waves - 1) / waves));
         const int nt = (g.C_out + kWave - 1) / kWave;
         ProfScope prof("conv_dtp", st);
-#define DTP_LAUNCH(KHV, NTV)                                                                  \
-    hipLaunchKernelGGL((conv_dtp_kernel<KHV, NTV>), grid, dim3(waves * kWave), 0, st, C, g,    \
-                       n_pos, ws.wt, ws.srt, ws.gam, ws.uq, ws.q)
+#define DTP_LAUNCH_K(KHV, NTV, KSV)                                                           \
+    hipLaunchKernelGGL((conv_dtp_kernel<KHV, NTV, KSV>), grid, dim3(waves * kWave), 0, st, C,  \
+                       g, n_pos, ws.wt, ws.srt, ws.gam, ws.uq, ws.q)
+#define DTP_LAUNCH(KHV, NTV)                                              \
+    do {                                                                  \
+        if (C.kind == kGeneral) DTP_LAUNCH_K(KHV, NTV, kGeneral);         \
+        else DTP_LAUNCH_K(KHV, NTV, kAnyKind);                            \
+    } while (0)
 #define DTP_NT(KHV)                               \
     do {                                          \
         if (nt == 1) DTP_LAUNCH(KHV, 1);          \
@@ -1099,6 +1114,7 @@ hipError_t launch_conv_backward(const LifConst &C, const ConvGeom &g, int64_t B,
         else DTP_NT(kConvMaxK);
 #undef DTP_NT
 #undef DTP_LAUNCH
+#undef DTP_LAUNCH_K
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     {

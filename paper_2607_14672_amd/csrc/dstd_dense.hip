@@ -35,6 +35,7 @@ constexpr int kPrepThreads = kSortWaves * 64;
 // (dt_in, whose inputs with events are written later).
 struct SortOut { int *row; float *L; float *R; float *zero; };
 
+template <int KS>
 __device__ void sort_sample(const LifConst &C, int b, int N_in, const float *__restrict__ t_in,
                             SortedEv srt, int *__restrict__ n_valid, int deriv, SortOut xo,
                             int *sh) {
@@ -83,7 +84,7 @@ __device__ void sort_sample(const LifConst &C, int b, int N_in, const float *__r
     for (int j0 = j_lo; j0 < j_hi; j0 += kWave) {
         const int j = j0 + lane;
         Event e{-1, 0.f, 0.f, 0.f, 0.f};
-        if (j < j_hi) e = bin_event(C, tb[j]);
+        if (j < j_hi) e = bin_event<KS>(C, tb[j]);
         const int r = e.row;
         if (j < j_hi) {
             if (xo.row) {
@@ -151,7 +152,7 @@ struct PrepGrad {
     int B;
 };
 
-template <typename WT>
+template <typename WT, int KS>
 __global__ __launch_bounds__(kPrepThreads) void prep_kernel(LifConst C, int n_sort, int n_tr,
                                                             int N_in, int N_out,
                                                             const float *__restrict__ t_in,
@@ -164,7 +165,7 @@ __global__ __launch_bounds__(kPrepThreads) void prep_kernel(LifConst C, int n_so
     __shared__ WT buf[32][33];
     const int blk = blockIdx.x;
     if (blk < n_sort) {
-        sort_sample(C, blk, N_in, t_in, srt, n_valid, deriv, xo, sh);
+        sort_sample<KS>(C, blk, N_in, t_in, srt, n_valid, deriv, xo, sh);
     } else if (blk < n_sort + n_tr) {
         transpose_tile<WT>(N_out, N_in, W, Wt, blk - n_sort, buf);
     } else {
@@ -236,7 +237,7 @@ __device__ __forceinline__ RowRange row_range(const int *rs, int R, int n, int t
 // interval, later events cannot change the outputs and the wave stops.
 constexpr int kBatch = 8;
 
-template <typename WT>
+template <typename WT, int KS>
 __global__ __launch_bounds__(256) void fwd_sorted_kernel(LifConst C, int B, int N_in, int N_out,
                                                          const WT *__restrict__ Wt,
                                                          SortedEv srt,
@@ -257,7 +258,7 @@ __global__ __launch_bounds__(256) void fwd_sorted_kernel(LifConst C, int B, int 
     const int *er = srt.r + eo;
     const float *eL = srt.L + eo;
     const float *eR = srt.R + eo;
-    Scan sc;
+    Scan<KS> sc;
     int cur = 0;  // row whose records are being summed
     float aL = 0.f, aR = 0.f, carry = 0.f;
     bool done = false;
@@ -362,7 +363,7 @@ constexpr int kRowsMaxM = 64;
 constexpr int kRowChunk = 32;  // records per vector load; the lookahead stays within kSortPad
 constexpr int kRowSub = 8;     // records whose NT tile loads are in flight together
 
-template <typename WT, int NT>
+template <typename WT, int NT, int KS>
 __global__ __launch_bounds__(kRowWaves * 64) void fwd_rows_kernel(LifConst C, int N_in, int N_out,
                                                                   const WT *__restrict__ Wt,
                                                                   SortedEv srt,
@@ -511,7 +512,7 @@ __global__ __launch_bounds__(kRowWaves * 64) void fwd_rows_kernel(LifConst C, in
             prev = w;
         }
     }
-    Scan sc;
+    Scan<KS> sc;
     float wn = tp[lane];  // next grid point's sum, read ahead
     for (int m = 0; m <= C.M; ++m) {
         const float wc = wn;
@@ -544,7 +545,7 @@ __global__ __launch_bounds__(kRowWaves * 64) void fwd_rows_kernel(LifConst C, in
 // inputs without events). The next sample's G values and events are fetched
 // while this one is consumed; a sample whose tile is all zero is skipped.
 // Batch splits write partial sums, reduced in order.
-template <int TI, int NPER>
+template <int TI, int NPER, int KS>
 __global__ __launch_bounds__(256) void dw_dense_kernel(LifConst C, int B, int N_in, int N_out,
                                                         int b_per_split,
                                                         const float *__restrict__ gam,
@@ -572,7 +573,7 @@ __global__ __launch_bounds__(256) void dw_dense_kernel(LifConst C, int B, int N_
     // element c of this thread: row r = r_first + c * (256 / TI), neuron l
     const int l_own = threadIdx.x % TI, r_first = threadIdx.x / TI;
     constexpr int kRowStep = 256 / TI;
-    const GStep gst = g_step(C, kRowStep);
+    const GStep gst = g_step<KS>(C, kRowStep);
     float pre[NPER];
     // gradient triple of this thread's neuron in sample b (q = -1: none, or
     // past the block's share); loaded two samples ahead of its use
@@ -588,7 +589,7 @@ __global__ __launch_bounds__(256) void dw_dense_kernel(LifConst C, int B, int N_
         return t;
     };
     auto fetch = [&](const Tri &t) {
-        g_strided<NPER>(C, gst, t.gm, t.u, t.q, r_first - 1, kRowStep, pre);
+        g_strided<NPER, KS>(C, gst, t.gm, t.u, t.q, r_first - 1, kRowStep, pre);
         bool nz = false;
 #pragma unroll
         for (int c = 0; c < NPER; ++c) nz = nz || pre[c] != 0.f;
@@ -692,7 +693,7 @@ constexpr int kDtRanges = 16;
 // split reduction of the same layer (independent work, one launch less).
 struct RedJob { int64_t n; int nsplit; const float *part; float *out; const float *dq; int row_len; };
 
-template <typename WT, int NTW>
+template <typename WT, int NTW, int KS>
 __global__ __launch_bounds__(256) void dtin_rows_kernel(LifConst C, int B, int N_in, int N_out,
                                                         const WT *__restrict__ Wt, SortedEv srt,
                                                         const float *__restrict__ gam,
@@ -753,8 +754,8 @@ __global__ __launch_bounds__(256) void dtin_rows_kernel(LifConst C, int B, int N
         float h0[NTW], h1[NTW];
 #pragma unroll
         for (int t = 0; t < NTW; ++t) {
-            h0[t] = g_at(C, gm0[t], ua0[t], qa0[t], r - 1);
-            h1[t] = g_at(C, gm0[t], ua0[t], qa0[t], r);
+            h0[t] = g_at<KS>(C, gm0[t], ua0[t], qa0[t], r - 1);
+            h1[t] = g_at<KS>(C, gm0[t], ua0[t], qa0[t], r);
         }
         for (int k0 = s; k0 < e; k0 += kBatch) {
             const int nk = min(kBatch, e - k0);
@@ -783,8 +784,8 @@ __global__ __launch_bounds__(256) void dtin_rows_kernel(LifConst C, int B, int N
                         const float gm = ok ? gam[nb + ic] : 0.f;
                         const float u = ok ? uq[nb + ic] : 0.f;
                         const int q = ok ? qv[nb + ic] : -1;
-                        g0[t] = g_at(C, gm, u, q, r - 1);
-                        g1[t] = g_at(C, gm, u, q, r);
+                        g0[t] = g_at<KS>(C, gm, u, q, r - 1);
+                        g1[t] = g_at<KS>(C, gm, u, q, r);
                         voff[t] = ic * static_cast<int>(sizeof(WT));
                     }
                 }
@@ -929,18 +930,19 @@ static hipError_t launch_prep(const LifConst &C, int64_t B, int64_t N_in, int64_
     const int64_t blocks = B + n_tr + n_gb + n_db;
     if (blocks == 0) return hipSuccess;
     ProfScope prof(name, st);
-    if (bf16)
-        hipLaunchKernelGGL(prep_kernel<uint16_t>, dim3(static_cast<unsigned>(blocks)),
-                           dim3(kPrepThreads), sort_lds_bytes(C), st, C, static_cast<int>(B), n_tr,
-                           static_cast<int>(N_in), static_cast<int>(N_out), t_in, srt, n_valid,
-                           deriv ? 1 : 0, xo, static_cast<const uint16_t *>(W),
-                           static_cast<uint16_t *>(Wt), pg, n_grad);
-    else
-        hipLaunchKernelGGL(prep_kernel<float>, dim3(static_cast<unsigned>(blocks)),
-                           dim3(kPrepThreads), sort_lds_bytes(C), st, C, static_cast<int>(B), n_tr,
-                           static_cast<int>(N_in), static_cast<int>(N_out), t_in, srt, n_valid,
-                           deriv ? 1 : 0, xo, static_cast<const float *>(W),
-                           static_cast<float *>(Wt), pg, n_grad);
+#define PREP(WTY, KSV)                                                                             \
+    hipLaunchKernelGGL((prep_kernel<WTY, KSV>), dim3(static_cast<unsigned>(blocks)),              \
+                       dim3(kPrepThreads), sort_lds_bytes(C), st, C, static_cast<int>(B), n_tr,   \
+                       static_cast<int>(N_in), static_cast<int>(N_out), t_in, srt, n_valid,        \
+                       deriv ? 1 : 0, xo, static_cast<const WTY *>(W), static_cast<WTY *>(Wt), pg, \
+                       n_grad)
+    const bool gen = C.kind == kGeneral;
+    if (bf16) {
+        if (gen) PREP(uint16_t, kGeneral); else PREP(uint16_t, kAnyKind);
+    } else {
+        if (gen) PREP(float, kGeneral); else PREP(float, kAnyKind);
+    }
+#undef PREP
     return hipGetLastError();
 }
 
@@ -968,10 +970,15 @@ hipError_t launch_forward(const LifConst &C, int64_t B, int64_t N_in, int64_t N_
             if (nt == 1 && tiles >= t && lds_of(t) <= kRowLdsCap) nt = t;
         dim3 grid(static_cast<unsigned>((tiles + nt - 1) / nt), static_cast<unsigned>(B));
         const size_t lds = lds_of(nt);
-#define FWR(WTY, NTV)                                                                            \
-    hipLaunchKernelGGL((fwd_rows_kernel<WTY, NTV>), grid, dim3(kRowWaves * kWave), lds, st, C,  \
-                       static_cast<int>(N_in), static_cast<int>(N_out),                          \
+#define FWR_K(WTY, NTV, KSV)                                                                      \
+    hipLaunchKernelGGL((fwd_rows_kernel<WTY, NTV, KSV>), grid, dim3(kRowWaves * kWave), lds, st, \
+                       C, static_cast<int>(N_in), static_cast<int>(N_out),                        \
                        static_cast<const WTY *>(Wt), srt, t_out, slope, q_idx)
+#define FWR(WTY, NTV)                                                     \
+    do {                                                                  \
+        if (C.kind == kGeneral) FWR_K(WTY, NTV, kGeneral);                \
+        else FWR_K(WTY, NTV, kAnyKind);                                   \
+    } while (0)
         if (bf16) {
             if (nt == 4) FWR(uint16_t, 4);
             else if (nt == 2) FWR(uint16_t, 2);
@@ -982,19 +989,23 @@ hipError_t launch_forward(const LifConst &C, int64_t B, int64_t N_in, int64_t N_
             else FWR(float, 1);
         }
 #undef FWR
+#undef FWR_K
         return hipGetLastError();
     }
     constexpr int waves = 4;
     dim3 grid(static_cast<unsigned>((N_out + kWave - 1) / kWave),
               static_cast<unsigned>((B + waves - 1) / waves));
-    if (bf16)
-        hipLaunchKernelGGL(fwd_sorted_kernel<uint16_t>, grid, dim3(waves * kWave), 0, st, C,
-                           static_cast<int>(B), static_cast<int>(N_in), static_cast<int>(N_out),
-                           static_cast<const uint16_t *>(Wt), srt, n_valid, t_out, slope, q_idx);
-    else
-        hipLaunchKernelGGL(fwd_sorted_kernel<float>, grid, dim3(waves * kWave), 0, st, C,
-                           static_cast<int>(B), static_cast<int>(N_in), static_cast<int>(N_out),
-                           static_cast<const float *>(Wt), srt, n_valid, t_out, slope, q_idx);
+#define FWS(WTY, KSV)                                                                           \
+    hipLaunchKernelGGL((fwd_sorted_kernel<WTY, KSV>), grid, dim3(waves * kWave), 0, st, C,      \
+                       static_cast<int>(B), static_cast<int>(N_in), static_cast<int>(N_out),     \
+                       static_cast<const WTY *>(Wt), srt, n_valid, t_out, slope, q_idx)
+    const bool gen = C.kind == kGeneral;
+    if (bf16) {
+        if (gen) FWS(uint16_t, kGeneral); else FWS(uint16_t, kAnyKind);
+    } else {
+        if (gen) FWS(float, kGeneral); else FWS(float, kAnyKind);
+    }
+#undef FWS
     return hipGetLastError();
 }
 
@@ -1032,10 +1043,15 @@ static hipError_t launch_dw(const LifConst &C, const DwPlan &p, int64_t B, int64
     size_t lds = 2 * static_cast<size_t>(C.M + 4) * (ti + 1) * sizeof(float);
     ProfScope prof("dw_dense", st);
     const int nper = dw_nper(C.M, ti);
-#define DW_LAUNCH(TIV, NP)                                                                        \
-    hipLaunchKernelGGL((dw_dense_kernel<TIV, NP>), grid, dim3(256), lds, st, C, static_cast<int>(B), \
-                       static_cast<int>(N_in), static_cast<int>(N_out), p.b_per_split,             \
-                       ws.gam, ws.uq, ws.q, ws.row, ws.L, ws.R, dq, dst)
+#define DW_LAUNCH_K(TIV, NP, KSV)                                                                  \
+    hipLaunchKernelGGL((dw_dense_kernel<TIV, NP, KSV>), grid, dim3(256), lds, st, C,               \
+                       static_cast<int>(B), static_cast<int>(N_in), static_cast<int>(N_out),        \
+                       p.b_per_split, ws.gam, ws.uq, ws.q, ws.row, ws.L, ws.R, dq, dst)
+#define DW_LAUNCH(TIV, NP)                                                \
+    do {                                                                  \
+        if (C.kind == kGeneral) DW_LAUNCH_K(TIV, NP, kGeneral);           \
+        else DW_LAUNCH_K(TIV, NP, kAnyKind);                              \
+    } while (0)
     if (ti == 64) {
         if (nper == 9) DW_LAUNCH(64, 9);
         else if (nper == 17) DW_LAUNCH(64, 17);
@@ -1046,6 +1062,7 @@ static hipError_t launch_dw(const LifConst &C, const DwPlan &p, int64_t B, int64
         else DW_LAUNCH(32, 33);
     }
 #undef DW_LAUNCH
+#undef DW_LAUNCH_K
     return hipGetLastError();
 }
 
@@ -1085,10 +1102,15 @@ hipError_t launch_backward(const LifConst &C, int64_t B, int64_t N_in, int64_t N
         const int64_t red_rows = (red.n + kDtRanges * 256 - 1) / (kDtRanges * 256);
         dim3 grid(kDtRanges, static_cast<unsigned>(B + red_rows));
         ProfScope prof("dtin_rows", st);
-#define DTR(WTY, NTV)                                                                            \
-    hipLaunchKernelGGL((dtin_rows_kernel<WTY, NTV>), grid, dim3(256), 0, st, C,                 \
+#define DTR_K(WTY, NTV, KSV)                                                                     \
+    hipLaunchKernelGGL((dtin_rows_kernel<WTY, NTV, KSV>), grid, dim3(256), 0, st, C,            \
                        static_cast<int>(B), static_cast<int>(N_in), static_cast<int>(N_out),     \
                        static_cast<const WTY *>(ws.wt), ws.srt, ws.gam, ws.uq, ws.q, grad_t_in, red)
+#define DTR(WTY, NTV)                                                     \
+    do {                                                                  \
+        if (C.kind == kGeneral) DTR_K(WTY, NTV, kGeneral);                \
+        else DTR_K(WTY, NTV, kAnyKind);                                   \
+    } while (0)
 #define DTR_NT(WTY)                                      \
     do {                                                 \
         if (tpw <= 1) DTR(WTY, 1);                       \
@@ -1099,6 +1121,7 @@ hipError_t launch_backward(const LifConst &C, int64_t B, int64_t N_in, int64_t N
         else DTR_NT(float);
 #undef DTR_NT
 #undef DTR
+#undef DTR_K
         return hipGetLastError();
     }
     if (split) {

@@ -19,6 +19,11 @@ enum KernelKind : int {
     kInfInf = 3,   // (inf, inf):  K = u
 };
 
+// Kernels take the row as a compile-time hint KS: a KernelKind when the
+// launcher knows it (the general row gets code without the other rows'
+// branches), kAnyKind to switch on LifConst::kind at run time.
+constexpr int kAnyKind = -1;
+
 // Layer constants, computed once per call on the host in double precision and
 // rounded to fp32. The kernel K (Table "tab:kernel") is symmetric in the time
 // constants; tv >= ti is the canonical order (an infinite constant is tv; the
@@ -52,6 +57,13 @@ struct LifConst {
     float inv_dt, e_mdt, inv_D;
 };
 
+template <int KS> __device__ __forceinline__ int kind_of(const LifConst &C) {
+    return (KS >= 0) ? KS : C.kind;
+}
+
+struct LifConst;
+template <int KS> __device__ __forceinline__ int kind_of(const LifConst &C);
+
 // Event rows in LDS / G tables: row r holds grid point m = r - 1, so the
 // dropped halves of inputs at the grid ends land in the two zero rows
 // r = 0 (m = -1) and r = M + 2 (m = M + 1).
@@ -72,8 +84,9 @@ template <> struct WLoad<uint16_t> {
 // K(u), u >= 0 (Table "tab:kernel"). General row: c (e^{-u/tv} - e^{-u/ti})
 // = -c e^{-u/tv} expm1(-kappa u), written with expm1 so small u keeps full
 // relative precision; likewise tau (1 - e^{-u/tau}) = -tau expm1(-u/tau).
+template <int KS = kAnyKind>
 __device__ __forceinline__ float kern(const LifConst &C, float u) {
-    switch (C.kind) {
+    switch (kind_of<KS>(C)) {
         case kEqual: return u * expf(-u * C.inv_ti);
         case kInfTau: return -C.ti * expm1f(-u * C.inv_ti);
         case kInfInf: return u;
@@ -103,7 +116,9 @@ __device__ __forceinline__ int bin_row(const LifConst &C, float t) {
     return static_cast<int>(qf) + 1;
 }
 
+template <int KS = kAnyKind>
 __device__ __forceinline__ Event bin_event(const LifConst &C, float t) {
+    const int kind = kind_of<KS>(C);
     Event e{-1, 0.f, 0.f, 0.f, 0.f};
     const int row = bin_row(C, t);
     if (row < 0) return e;
@@ -113,19 +128,19 @@ __device__ __forceinline__ Event bin_event(const LifConst &C, float t) {
     float x = fmaf(-qf, C.dt, rel);
     x = fminf(fmaxf(x, 0.f), C.dt);
     float y = C.dt - x;
-    if (C.kind == kEqual) {
+    if (kind == kEqual) {
         const float ex = expf(x * C.inv_ti), ey = expf(-y * C.inv_ti);
         e.L = y * C.inv_dt * ex;
         e.R = x * C.inv_dt * ey;
         e.dL = ex * C.inv_dt * fmaf(y, C.inv_ti, -1.f);
         e.dR = ey * C.inv_dt * fmaf(x, C.inv_ti, 1.f);
-    } else if (C.kind == kInfTau) {
+    } else if (kind == kInfTau) {
         const float ey = expf(-y * C.inv_ti);
         e.L = -expm1f(-y * C.inv_ti) * C.inv_D;
         e.R = C.e_mdt * expm1f(x * C.inv_ti) * C.inv_D;
         e.dR = ey * C.inv_ti * C.inv_D;
         e.dL = -e.dR;
-    } else if (C.kind == kInfInf) {
+    } else if (kind == kInfInf) {
         e.L = y * C.inv_dt;
         e.R = x * C.inv_dt;
         e.dL = -C.inv_dt;
@@ -157,21 +172,23 @@ struct SortedEv { int *j; int *r; float *L; float *R; int64_t stride; int *rs; }
 // (the state-space form of v^(t) = sum_{m<=q} w^_m K(t - T_m)).
 struct Seg { float V, I; };
 
+template <int KS = kAnyKind>
 __device__ __forceinline__ void seg_eval(const LifConst &C, const Seg &s, float u, float &f,
                                          float &fp) {
-    if (C.kind == kEqual) {  // v = (V + I u) e^{-u/tau}
+    const int kind = kind_of<KS>(C);
+    if (kind == kEqual) {  // v = (V + I u) e^{-u/tau}
         const float e = expf(-u * C.inv_ti);
         const float a = fmaf(s.I, u, s.V);
         f = a * e - C.theta;
         fp = e * fmaf(-a, C.inv_ti, s.I);
         return;
     }
-    if (C.kind == kInfTau) {  // v = V + I tau (1 - e^{-u/tau})
+    if (kind == kInfTau) {  // v = V + I tau (1 - e^{-u/tau})
         f = fmaf(s.I, -C.ti * expm1f(-u * C.inv_ti), s.V) - C.theta;
         fp = s.I * expf(-u * C.inv_ti);
         return;
     }
-    if (C.kind == kInfInf) {  // v = V + I u
+    if (kind == kInfInf) {  // v = V + I u
         f = fmaf(s.I, u, s.V) - C.theta;
         fp = s.I;
         return;
@@ -188,6 +205,7 @@ __device__ __forceinline__ void seg_eval(const LifConst &C, const Seg &s, float 
 // only root there: v has at most one extremum per interval, and [0, hi]
 // either ends at it or past the crossing). Safeguarded Newton started at the
 // regula-falsi point of the bracket, keeping the bracket.
+template <int KS = kAnyKind>
 __device__ __forceinline__ float seg_root(const LifConst &C, const Seg &s, float hi, float fhi,
                                           float &slope) {
     const float f0 = s.V - C.theta;  // f(0) < 0
@@ -195,14 +213,14 @@ __device__ __forceinline__ float seg_root(const LifConst &C, const Seg &s, float
     float u = (fhi > f0) ? hi * (-f0 / (fhi - f0)) : 0.5f * hi;
     if (!(u > 0.f && u < hi)) u = 0.5f * hi;
     float f, fp;
-    seg_eval(C, s, u, f, fp);
+    seg_eval<KS>(C, s, u, f, fp);
     for (int it = 0; it < 48; ++it) {
         if (f < 0.f) lo = u; else hi = u;
         float un = (fp > 0.f) ? u - f / fp : 0.5f * (lo + hi);
         if (!(un > lo && un < hi)) un = 0.5f * (lo + hi);
         const float step = un - u;
         u = un;
-        seg_eval(C, s, u, f, fp);
+        seg_eval<KS>(C, s, u, f, fp);
         // Newton converges quadratically: once a step is below 1e-6 of u the
         // next one is below an fp32 ulp. The bracket test catches bisection.
         const float tol = 1e-6f * fmaxf(u, 1e-6f * C.dt);
@@ -252,9 +270,10 @@ __device__ __forceinline__ GradPrep grad_prep(const LifConst &C, float t, float 
 // G[m] from the triple: t - T_m = (t - T_q) + (q - m) dt is formed with one
 // rounding from non-negative terms, and K(u) keeps full relative precision
 // (expm1 form), so no per-neuron recurrence over the grid is needed.
+template <int KS = kAnyKind>
 __device__ __forceinline__ float g_at(const LifConst &C, float gam, float uq, int q, int m) {
     if (m < 0 || m > q) return 0.f;
-    return gam * kern(C, fmaf(static_cast<float>(q - m), C.dt, uq));
+    return gam * kern<KS>(C, fmaf(static_cast<float>(q - m), C.dt, uq));
 }
 
 // G of one neuron at the grid points m_c = m0 + c * step, c = 0..N-1 (rows of
@@ -264,25 +283,26 @@ __device__ __forceinline__ float g_at(const LifConst &C, float gam, float uq, in
 // b_s e^{-u/ti} (s = step * dt), whose terms are all positive.
 struct GStep { float a, b, k; };  // e^{-s/tv}, e^{-s/ti}, K(s)
 
+template <int KS = kAnyKind>
 __device__ __forceinline__ GStep g_step(const LifConst &C, int step) {
     const float s = static_cast<float>(step) * C.dt;
-    return GStep{expf(-s * C.inv_tv), expf(-s * C.inv_ti), kern(C, s)};
+    return GStep{expf(-s * C.inv_tv), expf(-s * C.inv_ti), kern<KS>(C, s)};
 }
 
-template <int N>
+template <int N, int KS = kAnyKind>
 __device__ __forceinline__ void g_strided(const LifConst &C, const GStep &gs, float gam, float uq,
                                           int q, int m0, int step, float *out) {
     // highest c with m_c <= q (-1: none)
     const int c_top = (q < m0) ? -1 : min(N - 1, (q - m0) / step);
     const float u_top = fmaf(static_cast<float>(q - (m0 + max(c_top, 0) * step)), C.dt, uq);
     float K, E;  // K(u_top), e^{-u_top/ti}
-    if (C.kind == kGeneral) {
+    if (kind_of<KS>(C) == kGeneral) {
         const float ev = expf(-u_top * C.inv_tv);
         const float em = expm1f(-C.kappa * u_top);
         K = -C.c * ev * em;
         E = ev * (1.f + em);
     } else {
-        K = kern(C, u_top);
+        K = kern<KS>(C, u_top);
         E = expf(-u_top * C.inv_ti);
     }
 #pragma unroll
@@ -302,6 +322,7 @@ __device__ __forceinline__ void g_strided(const LifConst &C, const GStep &gs, fl
 // the recurrence would grow with M. Interval tests use the fp32-rounded state.
 // Only the crossing interval and its bracket are located here; the root is
 // solved once in finish(), with all lanes of the wave together.
+template <int KS = kAnyKind>
 struct Scan {
     double Vd = 0.0, Id = 0.0;
     int qf = -1;
@@ -309,6 +330,7 @@ struct Scan {
     float hi = 0.f, fhi = 0.f;  // bracket end of the crossing and v - theta there
 
     __device__ __forceinline__ void step(const LifConst &C, int q, float w) {
+        const int kind = kind_of<KS>(C);
         Id += static_cast<double>(w);
         const double vn_d = fma(Vd, C.alpha_d, Id * C.k_dt_d);
         if (qf < 0) {
@@ -326,20 +348,20 @@ struct Scan {
                     vend = static_cast<float>(vn_d);
                 } else if (fin) {
                     float f, fp;
-                    seg_eval(C, s, C.last_len, f, fp);
+                    seg_eval<KS>(C, s, C.last_len, f, fp);
                     vend = f + C.theta;
-                } else if (C.kind == kInfTau) {
+                } else if (kind == kInfTau) {
                     // open last interval: v rises to V + I tau (never reached)
                     const float lim = fmaf(s.I, C.ti, s.V);
                     if (s.I > 0.f && lim > C.theta) vend = lim;
-                } else if (C.kind == kInfInf) {
+                } else if (kind == kInfInf) {
                     if (s.I > 0.f) vend = INFINITY;  // v = V + I u grows without bound
                 }
                 if (s.V >= C.theta) {  // only through rounding: v is continuous
                     qf = q; sf = s; hi = 0.f;
                 } else if (vend >= C.theta) {
                     qf = q; sf = s; hi = len; fhi = vend - C.theta;
-                } else if (C.kind == kEqual) {
+                } else if (kind == kEqual) {
                     // interior maximum of (V + I u) e^{-u/tau} at u* = tau - V/I (I > 0),
                     // where v = I tau e^{-u*/tau} <= I tau
                     if (s.I > 0.f && s.I * C.ti * 1.0001f >= C.theta) {
@@ -349,7 +371,7 @@ struct Scan {
                             if (vs >= C.theta) { qf = q; sf = s; hi = us; fhi = vs - C.theta; }
                         }
                     }
-                } else if (C.kind == kGeneral && s.I > 0.f) {
+                } else if (kind == kGeneral && s.I > 0.f) {
                     // interior maximum: v'(u*) = 0 with e^{-kappa u*} = (ti/tv)(1 + V/(c I))
                     const float r = (C.ti * C.inv_tv) * (1.f + s.V / (C.c * s.I));
                     const float r_lo = last ? C.r_lo_last : C.r_lo_dt;
@@ -359,7 +381,7 @@ struct Scan {
                         fmaf(s.I * C.c, 1.f - r, s.V) * 1.0001f >= C.theta) {
                         const float us = -logf(r) / C.kappa;
                         float f, fp;
-                        seg_eval(C, s, us, f, fp);
+                        seg_eval<KS>(C, s, us, f, fp);
                         if (f >= 0.f) { qf = q; sf = s; hi = us; fhi = f; }
                     }
                 }
@@ -377,21 +399,22 @@ struct Scan {
         slope = 0.f;
         q_out = qf;
         if (qf < 0) return;
+        const int kind = kind_of<KS>(C);
         float u, sl;
-        if (hi > 0.f && C.kind == kInfInf) {
+        if (hi > 0.f && kind == kInfInf) {
             // Table "tab:timing_DSTD", row (inf, inf): V + I u = theta, I > 0
             u = fminf((C.theta - sf.V) / sf.I, hi);
             sl = sf.I;
-        } else if (hi > 0.f && C.kind == kInfTau) {
+        } else if (hi > 0.f && kind == kInfTau) {
             // row (inf, tau): V + I tau (1 - e^{-u/tau}) = theta, I > 0
             u = fminf(-C.ti * log1pf(-(C.theta - sf.V) / (sf.I * C.ti)), hi);
             sl = sf.I * expf(-u * C.inv_ti);
         } else if (hi > 0.f) {
-            u = seg_root(C, sf, hi, fhi, sl);
+            u = seg_root<KS>(C, sf, hi, fhi, sl);
         } else {
             float f;
             u = 0.f;
-            seg_eval(C, sf, 0.f, f, sl);
+            seg_eval<KS>(C, sf, 0.f, f, sl);
         }
         t_out = static_cast<float>(fma(static_cast<double>(qf), static_cast<double>(C.dt),
                                        static_cast<double>(C.t0)) + static_cast<double>(u));

@@ -342,20 +342,25 @@ struct PosWalk {
 // hold the KH segment bounds of their row and an exclusive prefix of the
 // row counts; for 64 list entries at a time each lane finds its entry's row
 // (binary search over the prefix with lane shuffles), its segment and its
-// record, and loads the record's fields with one vector load each. The
-// entries are then summed one by one (weight rows loaded 8 at a time), and
-// rows close into the interval scan as the row changes. Sums and their
-// order are those of a row-by-row walk.
+// record, and loads the record's fields with one vector load each; the
+// decoded entries (weight-row offset, row, L, R) go to a small LDS area of
+// the wave. The entries are then summed one by one, each read back as one
+// 16-byte LDS broadcast (weight rows loaded 8 at a time), and rows close
+// into the interval scan as the row changes. Sums and their order are those
+// of a row-by-row walk.
+struct FwdEntry { int wb, row; float L, R; };
 template <int KHT, int KS>
 __global__ __launch_bounds__(256) void conv_fwd_kernel(LifConst C, ConvGeom g, int64_t n_pos,
                                                        const float *__restrict__ Wt,
                                                        ConvSorted cs, float *__restrict__ t_out,
                                                        float *__restrict__ slope,
                                                        int *__restrict__ q_idx) {
+    __shared__ FwdEntry ent[4][kWave];
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = uniform(threadIdx.x >> 6);
     const int64_t p = static_cast<int64_t>(blockIdx.x) * (blockDim.x >> 6) + wave;
     if (p >= n_pos) return;  // wave-uniform; no block barrier below
+    FwdEntry *my = ent[wave];
     const int co = blockIdx.y * kWave + lane;
     const bool row_ok = co < g.C_out;
     const int HoWo = g.Ho * g.Wo;
@@ -375,9 +380,6 @@ __global__ __launch_bounds__(256) void conv_fwd_kernel(LifConst C, ConvGeom g, i
         Wt, static_cast<uint32_t>(static_cast<int64_t>(wk.wlim + 1) * g.C_out * sizeof(float)));
     const int voff = (row_ok ? co : 0) * static_cast<int>(sizeof(float));
     const int rstride = g.C_out * static_cast<int>(sizeof(float));
-    auto rdl = [](float v, int k) {
-        return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), k));
-    };
     Scan<KS> sc;
     float aL = 0.f, aR = 0.f, carry = 0.f;
     int cur = 0;  // row being summed
@@ -451,17 +453,20 @@ __global__ __launch_bounds__(256) void conv_fwd_kernel(LifConst C, ConvGeom g, i
             const float Lv = ok ? cs.L[gi] : 0.f;
             const float Rv = ok ? cs.R[gi] : 0.f;
             const int wb = min(max(key + wof, 0), wk.wlim) * rstride;
-            const int rrow = r0 + lo;
+            my[lane] = FwdEntry{wb, r0 + lo, Lv, Rv};
+            __builtin_amdgcn_wave_barrier();
             const int nc = min(kWave, total - c0);
             for (int s0 = 0; s0 < nc; s0 += kCBatch) {
+                FwdEntry e[kCBatch];
                 float w[kCBatch];
 #pragma unroll
-                for (int q = 0; q < kCBatch; ++q)
-                    w[q] = BufLoad<float>::get(wr, voff, __builtin_amdgcn_readlane(wb, s0 + q));
+                for (int q = 0; q < kCBatch; ++q) e[q] = my[s0 + q];  // LDS broadcasts
+#pragma unroll
+                for (int q = 0; q < kCBatch; ++q) w[q] = BufLoad<float>::get(wr, voff + e[q].wb, 0);
 #pragma unroll
                 for (int q = 0; q < kCBatch; ++q) {
                     if (s0 + q < nc) {
-                        const int row = __builtin_amdgcn_readlane(rrow, s0 + q);
+                        const int row = uniform(e[q].row);
                         if (row != cur) {
                             close_to(row);
                             if (__all(sc.found() || !row_ok)) {
@@ -469,12 +474,13 @@ __global__ __launch_bounds__(256) void conv_fwd_kernel(LifConst C, ConvGeom g, i
                                 break;
                             }
                         }
-                        aL = fmaf(w[q], rdl(Lv, s0 + q), aL);
-                        aR = fmaf(w[q], rdl(Rv, s0 + q), aR);
+                        aL = fmaf(w[q], e[q].L, aL);
+                        aR = fmaf(w[q], e[q].R, aR);
                     }
                 }
                 if (done) break;
             }
+            __builtin_amdgcn_wave_barrier();
         }
     }
     if (!done) close_to(R - 1);

@@ -104,8 +104,9 @@ LifConst make_const(const dstd_lif_params *p) {
     C.beta = (float)exp(-dt / ti);
     C.k_dt = (float)kern_d(kind, tv, ti, dt);
     C.inv_em1 = (kind == dstd::kGeneral) ? (float)(1.0 / expm1(-kap * dt)) : 0.f;
-    C.kmax_dt = (float)kern_d(kind, tv, ti, std::min(dt, upk));
-    C.kmax_last = (float)kern_d(kind, tv, ti, std::min(last, upk));
+    C.kmax_dt_d = kern_d(kind, tv, ti, std::min(dt, upk));
+    C.kmax_last_d = kern_d(kind, tv, ti, std::min(last, upk));
+    C.theta_lo_d = (double)p->threshold / 1.0001;
     C.inv_dt = (float)(1.0 / dt);
     C.e_mdt = (float)exp(-dt / ti);
     C.inv_D = (kind == dstd::kInfTau) ? (float)(-1.0 / expm1(-dt / ti)) : 0.f;

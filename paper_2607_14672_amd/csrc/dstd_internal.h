@@ -39,8 +39,6 @@ struct LifConst {
     float alpha, beta;     // exp(-dt/tv), exp(-dt/ti): one-interval decays
     float k_dt;            // K(dt)
     float inv_em1;         // 1/expm1(-kappa*dt)  (< 0)
-    float kmax_dt;         // max of K on [0, dt]
-    float kmax_last;       // max of K on [0, last_len]
     float theta;           // V_th
     float t0, dt;          // grid T_m = t0 + m*dt
     float last_len;        // t_max - T_M (may be +inf)
@@ -55,6 +53,9 @@ struct LifConst {
     // closed-form rows: 1/dt, and for (inf, tau) e^{-dt/tau} and
     // 1/(1 - e^{-dt/tau})
     float inv_dt, e_mdt, inv_D;
+    // the scan's interval filter in fp64: max K on [0, dt] and on the last
+    // interval, and theta / 1.0001 (the filter's margin)
+    double kmax_dt_d, kmax_last_d, theta_lo_d;
 };
 
 template <int KS> __device__ __forceinline__ int kind_of(const LifConst &C) {
@@ -334,13 +335,18 @@ struct Scan {
         Id += static_cast<double>(w);
         const double vn_d = fma(Vd, C.alpha_d, Id * C.k_dt_d);
         if (qf < 0) {
-            const Seg s{static_cast<float>(Vd), static_cast<float>(Id)};
             const bool last = (q == C.M);
-            const float kmax = last ? C.kmax_last : C.kmax_dt;
-            // v(u) = V e^{-u/tv} + I K(u) <= max(V,0) + max(I,0) max K (max K
-            // is +inf on the open last interval of the (inf, inf) row)
-            const float ub = fmaxf(s.V, 0.f) + (s.I > 0.f ? s.I * kmax : 0.f);
-            if (ub * 1.0001f >= C.theta) {
+            // v(u) = V e^{-u/tv} + I K(u) <= max(V,0) + max(I,0) max K, tested
+            // on the fp64 state against theta with a 1e-4 margin (only
+            // intervals that pass are analysed; max K is +inf on the open
+            // last interval of the (inf, inf) row, where I = 0 must not give
+            // inf * 0)
+            const double kmax = last ? C.kmax_last_d : C.kmax_dt_d;
+            const double vpos = fmax(Vd, 0.0);
+            const double ub = (kind == kInfInf) ? ((Id > 0.0) ? fma(Id, kmax, vpos) : vpos)
+                                                : fma(fmax(Id, 0.0), kmax, vpos);
+            if (ub >= C.theta_lo_d) {
+                const Seg s{static_cast<float>(Vd), static_cast<float>(Id)};
                 const float len = last ? C.last_len : C.dt;
                 const bool fin = !last || isfinite(C.last_len);
                 float vend = -INFINITY;

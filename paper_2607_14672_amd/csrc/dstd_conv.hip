@@ -130,6 +130,7 @@ __device__ void sort_cell_row(const LifConst &C, const ConvGeom &g, const float 
     const int cpi = (g.PC < kWave) ? kWave / g.PC : 1;  // cells per pass
     const int lsub = (g.PC < kWave) ? lane / g.PC : 0;
     const int lj = (g.PC < kWave) ? lane % g.PC : lane;
+    bool has = false;
     for (int i0 = 0; wave + nw * i0 < g.Wp; i0 += cpi) {
         const int px = wave + nw * (i0 + lsub);
         const bool cell_ok = lsub < cpi && px < g.Wp;
@@ -137,11 +138,29 @@ __device__ void sort_cell_row(const LifConst &C, const ConvGeom &g, const float 
             const int j = j0 + lj;
             if (cell_ok && j < g.PC) {
                 const int r = bin_row(C, t_at(px, j));
-                if (r >= 0) atomicAdd(&hist[r * g.Wp + px], 1);
+                if (r >= 0) {
+                    atomicAdd(&hist[r * g.Wp + px], 1);
+                    has = true;
+                }
             }
         }
     }
-    __syncthreads();
+    if (!__syncthreads_or(has)) {
+        // no input of this cell row has events: empty buckets, and (for dW)
+        // every input's event row -1
+        int *off0 = cs.off + static_cast<int64_t>(cr) * (nb + 1);
+        for (int f = threadIdx.x; f <= nb; f += blockDim.x) off0[f] = 0;
+        if (ev.row) {
+            const int per = g.Wp * g.PC;
+            const int64_t rb0 = static_cast<int64_t>(cr) * per;
+            for (int t = threadIdx.x; t < per; t += blockDim.x) {
+                ev.row[rb0 + t] = -1;
+                ev.L[rb0 + t] = 0.f;
+                ev.R[rb0 + t] = 0.f;
+            }
+        }
+        return;
+    }
     // exclusive prefix over the buckets in (r, px) order: per-thread chunk
     // sums, scanned by wave 0 (four per lane), then each chunk in order
     const int chunk = (nb + blockDim.x - 1) / blockDim.x;
@@ -596,11 +615,13 @@ __global__ __launch_bounds__(256) void conv_dtp_kernel(LifConst C, ConvGeom g, i
                                                        ConvSorted cs,
                                                        const float *__restrict__ gam,
                                                        const float *__restrict__ uq,
-                                                       const int *__restrict__ qv) {
+                                                       const int *__restrict__ qv,
+                                                       const int *__restrict__ live) {
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = uniform(threadIdx.x >> 6);
     const int64_t p = static_cast<int64_t>(blockIdx.x) * (blockDim.x >> 6) + wave;
     if (p >= n_pos) return;  // wave-uniform; no block barrier below
+    if (*as_const(live + p) == 0) return;  // no channel here passes gradient
     const int R = rows_of(C);
     const int KT = g.KH * g.KW;
     PosWalk<KHT> wk;
@@ -1051,13 +1072,13 @@ hipError_t launch_conv_backward(const LifConst &C, const ConvGeom &g, int64_t B,
                 hipLaunchKernelGGL(conv_bprep_kernel<uint16_t>, dim3(blocks), dim3(256), lds, st, C,
                                    g, n_cr, n_gr, n_z, n_dq, t_in, cs, ev, n_pos, t_out, slope,
                                    q_idx, grad_t, sf, ws.gam, ws.uq, ws.q,
-                                   grad_W ? ws.live : nullptr, grad_t_in, n_in,
+                                   ws.live, grad_t_in, n_in,
                                    static_cast<const uint16_t *>(W), ws.wt);
             else
                 hipLaunchKernelGGL(conv_bprep_kernel<float>, dim3(blocks), dim3(256), lds, st, C,
                                    g, n_cr, n_gr, n_z, n_dq, t_in, cs, ev, n_pos, t_out, slope,
                                    q_idx, grad_t, sf, ws.gam, ws.uq, ws.q,
-                                   grad_W ? ws.live : nullptr, grad_t_in, n_in,
+                                   ws.live, grad_t_in, n_in,
                                    static_cast<const float *>(W), ws.wt);
         }
         if ((e = hipGetLastError()) != hipSuccess) return e;
@@ -1102,7 +1123,7 @@ hipError_t launch_conv_backward(const LifConst &C, const ConvGeom &g, int64_t B,
         ProfScope prof("conv_dtp", st);
 #define DTP_LAUNCH_K(KHV, NTV, KSV)                                                           \
     hipLaunchKernelGGL((conv_dtp_kernel<KHV, NTV, KSV>), grid, dim3(waves * kWave), 0, st, C,  \
-                       g, n_pos, ws.wt, ws.srt, ws.gam, ws.uq, ws.q)
+                       g, n_pos, ws.wt, ws.srt, ws.gam, ws.uq, ws.q, ws.live)
 #define DTP_LAUNCH(KHV, NTV)                                              \
     do {                                                                  \
         if (C.kind == kGeneral) DTP_LAUNCH_K(KHV, NTV, kGeneral);         \

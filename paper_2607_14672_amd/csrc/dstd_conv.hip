@@ -676,25 +676,15 @@ __global__ __launch_bounds__(256) void conv_dtp_kernel(LifConst C, ConvGeom g, i
                         }
                         v[kk] = acc;
                     }
-                    // channel sums (butterfly; every lane ends with the total)
-#pragma unroll
-                    for (int m = kWave / 2; m >= 1; m >>= 1) {
-#pragma unroll
-                        for (int kk = 0; kk < kCBatch; ++kk) v[kk] += __shfl_xor(v[kk], m);
+                    // channel sums: lane 8kk ends with record kk's total and
+                    // stores it as the record's partial for its tap
+                    static_assert(kCBatch == 8, "wave_sum8 reduces eight records");
+                    const float tot = wave_sum8(v, lane);
+                    const int kl = lane >> 3;
+                    if ((lane & 7) == 0 && kl < nk) {
+                        const int pxl = cs.px[o + kl];
+                        cs.P[(o + kl) * KT + ky * g.KW + (pxl - wk.x0)] = tot;
                     }
-                    // lane kk stores record kk's partial for its tap
-                    float mine = 0.f;
-                    int pxl = 0;
-#pragma unroll
-                    for (int kk = 0; kk < kCBatch; ++kk) {
-                        const int pk = as_const(cs.px + o)[kk];
-                        if (lane == kk) {
-                            mine = v[kk];
-                            pxl = pk;
-                        }
-                    }
-                    if (lane < nk && lane < kCBatch)
-                        cs.P[(o + lane) * KT + ky * g.KW + (pxl - wk.x0)] = mine;
                 }
             }
         }

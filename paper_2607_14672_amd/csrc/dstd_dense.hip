@@ -799,16 +799,10 @@ __global__ __launch_bounds__(256) void dtin_rows_kernel(LifConst C, int B, int N
                     for (int t = 0; t < NTW; ++t)
                         v[kk] = fmaf(w[kk][t], fmaf(dl[kk], g0[t], dr[kk] * g1[t]), v[kk]);
             }
-#pragma unroll
-            for (int m = kWave / 2; m >= 1; m >>= 1) {
-#pragma unroll
-                for (int kk = 0; kk < kBatch; ++kk) v[kk] += __shfl_xor(v[kk], m);
-            }
-            float mine = 0.f;
-#pragma unroll
-            for (int kk = 0; kk < kBatch; ++kk)
-                if (lane == kk) mine = v[kk];
-            if (lane < kBatch) part[wave][lane] = mine;
+            // lane 8kk ends with record kk's sum over this wave's neurons
+            static_assert(kBatch == 8, "wave_sum8 reduces eight records");
+            const float tot = wave_sum8(v, lane);
+            if ((lane & 7) == 0) part[wave][lane >> 3] = tot;
             __syncthreads();
             if (wave == 0 && lane < nk) {
                 int jl = 0;

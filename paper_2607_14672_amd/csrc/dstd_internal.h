@@ -465,6 +465,46 @@ struct Scan {
 
 __device__ __forceinline__ int uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }
 
+// Eight per-lane values, each summed over the 64 lanes of the wave; the
+// totals come back scattered: every lane of the group 8k .. 8k+7 holds the
+// total of v[k]. Each halving step exchanges half of the values still held:
+// lanes l and l+32 (permlane32 swap: v[k] stays in the low half, v[k+4] in
+// the high half), then the 16-lane rows (permlane16 swap), then lanes l and
+// l^8 (DPP rotate by 8 within a row); the 8-lane groups finish with DPP quad
+// permutes and the half-row mirror. 18 VALU where eight butterflies take 96.
+// The summation order is fixed, so the totals are deterministic. Needs all
+// 64 lanes active.
+template <int kCtrl>
+__device__ __forceinline__ float dpp_c(float v) {
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), kCtrl, 0xF, 0xF, false));
+}
+__device__ __forceinline__ float wave_sum8(const float (&v)[8], int lane) {
+    float s[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v[k]), __float_as_uint(v[k + 4]),
+                                                        false, false);
+        s[k] = __uint_as_float(r[0]) + __uint_as_float(r[1]);
+    }
+    // lanes 0-31: v[0..3] over lane pairs (l, l+32); lanes 32-63: v[4..7]
+    float t[2];
+#pragma unroll
+    for (int k = 0; k < 2; ++k) {
+        const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(s[k]), __float_as_uint(s[k + 2]),
+                                                        false, false);
+        t[k] = __uint_as_float(r[0]) + __uint_as_float(r[1]);
+    }
+    // rows 0..3 of 16 lanes: t[0] holds v[0], v[2], v[4], v[6]; t[1] holds
+    // v[1], v[3], v[5], v[7]
+    const bool hi = (lane & 8) != 0;
+    const float keep = hi ? t[1] : t[0], send = hi ? t[0] : t[1];
+    float u = keep + dpp_c<0x128>(send);  // row_ror:8
+    u += dpp_c<0xB1>(u);                  // quad_perm [1,0,3,2]
+    u += dpp_c<0x4E>(u);                  // quad_perm [2,3,0,1]
+    u += dpp_c<0x141>(u);                 // row_half_mirror
+    return u;
+}
+
 // Raw buffer access: a per-lane byte offset plus a wave-uniform (scalar)
 // byte offset. Every caller keeps both offsets inside `bytes` (indices are
 // clamped); the descriptor's range check is only a backstop.

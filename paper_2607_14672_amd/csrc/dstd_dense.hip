@@ -357,11 +357,12 @@ __global__ __launch_bounds__(256) void fwd_sorted_kernel(LifConst C, int B, int 
 // stored apart (first row's L sums, last row's R sums, per wave) and added
 // by the scanning wave. The sums, and their order, are those of the
 // single-wave walk; one value per point halves the LDS a tile needs.
+// LDS is tile-minor (point, tile, lane): a row close writes its NT tiles
+// from one address with immediate offsets.
 constexpr int kRowWaves = 4;
 constexpr int kRowLdsCap = 48 * 1024;  // LDS budget per block when choosing NT
 constexpr int kRowsMaxM = 64;
-constexpr int kRowChunk = 32;  // records per vector load; the lookahead stays within kSortPad
-constexpr int kRowSub = 8;     // records whose NT tile loads are in flight together
+constexpr int kRowSub = 8;  // records per scalar load group; their NT tile loads fly together
 
 template <typename WT, int NT, int KS>
 __global__ __launch_bounds__(kRowWaves * 64) void fwd_rows_kernel(LifConst C, int N_in, int N_out,
@@ -370,17 +371,18 @@ __global__ __launch_bounds__(kRowWaves * 64) void fwd_rows_kernel(LifConst C, in
                                                                   float *__restrict__ t_out,
                                                                   float *__restrict__ slope,
                                                                   int *__restrict__ q_idx) {
-    // LDS: P[NT][R][64] point sums, BL[NT][kRowWaves][64] and
-    // BR[NT][kRowWaves][64] range-boundary halves, span[2][kRowWaves] ranges
+    // LDS: P[R][NT][64] point sums, BL[kRowWaves][NT][64] and
+    // BR[kRowWaves][NT][64] range-boundary halves, span[2][kRowWaves] ranges
     extern __shared__ float rsum[];
+    constexpr int kPt = NT * kWave;  // floats per point (all tiles)
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = uniform(threadIdx.x >> 6);
     const int b = blockIdx.y;
     const int R = rows_of(C);
     float *P = rsum;
-    float *BL = rsum + NT * R * kWave;
-    float *BR = BL + NT * kRowWaves * kWave;
-    int *span = reinterpret_cast<int *>(BR + NT * kRowWaves * kWave);
+    float *BL = rsum + R * kPt;
+    float *BR = BL + kRowWaves * kPt;
+    int *span = reinterpret_cast<int *>(BR + kRowWaves * kPt);
     const int *rs = srt.rs + static_cast<int64_t>(b) * (R + 1);
     const int n = *as_const(rs + R);
     // range w: the rows holding records [w*n/kRowWaves, (w+1)*n/kRowWaves)
@@ -402,22 +404,34 @@ __global__ __launch_bounds__(kRowWaves * 64) void fwd_rows_kernel(LifConst C, in
         aR[t] = 0.f;
         cy[t] = 0.f;
     }
-    // close rows cur .. target-1 of this wave's range: point cur-1 gets this
-    // row's L sums plus the previous row's R sums (cy)
+    // close row cur (target > cur): point cur-1 gets this row's L sums plus
+    // the previous row's R sums (cy); rows cur+1 .. target-1 have no records,
+    // so point cur is row cur's R sums alone and the points after it are 0
     auto close_to = [&](int target) {
-        while (cur < target) {
+        float *d = ((cur == r_lo) ? BL + wave * kPt : P + (cur - 1) * kPt) + lane;
 #pragma unroll
-            for (int t = 0; t < NT; ++t) {
-                if (cur == r_lo)
-                    BL[(t * kRowWaves + wave) * kWave + lane] = aL[t];
-                else
-                    P[(t * R + cur - 1) * kWave + lane] = aL[t] + cy[t];
-                cy[t] = aR[t];
-                aL[t] = 0.f;
-                aR[t] = 0.f;
+        for (int t = 0; t < NT; ++t) d[t * kWave] = aL[t] + cy[t];
+        if (target > cur + 1) {
+            float *e = P + cur * kPt + lane;
+#pragma unroll
+            for (int t = 0; t < NT; ++t) e[t * kWave] = aR[t];
+            for (int r = cur + 2; r < target; ++r) {
+                float *z = P + (r - 1) * kPt + lane;
+#pragma unroll
+                for (int t = 0; t < NT; ++t) z[t * kWave] = 0.f;
             }
-            ++cur;
+#pragma unroll
+            for (int t = 0; t < NT; ++t) cy[t] = 0.f;
+        } else {
+#pragma unroll
+            for (int t = 0; t < NT; ++t) cy[t] = aR[t];
         }
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+            aL[t] = 0.f;
+            aR[t] = 0.f;
+        }
+        cur = target;
     };
     const __amdgpu_buffer_rsrc_t wr =
         make_rsrc(Wt, static_cast<uint32_t>(static_cast<int64_t>(N_in) * N_out * sizeof(WT)));
@@ -429,61 +443,63 @@ __global__ __launch_bounds__(kRowWaves * 64) void fwd_rows_kernel(LifConst C, in
     }
     const int rstride = N_out * static_cast<int>(sizeof(WT));
     const int jmax = max(N_in - 1, 0);
-    // Records come kRowChunk at a time, one per lane, with vector loads (the
-    // next chunk's in flight while this one is summed); each record's
-    // fields are broadcast with readlane, its weight-row offset precomputed
-    // per lane (clamped: lanes past the range read stale records).
-    auto rdl = [](float v, int k) { return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), k)); };
-    int jn = min(max(ej[k_lo + lane], 0), jmax) * rstride, rn = er[k_lo + lane];
-    float Ln = eL[k_lo + lane], Rn = eR[k_lo + lane];
-    for (int c0 = k_lo; c0 < k_hi; c0 += kRowChunk) {
-        const int jc = jn, rc = rn;
-        const float Lc = Ln, Rc = Rn;
-        jn = min(max(ej[c0 + kRowChunk + lane], 0), jmax) * rstride;
-        rn = er[c0 + kRowChunk + lane];
-        Ln = eL[c0 + kRowChunk + lane];
-        Rn = eR[c0 + kRowChunk + lane];
-        const int nc = min(kRowChunk, k_hi - c0);
-        const bool one_row = nc == kRowChunk && __builtin_amdgcn_readlane(rc, kRowChunk - 1) == cur;
+    // Record fields come through the scalar cache, kRowSub records per load
+    // (the next group's in flight while this one is summed; reads past the
+    // range stay inside the sorted lists' padding and are not summed). The
+    // group's weight rows, all NT tiles, are loaded together.
+    int nj[kRowSub], nr[kRowSub];
+    float nL[kRowSub], nR[kRowSub];
+    auto fetch = [&](int k) {
 #pragma unroll
-        for (int s0 = 0; s0 < kRowChunk; s0 += kRowSub) {
-            float w[kRowSub][NT];
+        for (int kk = 0; kk < kRowSub; ++kk) {
+            nj[kk] = as_const(ej + k)[kk];
+            nr[kk] = as_const(er + k)[kk];
+            nL[kk] = as_const(eL + k)[kk];
+            nR[kk] = as_const(eR + k)[kk];
+        }
+    };
+    fetch(k_lo);
+    for (int k0 = k_lo; k0 < k_hi; k0 += kRowSub) {
+        int cr[kRowSub];
+        float cL[kRowSub], cR[kRowSub], w[kRowSub][NT];
+#pragma unroll
+        for (int kk = 0; kk < kRowSub; ++kk) {
+            const int jo = min(max(nj[kk], 0), jmax) * rstride;
+#pragma unroll
+            for (int t = 0; t < NT; ++t) w[kk][t] = BufLoad<WT>::get(wr, voff[t], jo);
+            cr[kk] = nr[kk];
+            cL[kk] = nL[kk];
+            cR[kk] = nR[kk];
+        }
+        fetch(k0 + kRowSub);
+        const int nk = min(kRowSub, k_hi - k0);
+        if (nk == kRowSub && cr[kRowSub - 1] == cur) {
+            // common case: the whole group continues the current row
 #pragma unroll
             for (int kk = 0; kk < kRowSub; ++kk)
 #pragma unroll
-                for (int t = 0; t < NT; ++t)
-                    w[kk][t] = BufLoad<WT>::get(wr, voff[t], __builtin_amdgcn_readlane(jc, s0 + kk));
-            if (one_row) {
+                for (int t = 0; t < NT; ++t) {
+                    aL[t] = fmaf(w[kk][t], cL[kk], aL[t]);
+                    aR[t] = fmaf(w[kk][t], cR[kk], aR[t]);
+                }
+        } else {
 #pragma unroll
-                for (int kk = 0; kk < kRowSub; ++kk) {
-                    const float l = rdl(Lc, s0 + kk), r = rdl(Rc, s0 + kk);
+            for (int kk = 0; kk < kRowSub; ++kk) {
+                if (kk < nk) {
+                    if (cr[kk] != cur) close_to(cr[kk]);
 #pragma unroll
                     for (int t = 0; t < NT; ++t) {
-                        aL[t] = fmaf(w[kk][t], l, aL[t]);
-                        aR[t] = fmaf(w[kk][t], r, aR[t]);
-                    }
-                }
-            } else {
-#pragma unroll
-                for (int kk = 0; kk < kRowSub; ++kk) {
-                    if (s0 + kk < nc) {
-                        const int row = __builtin_amdgcn_readlane(rc, s0 + kk);
-                        if (row != cur) close_to(row);
-                        const float l = rdl(Lc, s0 + kk), r = rdl(Rc, s0 + kk);
-#pragma unroll
-                        for (int t = 0; t < NT; ++t) {
-                            aL[t] = fmaf(w[kk][t], l, aL[t]);
-                            aR[t] = fmaf(w[kk][t], r, aR[t]);
-                        }
+                        aL[t] = fmaf(w[kk][t], cL[kk], aL[t]);
+                        aR[t] = fmaf(w[kk][t], cR[kk], aR[t]);
                     }
                 }
             }
         }
     }
-    close_to(r_hi);
+    if (r_hi > cur) close_to(r_hi);
     if (r_hi > r_lo) {
 #pragma unroll
-        for (int t = 0; t < NT; ++t) BR[(t * kRowWaves + wave) * kWave + lane] = cy[t];
+        for (int t = 0; t < NT; ++t) BR[wave * kPt + t * kWave + lane] = cy[t];
     }
     if (lane == 0) {
         span[wave] = r_lo;
@@ -500,23 +516,23 @@ __global__ __launch_bounds__(kRowWaves * 64) void fwd_rows_kernel(LifConst C, in
     // 0's range always holds row 0 and is never empty) is w's first-row L
     // sums plus the last-row R sums of the nonempty range before it; this
     // wave writes it into its own tile's slot (no other wave stores there)
-    float *tp = P + tile * R * kWave;
-    const float *tbl = BL + tile * kRowWaves * kWave;
-    const float *tbr = BR + tile * kRowWaves * kWave;
+    float *tp = P + tile * kWave + lane;
+    const float *tbl = BL + tile * kWave + lane;
+    const float *tbr = BR + tile * kWave + lane;
     int prev = 0;
 #pragma unroll
     for (int w = 1; w < kRowWaves; ++w) {
         const int lo = uniform(span[w]), hi = uniform(span[kRowWaves + w]);
         if (hi > lo) {
-            tp[(lo - 1) * kWave + lane] = tbl[w * kWave + lane] + tbr[prev * kWave + lane];
+            tp[(lo - 1) * kPt] = tbl[w * kPt] + tbr[prev * kPt];
             prev = w;
         }
     }
     Scan<KS> sc;
-    float wn = tp[lane];  // next grid point's sum, read ahead
+    float wn = tp[0];  // next grid point's sum, read ahead
     for (int m = 0; m <= C.M; ++m) {
         const float wc = wn;
-        if (m < C.M) wn = tp[(m + 1) * kWave + lane];
+        if (m < C.M) wn = tp[(m + 1) * kPt];
         sc.step(C, m, wc);
         if (__all(sc.found() || !row_ok)) break;
     }

@@ -11,6 +11,7 @@
 // and reduces dW over the batch with per-input events.
 #include "dstd_internal.h"
 #include "dstd_kernels.h"
+#include "dstd_lif.h"
 #include "dstd_profile.h"
 
 #include <algorithm>
@@ -23,12 +24,16 @@ namespace dstd {
 // (with deriv: the derivatives dL, dR in place of L, R), plus the row starts.
 // One block of kSortWaves wavefronts per sample; wave w owns a contiguous
 // range of inputs. Row histograms per wave (integer LDS atomics, order-free)
-// give every (row, wave) pair its start offset; each wave then places its
-// inputs 64 at a time, each lane ranked among the lanes of its batch with the
-// same row (one ballot per distinct row). The fixed order keeps every sum of
+// give every (row, wave) pair its start offset (wave 0 scans the row totals
+// across its lanes); each wave then places its inputs 64 at a time: a lane's
+// rank among the lanes of its batch with the same row comes from a match
+// mask built bit by bit from ballots of the row index, and the lowest lane
+// of each row advances that row's slot. The fixed order keeps every sum of
 // the forward pass bitwise reproducible.
 constexpr int kSortWaves = 8;
 constexpr int kPrepThreads = kSortWaves * 64;
+constexpr int kRowBits = 9;  // row + 1 < 512 covers R = M + 3 rows for every M <= 256
+static_assert(DSTD_MAX_M + 3 < (1 << kRowBits), "row keys must fit kRowBits");
 
 // Optional per-input outputs of the sort, in input order [B][N_in]: the
 // events (row -1: none) for the dW reduction, and an array set to zero
@@ -55,15 +60,24 @@ __device__ void sort_sample(const LifConst &C, int b, int N_in, const float *__r
         if (r >= 0) atomicAdd(&hist[wave * R + r], 1);
     }
     __syncthreads();
-    for (int r = threadIdx.x; r < R; r += blockDim.x) {
-        int t = 0;
-        for (int w = 0; w < kSortWaves; ++w) t += hist[w * R + r];
-        rowstart[r + 1] = t;
-    }
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        for (int r = 1; r <= R; ++r) rowstart[r] += rowstart[r - 1];
-        n_valid[b] = rowstart[R];
+    if (wave == 0) {
+        // rowstart[r + 1] = events in rows <= r: an inclusive scan of the row
+        // totals, 64 rows per pass
+        int acc = 0;
+        for (int r0 = 0; r0 < R; r0 += kWave) {
+            const int r = r0 + lane;
+            int v = 0;
+            if (r < R)
+                for (int w = 0; w < kSortWaves; ++w) v += hist[w * R + r];
+#pragma unroll
+            for (int m = 1; m < kWave; m <<= 1) {
+                const int o = __shfl_up(v, m);
+                if (lane >= m) v += o;
+            }
+            if (r < R) rowstart[r + 1] = acc + v;
+            acc += __shfl(v, kWave - 1);
+        }
+        if (lane == 0) n_valid[b] = acc;
     }
     __syncthreads();
     for (int r = threadIdx.x; r <= R; r += blockDim.x)
@@ -94,18 +108,21 @@ __device__ void sort_sample(const LifConst &C, int b, int N_in, const float *__r
             }
             if (xo.zero) xo.zero[ib + j] = 0.f;
         }
+        // lanes with the same row: agree with this lane on every bit of r + 1
+        // (lanes without an event, r + 1 = 0, match only each other)
+        const unsigned key = static_cast<unsigned>(r + 1);
+        uint64_t same = ~0ull;
+#pragma unroll
+        for (int bit = 0; bit < kRowBits; ++bit) {
+            const uint64_t ones = __ballot((key >> bit) & 1u);
+            same &= ((key >> bit) & 1u) ? ones : ~ones;
+        }
+        const int rank = __popcll(same & below);
         int pos = 0;
-        uint64_t todo = __ballot(r >= 0);
-        while (todo) {
-            const int lead = __ffsll(static_cast<unsigned long long>(todo)) - 1;
-            const int rl = __builtin_amdgcn_readlane(r, lead);
-            const uint64_t same = __ballot(r == rl);
-            const int base = next[rl];
-            if (r == rl) pos = base + __popcll(same & below);
-            __builtin_amdgcn_wave_barrier();
-            if (lane == lead) next[rl] = base + __popcll(same);
-            __builtin_amdgcn_wave_barrier();
-            todo &= ~same;
+        if (r >= 0) {
+            const int base = next[r];
+            pos = base + rank;
+            if (rank == 0) next[r] = base + __popcll(same);
         }
         if (r >= 0) {
             const int64_t o = ob + pos;

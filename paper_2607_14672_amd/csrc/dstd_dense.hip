@@ -852,6 +852,88 @@ __global__ __launch_bounds__(256) void dtin_rows_kernel(LifConst C, int B, int N
     }
 }
 
+// dt_in for a layer of at most 64 neurons (one tile, lane = neuron): the
+// block's four waves take turns over its range's records, kBatch at a time,
+// so no wave walks an empty tile and no block-wide combine is needed. G at
+// the grid points the range's rows read (points r_lo - 1 .. r_hi - 1) is
+// evaluated once per block into LDS; record k of a batch adds
+// W[i, j] (dL G[r-1] + dR G[r]) on its lane and the wave sums the lanes.
+// The per-record arithmetic and its order are those of dtin_rows_kernel.
+template <typename WT, int KS>
+__global__ __launch_bounds__(256) void dtin_tile_kernel(LifConst C, int B, int N_in, int N_out,
+                                                        const WT *__restrict__ Wt, SortedEv srt,
+                                                        const float *__restrict__ gam,
+                                                        const float *__restrict__ uq,
+                                                        const int *__restrict__ qv,
+                                                        float *__restrict__ dt_in, RedJob red) {
+    extern __shared__ float gtab[];  // [r - r_lo][64]: G at point r - 1, r_lo <= r <= r_hi
+    if (static_cast<int>(blockIdx.y) >= B) {
+        const int64_t k = (static_cast<int64_t>(blockIdx.y - B) * gridDim.x + blockIdx.x) * blockDim.x +
+                          threadIdx.x;
+        if (k < red.n) {
+            float s = 0.f;
+            for (int z = 0; z < red.nsplit; ++z) s += red.part[static_cast<int64_t>(z) * red.n + k];
+            red.out[k] = red.dq ? s + red.dq[k / red.row_len] : s;
+        }
+        return;
+    }
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = uniform(threadIdx.x >> 6);
+    const int nw = blockDim.x >> 6;
+    const int range = blockIdx.x;
+    const int b = blockIdx.y;
+    const int R = rows_of(C);
+    const int *rs = srt.rs + static_cast<int64_t>(b) * (R + 1);
+    const int n = *as_const(rs + R);
+    const RowRange rg = row_range(rs, R, n, static_cast<int>((static_cast<int64_t>(n) * range) / kDtRanges),
+                                  static_cast<int>((static_cast<int64_t>(n) * (range + 1)) / kDtRanges),
+                                  range == 0, range == kDtRanges - 1, lane);
+    const int r_lo = uniform(rg.ra), r_hi = uniform(rg.rb);
+    const int k_lo = uniform(rg.ka), k_hi = uniform(rg.kb);
+    if (k_lo == k_hi) return;  // block-uniform: no records
+    const int64_t nb = static_cast<int64_t>(b) * N_out;
+    const bool ok = lane < N_out;
+    const int ic = min(lane, N_out - 1);
+    const float gm = ok ? gam[nb + ic] : 0.f;
+    const float ua = ok ? uq[nb + ic] : 0.f;
+    const int qa = ok ? qv[nb + ic] : -1;
+    for (int r = r_lo + wave; r <= r_hi; r += nw) gtab[(r - r_lo) * kWave + lane] = g_at<KS>(C, gm, ua, qa, r - 1);
+    __syncthreads();
+    const int64_t eo = static_cast<int64_t>(b) * srt.stride;
+    const int *ej = srt.j + eo;
+    const int *er = srt.r + eo;
+    const float *edl = srt.L + eo;
+    const float *edr = srt.R + eo;
+    const __amdgpu_buffer_rsrc_t wr =
+        make_rsrc(Wt, static_cast<uint32_t>(static_cast<int64_t>(N_in) * N_out * sizeof(WT)));
+    const int rstride = N_out * static_cast<int>(sizeof(WT));
+    const unsigned jmax = static_cast<unsigned>(max(N_in - 1, 0));
+    const int voff = ic * static_cast<int>(sizeof(WT));
+    static_assert(kBatch == 8, "wave_sum8 reduces eight records");
+    for (int k0 = k_lo + wave * kBatch; k0 < k_hi; k0 += nw * kBatch) {
+        const int nk = min(kBatch, k_hi - k0);
+        float w[kBatch], v[kBatch];
+#pragma unroll
+        for (int kk = 0; kk < kBatch; ++kk) {
+            const int jo = static_cast<int>(min(static_cast<unsigned>(as_const(ej + k0)[kk]), jmax)) * rstride;
+            w[kk] = BufLoad<WT>::get(wr, voff, jo);
+        }
+#pragma unroll
+        for (int kk = 0; kk < kBatch; ++kk) {
+            v[kk] = 0.f;
+            if (kk < nk) {
+                const int r = as_const(er + k0)[kk];
+                const float g0 = gtab[(r - r_lo) * kWave + lane];
+                const float g1 = gtab[(r - r_lo + 1) * kWave + lane];
+                v[kk] = fmaf(w[kk], fmaf(as_const(edl + k0)[kk], g0, as_const(edr + k0)[kk] * g1), 0.f);
+            }
+        }
+        const float tot = wave_sum8(v, lane);
+        const int kl = lane >> 3;
+        if ((lane & 7) == 0 && kl < nk) dt_in[static_cast<int64_t>(b) * N_in + ej[k0 + kl]] = tot;
+    }
+}
+
 // ---------------------------------------------------------------- losses --
 // One block per sample; block reductions run over a fixed LDS tree, so the
 // per-sample losses (loss[1 + b]) and their fixed-order sum (loss[0]) are
@@ -1036,8 +1118,12 @@ hipError_t launch_forward(const LifConst &C, int64_t B, int64_t N_in, int64_t N_
     return hipGetLastError();
 }
 
-// neuron tile: 64, or 32 where two 64-wide G buffers would pass 48 KB of LDS
-static int dw_ti(int M) {
+// neuron tile: 64, or 32 where two 64-wide G buffers would pass 48 KB of
+// LDS; narrower (16 or 32) where the layer has no more neurons than that, so
+// a sample's G reads and multiply-adds are not spent on empty columns
+static int dw_ti(int M, int64_t N_out) {
+    if (N_out <= 16) return 16;
+    if (N_out <= 32) return 32;
     return (2 * (M + 4) * 65 * 4 <= 48 * 1024) ? 64 : 32;
 }
 
@@ -1051,7 +1137,7 @@ static int dw_nper(int M, int ti) {
 DwPlan plan_dw(int64_t B, int64_t N_in, int64_t N_out, int M) {
     DwPlan p;
     p.waves = 4;
-    p.jw = dw_ti(M);
+    p.jw = dw_ti(M, N_out);
     int64_t tiles = ((N_in + 255) / 256) * ((N_out + p.jw - 1) / p.jw);
     p.nsplit = 1;
     // aim for >= 4 blocks per CU (256 CUs); keep >= 4 samples per split
@@ -1083,6 +1169,10 @@ static hipError_t launch_dw(const LifConst &C, const DwPlan &p, int64_t B, int64
         if (nper == 9) DW_LAUNCH(64, 9);
         else if (nper == 17) DW_LAUNCH(64, 17);
         else DW_LAUNCH(64, 33);
+    } else if (ti == 16) {
+        if (nper == 9) DW_LAUNCH(16, 9);
+        else if (nper == 17) DW_LAUNCH(16, 17);
+        else DW_LAUNCH(16, 33);
     } else {
         if (nper == 9) DW_LAUNCH(32, 9);
         else if (nper == 17) DW_LAUNCH(32, 17);
@@ -1144,8 +1234,27 @@ hipError_t launch_backward(const LifConst &C, int64_t B, int64_t N_in, int64_t N
         else if (tpw <= 2) DTR(WTY, 2);                  \
         else DTR(WTY, 4);                                \
     } while (0)
-        if (bf16) DTR_NT(uint16_t);
-        else DTR_NT(float);
+        if (tiles == 1) {
+            // one tile: the waves split the records instead of the tiles
+            const size_t lds = static_cast<size_t>(C.M + 4) * kWave * sizeof(float);  // R + 1 rows
+#define DTT_K(WTY, KSV)                                                                            \
+    hipLaunchKernelGGL((dtin_tile_kernel<WTY, KSV>), grid, dim3(256), lds, st, C,                  \
+                       static_cast<int>(B), static_cast<int>(N_in), static_cast<int>(N_out),       \
+                       static_cast<const WTY *>(ws.wt), ws.srt, ws.gam, ws.uq, ws.q, grad_t_in, red)
+#define DTT(WTY)                                                          \
+    do {                                                                  \
+        if (C.kind == kGeneral) DTT_K(WTY, kGeneral);                     \
+        else DTT_K(WTY, kAnyKind);                                        \
+    } while (0)
+            if (bf16) DTT(uint16_t);
+            else DTT(float);
+#undef DTT
+#undef DTT_K
+        } else if (bf16) {
+            DTR_NT(uint16_t);
+        } else {
+            DTR_NT(float);
+        }
 #undef DTR_NT
 #undef DTR
 #undef DTR_K

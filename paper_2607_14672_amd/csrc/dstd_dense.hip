@@ -695,17 +695,56 @@ __global__ __launch_bounds__(256) void dw_dense_kernel(LifConst C, int B, int N_
 }
 
 // dW[k] = sum of the split partials in split order (+ the row's dead-neuron
-// term dq[k / row_len] when dq is set)
+// term dq[k / row_len] when dq is set). Thread t takes outputs 4t .. 4t+3:
+// one 16-byte load per split where n is a multiple of 4 (every partial
+// then starts 16-byte aligned), with the split loop unrolled so that four
+// splits' loads are in flight together; the additions keep split order.
+__device__ __forceinline__ void reduce_parts4(int64_t n, int nsplit, const float *__restrict__ part,
+                                              const float *__restrict__ dq, int row_len,
+                                              float *__restrict__ out, int64_t t) {
+    const int64_t k = 4 * t;
+    if (k >= n) return;
+    float s[4] = {0.f, 0.f, 0.f, 0.f};
+    if ((n & 3) == 0) {
+        int z = 0;
+        for (; z + 4 <= nsplit; z += 4) {
+            float4 a[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+                a[u] = *reinterpret_cast<const float4 *>(part + static_cast<int64_t>(z + u) * n + k);
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                s[0] += a[u].x;
+                s[1] += a[u].y;
+                s[2] += a[u].z;
+                s[3] += a[u].w;
+            }
+        }
+        for (; z < nsplit; ++z) {
+            const float4 a = *reinterpret_cast<const float4 *>(part + static_cast<int64_t>(z) * n + k);
+            s[0] += a.x;
+            s[1] += a.y;
+            s[2] += a.z;
+            s[3] += a.w;
+        }
+    } else {
+        for (int z = 0; z < nsplit; ++z)
+#pragma unroll
+            for (int c = 0; c < 4; ++c)
+                if (k + c < n) s[c] += part[static_cast<int64_t>(z) * n + k + c];
+    }
+#pragma unroll
+    for (int c = 0; c < 4; ++c)
+        if (k + c < n) out[k + c] = dq ? s[c] + dq[(k + c) / row_len] : s[c];
+}
+
 __global__ __launch_bounds__(256) void reduce_splits_kernel(int64_t n, int nsplit,
                                                             const float *__restrict__ part,
                                                             const float *__restrict__ dq,
                                                             int row_len,
                                                             float *__restrict__ out) {
-    int64_t k = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
-    if (k >= n) return;
-    float s = 0.f;
-    for (int z = 0; z < nsplit; ++z) s += part[static_cast<int64_t>(z) * n + k];
-    out[k] = dq ? s + dq[k / row_len] : s;
+    reduce_parts4(n, nsplit, part, dq, row_len, out,
+                  static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x);
 }
 
 // -------------------------------------------------------- dt_in (rows) --
@@ -735,13 +774,9 @@ __global__ __launch_bounds__(256) void dtin_rows_kernel(LifConst C, int B, int N
                                                         float *__restrict__ dt_in, RedJob red) {
     __shared__ float part[4][kBatch];
     if (static_cast<int>(blockIdx.y) >= B) {
-        const int64_t k = (static_cast<int64_t>(blockIdx.y - B) * gridDim.x + blockIdx.x) * blockDim.x +
-                          threadIdx.x;
-        if (k < red.n) {
-            float s = 0.f;
-            for (int z = 0; z < red.nsplit; ++z) s += red.part[static_cast<int64_t>(z) * red.n + k];
-            red.out[k] = red.dq ? s + red.dq[k / red.row_len] : s;
-        }
+        reduce_parts4(red.n, red.nsplit, red.part, red.dq, red.row_len, red.out,
+                      (static_cast<int64_t>(blockIdx.y - B) * gridDim.x + blockIdx.x) * blockDim.x +
+                          threadIdx.x);
         return;
     }
     const int lane = threadIdx.x & (kWave - 1);
@@ -868,13 +903,9 @@ __global__ __launch_bounds__(256) void dtin_tile_kernel(LifConst C, int B, int N
                                                         float *__restrict__ dt_in, RedJob red) {
     extern __shared__ float gtab[];  // [r - r_lo][64]: G at point r - 1, r_lo <= r <= r_hi
     if (static_cast<int>(blockIdx.y) >= B) {
-        const int64_t k = (static_cast<int64_t>(blockIdx.y - B) * gridDim.x + blockIdx.x) * blockDim.x +
-                          threadIdx.x;
-        if (k < red.n) {
-            float s = 0.f;
-            for (int z = 0; z < red.nsplit; ++z) s += red.part[static_cast<int64_t>(z) * red.n + k];
-            red.out[k] = red.dq ? s + red.dq[k / red.row_len] : s;
-        }
+        reduce_parts4(red.n, red.nsplit, red.part, red.dq, red.row_len, red.out,
+                      (static_cast<int64_t>(blockIdx.y - B) * gridDim.x + blockIdx.x) * blockDim.x +
+                          threadIdx.x);
         return;
     }
     const int lane = threadIdx.x & (kWave - 1);
@@ -1216,7 +1247,7 @@ hipError_t launch_backward(const LifConst &C, int64_t B, int64_t N_in, int64_t N
     if (run_dt) {
         const int tiles = static_cast<int>((N_out + kWave - 1) / kWave);
         const int tpw = (tiles + 3) / 4;  // tiles per wave
-        const int64_t red_rows = (red.n + kDtRanges * 256 - 1) / (kDtRanges * 256);
+        const int64_t red_rows = ((red.n + 3) / 4 + kDtRanges * 256 - 1) / (kDtRanges * 256);
         dim3 grid(kDtRanges, static_cast<unsigned>(B + red_rows));
         ProfScope prof("dtin_rows", st);
 #define DTR_K(WTY, NTV, KSV)                                                                     \
@@ -1262,7 +1293,7 @@ hipError_t launch_backward(const LifConst &C, int64_t B, int64_t N_in, int64_t N
     }
     if (split) {
         ProfScope prof("dw_reduce", st);
-        hipLaunchKernelGGL(reduce_splits_kernel, dim3(static_cast<unsigned>((red.n + 255) / 256)),
+        hipLaunchKernelGGL(reduce_splits_kernel, dim3(static_cast<unsigned>(((red.n + 3) / 4 + 255) / 256)),
                            dim3(256), 0, st, red.n, p.nsplit, ws.part, dq,
                            static_cast<int>(N_in), grad_W);
         return hipGetLastError();

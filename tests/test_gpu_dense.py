@@ -236,11 +236,11 @@ def test_wide_layer_full_size_sampled(dev, M):
 
 
 # ---------------------------------------------------------------- losses --
-def test_softmax_ce_grad(dev):
+@pytest.mark.parametrize("B,N", [(37, 10), (300, 64), (50, 65), (1024, 64), (1025, 64)])
+def test_softmax_ce_grad(dev, B, N):
     import torch
     from paper_2607_14672_amd import dstd
-    rng = np.random.default_rng(1)
-    B, N = 37, 10
+    rng = np.random.default_rng(1 + B + N)
     t = rng.random((B, N)).astype(np.float32) * 2 + 1
     t[rng.random((B, N)) < 0.2] = np.inf
     lab = rng.integers(0, N, B).astype(np.int32)
@@ -261,11 +261,11 @@ def test_softmax_ce_grad(dev):
     np.testing.assert_allclose(loss[1:], per, rtol=1e-5, atol=1e-7)
 
 
-def test_mse_grad(dev):
+@pytest.mark.parametrize("B,N", [(21, 100), (21, 64), (1024, 64), (7, 3)])
+def test_mse_grad(dev, B, N):
     import torch
     from paper_2607_14672_amd import dstd
-    rng = np.random.default_rng(2)
-    B, N = 21, 100
+    rng = np.random.default_rng(2 + B + N)
     t = (rng.random((B, N)) * 2).astype(np.float32)
     t[rng.random((B, N)) < 0.3] = np.inf
     y = (1 + rng.random((B, N))).astype(np.float32)

@@ -578,42 +578,49 @@ __global__ __launch_bounds__(kRowWaves * 64) void fwd_rows_kernel(LifConst C, in
 // inputs without events). The next sample's G values and events are fetched
 // while this one is consumed; a sample whose tile is all zero is skipped.
 // Batch splits write partial sums, reduced in order.
-template <int TI, int NPER, int KS>
-__global__ __launch_bounds__(256) void dw_dense_kernel(LifConst C, int B, int N_in, int N_out,
-                                                        int b_per_split,
-                                                        const float *__restrict__ gam,
-                                                        const float *__restrict__ uq,
-                                                        const int *__restrict__ qv,
-                                                        const int *__restrict__ ev_row,
-                                                        const float *__restrict__ ev_L,
-                                                        const float *__restrict__ ev_R,
-                                                        const float *__restrict__ dq,
-                                                        float *__restrict__ dW_part) {
-    extern __shared__ float gs[];  // [2][R + 1][TI + 1]
+template <int TI, int NPER, int GW, int KS>
+__global__ __launch_bounds__(256 * GW) void dw_dense_kernel(LifConst C, int B, int N_in, int N_out,
+                                                             int b_per_split,
+                                                             const float *__restrict__ gam,
+                                                             const float *__restrict__ uq,
+                                                             const int *__restrict__ qv,
+                                                             const int *__restrict__ ev_row,
+                                                             const float *__restrict__ ev_L,
+                                                             const float *__restrict__ ev_R,
+                                                             const float *__restrict__ dq,
+                                                             float *__restrict__ dW_part) {
+    extern __shared__ float gs[];  // [GW][2][R + 1][TI + 1]
+    __shared__ int wlive[2][4 * GW];
     constexpr int kStr = TI + 1;
     const int R = rows_of(C);
     const int gbuf = (R + 1) * kStr;
-    const int j = blockIdx.x * blockDim.x + threadIdx.x;
+    const int grp = threadIdx.x >> 8;  // sample group of this thread
+    const int tid = threadIdx.x & 255;
+    float *gsg = gs + grp * 2 * gbuf;
+    const int j = blockIdx.x * 256 + tid;
     const int i0 = blockIdx.y * TI;
     const int ni = min(TI, N_out - i0);
-    const int b_lo = blockIdx.z * b_per_split;
-    const int b_hi = min(B, b_lo + b_per_split);
+    // the block's samples [b0, b_end); group g takes b0 + g, b0 + g + GW, ...
+    const int b0 = blockIdx.z * b_per_split;
+    const int b_end = min(B, b0 + b_per_split);
+    const int n_it = (b_per_split + GW - 1) / GW;  // iterations, equal for every group
     const bool j_ok = j < N_in;
     float acc[TI];
 #pragma unroll
     for (int ii = 0; ii < TI; ++ii) acc[ii] = 0.f;
     const int total = R * TI;
     // element c of this thread: row r = r_first + c * (256 / TI), neuron l
-    const int l_own = threadIdx.x % TI, r_first = threadIdx.x / TI;
+    const int l_own = tid % TI, r_first = tid / TI;
     constexpr int kRowStep = 256 / TI;
     const GStep gst = g_step<KS>(C, kRowStep);
     float pre[NPER];
+    auto sample = [&](int it) { return b0 + grp + it * GW; };
     // gradient triple of this thread's neuron in sample b (q = -1: none, or
     // past the block's share); loaded two samples ahead of its use
     struct Tri { float gm, u; int q; };
     auto load_tri = [&](int b) {
         Tri t{0.f, 0.f, -1};
-        if (l_own < ni && b < b_hi) {
+        if (l_own < ni && b < b_end) {
             const int64_t k = static_cast<int64_t>(b) * N_out + i0 + l_own;
             t.gm = gam[k];
             t.u = uq[k];
@@ -631,7 +638,7 @@ __global__ __launch_bounds__(256) void dw_dense_kernel(LifConst C, int B, int N_
     auto store = [&](float *buf) {
 #pragma unroll
         for (int c = 0; c < NPER; ++c) {
-            const int k = threadIdx.x + c * 256;
+            const int k = tid + c * 256;
             if (k < total) {
                 const int r = k / TI, l = k % TI;
                 if (r < R - 1) buf[r * kStr + l] = pre[c];
@@ -643,7 +650,7 @@ __global__ __launch_bounds__(256) void dw_dense_kernel(LifConst C, int B, int N_
         slot = R - 1;
         L = 0.f;
         Rv = 0.f;
-        if (j_ok && b < b_hi) {
+        if (j_ok && b < b_end) {
             const int64_t o = static_cast<int64_t>(b) * N_in + j;
             const int r = ev_row[o];
             if (r >= 0) {
@@ -653,26 +660,36 @@ __global__ __launch_bounds__(256) void dw_dense_kernel(LifConst C, int B, int N_
             }
         }
     };
-    for (int k = threadIdx.x; k < 2 * 2 * kStr; k += blockDim.x)
-        gs[(k / (2 * kStr)) * gbuf + (R - 1) * kStr + k % (2 * kStr)] = 0.f;
+    // whether any thread of this group has a nonzero G tile for the next
+    // sample: wave votes through LDS, double buffered by iteration parity
+    auto group_live = [&](bool v, int par) {
+        const int wv = threadIdx.x >> 6;
+        const bool any = __any(v);
+        if ((threadIdx.x & (kWave - 1)) == 0) wlive[par][wv] = any ? 1 : 0;
+        __syncthreads();
+        const int g0 = grp * 4;
+        return (wlive[par][g0] | wlive[par][g0 + 1] | wlive[par][g0 + 2] | wlive[par][g0 + 3]) != 0;
+    };
+    for (int k = tid; k < 2 * 2 * kStr; k += 256)
+        gsg[(k / (2 * kStr)) * gbuf + (R - 1) * kStr + k % (2 * kStr)] = 0.f;
     bool live = false;
-    if (b_lo < b_hi) {
-        live = fetch(load_tri(b_lo));
-        store(gs);
+    if (n_it > 0) {
+        live = fetch(load_tri(sample(0)));
+        store(gsg);
     }
-    Tri tri_n = load_tri(b_lo + 1);
+    Tri tri_n = load_tri(sample(1));
     int slot_n;
     float L_n, R_n;
-    event(b_lo, slot_n, L_n, R_n);
-    live = __syncthreads_or(live);
-    for (int b = b_lo; b < b_hi; ++b) {
-        const float *cur = gs + ((b - b_lo) & 1) * gbuf;
-        const bool more = b + 1 < b_hi;
+    event(sample(0), slot_n, L_n, R_n);
+    live = group_live(live, 0);
+    for (int it = 0; it < n_it; ++it) {
+        const float *cur = gsg + (it & 1) * gbuf;
+        const bool more = it + 1 < n_it;
         const int slot = slot_n;
         const float L = L_n, Rv = R_n;
-        event(b + 1, slot_n, L_n, R_n);
+        event(sample(it + 1), slot_n, L_n, R_n);
         const Tri tri = tri_n;
-        tri_n = load_tri(b + 2);
+        tri_n = load_tri(sample(it + 2));
         bool live_next = false;
         if (more) live_next = fetch(tri);
         if (live) {
@@ -681,8 +698,29 @@ __global__ __launch_bounds__(256) void dw_dense_kernel(LifConst C, int B, int N_
             for (int ii = 0; ii < TI; ++ii)
                 acc[ii] = fmaf(p[ii], L, fmaf(p[ii + kStr], Rv, acc[ii]));
         }
-        if (more) store(gs + ((b + 1 - b_lo) & 1) * gbuf);
-        live = __syncthreads_or(live_next);
+        if (more) store(gsg + ((it + 1) & 1) * gbuf);
+        live = group_live(live_next, (it + 1) & 1);
+    }
+    if (GW > 1) {
+        // groups 1 .. GW-1 hand their sums to group 0 through the (now idle)
+        // G buffers, kCh per thread per round; group 0 adds them in group order
+        constexpr int kCh = (TI < 16) ? TI : 16;
+        float *xch = gs;
+#pragma unroll
+        for (int c0 = 0; c0 < TI; c0 += kCh) {
+            __syncthreads();
+            if (grp > 0) {
+#pragma unroll
+                for (int c = 0; c < kCh; ++c) xch[((grp - 1) * kCh + c) * 256 + tid] = acc[c0 + c];
+            }
+            __syncthreads();
+            if (grp == 0) {
+#pragma unroll
+                for (int c = 0; c < kCh; ++c)
+                    for (int g = 1; g < GW; ++g) acc[c0 + c] += xch[((g - 1) * kCh + c) * 256 + tid];
+            }
+        }
+        if (grp > 0) return;
     }
     if (!j_ok) return;
     float *out = dW_part + static_cast<int64_t>(blockIdx.z) * N_out * N_in +
@@ -1165,14 +1203,21 @@ static int dw_nper(int M, int ti) {
     return -1;
 }
 
+// Batch splits: enough that the grid holds ~4 groups of 4 waves per CU
+// (256 CUs), keeping >= 4 samples per group. Where that takes 4 or more
+// splits (and two groups' G buffers fit 64 KB), blocks carry two sample
+// groups (8 waves) and half the splits: the same waves in flight, half the
+// partials to write and read back.
 DwPlan plan_dw(int64_t B, int64_t N_in, int64_t N_out, int M) {
     DwPlan p;
-    p.waves = 4;
     p.jw = dw_ti(M, N_out);
-    int64_t tiles = ((N_in + 255) / 256) * ((N_out + p.jw - 1) / p.jw);
+    const int64_t tiles = ((N_in + 255) / 256) * ((N_out + p.jw - 1) / p.jw);
     p.nsplit = 1;
-    // aim for >= 4 blocks per CU (256 CUs); keep >= 4 samples per split
     while (tiles * p.nsplit < 1024 && B / (p.nsplit * 2) >= 4) p.nsplit *= 2;
+    const size_t g_lds = 2 * static_cast<size_t>(M + 4) * (p.jw + 1) * sizeof(float);  // one group
+    const int groups = (p.nsplit >= 4 && 2 * g_lds <= 64 * 1024) ? 2 : 1;
+    p.nsplit /= groups;
+    p.waves = 4 * groups;
     p.b_per_split = static_cast<int>(std::max<int64_t>(1, (B + p.nsplit - 1) / p.nsplit));
     p.nsplit = static_cast<int>(std::max<int64_t>(1, (B + p.b_per_split - 1) / p.b_per_split));
     return p;
@@ -1184,13 +1229,23 @@ static hipError_t launch_dw(const LifConst &C, const DwPlan &p, int64_t B, int64
     const int ti = p.jw;
     dim3 grid(static_cast<unsigned>((N_in + 255) / 256),
               static_cast<unsigned>((N_out + ti - 1) / ti), static_cast<unsigned>(p.nsplit));
-    size_t lds = 2 * static_cast<size_t>(C.M + 4) * (ti + 1) * sizeof(float);
+    // G buffers of every group; after the samples, the same LDS carries the
+    // groups' sums to group 0 (16 per thread per round)
+    const int groups = p.waves / 4;
+    const size_t lds = std::max(groups * 2 * static_cast<size_t>(C.M + 4) * (ti + 1),
+                                static_cast<size_t>(groups - 1) * 16 * 256) *
+                       sizeof(float);
     ProfScope prof("dw_dense", st);
     const int nper = dw_nper(C.M, ti);
-#define DW_LAUNCH_K(TIV, NP, KSV)                                                                  \
-    hipLaunchKernelGGL((dw_dense_kernel<TIV, NP, KSV>), grid, dim3(256), lds, st, C,               \
+#define DW_LAUNCH_G(TIV, NP, GWV, KSV)                                                             \
+    hipLaunchKernelGGL((dw_dense_kernel<TIV, NP, GWV, KSV>), grid, dim3(256 * GWV), lds, st, C,    \
                        static_cast<int>(B), static_cast<int>(N_in), static_cast<int>(N_out),        \
                        p.b_per_split, ws.gam, ws.uq, ws.q, ws.row, ws.L, ws.R, dq, dst)
+#define DW_LAUNCH_K(TIV, NP, KSV)                                          \
+    do {                                                                   \
+        if (groups == 2) DW_LAUNCH_G(TIV, NP, 2, KSV);                     \
+        else DW_LAUNCH_G(TIV, NP, 1, KSV);                                 \
+    } while (0)
 #define DW_LAUNCH(TIV, NP)                                                \
     do {                                                                  \
         if (C.kind == kGeneral) DW_LAUNCH_K(TIV, NP, kGeneral);           \
@@ -1211,6 +1266,7 @@ static hipError_t launch_dw(const LifConst &C, const DwPlan &p, int64_t B, int64
     }
 #undef DW_LAUNCH
 #undef DW_LAUNCH_K
+#undef DW_LAUNCH_G
     return hipGetLastError();
 }
 

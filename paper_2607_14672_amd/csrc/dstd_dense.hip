@@ -797,7 +797,7 @@ __global__ __launch_bounds__(256) void reduce_splits_kernel(int64_t n, int nspli
 // Records go 8 at a time: each wave reduces its lanes (fixed butterfly), the
 // four wave sums are added in wave order through LDS. Inputs without events
 // are not visited (their dt_in was zeroed earlier).
-constexpr int kDtRanges = 16;
+constexpr int kDtRanges = 6;
 
 // The launch may carry extra blocks (blockIdx.y >= B) that finish the dW
 // split reduction of the same layer (independent work, one launch less).

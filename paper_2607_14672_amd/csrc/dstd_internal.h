@@ -231,9 +231,9 @@ __device__ __forceinline__ void seg_eval_fast(const LifConst &C, const Seg &s, f
 // only root there: v has at most one extremum per interval, and [0, hi]
 // either ends at it or past the crossing). Halley iteration on the fast
 // evaluation, started at the regula-falsi point and kept inside the bracket
-// (bisection where a step leaves it), until a step falls below 3e-5 of u; the
-// cubic convergence puts that iterate within the fast evaluation's own error
-// of the root. One Newton step on the exact evaluation then places the root
+// (bisection where a step leaves it), until |v - theta| <= 1e-6 theta or a
+// step falls below 3e-5 of u; the cubic convergence puts that iterate within
+// the fast evaluation's own error of the root. One Newton step on the exact evaluation then places the root
 // to fp32 precision; the slope is the exact v' there, carried over the step
 // with the fast v''.
 template <int KS = kAnyKind>
@@ -247,6 +247,9 @@ __device__ __forceinline__ float seg_root(const LifConst &C, const Seg &s, float
     float f, fp, fpp = 0.f;
     for (int it = 0; it < 40; ++it) {
         seg_eval_fast<KS>(C, s, u, f, fp, fpp);
+        // at the fast evaluation's resolution: stepping further only follows
+        // its rounding (an exact zero would also collapse the bracket onto u)
+        if (fabsf(f) <= 1e-6f * C.theta) break;
         if (f < 0.f) lo = u; else hi = u;
         // Halley: u - 2 f f' / (2 f'^2 - f f'')
         const float den = fmaf(2.f * fp, fp, -f * fpp);

@@ -107,6 +107,7 @@ LifConst make_const(const dstd_lif_params *p) {
     C.kmax_dt_d = kern_d(kind, tv, ti, std::min(dt, upk));
     C.kmax_last_d = kern_d(kind, tv, ti, std::min(last, upk));
     C.theta_lo_d = (double)p->threshold / 1.0001;
+    C.twice = (kind == dstd::kGeneral && tv == 2.0 * ti) ? 1 : 0;
     C.inv_dt = (float)(1.0 / dt);
     C.e_mdt = (float)exp(-dt / ti);
     C.inv_D = (kind == dstd::kInfTau) ? (float)(-1.0 / expm1(-dt / ti)) : 0.f;

@@ -56,6 +56,7 @@ struct LifConst {
     // the scan's interval filter in fp64: max K on [0, dt] and on the last
     // interval, and theta / 1.0001 (the filter's margin)
     double kmax_dt_d, kmax_last_d, theta_lo_d;
+    int twice;  // general row with tv = 2 ti exactly: closed-form crossing
 };
 
 template <int KS> __device__ __forceinline__ int kind_of(const LifConst &C) {
@@ -453,6 +454,17 @@ struct Scan {
             // row (inf, tau): V + I tau (1 - e^{-u/tau}) = theta, I > 0
             u = fminf(-C.ti * log1pf(-(C.theta - sf.V) / (sf.I * C.ti)), hi);
             sl = sf.I * expf(-u * C.inv_ti);
+        } else if (hi > 0.f && kind == kGeneral && C.twice) {
+            // Table "tab:timing_DSTD", row (2tau, tau): with x = e^{-u/(2tau)}
+            // the segment is v = A x - B x^2 (A = V + cI, B = cI, c = 2tau), so
+            // v = theta is a quadratic in x; the crossing is the root below 1
+            // nearest to it (the larger root for B > 0), in its stable form
+            const float Bq = C.c * sf.I, Aq = sf.V + Bq;
+            const float sq = sqrtf(fmaxf(fmaf(Aq, Aq, -4.f * Bq * C.theta), 0.f));
+            const float x = (Bq > 0.f) ? (Aq + sq) / (2.f * Bq) : 2.f * C.theta / (Aq + sq);
+            u = fminf(fmaxf(-C.tv * logf(x), 0.f), hi);
+            const float xu = expf(-u * C.inv_tv);
+            sl = fmaf(-Aq * xu, C.inv_tv, Bq * xu * xu * C.inv_ti);
         } else if (hi > 0.f) {
             u = seg_root<KS>(C, sf, hi, fhi, sl);
         } else {

@@ -1,6 +1,7 @@
 """GPU parity of the closed-form kernel rows (Table "tab:kernel" rows
-(tau, tau), (inf, tau), (inf, inf)) against the fp64 oracle, dense and conv,
-through the C ABI."""
+(tau, tau), (inf, tau), (inf, inf), and the general row at tau_v = 2 tau_I,
+whose crossing has the quadratic closed form of Table "tab:timing_DSTD")
+against the fp64 oracle, dense and conv, through the C ABI."""
 import math
 
 import numpy as np
@@ -16,8 +17,8 @@ INF = math.inf
 # fire; (inf, inf) potentials with positive input grow without bound, so that
 # row closes the last interval to keep silent neurons in the cases
 ROWS = [(INF, 0.5, 3.0, INF), (INF, INF, 1.2, 1.6), (0.5, 0.5, 8.0, INF), (1.0, 1.0, 4.5, INF),
-        (0.3, INF, 5.0, INF)]
-IDS = ["inf-tau", "inf-inf", "tau-tau-0.5", "tau-tau-1", "tau-inf"]
+        (0.3, INF, 5.0, INF), (1.0, 0.5, 8.0, INF), (0.4, 0.8, 8.0, 1.5)]
+IDS = ["inf-tau", "inf-inf", "tau-tau-0.5", "tau-tau-1", "tau-inf", "2tau-tau", "tau-2tau-tmax"]
 
 
 @pytest.mark.parametrize("M", [8, 16, 33])

@@ -13,6 +13,7 @@ from .oracle import (  # noqa: F401
     dstd_scan,
     dstd_backward,
     exact_forward,
+    exact_backward,
     conv_forward,
     conv_backward,
     num_threads,

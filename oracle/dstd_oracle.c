@@ -12,6 +12,8 @@
  *                                                  Table "tab:kernel" (rows tau_v != tau_I,
  *                                                  (tau, tau), (inf, tau), (inf, inf))
  *   exact spike time (sort + interval candidates) App. A, Eq. (timing_exact), Alg. 1
+ *   exact spike-time gradients .................. implicit function theorem on
+ *                                                  v(t) = V_th over the causal set (App. A)
  *   DSTD grid T_m = T_first + m*dt - t_offset .. App. B.1
  *   DSTD event weights s_jm ..................... Eq. (DSTD_kernel), Table "tab:DSTD_kernels"
  *   weighted events w^_im = sum_j w_ij s_jm ..... App. B.1 (definition of w^)
@@ -603,14 +605,45 @@ static int cmp_tw(const void *x, const void *y) {
     return (a > b) - (a < b);
 }
 
+/* K'(t), the derivative of each row of Table "tab:kernel" with respect to its
+   argument, for t >= 0 (the jump of the Heaviside factor at 0 is not part of
+   it; at t = 0 this is the right derivative). */
+static double kern_dt(double tv, double ti, double t) {
+    if (t < 0.0) return 0.0;
+    switch (row_of(tv, ti)) {
+        case ROW_INF_INF: return 1.0;                                   /* d/dt t */
+        case ROW_INF_TAU: return exp(-t / finite_of(tv, ti));          /* d/dt tau (1 - e^{-t/tau}) */
+        case ROW_EQUAL: return exp(-t / tv) * (1.0 - t / tv);           /* d/dt t e^{-t/tau} */
+        default: {
+            double c = tv * ti / (tv - ti);
+            return c * (exp(-t / ti) / ti - exp(-t / tv) / tv);        /* d/dt c (e^{-t/tv} - e^{-t/ti}) */
+        }
+    }
+}
+
 /*
  * Sort the presynaptic spikes ascending; on [t~_k, t~_{k+1}) the potential is
  * sum_{j<=k} w_j K(t - t~_j); take the first interval whose candidate lies in
  * it (t~_{N+1} = t_max, +inf by default). Non-finite inputs are silent.
+ *
+ * Optional outputs (NULL to skip):
+ *  k_out  : position (0-based, ascending order of the finite inputs) of the
+ *           left end of the crossing interval, -1 when the neuron is silent.
+ *           Simultaneous spikes add up before their interval is tested, so
+ *           this is the last position of a group of equal times: the causal
+ *           set of the spike is exactly the inputs with t_j <= t~_k.
+ *  margin : distance of the firing decision from the threshold, as for the
+ *           DSTD scan: min over earlier intervals of (V_th - peak), and at the
+ *           crossing interval |peak - V_th|, |v(t~_k) - V_th| and
+ *           |v(t~_{k+1}) - V_th| (finite right end); silent neurons get the
+ *           min over all intervals of (V_th - peak).
+ *  vabs   : sum over the causal set of |w_j K(t - t_j)| at the spike (the
+ *           magnitude of the terms of v(t) = V_th, for rounding estimates).
  */
 void oracle_exact_forward(double tau_m, double tau_s, double theta, double t_max,
                           int64_t B, int64_t N_in, int64_t N_out,
-                          const double *t_in, const double *W, double *t_out, double *slope) {
+                          const double *t_in, const double *W, double *t_out, double *slope,
+                          int32_t *k_out, double *margin, double *vabs) {
     double tv = fmax(tau_m, tau_s), ti = fmin(tau_m, tau_s);
 #pragma omp parallel for schedule(dynamic, 1)
     for (int64_t b = 0; b < B; ++b) {
@@ -622,7 +655,8 @@ void oracle_exact_forward(double tau_m, double tau_s, double theta, double t_max
                 if (isfinite(t)) { s[n].t = t; s[n].w = W[i * N_in + j]; ++n; }
             }
             qsort(s, (size_t)n, sizeof(tw_t), cmp_tw);
-            double to = INFINITY, sl = 0.0;
+            double to = INFINITY, sl = 0.0, pre = INFINITY, mg = INFINITY, va = 0.0;
+            int32_t kk = -1;
             if (n > 0) {
                 piece_t pc;
                 piece_init(&pc, tv, ti, theta, s[0].t);
@@ -634,17 +668,108 @@ void oracle_exact_forward(double tau_m, double tau_s, double theta, double t_max
                     if (lo >= t_max) break;
                     if (hi > t_max) hi = t_max;
                     double root, peak;
-                    if (first_crossing(&pc, lo, hi, &root, &peak)) {
-                        to = root; sl = pdv(&pc, root);
+                    int hit = first_crossing(&pc, lo, hi, &root, &peak);
+                    if (hit) {
+                        to = root; sl = pdv(&pc, root); kk = (int32_t)k;
+                        mg = fmin(pre, fabs(peak - theta));
+                        mg = fmin(mg, fabs(pv(&pc, lo) - theta));
+                        if (!isinf(hi)) mg = fmin(mg, fabs(pv(&pc, hi) - theta));
+                        for (int64_t j = 0; j <= k; ++j) va += fabs(s[j].w * kern(tv, ti, root - s[j].t));
                         break;
                     }
+                    pre = fmin(pre, theta - peak);
                 }
             }
+            if (kk < 0) mg = pre;
             t_out[b * N_out + i] = to;
             slope[b * N_out + i] = sl;
+            if (k_out) k_out[b * N_out + i] = kk;
+            if (margin) margin[b * N_out + i] = mg;
+            if (vabs) vabs[b * N_out + i] = va;
         }
         free(s);
     }
+}
+
+static int cmp_d(const void *x, const void *y) {
+    double a = *(const double *)x, b = *(const double *)y;
+    return (a > b) - (a < b);
+}
+
+/*
+ * Gradients of the exact spike times (App. A, Eq. (timing_exact)) by the
+ * implicit function theorem on v_i(t_i) = V_th with
+ * v_i(t) = sum_{j in S_i} w_ij K(t - t_j), S_i = {j : t_j <= t~_k} the causal
+ * set of the crossing interval k (the candidate of the selected interval is
+ * that root, and the min over intervals is piecewise constant):
+ *   d t_i / d w_ij = -K(t_i - t_j) / v'(t_i)
+ *   d t_i / d t_j  =  w_ij K'(t_i - t_j) / v'(t_i)
+ * so with g = dL/dt_out and gamma = -g / slope:
+ *   grad_W[i][j]    = sum_b gamma_bi K(t_bi - t_bj)          (j in S_bi)
+ *   grad_t_in[b][j] = -sum_i gamma_bi W_ij K'(t_bi - t_bj)   (j in S_bi)
+ * Silent neurons (k < 0) and g = 0 contribute nothing; non-finite inputs get
+ * zero gradient. *_abs (optional) receive the sums of |terms|.
+ */
+void oracle_exact_backward(double tau_m, double tau_s, int64_t B, int64_t N_in, int64_t N_out,
+                           const double *t_in, const double *W, const double *t_out,
+                           const double *slope, const int32_t *k_idx, const double *grad_t_out,
+                           double *grad_W, double *grad_t_in, double *grad_W_abs,
+                           double *grad_t_in_abs) {
+    double tv = fmax(tau_m, tau_s), ti = fmin(tau_m, tau_s);
+    double *gam = (double *)calloc((size_t)(B * N_out > 0 ? B * N_out : 1), sizeof(double));
+    double *tl = (double *)calloc((size_t)(B * N_out > 0 ? B * N_out : 1), sizeof(double));
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t b = 0; b < B; ++b) {
+        double *ts = (double *)malloc(sizeof(double) * (size_t)(N_in > 0 ? N_in : 1));
+        int64_t n = 0;
+        for (int64_t j = 0; j < N_in; ++j)
+            if (isfinite(t_in[b * N_in + j])) ts[n++] = t_in[b * N_in + j];
+        qsort(ts, (size_t)n, sizeof(double), cmp_d);
+        for (int64_t i = 0; i < N_out; ++i) {
+            int64_t o = b * N_out + i;
+            int32_t k = k_idx[o];
+            if (k < 0 || k >= n || grad_t_out[o] == 0.0) continue;
+            gam[o] = -grad_t_out[o] / slope[o];
+            tl[o] = ts[k];
+        }
+        free(ts);
+    }
+    if (grad_W) {
+#pragma omp parallel for schedule(dynamic, 1)
+        for (int64_t i = 0; i < N_out; ++i)
+            for (int64_t j = 0; j < N_in; ++j) {
+                double acc = 0.0, aabs = 0.0;
+                for (int64_t b = 0; b < B; ++b) {
+                    int64_t o = b * N_out + i;
+                    double t = t_in[b * N_in + j];
+                    if (gam[o] == 0.0 || !isfinite(t) || !(t <= tl[o])) continue;
+                    double term = gam[o] * kern(tv, ti, t_out[o] - t);
+                    acc += term;
+                    aabs += fabs(term);
+                }
+                grad_W[i * N_in + j] = acc;
+                if (grad_W_abs) grad_W_abs[i * N_in + j] = aabs;
+            }
+    }
+    if (grad_t_in) {
+#pragma omp parallel for schedule(dynamic, 1)
+        for (int64_t b = 0; b < B; ++b)
+            for (int64_t j = 0; j < N_in; ++j) {
+                double acc = 0.0, aabs = 0.0, t = t_in[b * N_in + j];
+                if (isfinite(t))
+                    for (int64_t i = 0; i < N_out; ++i) {
+                        int64_t o = b * N_out + i;
+                        if (gam[o] == 0.0 || !(t <= tl[o])) continue;
+                        double term = -gam[o] * W[i * N_in + j] * kern_dt(tv, ti, t_out[o] - t);
+                        acc += term;
+                        aabs += fabs(term);
+                    }
+                grad_t_in[b * N_in + j] = acc;
+                if (grad_t_in_abs) grad_t_in_abs[b * N_in + j] = aabs;
+            }
+    }
+    free(gam);
+    free(tl);
 }
 
 int oracle_num_threads(void) {

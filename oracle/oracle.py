@@ -60,7 +60,10 @@ def _load():
     lib.oracle_dstd_backward.argtypes = [_D, _D, _D, _I, _D, _D, _D, _L, _L, _L,
                                          _P, _P, _P, _P, _P, _P, _L, _P, _P, _L, _P, _P, _P, _P]
     lib.oracle_exact_forward.restype = None
-    lib.oracle_exact_forward.argtypes = [_D, _D, _D, _D, _L, _L, _L, _P, _P, _P, _P]
+    lib.oracle_exact_forward.argtypes = [_D, _D, _D, _D, _L, _L, _L, _P, _P, _P, _P, _P, _P, _P]
+    lib.oracle_exact_backward.restype = None
+    lib.oracle_exact_backward.argtypes = [_D, _D, _L, _L, _L, _P, _P, _P, _P, _P, _P,
+                                          _P, _P, _P, _P]
     lib.oracle_conv_forward.restype = None
     lib.oracle_conv_forward.argtypes = [_D, _D, _D, _I, _D, _D, _D, _L,
                                         _I, _I, _I, _I, _I, _I, _I, _I, _I,
@@ -195,17 +198,44 @@ def dstd_backward(p, t_in, W, fwd, grad_t_out, isel=None, bsel=None, want_dW=Tru
 
 
 def exact_forward(p, t_in, W):
-    """Exact continuous-time LIF spike times (Alg. 1, Eq. (timing_exact))."""
+    """Exact continuous-time LIF spike times (Alg. 1, Eq. (timing_exact)).
+    Returns t_out, slope, q (position in ascending input order of the left end
+    of the crossing interval, -1 = silent), margin and vabs."""
     t_in = _f64(t_in)
     W = _f64(W)
     B, N_in = t_in.shape
     N_out = W.shape[0]
     t_out = np.empty((B, N_out))
     slope = np.empty((B, N_out))
+    q = np.empty((B, N_out), dtype=np.int32)
+    margin = np.empty((B, N_out))
+    vabs = np.empty((B, N_out))
     _load().oracle_exact_forward(float(p["tau_m"]), float(p["tau_s"]), float(p["threshold"]),
                                  float(p.get("t_max", np.inf)), B, N_in, N_out, _ptr(t_in), _ptr(W),
-                                 _ptr(t_out), _ptr(slope))
-    return dict(t_out=t_out, slope=slope)
+                                 _ptr(t_out), _ptr(slope), _ptr(q), _ptr(margin), _ptr(vabs))
+    return dict(t_out=t_out, slope=slope, q=q, margin=margin, vabs=vabs)
+
+
+def exact_backward(p, t_in, W, fwd, grad_t_out):
+    """Gradients of the exact spike times (implicit function theorem over the
+    causal set of the crossing interval). fwd: dict with t_out, slope, q.
+    Returns grad_W [N_out, N_in], grad_t_in [B, N_in] and their |term| sums."""
+    t_in = _f64(t_in)
+    W = _f64(W)
+    B, N_in = t_in.shape
+    N_out = W.shape[0]
+    t_out = _f64(fwd["t_out"])
+    slope = _f64(fwd["slope"])
+    q = np.ascontiguousarray(fwd["q"], dtype=np.int32)
+    g = _f64(grad_t_out)
+    gW = np.empty((N_out, N_in))
+    gt = np.empty((B, N_in))
+    gWa = np.empty((N_out, N_in))
+    gta = np.empty((B, N_in))
+    _load().oracle_exact_backward(float(p["tau_m"]), float(p["tau_s"]), B, N_in, N_out,
+                                  _ptr(t_in), _ptr(W), _ptr(t_out), _ptr(slope), _ptr(q), _ptr(g),
+                                  _ptr(gW), _ptr(gt), _ptr(gWa), _ptr(gta))
+    return dict(grad_W=gW, grad_t_in=gt, grad_W_abs=gWa, grad_t_in_abs=gta)
 
 
 def _conv_geom(cs):

@@ -54,11 +54,15 @@ typedef enum { DSTD_F32 = 0, DSTD_BF16 = 1 } dstd_dtype;
 /*
  * Layer parameters.
  *  tau_m, tau_s : membrane and synaptic time constants (the paper's tau_v,
- *                 tau_I; LIF model Eq. (LIF_model_TTFS)); finite, > 0. The
- *                 spike kernel (Table "tab:kernel") is symmetric in the
- *                 pair; |tau_m - tau_s| <= 1e-3 * max(tau_m, tau_s) is
- *                 DSTD_ERR_UNSUPPORTED (the equal-constant case uses other
- *                 formulas, Eqs. (equal_tau_*)).
+ *                 tau_I; LIF model Eq. (LIF_model_TTFS)); each > 0, finite
+ *                 or +INFINITY. The spike kernel (Table "tab:kernel") is
+ *                 symmetric in the pair; its rows are selected by the pair:
+ *                 two different finite constants (general row), two equal
+ *                 finite constants ((tau, tau)), one infinite ((inf, tau)),
+ *                 both infinite ((inf, inf)). Finite constants that differ by
+ *                 no more than 1e-3 * max(tau_m, tau_s) without being equal
+ *                 are DSTD_ERR_UNSUPPORTED (the general row loses precision
+ *                 there and the paper defines no blend).
  *  threshold    : firing threshold V_th > 0. A neuron fires at the first t
  *                 where v(t) >= V_th.
  *  M            : number of DSTD intervals, 1 <= M <= DSTD_MAX_M; the grid
@@ -297,6 +301,62 @@ int32_t dstd_profile_count(void);
 dstd_status dstd_profile_entry(int32_t idx, const char **name, int64_t *launches,
                                double *total_ms);
 void dstd_profile_reset(void);
+
+/* ---------------------------------------------------------------- exact -- */
+
+/*
+ * Exact spike times of a dense layer without discretization (App. A, Alg. 1,
+ * Eq. (timing_exact)): the method DSTD approximates, for measuring it against
+ * DSTD. Of dstd_lif_params only tau_m, tau_s, threshold, t_max and flags are
+ * used (validated as for the DSTD calls; t_max may be any non-NaN value); M,
+ * t0 and dt are ignored. Supported: N_in <= 8192 (DSTD_ERR_UNSUPPORTED
+ * beyond: one workgroup sorts a sample's inputs), the other size limits as in
+ * dstd_lif_forward.
+ */
+size_t dstd_exact_forward_workspace_size(const dstd_lif_params *p, int64_t B, int64_t N_in,
+                                         int64_t N_out);
+size_t dstd_exact_backward_workspace_size(const dstd_lif_params *p, int64_t B, int64_t N_in,
+                                          int64_t N_out);
+
+/*
+ * Forward: per sample the finite inputs with t < t_max are sorted ascending
+ * (t~_1 <= t~_2 <= ...); on [t~_k, t~_{k+1}) the potential is
+ * sum_{j <= k} w_ij K(t - t~_j), and the spike is the first time it reaches
+ * the threshold, the first interval whose candidate lies inside it
+ * (Eq. (timing_exact); the last interval ends at t_max, +INFINITY = open).
+ * Simultaneous inputs add up before their interval is tested.
+ *  t_in  [B][N_in]     input spike times; non-finite = no spike.
+ *  W     [N_out][N_in] fp32 or bf16.
+ *  t_out [B][N_out]    out: spike time, +inf if none.
+ *  slope [B][N_out]    out: dv/dt at the spike (0 if none).
+ *  k_idx [B][N_out]    out: position (0-based) in the sorted order of the
+ *                      left end of the crossing interval, -1 if none; the
+ *                      causal set of the spike is every input with
+ *                      t_j <= t~_k.
+ */
+dstd_status dstd_exact_forward(const dstd_lif_params *p, int64_t B, int64_t N_in, int64_t N_out,
+                               const float *t_in, const void *W, dstd_dtype w_dtype,
+                               float *t_out, float *slope, int32_t *k_idx,
+                               void *ws, size_t ws_bytes, void *stream);
+
+/*
+ * Backward: with the causal set fixed (piecewise-constant, as is the choice
+ * of interval), the implicit-function theorem on v(t_i) = V_th gives
+ * d t_i / d w_ij = -K(t_i - t_j) / slope_i and
+ * d t_i / d t_j = w_ij K'(t_i - t_j) / slope_i for t_j <= t~_k; this equals
+ * differentiating the selected candidate of Table "tab:spike_timing".
+ *  t_out, slope, k_idx  the forward's outputs for the same (t_in, W, p).
+ *  grad_t_out [B][N_out] dL/dt_out; ignored where k_idx < 0.
+ *  grad_W [N_out][N_in]  out (fp32, overwritten), or NULL to skip.
+ *  grad_t_in [B][N_in]   out (overwritten), or NULL to skip; inputs that
+ *                        are not finite get 0.
+ * Slopes below 1e-12 * threshold use that floor, as in dstd_lif_backward.
+ */
+dstd_status dstd_exact_backward(const dstd_lif_params *p, int64_t B, int64_t N_in, int64_t N_out,
+                                const float *t_in, const void *W, dstd_dtype w_dtype,
+                                const float *t_out, const float *slope, const int32_t *k_idx,
+                                const float *grad_t_out, float *grad_W, float *grad_t_in,
+                                void *ws, size_t ws_bytes, void *stream);
 
 /* ----------------------------------------------------------------- misc -- */
 

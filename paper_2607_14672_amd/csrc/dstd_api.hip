@@ -614,3 +614,125 @@ dstd_status conv_backward(const dstd_lif_params *p, const dstd_synfire_params *s
 }
 
 }  // namespace
+
+// ------------------------------------------------------------------ exact --
+namespace {
+
+// The exact path uses tau_m, tau_s, threshold, t_max and flags; the grid
+// fields (M, t0, dt) do not apply and are not read.
+dstd_status check_exact(const dstd_lif_params *p, int64_t B, int64_t N_in, int64_t N_out,
+                        dstd_lif_params *q) {
+    if (!p) return fail(DSTD_ERR_NULL, "params is NULL");
+    *q = *p;
+    q->M = 1;
+    q->t0 = 0.f;
+    q->dt = 1.f;
+    q->t_max = INFINITY;
+    dstd_status s = check_params(q);
+    if (s != DSTD_OK) return s;
+    if (isnan(p->t_max)) return fail(DSTD_ERR_PARAM, "t_max must not be NaN");
+    if ((s = check_dims(B, N_in, N_out)) != DSTD_OK) return s;
+    if (N_in > dstd::kExactMaxIn)
+        return fail(DSTD_ERR_UNSUPPORTED, "the exact path sorts at most %d inputs per sample (N_in = %lld)",
+                    dstd::kExactMaxIn, (long long)N_in);
+    return DSTD_OK;
+}
+
+struct ExactWs {
+    size_t wt, j, t, len, r_lo, alpha, beta, kl, kmax, n, P, PT, total;
+};
+
+ExactWs exact_ws_layout(int64_t B, int64_t N_in, int64_t N_out, bool backward) {
+    ExactWs w{};
+    size_t off = 0;
+    if (backward) {
+        w.P = off; off += align_up((size_t)B * (size_t)N_out * 4 * sizeof(float));
+        w.PT = off; off += align_up((size_t)B * (size_t)N_out * 4 * sizeof(float));
+    } else if (B * N_out > 0) {
+        const size_t ns = (size_t)(B * N_in) + dstd::kExactPad;
+        w.wt = off; off += align_up((size_t)N_in * (size_t)N_out * sizeof(float));
+        w.j = off; off += align_up(ns * sizeof(int));
+        w.t = off; off += align_up(ns * sizeof(float));
+        w.len = off; off += align_up(ns * sizeof(float));
+        w.r_lo = off; off += align_up(ns * sizeof(float));
+        w.alpha = off; off += align_up(ns * sizeof(double));
+        w.beta = off; off += align_up(ns * sizeof(double));
+        w.kl = off; off += align_up(ns * sizeof(double));
+        w.kmax = off; off += align_up(ns * sizeof(double));
+        w.n = off; off += align_up((size_t)B * sizeof(int));
+    }
+    w.total = off;
+    return w;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t dstd_exact_forward_workspace_size(const dstd_lif_params *p, int64_t B, int64_t N_in,
+                                         int64_t N_out) {
+    dstd_lif_params q;
+    if (check_exact(p, B, N_in, N_out, &q) != DSTD_OK) return 0;
+    return exact_ws_layout(B, N_in, N_out, false).total;
+}
+
+size_t dstd_exact_backward_workspace_size(const dstd_lif_params *p, int64_t B, int64_t N_in,
+                                          int64_t N_out) {
+    dstd_lif_params q;
+    if (check_exact(p, B, N_in, N_out, &q) != DSTD_OK) return 0;
+    return exact_ws_layout(B, N_in, N_out, true).total;
+}
+
+dstd_status dstd_exact_forward(const dstd_lif_params *p, int64_t B, int64_t N_in, int64_t N_out,
+                               const float *t_in, const void *W, dstd_dtype w_dtype, float *t_out,
+                               float *slope, int32_t *k_idx, void *ws, size_t ws_bytes,
+                               void *stream) {
+    dstd_lif_params q;
+    dstd_status s = check_exact(p, B, N_in, N_out, &q);
+    if (s != DSTD_OK) return s;
+    if (w_dtype != DSTD_F32 && w_dtype != DSTD_BF16)
+        return fail(DSTD_ERR_PARAM, "unknown weight dtype %d", (int)w_dtype);
+    if (B * N_out > 0 && (!t_out || !slope || !k_idx))
+        return fail(DSTD_ERR_NULL, "t_out, slope and k_idx are required");
+    if (B * N_in > 0 && !t_in) return fail(DSTD_ERR_NULL, "t_in is NULL");
+    if (N_in * N_out > 0 && !W) return fail(DSTD_ERR_NULL, "W is NULL");
+    ExactWs L = exact_ws_layout(B, N_in, N_out, false);
+    if ((s = check_ws(ws, ws_bytes, L.total)) != DSTD_OK) return s;
+    if (B * N_out == 0) return DSTD_OK;
+    LifConst C = make_const(&q);
+    dstd::ExactRecs rec{at<int>(ws, L.j), at<float>(ws, L.t), at<float>(ws, L.len),
+                        at<float>(ws, L.r_lo), at<double>(ws, L.alpha), at<double>(ws, L.beta),
+                        at<double>(ws, L.kl), at<double>(ws, L.kmax), at<int>(ws, L.n), N_in};
+    hipError_t e = dstd::launch_exact_forward(C, B, N_in, N_out, W, w_dtype == DSTD_BF16,
+                                              at<void>(ws, L.wt), rec, t_in, p->t_max, t_out,
+                                              slope, k_idx, static_cast<hipStream_t>(stream));
+    return hip_status(e, "exact forward launch");
+}
+
+dstd_status dstd_exact_backward(const dstd_lif_params *p, int64_t B, int64_t N_in, int64_t N_out,
+                                const float *t_in, const void *W, dstd_dtype w_dtype,
+                                const float *t_out, const float *slope, const int32_t *k_idx,
+                                const float *grad_t_out, float *grad_W, float *grad_t_in,
+                                void *ws, size_t ws_bytes, void *stream) {
+    dstd_lif_params q;
+    dstd_status s = check_exact(p, B, N_in, N_out, &q);
+    if (s != DSTD_OK) return s;
+    if (w_dtype != DSTD_F32 && w_dtype != DSTD_BF16)
+        return fail(DSTD_ERR_PARAM, "unknown weight dtype %d", (int)w_dtype);
+    if (B * N_out > 0 && (!t_out || !slope || !k_idx || !grad_t_out))
+        return fail(DSTD_ERR_NULL, "t_out, slope, k_idx and grad_t_out are required");
+    if (B * N_in > 0 && (grad_W || grad_t_in) && !t_in) return fail(DSTD_ERR_NULL, "t_in is NULL");
+    if (grad_t_in && N_in * N_out > 0 && !W) return fail(DSTD_ERR_NULL, "W is NULL");
+    ExactWs L = exact_ws_layout(B, N_in, N_out, true);
+    if ((s = check_ws(ws, ws_bytes, L.total)) != DSTD_OK) return s;
+    LifConst C = make_const(&q);
+    // B == 0: the dW kernel still runs and writes zeros; N_out == 0: the
+    // dt_in kernel sums nothing and writes zeros
+    hipError_t e = dstd::launch_exact_backward(
+        C, B, N_in, N_out, W, w_dtype == DSTD_BF16, t_in, p->t_max, t_out, slope, k_idx,
+        grad_t_out, at<float4>(ws, L.P), at<float4>(ws, L.PT), grad_W, grad_t_in,
+        static_cast<hipStream_t>(stream));
+    return hip_status(e, "exact backward launch");
+}
+
+}  // extern "C"

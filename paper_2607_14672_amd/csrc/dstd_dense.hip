@@ -134,25 +134,6 @@ __device__ void sort_sample(const LifConst &C, int b, int N_in, const float *__r
     }
 }
 
-// W [N_out][N_in] -> WT [N_in][N_out], one 32 x 32 tile through a padded LDS
-// tile (kPrepThreads threads: 32 x 16).
-template <typename WT>
-__device__ void transpose_tile(int rows, int cols, const WT *__restrict__ in, WT *__restrict__ out,
-                               int tile, WT (*buf)[33]) {
-    const int ntx = (cols + 31) / 32;
-    const int c0 = (tile % ntx) * 32, r0 = (tile / ntx) * 32;
-    const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
-    for (int k = ty; k < 32; k += kPrepThreads / 32) {
-        const int r = r0 + k, c = c0 + tx;
-        if (r < rows && c < cols) buf[k][tx] = in[static_cast<int64_t>(r) * cols + c];
-    }
-    __syncthreads();
-    for (int k = ty; k < 32; k += kPrepThreads / 32) {
-        const int c = c0 + k, r = r0 + tx;
-        if (r < rows && c < cols) out[static_cast<int64_t>(c) * rows + r] = buf[tx][k];
-    }
-}
-
 // Independent setup work of a layer call in one launch, by block role:
 // blocks [0, n_sort) sort one sample each, the next n_tr blocks transpose one
 // weight tile each, then blocks writing the gradient triple (gamma, t - T_q,
@@ -184,7 +165,7 @@ __global__ __launch_bounds__(kPrepThreads) void prep_kernel(LifConst C, int n_so
     if (blk < n_sort) {
         sort_sample<KS>(C, blk, N_in, t_in, srt, n_valid, deriv, xo, sh);
     } else if (blk < n_sort + n_tr) {
-        transpose_tile<WT>(N_out, N_in, W, Wt, blk - n_sort, buf);
+        transpose_tile<WT, kPrepThreads>(N_out, N_in, W, Wt, blk - n_sort, buf);
     } else {
         const int64_t n_gb = (n_grad + kPrepThreads - 1) / kPrepThreads;
         const int64_t gb = blk - n_sort - n_tr;

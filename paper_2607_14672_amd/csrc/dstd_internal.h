@@ -355,6 +355,112 @@ __device__ __forceinline__ void g_strided(const LifConst &C, const GStep &gs, fl
     }
 }
 
+// Crossing test of one interval [0, len) of the state form v(u) = V e^{-u/tv}
+// + I K(u) (V = v at the interval's start, I the current just after its
+// input), for a neuron that has not fired before it. vn_d is v at the
+// interval's end carried by the fp64 recurrence (used unless `last`); the
+// last interval's end value is evaluated at len, or taken as the limit of an
+// open interval (len = +inf). kmax = max K on [0, len] (fp64), r_lo =
+// e^{-kappa len} (general row). On a crossing returns true with the fp32
+// segment, the bracket end hi (0: fires at u = 0, only through rounding) and
+// v - theta there.
+template <int KS = kAnyKind>
+__device__ __forceinline__ bool seg_test(const LifConst &C, double Vd, double Id, double vn_d,
+                                         bool last, float len, double kmax, float r_lo, Seg &sf,
+                                         float &hi, float &fhi) {
+    const int kind = kind_of<KS>(C);
+    // v(u) <= max(V,0) + max(I,0) max K, tested on the fp64 state against
+    // theta with a 1e-4 margin (only intervals that pass are analysed; max K
+    // is +inf on an open interval of the (inf, inf) row, where I = 0 must not
+    // give inf * 0)
+    const double vpos = fmax(Vd, 0.0);
+    const double ub = (kind == kInfInf) ? ((Id > 0.0) ? fma(Id, kmax, vpos) : vpos)
+                                        : fma(fmax(Id, 0.0), kmax, vpos);
+    if (!(ub >= C.theta_lo_d)) return false;
+    const Seg s{static_cast<float>(Vd), static_cast<float>(Id)};
+    const bool fin = !last || isfinite(len);
+    float vend = -INFINITY;
+    if (!last) {
+        vend = static_cast<float>(vn_d);
+    } else if (fin) {
+        float f, fp;
+        seg_eval<KS>(C, s, len, f, fp);
+        vend = f + C.theta;
+    } else if (kind == kInfTau) {
+        // open interval: v rises to V + I tau (never reached)
+        const float lim = fmaf(s.I, C.ti, s.V);
+        if (s.I > 0.f && lim > C.theta) vend = lim;
+    } else if (kind == kInfInf) {
+        if (s.I > 0.f) vend = INFINITY;  // v = V + I u grows without bound
+    }
+    if (s.V >= C.theta) {  // only through rounding: v is continuous
+        sf = s; hi = 0.f;
+        return true;
+    }
+    if (vend >= C.theta) {
+        sf = s; hi = len; fhi = vend - C.theta;
+        return true;
+    }
+    if (kind == kEqual) {
+        // interior maximum of (V + I u) e^{-u/tau} at u* = tau - V/I (I > 0),
+        // where v = I tau e^{-u*/tau} <= I tau
+        if (s.I > 0.f && s.I * C.ti * 1.0001f >= C.theta) {
+            const float us = C.ti - s.V / s.I;
+            if (us > 0.f && us < len) {
+                const float vs = s.I * C.ti * expf(-us * C.inv_ti);
+                if (vs >= C.theta) { sf = s; hi = us; fhi = vs - C.theta; return true; }
+            }
+        }
+    } else if (kind == kGeneral && s.I > 0.f) {
+        // interior maximum: v'(u*) = 0 with e^{-kappa u*} = (ti/tv)(1 + V/(c I))
+        const float r = (C.ti * C.inv_tv) * (1.f + s.V / (C.c * s.I));
+        // v(u*) = e^{-u*/tv} (V + c I (1 - r)) <= V + c I (1 - r): the
+        // maximum is evaluated only if this bound reaches theta
+        if (r > r_lo && r < 1.f && fmaf(s.I * C.c, 1.f - r, s.V) * 1.0001f >= C.theta) {
+            const float us = -logf(r) / C.kappa;
+            float f, fp;
+            seg_eval<KS>(C, s, us, f, fp);
+            if (f >= 0.f) { sf = s; hi = us; fhi = f; return true; }
+        }
+    }
+    return false;
+}
+
+// Spike time inside the crossing interval found by seg_test: u with v(u) =
+// theta on [0, hi] and the slope v'(u). The closed-form rows of Table
+// "tab:timing_DSTD" are solved directly; the general row by seg_root.
+template <int KS = kAnyKind>
+__device__ __forceinline__ void seg_solve(const LifConst &C, const Seg &sf, float hi, float fhi,
+                                          float &u, float &sl) {
+    const int kind = kind_of<KS>(C);
+    if (hi > 0.f && kind == kInfInf) {
+        // Table "tab:timing_DSTD", row (inf, inf): V + I u = theta, I > 0
+        u = fminf((C.theta - sf.V) / sf.I, hi);
+        sl = sf.I;
+    } else if (hi > 0.f && kind == kInfTau) {
+        // row (inf, tau): V + I tau (1 - e^{-u/tau}) = theta, I > 0
+        u = fminf(-C.ti * log1pf(-(C.theta - sf.V) / (sf.I * C.ti)), hi);
+        sl = sf.I * expf(-u * C.inv_ti);
+    } else if (hi > 0.f && kind == kGeneral && C.twice) {
+        // Table "tab:timing_DSTD", row (2tau, tau): with x = e^{-u/(2tau)}
+        // the segment is v = A x - B x^2 (A = V + cI, B = cI, c = 2tau), so
+        // v = theta is a quadratic in x; the crossing is the root below 1
+        // nearest to it (the larger root for B > 0), in its stable form
+        const float Bq = C.c * sf.I, Aq = sf.V + Bq;
+        const float sq = sqrtf(fmaxf(fmaf(Aq, Aq, -4.f * Bq * C.theta), 0.f));
+        const float x = (Bq > 0.f) ? (Aq + sq) / (2.f * Bq) : 2.f * C.theta / (Aq + sq);
+        u = fminf(fmaxf(-C.tv * logf(x), 0.f), hi);
+        const float xu = expf(-u * C.inv_tv);
+        sl = fmaf(-Aq * xu, C.inv_tv, Bq * xu * xu * C.inv_ti);
+    } else if (hi > 0.f) {
+        u = seg_root<KS>(C, sf, hi, fhi, sl);
+    } else {
+        float f;
+        u = 0.f;
+        seg_eval<KS>(C, sf, 0.f, f, sl);
+    }
+}
+
 // Interval scan of one neuron (Table "tab:timing_DSTD", Eq. (timing_DSTD)):
 // weighted events arrive in grid order through step(); the earliest interval
 // whose candidate lies inside it is kept. The state (v at T_q, current after
@@ -370,67 +476,14 @@ struct Scan {
     float hi = 0.f, fhi = 0.f;  // bracket end of the crossing and v - theta there
 
     __device__ __forceinline__ void step(const LifConst &C, int q, float w) {
-        const int kind = kind_of<KS>(C);
         Id += static_cast<double>(w);
         const double vn_d = fma(Vd, C.alpha_d, Id * C.k_dt_d);
         if (qf < 0) {
             const bool last = (q == C.M);
-            // v(u) = V e^{-u/tv} + I K(u) <= max(V,0) + max(I,0) max K, tested
-            // on the fp64 state against theta with a 1e-4 margin (only
-            // intervals that pass are analysed; max K is +inf on the open
-            // last interval of the (inf, inf) row, where I = 0 must not give
-            // inf * 0)
-            const double kmax = last ? C.kmax_last_d : C.kmax_dt_d;
-            const double vpos = fmax(Vd, 0.0);
-            const double ub = (kind == kInfInf) ? ((Id > 0.0) ? fma(Id, kmax, vpos) : vpos)
-                                                : fma(fmax(Id, 0.0), kmax, vpos);
-            if (ub >= C.theta_lo_d) {
-                const Seg s{static_cast<float>(Vd), static_cast<float>(Id)};
-                const float len = last ? C.last_len : C.dt;
-                const bool fin = !last || isfinite(C.last_len);
-                float vend = -INFINITY;
-                if (!last) {
-                    vend = static_cast<float>(vn_d);
-                } else if (fin) {
-                    float f, fp;
-                    seg_eval<KS>(C, s, C.last_len, f, fp);
-                    vend = f + C.theta;
-                } else if (kind == kInfTau) {
-                    // open last interval: v rises to V + I tau (never reached)
-                    const float lim = fmaf(s.I, C.ti, s.V);
-                    if (s.I > 0.f && lim > C.theta) vend = lim;
-                } else if (kind == kInfInf) {
-                    if (s.I > 0.f) vend = INFINITY;  // v = V + I u grows without bound
-                }
-                if (s.V >= C.theta) {  // only through rounding: v is continuous
-                    qf = q; sf = s; hi = 0.f;
-                } else if (vend >= C.theta) {
-                    qf = q; sf = s; hi = len; fhi = vend - C.theta;
-                } else if (kind == kEqual) {
-                    // interior maximum of (V + I u) e^{-u/tau} at u* = tau - V/I (I > 0),
-                    // where v = I tau e^{-u*/tau} <= I tau
-                    if (s.I > 0.f && s.I * C.ti * 1.0001f >= C.theta) {
-                        const float us = C.ti - s.V / s.I;
-                        if (us > 0.f && us < len) {
-                            const float vs = s.I * C.ti * expf(-us * C.inv_ti);
-                            if (vs >= C.theta) { qf = q; sf = s; hi = us; fhi = vs - C.theta; }
-                        }
-                    }
-                } else if (kind == kGeneral && s.I > 0.f) {
-                    // interior maximum: v'(u*) = 0 with e^{-kappa u*} = (ti/tv)(1 + V/(c I))
-                    const float r = (C.ti * C.inv_tv) * (1.f + s.V / (C.c * s.I));
-                    const float r_lo = last ? C.r_lo_last : C.r_lo_dt;
-                    // v(u*) = e^{-u*/tv} (V + c I (1 - r)) <= V + c I (1 - r): the
-                    // maximum is evaluated only if this bound reaches theta
-                    if (r > r_lo && r < 1.f &&
-                        fmaf(s.I * C.c, 1.f - r, s.V) * 1.0001f >= C.theta) {
-                        const float us = -logf(r) / C.kappa;
-                        float f, fp;
-                        seg_eval<KS>(C, s, us, f, fp);
-                        if (f >= 0.f) { qf = q; sf = s; hi = us; fhi = f; }
-                    }
-                }
-            }
+            if (seg_test<KS>(C, Vd, Id, vn_d, last, last ? C.last_len : C.dt,
+                             last ? C.kmax_last_d : C.kmax_dt_d, last ? C.r_lo_last : C.r_lo_dt,
+                             sf, hi, fhi))
+                qf = q;
         }
         Vd = vn_d;
         Id *= C.beta_d;
@@ -444,39 +497,32 @@ struct Scan {
         slope = 0.f;
         q_out = qf;
         if (qf < 0) return;
-        const int kind = kind_of<KS>(C);
         float u, sl;
-        if (hi > 0.f && kind == kInfInf) {
-            // Table "tab:timing_DSTD", row (inf, inf): V + I u = theta, I > 0
-            u = fminf((C.theta - sf.V) / sf.I, hi);
-            sl = sf.I;
-        } else if (hi > 0.f && kind == kInfTau) {
-            // row (inf, tau): V + I tau (1 - e^{-u/tau}) = theta, I > 0
-            u = fminf(-C.ti * log1pf(-(C.theta - sf.V) / (sf.I * C.ti)), hi);
-            sl = sf.I * expf(-u * C.inv_ti);
-        } else if (hi > 0.f && kind == kGeneral && C.twice) {
-            // Table "tab:timing_DSTD", row (2tau, tau): with x = e^{-u/(2tau)}
-            // the segment is v = A x - B x^2 (A = V + cI, B = cI, c = 2tau), so
-            // v = theta is a quadratic in x; the crossing is the root below 1
-            // nearest to it (the larger root for B > 0), in its stable form
-            const float Bq = C.c * sf.I, Aq = sf.V + Bq;
-            const float sq = sqrtf(fmaxf(fmaf(Aq, Aq, -4.f * Bq * C.theta), 0.f));
-            const float x = (Bq > 0.f) ? (Aq + sq) / (2.f * Bq) : 2.f * C.theta / (Aq + sq);
-            u = fminf(fmaxf(-C.tv * logf(x), 0.f), hi);
-            const float xu = expf(-u * C.inv_tv);
-            sl = fmaf(-Aq * xu, C.inv_tv, Bq * xu * xu * C.inv_ti);
-        } else if (hi > 0.f) {
-            u = seg_root<KS>(C, sf, hi, fhi, sl);
-        } else {
-            float f;
-            u = 0.f;
-            seg_eval<KS>(C, sf, 0.f, f, sl);
-        }
+        seg_solve<KS>(C, sf, hi, fhi, u, sl);
         t_out = static_cast<float>(fma(static_cast<double>(qf), static_cast<double>(C.dt),
                                        static_cast<double>(C.t0)) + static_cast<double>(u));
         slope = sl;
     }
 };
+
+// W [rows][cols] -> WT [cols][rows], one 32 x 32 tile through a padded LDS
+// tile (kThreads threads, a multiple of 32).
+template <typename WT, int kThreads>
+__device__ void transpose_tile(int rows, int cols, const WT *__restrict__ in, WT *__restrict__ out,
+                               int tile, WT (*buf)[33]) {
+    const int ntx = (cols + 31) / 32;
+    const int c0 = (tile % ntx) * 32, r0 = (tile / ntx) * 32;
+    const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
+    for (int k = ty; k < 32; k += kThreads / 32) {
+        const int r = r0 + k, c = c0 + tx;
+        if (r < rows && c < cols) buf[k][tx] = in[static_cast<int64_t>(r) * cols + c];
+    }
+    __syncthreads();
+    for (int k = ty; k < 32; k += kThreads / 32) {
+        const int c = c0 + k, r = r0 + tx;
+        if (r < rows && c < cols) out[static_cast<int64_t>(c) * rows + r] = buf[tx][k];
+    }
+}
 
 __device__ __forceinline__ int uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }
 
@@ -546,7 +592,9 @@ template <> struct BufLoad<uint16_t> {
 // consecutive. Only for data that no kernel in flight writes.
 typedef __attribute__((address_space(4))) const int cint_t;
 typedef __attribute__((address_space(4))) const float cflt_t;
+typedef __attribute__((address_space(4))) const double cdbl_t;
 __device__ __forceinline__ cint_t *as_const(const int *p) { return (cint_t *)p; }
 __device__ __forceinline__ cflt_t *as_const(const float *p) { return (cflt_t *)p; }
+__device__ __forceinline__ cdbl_t *as_const(const double *p) { return (cdbl_t *)p; }
 
 }  // namespace dstd

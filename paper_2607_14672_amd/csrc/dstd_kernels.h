@@ -103,4 +103,34 @@ hipError_t launch_synfire_value(const Synfire &sf, int64_t B, int64_t rows, int6
                                 int64_t row_len, const float *t_out, const void *W, bool bf16,
                                 float *ws, float *value, hipStream_t st);
 
+// ----------------------------------------------------------------- exact --
+// Exact spike times by sorting (App. A, Alg. 1). Per sample, the finite
+// inputs before t_max in ascending time order as records (SoA, each array
+// [B][stride], padded by kExactPad records at the end): input index j, time
+// t, candidate-interval length len (to the next input, or to t_max for the
+// last record) with e^{-kappa len}, and in fp64 the decays over len, K(len)
+// (carry the state to the next input) and max K on [0, len] (the interval
+// filter). n[b] = number of records of sample b.
+struct ExactRecs {
+    int *j;
+    float *t, *len, *r_lo;
+    double *alpha, *beta, *kl, *kmax;
+    int *n;
+    int64_t stride;
+};
+constexpr int kExactPad = 16;
+constexpr int kExactMaxIn = 8192;  // one block sorts a sample in 64 KB of LDS
+
+hipError_t launch_exact_forward(const LifConst &C, int64_t B, int64_t N_in, int64_t N_out,
+                                const void *W, bool bf16, void *Wt, ExactRecs rec,
+                                const float *t_in, float t_max, float *t_out, float *slope,
+                                int *k_idx, hipStream_t st);
+// per-neuron gradient data of the exact backward: {gamma = -g/slope, t_out,
+// left end of the crossing interval, 0}, as [B][N_out] and [N_out][B]
+hipError_t launch_exact_backward(const LifConst &C, int64_t B, int64_t N_in, int64_t N_out,
+                                 const void *W, bool bf16, const float *t_in, float t_max,
+                                 const float *t_out, const float *slope, const int *k_idx,
+                                 const float *grad_t, float4 *P, float4 *PT, float *grad_W,
+                                 float *grad_t_in, hipStream_t st);
+
 }  // namespace dstd

@@ -77,6 +77,10 @@ _SIGS = {
                                             _S, _P]),
     "dstd_synfire_penalty_workspace_size": (_S, [_L, _L, _L]),
     "dstd_synfire_penalty": (_I, [_P, _L, _L, _L, _L, _P, _P, _I, _P, _P, _S, _P]),
+    "dstd_exact_forward_workspace_size": (_S, [_P, _L, _L, _L]),
+    "dstd_exact_backward_workspace_size": (_S, [_P, _L, _L, _L]),
+    "dstd_exact_forward": (_I, [_P, _L, _L, _L, _P, _P, _I, _P, _P, _P, _P, _S, _P]),
+    "dstd_exact_backward": (_I, [_P, _L, _L, _L, _P, _P, _I, _P, _P, _P, _P, _P, _P, _P, _S, _P]),
     "dstd_softmax_ce_grad": (_I, [_L, _L, _P, _P, _F, _F, _P, _P, _P]),
     "dstd_mse_grad": (_I, [_L, _L, _P, _P, _P, _P, _P]),
     "dstd_profile_enable": (C.c_int32, [C.c_int32]),
@@ -131,6 +135,26 @@ def dstd_lif_backward(p, B, N_in, N_out, t_in, W, w_dtype, t_out, slope, q_idx, 
                       grad_W, grad_t_in, ws, ws_bytes, stream):
     return _load().dstd_lif_backward(_ref(p), B, N_in, N_out, t_in, W, w_dtype, t_out, slope, q_idx,
                                      grad_t_out, grad_W, grad_t_in, ws, ws_bytes, stream)
+
+
+def dstd_exact_forward_workspace_size(p, B, N_in, N_out):
+    return _load().dstd_exact_forward_workspace_size(_ref(p), B, N_in, N_out)
+
+
+def dstd_exact_backward_workspace_size(p, B, N_in, N_out):
+    return _load().dstd_exact_backward_workspace_size(_ref(p), B, N_in, N_out)
+
+
+def dstd_exact_forward(p, B, N_in, N_out, t_in, W, w_dtype, t_out, slope, k_idx, ws, ws_bytes,
+                       stream):
+    return _load().dstd_exact_forward(_ref(p), B, N_in, N_out, t_in, W, w_dtype, t_out, slope,
+                                      k_idx, ws, ws_bytes, stream)
+
+
+def dstd_exact_backward(p, B, N_in, N_out, t_in, W, w_dtype, t_out, slope, k_idx, grad_t_out,
+                        grad_W, grad_t_in, ws, ws_bytes, stream):
+    return _load().dstd_exact_backward(_ref(p), B, N_in, N_out, t_in, W, w_dtype, t_out, slope,
+                                       k_idx, grad_t_out, grad_W, grad_t_in, ws, ws_bytes, stream)
 
 
 def dstd_lif_conv_forward_workspace_size(p, cs, B):
@@ -336,6 +360,50 @@ def backward(p: dstd_lif_params, t_in, W, t_out, slope, q, grad_t_out, need_W=Tr
         _check("dstd_lif_backward", dstd_lif_backward(p, *args))
     else:
         _check("dstd_lif_backward_synfire", dstd_lif_backward_synfire(p, synfire, *args))
+    return gW, gt
+
+
+def exact_forward(p: dstd_lif_params, t_in, W, ws=None):
+    """Exact (sorted-input) forward of a dense layer; returns (t_out, slope,
+    k_idx). Only tau_m, tau_s, threshold and t_max of `p` are used."""
+    torch = _torch()
+    t_in = _cont(t_in, torch.float32)
+    W = _cont(W)
+    B, N_in = t_in.shape
+    N_out = W.shape[0]
+    assert W.shape[1] == N_in
+    dev = t_in.device
+    t_out = torch.empty((B, N_out), dtype=torch.float32, device=dev)
+    slope = torch.empty_like(t_out)
+    k = torch.empty((B, N_out), dtype=torch.int32, device=dev)
+    need = dstd_exact_forward_workspace_size(p, B, N_in, N_out)
+    if ws is None or ws.numel() < need:
+        ws = workspace(need, dev)
+    _check("dstd_exact_forward",
+           dstd_exact_forward(p, B, N_in, N_out, _ptr(t_in), _ptr(W), _wdtype(W), _ptr(t_out),
+                              _ptr(slope), _ptr(k), _ptr(ws), ws.numel(), _stream(dev)))
+    return t_out, slope, k
+
+
+def exact_backward(p: dstd_lif_params, t_in, W, t_out, slope, k, grad_t_out, need_W=True,
+                   need_t_in=True, ws=None):
+    """Exact backward of a dense layer; returns (grad_W or None, grad_t_in or None)."""
+    torch = _torch()
+    t_in = _cont(t_in, torch.float32)
+    W = _cont(W)
+    B, N_in = t_in.shape
+    N_out = W.shape[0]
+    dev = t_in.device
+    gW = torch.empty((N_out, N_in), dtype=torch.float32, device=dev) if need_W else None
+    gt = torch.empty((B, N_in), dtype=torch.float32, device=dev) if need_t_in else None
+    need = dstd_exact_backward_workspace_size(p, B, N_in, N_out)
+    if ws is None or ws.numel() < need:
+        ws = workspace(need, dev)
+    _check("dstd_exact_backward",
+           dstd_exact_backward(p, B, N_in, N_out, _ptr(t_in), _ptr(W), _wdtype(W),
+                               _ptr(_cont(t_out, torch.float32)), _ptr(_cont(slope, torch.float32)),
+                               _ptr(_cont(k, torch.int32)), _ptr(_cont(grad_t_out, torch.float32)),
+                               _ptr(gW), _ptr(gt), _ptr(ws), ws.numel(), _stream(dev)))
     return gW, gt
 
 

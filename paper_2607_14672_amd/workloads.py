@@ -243,3 +243,35 @@ class Draws:
 
 def with_batch(wl: Workload, batch: int) -> Workload:
     return replace(wl, batch=batch)
+
+
+# --------------------------------------------------- exact vs DSTD timing --
+# The paper's single-layer timing experiment (App. D.1, Fig. "DSTD_exp" (b)):
+# 1000 neurons, batch 100, input spikes uniform on [0, 1], the number of
+# inputs swept up to 6000, three neuron models, M in {10, 20}. The paper does
+# not give the weights; here W = (k / N_in) (1 + 0.3 sqrt(N_in) z), z ~ N(0, 1),
+# where k sets the mean summed weight per model (k = 2.5 V_th divided by the
+# peak of that model's kernel; for (inf, inf) the kernel has no peak and
+# k = 2.5), so most neurons fire within or shortly after the input window.
+EXACT_MODELS = {
+    "0.4-0.2": dict(tau_m=0.4, tau_s=0.2, k=25.0),
+    "inf-0.2": dict(tau_m=math.inf, tau_s=0.2, k=12.5),
+    "inf-inf": dict(tau_m=math.inf, tau_s=math.inf, k=2.5),
+}
+
+
+def exact_config(model: str = "0.4-0.2", n_in: int = 6000, M: int = 20, batch: int = 100,
+                 n_out: int = 1000, seed: int = 11) -> dict:
+    m = EXACT_MODELS[model]
+    return dict(model=model, batch=batch, n_in=n_in, n_out=n_out, M=M, t0=0.0, dt=1.0 / M,
+                tau_m=m["tau_m"], tau_s=m["tau_s"], threshold=1.0, k=m["k"], seed=seed)
+
+
+def exact_inputs(cfg: dict):
+    """(t_in [B, N_in], W [N_out, N_in]) float32 for an exact_config."""
+    rng = np.random.Generator(np.random.PCG64(cfg["seed"]))
+    t = rng.random((cfg["batch"], cfg["n_in"])).astype(np.float32)
+    n = cfg["n_in"]
+    z = rng.standard_normal((cfg["n_out"], n))
+    W = ((cfg["k"] / n) * (1.0 + 0.3 * math.sqrt(n) * z)).astype(np.float32)
+    return t, W

@@ -45,7 +45,7 @@ def excluded(orc, n_in, window):
     return amb, sens & ~amb
 
 
-def check_forward(gpu, orc, n_in, window, label=""):
+def check_forward(gpu, orc, n_in, window, label="", max_ambiguous=MAX_AMBIGUOUS):
     """gpu: dict of numpy arrays t_out, slope, q (fp32 path); orc: oracle dict.
     Returns the mask of neurons whose upstream gradient is zeroed."""
     amb, sens = excluded(orc, n_in, window)
@@ -75,7 +75,7 @@ def check_forward(gpu, orc, n_in, window, label=""):
     assert bad_t.sum() == 0, f"{label}: spike time beyond tolerance: {stats}"
     assert silent_ok, f"{label}: GPU fired where the oracle is silent"
     assert beyond.sum() <= MAX_BEYOND * nf + 1, f"{label}: ill-conditioned bucket too large: {stats}"
-    assert amb.sum() <= MAX_AMBIGUOUS * n + 1, f"{label}: ambiguity set too large: {stats}"
+    assert amb.sum() <= max_ambiguous * n + 1, f"{label}: ambiguity set too large: {stats}"
     return amb | sens | beyond, stats
 
 

@@ -216,3 +216,50 @@ def test_synfire_penalty_errors():
     assert dstd.dstd_synfire_penalty(sp, 4, 5, 1, 10, 1, 1, 0, 1, 256, need - 1, None) == dstd.DSTD_ERR_WORKSPACE
     assert dstd.dstd_synfire_penalty(sp, 1 << 16, 1 << 16, 1, 10, 1, 1, 0, 1, 256, 1 << 40,
                                      None) == dstd.DSTD_ERR_SHAPE
+
+
+# ------------------------------------------------------------------ exact --
+@pytest.mark.parametrize("kw,status", [
+    (dict(tau_m=1.0, tau_s=1.0005), dstd.DSTD_ERR_UNSUPPORTED),
+    (dict(tau_m=-1.0), dstd.DSTD_ERR_PARAM),
+    (dict(tau_s=math.nan), dstd.DSTD_ERR_PARAM),
+    (dict(threshold=0.0), dstd.DSTD_ERR_PARAM),
+    (dict(t_max=math.nan), dstd.DSTD_ERR_PARAM),
+])
+def test_exact_parameter_validation(kw, status):
+    p = _p(**kw)
+    assert dstd.dstd_exact_forward_workspace_size(p, 4, 10, 5) == 0
+    assert dstd.dstd_exact_forward(p, 4, 10, 5, 1, 1, 0, 1, 1, 1, 256, 1 << 20, None) == status
+    assert dstd.dstd_exact_backward(p, 4, 10, 5, 1, 1, 0, 1, 1, 1, 1, 1, 1, 256, 1 << 20,
+                                    None) == status
+    assert dstd.dstd_last_error()
+
+
+def test_exact_ignores_grid_and_bounds_inputs():
+    """The grid fields do not apply to the exact path (any values pass); a
+    finite t_max below the inputs is valid; N_in beyond one workgroup's sort
+    is unsupported."""
+    p = _p(M=0, dt=0.0, t0=math.nan, t_max=-5.0)
+    assert dstd.dstd_exact_forward_workspace_size(p, 4, 10, 5) > 0
+    assert dstd.dstd_exact_backward_workspace_size(p, 4, 10, 5) > 0
+    q = _p()
+    assert dstd.dstd_exact_forward_workspace_size(q, 2, 8192, 3) > 0
+    assert dstd.dstd_exact_forward_workspace_size(q, 2, 8193, 3) == 0
+    st = dstd.dstd_exact_forward(q, 2, 8193, 3, 1, 1, 0, 1, 1, 1, 256, 1 << 30, None)
+    assert st == dstd.DSTD_ERR_UNSUPPORTED
+
+
+def test_exact_null_and_workspace_errors():
+    p = _p()
+    need = dstd.dstd_exact_forward_workspace_size(p, 4, 10, 5)
+    assert dstd.dstd_exact_forward(p, 4, 10, 5, 1, 1, 0, None, 1, 1, 256, need, None) == dstd.DSTD_ERR_NULL
+    assert dstd.dstd_exact_forward(p, 4, 10, 5, 1, 1, 7, 1, 1, 1, 256, need, None) == dstd.DSTD_ERR_PARAM
+    assert dstd.dstd_exact_forward(p, 4, 10, 5, 1, 1, 0, 1, 1, 1, 256, need - 1, None) == dstd.DSTD_ERR_WORKSPACE
+    assert dstd.dstd_exact_forward(p, 4, 10, 5, 1, 1, 0, 1, 1, 1, 257, need, None) == dstd.DSTD_ERR_WORKSPACE
+    assert dstd.dstd_exact_forward(p, -1, 10, 5, 1, 1, 0, 1, 1, 1, 256, need, None) == dstd.DSTD_ERR_SHAPE
+    nb = dstd.dstd_exact_backward_workspace_size(p, 4, 10, 5)
+    assert dstd.dstd_exact_backward(p, 4, 10, 5, 1, 1, 0, 1, 1, 1, None, 1, 1, 256, nb, None) == dstd.DSTD_ERR_NULL
+    assert dstd.dstd_exact_backward(p, 4, 10, 5, 1, None, 0, 1, 1, 1, 1, 1, 1, 256, nb, None) == dstd.DSTD_ERR_NULL
+    # zero sizes: nothing to do, no workspace needed
+    assert dstd.dstd_exact_forward_workspace_size(p, 0, 10, 5) == 0
+    assert dstd.dstd_exact_forward(p, 0, 10, 5, None, 1, 0, None, None, None, None, 0, None) == dstd.DSTD_OK

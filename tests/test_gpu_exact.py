@@ -1,0 +1,240 @@
+"""GPU parity of the exact (sorted-input) spike-time path against the fp64
+oracle (App. A, Alg. 1, Eq. (timing_exact)), through the C ABI."""
+import math
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2607_14672_amd import workloads as wl
+from tests.parity import check_forward, check_grad
+
+pytestmark = pytest.mark.gpu
+
+INF = math.inf
+ROWS = [(1.0, 0.3), (1.0, 0.5), (0.4, 0.2), (2.0, 0.4), (0.5, 0.5), (INF, 0.3), (0.2, INF),
+        (INF, INF)]
+
+
+@pytest.fixture(scope="module")
+def dev():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    from paper_2607_14672_amd import dstd
+    dstd._load()  # fail loudly if the HIP library is missing
+    return torch.device("cuda:0")
+
+
+def _prm(p):
+    from paper_2607_14672_amd import dstd
+    # the grid fields do not apply to the exact path
+    return dstd.make_params(p["tau_m"], p["tau_s"], p["threshold"], 1, 0.0, 1.0,
+                            p.get("t_max", INF))
+
+
+def _gpu_forward(dev, p, t_in, W, bf16=False):
+    import torch
+    from paper_2607_14672_amd import dstd
+    prm = _prm(p)
+    tt = torch.from_numpy(np.ascontiguousarray(t_in, dtype=np.float32)).to(dev)
+    Wt = torch.from_numpy(np.ascontiguousarray(W, dtype=np.float32)).to(dev)
+    if bf16:
+        Wt = Wt.to(torch.bfloat16)
+    to, sl, k = dstd.exact_forward(prm, tt, Wt)
+    torch.cuda.synchronize()
+    return dict(t_out=to.cpu().numpy(), slope=sl.cpu().numpy(), q=k.cpu().numpy()), (prm, tt, Wt,
+                                                                                      to, sl, k)
+
+
+def _gpu_backward(dev, handles, g, need_W=True, need_t=True):
+    import torch
+    from paper_2607_14672_amd import dstd
+    prm, tt, Wt, to, sl, k = handles
+    gt = torch.from_numpy(np.ascontiguousarray(g, dtype=np.float32)).to(dev)
+    gW, gx = dstd.exact_backward(prm, tt, Wt, to, sl, k, gt, need_W=need_W, need_t_in=need_t)
+    torch.cuda.synchronize()
+    return (None if gW is None else gW.cpu().numpy()), (None if gx is None else gx.cpu().numpy())
+
+
+def _kpeak(tm, ts):
+    tv, ti = max(tm, ts), min(tm, ts)
+    if math.isinf(ti):
+        return 1.0
+    if math.isinf(tv):
+        return ti
+    if tv == ti:
+        return tv / math.e
+    return ti * (ti / tv) ** (ti / (tv - ti))
+
+
+def _case(seed, B, N_in, N_out, tm, ts, k=2.5, t_max=INF, threshold=1.0):
+    """Inputs U[0, 1) (the paper's single-layer timing workload, App. D.1);
+    weights with mean k * V_th / (N_in * peak of K) and a spread of the same
+    order, so most neurons fire inside or after the input window."""
+    rng = np.random.default_rng(seed)
+    p = dict(tau_m=tm, tau_s=ts, threshold=threshold, t_max=t_max)
+    t = rng.random((B, N_in)).astype(np.float32)
+    scale = k * threshold / (N_in * _kpeak(tm, ts))
+    W = (scale * (1 + 0.5 * math.sqrt(N_in) * rng.standard_normal((N_out, N_in)) / 4)).astype(np.float32)
+    return p, t, W
+
+
+def _special(t, rng):
+    """Silent (+inf), NaN, -inf inputs and exact ties."""
+    t = t.copy()
+    B, N = t.shape
+    for b in range(B):
+        idx = rng.choice(N, size=min(N, 8), replace=False)
+        vals = [np.inf, np.nan, -np.inf, np.inf]
+        for i, v in zip(idx[:4], vals):
+            t[b, i] = v
+        if N >= 8:
+            t[b, idx[5]] = t[b, idx[4]]          # a pair of simultaneous inputs
+            t[b, idx[6]] = t[b, idx[7]] = 0.5   # and a second group
+    return t.astype(np.float32)
+
+
+def _max_ambiguous(orc, n_in, window):
+    """Bound on the share of the ambiguity set for the exact path. Besides
+    near-tangent crossings (as for DSTD), the margin counts |v - V_th| at the
+    crossing interval's two ends. With N_in inputs over the window the ends are
+    about window/N_in apart, so a spike lies within 1e-5/slope of one of them
+    with probability e = 2e-5 N_in / (slope window). The bound is 1 % plus four
+    times the mean of e over the neurons (a margin for the spread of input
+    gaps)."""
+    f = orc["q"] >= 0
+    if not f.any():
+        return 0.01
+    e = np.minimum(1.0, 2e-5 * n_in / (np.abs(orc["slope"][f]) * window))
+    return 0.01 + 4.0 * float(e.sum()) / orc["q"].size
+
+
+def _parity(dev, p, t, W, label, bf16=False, seed=0, window=1.0):
+    Wq = wl.bf16_round(W) if bf16 else W
+    gpu, h = _gpu_forward(dev, p, t, Wq, bf16=bf16)
+    orc = oracle.exact_forward(p, t, Wq)
+    mask, stats = check_forward(gpu, orc, t.shape[1], window, label=label,
+                                max_ambiguous=_max_ambiguous(orc, t.shape[1], window))
+    g = np.random.default_rng(seed + 7).standard_normal(orc["t_out"].shape)
+    g = np.where(mask, 0.0, g).astype(np.float32)
+    gW, gx = _gpu_backward(dev, h, g)
+    ob = oracle.exact_backward(p, t, Wq, orc, np.where(orc["q"] >= 0, g.astype(np.float64), 0.0))
+    check_grad(gW, ob["grad_W"], label + " dW", ob["grad_W_abs"])
+    check_grad(gx, ob["grad_t_in"], label + " dt_in", ob["grad_t_in_abs"])
+    return gpu, orc, stats
+
+
+@pytest.mark.parametrize("tm,ts", ROWS)
+def test_exact_small_ragged(dev, tm, ts):
+    p, t, W = _case(3, 5, 37, 70, tm, ts)
+    t = _special(t, np.random.default_rng(4))
+    _, orc, st = _parity(dev, p, t, W, f"exact ragged tau=({tm},{ts})")
+    assert st["fired"] >= 0.3 * st["n"]
+
+
+def test_exact_multi_block_ragged(dev):
+    """Two 256-neuron blocks (the second ragged), 530 inputs, several batches
+    of records and an early stop per wave."""
+    p, t, W = _case(5, 9, 530, 300, 1.0, 0.3, k=3.0)
+    _parity(dev, p, t, W, "exact B=9 530->300")
+
+
+def test_exact_finite_t_max(dev):
+    """Inputs after t_max are ignored; the last interval ends at t_max."""
+    p, t, W = _case(6, 6, 120, 90, 1.0, 0.5, k=2.0, t_max=0.8)
+    gpu, orc, _ = _parity(dev, p, t, W, "exact t_max=0.8")
+    assert np.all(gpu["t_out"][np.isfinite(gpu["t_out"])] < 0.8)
+    assert np.isinf(orc["t_out"]).any()
+
+
+def test_exact_bf16_weights(dev):
+    p, t, W = _case(7, 4, 300, 130, 2.0, 0.4)
+    _parity(dev, p, t, W, "exact bf16", bf16=True)
+
+
+def test_exact_many_ties(dev):
+    """Inputs on a coarse time grid: long runs of simultaneous inputs, each
+    group added before its interval is tested."""
+    p, t, W = _case(8, 4, 400, 100, 1.0, 0.3, k=3.0)
+    t = (np.floor(t * 16) / 16).astype(np.float32)
+    _parity(dev, p, t, W, "exact ties")
+
+
+def test_exact_paper_width(dev):
+    """6000 inputs (the widest point of the paper's single-layer timing
+    experiment) on a few samples: records walked in many batches."""
+    p, t, W = _case(9, 3, 6000, 96, 0.4, 0.2, k=3.0)
+    _parity(dev, p, t, W, "exact 6000 inputs")
+
+
+def test_exact_bench_size_sampled(dev):
+    """The timed configuration (B = 100, N_in = 6000, N_out = 1000, the
+    general row): the forward and grad_t_in of sampled samples against the
+    oracle run on those samples alone (samples are independent); grad_W as a
+    sum over samples is checked at the smaller sizes above."""
+    import torch
+    from paper_2607_14672_amd import dstd
+    cfg = wl.exact_config()
+    p = dict(tau_m=cfg["tau_m"], tau_s=cfg["tau_s"], threshold=cfg["threshold"])
+    t, W = wl.exact_inputs(cfg)
+    gpu, h = _gpu_forward(dev, p, t, W)
+    rows = [0, 37, 99]
+    ts = t[rows]
+    orc = oracle.exact_forward(p, ts, W)
+    sub = {k: v[rows] for k, v in gpu.items()}
+    mask, _ = check_forward(sub, orc, t.shape[1], 1.0, label="exact bench-size sampled",
+                            max_ambiguous=_max_ambiguous(orc, t.shape[1], 1.0))
+    g = np.zeros(gpu["t_out"].shape, dtype=np.float32)
+    gs = np.random.default_rng(3).standard_normal((len(rows), W.shape[0]))
+    g[rows] = np.where(mask, 0.0, gs)
+    _, gx = _gpu_backward(dev, h, g, need_W=False)
+    ob = oracle.exact_backward(p, ts, W, orc, np.where(orc["q"] >= 0, g[rows].astype(np.float64), 0.0))
+    check_grad(gx[rows], ob["grad_t_in"], "exact bench-size dt_in", ob["grad_t_in_abs"])
+    others = np.setdiff1d(np.arange(t.shape[0]), rows)
+    assert not gx[others].any()  # samples with zero upstream gradient get none
+    del h
+    torch.cuda.synchronize()
+
+
+def test_exact_degenerate_sizes(dev):
+    import torch
+    from paper_2607_14672_amd import dstd
+    p = dict(tau_m=1.0, tau_s=0.3, threshold=1.0)
+    prm = _prm(p)
+    # no inputs: every neuron is silent, zero gradients
+    tt = torch.empty((3, 0), dtype=torch.float32, device=dev)
+    W = torch.empty((5, 0), dtype=torch.float32, device=dev)
+    to, sl, k = dstd.exact_forward(prm, tt, W)
+    assert torch.isinf(to).all() and (k == -1).all() and (sl == 0).all()
+    # all inputs silent
+    tt = torch.full((2, 40), math.inf, device=dev)
+    W = torch.ones((7, 40), device=dev)
+    to, sl, k = dstd.exact_forward(prm, tt, W)
+    assert torch.isinf(to).all() and (k == -1).all()
+    gW, gx = dstd.exact_backward(prm, tt, W, to, sl, k, torch.ones_like(to))
+    assert (gW == 0).all() and (gx == 0).all()
+    # no neurons: zero input gradients; no samples: zero weight gradients
+    tt = torch.rand((3, 20), device=dev)
+    W0 = torch.empty((0, 20), device=dev)
+    to, sl, k = dstd.exact_forward(prm, tt, W0)
+    gW, gx = dstd.exact_backward(prm, tt, W0, to, sl, k, torch.empty_like(to))
+    assert gx.shape == (3, 20) and (gx == 0).all()
+    tt = torch.empty((0, 20), device=dev)
+    W = torch.ones((4, 20), device=dev)
+    to, sl, k = dstd.exact_forward(prm, tt, W)
+    gW, gx = dstd.exact_backward(prm, tt, W, to, sl, k, torch.empty_like(to))
+    assert gW.shape == (4, 20) and (gW == 0).all()
+    torch.cuda.synchronize()
+
+
+def test_exact_deterministic(dev):
+    import torch
+    p, t, W = _case(11, 6, 500, 200, 1.0, 0.3, k=3.0)
+    _, h1 = _gpu_forward(dev, p, t, W)
+    _, h2 = _gpu_forward(dev, p, t, W)
+    for a, b in zip(h1[3:], h2[3:]):
+        assert torch.equal(a, b)
+    g = np.random.default_rng(2).standard_normal((6, 200)).astype(np.float32)
+    r1 = _gpu_backward(dev, h1, g)
+    r2 = _gpu_backward(dev, h2, g)
+    assert np.array_equal(r1[0], r2[0]) and np.array_equal(r1[1], r2[1])

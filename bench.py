@@ -350,6 +350,104 @@ def cpu_baseline(wl, min_seconds=10.0):
                        f"(fwd+bwd of all layers, fp64), {el:.1f} s")
 
 
+def exact_sweep(torch, dstd, workloads, dev, n_ins, models, Ms, reps=20, warmup=3):
+    """The paper's single-layer timing comparison (App. D.1, Fig. "DSTD_exp" (b)):
+    forward + backward (dL/dW and dL/dt_in) of one dense layer of 1000 neurons,
+    batch 100, inputs U[0, 1), by the exact sorted-input method and by DSTD
+    with M intervals on [0, 1], on the same inputs, weights and upstream
+    gradient. Times are wall-clock per pass over `reps` back-to-back passes
+    (eager launches on one stream); the library's workspace bytes of each
+    method are reported beside them."""
+    st = torch.cuda.current_stream(dev).cuda_stream
+    rows = []
+
+    def ck(name, s):
+        if s != 0:
+            raise RuntimeError(f"{name}: {dstd.dstd_last_error().decode()}")
+
+    def timed(fn):
+        for _ in range(warmup):
+            fn()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(reps):
+            fn()
+        torch.cuda.synchronize()
+        return 1e3 * (time.perf_counter() - t0) / reps
+
+    def kernels(fn, n=5):
+        """per-kernel ms per pass (library hipEvent timer, separate passes)"""
+        dstd.dstd_profile_reset()
+        dstd.dstd_profile_enable(True)
+        for _ in range(n):
+            fn()
+        torch.cuda.synchronize()
+        dstd.dstd_profile_enable(False)
+        return {k: round(v[1] / n, 4) for k, v in sorted(dstd.profile_table().items())}
+
+    for model in models:
+        for n_in in n_ins:
+            cfg = workloads.exact_config(model, n_in=n_in)
+            t_np, W_np = workloads.exact_inputs(cfg)
+            B, N_out = cfg["batch"], cfg["n_out"]
+            tt = torch.from_numpy(t_np).to(dev)
+            Wt = torch.from_numpy(W_np).to(dev)
+            g = torch.from_numpy(np.random.default_rng(1).standard_normal((B, N_out)).astype(np.float32)).to(dev)
+            to = torch.empty((B, N_out), device=dev)
+            sl = torch.empty_like(to)
+            ix = torch.empty((B, N_out), dtype=torch.int32, device=dev)
+            gW = torch.empty_like(Wt)
+            gx = torch.empty_like(tt)
+            pe = dstd.make_params(cfg["tau_m"], cfg["tau_s"], cfg["threshold"], 1, 0.0, 1.0)
+            nf = dstd.dstd_exact_forward_workspace_size(pe, B, n_in, N_out)
+            nb = dstd.dstd_exact_backward_workspace_size(pe, B, n_in, N_out)
+            wf = dstd.workspace(nf, dev)
+            wb = dstd.workspace(nb, dev)
+
+            def run_exact():
+                ck("dstd_exact_forward", dstd.dstd_exact_forward(
+                    pe, B, n_in, N_out, tt.data_ptr(), Wt.data_ptr(), dstd.DSTD_F32, to.data_ptr(),
+                    sl.data_ptr(), ix.data_ptr(), wf.data_ptr(), wf.numel(), st))
+                ck("dstd_exact_backward", dstd.dstd_exact_backward(
+                    pe, B, n_in, N_out, tt.data_ptr(), Wt.data_ptr(), dstd.DSTD_F32, to.data_ptr(),
+                    sl.data_ptr(), ix.data_ptr(), g.data_ptr(), gW.data_ptr(), gx.data_ptr(),
+                    wb.data_ptr(), wb.numel(), st))
+
+            ms_exact = timed(run_exact)
+            fired = float((ix >= 0).float().mean())
+            walked = float((ix.float() + 1).clamp(min=0).mean())
+            row = dict(model=model, n_in=n_in, exact_ms=round(ms_exact, 4),
+                       exact_ws_bytes=int(nf + nb), exact_fired=round(fired, 4),
+                       exact_mean_causal_inputs=round(walked, 1),
+                       exact_kernel_ms=kernels(run_exact), dstd={})
+            for M in Ms:
+                pd = dstd.make_params(cfg["tau_m"], cfg["tau_s"], cfg["threshold"], M, 0.0, 1.0 / M)
+                mf = dstd.dstd_lif_forward_workspace_size(pd, B, n_in, N_out)
+                mb = dstd.dstd_lif_backward_workspace_size(pd, B, n_in, N_out)
+                vf = dstd.workspace(mf, dev)
+                vb = dstd.workspace(mb, dev)
+
+                def run_dstd():
+                    ck("dstd_lif_forward", dstd.dstd_lif_forward(
+                        pd, B, n_in, N_out, tt.data_ptr(), Wt.data_ptr(), dstd.DSTD_F32,
+                        to.data_ptr(), sl.data_ptr(), ix.data_ptr(), vf.data_ptr(), vf.numel(), st))
+                    ck("dstd_lif_backward", dstd.dstd_lif_backward(
+                        pd, B, n_in, N_out, tt.data_ptr(), Wt.data_ptr(), dstd.DSTD_F32,
+                        to.data_ptr(), sl.data_ptr(), ix.data_ptr(), g.data_ptr(), gW.data_ptr(),
+                        gx.data_ptr(), vb.data_ptr(), vb.numel(), st))
+
+                ms = timed(run_dstd)
+                row["dstd"][str(M)] = dict(ms=round(ms, 4), ws_bytes=int(mf + mb),
+                                           fired=round(float((ix >= 0).float().mean()), 4),
+                                           speedup_vs_exact=round(ms_exact / ms, 3),
+                                           kernel_ms=kernels(run_dstd))
+                del vf, vb
+            rows.append(row)
+            print(json.dumps(row), file=sys.stderr, flush=True)
+            del wf, wb
+    return rows
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -365,6 +463,12 @@ def main():
                     help="add per-layer kernel times to the detail section")
     ap.add_argument("--copy-probe", action="store_true",
                     help="also run a 256 MiB device copy (HBM counter calibration)")
+    ap.add_argument("--exact-sweep", action="store_true",
+                    help="instead of the training step: time the exact sorted-input method "
+                         "against DSTD on the paper's single-layer timing workload")
+    ap.add_argument("--exact-n-in", default="1000,2000,4000,6000")
+    ap.add_argument("--exact-models", default="0.4-0.2,inf-0.2,inf-inf")
+    ap.add_argument("--exact-M", default="10,20")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build measures one GPU only; --gpus {args.gpus} is not supported "
@@ -376,6 +480,15 @@ def main():
     dstd._load()
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    if args.exact_sweep:
+        rows = exact_sweep(torch, dstd, workloads, dev,
+                           [int(x) for x in args.exact_n_in.split(",")],
+                           args.exact_models.split(","), [int(x) for x in args.exact_M.split(",")])
+        print(json.dumps({"report": "exact vs DSTD, single dense layer fwd+bwd",
+                          "config": {"batch": 100, "n_out": 1000, "inputs": "U[0,1) per input",
+                                     "grid": "[0,1] with M intervals"},
+                          "rows": rows}), flush=True)
+        return
     wl = workloads.get(args.workload)
     net = Net(wl, dev)
 

@@ -658,7 +658,7 @@ ExactWs exact_ws_layout(int64_t B, int64_t N_in, int64_t N_out, bool backward) {
         w.alpha = off; off += align_up(ns * sizeof(double));
         w.beta = off; off += align_up(ns * sizeof(double));
         w.kl = off; off += align_up(ns * sizeof(double));
-        w.kmax = off; off += align_up(ns * sizeof(double));
+        w.kmax = off; off += align_up(ns * sizeof(float));
         w.n = off; off += align_up((size_t)B * sizeof(int));
     }
     w.total = off;
@@ -701,8 +701,8 @@ dstd_status dstd_exact_forward(const dstd_lif_params *p, int64_t B, int64_t N_in
     if (B * N_out == 0) return DSTD_OK;
     LifConst C = make_const(&q);
     dstd::ExactRecs rec{at<int>(ws, L.j), at<float>(ws, L.t), at<float>(ws, L.len),
-                        at<float>(ws, L.r_lo), at<double>(ws, L.alpha), at<double>(ws, L.beta),
-                        at<double>(ws, L.kl), at<double>(ws, L.kmax), at<int>(ws, L.n), N_in};
+                        at<float>(ws, L.r_lo), at<float>(ws, L.kmax), at<double>(ws, L.alpha),
+                        at<double>(ws, L.beta), at<double>(ws, L.kl), at<int>(ws, L.n), N_in};
     hipError_t e = dstd::launch_exact_forward(C, B, N_in, N_out, W, w_dtype == DSTD_BF16,
                                               at<void>(ws, L.wt), rec, t_in, p->t_max, t_out,
                                               slope, k_idx, static_cast<hipStream_t>(stream));

@@ -26,12 +26,11 @@ namespace dstd {
 namespace {
 
 constexpr int kSortThreads = 1024;
-constexpr int kFwdThreads = 256;
-constexpr int kChunk = 8;       // records per batch of weight loads
-constexpr int kDwThreads = 128;
-constexpr int kDwTile = 16;     // neurons per dW block (accumulators per thread)
-constexpr int kDtThreads = 128;
-constexpr int kDtSamples = 4;   // samples per dt_in block (accumulators per thread)
+constexpr int kFwdThreads = 4 * kWave;
+constexpr int kChunk = 32;      // records per batch of weight and constant loads
+constexpr int kGradWaves = 4;   // waves splitting the summed dimension (LDS reduction)
+constexpr int kDwTile = 16;     // neurons per dW block (accumulators per lane)
+constexpr int kDtSamples = 4;   // samples per dt_in block (accumulators per lane)
 constexpr uint64_t kNoKey = ~0ull;
 
 // order-preserving map of a float to an unsigned key (and back)
@@ -144,7 +143,8 @@ __global__ __launch_bounds__(kSortThreads) void exact_prep_kernel(LifConst C, in
         rec.alpha[o + k] = last ? 0.0 : exp(-len * inv_tv);
         rec.beta[o + k] = last ? 0.0 : exp(-len * inv_ti);
         rec.kl[o + k] = last ? 0.0 : kern_dd(C.kind, tv, ti, len);
-        rec.kmax[o + k] = kern_dd(C.kind, tv, ti, fmin(len, upk));
+        // rounded up: a bound for the interval filter
+        rec.kmax[o + k] = __double2float_ru(kern_dd(C.kind, tv, ti, fmin(len, upk)));
     }
     if (threadIdx.x == 0) rec.n[b] = n;
 }
@@ -153,10 +153,11 @@ __global__ __launch_bounds__(kSortThreads) void exact_prep_kernel(LifConst C, in
 // time order. At input k the current jumps by w_ik; the interval [t~_k,
 // t~_k + len) is tested (zero-length intervals of simultaneous inputs are
 // skipped: they add up first); the state is then carried to the next input
-// with that interval's fp64 decays. A lane stops at its first crossing and
-// the wave once all its lanes have stopped; the roots are then solved
-// together. Weights of a batch of kChunk records are loaded before the batch
-// is processed and the next batch's loads are issued before its first step.
+// with that interval's fp64 decays. Records come in batches of kChunk (fully
+// unrolled); the weights and the interval constants of the next batch are
+// loaded during this one. A lane stops testing at its first crossing and the
+// wave stops once all its lanes have; the roots are then solved together.
+// The last partial batch is walked one record at a time.
 template <typename WT, int KS>
 __global__ __launch_bounds__(kFwdThreads) void exact_fwd_kernel(LifConst C, int N_in, int N_out,
                                                                 const WT *__restrict__ Wt,
@@ -170,62 +171,102 @@ __global__ __launch_bounds__(kFwdThreads) void exact_fwd_kernel(LifConst C, int 
     const int n = *as_const(rec.n + b);
     const int64_t o = static_cast<int64_t>(b) * rec.stride;
     const int *rj = rec.j + o;
-    const float *rt = rec.t + o, *rlen = rec.len + o, *rrl = rec.r_lo + o;
-    const double *ra = rec.alpha + o, *rb = rec.beta + o, *rk = rec.kl + o, *rm = rec.kmax + o;
+    const float *rlen = rec.len + o, *rrl = rec.r_lo + o, *rm = rec.kmax + o;
+    const double *ra = rec.alpha + o, *rb = rec.beta + o, *rk = rec.kl + o;
     const __amdgpu_buffer_rsrc_t wr =
         make_rsrc(Wt, static_cast<uint32_t>(static_cast<int64_t>(N_in) * N_out * sizeof(WT)));
     const int voff = (act ? i : 0) * static_cast<int>(sizeof(WT));
     const int rstride = N_out * static_cast<int>(sizeof(WT));
-    // records past n (the padding, or the next sample's) are never used, but
-    // their input index still forms a load offset: clamp it into [0, N_in)
-    const unsigned jmax = static_cast<unsigned>(max(N_in - 1, 0));
-    auto wrow = [&](int j) { return static_cast<int>(min(static_cast<unsigned>(j), jmax)) * rstride; };
+    auto wrow = [&](int k) { return as_const(rj)[k] * rstride; };  // k < n: j in [0, N_in)
 
     double Vd = 0.0, Id = 0.0;
     bool done = !act;
     int kf = -1;
     Seg sf{0.f, 0.f};
-    float hi = 0.f, fhi = 0.f, tf = 0.f;
+    float hi = 0.f, fhi = 0.f;
+    const double itv = static_cast<double>(C.inv_tv);
+    // one record: the jump of the current, the state carried over the
+    // interval, and the interval test where the filter lets it through
+    auto step = [&](int k, float wk, double al, double be, double kl, float kmax) {
+        Id = Id + static_cast<double>(wk);
+        const double vn = fma(Vd, al, Id * kl);
+        const double km = static_cast<double>(kmax);
+        const double vpos = fmax(Vd, 0.0);
+        const double ub = (kind_of<KS>(C) == kInfInf) ? ((Id > 0.0) ? fma(Id, km, vpos) : vpos)
+                                                      : fma(fmax(Id, 0.0), km, vpos);
+        // bitwise: the bound is formed on every step, not behind a branch on
+        // `done`
+        if ((ub >= C.theta_lo_d) & !done) {
+            // Inside an interval v has at most one critical point, so a
+            // crossing needs v near the threshold at an end of the interval
+            // or an interior maximum: v rising at the start and falling at
+            // the end (v' = -v/tv + I(u), I(u) = I e^{-u/ti}). The last
+            // interval's end value is not carried by the recurrence: always
+            // tested. Only these lanes run the full test.
+            const bool last = k + 1 == n;
+            const bool maybe = last || vn >= C.theta_lo_d || Vd >= C.theta_lo_d ||
+                               (fma(-Vd, itv, Id) > 0.0 && fma(-vn, itv, Id * be) < 0.0);
+            const float len = as_const(rlen)[k];
+            if (maybe && len > 0.f &&
+                seg_test<KS>(C, Vd, Id, vn, last, len, km, as_const(rrl)[k], sf, hi, fhi)) {
+                done = true;
+                kf = k;
+            }
+        }
+        Vd = vn;
+        Id = Id * be;
+    };
+    // Per batch, lane u < kChunk holds record u's constants (vector loads
+    // issued with the batch's weights, one batch ahead); each step reads them
+    // back as scalars with readlane.
+    static_assert(kChunk <= kWave, "one record's constants per lane");
+    const int lane = threadIdx.x & (kWave - 1);
+    const int ul = lane < kChunk ? lane : 0;
     float w[kChunk], wn[kChunk];
-    if (n > 0) {
+    double ca = 0.0, cb = 0.0, ck = 0.0, na = 0.0, nb = 0.0, nk = 0.0;
+    float cm = 0.f, nm = 0.f;
+    auto load_consts = [&](int kb) {
+        na = ra[kb + ul];
+        nb = rb[kb + ul];
+        nk = rk[kb + ul];
+        nm = rm[kb + ul];
+    };
+    auto lane_d = [](double v, int u) {
+        const int lo = __builtin_amdgcn_readlane(__double2loint(v), u);
+        const int hi = __builtin_amdgcn_readlane(__double2hiint(v), u);
+        return __hiloint2double(hi, lo);
+    };
+    if (n >= kChunk) {
 #pragma unroll
-        for (int u = 0; u < kChunk; ++u) wn[u] = BufLoad<WT>::get(wr, voff, wrow(as_const(rj)[u]));
+        for (int u = 0; u < kChunk; ++u) wn[u] = BufLoad<WT>::get(wr, voff, wrow(u));
+        load_consts(0);
     }
-    for (int k0 = 0; k0 < n; k0 += kChunk) {
+    int k0 = 0;
+    for (; k0 + kChunk <= n; k0 += kChunk) {
         if (__all(done)) break;
 #pragma unroll
         for (int u = 0; u < kChunk; ++u) w[u] = wn[u];
-        if (k0 + kChunk < n) {
+        ca = na; cb = nb; ck = nk; cm = nm;
+        if (k0 + 2 * kChunk <= n) {
 #pragma unroll
-            for (int u = 0; u < kChunk; ++u)
-                wn[u] = BufLoad<WT>::get(wr, voff, wrow(as_const(rj + k0 + kChunk)[u]));
+            for (int u = 0; u < kChunk; ++u) wn[u] = BufLoad<WT>::get(wr, voff, wrow(k0 + kChunk + u));
+            load_consts(k0 + kChunk);
         }
 #pragma unroll
-        for (int u = 0; u < kChunk; ++u) {
-            const int k = k0 + u;
-            if (k >= n) break;
-            if (!done) {
-                Id += static_cast<double>(w[u]);
-                const double vn = fma(Vd, as_const(ra)[k], Id * as_const(rk)[k]);
-                const float len = as_const(rlen)[k];
-                if (len > 0.f &&
-                    seg_test<KS>(C, Vd, Id, vn, k + 1 == n, len, as_const(rm)[k],
-                                 as_const(rrl)[k], sf, hi, fhi)) {
-                    done = true;
-                    kf = k;
-                    tf = as_const(rt)[k];
-                }
-                Vd = vn;
-                Id *= as_const(rb)[k];
-            }
-        }
+        for (int u = 0; u < kChunk; ++u)
+            step(k0 + u, w[u], lane_d(ca, u), lane_d(cb, u), lane_d(ck, u),
+                 __int_as_float(__builtin_amdgcn_readlane(__float_as_int(cm), u)));
     }
+    if (!__all(done))
+        for (int k = k0; k < n; ++k)
+            step(k, BufLoad<WT>::get(wr, voff, wrow(k)), as_const(ra)[k], as_const(rb)[k],
+                 as_const(rk)[k], as_const(rm)[k]);
     if (!act) return;
     float to = INFINITY, sl = 0.f;
     if (kf >= 0) {
         float u;
         seg_solve<KS>(C, sf, hi, fhi, u, sl);
-        to = static_cast<float>(static_cast<double>(tf) + static_cast<double>(u));
+        to = static_cast<float>(static_cast<double>(rec.t[o + kf]) + static_cast<double>(u));
     }
     const int64_t oo = static_cast<int64_t>(b) * N_out + i;
     t_out[oo] = to;
@@ -284,22 +325,28 @@ __device__ __forceinline__ void kern_pair(const LifConst &C, float d, float &K, 
     }
 }
 
-// grad_W[i][j] = sum_b gamma_bi K(t_bi - t_bj) over t_bj <= tl_bi: lane = input
-// j, kDwTile neurons per block (blockIdx.x: neuron tile, blockIdx.y: input
-// block), the per-neuron data read as scalars.
+// grad_W[i][j] = sum_b gamma_bi K(t_bi - t_bj) over t_bj <= tl_bi. Block:
+// kDwTile neurons (blockIdx.x) x 64 inputs (blockIdx.y, lane = input); its
+// kGradWaves waves take every kGradWaves-th sample and their partial sums
+// meet in LDS. The per-neuron data of a sample is read as scalars.
 template <int KS>
-__global__ __launch_bounds__(kDwThreads) void exact_dw_kernel(LifConst C, int B, int N_in, int N_out,
-                                                              const float *__restrict__ t_in,
-                                                              const float4 *__restrict__ P,
-                                                              float *__restrict__ grad_W) {
-    const int j = blockIdx.y * kDwThreads + threadIdx.x;
+__global__ __launch_bounds__(kGradWaves * kWave) void exact_dw_kernel(LifConst C, int B, int N_in,
+                                                                      int N_out,
+                                                                      const float *__restrict__ t_in,
+                                                                      const float4 *__restrict__ P,
+                                                                      float *__restrict__ grad_W) {
+    __shared__ float red[kGradWaves][kDwTile][kWave];
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = uniform(threadIdx.x >> 6);
+    const int j0 = blockIdx.y * kWave;
+    const int j = j0 + lane;
     const int i0 = blockIdx.x * kDwTile;
     const int ni = min(kDwTile, N_out - i0);
     const bool ok = j < N_in;
     float acc[kDwTile];
 #pragma unroll
     for (int ii = 0; ii < kDwTile; ++ii) acc[ii] = 0.f;
-    for (int b = 0; b < B; ++b) {
+    for (int b = wave; b < B; b += kGradWaves) {
         float t = ok ? t_in[static_cast<int64_t>(b) * N_in + j] : INFINITY;
         if (!isfinite(t)) t = INFINITY;
         const float *pb = reinterpret_cast<const float *>(P + static_cast<int64_t>(b) * N_out + i0);
@@ -316,22 +363,33 @@ __global__ __launch_bounds__(kDwThreads) void exact_dw_kernel(LifConst C, int B,
             }
         }
     }
-    if (!ok) return;
 #pragma unroll
-    for (int ii = 0; ii < kDwTile; ++ii)
-        if (ii < ni) grad_W[static_cast<int64_t>(i0 + ii) * N_in + j] = acc[ii];
+    for (int ii = 0; ii < kDwTile; ++ii) red[wave][ii][lane] = acc[ii];
+    __syncthreads();
+    for (int r = threadIdx.x; r < kDwTile * kWave; r += kGradWaves * kWave) {
+        const int ii = r / kWave, l = r % kWave;
+        if (ii < ni && j0 + l < N_in) {
+            float sum = 0.f;
+#pragma unroll
+            for (int w = 0; w < kGradWaves; ++w) sum += red[w][ii][l];
+            grad_W[static_cast<int64_t>(i0 + ii) * N_in + j0 + l] = sum;
+        }
+    }
 }
 
-// grad_t_in[b][j] = -sum_i gamma_bi w_ij K'(t_bi - t_bj) over t_bj <= tl_bi:
-// lane = input j, kDtSamples samples per block; row i of W is one coalesced
-// load per step.
+// grad_t_in[b][j] = -sum_i gamma_bi w_ij K'(t_bi - t_bj) over t_bj <= tl_bi.
+// Block: 64 inputs (blockIdx.x, lane = input) x kDtSamples samples
+// (blockIdx.y); its kGradWaves waves take every kGradWaves-th neuron (row i
+// of W is one coalesced load) and their partial sums meet in LDS.
 template <typename WT, int KS>
-__global__ __launch_bounds__(kDtThreads) void exact_dtin_kernel(LifConst C, int B, int N_in,
-                                                                int N_out, const WT *__restrict__ W,
-                                                                const float *__restrict__ t_in,
-                                                                const float4 *__restrict__ PT,
-                                                                float *__restrict__ grad_t_in) {
-    const int j = blockIdx.x * kDtThreads + threadIdx.x;
+__global__ __launch_bounds__(kGradWaves * kWave) void exact_dtin_kernel(
+    LifConst C, int B, int N_in, int N_out, const WT *__restrict__ W, const float *__restrict__ t_in,
+    const float4 *__restrict__ PT, float *__restrict__ grad_t_in) {
+    __shared__ float red[kGradWaves][kDtSamples][kWave];
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = uniform(threadIdx.x >> 6);
+    const int j0 = blockIdx.x * kWave;
+    const int j = j0 + lane;
     const int b0 = blockIdx.y * kDtSamples;
     const int nb = min(kDtSamples, B - b0);
     const bool ok = j < N_in;
@@ -342,8 +400,8 @@ __global__ __launch_bounds__(kDtThreads) void exact_dtin_kernel(LifConst C, int 
         t[bb] = isfinite(x) ? x : INFINITY;
         acc[bb] = 0.f;
     }
-#pragma unroll 4
-    for (int i = 0; i < N_out; ++i) {
+#pragma unroll 2
+    for (int i = wave; i < N_out; i += kGradWaves) {
         const float w = ok ? WLoad<WT>::get(W, static_cast<int64_t>(i) * N_in + j) : 0.f;
         const float *pi = reinterpret_cast<const float *>(PT + static_cast<int64_t>(i) * B + b0);
 #pragma unroll
@@ -359,10 +417,18 @@ __global__ __launch_bounds__(kDtThreads) void exact_dtin_kernel(LifConst C, int 
             }
         }
     }
-    if (!ok) return;
 #pragma unroll
-    for (int bb = 0; bb < kDtSamples; ++bb)
-        if (bb < nb) grad_t_in[static_cast<int64_t>(b0 + bb) * N_in + j] = acc[bb];
+    for (int bb = 0; bb < kDtSamples; ++bb) red[wave][bb][lane] = acc[bb];
+    __syncthreads();
+    for (int r = threadIdx.x; r < kDtSamples * kWave; r += kGradWaves * kWave) {
+        const int bb = r / kWave, l = r % kWave;
+        if (bb < nb && j0 + l < N_in) {
+            float sum = 0.f;
+#pragma unroll
+            for (int w = 0; w < kGradWaves; ++w) sum += red[w][bb][l];
+            grad_t_in[static_cast<int64_t>(b0 + bb) * N_in + j0 + l] = sum;
+        }
+    }
 }
 
 size_t sort_lds(int64_t N_in) {
@@ -428,13 +494,13 @@ hipError_t launch_exact_backward(const LifConst &C, int64_t B, int64_t N_in, int
     }
     if (grad_W && N_in * N_out > 0) {
         ProfScope prof("exact_dw", st);
-        dim3 grid(cdiv(N_out, kDwTile), cdiv(N_in, kDwThreads));
+        dim3 grid(cdiv(N_out, kDwTile), cdiv(N_in, kWave));
         if (gen)
-            hipLaunchKernelGGL(exact_dw_kernel<kGeneral>, grid, dim3(kDwThreads), 0, st, C,
+            hipLaunchKernelGGL(exact_dw_kernel<kGeneral>, grid, dim3(kGradWaves * kWave), 0, st, C,
                                static_cast<int>(B), static_cast<int>(N_in), static_cast<int>(N_out),
                                t_in, P, grad_W);
         else
-            hipLaunchKernelGGL(exact_dw_kernel<kAnyKind>, grid, dim3(kDwThreads), 0, st, C,
+            hipLaunchKernelGGL(exact_dw_kernel<kAnyKind>, grid, dim3(kGradWaves * kWave), 0, st, C,
                                static_cast<int>(B), static_cast<int>(N_in), static_cast<int>(N_out),
                                t_in, P, grad_W);
         hipError_t e = hipGetLastError();
@@ -442,9 +508,9 @@ hipError_t launch_exact_backward(const LifConst &C, int64_t B, int64_t N_in, int
     }
     if (grad_t_in && B * N_in > 0) {
         ProfScope prof("exact_dtin", st);
-        dim3 grid(cdiv(N_in, kDtThreads), cdiv(B, kDtSamples));
+        dim3 grid(cdiv(N_in, kWave), cdiv(B, kDtSamples));
 #define EXD(WTY, KSV)                                                                            \
-    hipLaunchKernelGGL((exact_dtin_kernel<WTY, KSV>), grid, dim3(kDtThreads), 0, st, C,          \
+    hipLaunchKernelGGL((exact_dtin_kernel<WTY, KSV>), grid, dim3(kGradWaves * kWave), 0, st, C,  \
                        static_cast<int>(B), static_cast<int>(N_in), static_cast<int>(N_out),      \
                        static_cast<const WTY *>(W), t_in, PT, grad_t_in)
         if (bf16) {

@@ -108,17 +108,18 @@ hipError_t launch_synfire_value(const Synfire &sf, int64_t B, int64_t rows, int6
 // inputs before t_max in ascending time order as records (SoA, each array
 // [B][stride], padded by kExactPad records at the end): input index j, time
 // t, candidate-interval length len (to the next input, or to t_max for the
-// last record) with e^{-kappa len}, and in fp64 the decays over len, K(len)
-// (carry the state to the next input) and max K on [0, len] (the interval
-// filter). n[b] = number of records of sample b.
+// last record) with e^{-kappa len} and max K on [0, len] (the interval
+// filter's bound, rounded up), and in fp64 the decays over len and K(len)
+// (they carry the state to the next input). n[b] = number of records of
+// sample b.
 struct ExactRecs {
     int *j;
-    float *t, *len, *r_lo;
-    double *alpha, *beta, *kl, *kmax;
+    float *t, *len, *r_lo, *kmax;
+    double *alpha, *beta, *kl;
     int *n;
     int64_t stride;
 };
-constexpr int kExactPad = 16;
+constexpr int kExactPad = 32;
 constexpr int kExactMaxIn = 8192;  // one block sorts a sample in 64 KB of LDS
 
 hipError_t launch_exact_forward(const LifConst &C, int64_t B, int64_t N_in, int64_t N_out,

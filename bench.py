@@ -68,6 +68,16 @@ class Net:
                 W = W.to(torch.bfloat16)
             p = dstd.make_params(lay.tau_m, lay.tau_s, lay.threshold, lay.M, lay.t0, lay.dt,
                                  lay.t_max)
+            skip = None
+            if lay.skip_back:
+                # SD block's third layer: t_in = cat(block input + delay, t_prev)
+                src = l - lay.skip_back
+                blk_in = self.t0 if src < 0 else self.L[src]["t_out"]
+                C1 = lay.C_in - t_prev.shape[1]
+                cat = torch.empty((B, lay.C_in, lay.H, lay.W), dtype=torch.float32, device=dev)
+                skip = dict(src=src, t1=blk_in, C1=C1, C2=t_prev.shape[1], HW=lay.H * lay.W,
+                            t2=t_prev, cat=cat, g_cat=torch.empty_like(cat))
+                t_prev = cat
             if lay.kind == "conv":
                 cs = dstd.make_conv_shape(**lay.conv_shape())
                 out_shape = (B, lay.C_out) + dstd.conv_out_hw(cs)
@@ -90,10 +100,17 @@ class Net:
                      gW=torch.empty(tuple(W.shape), dtype=torch.float32, device=dev))
             e["ws_f"] = dstd.workspace(ws_f, dev)
             e["ws_b"] = dstd.workspace(ws_b, dev)
+            e["skip"] = skip
             self.L.append(e)
             t_prev = e["t_out"]
+        # the skip channels' gradient joins the block input's gradient once the
+        # block's first layer has written its dt_in there
+        self.skip_adds = {}
         for l in range(1, len(self.L)):
-            self.L[l]["g_in_buf"] = self.L[l - 1]["g_out"]
+            sk = self.L[l]["skip"]
+            self.L[l]["g_in_buf"] = sk["g_cat"] if sk else self.L[l - 1]["g_out"]
+            if sk and sk["src"] >= 0:
+                self.skip_adds.setdefault(sk["src"] + 1, []).append(l)
         last = wl.layers[-1]
         self.t_cap = float(last.t0 + last.M * last.dt + 2.0)
         if wl.loss == "ce":
@@ -114,6 +131,11 @@ class Net:
         ds = self.dstd
         e = self.L[l]
         lay = e["lay"]
+        sk = e["skip"]
+        if sk is not None:
+            self._ck("dstd_skip_delay_concat", ds.dstd_skip_delay_concat(
+                self.B, sk["C1"], sk["C2"], sk["HW"], sk["t1"].data_ptr(), lay.skip_delay,
+                sk["t2"].data_ptr(), sk["cat"].data_ptr(), self.stream))
         if e["cs"] is not None:
             self._ck("dstd_lif_conv_forward", ds.dstd_lif_conv_forward(
                 e["p"], e["cs"], self.B, e["t_in"].data_ptr(), e["W"].data_ptr(), e["wdt"],
@@ -138,8 +160,19 @@ class Net:
                 e["g_out"].data_ptr(), self.loss.data_ptr(), self.stream))
 
     def backward(self):
+        ds = self.dstd
         for l in reversed(range(len(self.L))):
             self.backward_layer(l)
+            sk = self.L[l]["skip"]
+            if sk is not None:  # the second layer's share of the concatenated input's gradient
+                self._ck("dstd_skip_delay_concat_backward", ds.dstd_skip_delay_concat_backward(
+                    self.B, sk["C1"], sk["C2"], sk["HW"], sk["g_cat"].data_ptr(), None, 0,
+                    self.L[l - 1]["g_out"].data_ptr(), self.stream))
+            for m in self.skip_adds.get(l, ()):  # the block input's share, added
+                sm = self.L[m]["skip"]
+                self._ck("dstd_skip_delay_concat_backward", ds.dstd_skip_delay_concat_backward(
+                    self.B, sm["C1"], sm["C2"], sm["HW"], sm["g_cat"].data_ptr(),
+                    self.L[sm["src"]]["g_out"].data_ptr(), 1, None, self.stream))
 
     def backward_layer(self, l):
         ds = self.dstd
@@ -321,6 +354,10 @@ def cpu_baseline(wl, min_seconds=10.0):
         t = t_first
         fw = []
         for l, lay in enumerate(wl.layers):
+            if lay.skip_back:  # SD block: cat(block input + delay, previous output)
+                blk = fw[l - lay.skip_back][1]["t_out"].astype(np.float32)
+                t = np.concatenate([blk + np.float32(lay.skip_delay), t.reshape(blk.shape[0], -1,
+                                    *blk.shape[2:])], axis=1)
             r = fwd(lay, t, Ws[l])
             fw.append((t, r))
             t = r["t_out"].astype(np.float32)
@@ -335,9 +372,17 @@ def cpu_baseline(wl, min_seconds=10.0):
             g = np.where(np.isfinite(to), -(s - np.eye(to.shape[1])[labels]) / nb, 0.0)
         else:
             g = np.where(np.isfinite(to), (to - targets) / nb, 0.0)
+        pend = {}  # block input's share of a skip gradient, keyed by the block's first layer
         for l in reversed(range(len(wl.layers))):
             tin, r = fw[l]
             gx = bwd(wl.layers[l], tin, Ws[l], r, g, l > 0)
+            lay = wl.layers[l]
+            if lay.skip_back and l > 0:
+                c1 = fw[l - lay.skip_back][1]["t_out"].shape[1]
+                pend[l - lay.skip_back + 1] = gx[:, :c1]
+                gx = gx[:, c1:]
+            if l in pend and l > 0:
+                gx = gx.reshape(pend[l].shape) + pend.pop(l)
             if l > 0:
                 g = gx
         reps += 1

@@ -302,6 +302,38 @@ dstd_status dstd_profile_entry(int32_t idx, const char **name, int64_t *launches
                                double *total_ms);
 void dstd_profile_reset(void);
 
+/* ----------------------------------------------------------------- skip -- */
+
+/*
+ * Skip-and-delay connection of an SD block (App. C.3, Fig. "skip_connection",
+ * Table "tab:architectures"): the block's third layer receives the spikes
+ * entering the block, delayed by a fixed 2 tau_shift, together with the
+ * second layer's spikes. The delay moves those inputs into the third layer's
+ * synfire window. The two maps are concatenated along channels (block input
+ * first), and the result is the t_in of an ordinary conv call.
+ *  t1  [B][C1][HW]       spikes entering the block
+ *  t2  [B][C2][HW]       the block's second-layer output (same H x W = HW)
+ *  out [B][C1 + C2][HW]  out: t1 + delay, then t2 (non-finite times stay
+ *                        silent: +inf + delay = +inf)
+ * delay finite; sizes >= 0 with (C1 + C2) * HW < 2^30 and B <= 65535.
+ */
+dstd_status dstd_skip_delay_concat(int64_t B, int64_t C1, int64_t C2, int64_t HW, const float *t1,
+                                   float delay, const float *t2, float *out, void *stream);
+
+/*
+ * Its backward: the delay is a constant shift, so each channel's gradient
+ * passes back unchanged.
+ *  g  [B][C1 + C2][HW]  dL/d(out)
+ *  g1 [B][C1][HW]       out: the first C1 channels of g; added to g1's
+ *                       contents when accumulate = 1 (the block input also
+ *                       feeds the block's first layer, whose dt_in is already
+ *                       there), written when 0; NULL to skip
+ *  g2 [B][C2][HW]       out (written): the remaining channels; NULL to skip
+ */
+dstd_status dstd_skip_delay_concat_backward(int64_t B, int64_t C1, int64_t C2, int64_t HW,
+                                            const float *g, float *g1, int32_t accumulate,
+                                            float *g2, void *stream);
+
 /* ---------------------------------------------------------------- exact -- */
 
 /*

@@ -736,3 +736,48 @@ dstd_status dstd_exact_backward(const dstd_lif_params *p, int64_t B, int64_t N_i
 }
 
 }  // extern "C"
+
+// ------------------------------------------------------------------- skip --
+namespace {
+
+dstd_status check_skip(int64_t B, int64_t C1, int64_t C2, int64_t HW) {
+    if (B < 0 || C1 < 0 || C2 < 0 || HW < 0)
+        return fail(DSTD_ERR_SHAPE, "sizes must be >= 0 (B=%lld C1=%lld C2=%lld HW=%lld)",
+                    (long long)B, (long long)C1, (long long)C2, (long long)HW);
+    if (B > 65535) return fail(DSTD_ERR_SHAPE, "B = %lld exceeds 65535", (long long)B);
+    if ((C1 + C2) * HW >= ((int64_t)1 << 30))
+        return fail(DSTD_ERR_SHAPE, "(C1 + C2) * HW must be below 2^30 per sample");
+    return DSTD_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+dstd_status dstd_skip_delay_concat(int64_t B, int64_t C1, int64_t C2, int64_t HW, const float *t1,
+                                   float delay, const float *t2, float *out, void *stream) {
+    dstd_status s = check_skip(B, C1, C2, HW);
+    if (s != DSTD_OK) return s;
+    if (!isfinite(delay)) return fail(DSTD_ERR_PARAM, "delay must be finite");
+    if (B * (C1 + C2) * HW == 0) return DSTD_OK;
+    if (!out || (C1 * HW > 0 && !t1) || (C2 * HW > 0 && !t2))
+        return fail(DSTD_ERR_NULL, "t1, t2 and out are required");
+    hipError_t e = dstd::launch_skip_concat(B, C1 * HW, C2 * HW, t1, delay, t2, out,
+                                            static_cast<hipStream_t>(stream));
+    return hip_status(e, "skip concat launch");
+}
+
+dstd_status dstd_skip_delay_concat_backward(int64_t B, int64_t C1, int64_t C2, int64_t HW,
+                                            const float *g, float *g1, int32_t accumulate,
+                                            float *g2, void *stream) {
+    dstd_status s = check_skip(B, C1, C2, HW);
+    if (s != DSTD_OK) return s;
+    if (accumulate != 0 && accumulate != 1) return fail(DSTD_ERR_PARAM, "accumulate must be 0 or 1");
+    if (B * (C1 + C2) * HW == 0) return DSTD_OK;
+    if (!g) return fail(DSTD_ERR_NULL, "g is NULL");
+    hipError_t e = dstd::launch_skip_split(B, C1 * HW, C2 * HW, g, g1, accumulate, g2,
+                                           static_cast<hipStream_t>(stream));
+    return hip_status(e, "skip split launch");
+}
+
+}  // extern "C"

@@ -103,6 +103,15 @@ hipError_t launch_synfire_value(const Synfire &sf, int64_t B, int64_t rows, int6
                                 int64_t row_len, const float *t_out, const void *W, bool bf16,
                                 float *ws, float *value, hipStream_t st);
 
+// ------------------------------------------------------------------ skip --
+// Skip-and-delay input of an SD block: per sample n1 = C1*HW delayed block
+// inputs then n2 = C2*HW second-layer outputs (concatenation along channels),
+// and the split of its gradient (acc: add into g1 instead of overwriting).
+hipError_t launch_skip_concat(int64_t B, int64_t n1, int64_t n2, const float *t1, float delay,
+                              const float *t2, float *out, hipStream_t st);
+hipError_t launch_skip_split(int64_t B, int64_t n1, int64_t n2, const float *g, float *g1, int acc,
+                             float *g2, hipStream_t st);
+
 // ----------------------------------------------------------------- exact --
 // Exact spike times by sorting (App. A, Alg. 1). Per sample, the finite
 // inputs before t_max in ascending time order as records (SoA, each array

@@ -81,6 +81,8 @@ _SIGS = {
     "dstd_exact_backward_workspace_size": (_S, [_P, _L, _L, _L]),
     "dstd_exact_forward": (_I, [_P, _L, _L, _L, _P, _P, _I, _P, _P, _P, _P, _S, _P]),
     "dstd_exact_backward": (_I, [_P, _L, _L, _L, _P, _P, _I, _P, _P, _P, _P, _P, _P, _P, _S, _P]),
+    "dstd_skip_delay_concat": (_I, [_L, _L, _L, _L, _P, _F, _P, _P, _P]),
+    "dstd_skip_delay_concat_backward": (_I, [_L, _L, _L, _L, _P, _P, C.c_int32, _P, _P]),
     "dstd_softmax_ce_grad": (_I, [_L, _L, _P, _P, _F, _F, _P, _P, _P]),
     "dstd_mse_grad": (_I, [_L, _L, _P, _P, _P, _P, _P]),
     "dstd_profile_enable": (C.c_int32, [C.c_int32]),
@@ -155,6 +157,14 @@ def dstd_exact_backward(p, B, N_in, N_out, t_in, W, w_dtype, t_out, slope, k_idx
                         grad_W, grad_t_in, ws, ws_bytes, stream):
     return _load().dstd_exact_backward(_ref(p), B, N_in, N_out, t_in, W, w_dtype, t_out, slope,
                                        k_idx, grad_t_out, grad_W, grad_t_in, ws, ws_bytes, stream)
+
+
+def dstd_skip_delay_concat(B, C1, C2, HW, t1, delay, t2, out, stream):
+    return _load().dstd_skip_delay_concat(B, C1, C2, HW, t1, delay, t2, out, stream)
+
+
+def dstd_skip_delay_concat_backward(B, C1, C2, HW, g, g1, accumulate, g2, stream):
+    return _load().dstd_skip_delay_concat_backward(B, C1, C2, HW, g, g1, accumulate, g2, stream)
 
 
 def dstd_lif_conv_forward_workspace_size(p, cs, B):
@@ -361,6 +371,43 @@ def backward(p: dstd_lif_params, t_in, W, t_out, slope, q, grad_t_out, need_W=Tr
     else:
         _check("dstd_lif_backward_synfire", dstd_lif_backward_synfire(p, synfire, *args))
     return gW, gt
+
+
+def skip_delay_concat(t1, delay: float, t2):
+    """SD-block skip input: cat([t1 + delay, t2], channels). t1 [B, C1, H, W], t2 [B, C2, H, W]."""
+    torch = _torch()
+    t1 = _cont(t1, torch.float32)
+    t2 = _cont(t2, torch.float32)
+    B, C1 = t1.shape[:2]
+    C2 = t2.shape[1]
+    assert t2.shape[0] == B and t1.shape[2:] == t2.shape[2:]
+    HW = int(math.prod(t1.shape[2:]))
+    out = torch.empty((B, C1 + C2) + tuple(t1.shape[2:]), dtype=torch.float32, device=t1.device)
+    _check("dstd_skip_delay_concat",
+           dstd_skip_delay_concat(B, C1, C2, HW, _ptr(t1), float(delay), _ptr(t2), _ptr(out),
+                                  _stream(t1.device)))
+    return out
+
+
+def skip_delay_concat_backward(g, C1: int, g1=None, want_g2=True):
+    """Split dL/d(concat) [B, C1 + C2, H, W]: adds the first C1 channels into g1
+    (written when g1 is None) and returns (g1, g2)."""
+    torch = _torch()
+    g = _cont(g, torch.float32)
+    B, C = g.shape[:2]
+    C2 = C - C1
+    HW = int(math.prod(g.shape[2:]))
+    acc = 1
+    if g1 is None:
+        g1 = torch.empty((B, C1) + tuple(g.shape[2:]), dtype=torch.float32, device=g.device)
+        acc = 0
+    else:
+        assert g1.is_contiguous() and g1.dtype == torch.float32 and g1.shape[:2] == (B, C1)
+    g2 = torch.empty((B, C2) + tuple(g.shape[2:]), dtype=torch.float32, device=g.device) if want_g2 else None
+    _check("dstd_skip_delay_concat_backward",
+           dstd_skip_delay_concat_backward(B, C1, C2, HW, _ptr(g), _ptr(g1), acc, _ptr(g2),
+                                           _stream(g.device)))
+    return g1, g2
 
 
 def exact_forward(p: dstd_lif_params, t_in, W, ws=None):

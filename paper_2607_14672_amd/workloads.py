@@ -50,6 +50,11 @@ class LayerSpec:
     stride: int = 1
     pad: int = 1
     pool_in: int = 1          # 1 none, 2 = 2x2 average of input events, 0 = global average
+    # skip-and-delay (third layer of an SD block): the input is the channel
+    # concatenation of the output of the layer skip_back positions earlier
+    # (the block input) delayed by skip_delay, then the previous layer's output
+    skip_back: int = 0
+    skip_delay: float = 0.0
 
     def params(self) -> dict:
         return dict(tau_m=self.tau_m, tau_s=self.tau_s, threshold=self.threshold, M=self.M,
@@ -161,6 +166,40 @@ def conv20() -> Workload:
                     description="20-layer conv DSTD-LIF net on 28x28x1, batch 128, M=16")
 
 
+def synsnn20_sd(n_ch: int = 32) -> Workload:
+    """Syn-SNN-20 of Table "tab:architectures": C(N,3,1)-SD2(N)-SD1(N)-SD2(2N)-
+    SD1(2N)-SD2(4N)-SD1(4N)-10 on 28x28x1, B 128, M 16, tau (1.5, 0.5). An SD
+    block is three 3x3 convs; its third reads cat(block input delayed by
+    2 tau_shift, second layer's output) (App. C.3, Fig. "skip_connection"),
+    with stride 2 and doubled channels in SD1, stride 1 in SD2. Layer l
+    (1-based) discretizes [l-1, l] (tau_shift = 1), so the delay is 2. The
+    classifier is a global pool of events and a dense 4N -> 10 layer, as for
+    conv20. Weights: a fixed k = 7 for every layer (no calibration; deep
+    layers mostly stay silent at random init, as in the conv workloads)."""
+    M, tm, ts = 16, 1.5, 0.5
+    L, H, C, l = [], 28, 1, 1
+    L.append(_conv_layer(l, C, H, H, n_ch, M, tm, ts))
+    C = n_ch
+    for kind, mult in (("SD2", 1), ("SD1", 1), ("SD2", 2), ("SD1", 2), ("SD2", 4), ("SD1", 4)):
+        N = n_ch * mult
+        Cb = C  # block input channels (= N)
+        L.append(_conv_layer(l + 1, Cb, H, H, N, M, tm, ts))
+        L.append(_conv_layer(l + 2, N, H, H, N, M, tm, ts))
+        st = 2 if kind == "SD1" else 1
+        N3 = 2 * N if kind == "SD1" else N
+        lay = _conv_layer(l + 3, Cb + N, H, H, N3, M, tm, ts, stride=st)
+        lay.skip_back, lay.skip_delay = 3, 2.0
+        L.append(lay)
+        H = (H + 2 - 3) // st + 1
+        C = N3
+        l += 3
+    L.append(LayerSpec("conv", C * H * H, 10, M, float(l), 1.0 / M, tm, ts, C_in=C, H=H, W=H,
+                       C_out=10, KH=1, KW=1, stride=1, pad=0, pool_in=0))
+    return Workload("synsnn20-sd", 128, L, "u", loss="ce", seed=6,
+                    description="Syn-SNN-20 with skip-and-delay blocks on 28x28x1, batch 128, M=16",
+                    extra={"k": [7.0] * len(L)})
+
+
 WORKLOADS = {
     "dense1": lambda: dense1(False),
     "dense1-cal": lambda: dense1(True),
@@ -171,6 +210,7 @@ WORKLOADS = {
     "wide-M128": lambda: wide(128),
     "conv9": conv9,
     "conv20": conv20,
+    "synsnn20-sd": synsnn20_sd,
 }
 
 
@@ -229,6 +269,8 @@ class Draws:
             n = lay.fan_in()
             w = z * (2.0 / n) + 0.5 / n
         else:
+            if k is None and "k" in self.wl.extra:
+                k = self.wl.extra["k"][l]
             if k is None:
                 k = load_calibration().get(self.wl.name, {}).get("k", [None] * len(self.wl.layers))[l]
                 if k is None:

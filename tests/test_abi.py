@@ -263,3 +263,16 @@ def test_exact_null_and_workspace_errors():
     # zero sizes: nothing to do, no workspace needed
     assert dstd.dstd_exact_forward_workspace_size(p, 0, 10, 5) == 0
     assert dstd.dstd_exact_forward(p, 0, 10, 5, None, 1, 0, None, None, None, None, 0, None) == dstd.DSTD_OK
+
+
+# ------------------------------------------------------------------- skip --
+def test_skip_delay_validation():
+    assert dstd.dstd_skip_delay_concat(-1, 2, 2, 4, 1, 1.0, 1, 1, None) == dstd.DSTD_ERR_SHAPE
+    assert dstd.dstd_skip_delay_concat(2, 2, 2, 4, 1, math.inf, 1, 1, None) == dstd.DSTD_ERR_PARAM
+    assert dstd.dstd_skip_delay_concat(2, 2, 2, 4, None, 1.0, 1, 1, None) == dstd.DSTD_ERR_NULL
+    assert dstd.dstd_skip_delay_concat(2, 2, 2, 4, 1, 1.0, 1, None, None) == dstd.DSTD_ERR_NULL
+    assert dstd.dstd_skip_delay_concat(0, 2, 2, 4, None, 1.0, None, None, None) == dstd.DSTD_OK
+    assert dstd.dstd_skip_delay_concat(2, 1 << 15, 1 << 15, 1 << 15, 1, 1.0, 1, 1, None) == dstd.DSTD_ERR_SHAPE
+    assert dstd.dstd_skip_delay_concat_backward(2, 2, 2, 4, None, 1, 0, 1, None) == dstd.DSTD_ERR_NULL
+    assert dstd.dstd_skip_delay_concat_backward(2, 2, 2, 4, 1, 1, 2, 1, None) == dstd.DSTD_ERR_PARAM
+    assert dstd.dstd_skip_delay_concat_backward(2, -2, 2, 4, 1, 1, 0, 1, None) == dstd.DSTD_ERR_SHAPE

@@ -14,6 +14,8 @@ from .oracle import (  # noqa: F401
     dstd_backward,
     exact_forward,
     exact_backward,
+    ms_forward,
+    ms_backward,
     conv_forward,
     conv_backward,
     num_threads,

@@ -14,6 +14,7 @@
  *   exact spike time (sort + interval candidates) App. A, Eq. (timing_exact), Alg. 1
  *   exact spike-time gradients .................. implicit function theorem on
  *                                                  v(t) = V_th over the causal set (App. A)
+ *   multi-spike DSTD (reset of v, current kept) . App. "multi-spikes", Eq. (Vmem_multiSpikes)
  *   DSTD grid T_m = T_first + m*dt - t_offset .. App. B.1
  *   DSTD event weights s_jm ..................... Eq. (DSTD_kernel), Table "tab:DSTD_kernels"
  *   weighted events w^_im = sum_j w_ij s_jm ..... App. B.1 (definition of w^)
@@ -770,6 +771,224 @@ void oracle_exact_backward(double tau_m, double tau_s, int64_t B, int64_t N_in, 
     }
     free(gam);
     free(tl);
+}
+
+/* ------------------------------------------------------------------------ */
+/* Multi-spike DSTD (App. "multi-spikes", Eq. (Vmem_multiSpikes) and the      */
+/* DSTD form after it).                                                      */
+/*                                                                           */
+/* Each input neuron j may fire F_in times; every input spike gets its own   */
+/* events s_jm^f and the weighted events sum them. After an output spike at  */
+/* t_k the membrane potential is reset to 0 and the synaptic current is not, */
+/* so from t_k on                                                            */
+/*   v(t) = I(t_k) K(t - t_k) + sum_{t_k < T_q <= t} w^_q K(t - T_q),        */
+/*   I(t_k) = sum_{T_q <= t_k} w^_q e^{-(t_k - T_q)/tau_I}.                  */
+/* The spikes are the successive first crossings of V_th (several may fall   */
+/* in one interval); the first F_out are kept.                               */
+/* ------------------------------------------------------------------------ */
+
+/* current at time t from the events at T_0..T_q (T_q <= t) */
+static double ms_current(const prm_t *p, const double *wh, int q, double t) {
+    double I = 0.0;
+    for (int m = 0; m <= q; ++m) I += wh[m] * exp(-(t - grid(p->t0, p->dt, m)) / p->ti);
+    return I;
+}
+
+/* coefficient of w^_m in v_k(t_k): K(t_k - T_m) for T_m after the previous
+   spike (m > q_prev), e^{-(t_prev - T_m)/tau_I} K(t_k - t_prev) for T_m at or
+   before it (m <= q_prev), 0 after t_k (m > q_k); q_prev = -1 for k = 0 */
+static double ms_coef(const prm_t *p, int m, double tk, int qk, double tprev, int qprev) {
+    if (m > qk) return 0.0;
+    double Tm = grid(p->t0, p->dt, m);
+    if (m > qprev) return kern(p->tv, p->ti, tk - Tm);
+    return exp(-(tprev - Tm) / p->ti) * kern(p->tv, p->ti, tk - tprev);
+}
+
+/* scan of one neuron with reset; outputs per spike k < F (unset spikes:
+   t = +inf, slope 0, q -1, cur 0, margin min over the rest of the grid) */
+static void ms_scan(const prm_t *p, const double *wh, const double *wabs, int F, double *t_out,
+                    double *slope, int32_t *q_out, double *cur, double *margin, double *vabs) {
+    for (int k = 0; k < F; ++k) {
+        t_out[k] = INFINITY; slope[k] = 0.0; q_out[k] = -1; cur[k] = 0.0;
+        if (margin) margin[k] = INFINITY;
+        if (vabs) vabs[k] = 0.0;
+    }
+    int nk = 0, qprev = -1;
+    double tprev = -INFINITY, pre = INFINITY;
+    piece_t pc;
+    piece_init(&pc, p->tv, p->ti, p->theta, p->t0);
+    for (int q = 0; q <= p->M && nk < F; ++q) {
+        double Tq = grid(p->t0, p->dt, q);
+        piece_add(&pc, wh[q], Tq);
+        double hi = (q < p->M) ? grid(p->t0, p->dt, q + 1) : p->t_max;
+        double lo = Tq > tprev ? Tq : tprev;
+        while (nk < F) {
+            double root, peak;
+            if (!(hi > lo) || !first_crossing(&pc, lo, hi, &root, &peak)) {
+                if (hi > lo) pre = fmin(pre, p->theta - peak);
+                break;
+            }
+            double mg = fmin(pre, fabs(peak - p->theta));
+            mg = fmin(mg, fabs(pv(&pc, lo) - p->theta));
+            if (q < p->M) mg = fmin(mg, fabs(pv(&pc, hi) - p->theta));
+            t_out[nk] = root;
+            slope[nk] = pdv(&pc, root);
+            q_out[nk] = q;
+            cur[nk] = ms_current(p, wh, q, root);
+            if (margin) margin[nk] = mg;
+            if (vabs) {
+                double va = 0.0;
+                for (int m = 0; m <= q; ++m)
+                    va += wabs[m] * fabs(ms_coef(p, m, root, q, tprev, qprev));
+                vabs[nk] = va;
+            }
+            ++nk;
+            /* reset: v = 0 at root, the current carries on */
+            tprev = root;
+            qprev = q;
+            piece_init(&pc, p->tv, p->ti, p->theta, root);
+            piece_add(&pc, cur[nk - 1], root);
+            pre = INFINITY;
+            lo = root;
+        }
+    }
+    if (margin && nk < F) margin[nk] = pre;
+}
+
+/*
+ * Forward: t_in [B][N_in][F_in] (non-finite = no spike), W [N_out][N_in];
+ * per output spike [B][N_out][F_out]: t_out (+inf = none), slope, q_idx
+ * (-1 = none), cur = I(t_k) (the current at the spike, which carries over the
+ * reset), and optionally margin, vabs, and dprev = d t_k / d t_{k-1} through
+ * the reset (0 for k = 0):
+ *   d t_k / d t_{k-1} = I(t_{k-1}) (K(d)/tau_I + K'(d)) / slope_k,  d = t_k - t_{k-1}.
+ */
+void oracle_ms_forward(double tau_m, double tau_s, double theta, int M, double t0, double dt,
+                       double t_max, int64_t B, int64_t N_in, int64_t F_in, int64_t N_out,
+                       int64_t F_out, const double *t_in, const double *W, double *t_out,
+                       double *slope, int32_t *q_idx, double *cur, double *margin, double *vabs,
+                       double *dprev) {
+    prm_t p;
+    canon(&p, tau_m, tau_s);
+    p.theta = theta; p.M = M; p.t0 = t0; p.dt = dt; p.t_max = t_max;
+    int64_t NV = N_in * F_in;
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t b = 0; b < B; ++b) {
+        ev_t *ev = (ev_t *)malloc(sizeof(ev_t) * (size_t)(NV > 0 ? NV : 1));
+        double *wh = (double *)malloc(sizeof(double) * (size_t)(M + 1));
+        double *wabs = (double *)malloc(sizeof(double) * (size_t)(M + 1));
+        sample_events(&p, t_in + b * NV, NV, ev); /* every input spike */
+        for (int64_t i = 0; i < N_out; ++i) {
+            for (int m = 0; m <= M; ++m) { wh[m] = 0.0; wabs[m] = 0.0; }
+            const double *wr = W + i * N_in;
+            for (int64_t v = 0; v < NV; ++v)
+                for (int k = 0; k < ev[v].n; ++k) {
+                    wh[ev[v].m[k]] += wr[v / F_in] * ev[v].s[k];
+                    wabs[ev[v].m[k]] += fabs(wr[v / F_in] * ev[v].s[k]);
+                }
+            int64_t o = (b * N_out + i) * F_out;
+            ms_scan(&p, wh, wabs, (int)F_out, t_out + o, slope + o, q_idx + o, cur + o,
+                    margin ? margin + o : NULL, vabs ? vabs + o : NULL);
+            if (dprev)
+                for (int64_t k = 0; k < F_out; ++k) {
+                    dprev[o + k] = 0.0;
+                    if (k == 0 || q_idx[o + k] < 0) continue;
+                    double d = t_out[o + k] - t_out[o + k - 1];
+                    dprev[o + k] = cur[o + k - 1] * (kern(p.tv, p.ti, d) / p.ti + kern_dt(p.tv, p.ti, d)) /
+                                   slope[o + k];
+                }
+        }
+        free(ev); free(wh); free(wabs);
+    }
+}
+
+/*
+ * Backward by the implicit function theorem on each spike's v_k(t_k) = V_th,
+ * with the intervals fixed: F_k depends on w^ and, through the reset, on
+ * t_{k-1} (dF_k/dt_{k-1} = -I(t_{k-1}) (K(d)/tau_I + K'(d))). Adjoints run
+ * from the last spike back: gbar_k = g_k + gbar_{k+1} (d t_{k+1} / d t_k),
+ * gamma_k = -gbar_k / slope_k, and dL/dw^_m = sum_k gamma_k dF_k/dw^_m with
+ * the coefficients of ms_coef; then dW and dt_in through the events as in the
+ * single-spike backward (every input spike has its own events and slope
+ * derivative). grad_t_in is [B][N_in][F_in]; *_abs (optional) get the sums
+ * of |terms|.
+ */
+void oracle_ms_backward(double tau_m, double tau_s, double theta, int M, double t0, double dt,
+                        double t_max, int64_t B, int64_t N_in, int64_t F_in, int64_t N_out,
+                        int64_t F_out, const double *t_in, const double *W, const double *t_out,
+                        const double *slope, const int32_t *q_idx, const double *cur,
+                        const double *grad_t_out, double *grad_W, double *grad_t_in,
+                        double *grad_W_abs, double *grad_t_in_abs) {
+    prm_t p;
+    canon(&p, tau_m, tau_s);
+    p.theta = theta; p.M = M; p.t0 = t0; p.dt = dt; p.t_max = t_max;
+    int64_t NV = N_in * F_in;
+    ev_t *ev = (ev_t *)malloc(sizeof(ev_t) * (size_t)(B * NV > 0 ? B * NV : 1));
+    double *G = (double *)calloc((size_t)(B * N_out * (M + 1) > 0 ? B * N_out * (M + 1) : 1),
+                                 sizeof(double));
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t b = 0; b < B; ++b) {
+        sample_events(&p, t_in + b * NV, NV, ev + b * NV);
+        double *gb = (double *)malloc(sizeof(double) * (size_t)(F_out > 0 ? F_out : 1));
+        for (int64_t i = 0; i < N_out; ++i) {
+            int64_t o = (b * N_out + i) * F_out;
+            int K = 0;
+            while (K < F_out && q_idx[o + K] >= 0) ++K;
+            for (int k = K - 1; k >= 0; --k) {
+                gb[k] = grad_t_out[o + k];
+                if (k + 1 < K) {
+                    double d = t_out[o + k + 1] - t_out[o + k];
+                    double dFdprev = -cur[o + k] * (kern(p.tv, p.ti, d) / p.ti + kern_dt(p.tv, p.ti, d));
+                    gb[k] += gb[k + 1] * (-dFdprev / slope[o + k + 1]);
+                }
+            }
+            double *Gi = G + (b * N_out + i) * (M + 1);
+            for (int k = 0; k < K; ++k) {
+                double gam = -gb[k] / slope[o + k];
+                double tprev = k > 0 ? t_out[o + k - 1] : -INFINITY;
+                int qprev = k > 0 ? q_idx[o + k - 1] : -1;
+                for (int m = 0; m <= q_idx[o + k]; ++m)
+                    Gi[m] += gam * ms_coef(&p, m, t_out[o + k], q_idx[o + k], tprev, qprev);
+            }
+        }
+        free(gb);
+    }
+    if (grad_t_in) {
+#pragma omp parallel for schedule(dynamic, 1)
+        for (int64_t b = 0; b < B; ++b)
+            for (int64_t v = 0; v < NV; ++v) {
+                const ev_t *e = ev + b * NV + v;
+                double acc = 0.0, aabs = 0.0;
+                for (int k = 0; k < e->n; ++k)
+                    for (int64_t i = 0; i < N_out; ++i) {
+                        double term = G[(b * N_out + i) * (M + 1) + e->m[k]] * W[i * N_in + v / F_in] * e->ds[k];
+                        acc += term;
+                        aabs += fabs(term);
+                    }
+                grad_t_in[b * NV + v] = acc;
+                if (grad_t_in_abs) grad_t_in_abs[b * NV + v] = aabs;
+            }
+    }
+    if (grad_W) {
+#pragma omp parallel for schedule(dynamic, 1)
+        for (int64_t i = 0; i < N_out; ++i)
+            for (int64_t j = 0; j < N_in; ++j) {
+                double acc = 0.0, aabs = 0.0;
+                for (int64_t b = 0; b < B; ++b)
+                    for (int64_t f = 0; f < F_in; ++f) {
+                        const ev_t *e = ev + b * NV + j * F_in + f;
+                        for (int k = 0; k < e->n; ++k) {
+                            double term = G[(b * N_out + i) * (M + 1) + e->m[k]] * e->s[k];
+                            acc += term;
+                            aabs += fabs(term);
+                        }
+                    }
+                grad_W[i * N_in + j] = acc;
+                if (grad_W_abs) grad_W_abs[i * N_in + j] = aabs;
+            }
+    }
+    free(ev);
+    free(G);
 }
 
 int oracle_num_threads(void) {

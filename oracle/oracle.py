@@ -64,6 +64,12 @@ def _load():
     lib.oracle_exact_backward.restype = None
     lib.oracle_exact_backward.argtypes = [_D, _D, _L, _L, _L, _P, _P, _P, _P, _P, _P,
                                           _P, _P, _P, _P]
+    lib.oracle_ms_forward.restype = None
+    lib.oracle_ms_forward.argtypes = [_D, _D, _D, _I, _D, _D, _D, _L, _L, _L, _L, _L, _P, _P, _P,
+                                      _P, _P, _P, _P, _P, _P]
+    lib.oracle_ms_backward.restype = None
+    lib.oracle_ms_backward.argtypes = [_D, _D, _D, _I, _D, _D, _D, _L, _L, _L, _L, _L, _P, _P,
+                                       _P, _P, _P, _P, _P, _P, _P, _P, _P]
     lib.oracle_conv_forward.restype = None
     lib.oracle_conv_forward.argtypes = [_D, _D, _D, _I, _D, _D, _D, _L,
                                         _I, _I, _I, _I, _I, _I, _I, _I, _I,
@@ -235,6 +241,46 @@ def exact_backward(p, t_in, W, fwd, grad_t_out):
     _load().oracle_exact_backward(float(p["tau_m"]), float(p["tau_s"]), B, N_in, N_out,
                                   _ptr(t_in), _ptr(W), _ptr(t_out), _ptr(slope), _ptr(q), _ptr(g),
                                   _ptr(gW), _ptr(gt), _ptr(gWa), _ptr(gta))
+    return dict(grad_W=gW, grad_t_in=gt, grad_W_abs=gWa, grad_t_in_abs=gta)
+
+
+def ms_forward(p, t_in, W, F_out):
+    """Multi-spike DSTD forward (App. "multi-spikes"): t_in [B, N_in, F_in],
+    W [N_out, N_in]. Returns per output spike [B, N_out, F_out]: t_out, slope,
+    q, cur (current at the spike), margin, vabs, dprev (d t_k / d t_{k-1})."""
+    t_in = _f64(t_in)
+    W = _f64(W)
+    B, N_in, F_in = t_in.shape
+    N_out = W.shape[0]
+    shp = (B, N_out, F_out)
+    out = {k: np.empty(shp) for k in ("t_out", "slope", "cur", "margin", "vabs", "dprev")}
+    out["q"] = np.empty(shp, dtype=np.int32)
+    _load().oracle_ms_forward(float(p["tau_m"]), float(p["tau_s"]), float(p["threshold"]),
+                              int(p["M"]), float(p["t0"]), float(p["dt"]),
+                              float(p.get("t_max", np.inf)), B, N_in, F_in, N_out, F_out,
+                              _ptr(t_in), _ptr(W), _ptr(out["t_out"]), _ptr(out["slope"]),
+                              _ptr(out["q"]), _ptr(out["cur"]), _ptr(out["margin"]),
+                              _ptr(out["vabs"]), _ptr(out["dprev"]))
+    return out
+
+
+def ms_backward(p, t_in, W, fwd, grad_t_out):
+    """Multi-spike DSTD backward. grad_t_out [B, N_out, F_out]; returns grad_W,
+    grad_t_in [B, N_in, F_in] and their |term| sums."""
+    t_in = _f64(t_in)
+    W = _f64(W)
+    B, N_in, F_in = t_in.shape
+    N_out = W.shape[0]
+    F_out = fwd["t_out"].shape[2]
+    gW, gWa = np.empty((N_out, N_in)), np.empty((N_out, N_in))
+    gt, gta = np.empty(t_in.shape), np.empty(t_in.shape)
+    _load().oracle_ms_backward(float(p["tau_m"]), float(p["tau_s"]), float(p["threshold"]),
+                               int(p["M"]), float(p["t0"]), float(p["dt"]),
+                               float(p.get("t_max", np.inf)), B, N_in, F_in, N_out, F_out,
+                               _ptr(t_in), _ptr(W), _ptr(_f64(fwd["t_out"])), _ptr(_f64(fwd["slope"])),
+                               _ptr(np.ascontiguousarray(fwd["q"], dtype=np.int32)),
+                               _ptr(_f64(fwd["cur"])), _ptr(_f64(grad_t_out)), _ptr(gW), _ptr(gt),
+                               _ptr(gWa), _ptr(gta))
     return dict(grad_W=gW, grad_t_in=gt, grad_W_abs=gWa, grad_t_in_abs=gta)
 
 

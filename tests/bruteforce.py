@@ -70,3 +70,40 @@ def simulate(tau_v, tau_i, times, weights, t_end, theta=None, query=(), rtol=1e-
 def _final(f, a, b, y, rtol, atol):
     sol = solve_ivp(f, (a, b), y, method="DOP853", rtol=rtol, atol=atol)
     return sol.y[:, -1]
+
+
+def simulate_reset(tau_v, tau_i, times, weights, t_end, theta, n_spikes, rtol=1e-12, atol=1e-14):
+    """The same ODE with the multi-spike reset: when v reaches theta the time
+    is recorded and v is set to 0 while I carries on. Returns the first
+    n_spikes spike times (fewer if the neuron stops firing before t_end)."""
+    times = np.asarray(times, dtype=float)
+    weights = np.asarray(weights, dtype=float)
+    keep = np.isfinite(times)
+    times, weights = times[keep], weights[keep]
+    f = _rhs(tau_v, tau_i)
+    uniq = np.unique(times)
+    spikes = []
+    y = np.array([0.0, 0.0])
+
+    def ev(tt, yy):
+        return yy[0] - theta
+    ev.direction = 1
+    ev.terminal = True
+    for k, tk in enumerate(uniq):
+        y = y.copy()
+        y[1] += weights[times == tk].sum()
+        t_next = uniq[k + 1] if k + 1 < len(uniq) else t_end
+        t = tk
+        while t < t_next and len(spikes) < n_spikes:
+            sol = solve_ivp(f, (t, t_next), y, method="DOP853", rtol=rtol, atol=atol, events=ev)
+            if sol.status == 1 and len(sol.t_events[0]):
+                ts = float(sol.t_events[0][0])
+                spikes.append(ts)
+                y = np.array([0.0, sol.y_events[0][0][1]])
+                t = ts
+            else:
+                y = sol.y[:, -1]
+                t = t_next
+        if len(spikes) >= n_spikes:
+            break
+    return spikes

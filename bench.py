@@ -493,6 +493,92 @@ def exact_sweep(torch, dstd, workloads, dev, n_ins, models, Ms, reps=20, warmup=
     return rows
 
 
+def multispike_bench(torch, dstd, dev, reps=20, warmup=3):
+    """One multi-spike dense layer (App. "multi-spikes") fwd + bwd at the mlp3
+    first layer's size (B 128, 784 inputs, 1000 neurons, M 32 on [0, 1],
+    tau (1.0, 0.5)) for several input / output spike counts, against the TTFS
+    layer on the same first input spikes. Inputs U[0, 1) per spike; weights
+    (k / (N_in F_in)) (1 + 0.3 sqrt(N_in F_in) z) with k = 24 (most neurons
+    fire F_out times). Eager launches; ms per pass and per kernel."""
+    st = torch.cuda.current_stream(dev).cuda_stream
+    B, N_in, N_out, M = 128, 784, 1000, 32
+    p = dstd.make_params(1.0, 0.5, 1.0, M, 0.0, 1.0 / M)
+    rows = []
+
+    def ck(name, s):
+        if s != 0:
+            raise RuntimeError(f"{name}: {dstd.dstd_last_error().decode()}")
+
+    def timed(fn):
+        for _ in range(warmup):
+            fn()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(reps):
+            fn()
+        torch.cuda.synchronize()
+        ms = 1e3 * (time.perf_counter() - t0) / reps
+        dstd.dstd_profile_reset()
+        dstd.dstd_profile_enable(True)
+        for _ in range(5):
+            fn()
+        torch.cuda.synchronize()
+        dstd.dstd_profile_enable(False)
+        return ms, {k: round(v[1] / 5, 4) for k, v in sorted(dstd.profile_table().items())}
+
+    for F_in, F_out in [(1, 1), (2, 4), (4, 8)]:
+        rng = np.random.Generator(np.random.PCG64(12))
+        t = rng.random((B, N_in, F_in)).astype(np.float32)
+        n = N_in * F_in
+        W = ((24.0 / n) * (1 + 0.3 * math.sqrt(n) * rng.standard_normal((N_out, N_in)))).astype(np.float32)
+        tt, Wt = torch.from_numpy(t).to(dev), torch.from_numpy(W).to(dev)
+        shp = (B, N_out, F_out)
+        to = torch.empty(shp, device=dev)
+        sl, cur = torch.empty_like(to), torch.empty_like(to)
+        q = torch.empty(shp, dtype=torch.int32, device=dev)
+        g = torch.from_numpy(rng.standard_normal(shp).astype(np.float32)).to(dev)
+        gW = torch.empty_like(Wt)
+        gx = torch.empty_like(tt)
+        wf = dstd.workspace(dstd.dstd_lif_multispike_forward_workspace_size(p, B, N_in, F_in, N_out, F_out), dev)
+        wb = dstd.workspace(dstd.dstd_lif_multispike_backward_workspace_size(p, B, N_in, F_in, N_out, F_out), dev)
+
+        def run():
+            ck("ms fwd", dstd.dstd_lif_multispike_forward(
+                p, B, N_in, F_in, N_out, F_out, tt.data_ptr(), Wt.data_ptr(), dstd.DSTD_F32,
+                to.data_ptr(), sl.data_ptr(), q.data_ptr(), cur.data_ptr(), wf.data_ptr(),
+                wf.numel(), st))
+            ck("ms bwd", dstd.dstd_lif_multispike_backward(
+                p, B, N_in, F_in, N_out, F_out, tt.data_ptr(), Wt.data_ptr(), dstd.DSTD_F32,
+                to.data_ptr(), sl.data_ptr(), q.data_ptr(), cur.data_ptr(), g.data_ptr(),
+                gW.data_ptr(), gx.data_ptr(), wb.data_ptr(), wb.numel(), st))
+
+        ms, kern = timed(run)
+        spikes = (q >= 0).float().sum(dim=2)
+        row = dict(F_in=F_in, F_out=F_out, multispike_ms=round(ms, 4), kernel_ms=kern,
+                   mean_spikes_per_neuron=round(float(spikes.mean()), 3))
+        # the TTFS layer on the first input spikes
+        t1 = tt[:, :, 0].contiguous()
+        o1, s1 = torch.empty((B, N_out), device=dev), torch.empty((B, N_out), device=dev)
+        q1 = torch.empty((B, N_out), dtype=torch.int32, device=dev)
+        g1, gx1 = g[:, :, 0].contiguous(), torch.empty_like(t1)
+        vf = dstd.workspace(dstd.dstd_lif_forward_workspace_size(p, B, N_in, N_out), dev)
+        vb = dstd.workspace(dstd.dstd_lif_backward_workspace_size(p, B, N_in, N_out), dev)
+
+        def run1():
+            ck("fwd", dstd.dstd_lif_forward(p, B, N_in, N_out, t1.data_ptr(), Wt.data_ptr(),
+                                            dstd.DSTD_F32, o1.data_ptr(), s1.data_ptr(),
+                                            q1.data_ptr(), vf.data_ptr(), vf.numel(), st))
+            ck("bwd", dstd.dstd_lif_backward(p, B, N_in, N_out, t1.data_ptr(), Wt.data_ptr(),
+                                             dstd.DSTD_F32, o1.data_ptr(), s1.data_ptr(),
+                                             q1.data_ptr(), g1.data_ptr(), gW.data_ptr(),
+                                             gx1.data_ptr(), vb.data_ptr(), vb.numel(), st))
+
+        row["ttfs_ms"] = round(timed(run1)[0], 4)
+        rows.append(row)
+        print(json.dumps(row), file=sys.stderr, flush=True)
+    return rows
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -511,6 +597,8 @@ def main():
     ap.add_argument("--exact-sweep", action="store_true",
                     help="instead of the training step: time the exact sorted-input method "
                          "against DSTD on the paper's single-layer timing workload")
+    ap.add_argument("--multispike", action="store_true",
+                    help="instead of the training step: time the multi-spike dense layer")
     ap.add_argument("--exact-n-in", default="1000,2000,4000,6000")
     ap.add_argument("--exact-models", default="0.4-0.2,inf-0.2,inf-inf")
     ap.add_argument("--exact-M", default="10,20")
@@ -533,6 +621,10 @@ def main():
                           "config": {"batch": 100, "n_out": 1000, "inputs": "U[0,1) per input",
                                      "grid": "[0,1] with M intervals"},
                           "rows": rows}), flush=True)
+        return
+    if args.multispike:
+        print(json.dumps({"report": "multi-spike dense layer fwd+bwd (B 128, 784 -> 1000, M 32)",
+                          "rows": multispike_bench(torch, dstd, dev)}), flush=True)
         return
     wl = workloads.get(args.workload)
     net = Net(wl, dev)

@@ -302,6 +302,58 @@ dstd_status dstd_profile_entry(int32_t idx, const char **name, int64_t *launches
                                double *total_ms);
 void dstd_profile_reset(void);
 
+/* ----------------------------------------------------------- multispike -- */
+
+/*
+ * Multi-spike DSTD for a dense layer (App. "multi-spikes", Eq.
+ * (Vmem_multiSpikes) and its DSTD form). Every input neuron may fire up to
+ * F_in times; each input spike gets its own events (Eq. (DSTD_kernel)) and
+ * the weighted events sum them. An output neuron fires whenever v reaches
+ * V_th; v is then reset to 0 and the synaptic current is not, so after a
+ * spike at t_k the potential is I(t_k) K(t - t_k) plus the events after t_k.
+ * The first F_out spikes are computed, in time order (several may fall in
+ * one interval).
+ *  t_in  [B][N_in][F_in]   input spike times (non-finite = no spike; any order)
+ *  W     [N_out][N_in]     fp32 or bf16
+ *  t_out, slope, q_idx, cur [B][N_out][F_out]  out: spike times (+inf after
+ *          the last), dv/dt at each spike, its interval (-1 after the last)
+ *          and the synaptic current at the spike (kept for the backward)
+ * 1 <= F_in, F_out <= 64; M <= 250 (DSTD_ERR_UNSUPPORTED beyond); the grid,
+ * t_max and other limits as in dstd_lif_forward.
+ */
+size_t dstd_lif_multispike_forward_workspace_size(const dstd_lif_params *p, int64_t B,
+                                                  int64_t N_in, int64_t F_in, int64_t N_out,
+                                                  int64_t F_out);
+size_t dstd_lif_multispike_backward_workspace_size(const dstd_lif_params *p, int64_t B,
+                                                   int64_t N_in, int64_t F_in, int64_t N_out,
+                                                   int64_t F_out);
+dstd_status dstd_lif_multispike_forward(const dstd_lif_params *p, int64_t B, int64_t N_in,
+                                        int64_t F_in, int64_t N_out, int64_t F_out,
+                                        const float *t_in, const void *W, dstd_dtype w_dtype,
+                                        float *t_out, float *slope, int32_t *q_idx, float *cur,
+                                        void *ws, size_t ws_bytes, void *stream);
+
+/*
+ * Backward: with the intervals fixed, each spike solves v_k(t_k) = V_th, and
+ * v_k depends on the weighted events and, through the reset, on t_{k-1}
+ * (d t_k / d t_{k-1} = I(t_{k-1}) (K(d)/tau_I + K'(d)) / slope_k,
+ * d = t_k - t_{k-1}). Adjoints run from the last spike back, then dL/dW and
+ * dL/dt_in follow through the events as in dstd_lif_backward.
+ *  t_out, slope, q_idx, cur  the forward's outputs for the same inputs
+ *  grad_t_out [B][N_out][F_out]  dL/dt_out; ignored where q_idx < 0
+ *  grad_W [N_out][N_in]          out (fp32, overwritten), or NULL
+ *  grad_t_in [B][N_in][F_in]     out (overwritten), or NULL; input spikes
+ *                                without events get 0
+ */
+dstd_status dstd_lif_multispike_backward(const dstd_lif_params *p, int64_t B, int64_t N_in,
+                                         int64_t F_in, int64_t N_out, int64_t F_out,
+                                         const float *t_in, const void *W, dstd_dtype w_dtype,
+                                         const float *t_out, const float *slope,
+                                         const int32_t *q_idx, const float *cur,
+                                         const float *grad_t_out, float *grad_W,
+                                         float *grad_t_in, void *ws, size_t ws_bytes,
+                                         void *stream);
+
 /* ----------------------------------------------------------------- skip -- */
 
 /*

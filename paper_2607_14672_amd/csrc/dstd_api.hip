@@ -781,3 +781,118 @@ dstd_status dstd_skip_delay_concat_backward(int64_t B, int64_t C1, int64_t C2, i
 }
 
 }  // extern "C"
+
+// ------------------------------------------------------------- multispike --
+namespace {
+
+dstd_status check_ms(const dstd_lif_params *p, int64_t B, int64_t N_in, int64_t F_in,
+                     int64_t N_out, int64_t F_out) {
+    dstd_status s = check_params(p);
+    if (s != DSTD_OK) return s;
+    if (p->M > dstd::kMsMaxM)
+        return fail(DSTD_ERR_UNSUPPORTED, "multi-spike layers support M <= %d (got %d)",
+                    dstd::kMsMaxM, p->M);
+    if (F_in < 1 || F_out < 1 || F_in > dstd::kMsMaxF || F_out > dstd::kMsMaxF)
+        return fail(DSTD_ERR_SHAPE, "F_in and F_out must be in [1, %d]", dstd::kMsMaxF);
+    if ((s = check_dims(B, N_in * F_in, N_out)) != DSTD_OK) return s;
+    if (N_out * F_out >= ((int64_t)1 << 24) || N_out >= ((int64_t)1 << 22) ||
+        B * N_out * (p->M + 1) >= ((int64_t)1 << 31))
+        return fail(DSTD_ERR_SHAPE, "N_out (< 2^22), N_out * F_out (< 2^24) or B * N_out * (M + 1) "
+                    "(< 2^31) too large");
+    return DSTD_OK;
+}
+
+struct MsWs { size_t row, L, R, dL, dR, wt, G, total; };
+
+MsWs ms_ws_layout(int M, int64_t B, int64_t N_in, int64_t F_in, int64_t N_out, bool backward) {
+    MsWs w{};
+    size_t off = 0;
+    const size_t n = (size_t)(B * N_in * F_in);
+    w.row = off; off += align_up(n * sizeof(int));
+    w.L = off; off += align_up(n * sizeof(float));
+    w.R = off; off += align_up(n * sizeof(float));
+    w.dL = off; off += align_up(n * sizeof(float));
+    w.dR = off; off += align_up(n * sizeof(float));
+    w.wt = off; off += align_up((size_t)N_in * (size_t)N_out * sizeof(float));
+    if (backward) { w.G = off; off += align_up((size_t)B * (size_t)(M + 1) * (size_t)N_out * sizeof(float)); }
+    w.total = off;
+    return w;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t dstd_lif_multispike_forward_workspace_size(const dstd_lif_params *p, int64_t B,
+                                                  int64_t N_in, int64_t F_in, int64_t N_out,
+                                                  int64_t F_out) {
+    if (check_ms(p, B, N_in, F_in, N_out, F_out) != DSTD_OK) return 0;
+    if (B * N_out == 0) return 0;
+    return ms_ws_layout(p->M, B, N_in, F_in, N_out, false).total;
+}
+
+size_t dstd_lif_multispike_backward_workspace_size(const dstd_lif_params *p, int64_t B,
+                                                   int64_t N_in, int64_t F_in, int64_t N_out,
+                                                   int64_t F_out) {
+    if (check_ms(p, B, N_in, F_in, N_out, F_out) != DSTD_OK) return 0;
+    return ms_ws_layout(p->M, B, N_in, F_in, N_out, true).total;
+}
+
+dstd_status dstd_lif_multispike_forward(const dstd_lif_params *p, int64_t B, int64_t N_in,
+                                        int64_t F_in, int64_t N_out, int64_t F_out,
+                                        const float *t_in, const void *W, dstd_dtype w_dtype,
+                                        float *t_out, float *slope, int32_t *q_idx, float *cur,
+                                        void *ws, size_t ws_bytes, void *stream) {
+    dstd_status s = check_ms(p, B, N_in, F_in, N_out, F_out);
+    if (s != DSTD_OK) return s;
+    if (w_dtype != DSTD_F32 && w_dtype != DSTD_BF16)
+        return fail(DSTD_ERR_PARAM, "unknown weight dtype %d", (int)w_dtype);
+    if (B * N_out == 0) return DSTD_OK;
+    if (!t_out || !slope || !q_idx || !cur)
+        return fail(DSTD_ERR_NULL, "t_out, slope, q_idx and cur are required");
+    if (N_in > 0 && !t_in) return fail(DSTD_ERR_NULL, "t_in is NULL");
+    if (N_in > 0 && !W) return fail(DSTD_ERR_NULL, "W is NULL");
+    MsWs L = ms_ws_layout(p->M, B, N_in, F_in, N_out, false);
+    if ((s = check_ws(ws, ws_bytes, L.total)) != DSTD_OK) return s;
+    LifConst C = make_const(p);
+    dstd::MsEvents ev{at<int>(ws, L.row), at<float>(ws, L.L), at<float>(ws, L.R),
+                      at<float>(ws, L.dL), at<float>(ws, L.dR)};
+    hipError_t e = dstd::launch_ms_forward(C, B, N_in, F_in, N_out, F_out, W,
+                                           w_dtype == DSTD_BF16, at<void>(ws, L.wt), ev, t_in,
+                                           t_out, slope, q_idx, cur,
+                                           static_cast<hipStream_t>(stream));
+    return hip_status(e, "multi-spike forward launch");
+}
+
+dstd_status dstd_lif_multispike_backward(const dstd_lif_params *p, int64_t B, int64_t N_in,
+                                         int64_t F_in, int64_t N_out, int64_t F_out,
+                                         const float *t_in, const void *W, dstd_dtype w_dtype,
+                                         const float *t_out, const float *slope,
+                                         const int32_t *q_idx, const float *cur,
+                                         const float *grad_t_out, float *grad_W,
+                                         float *grad_t_in, void *ws, size_t ws_bytes,
+                                         void *stream) {
+    dstd_status s = check_ms(p, B, N_in, F_in, N_out, F_out);
+    if (s != DSTD_OK) return s;
+    if (w_dtype != DSTD_F32 && w_dtype != DSTD_BF16)
+        return fail(DSTD_ERR_PARAM, "unknown weight dtype %d", (int)w_dtype);
+    if (B * N_out > 0 && (!t_out || !slope || !q_idx || !cur || !grad_t_out))
+        return fail(DSTD_ERR_NULL, "t_out, slope, q_idx, cur and grad_t_out are required");
+    if (B * N_in > 0 && !t_in) return fail(DSTD_ERR_NULL, "t_in is NULL");
+    if (grad_t_in && N_in * N_out > 0 && !W) return fail(DSTD_ERR_NULL, "W is NULL");
+    MsWs L = ms_ws_layout(p->M, B, N_in, F_in, N_out, true);
+    if ((s = check_ws(ws, ws_bytes, L.total)) != DSTD_OK) return s;
+    LifConst C = make_const(p);
+    dstd::MsEvents ev{at<int>(ws, L.row), at<float>(ws, L.L), at<float>(ws, L.R),
+                      at<float>(ws, L.dL), at<float>(ws, L.dR)};
+    // B == 0: the dW kernel still runs and writes zeros; N_out == 0: dt_in
+    // sums nothing and writes zeros
+    hipError_t e = dstd::launch_ms_backward(C, B, N_in, F_in, N_out, F_out, W,
+                                            w_dtype == DSTD_BF16, at<void>(ws, L.wt), ev, t_in,
+                                            t_out, slope, q_idx, cur, grad_t_out,
+                                            at<float>(ws, L.G), grad_W, grad_t_in,
+                                            static_cast<hipStream_t>(stream));
+    return hip_status(e, "multi-spike backward launch");
+}
+
+}  // extern "C"

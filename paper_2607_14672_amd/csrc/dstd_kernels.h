@@ -112,6 +112,33 @@ hipError_t launch_skip_concat(int64_t B, int64_t n1, int64_t n2, const float *t1
 hipError_t launch_skip_split(int64_t B, int64_t n1, int64_t n2, const float *g, float *g1, int acc,
                              float *g2, hipStream_t st);
 
+// ------------------------------------------------------------ multispike --
+// Events of every input spike ([B][N_in][F_in]: row = q + 1 or -1, L, R and
+// their time derivatives) and the backward's per-neuron inputs: the forward's
+// spikes [B][N_out][F] and the upstream gradient, G [B][M + 1][N_out] out.
+struct MsEvents { int *row; float *L, *R, *dL, *dR; };
+struct MsGrad {
+    const float *t, *slope;
+    const int *q;
+    const float *cur, *g;
+    float *G;
+    int64_t n;  // neurons B * N_out (0: no G role)
+    int F;
+};
+constexpr int kMsMaxM = 250;  // (M + 3) rows x 64 lanes of fp32 in 64 KB of LDS
+constexpr int kMsMaxF = 64;
+
+hipError_t launch_ms_forward(const LifConst &C, int64_t B, int64_t N_in, int64_t F_in,
+                             int64_t N_out, int64_t F_out, const void *W, bool bf16, void *Wt,
+                             MsEvents ev, const float *t_in, float *t_out, float *slope,
+                             int *q_idx, float *cur, hipStream_t st);
+hipError_t launch_ms_backward(const LifConst &C, int64_t B, int64_t N_in, int64_t F_in,
+                              int64_t N_out, int64_t F_out, const void *W, bool bf16, void *Wt,
+                              MsEvents ev, const float *t_in, const float *t_out,
+                              const float *slope, const int *q_idx, const float *cur,
+                              const float *grad_t, float *G, float *grad_W, float *grad_t_in,
+                              hipStream_t st);
+
 // ----------------------------------------------------------------- exact --
 // Exact spike times by sorting (App. A, Alg. 1). Per sample, the finite
 // inputs before t_max in ascending time order as records (SoA, each array

@@ -81,6 +81,12 @@ _SIGS = {
     "dstd_exact_backward_workspace_size": (_S, [_P, _L, _L, _L]),
     "dstd_exact_forward": (_I, [_P, _L, _L, _L, _P, _P, _I, _P, _P, _P, _P, _S, _P]),
     "dstd_exact_backward": (_I, [_P, _L, _L, _L, _P, _P, _I, _P, _P, _P, _P, _P, _P, _P, _S, _P]),
+    "dstd_lif_multispike_forward_workspace_size": (_S, [_P, _L, _L, _L, _L, _L]),
+    "dstd_lif_multispike_backward_workspace_size": (_S, [_P, _L, _L, _L, _L, _L]),
+    "dstd_lif_multispike_forward": (_I, [_P, _L, _L, _L, _L, _L, _P, _P, _I, _P, _P, _P, _P, _P,
+                                         _S, _P]),
+    "dstd_lif_multispike_backward": (_I, [_P, _L, _L, _L, _L, _L, _P, _P, _I, _P, _P, _P, _P, _P,
+                                          _P, _P, _P, _S, _P]),
     "dstd_skip_delay_concat": (_I, [_L, _L, _L, _L, _P, _F, _P, _P, _P]),
     "dstd_skip_delay_concat_backward": (_I, [_L, _L, _L, _L, _P, _P, C.c_int32, _P, _P]),
     "dstd_softmax_ce_grad": (_I, [_L, _L, _P, _P, _F, _F, _P, _P, _P]),
@@ -157,6 +163,28 @@ def dstd_exact_backward(p, B, N_in, N_out, t_in, W, w_dtype, t_out, slope, k_idx
                         grad_W, grad_t_in, ws, ws_bytes, stream):
     return _load().dstd_exact_backward(_ref(p), B, N_in, N_out, t_in, W, w_dtype, t_out, slope,
                                        k_idx, grad_t_out, grad_W, grad_t_in, ws, ws_bytes, stream)
+
+
+def dstd_lif_multispike_forward_workspace_size(p, B, N_in, F_in, N_out, F_out):
+    return _load().dstd_lif_multispike_forward_workspace_size(_ref(p), B, N_in, F_in, N_out, F_out)
+
+
+def dstd_lif_multispike_backward_workspace_size(p, B, N_in, F_in, N_out, F_out):
+    return _load().dstd_lif_multispike_backward_workspace_size(_ref(p), B, N_in, F_in, N_out, F_out)
+
+
+def dstd_lif_multispike_forward(p, B, N_in, F_in, N_out, F_out, t_in, W, w_dtype, t_out, slope,
+                                q_idx, cur, ws, ws_bytes, stream):
+    return _load().dstd_lif_multispike_forward(_ref(p), B, N_in, F_in, N_out, F_out, t_in, W,
+                                               w_dtype, t_out, slope, q_idx, cur, ws, ws_bytes,
+                                               stream)
+
+
+def dstd_lif_multispike_backward(p, B, N_in, F_in, N_out, F_out, t_in, W, w_dtype, t_out, slope,
+                                 q_idx, cur, grad_t_out, grad_W, grad_t_in, ws, ws_bytes, stream):
+    return _load().dstd_lif_multispike_backward(_ref(p), B, N_in, F_in, N_out, F_out, t_in, W,
+                                                w_dtype, t_out, slope, q_idx, cur, grad_t_out,
+                                                grad_W, grad_t_in, ws, ws_bytes, stream)
 
 
 def dstd_skip_delay_concat(B, C1, C2, HW, t1, delay, t2, out, stream):
@@ -370,6 +398,55 @@ def backward(p: dstd_lif_params, t_in, W, t_out, slope, q, grad_t_out, need_W=Tr
         _check("dstd_lif_backward", dstd_lif_backward(p, *args))
     else:
         _check("dstd_lif_backward_synfire", dstd_lif_backward_synfire(p, synfire, *args))
+    return gW, gt
+
+
+def multispike_forward(p: dstd_lif_params, t_in, W, F_out: int, ws=None):
+    """Multi-spike dense forward. t_in [B, N_in, F_in]; returns (t_out, slope, q, cur),
+    each [B, N_out, F_out]."""
+    torch = _torch()
+    t_in = _cont(t_in, torch.float32)
+    W = _cont(W)
+    B, N_in, F_in = t_in.shape
+    N_out = W.shape[0]
+    dev = t_in.device
+    shp = (B, N_out, F_out)
+    t_out = torch.empty(shp, dtype=torch.float32, device=dev)
+    slope = torch.empty_like(t_out)
+    cur = torch.empty_like(t_out)
+    q = torch.empty(shp, dtype=torch.int32, device=dev)
+    need = dstd_lif_multispike_forward_workspace_size(p, B, N_in, F_in, N_out, F_out)
+    if ws is None or ws.numel() < need:
+        ws = workspace(need, dev)
+    _check("dstd_lif_multispike_forward",
+           dstd_lif_multispike_forward(p, B, N_in, F_in, N_out, F_out, _ptr(t_in), _ptr(W),
+                                       _wdtype(W), _ptr(t_out), _ptr(slope), _ptr(q), _ptr(cur),
+                                       _ptr(ws), ws.numel(), _stream(dev)))
+    return t_out, slope, q, cur
+
+
+def multispike_backward(p: dstd_lif_params, t_in, W, t_out, slope, q, cur, grad_t_out,
+                        need_W=True, need_t_in=True, ws=None):
+    """Multi-spike dense backward; returns (grad_W or None, grad_t_in [B, N_in, F_in] or None)."""
+    torch = _torch()
+    t_in = _cont(t_in, torch.float32)
+    W = _cont(W)
+    B, N_in, F_in = t_in.shape
+    N_out = W.shape[0]
+    F_out = t_out.shape[2]
+    dev = t_in.device
+    gW = torch.empty((N_out, N_in), dtype=torch.float32, device=dev) if need_W else None
+    gt = torch.empty((B, N_in, F_in), dtype=torch.float32, device=dev) if need_t_in else None
+    need = dstd_lif_multispike_backward_workspace_size(p, B, N_in, F_in, N_out, F_out)
+    if ws is None or ws.numel() < need:
+        ws = workspace(need, dev)
+    _check("dstd_lif_multispike_backward",
+           dstd_lif_multispike_backward(p, B, N_in, F_in, N_out, F_out, _ptr(t_in), _ptr(W),
+                                        _wdtype(W), _ptr(_cont(t_out, torch.float32)),
+                                        _ptr(_cont(slope, torch.float32)),
+                                        _ptr(_cont(q, torch.int32)), _ptr(_cont(cur, torch.float32)),
+                                        _ptr(_cont(grad_t_out, torch.float32)), _ptr(gW), _ptr(gt),
+                                        _ptr(ws), ws.numel(), _stream(dev)))
     return gW, gt
 
 

@@ -276,3 +276,28 @@ def test_skip_delay_validation():
     assert dstd.dstd_skip_delay_concat_backward(2, 2, 2, 4, None, 1, 0, 1, None) == dstd.DSTD_ERR_NULL
     assert dstd.dstd_skip_delay_concat_backward(2, 2, 2, 4, 1, 1, 2, 1, None) == dstd.DSTD_ERR_PARAM
     assert dstd.dstd_skip_delay_concat_backward(2, -2, 2, 4, 1, 1, 0, 1, None) == dstd.DSTD_ERR_SHAPE
+
+
+# ------------------------------------------------------------- multispike --
+def test_multispike_validation():
+    p = _p()
+    assert dstd.dstd_lif_multispike_forward_workspace_size(p, 4, 10, 2, 5, 3) > 0
+    assert dstd.dstd_lif_multispike_backward_workspace_size(p, 4, 10, 2, 5, 3) > 0
+    for F_in, F_out in [(0, 3), (2, 0), (65, 3), (2, 65)]:
+        assert dstd.dstd_lif_multispike_forward_workspace_size(p, 4, 10, F_in, 5, F_out) == 0
+        st = dstd.dstd_lif_multispike_forward(p, 4, 10, F_in, 5, F_out, 1, 1, 0, 1, 1, 1, 1, 256,
+                                              1 << 20, None)
+        assert st == dstd.DSTD_ERR_SHAPE
+    q = _p(M=251, dt=1 / 251)
+    assert dstd.dstd_lif_multispike_forward(q, 4, 10, 2, 5, 3, 1, 1, 0, 1, 1, 1, 1, 256, 1 << 20,
+                                            None) == dstd.DSTD_ERR_UNSUPPORTED
+    need = dstd.dstd_lif_multispike_forward_workspace_size(p, 4, 10, 2, 5, 3)
+    assert dstd.dstd_lif_multispike_forward(p, 4, 10, 2, 5, 3, 1, 1, 0, 1, 1, 1, None, 256, need,
+                                            None) == dstd.DSTD_ERR_NULL
+    assert dstd.dstd_lif_multispike_forward(p, 4, 10, 2, 5, 3, 1, 1, 0, 1, 1, 1, 1, 256, need - 1,
+                                            None) == dstd.DSTD_ERR_WORKSPACE
+    nb = dstd.dstd_lif_multispike_backward_workspace_size(p, 4, 10, 2, 5, 3)
+    assert dstd.dstd_lif_multispike_backward(p, 4, 10, 2, 5, 3, 1, 1, 0, 1, 1, 1, None, 1, 1, 1,
+                                             256, nb, None) == dstd.DSTD_ERR_NULL
+    assert dstd.dstd_lif_multispike_forward(p, 0, 10, 2, 5, 3, None, None, 0, None, None, None,
+                                            None, None, 0, None) == dstd.DSTD_OK

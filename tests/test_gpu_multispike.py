@@ -1,0 +1,122 @@
+"""GPU parity of the multi-spike dense layer (App. "multi-spikes") against the
+fp64 oracle, through the C ABI. Spikes are compared one by one: the k-th
+spike of a neuron is ambiguous if it or any earlier spike of that neuron is
+(its margin or an earlier one below 1e-5), and its fp32 time error is
+bounded by its own rounding plus the earlier spike's error carried through
+the reset (d t_k / d t_{k-1})."""
+import math
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2607_14672_amd import workloads as wl
+from tests.parity import check_forward, check_grad, near_grid
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def dev():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    from paper_2607_14672_amd import dstd
+    dstd._load()  # fail loudly if the HIP library is missing
+    return torch.device("cuda:0")
+
+
+def _case(seed, B, N_in, F_in, N_out, M, tm, ts, k=3.0, t_max=math.inf):
+    """F_in spikes per input on [0, 1); weights (k / N_in) (1 + 0.3 sqrt(N_in) z)
+    scaled so most neurons fire several times."""
+    rng = np.random.default_rng(seed)
+    p = dict(tau_m=tm, tau_s=ts, threshold=1.0, M=M, t0=0.0, dt=1.0 / M, t_max=t_max)
+    t = rng.random((B, N_in, F_in)).astype(np.float32)
+    n = N_in * F_in
+    W = ((k * 8.0 / n) * (1 + 0.3 * math.sqrt(n) * rng.standard_normal((N_out, N_in)))).astype(np.float32)
+    return p, t, W
+
+
+def _flat_oracle(orc):
+    """Per-spike view for tests.parity: cumulative ambiguity along k and the
+    propagated fp32 error estimate folded into vabs."""
+    m = np.minimum.accumulate(orc["margin"], axis=2)
+    with np.errstate(divide="ignore", invalid="ignore"):
+        own = np.where(orc["q"] >= 0, 2.0 ** -24 * orc["vabs"] / np.abs(orc["slope"]), 0.0)
+    est = np.zeros_like(own)
+    for k in range(own.shape[2]):
+        est[:, :, k] = own[:, :, k] + (np.abs(orc["dprev"][:, :, k]) * est[:, :, k - 1] if k else 0.0)
+    vabs = np.where(orc["q"] >= 0, est * np.abs(orc["slope"]) * 2.0 ** 24, 0.0)
+    return dict(t_out=orc["t_out"], slope=orc["slope"], q=orc["q"], margin=m, vabs=vabs)
+
+
+def _parity(dev, p, t, W, F_out, label, bf16=False, seed=0):
+    import torch
+    from paper_2607_14672_amd import dstd
+    Wq = wl.bf16_round(W) if bf16 else W
+    prm = dstd.make_params(p["tau_m"], p["tau_s"], p["threshold"], p["M"], p["t0"], p["dt"],
+                           p.get("t_max", math.inf))
+    tt = torch.from_numpy(t).to(dev)
+    Wt = torch.from_numpy(Wq).to(dev)
+    if bf16:
+        Wt = Wt.to(torch.bfloat16)
+    to, sl, q, cur = dstd.multispike_forward(prm, tt, Wt, F_out)
+    torch.cuda.synchronize()
+    gpu = dict(t_out=to.cpu().numpy(), slope=sl.cpu().numpy(), q=q.cpu().numpy())
+    orc = oracle.ms_forward(p, t, Wq, F_out)
+    flat = _flat_oracle(orc)
+    mask, st = check_forward(gpu, flat, None, p["M"] * p["dt"], label=label)
+    # a masked spike masks the later spikes of its neuron too
+    mask = np.maximum.accumulate(mask, axis=2)
+    fired = orc["q"] >= 0
+    np.testing.assert_allclose(cur.cpu().numpy()[fired & ~mask], orc["cur"][fired & ~mask],
+                               rtol=1e-3, atol=1e-5)
+    g = np.random.default_rng(seed + 3).standard_normal(orc["t_out"].shape)
+    g = np.where(mask | ~fired, 0.0, g).astype(np.float32)
+    gW, gx = dstd.multispike_backward(prm, tt, Wt, to, sl, q, cur, torch.from_numpy(g).to(dev))
+    torch.cuda.synchronize()
+    ob = oracle.ms_backward(p, t, Wq, orc, g.astype(np.float64))
+    check_grad(gW.cpu().numpy(), ob["grad_W"], label + " dW", ob["grad_W_abs"])
+    kink = near_grid(t, p)
+    check_grad(gx.cpu().numpy()[~kink], ob["grad_t_in"][~kink], label + " dt_in",
+               ob["grad_t_in_abs"][~kink])
+    return gpu, orc, st
+
+
+ROWS = [(1.0, 0.3), (1.0, 0.5), (0.5, 0.5), (math.inf, 0.3), (math.inf, math.inf)]
+
+
+@pytest.mark.parametrize("tm,ts", ROWS)
+def test_multispike_small(dev, tm, ts):
+    k = {(math.inf, 0.3): 1.2, (math.inf, math.inf): 0.4}.get((tm, ts), 3.0)
+    p, t, W = _case(1, 3, 50, 2, 70, 16, tm, ts, k=k)
+    t[0, 3, 1] = np.inf  # an input that fires once
+    t[1, 4, :] = np.inf  # and one that never fires
+    gpu, orc, st = _parity(dev, p, t, W, 4, f"multispike tau=({tm},{ts})")
+    assert (orc["q"][:, :, 1] >= 0).mean() > 0.2, "case should give second spikes"
+
+
+def test_multispike_multi_block_bf16(dev):
+    p, t, W = _case(2, 4, 300, 3, 130, 32, 2.0, 0.4, k=3.0)
+    _parity(dev, p, t, W, 6, "multispike B=4 300x3->130 bf16", bf16=True)
+
+
+def test_multispike_finite_t_max(dev):
+    p, t, W = _case(3, 3, 80, 2, 90, 20, 1.0, 0.3, k=3.0, t_max=1.3)
+    gpu, orc, _ = _parity(dev, p, t, W, 5, "multispike t_max=1.3")
+    assert np.all(gpu["t_out"][np.isfinite(gpu["t_out"])] < 1.3)
+
+
+def test_multispike_single_spike_equals_ttfs(dev):
+    """F_in = F_out = 1 is the TTFS layer: the same spikes as dstd_lif_forward."""
+    import torch
+    from paper_2607_14672_amd import dstd
+    p, t, W = _case(4, 5, 120, 1, 100, 16, 1.0, 0.3, k=2.0)
+    prm = dstd.make_params(p["tau_m"], p["tau_s"], p["threshold"], p["M"], p["t0"], p["dt"])
+    tt = torch.from_numpy(t).to(dev)
+    Wt = torch.from_numpy(W).to(dev)
+    to, sl, q, cur = dstd.multispike_forward(prm, tt, Wt, 1)
+    t1, s1, q1 = dstd.forward(prm, tt[:, :, 0], Wt)
+    torch.cuda.synchronize()
+    assert torch.equal(q[:, :, 0], q1)
+    f = q1 >= 0
+    assert float((to[:, :, 0][f] - t1[f]).abs().max()) <= 2e-6

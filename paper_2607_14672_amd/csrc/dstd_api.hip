@@ -802,19 +802,31 @@ dstd_status check_ms(const dstd_lif_params *p, int64_t B, int64_t N_in, int64_t 
     return DSTD_OK;
 }
 
-struct MsWs { size_t row, L, R, dL, dR, wt, G, total; };
+struct MsWs { size_t row, L, R, dL, dR, wt, G, sj, sr, sL, sR, nvalid, rs, total; };
 
+// forward: the records of every input spike sorted by event row (as the TTFS
+// forward's lists) and W^T; backward: per-spike events, W^T and G
 MsWs ms_ws_layout(int M, int64_t B, int64_t N_in, int64_t F_in, int64_t N_out, bool backward) {
     MsWs w{};
     size_t off = 0;
     const size_t n = (size_t)(B * N_in * F_in);
-    w.row = off; off += align_up(n * sizeof(int));
-    w.L = off; off += align_up(n * sizeof(float));
-    w.R = off; off += align_up(n * sizeof(float));
-    w.dL = off; off += align_up(n * sizeof(float));
-    w.dR = off; off += align_up(n * sizeof(float));
+    if (backward) {
+        w.row = off; off += align_up(n * sizeof(int));
+        w.L = off; off += align_up(n * sizeof(float));
+        w.R = off; off += align_up(n * sizeof(float));
+        w.dL = off; off += align_up(n * sizeof(float));
+        w.dR = off; off += align_up(n * sizeof(float));
+        w.G = off; off += align_up((size_t)B * (size_t)(M + 1) * (size_t)N_out * sizeof(float));
+    } else {
+        const size_t ns = n + dstd::kSortPad;
+        w.sj = off; off += align_up(ns * sizeof(int));
+        w.sr = off; off += align_up(ns * sizeof(int));
+        w.sL = off; off += align_up(ns * sizeof(float));
+        w.sR = off; off += align_up(ns * sizeof(float));
+        w.nvalid = off; off += align_up((size_t)B * sizeof(int));
+        w.rs = off; off += align_up((size_t)B * (M + 4) * sizeof(int));
+    }
     w.wt = off; off += align_up((size_t)N_in * (size_t)N_out * sizeof(float));
-    if (backward) { w.G = off; off += align_up((size_t)B * (size_t)(M + 1) * (size_t)N_out * sizeof(float)); }
     w.total = off;
     return w;
 }
@@ -855,11 +867,11 @@ dstd_status dstd_lif_multispike_forward(const dstd_lif_params *p, int64_t B, int
     MsWs L = ms_ws_layout(p->M, B, N_in, F_in, N_out, false);
     if ((s = check_ws(ws, ws_bytes, L.total)) != DSTD_OK) return s;
     LifConst C = make_const(p);
-    dstd::MsEvents ev{at<int>(ws, L.row), at<float>(ws, L.L), at<float>(ws, L.R),
-                      at<float>(ws, L.dL), at<float>(ws, L.dR)};
+    dstd::SortedEv srt{at<int>(ws, L.sj), at<int>(ws, L.sr), at<float>(ws, L.sL),
+                       at<float>(ws, L.sR), N_in * F_in, at<int>(ws, L.rs)};
     hipError_t e = dstd::launch_ms_forward(C, B, N_in, F_in, N_out, F_out, W,
-                                           w_dtype == DSTD_BF16, at<void>(ws, L.wt), ev, t_in,
-                                           t_out, slope, q_idx, cur,
+                                           w_dtype == DSTD_BF16, at<void>(ws, L.wt), srt,
+                                           at<int>(ws, L.nvalid), t_in, t_out, slope, q_idx, cur,
                                            static_cast<hipStream_t>(stream));
     return hip_status(e, "multi-spike forward launch");
 }

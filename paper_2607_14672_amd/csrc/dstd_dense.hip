@@ -12,6 +12,7 @@
 #include "dstd_internal.h"
 #include "dstd_kernels.h"
 #include "dstd_lif.h"
+#include "dstd_walk.h"
 #include "dstd_profile.h"
 
 #include <algorithm>
@@ -233,7 +234,6 @@ __device__ __forceinline__ RowRange row_range(const int *rs, int R, int n, int t
 // the previous one) and goes straight into the interval scan: the weighted
 // events never exist in memory. Once every lane has found its crossing
 // interval, later events cannot change the outputs and the wave stops.
-constexpr int kBatch = 8;
 
 template <typename WT, int KS>
 __global__ __launch_bounds__(256) void fwd_sorted_kernel(LifConst C, int B, int N_in, int N_out,
@@ -251,89 +251,8 @@ __global__ __launch_bounds__(256) void fwd_sorted_kernel(LifConst C, int B, int 
     const int b = uniform(blockIdx.y * waves + wave);
     if (b >= B) return;  // wave-uniform; the kernel has no block barrier
     const int n = *as_const(n_valid + b);
-    const int64_t eo = static_cast<int64_t>(b) * srt.stride;
-    const int *ej = srt.j + eo;
-    const int *er = srt.r + eo;
-    const float *eL = srt.L + eo;
-    const float *eR = srt.R + eo;
     Scan<KS> sc;
-    int cur = 0;  // row whose records are being summed
-    float aL = 0.f, aR = 0.f, carry = 0.f;
-    bool done = false;
-    // close rows cur .. target-1: grid point cur-1 gets this row's L sums
-    // plus the previous row's R sums
-    auto close_to = [&](int target) {
-        while (cur < target && !done) {
-            if (cur >= 1) sc.step(C, cur - 1, aL + carry);
-            carry = aR;
-            aL = 0.f;
-            aR = 0.f;
-            ++cur;
-            if (__all(sc.found() || !row_ok)) done = true;
-        }
-    };
-    // Weight loads are raw buffer loads: per-lane column offset (constant)
-    // plus a scalar row offset j*N_out, so they need no address arithmetic
-    // in vector registers.
-    // Record arrays are padded by two batches, so the batched scalar reads
-    // are unconditional; only a partial last batch is masked. Lanes past
-    // N_out read column 0 (their results are never stored).
-    const __amdgpu_buffer_rsrc_t wr =
-        make_rsrc(Wt, static_cast<uint32_t>(static_cast<int64_t>(N_in) * N_out * sizeof(WT)));
-    const int voff = (row_ok ? i : 0) * static_cast<int>(sizeof(WT));
-    const int rstride = N_out * static_cast<int>(sizeof(WT));
-    // Reads past the end of the list see stale workspace: their input index
-    // is clamped into [0, N_in) so every scalar offset stays inside WT.
-    const unsigned jmax = static_cast<unsigned>(max(N_in - 1, 0));
-    auto wrow = [&](int j) { return static_cast<int>(min(static_cast<unsigned>(j), jmax)) * rstride; };
-    float w[kBatch], wn[kBatch];
-#pragma unroll
-    for (int kk = 0; kk < kBatch; ++kk) wn[kk] = BufLoad<WT>::get(wr, voff, wrow(as_const(ej)[kk]));
-    for (int k0 = 0; k0 < n && !done; k0 += kBatch) {
-        int rr[kBatch], jj1[kBatch];
-        float ll[kBatch], rv[kBatch];
-#pragma unroll
-        for (int kk = 0; kk < kBatch; ++kk) {
-            w[kk] = wn[kk];
-            rr[kk] = as_const(er + k0)[kk];
-            ll[kk] = as_const(eL + k0)[kk];
-            rv[kk] = as_const(eR + k0)[kk];
-            jj1[kk] = as_const(ej + k0 + kBatch)[kk];
-        }
-        // the next batch's weights are in flight while this one is consumed
-#pragma unroll
-        for (int kk = 0; kk < kBatch; ++kk) wn[kk] = BufLoad<WT>::get(wr, voff, wrow(jj1[kk]));
-        const int nk = min(kBatch, n - k0);
-        if (nk == kBatch && rr[kBatch - 1] == cur) {
-            // common case: a full batch that continues the current row
-#pragma unroll
-            for (int kk = 0; kk < kBatch; ++kk) {
-                aL = fmaf(w[kk], ll[kk], aL);
-                aR = fmaf(w[kk], rv[kk], aR);
-            }
-            continue;
-        }
-        int kk_start = 0;
-        while (!done) {
-            int stop = kBatch, target = 0;
-#pragma unroll
-            for (int kk = 0; kk < kBatch; ++kk) {
-                if (kk >= kk_start && kk < stop && kk < nk) {
-                    if (rr[kk] == cur) {
-                        aL = fmaf(w[kk], ll[kk], aL);
-                        aR = fmaf(w[kk], rv[kk], aR);
-                    } else {
-                        stop = kk;
-                        target = rr[kk];
-                    }
-                }
-            }
-            if (stop >= kBatch || stop >= nk) break;
-            close_to(target);
-            kk_start = stop;
-        }
-    }
-    close_to(C.M + 2);  // row M+2 has no records
+    walk_sorted_rows<WT, false>(C, N_in, N_out, Wt, srt, b, n, i, row_ok, 1, sc);
     if (!row_ok) return;
     float to, sl;
     int q;
@@ -1103,6 +1022,15 @@ static hipError_t launch_prep(const LifConst &C, int64_t B, int64_t N_in, int64_
     }
 #undef PREP
     return hipGetLastError();
+}
+
+hipError_t launch_sort_records(const LifConst &C, int64_t B, int64_t n_rec, const float *t_in,
+                               SortedEv srt, int *n_valid, const char *name, hipStream_t st) {
+    return launch_prep(C, B, n_rec, 0, t_in, srt, n_valid, false,
+                       SortOut{nullptr, nullptr, nullptr, nullptr}, nullptr, false, nullptr, false,
+                       PrepGrad{nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr,
+                                Synfire{}, 0},
+                       0, name, st);
 }
 
 hipError_t launch_forward(const LifConst &C, int64_t B, int64_t N_in, int64_t N_out, const void *W,

@@ -17,6 +17,11 @@ constexpr int kSortPad = 128;
 
 DwPlan plan_dw(int64_t B, int64_t N_in, int64_t N_out, int M);
 
+// per sample, the records with events (one per entry of t_in [B][n_rec])
+// sorted by event row, as the forward walks them
+hipError_t launch_sort_records(const LifConst &C, int64_t B, int64_t n_rec, const float *t_in,
+                               SortedEv srt, int *n_valid, const char *name, hipStream_t st);
+
 hipError_t launch_forward(const LifConst &C, int64_t B, int64_t N_in, int64_t N_out, const void *W,
                           bool bf16, void *Wt, SortedEv srt, int *n_valid, const float *t_in,
                           float *t_out, float *slope, int *q_idx, hipStream_t st);
@@ -130,8 +135,8 @@ constexpr int kMsMaxF = 64;
 
 hipError_t launch_ms_forward(const LifConst &C, int64_t B, int64_t N_in, int64_t F_in,
                              int64_t N_out, int64_t F_out, const void *W, bool bf16, void *Wt,
-                             MsEvents ev, const float *t_in, float *t_out, float *slope,
-                             int *q_idx, float *cur, hipStream_t st);
+                             SortedEv srt, int *n_valid, const float *t_in, float *t_out,
+                             float *slope, int *q_idx, float *cur, hipStream_t st);
 hipError_t launch_ms_backward(const LifConst &C, int64_t B, int64_t N_in, int64_t F_in,
                               int64_t N_out, int64_t F_out, const void *W, bool bf16, void *Wt,
                               MsEvents ev, const float *t_in, const float *t_out,

@@ -14,14 +14,15 @@
 //    once per call, and the transposed weights; the backward role also
 //    builds G[b][m][i] = dL/dw^_im from the neuron's spikes (adjoints through
 //    the reset chain, implicit function theorem per spike).
-//  ms_fwd_kernel: one lane per neuron; the weighted events of its sample are
-//    summed into a per-lane LDS column (row j of W^T is one coalesced load
-//    per input spike), then the grid is scanned with resets.
+//  ms_fwd_kernel: the TTFS forward's walk over the sample's input spikes
+//    sorted by event row (the records are input spikes), closing grid points
+//    into a scan with reset that solves each crossing at once.
 //  ms_dw_kernel / ms_dtin_kernel: the event contractions with G read from
 //    memory (lanes over neurons, so G rows are coalesced).
 #include "dstd_internal.h"
 #include "dstd_kernels.h"
 #include "dstd_profile.h"
+#include "dstd_walk.h"
 
 namespace dstd {
 
@@ -122,56 +123,37 @@ __global__ __launch_bounds__(kMsPrepThreads) void ms_prep_kernel(
     }
 }
 
-// One lane per neuron (blockIdx.x: 64 neurons, blockIdx.y: sample): the
-// weighted events of all the sample's input spikes go into the lane's LDS
-// column w^[row] (rows 0 and M+2 take the halves that fall off the grid),
-// then the intervals are scanned in order. In an interval the current
-// segment starts at offset u0 (0, or the last spike in it) with state (V, I);
-// each crossing is solved at once, recorded, and the segment restarts there
-// with V = 0 and the current at the spike. Without a spike in the interval
-// the state is carried by the fp64 recurrence; after one, from the segment
-// that ends it.
-template <typename WT, int KS>
-__global__ __launch_bounds__(kWave) void ms_fwd_kernel(LifConst C, int NV, int F_in, int N_out,
-                                                      int F_out, const WT *__restrict__ Wt,
-                                                      MsEvents ev, float *__restrict__ t_out,
-                                                      float *__restrict__ slope,
-                                                      int *__restrict__ q_idx,
-                                                      float *__restrict__ cur) {
-    extern __shared__ float acc[];  // [(M + 3) rows][kWave]
-    const int lane = threadIdx.x;
-    const int b = blockIdx.y;
-    const int i = blockIdx.x * kWave + lane;
-    const bool act = i < N_out;
-    const int R = C.M + 3;
-    for (int r = 0; r < R; ++r) acc[r * kWave + lane] = 0.f;
-    const int64_t eo = static_cast<int64_t>(b) * NV;
-    const int *erow = ev.row + eo;
-    const float *eL = ev.L + eo, *eR = ev.R + eo;
-    const int ic = act ? i : 0;
-    for (int v = 0; v < NV; ++v) {
-        const int row = *as_const(erow + v);
-        if (row < 0) continue;  // uniform: the input spike has no events
-        const float w = WLoad<WT>::get(Wt, static_cast<int64_t>(v / F_in) * N_out + ic);
-        acc[row * kWave + lane] = fmaf(w, *as_const(eL + v), acc[row * kWave + lane]);
-        acc[(row + 1) * kWave + lane] = fmaf(w, *as_const(eR + v), acc[(row + 1) * kWave + lane]);
-    }
-    if (!act) return;
-    const int64_t so = (static_cast<int64_t>(b) * N_out + i) * F_out;
-    int nk = 0;
+// Interval scan with reset for one neuron; the grid points arrive in order
+// through step() (the sorted-row walk of the TTFS forward). In an interval
+// the current segment starts at offset u0 (0, or the last spike in it) with
+// state (V, I); each crossing is solved at once (seg_test, seg_solve),
+// recorded, and the segment restarts there with V = 0 and the current at the
+// spike. Without a spike in the interval the state is carried by the fp64
+// recurrence; after one, from the segment that ends it.
+template <int KS>
+struct MsScan {
     double Vd = 0.0, Id = 0.0;
-    for (int m = 0; m <= C.M && nk < F_out; ++m) {
-        Id += static_cast<double>(acc[(m + 1) * kWave + lane]);
+    int nk = 0, F = 0;
+    bool ok = false;  // this lane has a neuron (outputs are written)
+    int64_t so = 0;   // its first output slot
+    float *t_out, *slope, *cur;
+    int *q_idx;
+
+    __device__ __forceinline__ bool found() const { return nk >= F; }
+
+    __device__ void step(const LifConst &C, int m, float w) {
+        if (nk >= F) return;
+        Id += static_cast<double>(w);
         const bool last = (m == C.M);
         const float len = last ? C.last_len : C.dt;
         const double Tm = fma(static_cast<double>(m), static_cast<double>(C.dt), static_cast<double>(C.t0));
         double u0 = 0.0, Vs = Vd, Is = Id;
         bool reset = false;
-        while (nk < F_out) {
+        while (nk < F) {
             const float seglen = static_cast<float>(static_cast<double>(len) - u0);
-            // end value of the segment (not used on the last interval) and
-            // its filter constants; after a reset the segment is shorter
-            // than the interval, whose max K still bounds it
+            // end value of the segment (not used on the last interval) and its
+            // filter constants; after a reset the segment is shorter than the
+            // interval, whose max K still bounds it
             double vn;
             float r_lo;
             if (!reset) {
@@ -190,10 +172,12 @@ __global__ __launch_bounds__(kWave) void ms_fwd_kernel(LifConst C, int NV, int F
             float u, sl;
             seg_solve<KS>(C, sf, hi, fhi, u, sl);
             const double Ik = Is * exp(-static_cast<double>(u) * static_cast<double>(C.inv_ti));
-            t_out[so + nk] = static_cast<float>(Tm + u0 + static_cast<double>(u));
-            slope[so + nk] = sl;
-            q_idx[so + nk] = m;
-            cur[so + nk] = static_cast<float>(Ik);
+            if (ok) {
+                t_out[so + nk] = static_cast<float>(Tm + u0 + static_cast<double>(u));
+                slope[so + nk] = sl;
+                q_idx[so + nk] = m;
+                cur[so + nk] = static_cast<float>(Ik);
+            }
             ++nk;
             u0 += static_cast<double>(u);
             Vs = 0.0;
@@ -209,12 +193,50 @@ __global__ __launch_bounds__(kWave) void ms_fwd_kernel(LifConst C, int NV, int F
             Id = Is * exp(-rest * static_cast<double>(C.inv_ti));
         }
     }
-    for (int k = nk; k < F_out; ++k) {
-        t_out[so + k] = INFINITY;
-        slope[so + k] = 0.f;
-        q_idx[so + k] = -1;
-        cur[so + k] = 0.f;
+
+    // slots after the last spike
+    __device__ void finish() {
+        if (!ok) return;
+        for (int k = nk; k < F; ++k) {
+            t_out[so + k] = INFINITY;
+            slope[so + k] = 0.f;
+            q_idx[so + k] = -1;
+            cur[so + k] = 0.f;
+        }
     }
+};
+
+// One sample per wave, one neuron per lane: the sample's input spikes,
+// sorted by event row, are walked as in the TTFS forward (records are input
+// spikes, so a record's weight row is its index / F_in) into the scan with
+// reset. The wave stops once every lane holds F_out spikes.
+template <typename WT, int KS>
+__global__ __launch_bounds__(256) void ms_fwd_kernel(LifConst C, int B, int N_in, int F_in,
+                                                     int N_out, int F_out,
+                                                     const WT *__restrict__ Wt, SortedEv srt,
+                                                     const int *__restrict__ n_valid,
+                                                     float *__restrict__ t_out,
+                                                     float *__restrict__ slope,
+                                                     int *__restrict__ q_idx,
+                                                     float *__restrict__ cur) {
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = uniform(threadIdx.x >> 6);
+    const int waves = blockDim.x >> 6;
+    const int i = blockIdx.x * kWave + lane;
+    const bool row_ok = i < N_out;
+    const int b = uniform(blockIdx.y * waves + wave);
+    if (b >= B) return;  // wave-uniform; the kernel has no block barrier
+    const int n = *as_const(n_valid + b);
+    MsScan<KS> sc;
+    sc.F = F_out;
+    sc.ok = row_ok;
+    sc.so = (static_cast<int64_t>(b) * N_out + (row_ok ? i : 0)) * F_out;
+    sc.t_out = t_out;
+    sc.slope = slope;
+    sc.cur = cur;
+    sc.q_idx = q_idx;
+    walk_sorted_rows<WT, true>(C, N_in, N_out, Wt, srt, b, n, i, row_ok, F_in, sc);
+    sc.finish();
 }
 
 // grad_W[i][j] = sum_b sum_f (G[b][m][i] L + G[b][m+1][i] R) over the events
@@ -308,27 +330,25 @@ hipError_t prep(const LifConst &C, int64_t n_spk, int N_in, int N_out, const flo
 
 hipError_t launch_ms_forward(const LifConst &C, int64_t B, int64_t N_in, int64_t F_in,
                              int64_t N_out, int64_t F_out, const void *W, bool bf16, void *Wt,
-                             MsEvents ev, const float *t_in, float *t_out, float *slope,
-                             int *q_idx, float *cur, hipStream_t st) {
-    const int64_t n_spk = B * N_in * F_in;
-    MsGrad none{};
+                             SortedEv srt, int *n_valid, const float *t_in, float *t_out,
+                             float *slope, int *q_idx, float *cur, hipStream_t st) {
+    hipError_t e = launch_sort_records(C, B, N_in * F_in, t_in, srt, n_valid, "ms_sort", st);
+    if (e != hipSuccess) return e;
     {
-        ProfScope prof("ms_prep", st);
-        hipError_t e = (C.kind == kGeneral)
-                           ? prep<kGeneral>(C, n_spk, static_cast<int>(N_in), static_cast<int>(N_out),
-                                            t_in, ev, W, bf16, Wt, true, none, st)
-                           : prep<kAnyKind>(C, n_spk, static_cast<int>(N_in), static_cast<int>(N_out),
-                                            t_in, ev, W, bf16, Wt, true, none, st);
+        ProfScope prof("ms_transpose", st);
+        MsEvents none_ev{};
+        e = prep<kAnyKind>(C, 0, static_cast<int>(N_in), static_cast<int>(N_out), t_in, none_ev,
+                           W, bf16, Wt, true, MsGrad{}, st);
         if (e != hipSuccess) return e;
     }
     ProfScope prof("ms_fwd", st);
-    dim3 grid(cdiv(N_out, kWave), static_cast<unsigned>(B));
-    const size_t lds = static_cast<size_t>(C.M + 3) * kWave * sizeof(float);
+    constexpr int waves = 4;
+    dim3 grid(cdiv(N_out, kWave), cdiv(B, waves));
 #define MSF(WTY, KSV)                                                                          \
-    hipLaunchKernelGGL((ms_fwd_kernel<WTY, KSV>), grid, dim3(kWave), lds, st, C,               \
-                       static_cast<int>(N_in * F_in), static_cast<int>(F_in),                  \
+    hipLaunchKernelGGL((ms_fwd_kernel<WTY, KSV>), grid, dim3(waves * kWave), 0, st, C,          \
+                       static_cast<int>(B), static_cast<int>(N_in), static_cast<int>(F_in),    \
                        static_cast<int>(N_out), static_cast<int>(F_out),                       \
-                       static_cast<const WTY *>(Wt), ev, t_out, slope, q_idx, cur)
+                       static_cast<const WTY *>(Wt), srt, n_valid, t_out, slope, q_idx, cur)
     const bool gen = C.kind == kGeneral;
     if (bf16) {
         if (gen) MSF(uint16_t, kGeneral); else MSF(uint16_t, kAnyKind);

@@ -604,7 +604,7 @@ def main():
     ap.add_argument("--exact-M", default="10,20")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(f"bench.py: this build measures one GPU only; --gpus {args.gpus} is not supported "
+        print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported "
               "(the data-parallel design is described, not built).", file=sys.stderr)
         sys.exit(2)
 

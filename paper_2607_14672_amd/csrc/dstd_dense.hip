@@ -281,7 +281,12 @@ constexpr int kRowLdsCap = 48 * 1024;  // LDS budget per block when choosing NT
 constexpr int kRowsMaxM = 64;
 constexpr int kRowSub = 8;  // records per scalar load group; their NT tile loads fly together
 
-template <typename WT, int NT, int KS>
+// VEC: lane l sums the NT consecutive neurons NT*l .. NT*l+NT-1 of the
+// block's NT*64 (one NT-wide weight load per record instead of NT loads one
+// tile apart; N_out % NT == 0 so the loads are aligned). The point sums then
+// sit at the same LDS offsets as without VEC (tile t, lane l' is neuron
+// 64 t + l' = NT l + c), so the scan reads them unchanged.
+template <typename WT, int NT, int KS, bool VEC>
 __global__ __launch_bounds__(kRowWaves * 64) void fwd_rows_kernel(LifConst C, int N_in, int N_out,
                                                                   const WT *__restrict__ Wt,
                                                                   SortedEv srt,
@@ -324,18 +329,21 @@ __global__ __launch_bounds__(kRowWaves * 64) void fwd_rows_kernel(LifConst C, in
     // close row cur (target > cur): point cur-1 gets this row's L sums plus
     // the previous row's R sums (cy); rows cur+1 .. target-1 have no records,
     // so point cur is row cur's R sums alone and the points after it are 0
+    // LDS slot of this lane's value t within a point's kPt floats
+    constexpr int kLs = VEC ? 1 : kWave;
+    const int lofs = VEC ? NT * lane : lane;
     auto close_to = [&](int target) {
-        float *d = ((cur == r_lo) ? BL + wave * kPt : P + (cur - 1) * kPt) + lane;
+        float *d = ((cur == r_lo) ? BL + wave * kPt : P + (cur - 1) * kPt) + lofs;
 #pragma unroll
-        for (int t = 0; t < NT; ++t) d[t * kWave] = aL[t] + cy[t];
+        for (int t = 0; t < NT; ++t) d[t * kLs] = aL[t] + cy[t];
         if (target > cur + 1) {
-            float *e = P + cur * kPt + lane;
+            float *e = P + cur * kPt + lofs;
 #pragma unroll
-            for (int t = 0; t < NT; ++t) e[t * kWave] = aR[t];
+            for (int t = 0; t < NT; ++t) e[t * kLs] = aR[t];
             for (int r = cur + 2; r < target; ++r) {
-                float *z = P + (r - 1) * kPt + lane;
+                float *z = P + (r - 1) * kPt + lofs;
 #pragma unroll
-                for (int t = 0; t < NT; ++t) z[t * kWave] = 0.f;
+                for (int t = 0; t < NT; ++t) z[t * kLs] = 0.f;
             }
 #pragma unroll
             for (int t = 0; t < NT; ++t) cy[t] = 0.f;
@@ -358,6 +366,10 @@ __global__ __launch_bounds__(kRowWaves * 64) void fwd_rows_kernel(LifConst C, in
         const int i = (blockIdx.x * NT + t) * kWave + lane;
         voff[t] = min(i, N_out - 1) * static_cast<int>(sizeof(WT));
     }
+    // VEC: one load of NT neurons; past N_out it reads the next row's first
+    // weights or, after the last row, zeros (buffer range check): those sums
+    // belong to lanes without a neuron and are never scanned into outputs
+    const int voffv = (blockIdx.x * NT * kWave + NT * lane) * static_cast<int>(sizeof(WT));
     const int rstride = N_out * static_cast<int>(sizeof(WT));
     const int jmax = max(N_in - 1, 0);
     // Record fields come through the scalar cache, kRowSub records per load
@@ -382,8 +394,12 @@ __global__ __launch_bounds__(kRowWaves * 64) void fwd_rows_kernel(LifConst C, in
 #pragma unroll
         for (int kk = 0; kk < kRowSub; ++kk) {
             const int jo = min(max(nj[kk], 0), jmax) * rstride;
+            if constexpr (VEC) {
+                BufLoadN<WT, NT>::get(wr, voffv, jo, w[kk]);
+            } else {
 #pragma unroll
-            for (int t = 0; t < NT; ++t) w[kk][t] = BufLoad<WT>::get(wr, voff[t], jo);
+                for (int t = 0; t < NT; ++t) w[kk][t] = BufLoad<WT>::get(wr, voff[t], jo);
+            }
             cr[kk] = nr[kk];
             cL[kk] = nL[kk];
             cR[kk] = nR[kk];
@@ -416,7 +432,7 @@ __global__ __launch_bounds__(kRowWaves * 64) void fwd_rows_kernel(LifConst C, in
     if (r_hi > cur) close_to(r_hi);
     if (r_hi > r_lo) {
 #pragma unroll
-        for (int t = 0; t < NT; ++t) BR[wave * kPt + t * kWave + lane] = cy[t];
+        for (int t = 0; t < NT; ++t) BR[wave * kPt + lofs + t * kLs] = cy[t];
     }
     if (lane == 0) {
         span[wave] = r_lo;
@@ -1057,10 +1073,17 @@ hipError_t launch_forward(const LifConst &C, int64_t B, int64_t N_in, int64_t N_
             if (nt == 1 && tiles >= t && lds_of(t) <= kRowLdsCap) nt = t;
         dim3 grid(static_cast<unsigned>((tiles + nt - 1) / nt), static_cast<unsigned>(B));
         const size_t lds = lds_of(nt);
-#define FWR_K(WTY, NTV, KSV)                                                                      \
-    hipLaunchKernelGGL((fwd_rows_kernel<WTY, NTV, KSV>), grid, dim3(kRowWaves * kWave), lds, st, \
-                       C, static_cast<int>(N_in), static_cast<int>(N_out),                        \
+        // NT neighbouring neurons per lane where rows keep NT-wide loads aligned
+        const bool vec = (N_out % nt) == 0;
+#define FWR_KV(WTY, NTV, KSV, VECV)                                                               \
+    hipLaunchKernelGGL((fwd_rows_kernel<WTY, NTV, KSV, VECV>), grid, dim3(kRowWaves * kWave), lds, \
+                       st, C, static_cast<int>(N_in), static_cast<int>(N_out),                    \
                        static_cast<const WTY *>(Wt), srt, t_out, slope, q_idx)
+#define FWR_K(WTY, NTV, KSV)                      \
+    do {                                          \
+        if (vec) FWR_KV(WTY, NTV, KSV, true);     \
+        else FWR_KV(WTY, NTV, KSV, false);        \
+    } while (0)
 #define FWR(WTY, NTV)                                                     \
     do {                                                                  \
         if (C.kind == kGeneral) FWR_K(WTY, NTV, kGeneral);                \
@@ -1077,6 +1100,7 @@ hipError_t launch_forward(const LifConst &C, int64_t B, int64_t N_in, int64_t N_
         }
 #undef FWR
 #undef FWR_K
+#undef FWR_KV
         return hipGetLastError();
     }
     constexpr int waves = 4;

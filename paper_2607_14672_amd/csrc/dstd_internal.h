@@ -587,6 +587,46 @@ template <> struct BufLoad<uint16_t> {
     }
 };
 
+// N consecutive weights (N = 1, 2 or 4) with one buffer load: fp32 as 4N
+// bytes, bf16 as 2N bytes, widened to fp32.
+template <typename WT, int N> struct BufLoadN;
+template <int N> struct BufLoadN<float, N> {
+    static __device__ __forceinline__ void get(__amdgpu_buffer_rsrc_t r, int voff, int soff,
+                                               float (&out)[N]) {
+        if constexpr (N == 4) {
+            const auto v = __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0);
+#pragma unroll
+            for (int c = 0; c < 4; ++c) out[c] = __int_as_float(static_cast<int>(v[c]));
+        } else if constexpr (N == 2) {
+            const auto v = __builtin_amdgcn_raw_buffer_load_b64(r, voff, soff, 0);
+            out[0] = __int_as_float(static_cast<int>(v[0]));
+            out[1] = __int_as_float(static_cast<int>(v[1]));
+        } else {
+            out[0] = BufLoad<float>::get(r, voff, soff);
+        }
+    }
+};
+template <int N> struct BufLoadN<uint16_t, N> {
+    static __device__ __forceinline__ void get(__amdgpu_buffer_rsrc_t r, int voff, int soff,
+                                               float (&out)[N]) {
+        if constexpr (N == 4) {
+            const auto v = __builtin_amdgcn_raw_buffer_load_b64(r, voff, soff, 0);
+#pragma unroll
+            for (int c = 0; c < 2; ++c) {
+                const uint32_t u = static_cast<uint32_t>(v[c]);
+                out[2 * c] = __uint_as_float(u << 16);
+                out[2 * c + 1] = __uint_as_float(u & 0xffff0000u);
+            }
+        } else if constexpr (N == 2) {
+            const uint32_t u = static_cast<uint32_t>(__builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, 0));
+            out[0] = __uint_as_float(u << 16);
+            out[1] = __uint_as_float(u & 0xffff0000u);
+        } else {
+            out[0] = BufLoad<uint16_t>::get(r, voff, soff);
+        }
+    }
+};
+
 // Reads through the constant address space: with a wave-uniform address the
 // compiler emits scalar (SMEM) loads, batched into s_load_dwordx16 when
 // consecutive. Only for data that no kernel in flight writes.

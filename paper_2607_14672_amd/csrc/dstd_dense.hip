@@ -719,7 +719,10 @@ constexpr int kDtRanges = 6;
 // split reduction of the same layer (independent work, one launch less).
 struct RedJob { int64_t n; int nsplit; const float *part; float *out; const float *dq; int row_len; };
 
-template <typename WT, int NTW, int KS>
+// VEC: lane l of wave w takes the NTW neighbouring neurons w*NTW*64 + NTW*l
+// + t of each group (one NTW-wide weight load per record; N_out % NTW == 0),
+// else neurons (w*NTW + t)*64 + l.
+template <typename WT, int NTW, int KS, bool VEC>
 __global__ __launch_bounds__(256) void dtin_rows_kernel(LifConst C, int B, int N_in, int N_out,
                                                         const WT *__restrict__ Wt, SortedEv srt,
                                                         const float *__restrict__ gam,
@@ -756,12 +759,18 @@ __global__ __launch_bounds__(256) void dtin_rows_kernel(LifConst C, int B, int N
     const unsigned jmax = static_cast<unsigned>(max(N_in - 1, 0));
     constexpr int kGroup = 4 * NTW * kWave;
     const int ngroups = (N_out + kGroup - 1) / kGroup;
+    auto neuron = [&](int grp, int t) {
+        return grp * kGroup + (VEC ? (wave * NTW * kWave + NTW * lane + t) : ((wave * NTW + t) * kWave + lane));
+    };
+    // VEC loads past N_out read the next row's weights or zeros; those
+    // neurons have G = 0
+    auto voffv = [&](int grp) { return neuron(grp, 0) * static_cast<int>(sizeof(WT)); };
     // this lane's neurons of group 0 (the only group when N_out <= kGroup)
     float gm0[NTW], ua0[NTW];
     int qa0[NTW], voff0[NTW];
 #pragma unroll
     for (int t = 0; t < NTW; ++t) {
-        const int i = (wave * NTW + t) * kWave + lane;
+        const int i = neuron(0, t);
         const int ic = min(i, N_out - 1);
         const bool ok = i < N_out;
         gm0[t] = ok ? gam[nb + ic] : 0.f;
@@ -800,7 +809,7 @@ __global__ __launch_bounds__(256) void dtin_rows_kernel(LifConst C, int B, int N
                         g1[t] = h1[t];
                         voff[t] = voff0[t];
                     } else {
-                        const int i = grp * kGroup + (wave * NTW + t) * kWave + lane;
+                        const int i = neuron(grp, t);
                         const int ic = min(i, N_out - 1);
                         const bool ok = i < N_out;
                         const float gm = ok ? gam[nb + ic] : 0.f;
@@ -811,10 +820,16 @@ __global__ __launch_bounds__(256) void dtin_rows_kernel(LifConst C, int B, int N
                         voff[t] = ic * static_cast<int>(sizeof(WT));
                     }
                 }
+                if constexpr (VEC) {
+                    const int vo = voffv(grp);
 #pragma unroll
-                for (int kk = 0; kk < kBatch; ++kk)
+                    for (int kk = 0; kk < kBatch; ++kk) BufLoadN<WT, NTW>::get(wr, vo, jo[kk], w[kk]);
+                } else {
 #pragma unroll
-                    for (int t = 0; t < NTW; ++t) w[kk][t] = BufLoad<WT>::get(wr, voff[t], jo[kk]);
+                    for (int kk = 0; kk < kBatch; ++kk)
+#pragma unroll
+                        for (int t = 0; t < NTW; ++t) w[kk][t] = BufLoad<WT>::get(wr, voff[t], jo[kk]);
+                }
 #pragma unroll
                 for (int kk = 0; kk < kBatch; ++kk)
 #pragma unroll
@@ -1239,10 +1254,15 @@ hipError_t launch_backward(const LifConst &C, int64_t B, int64_t N_in, int64_t N
         const int64_t red_rows = ((red.n + 3) / 4 + kDtRanges * 256 - 1) / (kDtRanges * 256);
         dim3 grid(kDtRanges, static_cast<unsigned>(B + red_rows));
         ProfScope prof("dtin_rows", st);
-#define DTR_K(WTY, NTV, KSV)                                                                     \
-    hipLaunchKernelGGL((dtin_rows_kernel<WTY, NTV, KSV>), grid, dim3(256), 0, st, C,            \
+#define DTR_KV(WTY, NTV, KSV, VECV)                                                              \
+    hipLaunchKernelGGL((dtin_rows_kernel<WTY, NTV, KSV, VECV>), grid, dim3(256), 0, st, C,       \
                        static_cast<int>(B), static_cast<int>(N_in), static_cast<int>(N_out),     \
                        static_cast<const WTY *>(ws.wt), ws.srt, ws.gam, ws.uq, ws.q, grad_t_in, red)
+#define DTR_K(WTY, NTV, KSV)                                   \
+    do {                                                       \
+        if (N_out % NTV == 0) DTR_KV(WTY, NTV, KSV, true);     \
+        else DTR_KV(WTY, NTV, KSV, false);                     \
+    } while (0)
 #define DTR(WTY, NTV)                                                     \
     do {                                                                  \
         if (C.kind == kGeneral) DTR_K(WTY, NTV, kGeneral);                \
@@ -1278,6 +1298,7 @@ hipError_t launch_backward(const LifConst &C, int64_t B, int64_t N_in, int64_t N
 #undef DTR_NT
 #undef DTR
 #undef DTR_K
+#undef DTR_KV
         return hipGetLastError();
     }
     if (split) {

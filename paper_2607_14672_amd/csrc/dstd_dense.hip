@@ -486,14 +486,22 @@ __global__ __launch_bounds__(kRowWaves * 64) void fwd_rows_kernel(LifConst C, in
 // its share of the batch. G[b, :, tile] is computed in place from the
 // gradient triples (each thread owns one neuron and a fixed set of rows, so
 // neurons without gradient cost no exponential) and staged in LDS (double
-// buffered) as rows of TI + 1 floats, G[r][neuron]: the two halves of an
-// event, G[r][i] and G[r+1][i], are TI + 1 dwords apart, so one two-address
-// LDS read with immediate offsets (i, i + TI + 1) serves both, and the odd
-// row stride spreads lanes with different event rows over the banks. Rows
+// buffered) as rows of dw_stride floats, G[r][neuron]: a thread reads the
+// two halves of its event, rows r and r+1, per neuron (or four neurons per
+// 16-byte read, see dw_stride). Rows
 // R-1 and R stay zero (R-1 is the point after the grid; slot R-1 serves
 // inputs without events). The next sample's G values and events are fetched
 // while this one is consumed; a sample whose tile is all zero is skipped.
 // Batch splits write partial sums, reduced in order.
+// LDS row stride (floats) of the dW kernel's G buffers for a TI-neuron tile.
+// One sample group per block reads four neurons per 16-byte LDS read (rows
+// padded to stay 16-byte aligned); two groups read one neuron of both halves
+// per two-address read over an odd stride (measured faster there: mlp3's
+// layers with two groups 0.069 ms against 0.093 ms, the 4096-wide layer
+// with one group 1.18 ms against 1.48 ms).
+constexpr bool dw_vec(int groups) { return groups == 1; }
+constexpr int dw_stride(int ti, int groups) { return dw_vec(groups) ? ti + 4 : ti + 1; }
+
 template <int TI, int NPER, int GW, int KS>
 __global__ __launch_bounds__(256 * GW) void dw_dense_kernel(LifConst C, int B, int N_in, int N_out,
                                                              int b_per_split,
@@ -505,9 +513,9 @@ __global__ __launch_bounds__(256 * GW) void dw_dense_kernel(LifConst C, int B, i
                                                              const float *__restrict__ ev_R,
                                                              const float *__restrict__ dq,
                                                              float *__restrict__ dW_part) {
-    extern __shared__ float gs[];  // [GW][2][R + 1][TI + 1]
+    extern __shared__ float gs[];  // [GW][2][R + 1][dw_stride(TI, GW)]
     __shared__ int wlive[2][4 * GW];
-    constexpr int kStr = TI + 1;
+    constexpr int kStr = dw_stride(TI, GW);
     const int R = rows_of(C);
     const int gbuf = (R + 1) * kStr;
     const int grp = threadIdx.x >> 8;  // sample group of this thread
@@ -609,10 +617,22 @@ __global__ __launch_bounds__(256 * GW) void dw_dense_kernel(LifConst C, int B, i
         bool live_next = false;
         if (more) live_next = fetch(tri);
         if (live) {
-            const float *p = cur + slot * kStr;
+            if constexpr (dw_vec(GW)) {
+                const float4 *p = reinterpret_cast<const float4 *>(cur + slot * kStr);
 #pragma unroll
-            for (int ii = 0; ii < TI; ++ii)
-                acc[ii] = fmaf(p[ii], L, fmaf(p[ii + kStr], Rv, acc[ii]));
+                for (int i4 = 0; i4 < TI / 4; ++i4) {
+                    const float4 a = p[i4], c = p[i4 + kStr / 4];
+                    acc[4 * i4] = fmaf(a.x, L, fmaf(c.x, Rv, acc[4 * i4]));
+                    acc[4 * i4 + 1] = fmaf(a.y, L, fmaf(c.y, Rv, acc[4 * i4 + 1]));
+                    acc[4 * i4 + 2] = fmaf(a.z, L, fmaf(c.z, Rv, acc[4 * i4 + 2]));
+                    acc[4 * i4 + 3] = fmaf(a.w, L, fmaf(c.w, Rv, acc[4 * i4 + 3]));
+                }
+            } else {
+                const float *p = cur + slot * kStr;
+#pragma unroll
+                for (int ii = 0; ii < TI; ++ii)
+                    acc[ii] = fmaf(p[ii], L, fmaf(p[ii + kStr], Rv, acc[ii]));
+            }
         }
         if (more) store(gsg + ((it + 1) & 1) * gbuf);
         live = group_live(live_next, (it + 1) & 1);
@@ -1141,7 +1161,7 @@ hipError_t launch_forward(const LifConst &C, int64_t B, int64_t N_in, int64_t N_
 static int dw_ti(int M, int64_t N_out) {
     if (N_out <= 16) return 16;
     if (N_out <= 32) return 32;
-    return (2 * (M + 4) * 65 * 4 <= 48 * 1024) ? 64 : 32;
+    return (2 * (M + 4) * dw_stride(64, 1) * 4 <= 48 * 1024) ? 64 : 32;
 }
 
 // register slots per thread for staging one tile (R * TI values / 256 threads)
@@ -1162,7 +1182,7 @@ DwPlan plan_dw(int64_t B, int64_t N_in, int64_t N_out, int M) {
     const int64_t tiles = ((N_in + 255) / 256) * ((N_out + p.jw - 1) / p.jw);
     p.nsplit = 1;
     while (tiles * p.nsplit < 1024 && B / (p.nsplit * 2) >= 4) p.nsplit *= 2;
-    const size_t g_lds = 2 * static_cast<size_t>(M + 4) * (p.jw + 1) * sizeof(float);  // one group
+    const size_t g_lds = 2 * static_cast<size_t>(M + 4) * dw_stride(p.jw, 2) * sizeof(float);  // one of two groups
     const int groups = (p.nsplit >= 4 && 2 * g_lds <= 64 * 1024) ? 2 : 1;
     p.nsplit /= groups;
     p.waves = 4 * groups;
@@ -1180,7 +1200,7 @@ static hipError_t launch_dw(const LifConst &C, const DwPlan &p, int64_t B, int64
     // G buffers of every group; after the samples, the same LDS carries the
     // groups' sums to group 0 (16 per thread per round)
     const int groups = p.waves / 4;
-    const size_t lds = std::max(groups * 2 * static_cast<size_t>(C.M + 4) * (ti + 1),
+    const size_t lds = std::max(groups * 2 * static_cast<size_t>(C.M + 4) * dw_stride(ti, groups),
                                 static_cast<size_t>(groups - 1) * 16 * 256) *
                        sizeof(float);
     ProfScope prof("dw_dense", st);

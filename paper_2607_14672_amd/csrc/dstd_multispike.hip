@@ -23,6 +23,7 @@
 #include "dstd_kernels.h"
 #include "dstd_profile.h"
 #include "dstd_walk.h"
+#include "dstd_rows.h"
 
 namespace dstd {
 
@@ -206,6 +207,43 @@ struct MsScan {
     }
 };
 
+// Multi-spike outputs of the row-parallel forward: a record is an input
+// spike j_in * F_in + f, whose weight row is its index divided by F_in
+// (multiplication by magic = ceil(2^40 / F_in), exact for indices below
+// 2^40 / F_in); the scan is the one with reset above, and runs until every
+// neuron of the tile holds F spikes or the grid ends.
+struct RowOutMs {
+    float *t_out, *slope, *cur;
+    int *q_idx;
+    int F;
+    uint64_t magic;
+
+    __device__ __forceinline__ int wrow(int j) const {
+        return j > 0 ? static_cast<int>((static_cast<uint64_t>(j) * magic) >> 40) : 0;
+    }
+
+    template <int KS>
+    __device__ __forceinline__ void scan(const LifConst &C, int N_out, int b, int i, bool row_ok,
+                                         const float *tp, int kPt) const {
+        MsScan<KS> sc;
+        sc.F = F;
+        sc.ok = row_ok;
+        sc.so = (static_cast<int64_t>(b) * N_out + (row_ok ? i : 0)) * F;
+        sc.t_out = t_out;
+        sc.slope = slope;
+        sc.cur = cur;
+        sc.q_idx = q_idx;
+        float wn = tp[0];  // next grid point's sum, read ahead
+        for (int m = 0; m <= C.M; ++m) {
+            const float wc = wn;
+            if (m < C.M) wn = tp[(m + 1) * kPt];
+            sc.step(C, m, wc);
+            if (__all(sc.found() || !row_ok)) break;
+        }
+        sc.finish();
+    }
+};
+
 // One sample per wave, one neuron per lane: the sample's input spikes,
 // sorted by event row, are walked as in the TTFS forward (records are input
 // spikes, so a record's weight row is its index / F_in) into the scan with
@@ -342,6 +380,46 @@ hipError_t launch_ms_forward(const LifConst &C, int64_t B, int64_t N_in, int64_t
         if (e != hipSuccess) return e;
     }
     ProfScope prof("ms_fwd", st);
+    if (B == 0 || N_out == 0) return hipSuccess;
+    const bool gen = C.kind == kGeneral;
+    if (C.M <= kRowsMaxM) {
+        // row-parallel: four waves sum a sample's spikes, one scan per tile
+        const int R = C.M + 3;
+        const int nt = rows_nt(N_out, R);
+        dim3 grid(cdiv(cdiv(N_out, kWave), nt), static_cast<unsigned>(B));
+        const size_t lds = rows_lds(nt, R);
+        const bool vec = (N_out % nt) == 0;
+        const uint64_t magic = ((uint64_t{1} << 40) + static_cast<uint64_t>(F_in) - 1) /
+                               static_cast<uint64_t>(F_in);
+        const RowOutMs out{t_out, slope, cur, q_idx, static_cast<int>(F_out), magic};
+#define MSR_KV(WTY, NTV, KSV, VECV)                                                              \
+    hipLaunchKernelGGL((fwd_rows_kernel<WTY, NTV, KSV, VECV, RowOutMs>), grid,                   \
+                       dim3(kRowWaves * kWave), lds, st, C, static_cast<int>(N_in),              \
+                       static_cast<int>(N_out), static_cast<const WTY *>(Wt), srt, out)
+#define MSR_K(WTY, NTV, KSV)                  \
+    do {                                      \
+        if (vec) MSR_KV(WTY, NTV, KSV, true); \
+        else MSR_KV(WTY, NTV, KSV, false);    \
+    } while (0)
+#define MSR(WTY, NTV)                                        \
+    do {                                                     \
+        if (gen) MSR_K(WTY, NTV, kGeneral);                  \
+        else MSR_K(WTY, NTV, kAnyKind);                      \
+    } while (0)
+        if (bf16) {
+            if (nt == 4) MSR(uint16_t, 4);
+            else if (nt == 2) MSR(uint16_t, 2);
+            else MSR(uint16_t, 1);
+        } else {
+            if (nt == 4) MSR(float, 4);
+            else if (nt == 2) MSR(float, 2);
+            else MSR(float, 1);
+        }
+#undef MSR
+#undef MSR_K
+#undef MSR_KV
+        return hipGetLastError();
+    }
     constexpr int waves = 4;
     dim3 grid(cdiv(N_out, kWave), cdiv(B, waves));
 #define MSF(WTY, KSV)                                                                          \
@@ -349,7 +427,6 @@ hipError_t launch_ms_forward(const LifConst &C, int64_t B, int64_t N_in, int64_t
                        static_cast<int>(B), static_cast<int>(N_in), static_cast<int>(F_in),    \
                        static_cast<int>(N_out), static_cast<int>(F_out),                       \
                        static_cast<const WTY *>(Wt), srt, n_valid, t_out, slope, q_idx, cur)
-    const bool gen = C.kind == kGeneral;
     if (bf16) {
         if (gen) MSF(uint16_t, kGeneral); else MSF(uint16_t, kAnyKind);
     } else {

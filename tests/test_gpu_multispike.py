@@ -106,6 +106,17 @@ def test_multispike_finite_t_max(dev):
     assert np.all(gpu["t_out"][np.isfinite(gpu["t_out"])] < 1.3)
 
 
+@pytest.mark.parametrize("M,N_in,F_in,N_out", [(80, 50, 2, 70), (24, 40, 3, 75), (16, 10, 64, 40)])
+def test_multispike_forward_paths(dev, M, N_in, F_in, N_out):
+    """M > 64 takes the one-wave-per-(sample, tile) walk, M <= 64 the
+    row-parallel kernel; an odd N_out takes its one-neuron-per-tile weight
+    loads, and F_in = 64 (the maximum) the largest divisor from spike index to
+    weight row."""
+    p, t, W = _case(5, 3, N_in, F_in, N_out, M, 1.0, 0.3, k=3.0)
+    _, orc, _ = _parity(dev, p, t, W, 4, f"multispike M={M} {N_in}x{F_in}->{N_out}")
+    assert (orc["q"][:, :, 1] >= 0).mean() > 0.3
+
+
 def test_multispike_single_spike_equals_ttfs(dev):
     """F_in = F_out = 1 is the TTFS layer: the same spikes as dstd_lif_forward."""
     import torch

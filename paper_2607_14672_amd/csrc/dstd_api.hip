@@ -802,7 +802,7 @@ dstd_status check_ms(const dstd_lif_params *p, int64_t B, int64_t N_in, int64_t 
     return DSTD_OK;
 }
 
-struct MsWs { size_t row, L, R, dL, dR, wt, G, sj, sr, sL, sR, nvalid, rs, total; };
+struct MsWs { size_t row, L, R, dL, dR, wt, G, part, sj, sr, sL, sR, nvalid, rs, total; };
 
 // forward: the records of every input spike sorted by event row (as the TTFS
 // forward's lists) and W^T; backward: per-spike events, W^T and G
@@ -817,6 +817,9 @@ MsWs ms_ws_layout(int M, int64_t B, int64_t N_in, int64_t F_in, int64_t N_out, b
         w.dL = off; off += align_up(n * sizeof(float));
         w.dR = off; off += align_up(n * sizeof(float));
         w.G = off; off += align_up((size_t)B * (size_t)(M + 1) * (size_t)N_out * sizeof(float));
+        const int S = dstd::ms_dw_splits(M, B, N_in, N_out);
+        w.part = off;
+        if (S > 1) off += align_up((size_t)S * (size_t)N_in * (size_t)N_out * sizeof(float));
     } else {
         const size_t ns = n + dstd::kSortPad;
         w.sj = off; off += align_up(ns * sizeof(int));
@@ -902,7 +905,8 @@ dstd_status dstd_lif_multispike_backward(const dstd_lif_params *p, int64_t B, in
     hipError_t e = dstd::launch_ms_backward(C, B, N_in, F_in, N_out, F_out, W,
                                             w_dtype == DSTD_BF16, at<void>(ws, L.wt), ev, t_in,
                                             t_out, slope, q_idx, cur, grad_t_out,
-                                            at<float>(ws, L.G), grad_W, grad_t_in,
+                                            at<float>(ws, L.G), at<float>(ws, L.part), grad_W,
+                                            grad_t_in,
                                             static_cast<hipStream_t>(stream));
     return hip_status(e, "multi-spike backward launch");
 }

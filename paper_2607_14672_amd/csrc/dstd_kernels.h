@@ -132,6 +132,20 @@ struct MsGrad {
 };
 constexpr int kMsMaxM = 250;  // (M + 3) rows x 64 lanes of fp32 in 64 KB of LDS
 constexpr int kMsMaxF = 64;
+// dW for M <= kMsDwMaxM stages G tiles in LDS, with the batch split S ways
+// (S from the shapes alone, so the workspace query and the launch agree);
+// S > 1 needs S * N_in * N_out floats of partials in the workspace. 0: the
+// one-wave-per-input kernel is used instead.
+constexpr int kMsDwMaxM = 64;
+inline int ms_dw_splits(int M, int64_t B, int64_t N_in, int64_t N_out) {
+    if (M > kMsDwMaxM || B < 1 || N_in < 1 || N_out < 1) return 0;
+    const int64_t blocks = ((N_out + 63) / 64) * ((N_in + 63) / 64);
+    int64_t s = (1024 + blocks - 1) / blocks;
+    s = s < 16 ? s : 16;
+    s = s < B ? s : B;
+    const int64_t per = (B + s - 1) / s;
+    return static_cast<int>((B + per - 1) / per);
+}
 
 hipError_t launch_ms_forward(const LifConst &C, int64_t B, int64_t N_in, int64_t F_in,
                              int64_t N_out, int64_t F_out, const void *W, bool bf16, void *Wt,
@@ -141,8 +155,8 @@ hipError_t launch_ms_backward(const LifConst &C, int64_t B, int64_t N_in, int64_
                               int64_t N_out, int64_t F_out, const void *W, bool bf16, void *Wt,
                               MsEvents ev, const float *t_in, const float *t_out,
                               const float *slope, const int *q_idx, const float *cur,
-                              const float *grad_t, float *G, float *grad_W, float *grad_t_in,
-                              hipStream_t st);
+                              const float *grad_t, float *G, float *dw_part, float *grad_W,
+                              float *grad_t_in, hipStream_t st);
 
 // ----------------------------------------------------------------- exact --
 // Exact spike times by sorting (App. A, Alg. 1). Per sample, the finite

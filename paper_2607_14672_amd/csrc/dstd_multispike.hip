@@ -308,6 +308,103 @@ __global__ __launch_bounds__(kMsWaves * kWave) void ms_dw_kernel(LifConst C, int
 // grad_t_in[b][j][f] = sum_i w_ij (G[b][m][i] dL + G[b][m+1][i] dR): one wave
 // per (b, j) summing over neurons (lanes) with row j of W^T, then across the
 // wave.
+// dW for M <= kMsDwMaxM. A block takes one 64-neuron tile (lane = neuron i)
+// and 64 inputs (kMsDwIn per wave) over a contiguous share of the batch. Per
+// sample the tile G[b][0..M][tile] is staged in LDS (the next sample's tile
+// is loaded into registers meanwhile), and each wave adds, input by input,
+// G[m][i] L + G[m+1][i] R for the events of its inputs' spikes, whose fields
+// are uniform (scalar loads, a whole spike index f for all kMsDwIn inputs at
+// once). G is read from memory once per (block, sample) instead of once per
+// (input, sample). Output: out[split][i][j], summed over splits in order
+// (or grad_W itself with one split).
+constexpr int kMsDwIn = 16;
+constexpr int kMsDwPre = ((kMsDwMaxM + 1) * kWave + kMsWaves * kWave - 1) / (kMsWaves * kWave);
+
+__global__ __launch_bounds__(kMsWaves * kWave) void ms_dw_tiled_kernel(
+    LifConst C, int B, int N_in, int F_in, int N_out, int b_per, MsEvents ev,
+    const float *__restrict__ G, float *__restrict__ out) {
+    extern __shared__ float gs[];  // [2][M + 1][64]
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = uniform(threadIdx.x >> 6);
+    const int R = C.M + 1;
+    const int n_el = R * kWave;
+    const int i0 = blockIdx.x * kWave;
+    const int j0 = (blockIdx.y * kMsWaves + wave) * kMsDwIn;
+    const int b0 = blockIdx.z * b_per;
+    const int b1 = min(B, b0 + b_per);
+    float pre[kMsDwPre];
+    // thread t holds elements e = t + 256 k of the tile: row e / 64, column e % 64
+    auto fetch = [&](int b) {
+        const float *Gb = G + static_cast<int64_t>(b) * R * N_out;
+#pragma unroll
+        for (int k = 0; k < kMsDwPre; ++k) {
+            const int e = threadIdx.x + k * kMsWaves * kWave;
+            const int ii = i0 + (e & (kWave - 1));
+            pre[k] = (e < n_el && ii < N_out) ? Gb[static_cast<int64_t>(e >> 6) * N_out + ii] : 0.f;
+        }
+    };
+    auto stage = [&](float *dst) {
+#pragma unroll
+        for (int k = 0; k < kMsDwPre; ++k) {
+            const int e = threadIdx.x + k * kMsWaves * kWave;
+            if (e < n_el) dst[e] = pre[k];
+        }
+    };
+    float acc[kMsDwIn];
+#pragma unroll
+    for (int k = 0; k < kMsDwIn; ++k) acc[k] = 0.f;
+    const int jl = N_in - 1;
+    if (b0 < b1) {
+        fetch(b0);
+        stage(gs);
+    }
+    __syncthreads();
+    for (int b = b0; b < b1; ++b) {
+        const int cb = (b - b0) & 1;
+        if (b + 1 < b1) fetch(b + 1);
+        const float *gb = gs + cb * n_el + lane;
+        for (int f = 0; f < F_in; ++f) {
+            int rw[kMsDwIn];
+            float lv[kMsDwIn], rv[kMsDwIn];
+#pragma unroll
+            for (int k = 0; k < kMsDwIn; ++k) {
+                const int64_t eo = (static_cast<int64_t>(b) * N_in + min(j0 + k, jl)) * F_in + f;
+                rw[k] = (j0 + k <= jl) ? *as_const(ev.row + eo) : -1;
+                lv[k] = *as_const(ev.L + eo);
+                rv[k] = *as_const(ev.R + eo);
+            }
+#pragma unroll
+            for (int k = 0; k < kMsDwIn; ++k) {
+                const int m = rw[k] - 1;  // L at grid point m, R at m + 1
+                if (rw[k] >= 0) {
+                    if (m >= 0 && m <= C.M) acc[k] = fmaf(gb[m * kWave], lv[k], acc[k]);
+                    if (m + 1 <= C.M) acc[k] = fmaf(gb[(m + 1) * kWave], rv[k], acc[k]);
+                }
+            }
+        }
+        if (b + 1 < b1) stage(gs + (cb ^ 1) * n_el);
+        __syncthreads();
+    }
+    const int i = i0 + lane;
+    if (i < N_out) {
+        float *o = out + (static_cast<int64_t>(blockIdx.z) * N_out + i) * N_in;
+#pragma unroll
+        for (int k = 0; k < kMsDwIn; ++k)
+            if (j0 + k <= jl) o[j0 + k] = acc[k];
+    }
+}
+
+// out[k] = sum over s of part[s][k], in split order
+__global__ __launch_bounds__(256) void ms_dw_reduce_kernel(int64_t n, int S,
+                                                           const float *__restrict__ part,
+                                                           float *__restrict__ out) {
+    const int64_t k = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+    if (k >= n) return;
+    float a = part[k];
+    for (int s = 1; s < S; ++s) a += part[s * n + k];
+    out[k] = a;
+}
+
 template <typename WT>
 __global__ __launch_bounds__(kMsWaves * kWave) void ms_dtin_kernel(LifConst C, int B, int N_in,
                                                                    int F_in, int N_out, MsEvents ev,
@@ -440,8 +537,8 @@ hipError_t launch_ms_backward(const LifConst &C, int64_t B, int64_t N_in, int64_
                               int64_t N_out, int64_t F_out, const void *W, bool bf16, void *Wt,
                               MsEvents ev, const float *t_in, const float *t_out,
                               const float *slope, const int *q_idx, const float *cur,
-                              const float *grad_t, float *G, float *grad_W, float *grad_t_in,
-                              hipStream_t st) {
+                              const float *grad_t, float *G, float *dw_part, float *grad_W,
+                              float *grad_t_in, hipStream_t st) {
     const int64_t n_spk = B * N_in * F_in;
     MsGrad gr{t_out, slope, q_idx, cur, grad_t, G, B * N_out, static_cast<int>(F_out)};
     {
@@ -455,12 +552,34 @@ hipError_t launch_ms_backward(const LifConst &C, int64_t B, int64_t N_in, int64_
     }
     if (grad_W && N_in * N_out > 0) {
         ProfScope prof("ms_dw", st);
-        hipLaunchKernelGGL(ms_dw_kernel, dim3(cdiv(N_out, kWave), cdiv(N_in, kMsWaves)),
-                           dim3(kMsWaves * kWave), 0, st, C, static_cast<int>(B),
-                           static_cast<int>(N_in), static_cast<int>(F_in), static_cast<int>(N_out),
-                           ev, G, grad_W);
-        hipError_t e = hipGetLastError();
-        if (e != hipSuccess) return e;
+        const int S = ms_dw_splits(C.M, B, N_in, N_out);
+        if (S > 0) {
+            const int per = static_cast<int>(cdiv(B, S));
+            float *dst = (S > 1) ? dw_part : grad_W;
+            const size_t lds = 2 * static_cast<size_t>(C.M + 1) * kWave * sizeof(float);
+            hipLaunchKernelGGL(ms_dw_tiled_kernel,
+                               dim3(cdiv(N_out, kWave), cdiv(N_in, kMsWaves * kMsDwIn),
+                                    static_cast<unsigned>(S)),
+                               dim3(kMsWaves * kWave), lds, st, C, static_cast<int>(B),
+                               static_cast<int>(N_in), static_cast<int>(F_in),
+                               static_cast<int>(N_out), per, ev, G, dst);
+            hipError_t e = hipGetLastError();
+            if (e != hipSuccess) return e;
+            if (S > 1) {
+                const int64_t n = N_in * N_out;
+                hipLaunchKernelGGL(ms_dw_reduce_kernel, dim3(cdiv(n, 256)), dim3(256), 0, st, n, S,
+                                   dw_part, grad_W);
+                e = hipGetLastError();
+                if (e != hipSuccess) return e;
+            }
+        } else {
+            hipLaunchKernelGGL(ms_dw_kernel, dim3(cdiv(N_out, kWave), cdiv(N_in, kMsWaves)),
+                               dim3(kMsWaves * kWave), 0, st, C, static_cast<int>(B),
+                               static_cast<int>(N_in), static_cast<int>(F_in), static_cast<int>(N_out),
+                               ev, G, grad_W);
+            hipError_t e = hipGetLastError();
+            if (e != hipSuccess) return e;
+        }
     }
     if (grad_t_in && B * N_in > 0) {
         ProfScope prof("ms_dtin", st);

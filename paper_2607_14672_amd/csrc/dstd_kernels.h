@@ -133,14 +133,15 @@ struct MsGrad {
 constexpr int kMsMaxM = 250;  // (M + 3) rows x 64 lanes of fp32 in 64 KB of LDS
 constexpr int kMsMaxF = 64;
 // dW for M <= kMsDwMaxM stages G tiles in LDS, with the batch split S ways
-// (S from the shapes alone, so the workspace query and the launch agree);
+// (S from the shapes alone, so the workspace query and the launch agree:
+// about 2048 blocks, at most 16 splits);
 // S > 1 needs S * N_in * N_out floats of partials in the workspace. 0: the
 // one-wave-per-input kernel is used instead.
 constexpr int kMsDwMaxM = 64;
 inline int ms_dw_splits(int M, int64_t B, int64_t N_in, int64_t N_out) {
     if (M > kMsDwMaxM || B < 1 || N_in < 1 || N_out < 1) return 0;
     const int64_t blocks = ((N_out + 63) / 64) * ((N_in + 63) / 64);
-    int64_t s = (1024 + blocks - 1) / blocks;
+    int64_t s = (2048 + blocks - 1) / blocks;
     s = s < 16 ? s : 16;
     s = s < B ? s : B;
     const int64_t per = (B + s - 1) / s;

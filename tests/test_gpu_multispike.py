@@ -136,3 +136,46 @@ def test_multispike_single_spike_equals_ttfs(dev):
     assert torch.equal(q[:, :, 0], q1)
     f = q1 >= 0
     assert float((to[:, :, 0][f] - t1[f]).abs().max()) <= 2e-6
+
+
+@pytest.mark.parametrize("F_in,F_out", [(1, 1), (4, 8)])
+def test_multispike_bench_size_sampled(dev, F_in, F_out):
+    """The timed multi-spike configuration (B 128, 784 -> 1000, M 32 on [0, 1],
+    tau (1.0, 0.5), the inputs and weights of the multi-spike bench): the
+    forward of three sampled samples against the oracle run on those samples
+    alone (samples are independent). The upstream gradient is nonzero on those
+    samples only, so grad_W (a sum over samples) and grad_t_in are checked in
+    full against the oracle's backward over the three."""
+    import torch
+    from paper_2607_14672_amd import dstd
+    B, N_in, N_out, M = 128, 784, 1000, 32
+    p = dict(tau_m=1.0, tau_s=0.5, threshold=1.0, M=M, t0=0.0, dt=1.0 / M)
+    rng = np.random.Generator(np.random.PCG64(12))
+    t = rng.random((B, N_in, F_in)).astype(np.float32)
+    n = N_in * F_in
+    W = ((24.0 / n) * (1 + 0.3 * math.sqrt(n) * rng.standard_normal((N_out, N_in)))).astype(np.float32)
+    prm = dstd.make_params(1.0, 0.5, 1.0, M, 0.0, 1.0 / M)
+    tt, Wt = torch.from_numpy(t).to(dev), torch.from_numpy(W).to(dev)
+    to, sl, q, cur = dstd.multispike_forward(prm, tt, Wt, F_out)
+    torch.cuda.synchronize()
+    rows = [0, 61, 127]
+    ts = np.ascontiguousarray(t[rows])
+    orc = oracle.ms_forward(p, ts, W, F_out)
+    gpu = dict(t_out=to.cpu().numpy()[rows], slope=sl.cpu().numpy()[rows], q=q.cpu().numpy()[rows])
+    mask, st = check_forward(gpu, _flat_oracle(orc), None, 1.0, label=f"multispike bench-size F=({F_in},{F_out})")
+    mask = np.maximum.accumulate(mask, axis=2)
+    fired = orc["q"] >= 0
+    assert fired.mean() > 0.5
+    gs = np.random.default_rng(9).standard_normal(orc["t_out"].shape)
+    gs = np.where(mask | ~fired, 0.0, gs)
+    g = np.zeros((B, N_out, F_out), dtype=np.float32)
+    g[rows] = gs
+    gW, gx = dstd.multispike_backward(prm, tt, Wt, to, sl, q, cur, torch.from_numpy(g).to(dev))
+    torch.cuda.synchronize()
+    ob = oracle.ms_backward(p, ts, W, orc, gs.astype(np.float32).astype(np.float64))
+    check_grad(gW.cpu().numpy(), ob["grad_W"], "bench-size dW", ob["grad_W_abs"])
+    gxs = gx.cpu().numpy()
+    kink = near_grid(ts, p)
+    check_grad(gxs[rows][~kink], ob["grad_t_in"][~kink], "bench-size dt_in", ob["grad_t_in_abs"][~kink])
+    others = np.setdiff1d(np.arange(B), rows)
+    assert not gxs[others].any()

@@ -31,6 +31,7 @@ namespace {
 
 constexpr int kMsPrepThreads = 256;
 constexpr int kMsWaves = 4;  // waves per dW / dt_in block (one input each)
+constexpr int kMsGReg = 8;   // spikes per neuron whose G terms are summed in registers
 
 // K(u) in fp64 for the state carried after a reset (Table "tab:kernel")
 __device__ __forceinline__ double kern_d64(const LifConst &C, double u) {
@@ -82,9 +83,66 @@ __global__ __launch_bounds__(kMsPrepThreads) void ms_prep_kernel(
     const int64_t so = o * F;
     const int R = C.M + 1;
     float *Gc = gr.G + b * R * N_out + i;  // G[b][m][i] at Gc[m * N_out]
-    for (int m = 0; m < R; ++m) Gc[static_cast<int64_t>(m) * N_out] = 0.f;
     int K = 0;
     while (K < F && gr.q[so + K] >= 0) ++K;
+    if (K <= kMsGReg) {
+        // gamma_k and the spike constants in registers (backward over k), then
+        // each G[m] summed over the spikes (same order, k descending) and
+        // written once
+        float gam[kMsGReg], tkv[kMsGReg], kdv[kMsGReg];
+        int qv[kMsGReg];
+        float gnext = 0.f;
+#pragma unroll
+        for (int k = kMsGReg - 1; k >= 0; --k) {
+            gam[k] = 0.f;
+            tkv[k] = 0.f;
+            kdv[k] = 0.f;
+            qv[k] = -1;
+            if (k < K) {
+                const float tk = gr.t[so + k];
+                const float gbar = gr.g[so + k] + gnext;
+                gam[k] = -gbar / fmaxf(gr.slope[so + k], C.slope_floor);
+                qv[k] = min(gr.q[so + k], C.M);
+                tkv[k] = tk;
+                if (k > 0) {
+                    const double tp = gr.t[so + k - 1];
+                    const double tkd = tk;
+                    kdv[k] = kern<KS>(C, static_cast<float>(tkd - tp));
+                    const float d = static_cast<float>(tkd - tp);
+                    float Kv, Kp;
+                    {
+                        float f, fp;
+                        const Seg sg{0.f, 1.f};  // v = K(u), v' = K'(u) for unit current, V = 0
+                        seg_eval<KS>(C, sg, d, f, fp);
+                        Kv = f + C.theta;
+                        Kp = fp;
+                    }
+                    const float dprev = gr.cur[so + k - 1] * (Kv * C.inv_ti + Kp) /
+                                        fmaxf(gr.slope[so + k], C.slope_floor);
+                    gnext = gbar * dprev;
+                }
+            }
+        }
+        for (int m = 0; m < R; ++m) {
+            const double Tm = fma(static_cast<double>(m), static_cast<double>(C.dt), static_cast<double>(C.t0));
+            float a = 0.f;
+#pragma unroll
+            for (int k = kMsGReg - 1; k >= 0; --k) {
+                const int qprev = (k > 0) ? qv[k > 0 ? k - 1 : 0] : -1;
+                if (m <= qv[k]) {
+                    const float c =
+                        (m > qprev)
+                            ? kern<KS>(C, static_cast<float>(static_cast<double>(tkv[k]) - Tm))
+                            : expf(-static_cast<float>(static_cast<double>(tkv[k > 0 ? k - 1 : 0]) - Tm) *
+                                   C.inv_ti) * kdv[k];
+                    a += gam[k] * c;
+                }
+            }
+            Gc[static_cast<int64_t>(m) * N_out] = a;
+        }
+        return;
+    }
+    for (int m = 0; m < R; ++m) Gc[static_cast<int64_t>(m) * N_out] = 0.f;
     float gnext = 0.f;  // gbar_{k+1} d t_{k+1} / d t_k
     for (int k = K - 1; k >= 0; --k) {
         const float tk = gr.t[so + k];

@@ -122,6 +122,16 @@ def test_multispike_forward_paths(dev, M, N_in, F_in, N_out, B, seed):
     assert (orc["q"][:, :, 1] >= 0).mean() > 0.3
 
 
+def test_multispike_more_than_eight_spikes(dev):
+    """Up to 12 spikes per neuron: neurons with at most 8 build their G column
+    in registers, the others by the per-spike accumulation in memory; both in
+    one launch."""
+    p, t, W = _case(7, 3, 60, 4, 70, 48, 1.0, 0.3, k=6.0)
+    _, orc, _ = _parity(dev, p, t, W, 12, "multispike 12 spikes")
+    n = (orc["q"] >= 0).sum(axis=2)
+    assert (n > 8).mean() > 0.3 and (n <= 8).mean() > 0.1
+
+
 def test_multispike_single_spike_equals_ttfs(dev):
     """F_in = F_out = 1 is the TTFS layer: the same spikes as dstd_lif_forward."""
     import torch

@@ -1,7 +1,8 @@
 """Build the gfx950 DSTD-LIF shared library in-tree with hipcc.
 
 ``python -m paper_2607_14672_amd.build`` compiles csrc/*.hip into
-``paper_2607_14672_amd/libdstd_lif.so`` (always rebuilds).
+``paper_2607_14672_amd/libdstd_lif.so`` (always rebuilds). Each source is
+compiled to an object in parallel, then the objects are linked.
 """
 from __future__ import annotations
 
@@ -9,6 +10,8 @@ import glob
 import os
 import subprocess
 import sys
+import tempfile
+from concurrent.futures import ThreadPoolExecutor
 
 PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
@@ -20,7 +23,6 @@ HIPCC_FLAGS = [
     "-O3",
     "-std=c++17",
     "-fPIC",
-    "-shared",
     "-Wall",
     # no packed-fp32 instructions (v_pk_*_f32) in any kernel
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
@@ -28,16 +30,28 @@ HIPCC_FLAGS = [
 ]
 
 
-def build(verbose: bool = False) -> str:
-    hipcc = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
-    tmp = LIB + ".tmp"
-    cmd = [hipcc] + HIPCC_FLAGS + ["-o", tmp] + SOURCES
+def _run(cmd, verbose):
     if verbose:
         print(" ".join(cmd), flush=True)
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         sys.stderr.write(r.stdout + r.stderr)
-        raise RuntimeError("hipcc failed building libdstd_lif.so")
+    return r.returncode
+
+
+def build(verbose: bool = False) -> str:
+    hipcc = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
+    jobs = max(1, min(len(SOURCES), int(os.environ.get("MAX_JOBS", os.cpu_count() or 4))))
+    with tempfile.TemporaryDirectory(prefix="dstd_build_") as tmpd:
+        objs = [os.path.join(tmpd, os.path.basename(s) + ".o") for s in SOURCES]
+        cmds = [[hipcc] + HIPCC_FLAGS + ["-c", "-o", o, s] for s, o in zip(SOURCES, objs)]
+        with ThreadPoolExecutor(max_workers=jobs) as ex:
+            rcs = list(ex.map(lambda c: _run(c, verbose), cmds))
+        if any(rcs):
+            raise RuntimeError("hipcc failed compiling the DSTD-LIF sources")
+        tmp = LIB + ".tmp"
+        if _run([hipcc, "--offload-arch=gfx950", "-shared", "-fPIC", "-o", tmp] + objs, verbose):
+            raise RuntimeError("hipcc failed linking libdstd_lif.so")
     os.replace(tmp, LIB)
     return LIB
 

@@ -5,6 +5,8 @@ Only the test suite, ``__graft_entry__.smoke()`` and the CPU-baseline leg of
 """
 from .oracle import (  # noqa: F401
     build_oracle,
+    compile_oracle,
+    use_library,
     kernel,
     kdstd,
     lambert_w0,

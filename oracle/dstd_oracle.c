@@ -133,6 +133,8 @@ static double kdstd_dt(double tv, double ti, double D, double t) {
 
 double oracle_kdstd(double tau_v, double tau_i, double dt, double t) { return kdstd(tau_v, tau_i, dt, t); }
 
+static double kern_dt(double tv, double ti, double t);
+
 /* Grid point T_m (App. B.1 with t_offset folded into t0). */
 static double grid(double t0, double dt, int m) { return t0 + (double)m * dt; }
 
@@ -443,13 +445,17 @@ static void sample_events(const prm_t *p, const double *t_row, int64_t N_in, ev_
  * t_out, q_idx = interval index (-1 = none), margin (distance of the
  * decision-relevant potentials from V_th), vabs = sum over m <= q* of
  * |K(t_out - T_m)| * sum_j |w_ij s_jm| (scale of the terms forming v^(t_out)),
+ * emass = sum over m <= q* (all m for a silent neuron) of sum_j |w_ij s_jm|
+ * (the event mass that v^ and its derivatives are formed from; with
+ * |K'| <= 1 it bounds the scale of the terms of the slope),
  * what (optional) [B][M+1][N_out] = weighted events.
+ * vabs, emass and what are conditioning / inspection outputs for the tests.
  */
 void oracle_dstd_forward(double tau_m, double tau_s, double theta, int M, double t0, double dt,
                          double t_max, int64_t B, int64_t N_in, int64_t N_out,
                          const double *t_in, const double *W,
                          double *t_out, double *slope, int32_t *q_idx, double *margin,
-                         double *vabs, double *what) {
+                         double *vabs, double *emass, double *what) {
     prm_t p;
     canon(&p, tau_m, tau_s);
     p.theta = theta; p.M = M; p.t0 = t0; p.dt = dt; p.t_max = t_max;
@@ -480,6 +486,11 @@ void oracle_dstd_forward(double tau_m, double tau_s, double theta, int M, double
                 for (int m = 0; m <= (q < 0 ? -1 : q); ++m)
                     va += fabs(kern(p.tv, p.ti, to - grid(t0, dt, m))) * wabs[m];
                 vabs[o] = va;
+            }
+            if (emass) {
+                double em = 0.0;
+                for (int m = 0; m <= (q < 0 ? M : q); ++m) em += wabs[m];
+                emass[o] = em;
             }
         }
         free(ev); free(wh); free(wabs);
@@ -530,19 +541,31 @@ void oracle_dstd_backward(double tau_m, double tau_s, double theta, int M, doubl
                           const double *grad_t_out,
                           int64_t n_isel, const int64_t *isel, double *grad_W,
                           int64_t n_bsel, const int64_t *bsel, double *grad_t_in,
-                          double *grad_W_abs, double *grad_t_in_abs) {
+                          double *grad_W_abs, double *grad_t_in_abs,
+                          const double *rho, const double *delta,
+                          double *grad_W_err, double *grad_t_in_err) {
     /* grad_W rows are computed for the n_isel neurons listed in isel (all when
        n_isel < 0) and stored as [n_isel][N_in]; grad_t_in rows likewise for the
        samples in bsel, stored as [n_bsel][N_in]. The optional *_abs outputs
        receive the sum of the absolute values of the terms of each gradient
-       element (its conditioning, used to judge rounding). */
+       element (its conditioning, used to judge rounding).
+       Error weights (test infrastructure): given per neuron a relative error
+       rho of the slope and an absolute error delta of the spike time, the
+       factor G[b,m,i] = gamma K(t - T_m) of a term moves by at most
+       |gamma| (rho K(t - T_m) + delta |K'(t - T_m)|) to first order. The
+       optional *_err outputs (rho, delta and both outputs given together)
+       receive each element's sum over its terms of that bound times the
+       term's other factors in absolute value. */
     prm_t p;
     canon(&p, tau_m, tau_s);
     p.theta = theta; p.M = M; p.t0 = t0; p.dt = dt; p.t_max = t_max;
     int64_t ni = n_isel < 0 ? N_out : n_isel;
     int64_t nb = n_bsel < 0 ? B : n_bsel;
+    int want_err = rho && delta;
+    size_t ng = (size_t)(B * N_out * (M + 1) > 0 ? B * N_out * (M + 1) : 1);
     ev_t *ev = (ev_t *)malloc(sizeof(ev_t) * (size_t)(B * N_in > 0 ? B * N_in : 1));
-    double *G = (double *)calloc((size_t)(B * N_out * (M + 1) > 0 ? B * N_out * (M + 1) : 1), sizeof(double));
+    double *G = (double *)calloc(ng, sizeof(double));
+    double *GE = want_err ? (double *)calloc(ng, sizeof(double)) : NULL;
 #pragma omp parallel for schedule(dynamic, 1)
     for (int64_t b = 0; b < B; ++b) {
         sample_events(&p, t_in + b * N_in, N_in, ev + b * N_in);
@@ -551,8 +574,13 @@ void oracle_dstd_backward(double tau_m, double tau_s, double theta, int M, doubl
             int q = q_idx[o];
             if (q < 0 || grad_t_out[o] == 0.0) continue;
             double gam = -grad_t_out[o] / slope[o];
-            for (int m = 0; m <= q; ++m)
-                G[o * (M + 1) + m] = gam * kern(p.tv, p.ti, t_out[o] - grid(t0, dt, m));
+            for (int m = 0; m <= q; ++m) {
+                double u = t_out[o] - grid(t0, dt, m);
+                G[o * (M + 1) + m] = gam * kern(p.tv, p.ti, u);
+                if (GE)
+                    GE[o * (M + 1) + m] = fabs(gam) * (rho[o] * fabs(kern(p.tv, p.ti, u)) +
+                                                       delta[o] * fabs(kern_dt(p.tv, p.ti, u)));
+            }
         }
     }
     if (grad_t_in) {
@@ -561,15 +589,18 @@ void oracle_dstd_backward(double tau_m, double tau_s, double theta, int M, doubl
             int64_t b = n_bsel < 0 ? r : bsel[r];
             for (int64_t j = 0; j < N_in; ++j) {
                 const ev_t *e = ev + b * N_in + j;
-                double acc = 0.0, aabs = 0.0;
+                double acc = 0.0, aabs = 0.0, aerr = 0.0;
                 for (int k = 0; k < e->n; ++k)
                     for (int64_t i = 0; i < N_out; ++i) {
-                        double term = G[(b * N_out + i) * (M + 1) + e->m[k]] * W[i * N_in + j] * e->ds[k];
+                        int64_t g = (b * N_out + i) * (M + 1) + e->m[k];
+                        double term = G[g] * W[i * N_in + j] * e->ds[k];
                         acc += term;
                         aabs += fabs(term);
+                        if (GE) aerr += GE[g] * fabs(W[i * N_in + j] * e->ds[k]);
                     }
                 grad_t_in[r * N_in + j] = acc;
                 if (grad_t_in_abs) grad_t_in_abs[r * N_in + j] = aabs;
+                if (GE && grad_t_in_err) grad_t_in_err[r * N_in + j] = aerr;
             }
         }
     }
@@ -578,22 +609,26 @@ void oracle_dstd_backward(double tau_m, double tau_s, double theta, int M, doubl
         for (int64_t r = 0; r < ni; ++r) {
             int64_t i = n_isel < 0 ? r : isel[r];
             for (int64_t j = 0; j < N_in; ++j) {
-                double acc = 0.0, aabs = 0.0;
+                double acc = 0.0, aabs = 0.0, aerr = 0.0;
                 for (int64_t b = 0; b < B; ++b) {
                     const ev_t *e = ev + b * N_in + j;
                     for (int k = 0; k < e->n; ++k) {
-                        double term = G[(b * N_out + i) * (M + 1) + e->m[k]] * e->s[k];
+                        int64_t g = (b * N_out + i) * (M + 1) + e->m[k];
+                        double term = G[g] * e->s[k];
                         acc += term;
                         aabs += fabs(term);
+                        if (GE) aerr += GE[g] * fabs(e->s[k]);
                     }
                 }
                 grad_W[r * N_in + j] = acc;
                 if (grad_W_abs) grad_W_abs[r * N_in + j] = aabs;
+                if (GE && grad_W_err) grad_W_err[r * N_in + j] = aerr;
             }
         }
     }
     free(ev);
     free(G);
+    free(GE);
 }
 
 /* ------------------------------------------------------------------------ */
@@ -644,7 +679,9 @@ static double kern_dt(double tv, double ti, double t) {
 void oracle_exact_forward(double tau_m, double tau_s, double theta, double t_max,
                           int64_t B, int64_t N_in, int64_t N_out,
                           const double *t_in, const double *W, double *t_out, double *slope,
-                          int32_t *k_out, double *margin, double *vabs) {
+                          int32_t *k_out, double *margin, double *vabs, double *emass) {
+    /* emass (optional): sum over the causal set of |w_j| (all finite inputs
+       for a silent neuron); with |K'| <= 1 it bounds the terms of the slope */
     double tv = fmax(tau_m, tau_s), ti = fmin(tau_m, tau_s);
 #pragma omp parallel for schedule(dynamic, 1)
     for (int64_t b = 0; b < B; ++b) {
@@ -656,7 +693,7 @@ void oracle_exact_forward(double tau_m, double tau_s, double theta, double t_max
                 if (isfinite(t)) { s[n].t = t; s[n].w = W[i * N_in + j]; ++n; }
             }
             qsort(s, (size_t)n, sizeof(tw_t), cmp_tw);
-            double to = INFINITY, sl = 0.0, pre = INFINITY, mg = INFINITY, va = 0.0;
+            double to = INFINITY, sl = 0.0, pre = INFINITY, mg = INFINITY, va = 0.0, em = 0.0;
             int32_t kk = -1;
             if (n > 0) {
                 piece_t pc;
@@ -675,13 +712,20 @@ void oracle_exact_forward(double tau_m, double tau_s, double theta, double t_max
                         mg = fmin(pre, fabs(peak - theta));
                         mg = fmin(mg, fabs(pv(&pc, lo) - theta));
                         if (!isinf(hi)) mg = fmin(mg, fabs(pv(&pc, hi) - theta));
-                        for (int64_t j = 0; j <= k; ++j) va += fabs(s[j].w * kern(tv, ti, root - s[j].t));
+                        for (int64_t j = 0; j <= k; ++j) {
+                            va += fabs(s[j].w * kern(tv, ti, root - s[j].t));
+                            em += fabs(s[j].w);
+                        }
                         break;
                     }
                     pre = fmin(pre, theta - peak);
                 }
             }
-            if (kk < 0) mg = pre;
+            if (kk < 0) {
+                mg = pre;
+                for (int64_t j = 0; j < n; ++j) em += fabs(s[j].w);
+            }
+            if (emass) emass[b * N_out + i] = em;
             t_out[b * N_out + i] = to;
             slope[b * N_out + i] = sl;
             if (k_out) k_out[b * N_out + i] = kk;
@@ -715,7 +759,17 @@ void oracle_exact_backward(double tau_m, double tau_s, int64_t B, int64_t N_in, 
                            const double *t_in, const double *W, const double *t_out,
                            const double *slope, const int32_t *k_idx, const double *grad_t_out,
                            double *grad_W, double *grad_t_in, double *grad_W_abs,
-                           double *grad_t_in_abs) {
+                           double *grad_t_in_abs, const double *rho, const double *delta,
+                           double *grad_W_err, double *grad_t_in_err) {
+    /* Error weights (test infrastructure; rho, delta [B][N_out] and both
+       outputs given together): with a relative slope error rho and a spike
+       time error delta, gamma K(t - t_j) moves by at most
+       |gamma| (rho K + delta |K'|) and gamma K'(t - t_j) by at most
+       |gamma| (rho |K'| + delta (1/tau_v + 1/tau_I)), the last factor bounding
+       |K''| on every row. *_err receive each element's sum of these bounds
+       times the term's other factors in absolute value. */
+    int want_err = rho && delta && grad_W_err && grad_t_in_err;
+    double k2 = 1.0 / fmax(tau_m, tau_s) + 1.0 / fmin(tau_m, tau_s);
     double tv = fmax(tau_m, tau_s), ti = fmin(tau_m, tau_s);
     double *gam = (double *)calloc((size_t)(B * N_out > 0 ? B * N_out : 1), sizeof(double));
     double *tl = (double *)calloc((size_t)(B * N_out > 0 ? B * N_out : 1), sizeof(double));
@@ -739,7 +793,7 @@ void oracle_exact_backward(double tau_m, double tau_s, int64_t B, int64_t N_in, 
 #pragma omp parallel for schedule(dynamic, 1)
         for (int64_t i = 0; i < N_out; ++i)
             for (int64_t j = 0; j < N_in; ++j) {
-                double acc = 0.0, aabs = 0.0;
+                double acc = 0.0, aabs = 0.0, aerr = 0.0;
                 for (int64_t b = 0; b < B; ++b) {
                     int64_t o = b * N_out + i;
                     double t = t_in[b * N_in + j];
@@ -747,26 +801,34 @@ void oracle_exact_backward(double tau_m, double tau_s, int64_t B, int64_t N_in, 
                     double term = gam[o] * kern(tv, ti, t_out[o] - t);
                     acc += term;
                     aabs += fabs(term);
+                    if (want_err)
+                        aerr += fabs(gam[o]) * (rho[o] * fabs(kern(tv, ti, t_out[o] - t)) +
+                                                delta[o] * fabs(kern_dt(tv, ti, t_out[o] - t)));
                 }
                 grad_W[i * N_in + j] = acc;
                 if (grad_W_abs) grad_W_abs[i * N_in + j] = aabs;
+                if (want_err) grad_W_err[i * N_in + j] = aerr;
             }
     }
     if (grad_t_in) {
 #pragma omp parallel for schedule(dynamic, 1)
         for (int64_t b = 0; b < B; ++b)
             for (int64_t j = 0; j < N_in; ++j) {
-                double acc = 0.0, aabs = 0.0, t = t_in[b * N_in + j];
+                double acc = 0.0, aabs = 0.0, aerr = 0.0, t = t_in[b * N_in + j];
                 if (isfinite(t))
                     for (int64_t i = 0; i < N_out; ++i) {
                         int64_t o = b * N_out + i;
                         if (gam[o] == 0.0 || !(t <= tl[o])) continue;
-                        double term = -gam[o] * W[i * N_in + j] * kern_dt(tv, ti, t_out[o] - t);
+                        double kd = kern_dt(tv, ti, t_out[o] - t);
+                        double term = -gam[o] * W[i * N_in + j] * kd;
                         acc += term;
                         aabs += fabs(term);
+                        if (want_err)
+                            aerr += fabs(gam[o] * W[i * N_in + j]) * (rho[o] * fabs(kd) + delta[o] * k2);
                     }
                 grad_t_in[b * N_in + j] = acc;
                 if (grad_t_in_abs) grad_t_in_abs[b * N_in + j] = aabs;
+                if (want_err) grad_t_in_err[b * N_in + j] = aerr;
             }
     }
     free(gam);
@@ -1046,7 +1108,9 @@ void oracle_conv_forward(double tau_m, double tau_s, double theta, int M, double
                          double t_max, int64_t B, int C_in, int H, int Wd, int C_out, int KH,
                          int KW, int stride, int pad, int pool,
                          const double *t_in, const double *W,
-                         double *t_out, double *slope, int32_t *q_idx, double *margin, double *vabs) {
+                         double *t_out, double *slope, int32_t *q_idx, double *margin, double *vabs,
+                         double *emass) {
+    /* margin, vabs and emass as for oracle_dstd_forward */
     prm_t p;
     canon(&p, tau_m, tau_s);
     p.theta = theta; p.M = M; p.t0 = t0; p.dt = dt; p.t_max = t_max;
@@ -1092,6 +1156,11 @@ void oracle_conv_forward(double tau_m, double tau_s, double theta, int M, double
                             va += fabs(kern(p.tv, p.ti, to - grid(t0, dt, m))) * wabs[m];
                         vabs[o] = va;
                     }
+                    if (emass) {
+                        double em = 0.0;
+                        for (int m = 0; m <= (q < 0 ? M : q); ++m) em += wabs[m];
+                        emass[o] = em;
+                    }
                 }
         free(ev); free(wh); free(wabs); free(ys); free(xs);
     }
@@ -1105,9 +1174,13 @@ void oracle_conv_backward(double tau_m, double tau_s, double theta, int M, doubl
                           const double *t_in, const double *W,
                           const double *t_out, const double *slope, const int32_t *q_idx,
                           const double *grad_t_out, double *grad_W, double *grad_t_in,
-                          double *grad_W_abs, double *grad_t_in_abs) {
+                          double *grad_W_abs, double *grad_t_in_abs,
+                          const double *rho, const double *delta,
+                          double *grad_W_err, double *grad_t_in_err) {
     /* The optional *_abs outputs (NULL to skip) receive, per gradient element,
-       the sum of the absolute values of its terms (its conditioning). */
+       the sum of the absolute values of its terms (its conditioning). The
+       optional error weights rho, delta [B][C_out][Ho][Wo] and *_err outputs
+       are those of oracle_dstd_backward (all four given together). */
     prm_t p;
     canon(&p, tau_m, tau_s);
     p.theta = theta; p.M = M; p.t0 = t0; p.dt = dt; p.t_max = t_max;
@@ -1121,10 +1194,13 @@ void oracle_conv_backward(double tau_m, double tau_s, double theta, int M, doubl
 #ifdef _OPENMP
     nth = omp_get_max_threads();
 #endif
+    int want_err = rho && delta && grad_W_err && grad_t_in_err;
     double *dWp = (double *)calloc((size_t)(nw * nth), sizeof(double));
     double *dWa = (double *)calloc((size_t)(nw * nth), sizeof(double));
+    double *dWe = (double *)calloc((size_t)(nw * nth), sizeof(double));
     memset(grad_t_in, 0, sizeof(double) * (size_t)(B * nin));
     if (grad_t_in_abs) memset(grad_t_in_abs, 0, sizeof(double) * (size_t)(B * nin));
+    if (want_err) memset(grad_t_in_err, 0, sizeof(double) * (size_t)(B * nin));
 #pragma omp parallel
     {
         int tid = 0;
@@ -1133,8 +1209,10 @@ void oracle_conv_backward(double tau_m, double tau_s, double theta, int M, doubl
 #endif
         double *dWl = dWp + (int64_t)tid * nw;
         double *dWal = dWa + (int64_t)tid * nw;
+        double *dWel = dWe + (int64_t)tid * nw;
         ev_t *ev = (ev_t *)malloc(sizeof(ev_t) * (size_t)nin);
         double *G = (double *)malloc(sizeof(double) * (size_t)(M + 1));
+        double *GE = (double *)malloc(sizeof(double) * (size_t)(M + 1));
         int *ys = (int *)malloc(sizeof(int) * (size_t)(H * Wd));
         int *xs = (int *)malloc(sizeof(int) * (size_t)(H * Wd));
 #pragma omp for schedule(dynamic, 1)
@@ -1142,6 +1220,7 @@ void oracle_conv_backward(double tau_m, double tau_s, double theta, int M, doubl
             sample_events(&p, t_in + b * nin, nin, ev);
             double *dt_row = grad_t_in + b * nin;
             double *dta_row = grad_t_in_abs ? grad_t_in_abs + b * nin : NULL;
+            double *dte_row = want_err ? grad_t_in_err + b * nin : NULL;
             for (int co = 0; co < C_out; ++co)
                 for (int oy = 0; oy < g.Ho; ++oy)
                     for (int ox = 0; ox < g.Wo; ++ox) {
@@ -1149,8 +1228,14 @@ void oracle_conv_backward(double tau_m, double tau_s, double theta, int M, doubl
                         int q = q_idx[o];
                         if (q < 0 || grad_t_out[o] == 0.0) continue;
                         double gam = -grad_t_out[o] / slope[o];
-                        for (int m = 0; m <= M; ++m)
-                            G[m] = (m <= q) ? gam * kern(p.tv, p.ti, t_out[o] - grid(t0, dt, m)) : 0.0;
+                        for (int m = 0; m <= M; ++m) {
+                            double u = t_out[o] - grid(t0, dt, m);
+                            G[m] = (m <= q) ? gam * kern(p.tv, p.ti, u) : 0.0;
+                            GE[m] = (m <= q && want_err)
+                                        ? fabs(gam) * (rho[o] * fabs(kern(p.tv, p.ti, u)) +
+                                                       delta[o] * fabs(kern_dt(p.tv, p.ti, u)))
+                                        : 0.0;
+                        }
                         for (int ci = 0; ci < C_in; ++ci)
                             for (int ky = 0; ky < KH; ++ky)
                                 for (int kx = 0; kx < KW; ++kx) {
@@ -1169,22 +1254,29 @@ void oracle_conv_backward(double tau_m, double tau_s, double theta, int M, doubl
                                             dWal[widx] += fabs(tw);
                                             dt_row[jin] += tt;
                                             if (dta_row) dta_row[jin] += fabs(tt);
+                                            if (want_err) {
+                                                dWel[widx] += GE[e->m[k]] * fabs(e->s[k]) / g.P;
+                                                dte_row[jin] += GE[e->m[k]] * fabs(w * e->ds[k]) / g.P;
+                                            }
                                         }
                                     }
                                 }
                     }
         }
-        free(ev); free(G); free(ys); free(xs);
+        free(ev); free(G); free(GE); free(ys); free(xs);
     }
     for (int64_t k = 0; k < nw; ++k) {
-        double s = 0.0, a = 0.0;
+        double s = 0.0, a = 0.0, e = 0.0;
         for (int t = 0; t < nth; ++t) {
             s += dWp[(int64_t)t * nw + k];
             a += dWa[(int64_t)t * nw + k];
+            e += dWe[(int64_t)t * nw + k];
         }
         grad_W[k] = s;
         if (grad_W_abs) grad_W_abs[k] = a;
+        if (want_err) grad_W_err[k] = e;
     }
     free(dWp);
     free(dWa);
+    free(dWe);
 }

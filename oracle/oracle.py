@@ -6,6 +6,7 @@ float64 arrays for finite-difference pins); results are float64.
 """
 from __future__ import annotations
 
+import contextlib
 import ctypes as C
 import os
 import subprocess
@@ -23,11 +24,17 @@ def build_oracle(force: bool = True) -> str:
     stale = (not os.path.exists(_LIB_PATH) or
              max(os.path.getmtime(f) for f in _SRC) > os.path.getmtime(_LIB_PATH))
     if force or stale:
-        cmd = ["gcc", "-O2", "-fopenmp", "-shared", "-fPIC", "-std=c11", "-Wall",
-               "-o", _LIB_PATH + ".tmp"] + _SRC + ["-lm"]
-        subprocess.run(cmd, check=True)
-        os.replace(_LIB_PATH + ".tmp", _LIB_PATH)
+        compile_oracle(_SRC[0], _LIB_PATH)
     return _LIB_PATH
+
+
+def compile_oracle(src: str, out: str) -> str:
+    """gcc -O2 -fopenmp, fp64, no fast-math: ``src`` -> shared library ``out``."""
+    cmd = ["gcc", "-O2", "-fopenmp", "-shared", "-fPIC", "-std=c11", "-Wall",
+           "-o", out + ".tmp", src, "-lm"]
+    subprocess.run(cmd, check=True)
+    os.replace(out + ".tmp", out)
+    return out
 
 
 _D = C.c_double
@@ -41,7 +48,24 @@ def _load():
     if _lib is not None:
         return _lib
     build_oracle(force=False)  # builds when missing or older than its source
-    lib = C.CDLL(_LIB_PATH)
+    _lib = _configure(C.CDLL(_LIB_PATH))
+    return _lib
+
+
+@contextlib.contextmanager
+def use_library(path):
+    """Bind this module to another build of the oracle for the duration of
+    the block (the mutation tests load copies with planted mistakes)."""
+    global _lib
+    saved = _load()
+    _lib = _configure(C.CDLL(path))
+    try:
+        yield
+    finally:
+        _lib = saved
+
+
+def _configure(lib):
     lib.oracle_kernel.restype = _D
     lib.oracle_kernel.argtypes = [_D, _D, _D]
     lib.oracle_kdstd.restype = _D
@@ -52,18 +76,19 @@ def _load():
     lib.oracle_dstd_events.argtypes = [_D, _D, _I, _D, _D, _L, _L, _P, _P, _P]
     lib.oracle_dstd_forward.restype = None
     lib.oracle_dstd_forward.argtypes = [_D, _D, _D, _I, _D, _D, _D, _L, _L, _L,
-                                        _P, _P, _P, _P, _P, _P, _P, _P]
+                                        _P, _P, _P, _P, _P, _P, _P, _P, _P]
     lib.oracle_dstd_scan.restype = None
     lib.oracle_dstd_scan.argtypes = [_D, _D, _D, _I, _D, _D, _D, _L, _L, _P,
                                      _P, _P, _P, _P, _P]
     lib.oracle_dstd_backward.restype = None
     lib.oracle_dstd_backward.argtypes = [_D, _D, _D, _I, _D, _D, _D, _L, _L, _L,
-                                         _P, _P, _P, _P, _P, _P, _L, _P, _P, _L, _P, _P, _P, _P]
+                                         _P, _P, _P, _P, _P, _P, _L, _P, _P, _L, _P, _P, _P, _P,
+                                         _P, _P, _P, _P]
     lib.oracle_exact_forward.restype = None
-    lib.oracle_exact_forward.argtypes = [_D, _D, _D, _D, _L, _L, _L, _P, _P, _P, _P, _P, _P, _P]
+    lib.oracle_exact_forward.argtypes = [_D, _D, _D, _D, _L, _L, _L, _P, _P, _P, _P, _P, _P, _P, _P]
     lib.oracle_exact_backward.restype = None
     lib.oracle_exact_backward.argtypes = [_D, _D, _L, _L, _L, _P, _P, _P, _P, _P, _P,
-                                          _P, _P, _P, _P]
+                                          _P, _P, _P, _P, _P, _P, _P, _P]
     lib.oracle_ms_forward.restype = None
     lib.oracle_ms_forward.argtypes = [_D, _D, _D, _I, _D, _D, _D, _L, _L, _L, _L, _L, _P, _P, _P,
                                       _P, _P, _P, _P, _P, _P]
@@ -73,14 +98,13 @@ def _load():
     lib.oracle_conv_forward.restype = None
     lib.oracle_conv_forward.argtypes = [_D, _D, _D, _I, _D, _D, _D, _L,
                                         _I, _I, _I, _I, _I, _I, _I, _I, _I,
-                                        _P, _P, _P, _P, _P, _P, _P]
+                                        _P, _P, _P, _P, _P, _P, _P, _P]
     lib.oracle_conv_backward.restype = None
     lib.oracle_conv_backward.argtypes = [_D, _D, _D, _I, _D, _D, _D, _L,
                                          _I, _I, _I, _I, _I, _I, _I, _I, _I,
-                                         _P, _P, _P, _P, _P, _P, _P, _P, _P, _P]
+                                         _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P]
     lib.oracle_num_threads.restype = _I
     lib.oracle_num_threads.argtypes = []
-    _lib = lib
     return lib
 
 
@@ -144,11 +168,12 @@ def dstd_forward(p, t_in, W, want_what=False):
     q = np.empty((B, N_out), dtype=np.int32)
     margin = np.empty((B, N_out))
     vabs = np.empty((B, N_out))
+    emass = np.empty((B, N_out))
     what = np.empty((B, M + 1, N_out)) if want_what else None
     _load().oracle_dstd_forward(*_pargs(p), B, N_in, N_out, _ptr(t_in), _ptr(W),
                                 _ptr(t_out), _ptr(slope), _ptr(q), _ptr(margin), _ptr(vabs),
-                                _ptr(what))
-    out = dict(t_out=t_out, slope=slope, q=q, margin=margin, vabs=vabs)
+                                _ptr(emass), _ptr(what))
+    out = dict(t_out=t_out, slope=slope, q=q, margin=margin, vabs=vabs, emass=emass)
     if want_what:
         out["what"] = what
     return out
@@ -170,12 +195,13 @@ def dstd_scan(p, what):
 
 
 def dstd_backward(p, t_in, W, fwd, grad_t_out, isel=None, bsel=None, want_dW=True, want_dt=True,
-                  want_abs=False):
+                  want_abs=False, err=None):
     """DSTD backward of a dense layer (implicit-function gradients).
 
     ``fwd`` is a dict with t_out, slope, q (the oracle's own forward outputs).
     Returns (grad_W rows, grad_t_in rows), plus (|terms| sums of each) when
-    ``want_abs``.
+    ``want_abs``, plus (error-weighted sums of each) when ``err`` = (rho, delta)
+    per neuron is given (see oracle_dstd_backward).
     """
     t_in = _f64(t_in)
     W = _f64(W)
@@ -193,14 +219,23 @@ def dstd_backward(p, t_in, W, fwd, grad_t_out, isel=None, bsel=None, want_dW=Tru
     dt = np.empty((nb, N_in)) if want_dt else None
     dWa = np.empty((ni, N_in)) if (want_dW and want_abs) else None
     dta = np.empty((nb, N_in)) if (want_dt and want_abs) else None
+    rho = delta = dWe = dte = None
+    if err is not None:
+        rho, delta = (np.ascontiguousarray(np.broadcast_to(a, (B, N_out)), dtype=np.float64)
+                      for a in err)
+        dWe = np.empty((ni, N_in)) if want_dW else None
+        dte = np.empty((nb, N_in)) if want_dt else None
     _load().oracle_dstd_backward(*_pargs(p), B, N_in, N_out, _ptr(t_in), _ptr(W), _ptr(t_out),
                                  _ptr(slope), _ptr(q), _ptr(g),
                                  -1 if isel is None else ni, _ptr(isel_a), _ptr(dW),
                                  -1 if bsel is None else nb, _ptr(bsel_a), _ptr(dt),
-                                 _ptr(dWa), _ptr(dta))
+                                 _ptr(dWa), _ptr(dta), _ptr(rho), _ptr(delta), _ptr(dWe), _ptr(dte))
+    out = (dW, dt)
     if want_abs:
-        return dW, dt, dWa, dta
-    return dW, dt
+        out = out + (dWa, dta)
+    if err is not None:
+        out = out + (dWe, dte)
+    return out
 
 
 def exact_forward(p, t_in, W):
@@ -216,16 +251,19 @@ def exact_forward(p, t_in, W):
     q = np.empty((B, N_out), dtype=np.int32)
     margin = np.empty((B, N_out))
     vabs = np.empty((B, N_out))
+    emass = np.empty((B, N_out))
     _load().oracle_exact_forward(float(p["tau_m"]), float(p["tau_s"]), float(p["threshold"]),
                                  float(p.get("t_max", np.inf)), B, N_in, N_out, _ptr(t_in), _ptr(W),
-                                 _ptr(t_out), _ptr(slope), _ptr(q), _ptr(margin), _ptr(vabs))
-    return dict(t_out=t_out, slope=slope, q=q, margin=margin, vabs=vabs)
+                                 _ptr(t_out), _ptr(slope), _ptr(q), _ptr(margin), _ptr(vabs),
+                                 _ptr(emass))
+    return dict(t_out=t_out, slope=slope, q=q, margin=margin, vabs=vabs, emass=emass)
 
 
-def exact_backward(p, t_in, W, fwd, grad_t_out):
+def exact_backward(p, t_in, W, fwd, grad_t_out, err=None):
     """Gradients of the exact spike times (implicit function theorem over the
     causal set of the crossing interval). fwd: dict with t_out, slope, q.
-    Returns grad_W [N_out, N_in], grad_t_in [B, N_in] and their |term| sums."""
+    Returns grad_W [N_out, N_in], grad_t_in [B, N_in] and their |term| sums,
+    and their error-weighted sums when ``err`` = (rho, delta) is given."""
     t_in = _f64(t_in)
     W = _f64(W)
     B, N_in = t_in.shape
@@ -238,10 +276,19 @@ def exact_backward(p, t_in, W, fwd, grad_t_out):
     gt = np.empty((B, N_in))
     gWa = np.empty((N_out, N_in))
     gta = np.empty((B, N_in))
+    rho = delta = gWe = gte = None
+    if err is not None:
+        rho, delta = (np.ascontiguousarray(np.broadcast_to(a, (B, N_out)), dtype=np.float64)
+                      for a in err)
+        gWe, gte = np.empty((N_out, N_in)), np.empty((B, N_in))
     _load().oracle_exact_backward(float(p["tau_m"]), float(p["tau_s"]), B, N_in, N_out,
                                   _ptr(t_in), _ptr(W), _ptr(t_out), _ptr(slope), _ptr(q), _ptr(g),
-                                  _ptr(gW), _ptr(gt), _ptr(gWa), _ptr(gta))
-    return dict(grad_W=gW, grad_t_in=gt, grad_W_abs=gWa, grad_t_in_abs=gta)
+                                  _ptr(gW), _ptr(gt), _ptr(gWa), _ptr(gta),
+                                  _ptr(rho), _ptr(delta), _ptr(gWe), _ptr(gte))
+    out = dict(grad_W=gW, grad_t_in=gt, grad_W_abs=gWa, grad_t_in_abs=gta)
+    if err is not None:
+        out.update(grad_W_err=gWe, grad_t_in_err=gte)
+    return out
 
 
 def ms_forward(p, t_in, W, F_out):
@@ -311,14 +358,16 @@ def conv_forward(p, cs, t_in, W):
     q = np.empty(shp, dtype=np.int32)
     margin = np.empty(shp)
     vabs = np.empty(shp)
+    emass = np.empty(shp)
     _load().oracle_conv_forward(*_pargs(p), B, *_conv_geom(cs), _ptr(t_in), _ptr(W), _ptr(t_out),
-                                _ptr(slope), _ptr(q), _ptr(margin), _ptr(vabs))
-    return dict(t_out=t_out, slope=slope, q=q, margin=margin, vabs=vabs)
+                                _ptr(slope), _ptr(q), _ptr(margin), _ptr(vabs), _ptr(emass))
+    return dict(t_out=t_out, slope=slope, q=q, margin=margin, vabs=vabs, emass=emass)
 
 
-def conv_backward(p, cs, t_in, W, fwd, grad_t_out, want_abs=False):
+def conv_backward(p, cs, t_in, W, fwd, grad_t_out, want_abs=False, err=None):
     """DSTD backward of a conv layer. Returns (grad_W, grad_t_in), plus the
-    per-element sums of |terms| of each when ``want_abs``."""
+    per-element sums of |terms| of each when ``want_abs``, plus the
+    error-weighted sums when ``err`` = (rho, delta) per output neuron is given."""
     t_in = _f64(t_in)
     W = _f64(W)
     t_out = np.ascontiguousarray(fwd["t_out"], dtype=np.float64)
@@ -330,9 +379,17 @@ def conv_backward(p, cs, t_in, W, fwd, grad_t_out, want_abs=False):
     dt = np.empty(t_in.shape)
     dWa = np.empty(W.shape) if want_abs else None
     dta = np.empty(t_in.shape) if want_abs else None
+    rho = delta = dWe = dte = None
+    if err is not None:
+        rho, delta = (np.ascontiguousarray(np.broadcast_to(a, t_out.shape), dtype=np.float64)
+                      for a in err)
+        dWe, dte = np.empty(W.shape), np.empty(t_in.shape)
     _load().oracle_conv_backward(*_pargs(p), B, *_conv_geom(cs), _ptr(t_in), _ptr(W), _ptr(t_out),
                                  _ptr(slope), _ptr(q), _ptr(g), _ptr(dW), _ptr(dt), _ptr(dWa),
-                                 _ptr(dta))
+                                 _ptr(dta), _ptr(rho), _ptr(delta), _ptr(dWe), _ptr(dte))
+    out = (dW, dt)
     if want_abs:
-        return dW, dt, dWa, dta
-    return dW, dt
+        out = out + (dWa, dta)
+    if err is not None:
+        out = out + (dWe, dte)
+    return out

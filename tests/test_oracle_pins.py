@@ -442,18 +442,30 @@ def test_conv_equals_dense_layer_with_conv_connectivity(cs):
     np.testing.assert_array_equal(fc["q"].reshape(B, -1), fd["q"])
     assert (fd["q"] >= 0).sum() > 0
     np.testing.assert_allclose(fc["t_out"].reshape(B, -1), fd["t_out"], atol=1e-12)
+    # conditioning outputs (pinned for dense layers in test_oracle_conditioning)
+    for k in ("margin", "vabs", "emass"):
+        np.testing.assert_allclose(fc[k].reshape(B, -1), fd[k], rtol=1e-10, atol=1e-13)
     g = rng.standard_normal(fc["t_out"].shape)
-    dWc, dtc, dWca, dtca = oracle.conv_backward(p, cs, t.reshape(B, cs["C_in"], cs["H"], cs["W"]),
-                                                Wc, fc, g, want_abs=True)
-    dWd, dtd, dWda, dtda = oracle.dstd_backward(p, t, Wd, fd, g.reshape(B, -1), want_abs=True)
+    rho = rng.random(g.shape) * 1e-3
+    delta = rng.random(g.shape) * 1e-4
+    dWc, dtc, dWca, dtca, dWce, dtce = oracle.conv_backward(
+        p, cs, t.reshape(B, cs["C_in"], cs["H"], cs["W"]), Wc, fc, g, want_abs=True, err=(rho, delta))
+    dWd, dtd, dWda, dtda, dWde, dtde = oracle.dstd_backward(
+        p, t, Wd, fd, g.reshape(B, -1), want_abs=True, err=(rho.reshape(B, -1), delta.reshape(B, -1)))
     np.testing.assert_allclose(dtc.reshape(B, -1), dtd, rtol=1e-10, atol=1e-12)
-    # each (output, input) pair is reached by one tap, so the |term| sums agree too
+    # each (output, input) pair is reached by one tap, so the |term| and the
+    # error-weighted sums agree too
     np.testing.assert_allclose(dtca.reshape(B, -1), dtda, rtol=1e-10, atol=1e-12)
+    np.testing.assert_allclose(dtce.reshape(B, -1), dtde, rtol=1e-10, atol=1e-15)
     ref = np.zeros(Wc.size)
     ref_abs = np.zeros(Wc.size)
+    ref_err = np.zeros(Wc.size)
     for o, j, wi, fac in idx:
         ref[wi] += dWd[o, j] * fac
         ref_abs[wi] += dWda[o, j] * fac
+        ref_err[wi] += dWde[o, j] * fac
     np.testing.assert_allclose(dWc.reshape(-1), ref, rtol=1e-10, atol=1e-12)
     np.testing.assert_allclose(dWca.reshape(-1), ref_abs, rtol=1e-10, atol=1e-12)
+    np.testing.assert_allclose(dWce.reshape(-1), ref_err, rtol=1e-10, atol=1e-15)
+    assert (dWce > 0).any()
     assert (dWca.reshape(-1) >= np.abs(dWc.reshape(-1)) - 1e-15).all()

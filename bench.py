@@ -11,7 +11,7 @@ Prints ONE JSON line (rank 0) with the throughput in samples/s, the roofline
 of the dominant kernel (timed with the library's hipEvent timer on the stream
 the kernels run on) and the fp64 CPU oracle timed on the host as a baseline.
 
-  python bench.py [--steps K] [--warmup W] [--workload mlp3]
+  python bench.py [--steps K] [--warmup W] [--workload conv9] [--no-configs]
 """
 from __future__ import annotations
 
@@ -584,7 +584,14 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--workload", default="mlp3")
+    ap.add_argument("--workload", default="conv9",
+                    help="the timed headline workload (default: the 9-layer conv net, the "
+                         "largest single-GPU configuration)")
+    ap.add_argument("--configs", default="dense1,dense1-cal,mlp3,wide-M8,wide-M32,wide-M64,"
+                                         "wide-M128,conv20",
+                    help="further workloads timed after the headline, reported in detail.configs")
+    ap.add_argument("--config-steps", type=int, default=50)
+    ap.add_argument("--no-configs", action="store_true")
     ap.add_argument("--profile-steps", type=int, default=20)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--eager", action="store_true",
@@ -627,48 +634,8 @@ def main():
                           "rows": multispike_bench(torch, dstd, dev)}), flush=True)
         return
     wl = workloads.get(args.workload)
-    net = Net(wl, dev)
-
-    run = net.step
-    if not args.eager:
-        graph = net.capture()
-        run = graph.replay
-    for _ in range(args.warmup):
-        run()
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        run()
-    torch.cuda.synchronize()
-    elapsed = time.perf_counter() - t0
-    ms = 1e3 * elapsed / max(args.steps, 1)
-    value = wl.batch * args.steps / elapsed
-
-    # per-kernel durations with the library's hipEvent timer (separate pass)
-    act = net.activity()
-    dstd.dstd_profile_reset()
-    dstd.dstd_profile_enable(True)
-    for _ in range(args.profile_steps):
-        net.step()
-    torch.cuda.synchronize()
-    dstd.dstd_profile_enable(False)
-    prof = dstd.profile_table()
-    per_step = {k: v[1] / args.profile_steps for k, v in prof.items()}
-    launches = {k: v[0] / args.profile_steps for k, v in prof.items()}
-    dom = max(per_step, key=per_step.get)
-    flops = kernel_algorithmic_flops(net, act)
-    sha = kernel_source_sha()
-    roof = None
-    if dom in flops:
-        achieved = flops[dom] / (per_step[dom] * 1e-3) / 1e12
-        n_launch = launches[dom]
-        roof = dict(bound="alu", achieved=round(achieved, 3), peak=PEAK_FP32_VECTOR_TFLOPS,
-                    unit="TFLOP/s", frac=round(achieved / PEAK_FP32_VECTOR_TFLOPS, 4),
-                    traffic=traffic_for(dom, args.workload, sha), traffic_unit="bytes per launch",
-                    kernel=dom, launches_per_step=n_launch,
-                    avg_launch_ms=round(per_step[dom] / n_launch, 4),
-                    algorithmic_flops_per_launch=round(flops[dom] / n_launch),
-                    kernel_ms_per_step=round(per_step[dom], 4))
+    head = measure(torch, dstd, wl, dev, args.steps, args.warmup, args.profile_steps, args.eager)
+    net = head.pop("net")
 
     if args.copy_probe:
         a = torch.empty(64 << 20, dtype=torch.float32, device=dev)
@@ -678,23 +645,106 @@ def main():
         torch.cuda.synchronize()
 
     per_layer = layer_profile(net, dstd, torch) if args.layer_profile else None
+    loss = float(net.loss[0].cpu())
+    del net
+    others = []
+    if not args.no_configs:
+        for name in [x for x in args.configs.split(",") if x and x != args.workload]:
+            r = measure(torch, dstd, workloads.get(name), dev, args.config_steps,
+                        max(3, args.config_steps // 5), 5, args.eager)
+            r.pop("net")
+            others.append(dict(workload=name, description=workloads.get(name).description,
+                               batch=workloads.get(name).batch, value=r["value"], unit="samples/s",
+                               ms_per_step=r["ms_per_step"], roofline=r["roofline"],
+                               hbm_kernels=r["hbm_kernels"],
+                               kernel_ms_per_step=r["kernel_ms_per_step"]))
+            print(json.dumps(dict(config=name, value=r["value"], ms_per_step=r["ms_per_step"])),
+                  file=sys.stderr, flush=True)
+            torch.cuda.empty_cache()
     cpu = None if args.no_cpu_baseline else cpu_baseline(wl)
     out = {
-        "metric": METRIC, "value": round(value, 1), "unit": "samples/s", "n_gpus": 1,
-        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4),
+        "metric": METRIC, "value": head["value"], "unit": "samples/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": head["ms_per_step"],
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
         "data": "synthetic (seeded uniform spike times; calibrated random weights)",
         "config": {"workload": wl.description, "name": wl.name, "global_batch": wl.batch,
-                   "layers": [layer_desc(e["lay"]) for e in net.L],
+                   "layers": [layer_desc(lay) for lay in wl.layers],
                    "parallelism": "single GPU",
                    "execution": "eager launches" if args.eager else "HIP graph of the step"},
-        "roofline": roof,
+        "roofline": head["roofline"],
         "cpu_baseline": cpu,
-        "detail": {"kernel_ms_per_step": {k: round(v, 4) for k, v in sorted(per_step.items())},
-                   "launches_per_step": launches, "activity": act, "kernel_source_sha": sha,
-                   "loss": float(net.loss[0].cpu()), "per_layer_ms": per_layer},
+        "detail": {"kernel_ms_per_step": head["kernel_ms_per_step"],
+                   "launches_per_step": head["launches_per_step"], "activity": head["activity"],
+                   "hbm_kernels": head["hbm_kernels"],
+                   "kernel_source_sha": head["kernel_source_sha"],
+                   "loss": loss, "per_layer_ms": per_layer, "configs": others},
     }
     print(json.dumps(out), flush=True)
+
+
+def measure(torch, dstd, wl, dev, steps, warmup, profile_steps, eager):
+    """Time `steps` whole training steps of workload `wl` (HIP graph replays
+    unless eager), then one profiling pass with the library's hipEvent timer:
+    samples/s, per-kernel ms per step, the dominant kernel's roofline and the
+    HBM rate of the bandwidth-bound kernels that have committed counters."""
+    net = Net(wl, dev)
+    run = net.step
+    if not eager:
+        graph = net.capture()
+        run = graph.replay
+    for _ in range(warmup):
+        run()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        run()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    ms = 1e3 * elapsed / max(steps, 1)
+    value = wl.batch * steps / elapsed
+
+    # per-kernel durations with the library's hipEvent timer (separate pass)
+    act = net.activity()
+    dstd.dstd_profile_reset()
+    dstd.dstd_profile_enable(True)
+    for _ in range(profile_steps):
+        net.step()
+    torch.cuda.synchronize()
+    dstd.dstd_profile_enable(False)
+    prof = dstd.profile_table()
+    per_step = {k: v[1] / profile_steps for k, v in prof.items()}
+    launches = {k: v[0] / profile_steps for k, v in prof.items()}
+    flops = kernel_algorithmic_flops(net, act)
+    sha = kernel_source_sha()
+    # the dominant contraction kernel (the step's largest kernel is one of them)
+    cand = {k: v for k, v in per_step.items() if k in flops and flops[k] > 0}
+    dom = max(cand, key=cand.get) if cand else None
+    roof = None
+    if dom is not None:
+        achieved = flops[dom] / (per_step[dom] * 1e-3) / 1e12
+        n_launch = launches[dom]
+        roof = dict(bound="alu", achieved=round(achieved, 3), peak=PEAK_FP32_VECTOR_TFLOPS,
+                    unit="TFLOP/s", frac=round(achieved / PEAK_FP32_VECTOR_TFLOPS, 4),
+                    traffic=traffic_for(dom, wl.name, sha), traffic_unit="bytes per launch",
+                    kernel=dom, launches_per_step=n_launch,
+                    avg_launch_ms=round(per_step[dom] / n_launch, 4),
+                    algorithmic_flops_per_launch=round(flops[dom] / n_launch),
+                    kernel_ms_per_step=round(per_step[dom], 4),
+                    largest_kernel=max(per_step, key=per_step.get))
+    hbm = {}
+    for k, v in per_step.items():
+        if k in flops:
+            continue
+        b = traffic_for(k, wl.name, sha)
+        if b is None:
+            continue
+        gbs = b * launches[k] / (v * 1e-3) / 1e9
+        hbm[k] = dict(bytes_per_launch=b, ms_per_step=round(v, 4), achieved_GBs=round(gbs, 1),
+                      frac=round(gbs / PEAK_HBM_GBS, 4))
+    return dict(net=net, value=round(value, 1), ms_per_step=round(ms, 4), roofline=roof,
+                kernel_ms_per_step={k: round(v, 4) for k, v in sorted(per_step.items())},
+                launches_per_step=launches, activity=act, hbm_kernels=hbm,
+                kernel_source_sha=sha)
 
 
 if __name__ == "__main__":

@@ -15,6 +15,7 @@ from .oracle import (  # noqa: F401
     dstd_scan,
     dstd_backward,
     exact_forward,
+    conv_out_hw,
     exact_backward,
     ms_forward,
     ms_backward,

@@ -7,7 +7,7 @@ import pytest
 
 import oracle
 from paper_2607_14672_amd import workloads as wl
-from tests.parity import check_forward, check_grad, near_grid
+from tests.parity import check_forward, check_grad, grad_err_inputs, near_grid
 
 pytestmark = pytest.mark.gpu
 
@@ -90,21 +90,40 @@ def _window(p):
     return p["M"] * p["dt"]
 
 
+def _taus(p):
+    return (max(p["tau_m"], p["tau_s"]), min(p["tau_m"], p["tau_s"]))
+
+
+def _n_terms(cs, B):
+    """Upper bounds of the number of terms of a dW and of a dt_in element."""
+    Ho, Wo = oracle.conv_out_hw(cs)
+    P = {1: 1, 2: 4, 0: cs["H"] * cs["W"]}[cs["pool_in"]]
+    return 2 * B * Ho * Wo * P, 2 * cs["C_out"] * cs["KH"] * cs["KW"]
+
+
+def _conv_grad_check(p, cs, t, W, orc, mask, st, g_sel, gW, gx_sel, label):
+    """Oracle backward on the (sampled) images t with upstream gradient
+    g_sel, error-weighted sums from the forward's error model, and the
+    per-element checks of dW and dt_in."""
+    oW, ox, oWa, oxa, oWe, oxe = oracle.conv_backward(
+        p, cs, t, W, orc, np.where(orc["q"] >= 0, g_sel.astype(np.float64), 0.0), want_abs=True,
+        err=grad_err_inputs(st, mask))
+    nW, nx = _n_terms(cs, t.shape[0])
+    check_grad(gW, oW, label + " dW", oWa, oWe, n_terms=nW)
+    if gx_sel is not None:
+        kink = near_grid(t, p)
+        check_grad(gx_sel[~kink], ox[~kink], label + " dt_in", oxa[~kink], oxe[~kink], n_terms=nx)
+
+
 def _conv_parity(dev, p, cs, t, W, label, bf16=False, need_t=True, seed=0):
     Wq = wl.bf16_round(W) if bf16 else W
     gpu, h = _gpu_forward(dev, p, cs, t, Wq, bf16=bf16)
     orc = oracle.conv_forward(p, cs, t, Wq)
-    mask, stats = check_forward(gpu, orc, None, _window(p), label=label)
+    mask, stats = check_forward(gpu, orc, None, _window(p), label=label, taus=_taus(p))
     g = np.random.default_rng(seed + 99).standard_normal(orc["t_out"].shape)
     g = np.where(mask, 0.0, g).astype(np.float32)
     gW, gx = _gpu_backward(dev, h, g, need_t=need_t)
-    oW, ox, oWa, oxa = oracle.conv_backward(p, cs, t, Wq, orc,
-                                            np.where(orc["q"] >= 0, g.astype(np.float64), 0.0),
-                                            want_abs=True)
-    check_grad(gW, oW, label + " dW", oWa)
-    if need_t:
-        kink = near_grid(t, p)
-        check_grad(gx[~kink], ox[~kink], label + " dt_in", oxa[~kink])
+    _conv_grad_check(p, cs, t, Wq, orc, mask, stats, g, gW, gx if need_t else None, label)
     return gpu, orc, stats
 
 
@@ -120,6 +139,11 @@ CASES = [
     ("1x1 no pool", 7, 3, _cs(20, 5, 6, 12, K=1, pad=0), 10, 0.3, 1.0, 6.0),
     ("3x1 kernel, pad 0", 8, 2, _cs(9, 6, 7, 15, K=3, KW=1, pad=0), 9, 1.0, 0.3, 7.0),
     ("pool + stride 2 + M 64", 9, 2, _cs(12, 12, 8, 24, stride=2, pool_in=2), 64, 1.0, 0.3, 7.0),
+    # channel counts of the deep conv layers: 129-256 and > 256 output channels
+    ("256 channels", 16, 2, _cs(24, 5, 6, 256), 32, 1.0, 0.3, 7.0),
+    ("200 channels (ragged tile)", 17, 2, _cs(20, 6, 8, 200, pool_in=2), 16, 1.0, 0.3, 7.0),
+    ("300 channels", 18, 2, _cs(16, 4, 5, 300), 16, 1.5, 0.5, 7.0),
+    ("3 input channels, 64 out", 19, 2, _cs(3, 12, 10, 64), 32, 1.0, 0.3, 7.0),
 ]
 
 
@@ -195,9 +219,18 @@ def _layer_inputs(lay, B, seed):
 
 
 @pytest.mark.parametrize("name,l,B,k", [
+    ("conv9", 0, 4, 7.0),    # 3 -> 64 at 32 x 32 (fan-in 27)
     ("conv9", 1, 4, 7.0),    # 64 -> 64 at 32 x 32
     ("conv9", 2, 4, 7.0),    # 2x2 event pool, 64 -> 128 at 16 x 16
+    ("conv9", 3, 4, 7.0),    # 128 -> 128 at 16 x 16
+    ("conv9", 4, 4, 7.0),    # 2x2 event pool, 128 -> 256 at 8 x 8
+    ("conv9", 5, 4, 7.0),    # 256 -> 256 at 8 x 8 (fan-in 2304)
+    ("conv9", 6, 6, 7.0),    # 2x2 event pool, 256 -> 256 at 4 x 4
+    ("conv9", 7, 6, 7.0),    # 256 -> 256 at 4 x 4
+    ("conv20", 0, 4, 7.0),   # 1 -> 32 at 28 x 28 (fan-in 9)
     ("conv20", 5, 8, 7.0),   # stride 2, 32 -> 32, 28 x 28 -> 14 x 14
+    ("conv20", 10, 8, 7.0),  # 32 -> 64 at 14 x 14
+    ("conv20", 12, 8, 7.0),  # stride 2, 64 -> 64, 14 x 14 -> 7 x 7
     ("conv20", 19, 16, 6.0), # global event pool of 7 x 7 x 64, dense 64 -> 10
 ])
 def test_workload_layer_shapes(dev, name, l, B, k):
@@ -228,17 +261,39 @@ def test_conv9_layer2_full_batch_sampled(dev):
     t = _layer_inputs(lay, w.batch, 8)
     gpu, h = _gpu_forward(dev, lay.params(), cs, t, W)
     bsel = np.array([0, 31, 63])
-    orc = oracle.conv_forward(lay.params(), cs, t[bsel], W)
-    mask, _ = check_forward({k: v[bsel] for k, v in gpu.items()}, orc, None, 1.0,
-                            label="conv9 layer 2 sampled images")
+    p = lay.params()
+    orc = oracle.conv_forward(p, cs, t[bsel], W)
+    mask, st = check_forward({k: v[bsel] for k, v in gpu.items()}, orc, None, 1.0,
+                             label="conv9 layer 2 sampled images", taus=_taus(p))
     g = np.zeros(gpu["t_out"].shape, dtype=np.float32)
     g[bsel] = np.where(mask, 0.0, rng.standard_normal(orc["t_out"].shape)).astype(np.float32)
     gW, gx = _gpu_backward(dev, h, g)
-    oW, ox, oWa, oxa = oracle.conv_backward(lay.params(), cs, t[bsel], W, orc,
-                                            np.where(orc["q"] >= 0, g[bsel].astype(np.float64), 0.0),
-                                            want_abs=True)
-    check_grad(gW, oW, "conv9 layer 2 dW (sampled images)", oWa)
-    kink = near_grid(t[bsel], lay.params())
-    check_grad(gx[bsel][~kink], ox[~kink], "conv9 layer 2 dt_in", oxa[~kink])
+    _conv_grad_check(p, cs, t[bsel], W, orc, mask, st, g[bsel], gW, gx[bsel],
+                     "conv9 layer 2 (sampled images)")
     others = np.setdiff1d(np.arange(w.batch), bsel)
     assert np.all(gx[others] == 0.0)
+
+
+@pytest.mark.parametrize("l,bsel", [(4, (0, 40, 63)), (6, (5, 62))])
+def test_conv9_deep_layer_full_batch_sampled(dev, l, bsel):
+    """conv9 layers 5 (pool, 128 -> 256 at 8 x 8) and 7 (pool, 256 -> 256 at
+    4 x 4) at the full batch of 64 on the GPU, the launch configuration of
+    the timed step; the oracle checks the sampled images."""
+    w = wl.get("conv9")
+    lay = w.layers[l]
+    cs = lay.conv_shape()
+    rng = np.random.default_rng(70 + l)
+    fan = lay.C_in * lay.KH * lay.KW
+    W = ((7.0 / fan) * (1 + 0.3 * math.sqrt(fan) * rng.standard_normal(lay.w_shape()))).astype(np.float32)
+    t = _layer_inputs(lay, w.batch, 80 + l)
+    gpu, h = _gpu_forward(dev, lay.params(), cs, t, W)
+    bsel = np.array(bsel)
+    p = lay.params()
+    orc = oracle.conv_forward(p, cs, t[bsel], W)
+    mask, st = check_forward({k: v[bsel] for k, v in gpu.items()}, orc, None, 1.0,
+                             label=f"conv9 layer {l + 1} sampled images", taus=_taus(p))
+    g = np.zeros(gpu["t_out"].shape, dtype=np.float32)
+    g[bsel] = np.where(mask, 0.0, rng.standard_normal(orc["t_out"].shape)).astype(np.float32)
+    gW, gx = _gpu_backward(dev, h, g)
+    _conv_grad_check(p, cs, t[bsel], W, orc, mask, st, g[bsel], gW, gx[bsel],
+                     f"conv9 layer {l + 1} (sampled images)")

@@ -6,7 +6,7 @@ import pytest
 
 import oracle
 from paper_2607_14672_amd import workloads as wl
-from tests.parity import check_forward, check_grad, near_grid
+from tests.parity import check_forward, check_grad, grad_err_inputs, near_grid
 
 pytestmark = pytest.mark.gpu
 
@@ -49,6 +49,10 @@ def _window(p):
     return p["M"] * p["dt"]
 
 
+def _taus(p):
+    return (max(p["tau_m"], p["tau_s"]), min(p["tau_m"], p["tau_s"]))
+
+
 def _layer_case(seed, B, N_in, N_out, M, tm, ts, k=6.0, t0=0.0, t_max=math.inf, spread=1.0):
     rng = np.random.default_rng(seed)
     p = dict(tau_m=tm, tau_s=ts, threshold=1.0, M=M, t0=t0, dt=1.0 / M, t_max=t_max)
@@ -76,17 +80,19 @@ def _fwd_bwd_parity(dev, p, t, W, label, bf16=False, need_t=True, seed=0):
     Wq = wl.bf16_round(W) if bf16 else W
     gpu, h = _gpu_forward(dev, p, t, Wq, bf16=bf16)
     orc = oracle.dstd_forward(p, t, Wq)
-    mask, _ = check_forward(gpu, orc, t.shape[1], _window(p), label=label)
+    mask, st = check_forward(gpu, orc, t.shape[1], _window(p), label=label, taus=_taus(p))
     g = np.random.default_rng(seed + 99).standard_normal(orc["t_out"].shape)
     g = np.where(mask, 0.0, g).astype(np.float32)
     gW, gx = _gpu_backward(dev, h, g, need_t=need_t)
     g64 = g.astype(np.float64)
-    oW, ox, oWa, oxa = oracle.dstd_backward(p, t, Wq, orc, np.where(orc["q"] >= 0, g64, 0.0),
-                                            want_dt=need_t, want_abs=True)
-    check_grad(gW, oW, label + " dW", oWa)
+    oW, ox, oWa, oxa, oWe, oxe = oracle.dstd_backward(
+        p, t, Wq, orc, np.where(orc["q"] >= 0, g64, 0.0), want_dt=need_t, want_abs=True,
+        err=grad_err_inputs(st, mask))
+    B, N_out = orc["q"].shape
+    check_grad(gW, oW, label + " dW", oWa, oWe, n_terms=2 * B)
     if need_t:
         kink = near_grid(t, p)
-        check_grad(gx[~kink], ox[~kink], label + " dt_in", oxa[~kink])
+        check_grad(gx[~kink], ox[~kink], label + " dt_in", oxa[~kink], oxe[~kink], n_terms=2 * N_out)
     return gpu, orc
 
 
@@ -126,7 +132,7 @@ def test_single_input_and_silent_layer(dev):
     W = np.array([[1.2 / kmax], [0.8 / kmax]], dtype=np.float32)
     gpu, _ = _gpu_forward(dev, p, t, W)
     orc = oracle.dstd_forward(p, t, W)
-    check_forward(gpu, orc, 1, 1.0, label="single input")
+    check_forward(gpu, orc, 1, 1.0, label="single input", taus=_taus(p))
     assert gpu["q"][1, 0] == -1 and gpu["q"][1, 1] == -1
     assert gpu["q"][0, 1] == -1 and gpu["q"][0, 0] >= 0
 
@@ -168,7 +174,7 @@ def test_dense1_as_stated_is_silent(dev):
     W = d.weights(0)
     gpu, _ = _gpu_forward(dev, lay.params(), d.t_in, W)
     orc = oracle.dstd_forward(lay.params(), d.t_in, W)
-    check_forward(gpu, orc, lay.n_in, 1.0, label="dense1 as stated")
+    check_forward(gpu, orc, lay.n_in, 1.0, label="dense1 as stated", taus=_taus(lay.params()))
     assert (orc["q"] < 0).all() and (gpu["q"] < 0).all()
 
 
@@ -192,6 +198,22 @@ def test_mlp3_layers_teacher_forced(dev):
         t = orc["t_out"].astype(np.float32)
 
 
+def test_conv9_dense_head(dev):
+    """The dense output layer of the 9-layer conv workload at its full batch
+    (4096 -> 10, B 64, M 32), with in-window inputs. (The 20-layer workload's
+    head is a conv layer with global event pooling, tested with the conv
+    layers.)"""
+    name, l = "conv9", 8
+    w = wl.get(name)
+    lay = w.layers[l]
+    p = lay.params()
+    rng = np.random.default_rng(300 + l)
+    t = (lay.t0 + rng.random((w.batch, lay.n_in))).astype(np.float32)
+    W = ((6.0 / lay.n_in) * (1 + 0.3 * math.sqrt(lay.n_in) *
+                              rng.standard_normal((lay.n_out, lay.n_in)))).astype(np.float32)
+    _fwd_bwd_parity(dev, p, t, W, f"{name} dense head {lay.n_in}->{lay.n_out}", seed=l)
+
+
 @pytest.mark.parametrize("M", [8, 32, 64, 128])
 def test_wide_layer_full_size_sampled(dev, M):
     """Full 256 x 4096 -> 4096 layer on the GPU; oracle on sampled rows: all
@@ -210,11 +232,11 @@ def test_wide_layer_full_size_sampled(dev, M):
     isel = np.array([0, 1, 999, 2048, 3071, 4000, 4094, 4095])
     # sampled forward + masks from the oracle
     orc_b = oracle.dstd_forward(p, d.t_in[bsel], W)
-    mask_b, _ = check_forward({k: v[bsel] for k, v in gpu.items()}, orc_b, lay.n_in, 1.0,
-                              label=f"wide M={M} rows")
+    mask_b, st_b = check_forward({k: v[bsel] for k, v in gpu.items()}, orc_b, lay.n_in, 1.0,
+                                 label=f"wide M={M} rows", taus=_taus(p))
     orc_i = oracle.dstd_forward(p, d.t_in, W[isel])
-    mask_i, _ = check_forward({k: v[:, isel] for k, v in gpu.items()}, orc_i, lay.n_in, 1.0,
-                              label=f"wide M={M} cols")
+    mask_i, st_i = check_forward({k: v[:, isel] for k, v in gpu.items()}, orc_i, lay.n_in, 1.0,
+                                 label=f"wide M={M} cols", taus=_taus(p))
     # full-batch mask for the GPU side: zero g wherever either sample found an
     # excluded neuron; neurons never sampled keep their g (they only enter the
     # sampled dt_in rows through their own sample, whose full row is checked)
@@ -223,15 +245,17 @@ def test_wide_layer_full_size_sampled(dev, M):
     gm[:, isel] = np.where(mask_i, 0.0, gm[:, isel])
     gm = gm.astype(np.float32)
     gW, gx = _gpu_backward(dev, h, gm)
-    oW, _, oWa, _ = oracle.dstd_backward(p, d.t_in, W[isel], orc_i,
-                                         np.where(orc_i["q"] >= 0, gm[:, isel].astype(np.float64), 0.0),
-                                         want_dt=False, want_abs=True)
-    check_grad(gW[isel], oW, f"wide M={M} dW rows", oWa)
-    _, ox, _, oxa = oracle.dstd_backward(p, d.t_in[bsel], W, orc_b,
-                                         np.where(orc_b["q"] >= 0, gm[bsel].astype(np.float64), 0.0),
-                                         want_dW=False, want_abs=True)
+    oW, _, oWa, _, oWe, _ = oracle.dstd_backward(
+        p, d.t_in, W[isel], orc_i, np.where(orc_i["q"] >= 0, gm[:, isel].astype(np.float64), 0.0),
+        want_dt=False, want_abs=True, err=grad_err_inputs(st_i, mask_i))
+    B = d.t_in.shape[0]
+    check_grad(gW[isel], oW, f"wide M={M} dW rows", oWa, oWe, n_terms=2 * B)
+    _, ox, _, oxa, _, oxe = oracle.dstd_backward(
+        p, d.t_in[bsel], W, orc_b, np.where(orc_b["q"] >= 0, gm[bsel].astype(np.float64), 0.0),
+        want_dW=False, want_abs=True, err=grad_err_inputs(st_b, mask_b))
     kink = near_grid(d.t_in[bsel], p)
-    check_grad(gx[bsel][~kink], ox[~kink], f"wide M={M} dt_in rows", oxa[~kink])
+    check_grad(gx[bsel][~kink], ox[~kink], f"wide M={M} dt_in rows", oxa[~kink], oxe[~kink],
+               n_terms=2 * W.shape[0])
     del torch
 
 

@@ -7,7 +7,7 @@ import pytest
 
 import oracle
 from paper_2607_14672_amd import workloads as wl
-from tests.parity import check_forward, check_grad
+from tests.parity import check_forward, check_grad, grad_err_inputs
 
 pytestmark = pytest.mark.gpu
 
@@ -94,6 +94,10 @@ def _special(t, rng):
     return t.astype(np.float32)
 
 
+def _taus(p):
+    return (max(p["tau_m"], p["tau_s"]), min(p["tau_m"], p["tau_s"]))
+
+
 def _max_ambiguous(orc, n_in, window):
     """Bound on the share of the ambiguity set for the exact path. Besides
     near-tangent crossings (as for DSTD), the margin counts |v - V_th| at the
@@ -113,14 +117,17 @@ def _parity(dev, p, t, W, label, bf16=False, seed=0, window=1.0):
     Wq = wl.bf16_round(W) if bf16 else W
     gpu, h = _gpu_forward(dev, p, t, Wq, bf16=bf16)
     orc = oracle.exact_forward(p, t, Wq)
-    mask, stats = check_forward(gpu, orc, t.shape[1], window, label=label,
+    mask, stats = check_forward(gpu, orc, t.shape[1], window, label=label, taus=_taus(p),
                                 max_ambiguous=_max_ambiguous(orc, t.shape[1], window))
     g = np.random.default_rng(seed + 7).standard_normal(orc["t_out"].shape)
     g = np.where(mask, 0.0, g).astype(np.float32)
     gW, gx = _gpu_backward(dev, h, g)
-    ob = oracle.exact_backward(p, t, Wq, orc, np.where(orc["q"] >= 0, g.astype(np.float64), 0.0))
-    check_grad(gW, ob["grad_W"], label + " dW", ob["grad_W_abs"])
-    check_grad(gx, ob["grad_t_in"], label + " dt_in", ob["grad_t_in_abs"])
+    ob = oracle.exact_backward(p, t, Wq, orc, np.where(orc["q"] >= 0, g.astype(np.float64), 0.0),
+                               err=grad_err_inputs(stats, mask))
+    B, N_out = orc["q"].shape
+    check_grad(gW, ob["grad_W"], label + " dW", ob["grad_W_abs"], ob["grad_W_err"], n_terms=B)
+    check_grad(gx, ob["grad_t_in"], label + " dt_in", ob["grad_t_in_abs"], ob["grad_t_in_err"],
+               n_terms=N_out)
     return gpu, orc, stats
 
 
@@ -182,14 +189,16 @@ def test_exact_bench_size_sampled(dev):
     ts = t[rows]
     orc = oracle.exact_forward(p, ts, W)
     sub = {k: v[rows] for k, v in gpu.items()}
-    mask, _ = check_forward(sub, orc, t.shape[1], 1.0, label="exact bench-size sampled",
-                            max_ambiguous=_max_ambiguous(orc, t.shape[1], 1.0))
+    mask, st = check_forward(sub, orc, t.shape[1], 1.0, label="exact bench-size sampled",
+                             taus=_taus(p), max_ambiguous=_max_ambiguous(orc, t.shape[1], 1.0))
     g = np.zeros(gpu["t_out"].shape, dtype=np.float32)
     gs = np.random.default_rng(3).standard_normal((len(rows), W.shape[0]))
     g[rows] = np.where(mask, 0.0, gs)
     _, gx = _gpu_backward(dev, h, g, need_W=False)
-    ob = oracle.exact_backward(p, ts, W, orc, np.where(orc["q"] >= 0, g[rows].astype(np.float64), 0.0))
-    check_grad(gx[rows], ob["grad_t_in"], "exact bench-size dt_in", ob["grad_t_in_abs"])
+    ob = oracle.exact_backward(p, ts, W, orc, np.where(orc["q"] >= 0, g[rows].astype(np.float64), 0.0),
+                               err=grad_err_inputs(st, mask))
+    check_grad(gx[rows], ob["grad_t_in"], "exact bench-size dt_in", ob["grad_t_in_abs"],
+               ob["grad_t_in_err"], n_terms=W.shape[0])
     others = np.setdiff1d(np.arange(t.shape[0]), rows)
     assert not gx[others].any()  # samples with zero upstream gradient get none
     del h

@@ -15,6 +15,14 @@ from tests.parity import check_forward, check_grad, near_grid
 
 pytestmark = pytest.mark.gpu
 
+# Gradient floor of the multi-spike layer: 1e-4 times each element's sum of
+# |terms|. Unlike the single-spike path, no first-order error model is
+# derived here (a spike's errors propagate to the later spikes of its neuron
+# through the reset chain), so this path keeps a fixed fraction, chosen well
+# above the fp32 rounding of the sums (~1e-6 of the |terms|) and well below
+# the 1e-3 relative tolerance.
+MS_KAPPA = 1e-4
+
 
 @pytest.fixture(scope="module")
 def dev():
@@ -75,10 +83,10 @@ def _parity(dev, p, t, W, F_out, label, bf16=False, seed=0):
     gW, gx = dstd.multispike_backward(prm, tt, Wt, to, sl, q, cur, torch.from_numpy(g).to(dev))
     torch.cuda.synchronize()
     ob = oracle.ms_backward(p, t, Wq, orc, g.astype(np.float64))
-    check_grad(gW.cpu().numpy(), ob["grad_W"], label + " dW", ob["grad_W_abs"])
+    check_grad(gW.cpu().numpy(), ob["grad_W"], label + " dW", ob["grad_W_abs"], kappa=MS_KAPPA)
     kink = near_grid(t, p)
     check_grad(gx.cpu().numpy()[~kink], ob["grad_t_in"][~kink], label + " dt_in",
-               ob["grad_t_in_abs"][~kink])
+               ob["grad_t_in_abs"][~kink], kappa=MS_KAPPA)
     return gpu, orc, st
 
 
@@ -183,9 +191,10 @@ def test_multispike_bench_size_sampled(dev, F_in, F_out):
     gW, gx = dstd.multispike_backward(prm, tt, Wt, to, sl, q, cur, torch.from_numpy(g).to(dev))
     torch.cuda.synchronize()
     ob = oracle.ms_backward(p, ts, W, orc, gs.astype(np.float32).astype(np.float64))
-    check_grad(gW.cpu().numpy(), ob["grad_W"], "bench-size dW", ob["grad_W_abs"])
+    check_grad(gW.cpu().numpy(), ob["grad_W"], "bench-size dW", ob["grad_W_abs"], kappa=MS_KAPPA)
     gxs = gx.cpu().numpy()
     kink = near_grid(ts, p)
-    check_grad(gxs[rows][~kink], ob["grad_t_in"][~kink], "bench-size dt_in", ob["grad_t_in_abs"][~kink])
+    check_grad(gxs[rows][~kink], ob["grad_t_in"][~kink], "bench-size dt_in", ob["grad_t_in_abs"][~kink],
+               kappa=MS_KAPPA)
     others = np.setdiff1d(np.arange(B), rows)
     assert not gxs[others].any()

@@ -8,7 +8,7 @@ import numpy as np
 import pytest
 
 import oracle
-from tests.parity import check_forward, check_grad, near_grid
+from tests.parity import check_forward, check_grad, grad_err_inputs, near_grid
 from tests.test_gpu_conv import _cs, _conv_case, _gpu_backward, _gpu_forward, _window
 
 pytestmark = pytest.mark.gpu
@@ -83,10 +83,11 @@ def test_sd_block_third_layer_and_input_gradient(dev, stride, label):
     assert np.array_equal(cat_np, np.concatenate([x + np.float32(delay), o2["t_out"]], axis=1))
     o3, h3 = _gpu_forward(dev, p3, cs3, cat_np, W3)
     orc3 = oracle.conv_forward(p3, cs3, cat_np, W3)
-    mask3, st3 = check_forward(o3, orc3, None, _window(p3), label=f"{label} layer 3")
+    taus = (max(tm, ts), min(tm, ts))
+    mask3, st3 = check_forward(o3, orc3, None, _window(p3), label=f"{label} layer 3", taus=taus)
     assert st3["fired"] > 0.1 * st3["n"]
     orc1 = oracle.conv_forward(p1, cs1, x, W1)
-    mask1, _ = check_forward(o1, orc1, None, _window(p1), label=f"{label} layer 1")
+    mask1, st1 = check_forward(o1, orc1, None, _window(p1), label=f"{label} layer 1", taus=taus)
     rng = np.random.default_rng(5)
     g3 = np.where(mask3, 0.0, rng.standard_normal(orc3["t_out"].shape)).astype(np.float32)
     g1 = np.where(mask1, 0.0, rng.standard_normal(orc1["t_out"].shape)).astype(np.float32)
@@ -95,16 +96,19 @@ def test_sd_block_third_layer_and_input_gradient(dev, stride, label):
     gx = torch.from_numpy(gx1).to(dev)
     _, g_o2 = dstd.skip_delay_concat_backward(torch.from_numpy(gcat).to(dev), C, g1=gx)
     torch.cuda.synchronize()
-    _, ocat, _, ocat_a = oracle.conv_backward(p3, cs3, cat_np, W3, orc3,
-                                              np.where(orc3["q"] >= 0, g3.astype(np.float64), 0.0),
-                                              want_abs=True)
-    _, ox1, _, ox1_a = oracle.conv_backward(p1, cs1, x, W1, orc1,
-                                            np.where(orc1["q"] >= 0, g1.astype(np.float64), 0.0),
-                                            want_abs=True)
+    _, ocat, _, ocat_a, _, ocat_e = oracle.conv_backward(
+        p3, cs3, cat_np, W3, orc3, np.where(orc3["q"] >= 0, g3.astype(np.float64), 0.0),
+        want_abs=True, err=grad_err_inputs(st3, mask3))
+    _, ox1, _, ox1_a, _, ox1_e = oracle.conv_backward(
+        p1, cs1, x, W1, orc1, np.where(orc1["q"] >= 0, g1.astype(np.float64), 0.0),
+        want_abs=True, err=grad_err_inputs(st1, mask1))
     ox = ox1 + ocat[:, :C]
     oxa = ox1_a + ocat_a[:, :C]
+    oxe = ox1_e + ocat_e[:, :C]
+    n_x = 2 * (N + N3) * 9
     kink = near_grid(x, p1) | near_grid(cat_np[:, :C], p3)
-    check_grad(gx.cpu().numpy()[~kink], ox[~kink], f"{label} block input dt", oxa[~kink])
+    check_grad(gx.cpu().numpy()[~kink], ox[~kink], f"{label} block input dt", oxa[~kink], oxe[~kink],
+               n_terms=n_x)
     kink2 = near_grid(cat_np[:, C:], p3)
     check_grad(g_o2.cpu().numpy()[~kink2], ocat[:, C:][~kink2], f"{label} layer-2 output dt",
-               ocat_a[:, C:][~kink2])
+               ocat_a[:, C:][~kink2], ocat_e[:, C:][~kink2], n_terms=2 * N3 * 9)

@@ -6,7 +6,7 @@ import numpy as np
 import pytest
 
 import oracle
-from tests.parity import check_forward, check_grad
+from tests.parity import check_forward, check_grad, grad_err_inputs
 
 pytestmark = pytest.mark.gpu
 
@@ -35,33 +35,34 @@ def _sp(scale, **kw):
                              d["gamma_q"], scale)
 
 
-def _compare(gW, gx, exp, mask, label):
+def _compare(gW, gx, exp, mask, label, n_terms):
     """dW rows and dt_in samples reached by an ill-conditioned spike (the
     oracle's own mask: tiny slope, both sides agree it fires) are left out:
     the penalty gradient of such a neuron flows through that slope on both
     sides."""
-    eW, ex, eWa, exa = exp
+    eW, ex, eWa, exa, eWe, exe = exp
     B, rows = mask.shape[0], mask.shape[1]
     m = mask.reshape(B, rows, -1)
     row_ok = ~m.any(axis=(0, 2))
     smp_ok = ~m.any(axis=(1, 2))
     assert row_ok.sum() >= 0.8 * rows and smp_ok.sum() >= 0.5 * B, (row_ok.sum(), smp_ok.sum())
-    check_grad(gW[row_ok], eW[row_ok], label + " dW", eWa[row_ok])
-    check_grad(gx[smp_ok], ex[smp_ok], label + " dt_in", exa[smp_ok])
+    check_grad(gW[row_ok], eW[row_ok], label + " dW", eWa[row_ok], eWe[row_ok], n_terms=n_terms[0])
+    check_grad(gx[smp_ok], ex[smp_ok], label + " dt_in", exa[smp_ok], exe[smp_ok], n_terms=n_terms[1])
 
 
-def _expected(p, t, W, orc, g, scale, conv_cs=None):
+def _expected(p, t, W, orc, g, scale, err, conv_cs=None):
     """Oracle gradients with the synfire terms: the upstream gradient plus
     dT/dt into the layer's backward, plus dQ/dW."""
     _, dT = oracle.temporal_penalty(orc["t_out"], SF["gamma_head"], SF["gamma_tail"],
                                     SF["t_head"], SF["t_tail"], scale)
     g_tot = np.where(orc["q"] >= 0, g.astype(np.float64) + dT, 0.0)
     if conv_cs is None:
-        oW, ox, oWa, oxa = oracle.dstd_backward(p, t, W, orc, g_tot, want_abs=True)
+        oW, ox, oWa, oxa, oWe, oxe = oracle.dstd_backward(p, t, W, orc, g_tot, want_abs=True, err=err)
     else:
-        oW, ox, oWa, oxa = oracle.conv_backward(p, conv_cs, t, W, orc, g_tot, want_abs=True)
+        oW, ox, oWa, oxa, oWe, oxe = oracle.conv_backward(p, conv_cs, t, W, orc, g_tot, want_abs=True,
+                                                          err=err)
     _, dQ = oracle.dead_neuron_penalty(orc["t_out"], W, SF["gamma_q"], scale)
-    return oW + dQ, ox, oWa + np.abs(dQ), oxa
+    return oW + dQ, ox, oWa + np.abs(dQ), oxa, oWe, oxe
 
 
 def test_dense_synfire_gradients(dev):
@@ -77,7 +78,7 @@ def test_dense_synfire_gradients(dev):
     to, sl, q = dstd.forward(prm, tt, Wt)
     gpu = dict(t_out=to.cpu().numpy(), slope=sl.cpu().numpy(), q=q.cpu().numpy())
     orc = oracle.dstd_forward(p, t, W)
-    mask, st = check_forward(gpu, orc, N_in, 1.0, label="dense synfire")
+    mask, st = check_forward(gpu, orc, N_in, 1.0, label="dense synfire", taus=(1.0, 0.3))
     # the terms need fire / no-fire agreement everywhere
     assert st["ambiguous"] == 0, st
     silent = int((orc["q"] < 0).sum())
@@ -86,8 +87,9 @@ def test_dense_synfire_gradients(dev):
     gt = torch.from_numpy(g).to(dev)
     gW, gx = dstd.backward(prm, tt, Wt, to, sl, q, gt, synfire=_sp(1.0 / B))
     torch.cuda.synchronize()
-    _compare(gW.cpu().numpy(), gx.cpu().numpy(), _expected(p, t, W, orc, g, 1.0 / B), mask,
-             "dense synfire")
+    _compare(gW.cpu().numpy(), gx.cpu().numpy(),
+             _expected(p, t, W, orc, g, 1.0 / B, grad_err_inputs(st, mask)), mask,
+             "dense synfire", (2 * B, 2 * N_out))
     # all gammas zero: bit-identical to the plain backward
     z = dstd.make_synfire(0.0, 0.0, SF["t_head"], SF["t_tail"], 0.0, 1.0)
     gW0, gx0 = dstd.backward(prm, tt, Wt, to, sl, q, gt, synfire=z)
@@ -115,14 +117,15 @@ def test_dense_synfire_split_dw(dev):
     to, sl, q = dstd.forward(prm, tt, Wt)
     gpu = dict(t_out=to.cpu().numpy(), slope=sl.cpu().numpy(), q=q.cpu().numpy())
     orc = oracle.dstd_forward(p, t, W)
-    mask, st = check_forward(gpu, orc, N_in, 1.0, label="dense synfire split")
+    mask, st = check_forward(gpu, orc, N_in, 1.0, label="dense synfire split", taus=(1.0, 0.3))
     assert st["ambiguous"] == 0, st
     g = rng.standard_normal((B, N_out)).astype(np.float32)
     gW, gx = dstd.backward(prm, tt, Wt, to, sl, q, torch.from_numpy(g).to(dev),
                            synfire=_sp(1.0 / B))
     torch.cuda.synchronize()
-    _compare(gW.cpu().numpy(), gx.cpu().numpy(), _expected(p, t, W, orc, g, 1.0 / B), mask,
-             "dense synfire split")
+    _compare(gW.cpu().numpy(), gx.cpu().numpy(),
+             _expected(p, t, W, orc, g, 1.0 / B, grad_err_inputs(st, mask)), mask,
+             "dense synfire split", (2 * B, 2 * N_out))
 
 
 def test_conv_synfire_gradients(dev):
@@ -141,7 +144,7 @@ def test_conv_synfire_gradients(dev):
     to, sl, q = dstd.conv_forward(prm, c, tt, Wt)
     gpu = dict(t_out=to.cpu().numpy(), slope=sl.cpu().numpy(), q=q.cpu().numpy())
     orc = oracle.conv_forward(p, cs, t, W)
-    mask, st = check_forward(gpu, orc, fan, 1.0, label="conv synfire")
+    mask, st = check_forward(gpu, orc, fan, 1.0, label="conv synfire", taus=(1.0, 0.3))
     assert st["ambiguous"] == 0, st
     silent = int((orc["q"] < 0).sum())
     assert 0 < silent < orc["q"].size
@@ -150,8 +153,9 @@ def test_conv_synfire_gradients(dev):
     gt = torch.from_numpy(g).to(dev)
     gW, gx = dstd.conv_backward(prm, c, tt, Wt, to, sl, q, gt, synfire=_sp(scale))
     torch.cuda.synchronize()
-    _compare(gW.cpu().numpy(), gx.cpu().numpy(), _expected(p, t, W, orc, g, scale, conv_cs=cs),
-             mask, "conv synfire")
+    _compare(gW.cpu().numpy(), gx.cpu().numpy(),
+             _expected(p, t, W, orc, g, scale, grad_err_inputs(st, mask), conv_cs=cs),
+             mask, "conv synfire", (2 * B * 100, 2 * 8 * 9))
     z = dstd.make_synfire(0.0, 0.0, SF["t_head"], SF["t_tail"], 0.0, 1.0)
     gW0, gx0 = dstd.conv_backward(prm, c, tt, Wt, to, sl, q, gt, synfire=z)
     gW1, gx1 = dstd.conv_backward(prm, c, tt, Wt, to, sl, q, gt)

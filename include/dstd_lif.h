@@ -14,7 +14,8 @@
  *
  * Conventions for every call:
  *  - All array pointers are DEVICE pointers owned by the caller; the library
- *    never allocates, frees or keeps device memory between calls.
+ *    never allocates, frees or keeps device memory between calls (the one
+ *    exception is the static scratch array of dstd_lif_forward_noalloc).
  *  - Arrays are dense, row-major, fp32 unless stated (W may be bf16).
  *  - Work is enqueued asynchronously on `stream` (a hipStream_t, passed as
  *    void*; NULL = the default stream); outputs are valid once the stream
@@ -114,6 +115,30 @@ dstd_status dstd_lif_forward(const dstd_lif_params *p, int64_t B, int64_t N_in, 
                              const float *t_in, const void *W, dstd_dtype w_dtype,
                              float *t_out, float *slope, int32_t *q_idx,
                              void *ws, size_t ws_bytes, void *stream);
+
+/*
+ * Allocation-free variant of dstd_lif_forward, for callers that cannot
+ * allocate device memory or take a workspace: code under HIP graph capture,
+ * tight serving loops, harnesses that forbid allocation. Same arguments,
+ * outputs, validation and bits as dstd_lif_forward, without ws / ws_bytes;
+ * its scratch is a static device array of DSTD_NOALLOC_SCRATCH_BYTES bytes
+ * that the library holds on each GPU it runs on until the process ends (its
+ * device address is looked up once per device, on the first call there).
+ *  - A layer whose dstd_lif_forward_workspace_size() exceeds
+ *    DSTD_NOALLOC_SCRATCH_BYTES is rejected with DSTD_ERR_WORKSPACE before
+ *    anything touches the device.
+ *  - It calls no hipMalloc / hipFree and no allocating routine.
+ *  - All calls on one GPU share that GPU's array: calls that overlap in time
+ *    on one GPU (different streams, or different threads without ordering)
+ *    race on it and give undefined results. Calls ordered on one stream are
+ *    safe; the forward writes every scratch word it reads, so nothing carries
+ *    over from the previous call.
+ */
+#define DSTD_NOALLOC_SCRATCH_BYTES (32u << 20)
+dstd_status dstd_lif_forward_noalloc(const dstd_lif_params *p, int64_t B, int64_t N_in,
+                                     int64_t N_out, const float *t_in, const void *W,
+                                     dstd_dtype w_dtype, float *t_out, float *slope,
+                                     int32_t *q_idx, void *stream);
 
 /*
  * Backward pass of one dense layer. t_out, slope, q_idx are the forward's

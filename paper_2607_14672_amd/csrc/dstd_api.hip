@@ -8,6 +8,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <mutex>
 
 #include "../../include/dstd_lif.h"
 #include "dstd_internal.h"
@@ -380,6 +381,64 @@ dstd_status dstd_lif_forward(const dstd_lif_params *p, int64_t B, int64_t N_in, 
     hipError_t e = dstd::launch_forward(C, B, N_in, N_out, W, w_dtype == DSTD_BF16, at<void>(ws, L.wt),
                                         srt, at<int>(ws, L.nvalid), t_in, t_out, slope, q_idx, st);
     return hip_status(e, "forward launch");
+}
+
+}  // extern "C"
+
+// Scratch of the allocation-free forward: one array per GPU, reserved when the
+// library's code object is loaded there and kept until the process ends. In
+// host code `scratch` only names the symbol; its device address comes from
+// hipGetSymbolAddress, once per device, with that device current.
+static __device__ __align__(256) unsigned char scratch[DSTD_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+void *g_scratch_ptr[kMaxDevices] = {};
+std::mutex g_scratch_mu;
+
+dstd_status scratch_for_current_device(void **out) {
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return fail(DSTD_ERR_HIP, "hipGetDevice: %s", hipGetErrorString(e));
+    if (dev < 0 || dev >= kMaxDevices)
+        return fail(DSTD_ERR_UNSUPPORTED, "device index %d beyond %d", dev, kMaxDevices);
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void *ptr = nullptr;
+        e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || !ptr)
+            return fail(DSTD_ERR_HIP, "hipGetSymbolAddress(scratch) on device %d: %s", dev,
+                        hipGetErrorString(e));
+        g_scratch_ptr[dev] = ptr;
+    }
+    *out = g_scratch_ptr[dev];
+    return DSTD_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+dstd_status dstd_lif_forward_noalloc(const dstd_lif_params *p, int64_t B, int64_t N_in,
+                                     int64_t N_out, const float *t_in, const void *W,
+                                     dstd_dtype w_dtype, float *t_out, float *slope,
+                                     int32_t *q_idx, void *stream) {
+    // host validation first: nothing touches the device before the sizes pass
+    dstd_status s = check_params(p);
+    if (s != DSTD_OK) return s;
+    if ((s = check_dims(B, N_in, N_out)) != DSTD_OK) return s;
+    const size_t need = dense_ws_layout(p->M, B, N_in, N_out, false).total;
+    if (need > (size_t)DSTD_NOALLOC_SCRATCH_BYTES)
+        return fail(DSTD_ERR_WORKSPACE,
+                    "layer needs %zu bytes of scratch; the allocation-free forward holds %zu "
+                    "(use dstd_lif_forward with a caller workspace)",
+                    need, (size_t)DSTD_NOALLOC_SCRATCH_BYTES);
+    void *ws = nullptr;
+    if (need > 0 && (s = scratch_for_current_device(&ws)) != DSTD_OK) return s;
+    // the forward's kernels write every scratch word they read: nothing to clear
+    return dstd_lif_forward(p, B, N_in, N_out, t_in, W, w_dtype, t_out, slope, q_idx, ws,
+                            need > 0 ? (size_t)DSTD_NOALLOC_SCRATCH_BYTES : 0, stream);
 }
 
 dstd_status dstd_lif_backward(const dstd_lif_params *p, int64_t B, int64_t N_in, int64_t N_out,

@@ -27,6 +27,7 @@ DSTD_ERR_HIP = -6
 DSTD_F32 = 0
 DSTD_BF16 = 1
 DSTD_MAX_M = 256
+DSTD_NOALLOC_SCRATCH_BYTES = 32 << 20
 
 
 class dstd_lif_params(C.Structure):
@@ -66,6 +67,7 @@ _SIGS = {
     "dstd_lif_forward_workspace_size": (_S, [_P, _L, _L, _L]),
     "dstd_lif_backward_workspace_size": (_S, [_P, _L, _L, _L]),
     "dstd_lif_forward": (_I, [_P, _L, _L, _L, _P, _P, _I, _P, _P, _P, _P, _S, _P]),
+    "dstd_lif_forward_noalloc": (_I, [_P, _L, _L, _L, _P, _P, _I, _P, _P, _P, _P]),
     "dstd_lif_backward": (_I, [_P, _L, _L, _L, _P, _P, _I, _P, _P, _P, _P, _P, _P, _P, _S, _P]),
     "dstd_lif_conv_forward_workspace_size": (_S, [_P, _P, _L]),
     "dstd_lif_conv_backward_workspace_size": (_S, [_P, _P, _L]),
@@ -137,6 +139,11 @@ def dstd_lif_backward_workspace_size(p, B, N_in, N_out):
 def dstd_lif_forward(p, B, N_in, N_out, t_in, W, w_dtype, t_out, slope, q_idx, ws, ws_bytes, stream):
     return _load().dstd_lif_forward(_ref(p), B, N_in, N_out, t_in, W, w_dtype, t_out, slope, q_idx,
                                     ws, ws_bytes, stream)
+
+
+def dstd_lif_forward_noalloc(p, B, N_in, N_out, t_in, W, w_dtype, t_out, slope, q_idx, stream):
+    return _load().dstd_lif_forward_noalloc(_ref(p), B, N_in, N_out, t_in, W, w_dtype, t_out,
+                                            slope, q_idx, stream)
 
 
 def dstd_lif_backward(p, B, N_in, N_out, t_in, W, w_dtype, t_out, slope, q_idx, grad_t_out,
@@ -371,6 +378,27 @@ def forward(p: dstd_lif_params, t_in, W, ws=None):
     _check("dstd_lif_forward",
            dstd_lif_forward(p, B, N_in, N_out, _ptr(t_in), _ptr(W), _wdtype(W), _ptr(t_out),
                             _ptr(slope), _ptr(q), _ptr(ws), ws.numel(), _stream(dev)))
+    return t_out, slope, q
+
+
+def forward_noalloc(p: dstd_lif_params, t_in, W, outputs=None):
+    """Dense layer forward through the allocation-free entry point (the
+    library's static scratch). `outputs` = (t_out, slope, q) preallocated
+    tensors, or None to allocate them here."""
+    torch = _torch()
+    t_in = _cont(t_in, torch.float32)
+    W = _cont(W)
+    B, N_in = t_in.shape
+    N_out = W.shape[0]
+    assert W.shape[1] == N_in
+    dev = t_in.device
+    if outputs is None:
+        t_out = torch.empty((B, N_out), dtype=torch.float32, device=dev)
+        outputs = (t_out, torch.empty_like(t_out), torch.empty((B, N_out), dtype=torch.int32, device=dev))
+    t_out, slope, q = outputs
+    _check("dstd_lif_forward_noalloc",
+           dstd_lif_forward_noalloc(p, B, N_in, N_out, _ptr(t_in), _ptr(W), _wdtype(W), _ptr(t_out),
+                                    _ptr(slope), _ptr(q), _stream(dev)))
     return t_out, slope, q
 
 

@@ -301,3 +301,17 @@ def test_multispike_validation():
                                              256, nb, None) == dstd.DSTD_ERR_NULL
     assert dstd.dstd_lif_multispike_forward(p, 0, 10, 2, 5, 3, None, None, 0, None, None, None,
                                             None, None, 0, None) == dstd.DSTD_OK
+
+
+def test_noalloc_forward_validates_before_the_device():
+    """The allocation-free forward checks parameters and its scratch limit on
+    the host; an oversized layer is refused before any device access."""
+    p = _p()
+    assert dstd.dstd_lif_forward_noalloc(_p(M=0), 4, 10, 5, 1, 1, 0, 1, 1, 1, None) == dstd.DSTD_ERR_PARAM
+    need = dstd.dstd_lif_forward_workspace_size(p, 256, 4096, 4096)
+    assert need > dstd.DSTD_NOALLOC_SCRATCH_BYTES
+    st = dstd.dstd_lif_forward_noalloc(p, 256, 4096, 4096, 1, 1, 0, 1, 1, 1, None)
+    assert st == dstd.DSTD_ERR_WORKSPACE
+    assert "scratch" in dstd.dstd_last_error()
+    # empty layers are no-ops that need no scratch
+    assert dstd.dstd_lif_forward_noalloc(p, 0, 10, 5, 0, 1, 0, 0, 0, 0, None) == dstd.DSTD_OK

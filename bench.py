@@ -34,6 +34,7 @@ METRIC = "DSTD LIF fwd+bwd samples/s; % MFMA peak (GEMM) and % HBM peak (scan)"
 # MI355X published peaks (dense, per GPU)
 PEAK_FP32_VECTOR_TFLOPS = 157.3
 PEAK_HBM_GBS = 8000.0
+PEAK_BF16_MFMA_TFLOPS = 2500.0
 # algorithmic flops per (sample, input with events, neuron) update: the two
 # halves of an event are multiplied by the weight and added to two bins
 FLOPS_PER_UPDATE = 4
@@ -50,7 +51,7 @@ def kernel_source_sha():
 class Net:
     """Preallocated buffers and raw C-ABI calls for one workload."""
 
-    def __init__(self, wl, dev):
+    def __init__(self, wl, dev, contract="auto"):
         import torch
         from paper_2607_14672_amd import dstd, workloads
         self.torch, self.dstd, self.wl, self.dev = torch, dstd, wl, dev
@@ -66,8 +67,12 @@ class Net:
             W = torch.from_numpy(d.weights(l)).to(dev)
             if lay.w_dtype == "bf16":
                 W = W.to(torch.bfloat16)
+            flags = 0
+            if lay.kind != "conv":
+                flags = {"auto": 0, "sparse": dstd.DSTD_FLAG_CONTRACT_SPARSE,
+                         "mfma": dstd.DSTD_FLAG_CONTRACT_MFMA}[contract]
             p = dstd.make_params(lay.tau_m, lay.tau_s, lay.threshold, lay.M, lay.t0, lay.dt,
-                                 lay.t_max)
+                                 lay.t_max, flags)
             skip = None
             if lay.skip_back:
                 # SD block's third layer: t_in = cat(block input + delay, t_prev)
@@ -292,7 +297,7 @@ def kernel_algorithmic_flops(net, act):
     """Algorithmic flops of one step, per kernel name (2-sparse events:
     FLOPS_PER_UPDATE per (sample, input with events, neuron))."""
     fl = {k: 0.0 for k in ("fwd_dense", "dw_dense", "dtin_rows", "conv_fwd", "conv_dw",
-                           "conv_dtp")}
+                           "conv_dtp", "fwd_mfma")}
     for l, (e, a) in enumerate(zip(net.L, act)):
         upd = a["updates"]
         fwd, dw, dt = (("conv_fwd", "conv_dw", "conv_dtp") if e["cs"] is not None else
@@ -591,6 +596,9 @@ def main():
                                          "wide-M128,conv20",
                     help="further workloads timed after the headline, reported in detail.configs")
     ap.add_argument("--config-steps", type=int, default=50)
+    ap.add_argument("--contract", default="auto", choices=["auto", "sparse", "mfma"],
+                    help="dense layers' forward contraction: the library's choice by shape, the "
+                         "event-sparse kernels, or the bf16 MFMA product (bf16 weights only)")
     ap.add_argument("--no-configs", action="store_true")
     ap.add_argument("--profile-steps", type=int, default=20)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -634,7 +642,8 @@ def main():
                           "rows": multispike_bench(torch, dstd, dev)}), flush=True)
         return
     wl = workloads.get(args.workload)
-    head = measure(torch, dstd, wl, dev, args.steps, args.warmup, args.profile_steps, args.eager)
+    head = measure(torch, dstd, wl, dev, args.steps, args.warmup, args.profile_steps, args.eager,
+                   args.contract)
     net = head.pop("net")
 
     if args.copy_probe:
@@ -651,11 +660,12 @@ def main():
     if not args.no_configs:
         for name in [x for x in args.configs.split(",") if x and x != args.workload]:
             r = measure(torch, dstd, workloads.get(name), dev, args.config_steps,
-                        max(3, args.config_steps // 5), 5, args.eager)
+                        max(3, args.config_steps // 5), 5, args.eager, args.contract)
             r.pop("net")
             others.append(dict(workload=name, description=workloads.get(name).description,
                                batch=workloads.get(name).batch, value=r["value"], unit="samples/s",
                                ms_per_step=r["ms_per_step"], roofline=r["roofline"],
+                               roofline_mfma=r["roofline_mfma"],
                                hbm_kernels=r["hbm_kernels"],
                                kernel_ms_per_step=r["kernel_ms_per_step"]))
             print(json.dumps(dict(config=name, value=r["value"], ms_per_step=r["ms_per_step"])),
@@ -672,6 +682,7 @@ def main():
                    "parallelism": "single GPU",
                    "execution": "eager launches" if args.eager else "HIP graph of the step"},
         "roofline": head["roofline"],
+        "roofline_mfma": head["roofline_mfma"],
         "cpu_baseline": cpu,
         "detail": {"kernel_ms_per_step": head["kernel_ms_per_step"],
                    "launches_per_step": head["launches_per_step"], "activity": head["activity"],
@@ -682,12 +693,12 @@ def main():
     print(json.dumps(out), flush=True)
 
 
-def measure(torch, dstd, wl, dev, steps, warmup, profile_steps, eager):
+def measure(torch, dstd, wl, dev, steps, warmup, profile_steps, eager, contract="auto"):
     """Time `steps` whole training steps of workload `wl` (HIP graph replays
     unless eager), then one profiling pass with the library's hipEvent timer:
     samples/s, per-kernel ms per step, the dominant kernel's roofline and the
     HBM rate of the bandwidth-bound kernels that have committed counters."""
-    net = Net(wl, dev)
+    net = Net(wl, dev, contract)
     run = net.step
     if not eager:
         graph = net.capture()
@@ -715,6 +726,8 @@ def measure(torch, dstd, wl, dev, steps, warmup, profile_steps, eager):
     per_step = {k: v[1] / profile_steps for k, v in prof.items()}
     launches = {k: v[0] / profile_steps for k, v in prof.items()}
     flops = kernel_algorithmic_flops(net, act)
+    if "fwd_mfma" in per_step and "fwd_dense" not in per_step:
+        flops["fwd_mfma"] = flops.pop("fwd_dense")
     sha = kernel_source_sha()
     # the dominant contraction kernel (the step's largest kernel is one of them)
     cand = {k: v for k, v in per_step.items() if k in flops and flops[k] > 0}
@@ -731,6 +744,17 @@ def measure(torch, dstd, wl, dev, steps, warmup, profile_steps, eager):
                     algorithmic_flops_per_launch=round(flops[dom] / n_launch),
                     kernel_ms_per_step=round(per_step[dom], 4),
                     largest_kernel=max(per_step, key=per_step.get))
+    mfma = None
+    if "fwd_mfma" in per_step:
+        # the dense product: 2 flops per (row (b, m), input, neuron) and event plane
+        ex = sum(2 * 3 * wl.batch * (e["lay"].M + 1) * e["lay"].n_in * e["lay"].n_out
+                 for e in net.L if e["cs"] is None)
+        t = per_step["fwd_mfma"] * 1e-3
+        mfma = dict(bound="mfma", kernel="fwd_mfma", executed_flops_per_step=ex,
+                    achieved=round(ex / t / 1e12, 2), peak=PEAK_BF16_MFMA_TFLOPS, unit="TFLOP/s",
+                    frac=round(ex / t / 1e12 / PEAK_BF16_MFMA_TFLOPS, 4),
+                    algorithmic_TFLOPs=round(flops["fwd_mfma"] / t / 1e12, 3),
+                    kernel_ms_per_step=round(per_step["fwd_mfma"], 4))
     hbm = {}
     for k, v in per_step.items():
         if k in flops:
@@ -742,6 +766,7 @@ def measure(torch, dstd, wl, dev, steps, warmup, profile_steps, eager):
         hbm[k] = dict(bytes_per_launch=b, ms_per_step=round(v, 4), achieved_GBs=round(gbs, 1),
                       frac=round(gbs / PEAK_HBM_GBS, 4))
     return dict(net=net, value=round(value, 1), ms_per_step=round(ms, 4), roofline=roof,
+                roofline_mfma=mfma,
                 kernel_ms_per_step={k: round(v, 4) for k, v in sorted(per_step.items())},
                 launches_per_step=launches, activity=act, hbm_kernels=hbm,
                 kernel_source_sha=sha)

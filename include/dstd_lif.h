@@ -73,7 +73,21 @@ typedef enum { DSTD_F32 = 0, DSTD_BF16 = 1 } dstd_dtype;
  *  t_max        : end of the last candidate interval [T_M, t_max); +INFINITY
  *                 leaves it open (the exact method's t_{N+1} = inf, App. A).
  *                 Must be > T_M.
- *  flags        : reserved, must be 0.
+ *  flags        : 0, or one of the contraction choices of the dense forward
+ *                 (ignored by the dense backward; any other call with a
+ *                 contraction flag returns DSTD_ERR_UNSUPPORTED):
+ *                  DSTD_FLAG_CONTRACT_SPARSE: the event-sparse contraction
+ *                    (two-point event supports, vector ALU);
+ *                  DSTD_FLAG_CONTRACT_MFMA: the dense product of the event
+ *                    matrix [B(M+1)][N_in] and W on the matrix cores (bf16
+ *                    weights only, else DSTD_ERR_UNSUPPORTED; the events are
+ *                    split into three bf16 planes, so the products carry fp32
+ *                    precision); it does (M+1)/2 times the method's
+ *                    multiply-adds (App. B.3).
+ *                 With neither, the library picks by shape (the MFMA product
+ *                 for bf16 weights, M <= 8 and large layers, where it was
+ *                 measured faster). Both set: DSTD_ERR_PARAM. Other bits must
+ *                 be 0.
  */
 typedef struct {
     float tau_m, tau_s;
@@ -85,6 +99,8 @@ typedef struct {
 } dstd_lif_params;
 
 #define DSTD_MAX_M 256
+#define DSTD_FLAG_CONTRACT_SPARSE 0x2
+#define DSTD_FLAG_CONTRACT_MFMA 0x4
 
 /* ---------------------------------------------------------------- dense -- */
 

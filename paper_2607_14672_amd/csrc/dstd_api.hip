@@ -32,7 +32,7 @@ constexpr size_t kAlign = 256;
 size_t align_up(size_t n) { return (n + kAlign - 1) / kAlign * kAlign; }
 
 // Host validation of the layer parameters (no device access).
-dstd_status check_params(const dstd_lif_params *p) {
+dstd_status check_params(const dstd_lif_params *p, int32_t allowed_flags = 0) {
     if (!p) return fail(DSTD_ERR_NULL, "params is NULL");
     // each time constant is > 0, finite or +inf (the closed-form rows)
     if (!(p->tau_m > 0.f) || !(p->tau_s > 0.f))
@@ -56,8 +56,39 @@ dstd_status check_params(const dstd_lif_params *p) {
     if (isnan(p->t_max) || !((double)p->t_max > TM))
         return fail(DSTD_ERR_PARAM, "t_max must be > T_M = t0 + M*dt (got %g, T_M = %g)",
                     (double)p->t_max, TM);
-    if (p->flags != 0) return fail(DSTD_ERR_PARAM, "flags must be 0");
+    if ((p->flags & ~allowed_flags) != 0) {
+        if (p->flags & (DSTD_FLAG_CONTRACT_SPARSE | DSTD_FLAG_CONTRACT_MFMA))
+            return fail(DSTD_ERR_UNSUPPORTED, "the contraction flags apply to dense layers only");
+        return fail(DSTD_ERR_PARAM, "unknown flags 0x%x", (unsigned)p->flags);
+    }
+    if ((p->flags & DSTD_FLAG_CONTRACT_SPARSE) && (p->flags & DSTD_FLAG_CONTRACT_MFMA))
+        return fail(DSTD_ERR_PARAM, "DSTD_FLAG_CONTRACT_SPARSE and _MFMA exclude each other");
     return DSTD_OK;
+}
+
+constexpr int32_t kDenseFlags = DSTD_FLAG_CONTRACT_SPARSE | DSTD_FLAG_CONTRACT_MFMA;
+
+// The dense forward's contraction: the event-sparse VALU kernels, or the
+// dense bf16 MFMA product of the event matrix and W (bf16 weights only). The
+// automatic choice is by shape, from measured times on MI355X (the dense
+// product does (M+1)/2 times the method's work, so it wins only for small M
+// on large layers).
+bool mfma_shape_auto(int M, int64_t B, int64_t N_in, int64_t N_out) {
+    return M <= dstd::kMfmaAutoMaxM && N_out >= 1024 && N_in >= 1024 && B * N_out >= (int64_t)1 << 18;
+}
+
+// could this call take the MFMA path (the workspace query does not know the
+// weight type, so it reserves room whenever it could)
+bool mfma_possible(const dstd_lif_params *p, int64_t B, int64_t N_in, int64_t N_out) {
+    if (p->flags & DSTD_FLAG_CONTRACT_SPARSE) return false;
+    if (p->flags & DSTD_FLAG_CONTRACT_MFMA) return true;
+    return mfma_shape_auto(p->M, B, N_in, N_out);
+}
+
+size_t mfma_ws_events(int64_t B, int64_t N_in) { return align_up((size_t)(B * N_in) * 16); }
+size_t mfma_ws_bytes(int M, int64_t B, int64_t N_in, int64_t N_out) {
+    if (B * N_out == 0) return 0;
+    return mfma_ws_events(B, N_in) + align_up((size_t)B * (size_t)(M + 1) * (size_t)N_out * sizeof(float));
 }
 
 // Row of Table "tab:kernel" for the canonical pair tv >= ti (tv may be inf).
@@ -348,13 +379,15 @@ int32_t dstd_version(void) { return 100; }
 
 size_t dstd_lif_forward_workspace_size(const dstd_lif_params *p, int64_t B, int64_t N_in,
                                        int64_t N_out) {
-    if (check_params(p) != DSTD_OK || check_dims(B, N_in, N_out) != DSTD_OK) return 0;
-    return dense_ws_layout(p->M, B, N_in, N_out, false).total;
+    if (check_params(p, kDenseFlags) != DSTD_OK || check_dims(B, N_in, N_out) != DSTD_OK) return 0;
+    size_t need = (p->flags & DSTD_FLAG_CONTRACT_MFMA) ? 0 : dense_ws_layout(p->M, B, N_in, N_out, false).total;
+    if (mfma_possible(p, B, N_in, N_out)) need = std::max(need, mfma_ws_bytes(p->M, B, N_in, N_out));
+    return need;
 }
 
 size_t dstd_lif_backward_workspace_size(const dstd_lif_params *p, int64_t B, int64_t N_in,
                                         int64_t N_out) {
-    if (check_params(p) != DSTD_OK || check_dims(B, N_in, N_out) != DSTD_OK) return 0;
+    if (check_params(p, kDenseFlags) != DSTD_OK || check_dims(B, N_in, N_out) != DSTD_OK) return 0;
     return dense_ws_layout(p->M, B, N_in, N_out, true).total;
 }
 
@@ -362,15 +395,28 @@ dstd_status dstd_lif_forward(const dstd_lif_params *p, int64_t B, int64_t N_in, 
                              const float *t_in, const void *W, dstd_dtype w_dtype, float *t_out,
                              float *slope, int32_t *q_idx, void *ws, size_t ws_bytes,
                              void *stream) {
-    dstd_status s = check_params(p);
+    dstd_status s = check_params(p, kDenseFlags);
     if (s != DSTD_OK) return s;
     if ((s = check_dims(B, N_in, N_out)) != DSTD_OK) return s;
     if (w_dtype != DSTD_F32 && w_dtype != DSTD_BF16)
         return fail(DSTD_ERR_PARAM, "unknown weight dtype %d", (int)w_dtype);
+    if ((p->flags & DSTD_FLAG_CONTRACT_MFMA) && w_dtype != DSTD_BF16)
+        return fail(DSTD_ERR_UNSUPPORTED, "the MFMA contraction takes bf16 weights");
     if (B * N_out > 0 && (!t_out || !slope || !q_idx))
         return fail(DSTD_ERR_NULL, "t_out, slope and q_idx are required");
     if (B * N_in > 0 && !t_in) return fail(DSTD_ERR_NULL, "t_in is NULL");
     if (N_in * N_out > 0 && !W) return fail(DSTD_ERR_NULL, "W is NULL");
+    const bool mfma = w_dtype == DSTD_BF16 && mfma_possible(p, B, N_in, N_out);
+    if (mfma) {
+        if ((s = check_ws(ws, ws_bytes, mfma_ws_bytes(p->M, B, N_in, N_out))) != DSTD_OK) return s;
+        if (B * N_out == 0) return DSTD_OK;
+        LifConst C = make_const(p);
+        hipError_t e = dstd::launch_forward_mfma(
+            C, B, N_in, N_out, static_cast<const uint16_t *>(W), ws,
+            at<float>(ws, mfma_ws_events(B, N_in)), t_in, t_out, slope, q_idx,
+            static_cast<hipStream_t>(stream));
+        return hip_status(e, "forward (MFMA) launch");
+    }
     DenseWs L = dense_ws_layout(p->M, B, N_in, N_out, false);
     if ((s = check_ws(ws, ws_bytes, L.total)) != DSTD_OK) return s;
     if (B * N_out == 0) return DSTD_OK;
@@ -425,10 +471,10 @@ dstd_status dstd_lif_forward_noalloc(const dstd_lif_params *p, int64_t B, int64_
                                      dstd_dtype w_dtype, float *t_out, float *slope,
                                      int32_t *q_idx, void *stream) {
     // host validation first: nothing touches the device before the sizes pass
-    dstd_status s = check_params(p);
+    dstd_status s = check_params(p, kDenseFlags);
     if (s != DSTD_OK) return s;
     if ((s = check_dims(B, N_in, N_out)) != DSTD_OK) return s;
-    const size_t need = dense_ws_layout(p->M, B, N_in, N_out, false).total;
+    const size_t need = dstd_lif_forward_workspace_size(p, B, N_in, N_out);
     if (need > (size_t)DSTD_NOALLOC_SCRATCH_BYTES)
         return fail(DSTD_ERR_WORKSPACE,
                     "layer needs %zu bytes of scratch; the allocation-free forward holds %zu "
@@ -469,7 +515,8 @@ dstd_status dense_backward(const dstd_lif_params *p, const dstd_synfire_params *
                            dstd_dtype w_dtype, const float *t_out, const float *slope,
                            const int32_t *q_idx, const float *grad_t_out, float *grad_W,
                            float *grad_t_in, void *ws, size_t ws_bytes, void *stream) {
-    dstd_status s = check_params(p);
+    // the contraction flags select the forward's kernels; the backward takes them as given
+    dstd_status s = check_params(p, kDenseFlags);
     if (s != DSTD_OK) return s;
     if ((s = check_synfire(sp)) != DSTD_OK) return s;
     if ((s = check_dims(B, N_in, N_out)) != DSTD_OK) return s;

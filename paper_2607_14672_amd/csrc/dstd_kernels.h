@@ -44,6 +44,13 @@ hipError_t launch_backward(const LifConst &C, int64_t B, int64_t N_in, int64_t N
                            const float *slope, const int *q_idx, const float *grad_t,
                            DenseBwdWs ws, float *grad_W, float *grad_t_in, const Synfire &sf,
                            hipStream_t st);
+// The dense forward's bf16 MFMA contraction (App. B.1's w^ as one product
+// of the event matrix and W), then the interval scan. ev: 16 B per input;
+// wh: [B][M+1][N_out] fp32.
+constexpr int kMfmaAutoMaxM = 8;  // largest M the automatic choice sends there (measured)
+hipError_t launch_forward_mfma(const LifConst &C, int64_t B, int64_t N_in, int64_t N_out,
+                               const uint16_t *W, void *ev, float *wh, const float *t_in,
+                               float *t_out, float *slope, int *q_idx, hipStream_t st);
 hipError_t launch_softmax_ce(int64_t B, int64_t N, const float *t, const int *labels,
                              float tau_soft, float t_cap, float *grad, float *loss, hipStream_t st);
 hipError_t launch_mse(int64_t B, int64_t N, const float *t, const float *y, float *grad,

@@ -28,6 +28,8 @@ DSTD_F32 = 0
 DSTD_BF16 = 1
 DSTD_MAX_M = 256
 DSTD_NOALLOC_SCRATCH_BYTES = 32 << 20
+DSTD_FLAG_CONTRACT_SPARSE = 0x2
+DSTD_FLAG_CONTRACT_MFMA = 0x4
 
 
 class dstd_lif_params(C.Structure):
@@ -297,9 +299,9 @@ def profile_table():
 
 
 # -------------------------------------------------------- tensor helpers --
-def make_params(tau_m, tau_s, threshold, M, t0, dt, t_max=math.inf) -> dstd_lif_params:
+def make_params(tau_m, tau_s, threshold, M, t0, dt, t_max=math.inf, flags=0) -> dstd_lif_params:
     return dstd_lif_params(float(tau_m), float(tau_s), float(threshold), int(M), float(t0),
-                           float(dt), float(t_max), 0)
+                           float(dt), float(t_max), int(flags))
 
 
 def make_synfire(gamma_head, gamma_tail, t_head, t_tail, gamma_q, scale) -> dstd_synfire_params:

@@ -315,3 +315,33 @@ def test_noalloc_forward_validates_before_the_device():
     assert "scratch" in dstd.dstd_last_error()
     # empty layers are no-ops that need no scratch
     assert dstd.dstd_lif_forward_noalloc(p, 0, 10, 5, 0, 1, 0, 0, 0, 0, None) == dstd.DSTD_OK
+
+
+def test_contraction_flags():
+    """The dense forward's contraction choice: both flags together, the MFMA
+    product with fp32 weights and the flags on other layer kinds are refused
+    on the host; the workspace query reserves room for the chosen path."""
+    S, Mf = dstd.DSTD_FLAG_CONTRACT_SPARSE, dstd.DSTD_FLAG_CONTRACT_MFMA
+    both = _p()
+    both.flags = S | Mf
+    assert dstd.dstd_lif_forward(both, 4, 10, 5, 1, 1, 0, 1, 1, 1, 256, 1 << 20, None) == dstd.DSTD_ERR_PARAM
+    mf = _p()
+    mf.flags = Mf
+    st = dstd.dstd_lif_forward(mf, 4, 10, 5, 1, 1, dstd.DSTD_F32, 1, 1, 1, 256, 1 << 20, None)
+    assert st == dstd.DSTD_ERR_UNSUPPORTED and "bf16" in dstd.dstd_last_error()
+    bad = _p()
+    bad.flags = 0x8
+    assert dstd.dstd_lif_forward(bad, 4, 10, 5, 1, 1, 0, 1, 1, 1, 256, 1 << 20, None) == dstd.DSTD_ERR_PARAM
+    cs = dstd.make_conv_shape(2, 5, 5, 3)
+    assert dstd.dstd_lif_conv_forward_workspace_size(mf, cs, 2) == 0
+    # MFMA room: events (16 B per input) + w^ (4 B per (b, m, i))
+    B, N_in, N_out = 8, 64, 96
+    need = dstd.dstd_lif_forward_workspace_size(mf, B, N_in, N_out)
+    assert need >= B * N_in * 16 + B * (mf.M + 1) * N_out * 4
+    sp = _p()
+    sp.flags = S
+    assert dstd.dstd_lif_forward_workspace_size(sp, B, N_in, N_out) == \
+        dstd.dstd_lif_forward_workspace_size(_p(), B, N_in, N_out)
+    # the backward accepts the same parameters
+    assert dstd.dstd_lif_backward_workspace_size(mf, B, N_in, N_out) == \
+        dstd.dstd_lif_backward_workspace_size(_p(), B, N_in, N_out)

@@ -24,7 +24,7 @@ def _gpu_forward(dev, p, t_in, W, bf16=False):
     import torch
     from paper_2607_14672_amd import dstd
     prm = dstd.make_params(p["tau_m"], p["tau_s"], p["threshold"], p["M"], p["t0"], p["dt"],
-                           p.get("t_max", math.inf))
+                           p.get("t_max", math.inf), p.get("flags", 0))
     tt = torch.from_numpy(np.ascontiguousarray(t_in, dtype=np.float32)).to(dev)
     Wt = torch.from_numpy(np.ascontiguousarray(W, dtype=np.float32)).to(dev)
     if bf16:
@@ -214,15 +214,18 @@ def test_conv9_dense_head(dev):
     _fwd_bwd_parity(dev, p, t, W, f"{name} dense head {lay.n_in}->{lay.n_out}", seed=l)
 
 
-@pytest.mark.parametrize("M", [8, 32, 64, 128])
-def test_wide_layer_full_size_sampled(dev, M):
+@pytest.mark.parametrize("M,flags", [(8, 0), (32, 0), (64, 0), (128, 0), (8, 0x2), (32, 0x4)],
+                         ids=["M8-auto", "M32-auto", "M64-auto", "M128-auto", "M8-sparse", "M32-mfma"])
+def test_wide_layer_full_size_sampled(dev, M, flags):
     """Full 256 x 4096 -> 4096 layer on the GPU; oracle on sampled rows: all
     neurons of 4 samples (forward, dt_in) and 8 neurons over the whole batch
-    (forward, dW)."""
+    (forward, dW). The automatic contraction choice takes the MFMA product at
+    M = 8; the forced cases run the other path at M = 8 and the MFMA product
+    at M = 32."""
     w = wl.get(f"wide-M{M}")
     d = wl.Draws(w)
     lay = w.layers[0]
-    p = lay.params()
+    p = dict(lay.params(), flags=flags)
     W = d.weights(0)
     import torch
     gpu, h = _gpu_forward(dev, p, d.t_in, W, bf16=True)

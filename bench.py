@@ -38,6 +38,11 @@ PEAK_BF16_MFMA_TFLOPS = 2500.0
 # algorithmic flops per (sample, input with events, neuron) update: the two
 # halves of an event are multiplied by the weight and added to two bins
 FLOPS_PER_UPDATE = 4
+# algorithmic flops of the interval scan per (neuron, grid point): the state
+# recurrences V <- alpha V + K(dt) I (a multiply and an FMA) and I <- beta I + w
+# (an add and a multiply), and the interval bound max(V,0) + max(I,0) K_max
+# (an FMA); the forward kernels fuse it with the contraction
+FLOPS_PER_SCAN_STEP = 7
 
 
 def kernel_source_sha():
@@ -293,9 +298,11 @@ def layer_desc(lay):
     return f"{lay.n_in}->{lay.n_out} M={lay.M}"
 
 
-def kernel_algorithmic_flops(net, act):
+def kernel_algorithmic_flops(net, act, with_scan=True):
     """Algorithmic flops of one step, per kernel name (2-sparse events:
-    FLOPS_PER_UPDATE per (sample, input with events, neuron))."""
+    FLOPS_PER_UPDATE per (sample, input with events, neuron)); the forward
+    kernels, which run the interval scan of their neurons too, also count
+    FLOPS_PER_SCAN_STEP per (neuron, grid point) when with_scan."""
     fl = {k: 0.0 for k in ("fwd_dense", "dw_dense", "dtin_rows", "conv_fwd", "conv_dw",
                            "conv_dtp", "fwd_mfma")}
     for l, (e, a) in enumerate(zip(net.L, act)):
@@ -303,6 +310,8 @@ def kernel_algorithmic_flops(net, act):
         fwd, dw, dt = (("conv_fwd", "conv_dw", "conv_dtp") if e["cs"] is not None else
                        ("fwd_dense", "dw_dense", "dtin_rows"))
         fl[fwd] += FLOPS_PER_UPDATE * upd
+        if with_scan:
+            fl[fwd] += FLOPS_PER_SCAN_STEP * e["t_out"].numel() * (e["lay"].M + 1)
         fl[dw] += FLOPS_PER_UPDATE * upd
         if l > 0:
             fl[dt] += FLOPS_PER_UPDATE * upd
@@ -726,8 +735,12 @@ def measure(torch, dstd, wl, dev, steps, warmup, profile_steps, eager, contract=
     per_step = {k: v[1] / profile_steps for k, v in prof.items()}
     launches = {k: v[0] / profile_steps for k, v in prof.items()}
     flops = kernel_algorithmic_flops(net, act)
+    contraction = kernel_algorithmic_flops(net, act, with_scan=False)
     if "fwd_mfma" in per_step and "fwd_dense" not in per_step:
-        flops["fwd_mfma"] = flops.pop("fwd_dense")
+        # the MFMA kernel only contracts; its scan runs in mfma_scan
+        flops["fwd_mfma"] = contraction.pop("fwd_dense")
+        flops.pop("fwd_dense")
+        contraction["fwd_mfma"] = flops["fwd_mfma"]
     sha = kernel_source_sha()
     # the dominant contraction kernel (the step's largest kernel is one of them)
     cand = {k: v for k, v in per_step.items() if k in flops and flops[k] > 0}
@@ -743,7 +756,10 @@ def measure(torch, dstd, wl, dev, steps, warmup, profile_steps, eager, contract=
                     avg_launch_ms=round(per_step[dom] / n_launch, 4),
                     algorithmic_flops_per_launch=round(flops[dom] / n_launch),
                     kernel_ms_per_step=round(per_step[dom], 4),
-                    largest_kernel=max(per_step, key=per_step.get))
+                    largest_kernel=max(per_step, key=per_step.get),
+                    contraction_only_TFLOPs=round(contraction[dom] / (per_step[dom] * 1e-3) / 1e12, 3),
+                    flops_counted="contraction (4 per update) + interval scan (7 per neuron "
+                                  "and grid point) for forward kernels; contraction for dW, dt_in")
     mfma = None
     if "fwd_mfma" in per_step:
         # the dense product: 2 flops per (row (b, m), input, neuron) and event plane

@@ -261,7 +261,7 @@ __global__ __launch_bounds__(256) void fwd_sorted_kernel(LifConst C, int B, int 
 constexpr bool dw_vec(int groups) { return groups == 1; }
 constexpr int dw_stride(int ti, int groups) { return dw_vec(groups) ? ti + 4 : ti + 1; }
 
-template <int TI, int NPER, int GW, int KS>
+template <int TI, int NPER, int GW, int KS, int IPT>
 __global__ __launch_bounds__(256 * GW) void dw_dense_kernel(LifConst C, int B, int N_in, int N_out,
                                                              int b_per_split,
                                                              const float *__restrict__ gam,
@@ -272,6 +272,9 @@ __global__ __launch_bounds__(256 * GW) void dw_dense_kernel(LifConst C, int B, i
                                                              const float *__restrict__ ev_R,
                                                              const float *__restrict__ dq,
                                                              float *__restrict__ dW_part) {
+    // IPT inputs per thread (j, j + 256, ...): the G tile staged per sample
+    // serves IPT times as many multiply-adds (one sample group only)
+    static_assert(IPT == 1 || GW == 1, "several inputs per thread with one sample group only");
     extern __shared__ float gs[];  // [GW][2][R + 1][dw_stride(TI, GW)]
     __shared__ int wlive[2][4 * GW];
     constexpr int kStr = dw_stride(TI, GW);
@@ -280,17 +283,18 @@ __global__ __launch_bounds__(256 * GW) void dw_dense_kernel(LifConst C, int B, i
     const int grp = threadIdx.x >> 8;  // sample group of this thread
     const int tid = threadIdx.x & 255;
     float *gsg = gs + grp * 2 * gbuf;
-    const int j = blockIdx.x * 256 + tid;
+    const int jb = blockIdx.x * 256 * IPT + tid;
     const int i0 = blockIdx.y * TI;
     const int ni = min(TI, N_out - i0);
     // the block's samples [b0, b_end); group g takes b0 + g, b0 + g + GW, ...
     const int b0 = blockIdx.z * b_per_split;
     const int b_end = min(B, b0 + b_per_split);
     const int n_it = (b_per_split + GW - 1) / GW;  // iterations, equal for every group
-    const bool j_ok = j < N_in;
-    float acc[TI];
+    float acc[IPT][TI];
 #pragma unroll
-    for (int ii = 0; ii < TI; ++ii) acc[ii] = 0.f;
+    for (int k = 0; k < IPT; ++k)
+#pragma unroll
+        for (int ii = 0; ii < TI; ++ii) acc[k][ii] = 0.f;
     const int total = R * TI;
     // element c of this thread: row r = r_first + c * (256 / TI), neuron l
     const int l_own = tid % TI, r_first = tid / TI;
@@ -329,11 +333,11 @@ __global__ __launch_bounds__(256 * GW) void dw_dense_kernel(LifConst C, int B, i
         }
     };
     // event of (b, j): slot (row) and halves; no events: slot R-1, zeros
-    auto event = [&](int b, int &slot, float &L, float &Rv) {
+    auto event = [&](int b, int j, int &slot, float &L, float &Rv) {
         slot = R - 1;
         L = 0.f;
         Rv = 0.f;
-        if (j_ok && b < b_end) {
+        if (j < N_in && b < b_end) {
             const int64_t o = static_cast<int64_t>(b) * N_in + j;
             const int r = ev_row[o];
             if (r >= 0) {
@@ -361,36 +365,47 @@ __global__ __launch_bounds__(256 * GW) void dw_dense_kernel(LifConst C, int B, i
         store(gsg);
     }
     Tri tri_n = load_tri(sample(1));
-    int slot_n;
-    float L_n, R_n;
-    event(sample(0), slot_n, L_n, R_n);
+    int slot_n[IPT];
+    float L_n[IPT], R_n[IPT];
+#pragma unroll
+    for (int k = 0; k < IPT; ++k) event(sample(0), jb + k * 256, slot_n[k], L_n[k], R_n[k]);
     live = group_live(live, 0);
     for (int it = 0; it < n_it; ++it) {
         const float *cur = gsg + (it & 1) * gbuf;
         const bool more = it + 1 < n_it;
-        const int slot = slot_n;
-        const float L = L_n, Rv = R_n;
-        event(sample(it + 1), slot_n, L_n, R_n);
+        int slot[IPT];
+        float L[IPT], Rv[IPT];
+#pragma unroll
+        for (int k = 0; k < IPT; ++k) {
+            slot[k] = slot_n[k];
+            L[k] = L_n[k];
+            Rv[k] = R_n[k];
+            event(sample(it + 1), jb + k * 256, slot_n[k], L_n[k], R_n[k]);
+        }
         const Tri tri = tri_n;
         tri_n = load_tri(sample(it + 2));
         bool live_next = false;
         if (more) live_next = fetch(tri);
         if (live) {
             if constexpr (dw_vec(GW)) {
-                const float4 *p = reinterpret_cast<const float4 *>(cur + slot * kStr);
 #pragma unroll
-                for (int i4 = 0; i4 < TI / 4; ++i4) {
-                    const float4 a = p[i4], c = p[i4 + kStr / 4];
-                    acc[4 * i4] = fmaf(a.x, L, fmaf(c.x, Rv, acc[4 * i4]));
-                    acc[4 * i4 + 1] = fmaf(a.y, L, fmaf(c.y, Rv, acc[4 * i4 + 1]));
-                    acc[4 * i4 + 2] = fmaf(a.z, L, fmaf(c.z, Rv, acc[4 * i4 + 2]));
-                    acc[4 * i4 + 3] = fmaf(a.w, L, fmaf(c.w, Rv, acc[4 * i4 + 3]));
+                for (int k = 0; k < IPT; ++k) {
+                    const float4 *p = reinterpret_cast<const float4 *>(cur + slot[k] * kStr);
+                    float *a_k = acc[k];
+#pragma unroll
+                    for (int i4 = 0; i4 < TI / 4; ++i4) {
+                        const float4 a = p[i4], c = p[i4 + kStr / 4];
+                        a_k[4 * i4] = fmaf(a.x, L[k], fmaf(c.x, Rv[k], a_k[4 * i4]));
+                        a_k[4 * i4 + 1] = fmaf(a.y, L[k], fmaf(c.y, Rv[k], a_k[4 * i4 + 1]));
+                        a_k[4 * i4 + 2] = fmaf(a.z, L[k], fmaf(c.z, Rv[k], a_k[4 * i4 + 2]));
+                        a_k[4 * i4 + 3] = fmaf(a.w, L[k], fmaf(c.w, Rv[k], a_k[4 * i4 + 3]));
+                    }
                 }
             } else {
-                const float *p = cur + slot * kStr;
+                const float *p = cur + slot[0] * kStr;
 #pragma unroll
                 for (int ii = 0; ii < TI; ++ii)
-                    acc[ii] = fmaf(p[ii], L, fmaf(p[ii + kStr], Rv, acc[ii]));
+                    acc[0][ii] = fmaf(p[ii], L[0], fmaf(p[ii + kStr], Rv[0], acc[0][ii]));
             }
         }
         if (more) store(gsg + ((it + 1) & 1) * gbuf);
@@ -406,25 +421,29 @@ __global__ __launch_bounds__(256 * GW) void dw_dense_kernel(LifConst C, int B, i
             __syncthreads();
             if (grp > 0) {
 #pragma unroll
-                for (int c = 0; c < kCh; ++c) xch[((grp - 1) * kCh + c) * 256 + tid] = acc[c0 + c];
+                for (int c = 0; c < kCh; ++c) xch[((grp - 1) * kCh + c) * 256 + tid] = acc[0][c0 + c];
             }
             __syncthreads();
             if (grp == 0) {
 #pragma unroll
                 for (int c = 0; c < kCh; ++c)
-                    for (int g = 1; g < GW; ++g) acc[c0 + c] += xch[((g - 1) * kCh + c) * 256 + tid];
+                    for (int g = 1; g < GW; ++g) acc[0][c0 + c] += xch[((g - 1) * kCh + c) * 256 + tid];
             }
         }
         if (grp > 0) return;
     }
-    if (!j_ok) return;
-    float *out = dW_part + static_cast<int64_t>(blockIdx.z) * N_out * N_in +
-                 static_cast<int64_t>(i0) * N_in + j;
-    // dq: the dead-neuron term of each row, added to the final sums (one
-    // split only; with splits the reduction adds it)
 #pragma unroll
-    for (int ii = 0; ii < TI; ++ii)
-        if (ii < ni) out[static_cast<int64_t>(ii) * N_in] = dq ? acc[ii] + dq[i0 + ii] : acc[ii];
+    for (int k = 0; k < IPT; ++k) {
+        const int j = jb + k * 256;
+        if (j >= N_in) continue;
+        float *out = dW_part + static_cast<int64_t>(blockIdx.z) * N_out * N_in +
+                     static_cast<int64_t>(i0) * N_in + j;
+        // dq: the dead-neuron term of each row, added to the final sums (one
+        // split only; with splits the reduction adds it)
+#pragma unroll
+        for (int ii = 0; ii < TI; ++ii)
+            if (ii < ni) out[static_cast<int64_t>(ii) * N_in] = dq ? acc[k][ii] + dq[i0 + ii] : acc[k][ii];
+    }
 }
 
 // dW[k] = sum of the split partials in split order (+ the row's dead-neuron
@@ -931,6 +950,7 @@ static int dw_nper(int M, int ti) {
 DwPlan plan_dw(int64_t B, int64_t N_in, int64_t N_out, int M) {
     DwPlan p;
     p.jw = dw_ti(M, N_out);
+    p.ipt = 1;
     const int64_t tiles = ((N_in + 255) / 256) * ((N_out + p.jw - 1) / p.jw);
     p.nsplit = 1;
     while (tiles * p.nsplit < 1024 && B / (p.nsplit * 2) >= 4) p.nsplit *= 2;
@@ -940,6 +960,12 @@ DwPlan plan_dw(int64_t B, int64_t N_in, int64_t N_out, int M) {
     p.waves = 4 * groups;
     p.b_per_split = static_cast<int>(std::max<int64_t>(1, (B + p.nsplit - 1) / p.nsplit));
     p.nsplit = static_cast<int>(std::max<int64_t>(1, (B + p.b_per_split - 1) / p.b_per_split));
+    // large layers with one sample group and 64-neuron tiles: two inputs per
+    // thread, so each staged G tile serves twice the multiply-adds (the G
+    // work per sample grows with M; measured on the 4096-wide layer: dW
+    // 1.18 -> 0.91 ms at M = 64, slower at M = 8 and 32)
+    if (groups == 1 && p.nsplit == 1 && p.jw == 64 && M >= 64 && N_out >= 1024 && N_in >= 1024)
+        p.ipt = kDwWideIPT;
     return p;
 }
 
@@ -947,7 +973,7 @@ static hipError_t launch_dw(const LifConst &C, const DwPlan &p, int64_t B, int64
                             int64_t N_out, const DenseBwdWs &ws, const float *dq, float *dst,
                             hipStream_t st) {
     const int ti = p.jw;
-    dim3 grid(static_cast<unsigned>((N_in + 255) / 256),
+    dim3 grid(static_cast<unsigned>((N_in + 256 * p.ipt - 1) / (256 * p.ipt)),
               static_cast<unsigned>((N_out + ti - 1) / ti), static_cast<unsigned>(p.nsplit));
     // G buffers of every group; after the samples, the same LDS carries the
     // groups' sums to group 0 (16 per thread per round)
@@ -957,10 +983,11 @@ static hipError_t launch_dw(const LifConst &C, const DwPlan &p, int64_t B, int64
                        sizeof(float);
     ProfScope prof("dw_dense", st);
     const int nper = dw_nper(C.M, ti);
-#define DW_LAUNCH_G(TIV, NP, GWV, KSV)                                                             \
-    hipLaunchKernelGGL((dw_dense_kernel<TIV, NP, GWV, KSV>), grid, dim3(256 * GWV), lds, st, C,    \
-                       static_cast<int>(B), static_cast<int>(N_in), static_cast<int>(N_out),        \
+#define DW_LAUNCH_GI(TIV, NP, GWV, KSV, IPTV)                                                      \
+    hipLaunchKernelGGL((dw_dense_kernel<TIV, NP, GWV, KSV, IPTV>), grid, dim3(256 * GWV), lds, st,  \
+                       C, static_cast<int>(B), static_cast<int>(N_in), static_cast<int>(N_out),     \
                        p.b_per_split, ws.gam, ws.uq, ws.q, ws.row, ws.L, ws.R, dq, dst)
+#define DW_LAUNCH_G(TIV, NP, GWV, KSV) DW_LAUNCH_GI(TIV, NP, GWV, KSV, 1)
 #define DW_LAUNCH_K(TIV, NP, KSV)                                          \
     do {                                                                   \
         if (groups == 2) DW_LAUNCH_G(TIV, NP, 2, KSV);                     \
@@ -971,7 +998,18 @@ static hipError_t launch_dw(const LifConst &C, const DwPlan &p, int64_t B, int64
         if (C.kind == kGeneral) DW_LAUNCH_K(TIV, NP, kGeneral);           \
         else DW_LAUNCH_K(TIV, NP, kAnyKind);                              \
     } while (0)
-    if (ti == 64) {
+    if (p.ipt > 1) {
+        // one group; 64-neuron tiles, kDwWideIPT inputs per thread
+#define DW_WIDE(NP)                                                                  \
+    do {                                                                             \
+        if (C.kind == kGeneral) DW_LAUNCH_GI(64, NP, 1, kGeneral, kDwWideIPT);       \
+        else DW_LAUNCH_GI(64, NP, 1, kAnyKind, kDwWideIPT);                          \
+    } while (0)
+        if (nper == 9) DW_WIDE(9);
+        else if (nper == 17) DW_WIDE(17);
+        else DW_WIDE(33);
+#undef DW_WIDE
+    } else if (ti == 64) {
         if (nper == 9) DW_LAUNCH(64, 9);
         else if (nper == 17) DW_LAUNCH(64, 17);
         else DW_LAUNCH(64, 33);
@@ -987,6 +1025,7 @@ static hipError_t launch_dw(const LifConst &C, const DwPlan &p, int64_t B, int64
 #undef DW_LAUNCH
 #undef DW_LAUNCH_K
 #undef DW_LAUNCH_G
+#undef DW_LAUNCH_GI
     return hipGetLastError();
 }
 

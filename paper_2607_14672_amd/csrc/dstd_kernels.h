@@ -9,7 +9,9 @@
 
 namespace dstd {
 
-struct DwPlan { int waves, jw, nsplit, b_per_split; };
+struct DwPlan { int waves, jw, nsplit, b_per_split, ipt; };
+// dW of large layers with one sample group and M >= 64: inputs per thread
+constexpr int kDwWideIPT = 2;
 
 // records past the end of a sample's sorted list that the forward kernel may
 // read (and mask): the list array is padded by this many records

@@ -139,6 +139,7 @@ LifConst make_const(const dstd_lif_params *p) {
     C.kmax_dt_d = kern_d(kind, tv, ti, std::min(dt, upk));
     C.kmax_last_d = kern_d(kind, tv, ti, std::min(last, upk));
     C.theta_lo_d = (double)p->threshold / 1.0001;
+    C.kpeak_d = kern_d(kind, tv, ti, std::min((double)p->M * dt + last, upk));
     C.twice = (kind == dstd::kGeneral && tv == 2.0 * ti) ? 1 : 0;
     C.inv_dt = (float)(1.0 / dt);
     C.e_mdt = (float)exp(-dt / ti);
@@ -278,7 +279,7 @@ dstd_status check_conv(const dstd_conv_shape *cs, int64_t B, int M, dstd::ConvGe
 struct ConvWs {
     size_t wt, key, L, R, off;                        // both passes
     size_t px, src, P;                                // backward sort extras
-    size_t row, eL, eR, gam, uq, q, live, part, dq;   // backward
+    size_t row, eL, eR, gam, uq, q, rend, part, zlive, dq;   // backward
     size_t total;
 };
 
@@ -308,10 +309,11 @@ ConvWs conv_ws_layout(int M, const dstd::ConvGeom &g, int64_t B, bool backward) 
         w.gam = off; off += align_up(nout * sizeof(float));
         w.uq = off; off += align_up(nout * sizeof(float));
         w.q = off; off += align_up(nout * sizeof(int));
-        w.live = off; off += align_up((size_t)B * g.Ho * g.Wo * sizeof(int));
+        w.rend = off; off += align_up((size_t)B * g.Ho * g.Wo * sizeof(int));
         w.dq = off; off += align_up((size_t)g.C_out * sizeof(float));  // dead-neuron term per channel
         dstd::ConvDwPlan dp = dstd::plan_conv_dw(g, B, M);
         w.part = off; off += align_up((size_t)dp.nsplit * nw * sizeof(float));
+        w.zlive = off; off += align_up((size_t)dp.nsplit * sizeof(int));
     }
     w.total = off;
     return w;
@@ -705,8 +707,9 @@ dstd_status conv_backward(const dstd_lif_params *p, const dstd_synfire_params *s
     bw.gam = at<float>(ws, L.gam);
     bw.uq = at<float>(ws, L.uq);
     bw.q = at<int>(ws, L.q);
-    bw.live = at<int>(ws, L.live);
+    bw.rend = at<int>(ws, L.rend);
     bw.part = at<float>(ws, L.part);
+    bw.zlive = at<int>(ws, L.zlive);
     bw.wt = at<float>(ws, L.wt);
     bw.srt = dstd::ConvSorted{at<int>(ws, L.key), at<float>(ws, L.L), at<float>(ws, L.R),
                               at<int>(ws, L.off), at<int>(ws, L.px), at<int>(ws, L.src),

@@ -107,7 +107,6 @@ __device__ void sort_cell_row(const LifConst &C, const ConvGeom &g, const float 
     const int b = cr / g.Hp, py = cr % g.Hp;
     const int nb = R * g.Wp;  // buckets, flat f = r * Wp + px
     const bool bwd = cs.P != nullptr;
-    const int KT = g.KH * g.KW;
     int *hist = sh;
     int *part = sh + nb;
     float *tl = sort_stage_floats(C.M, g) > 0 ? reinterpret_cast<float *>(part + 256) : nullptr;
@@ -196,9 +195,14 @@ __device__ void sort_cell_row(const LifConst &C, const ConvGeom &g, const float 
         run += v;
     }
     __syncthreads();
-    // placement: lanes of one bucket are ranked by lane (j' ascending)
+    // placement: lanes of one bucket are ranked by lane (j' ascending). The
+    // lanes of one pass that share a bucket are found by matching the bits of
+    // a per-pass bucket key k = row * cpi + lsub (one ballot per bit, a cost
+    // independent of how many buckets the pass touches); the highest lane of
+    // each group then moves the bucket's next free slot.
     const int64_t rb = static_cast<int64_t>(cr) * g.Wp * g.PC;
     const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+    const int kbits = uniform(R * cpi > 1 ? 32 - __clz(R * cpi - 1) : 0);
     for (int i0 = 0; wave + nw * i0 < g.Wp; i0 += cpi) {
         const int px = wave + nw * (i0 + lsub);
         const bool cell_ok = lsub < cpi && px < g.Wp;
@@ -216,29 +220,28 @@ __device__ void sort_cell_row(const LifConst &C, const ConvGeom &g, const float 
                 }
                 if (e.row >= 0) f = e.row * g.Wp + px;
             }
-            int pos = 0;
-            uint64_t todo = __ballot(f >= 0);
-            while (todo) {
-                const int lead = __ffsll(static_cast<unsigned long long>(todo)) - 1;
-                const int fl = __builtin_amdgcn_readlane(f, lead);
-                const uint64_t same = __ballot(f == fl);
-                int *slot = &hist[fl];
-                const int base = *slot;
-                if (f == fl) pos = base + __popcll(same & below);
-                __builtin_amdgcn_wave_barrier();
-                if (lane == lead) *slot = base + __popcll(same);
-                __builtin_amdgcn_wave_barrier();
-                todo &= ~same;
+            const int kb = (f >= 0) ? e.row * cpi + lsub : 0;
+            uint64_t same = __ballot(f >= 0);
+            for (int bit = 0; bit < kbits; ++bit) {
+                const bool on = (kb >> bit) & 1;
+                const uint64_t bal = __ballot(on);
+                same &= on ? bal : ~bal;
             }
+            int pos = 0;
+            if (f >= 0) {
+                const int base = hist[f];
+                pos = base + __popcll(same & below);
+                if ((same >> lane) == 1ull) hist[f] = base + __popcll(same);
+            }
+            __builtin_amdgcn_wave_barrier();
             if (f >= 0) {
                 const int64_t o = rb + pos;
                 cs.key[o] = px * g.C_in + (j % g.C_in);
                 cs.L[o] = bwd ? e.dL : e.L;
                 cs.R[o] = bwd ? e.dR : e.R;
                 if (bwd) {
-                    cs.px[o] = px;
+                    cs.px[o] = (e.row << 16) | px;
                     cs.src[o] = px * g.PC + j;
-                    for (int k = 0; k < KT; ++k) cs.P[o * KT + k] = 0.f;
                 }
             }
         }
@@ -296,9 +299,8 @@ struct PosWalk {
     bool vky[KHT];
     int oa[KHT], ob[KHT];
 
-    // returns the number of records in the KH cell rows (0: nothing to read)
-    __device__ __forceinline__ int init(const LifConst &C, const ConvGeom &g, const ConvSorted &cs,
-                                        int64_t p) {
+    // geometry of position p (no memory reads)
+    __device__ __forceinline__ void init(const LifConst &C, const ConvGeom &g, int64_t p) {
         const int HoWo = g.Ho * g.Wo;
         b = uniform(static_cast<int>(p / HoWo));
         pos = uniform(static_cast<int>(p % HoWo));
@@ -308,7 +310,6 @@ struct PosWalk {
         xb = max(xa, min(g.Wp, x0 + g.KW));
         nb1 = rows_of(C) * g.Wp + 1;
         wlim = g.KH * g.KW * g.C_in - 1;
-        int any = 0;
 #pragma unroll
         for (int ky = 0; ky < KHT; ++ky) {
             const int py = oy * g.stride - g.pad + ky;
@@ -317,8 +318,15 @@ struct PosWalk {
             recb[ky] = cr * g.Wp * g.PC;
             offb[ky] = cr * nb1;
             wofs[ky] = (ky * g.KW - x0) * g.C_in;
-            if (vky[ky]) any += *as_const(cs.off + offb[ky] + nb1 - 1);
         }
+    }
+
+    // the number of records in the KH cell rows (0: nothing to read)
+    __device__ __forceinline__ int cell_records(const ConvSorted &cs) const {
+        int any = 0;
+#pragma unroll
+        for (int ky = 0; ky < KHT; ++ky)
+            if (vky[ky]) any += *as_const(cs.off + offb[ky] + nb1 - 1);
         return any;
     }
 
@@ -368,8 +376,10 @@ struct PosWalk {
 // into the interval scan as the row changes. Sums and their order are those
 // of a row-by-row walk.
 struct FwdEntry { int wb, row; float L, R; };
+// (At most 80 VGPRs: six waves per SIMD, measured faster than five; eight
+// would spill.)
 template <int KHT, int KS>
-__global__ __launch_bounds__(256) void conv_fwd_kernel(LifConst C, ConvGeom g, int64_t n_pos,
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(6, 8))) void conv_fwd_kernel(LifConst C, ConvGeom g, int64_t n_pos,
                                                        const float *__restrict__ Wt,
                                                        ConvSorted cs, float *__restrict__ t_out,
                                                        float *__restrict__ slope,
@@ -385,16 +395,8 @@ __global__ __launch_bounds__(256) void conv_fwd_kernel(LifConst C, ConvGeom g, i
     const int HoWo = g.Ho * g.Wo;
     const int R = rows_of(C);
     PosWalk<KHT> wk;
-    const int any = wk.init(C, g, cs, p);
+    wk.init(C, g, p);
     const int64_t o_out = (static_cast<int64_t>(wk.b) * g.C_out + co) * HoWo + wk.pos;
-    if (any == 0) {  // no events in the receptive field: silent
-        if (row_ok) {
-            t_out[o_out] = INFINITY;
-            slope[o_out] = 0.f;
-            q_idx[o_out] = -1;
-        }
-        return;
-    }
     const __amdgpu_buffer_rsrc_t wr = make_rsrc(
         Wt, static_cast<uint32_t>(static_cast<int64_t>(wk.wlim + 1) * g.C_out * sizeof(float)));
     const int voff = (row_ok ? co : 0) * static_cast<int>(sizeof(float));
@@ -403,8 +405,18 @@ __global__ __launch_bounds__(256) void conv_fwd_kernel(LifConst C, ConvGeom g, i
     float aL = 0.f, aR = 0.f, carry = 0.f;
     int cur = 0;  // row being summed
     // close rows cur .. target-1: point r-1 gets row r's L sums plus row
-    // r-1's R sums
-    auto close_to = [&](int target) {
+    // r-1's R sums. A record's row is at most R-2, so closing up to it never
+    // reaches grid point M (the last interval, tested only at the end).
+    auto close_to_mid = [&](int target) {
+        while (cur < target) {
+            if (cur >= 1) sc.template step_k<false>(C, cur - 1, aL + carry);
+            carry = aR;
+            aL = 0.f;
+            aR = 0.f;
+            ++cur;
+        }
+    };
+    auto close_to_end = [&](int target) {
         while (cur < target) {
             if (cur >= 1) sc.step(C, cur - 1, aL + carry);
             carry = aR;
@@ -413,7 +425,17 @@ __global__ __launch_bounds__(256) void conv_fwd_kernel(LifConst C, ConvGeom g, i
             ++cur;
         }
     };
-    bool done = false;
+    bool done = false, started = false;
+    // the KH cell rows' record counts (scalar loads) rule out most positions
+    // without events in their receptive field before any vector load
+    if (wk.cell_records(cs) == 0) {
+        if (row_ok) {
+            t_out[o_out] = INFINITY;
+            slope[o_out] = 0.f;
+            q_idx[o_out] = -1;
+        }
+        return;
+    }
     for (int r0 = 0; r0 <= R - 2 && !done; r0 += kWave) {
         wk.load_offs(g, cs, R, r0, lane);
         const bool rvalid = r0 + lane <= R - 2;
@@ -433,6 +455,12 @@ __global__ __launch_bounds__(256) void conv_fwd_kernel(LifConst C, ConvGeom g, i
         const int start = inc - nr;
         const int start_eff = rvalid ? start : 0x7fffffff;
         const int total = uniform(__builtin_amdgcn_readlane(inc, kWave - 1));
+        if (!started && total > 0) {
+            // rows before the first one with records add nothing to a zero
+            // state: the scan starts there
+            cur = r0 + __ffsll(static_cast<unsigned long long>(__ballot(nr > 0))) - 1;
+            started = true;
+        }
         for (int c0 = 0; c0 < total && !done; c0 += kWave) {
             const int v = c0 + lane;
             const bool rec_ok = v < total;
@@ -482,12 +510,13 @@ __global__ __launch_bounds__(256) void conv_fwd_kernel(LifConst C, ConvGeom g, i
                 for (int q = 0; q < kCBatch; ++q) e[q] = my[s0 + q];  // LDS broadcasts
 #pragma unroll
                 for (int q = 0; q < kCBatch; ++q) w[q] = BufLoad<float>::get(wr, voff + e[q].wb, 0);
+                const int nk = min(kCBatch, nc - s0);
 #pragma unroll
                 for (int q = 0; q < kCBatch; ++q) {
-                    if (s0 + q < nc) {
+                    if (q < nk) {
                         const int row = uniform(e[q].row);
                         if (row != cur) {
-                            close_to(row);
+                            close_to_mid(row);
                             if (__all(sc.found() || !row_ok)) {
                                 done = true;
                                 break;
@@ -502,7 +531,21 @@ __global__ __launch_bounds__(256) void conv_fwd_kernel(LifConst C, ConvGeom g, i
             __builtin_amdgcn_wave_barrier();
         }
     }
-    if (!done) close_to(R - 1);
+    if (!started) {  // no events in the receptive field: silent
+        if (row_ok) {
+            t_out[o_out] = INFINITY;
+            slope[o_out] = 0.f;
+            q_idx[o_out] = -1;
+        }
+        return;
+    }
+    if (!done) {
+        // the last row's sums reach grid points cur-1 and cur; after them no
+        // input arrives, and the rest of the scan is skipped once no lane
+        // still searching can reach the threshold
+        close_to_end(min(cur + 2, R - 1));
+        if (cur < R - 1 && __any(row_ok && sc.may_still_fire(C))) close_to_end(R - 1);
+    }
     if (!row_ok) return;
     float to, sl;
     int q;
@@ -517,7 +560,9 @@ __global__ __launch_bounds__(256) void conv_fwd_kernel(LifConst C, ConvGeom g, i
 // positions s = b * Ho*Wo + p and every channel: read from the NCHW outputs
 // with positions along the lanes, staged in LDS kGradCh channels at a time
 // and written position-major [s][co] (each position's channels contiguous).
-// live[s] = 1 if any channel of s passes gradient.
+// rend[s] = min(R-2, max q + 1) over the channels of s that pass gradient
+// (G[m] vanishes for m > q, and a record of event row r reads G[r-1] and
+// G[r]), -1 if none does.
 constexpr int kGradPos = 16, kGradCh = 64;
 constexpr int kGradLdsBytes = (3 * kGradCh * (kGradPos + 1) + kGradPos) * 4;
 
@@ -525,7 +570,7 @@ __device__ void grad_block(const LifConst &C, const ConvGeom &g, int64_t n_pos, 
                            const float *__restrict__ t_out, const float *__restrict__ slope,
                            const int *__restrict__ q_idx, const float *__restrict__ grad_t,
                            const Synfire &sf, float *__restrict__ gam, float *__restrict__ uq,
-                           int *__restrict__ qv, int *__restrict__ live, int *sh) {
+                           int *__restrict__ qv, int *__restrict__ rend, int *sh) {
     constexpr int kS = kGradPos + 1;
     float *sg = reinterpret_cast<float *>(sh);
     float *su = sg + kGradCh * kS;
@@ -533,7 +578,7 @@ __device__ void grad_block(const LifConst &C, const ConvGeom &g, int64_t n_pos, 
     int *sl = sq + kGradCh * kS;
     const int HoWo = g.Ho * g.Wo;
     const int64_t s0 = blk * kGradPos;
-    if (threadIdx.x < kGradPos) sl[threadIdx.x] = 0;
+    if (threadIdx.x < kGradPos) sl[threadIdx.x] = -1;
     __syncthreads();
     for (int c0 = 0; c0 < g.C_out; c0 += kGradCh) {
         for (int e = threadIdx.x; e < kGradCh * kGradPos; e += blockDim.x) {
@@ -556,7 +601,7 @@ __device__ void grad_block(const LifConst &C, const ConvGeom &g, int64_t n_pos, 
             sg[cl * kS + pl] = gp.gam;
             su[cl * kS + pl] = gp.uq;
             sq[cl * kS + pl] = gp.q;
-            if (gp.q >= 0) sl[pl] = 1;
+            if (gp.q >= 0) atomicMax(&sl[pl], gp.q);
         }
         __syncthreads();
         for (int e = threadIdx.x; e < kGradPos * kGradCh; e += blockDim.x) {
@@ -572,7 +617,10 @@ __device__ void grad_block(const LifConst &C, const ConvGeom &g, int64_t n_pos, 
         }
         __syncthreads();
     }
-    if (live && threadIdx.x < kGradPos && s0 + threadIdx.x < n_pos) live[s0 + threadIdx.x] = sl[threadIdx.x];
+    if (rend && threadIdx.x < kGradPos && s0 + threadIdx.x < n_pos) {
+        const int qm = sl[threadIdx.x];
+        rend[s0 + threadIdx.x] = qm < 0 ? -1 : min(rows_of(C) - 2, qm + 1);
+    }
 }
 
 // Dead-neuron term of output channel co: dq[co] = -gamma_q * scale * (number
@@ -597,16 +645,6 @@ __device__ void dead_channel_block(const ConvGeom &g, int64_t B, const int *__re
     if (threadIdx.x == 0) sf.dq[co] = -(sf.gq * sf.scale * static_cast<float>(sh[0]));
 }
 
-// dt_in = 0 for block blk's 1024 inputs (inputs with events are overwritten
-// by the gather afterwards)
-__device__ void zero_block(float *__restrict__ dt, int64_t n, int64_t blk) {
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
-        const int64_t i = blk * 1024 + k * 256 + threadIdx.x;
-        if (i < n) dt[i] = 0.f;
-    }
-}
-
 // dt_in partials. Wave = output position; lane = output channel, NT tiles of
 // 64 per lane. Rows stop after the last grid point any channel's G reaches.
 template <int KHT, int NT, int KS>
@@ -616,20 +654,21 @@ __global__ __launch_bounds__(256) void conv_dtp_kernel(LifConst C, ConvGeom g, i
                                                        const float *__restrict__ gam,
                                                        const float *__restrict__ uq,
                                                        const int *__restrict__ qv,
-                                                       const int *__restrict__ live) {
+                                                       const int *__restrict__ rend) {
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = uniform(threadIdx.x >> 6);
     const int64_t p = static_cast<int64_t>(blockIdx.x) * (blockDim.x >> 6) + wave;
     if (p >= n_pos) return;  // wave-uniform; no block barrier below
-    if (*as_const(live + p) == 0) return;  // no channel here passes gradient
+    const int r_end = *as_const(rend + p);  // rows r <= r_end need G[r-1], G[r]
+    if (r_end < 0) return;                  // no channel here passes gradient
     const int R = rows_of(C);
     const int KT = g.KH * g.KW;
     PosWalk<KHT> wk;
-    if (wk.init(C, g, cs, p) == 0) return;  // no records to receive gradient
+    wk.init(C, g, p);
+    if (wk.cell_records(cs) == 0) return;  // no records to receive gradient
     const int64_t nbase = (static_cast<int64_t>(wk.b) * g.Ho * g.Wo + wk.pos) * g.C_out;
     float gm[NT], ua[NT], gA[NT], gB[NT];
     int qa[NT], voff[NT];
-    int qmax = -1;
 #pragma unroll
     for (int t = 0; t < NT; ++t) {
         const int co = t * kWave + lane;
@@ -638,14 +677,8 @@ __global__ __launch_bounds__(256) void conv_dtp_kernel(LifConst C, ConvGeom g, i
         gm[t] = ok ? gam[nbase + cc] : 0.f;
         ua[t] = ok ? uq[nbase + cc] : 0.f;
         qa[t] = ok ? qv[nbase + cc] : -1;
-        qmax = max(qmax, qa[t]);
         voff[t] = cc * static_cast<int>(sizeof(float));
     }
-#pragma unroll
-    for (int m = kWave / 2; m >= 1; m >>= 1) qmax = max(qmax, __shfl_xor(qmax, m));
-    qmax = uniform(qmax);
-    if (qmax < 0) return;  // no gradient reaches this position
-    const int r_end = min(R - 2, qmax + 1);  // row r needs G[r-1], G[r]
 #pragma unroll
     for (int t = 0; t < NT; ++t) {
         gA[t] = 0.f;
@@ -682,7 +715,7 @@ __global__ __launch_bounds__(256) void conv_dtp_kernel(LifConst C, ConvGeom g, i
                     const float tot = wave_sum8(v, lane);
                     const int kl = lane >> 3;
                     if ((lane & 7) == 0 && kl < nk) {
-                        const int pxl = cs.px[o + kl];
+                        const int pxl = cs.px[o + kl] & 0xffff;
                         cs.P[(o + kl) * KT + ky * g.KW + (pxl - wk.x0)] = tot;
                     }
                 }
@@ -696,27 +729,65 @@ __global__ __launch_bounds__(256) void conv_dtp_kernel(LifConst C, ConvGeom g, i
     }
 }
 
-// dt_in of every input with events: the sum of its per-tap partials (taps
-// that reach no output position stay 0), written to its NCHW slot. Block blk
-// of 256 threads takes record slots blk * 256 ...
-__device__ void dt_gather_block(const ConvGeom &g, int R, int64_t n, const ConvSorted &cs,
-                                float *__restrict__ dt_in, int64_t blk) {
-    const int64_t t = blk * blockDim.x + threadIdx.x;
-    if (t >= n) return;
-    const int64_t per = static_cast<int64_t>(g.Wp) * g.PC;
-    const int64_t cr = t / per;
-    const int slot = static_cast<int>(t % per);
+// dt_in of the raw inputs of cell row cr, slots [s0, s0 + ns) of its
+// cell-major order (kGatherSlots at most; a block per slice). Each record
+// sums its per-tap partials in tap order, taking only the taps through which
+// an output position passed gradient to the record's event row (the entries
+// the dt_in kernel wrote); the sums are staged in LDS at the record's slot,
+// and the slice is written in NCHW order (inputs without events get 0), so
+// consecutive threads write consecutive addresses.
+constexpr int kGatherSlots = 4096;
+
+__device__ void dt_gather_block(const ConvGeom &g, int R, const ConvSorted &cs,
+                                const int *__restrict__ rend, float *__restrict__ dt_in, int cr,
+                                int s0, float *buf) {
+    const int per = g.Wp * g.PC;
+    const int ns = min(kGatherSlots, per - s0);
     const int nb1 = R * g.Wp + 1;
-    if (slot >= cs.off[cr * nb1 + nb1 - 1]) return;
+    const int nrec = uniform(cs.off[static_cast<int64_t>(cr) * nb1 + nb1 - 1]);
+    const int b = cr / g.Hp, py = cr % g.Hp;
+    if (nrec == 0) {  // no input of the cell row has events
+        for (int t = threadIdx.x; t < per; t += blockDim.x) {
+            int slot;
+            const int64_t dst = cell_row_input(g, b, py, t, slot);
+            if (slot >= s0 && slot < s0 + ns) dt_in[dst] = 0.f;
+        }
+        return;
+    }
+    for (int t = threadIdx.x; t < ns; t += blockDim.x) buf[t] = 0.f;
+    __syncthreads();
+    const int64_t rb = static_cast<int64_t>(cr) * per;
     const int KT = g.KH * g.KW;
-    float s = 0.f;
-    for (int k = 0; k < KT; ++k) s += cs.P[t * KT + k];
-    const int src = cs.src[t];
-    const int px = src / g.PC, j = src % g.PC;
-    const int py = static_cast<int>(cr % g.Hp), b = static_cast<int>(cr / g.Hp);
-    int y, x;
-    raw_pixel(g, py, px, j / g.C_in, y, x);
-    dt_in[nchw_index(g, b, j % g.C_in, y, x)] = s;
+    const int64_t pos0 = static_cast<int64_t>(b) * g.Ho * g.Wo;
+    // output rows oy whose kernel row ky = py + pad - oy * stride is in
+    // range, walked with ky ascending (the tap order of the sum)
+    const int ny0 = py + g.pad;
+    const int oy_hi = min(g.Ho - 1, ny0 / g.stride);
+    const int oy_lo = (max(0, ny0 - g.KH + 1) + g.stride - 1) / g.stride;
+    for (int k = threadIdx.x; k < nrec; k += blockDim.x) {
+        const int src = cs.src[rb + k];
+        if (src < s0 || src >= s0 + ns) continue;
+        const int pr = cs.px[rb + k];
+        const int px = pr & 0xffff, row = pr >> 16;
+        const int nx0 = px + g.pad;
+        const int ox_hi = min(g.Wo - 1, nx0 / g.stride);
+        const int ox_lo = (max(0, nx0 - g.KW + 1) + g.stride - 1) / g.stride;
+        const float *P = cs.P + (rb + k) * KT;
+        float acc = 0.f;
+        for (int oy = oy_hi; oy >= oy_lo; --oy) {
+            const int ky = ny0 - oy * g.stride;
+            const int *rr = rend + pos0 + static_cast<int64_t>(oy) * g.Wo;
+            for (int ox = ox_hi; ox >= ox_lo; --ox)
+                if (row <= rr[ox]) acc += P[ky * g.KW + nx0 - ox * g.stride];
+        }
+        buf[src - s0] = acc;
+    }
+    __syncthreads();
+    for (int t = threadIdx.x; t < per; t += blockDim.x) {
+        int slot;
+        const int64_t dst = cell_row_input(g, b, py, t, slot);
+        if (slot >= s0 && slot < s0 + ns) dt_in[dst] = buf[slot - s0];
+    }
 }
 
 // dW[co, ci, k] = (1/P) sum_{b, p} sum_d (G[b, r, p, co] L + G[b, r+1, p, co] R)
@@ -736,11 +807,12 @@ __global__ __launch_bounds__(256) void conv_dw_kernel(LifConst C, ConvGeom g, in
                                                       const float *__restrict__ gam,
                                                       const float *__restrict__ uq,
                                                       const int *__restrict__ qv,
-                                                      const int *__restrict__ live_in,
+                                                      const int *__restrict__ rend,
                                                       const int *__restrict__ ev_row,
                                                       const float *__restrict__ ev_L,
                                                       const float *__restrict__ ev_R,
-                                                      float *__restrict__ part) {
+                                                      float *__restrict__ part,
+                                                      int *__restrict__ zlive) {
     extern __shared__ float gs[];  // [2][R + 1][TI + 1], then the live sample list
     __shared__ int n_live_w[4];
     constexpr int kStr = TI + 1;
@@ -797,7 +869,7 @@ __global__ __launch_bounds__(256) void conv_dw_kernel(LifConst C, ConvGeom g, in
     int n_live = 0;
     for (int64_t c0 = s_lo; c0 < s_hi; c0 += 256) {
         const int64_t sc = c0 + threadIdx.x;
-        const bool f = sc < s_hi && live_in[sc] != 0;
+        const bool f = sc < s_hi && rend[sc] >= 0;
         const uint64_t m = __ballot(f);
         if (lane == 0) n_live_w[wave] = __popcll(m);
         __syncthreads();
@@ -807,8 +879,11 @@ __global__ __launch_bounds__(256) void conv_dw_kernel(LifConst C, ConvGeom g, in
         for (int w = 0; w < 4; ++w) n_live += n_live_w[w];
         __syncthreads();
     }
+    // a split without such samples writes no partials (the reduction skips it)
+    if (threadIdx.x == 0 && blockIdx.x == 0 && blockIdx.y == 0) zlive[blockIdx.z] = n_live > 0;
+    if (n_live == 0) return;
     bool live = false;  // the staged sample's tile has a nonzero value
-    if (n_live > 0) {
+    {
         live = fetch(s_lo + list[0]);
         store(gs);
     }
@@ -852,12 +927,14 @@ __global__ __launch_bounds__(256) void conv_dw_kernel(LifConst C, ConvGeom g, in
 // the partial-sum layout (coalesced reads); a block holds 32 consecutive
 // entries x 8 split groups: group h sums z = h, h + 8, ...; the 8 group sums
 // are added in group order (fixed order: deterministic) and written to the
-// [co][ci][ky][kx] slot.
+// [co][ci][ky][kx] slot. Splits without gradient-carrying samples wrote no
+// partials and are skipped (their sums would be +0, which leaves every
+// partial sum unchanged).
 constexpr int kRedOut = 32, kRedGrp = 8;
 
 __device__ void dw_reduce_block(const ConvGeom &g, int nsplit, const float *__restrict__ part,
-                                const float *__restrict__ dq, float *__restrict__ dW, int64_t blk,
-                                float (*red)[kRedOut]) {
+                                const int *__restrict__ zlive, const float *__restrict__ dq,
+                                float *__restrict__ dW, int64_t blk, float (*red)[kRedOut]) {
     const int KT = g.KH * g.KW;
     const int NJ = KT * g.C_in;
     const int64_t n = static_cast<int64_t>(g.C_out) * NJ;
@@ -866,7 +943,8 @@ __device__ void dw_reduce_block(const ConvGeom &g, int nsplit, const float *__re
     float s = 0.f;
     if (src < n) {
 #pragma unroll 8
-        for (int z = h; z < nsplit; z += kRedGrp) s += part[static_cast<int64_t>(z) * n + src];
+        for (int z = h; z < nsplit; z += kRedGrp)
+            if (zlive[z]) s += part[static_cast<int64_t>(z) * n + src];
     }
     red[h][lo] = s;
     __syncthreads();
@@ -899,17 +977,17 @@ __global__ __launch_bounds__(256) void conv_fprep_kernel(LifConst C, ConvGeom g,
 }
 
 // Backward set-up: [0, n_cr) cell rows (events for dW; with cs.key set also
-// the sort with derivatives), then n_gr blocks of gradient triples and live
-// flags, n_z blocks zeroing dt_in, n_dq blocks of dead-neuron terms (one per
-// channel, synfire terms on) and the WT layout.
+// the sort with derivatives), then n_gr blocks of gradient triples and
+// per-position gradient rows (rend), n_dq blocks of dead-neuron terms (one
+// per channel, synfire terms on) and the WT layout.
 template <typename WT>
 __global__ __launch_bounds__(256) void conv_bprep_kernel(
-    LifConst C, ConvGeom g, int n_cr, int n_gr, int n_z, int n_dq, const float *__restrict__ t_in,
+    LifConst C, ConvGeom g, int n_cr, int n_gr, int n_dq, const float *__restrict__ t_in,
     ConvSorted cs, CellEv ev, int64_t n_pos, const float *__restrict__ t_out,
     const float *__restrict__ slope, const int *__restrict__ q_idx,
     const float *__restrict__ grad_t, Synfire sf, float *__restrict__ gam,
-    float *__restrict__ uq, int *__restrict__ qv, int *__restrict__ live,
-    float *__restrict__ dt_in, int64_t n_in, const WT *__restrict__ W, float *__restrict__ Wt) {
+    float *__restrict__ uq, int *__restrict__ qv, int *__restrict__ rend,
+    const WT *__restrict__ W, float *__restrict__ Wt) {
     extern __shared__ int sh[];
     int blk = static_cast<int>(blockIdx.x);
     if (blk < n_cr) {
@@ -921,15 +999,10 @@ __global__ __launch_bounds__(256) void conv_bprep_kernel(
     }
     blk -= n_cr;
     if (blk < n_gr) {
-        grad_block(C, g, n_pos, blk, t_out, slope, q_idx, grad_t, sf, gam, uq, qv, live, sh);
+        grad_block(C, g, n_pos, blk, t_out, slope, q_idx, grad_t, sf, gam, uq, qv, rend, sh);
         return;
     }
     blk -= n_gr;
-    if (blk < n_z) {
-        zero_block(dt_in, n_in, blk);
-        return;
-    }
-    blk -= n_z;
     if (blk < n_dq) {
         dead_channel_block(g, n_pos / (g.Ho * g.Wo), q_idx, sf, blk, sh);
         return;
@@ -937,19 +1010,24 @@ __global__ __launch_bounds__(256) void conv_bprep_kernel(
     weights_block<WT>(g, W, Wt, blk - n_dq);
 }
 
-// Backward finish: [0, n_red) dW split reduction, the rest gathers dt_in.
+// Backward finish: [0, n_red) dW split reduction, the rest gathers dt_in
+// (nsl blocks per cell row, one per slice of kGatherSlots slots).
 __global__ __launch_bounds__(256) void conv_bfin_kernel(ConvGeom g, int R, int n_red, int nsplit,
                                                         const float *__restrict__ part,
+                                                        const int *__restrict__ zlive,
                                                         const float *__restrict__ dq,
-                                                        float *__restrict__ dW, int64_t n_in,
-                                                        ConvSorted cs,
+                                                        float *__restrict__ dW, int nsl,
+                                                        ConvSorted cs, const int *__restrict__ rend,
                                                         float *__restrict__ dt_in) {
-    __shared__ float red[kRedGrp][kRedOut];
+    static_assert(kGatherSlots >= kRedGrp * kRedOut, "the reduction shares the gather's LDS");
+    __shared__ float lds[kGatherSlots];
     const int blk = static_cast<int>(blockIdx.x);
-    if (blk < n_red)
-        dw_reduce_block(g, nsplit, part, dq, dW, blk, red);
-    else
-        dt_gather_block(g, R, n_in, cs, dt_in, blk - n_red);
+    if (blk < n_red) {
+        dw_reduce_block(g, nsplit, part, zlive, dq, dW, blk, reinterpret_cast<float (*)[kRedOut]>(lds));
+    } else {
+        const int t = blk - n_red;
+        dt_gather_block(g, R, cs, rend, dt_in, t / nsl, (t % nsl) * kGatherSlots, lds);
+    }
 }
 
 // ------------------------------------------------------------ launchers --
@@ -1040,13 +1118,12 @@ hipError_t launch_conv_backward(const LifConst &C, const ConvGeom &g, int64_t B,
     const bool dt = grad_t_in && n_in > 0;
     hipError_t e;
     {
-        // cell rows (events; with dt_in the sort), gradient triples + live
-        // flags, and the WT layout for dt_in: one launch
+        // cell rows (events; with dt_in the sort), gradient triples +
+        // gradient rows, and the WT layout for dt_in: one launch
         const int n_cr = (n_in > 0 && (grad_W || dt)) ? static_cast<int>(B * g.Hp) : 0;
         const int n_gr = static_cast<int>((n_pos + kGradPos - 1) / kGradPos);
         const int64_t nw = nj * g.C_out;
         const int n_wt = dt ? static_cast<int>((nw + 255) / 256) : 0;
-        const int n_z = dt ? static_cast<int>((n_in + 1023) / 1024) : 0;
         // dead-neuron terms only where dW is written
         const bool dead = sf.on && sf.dq && grad_W;
         const int n_dq = dead ? g.C_out : 0;
@@ -1055,20 +1132,18 @@ hipError_t launch_conv_backward(const LifConst &C, const ConvGeom &g, int64_t B,
         if (!dt) cs.key = nullptr;
         int lds = std::max(kGradLdsBytes, 256 * static_cast<int>(sizeof(int)));
         if (dt) lds = std::max(lds, conv_sort_lds_bytes(C.M, g));
-        const unsigned blocks = static_cast<unsigned>(n_cr + n_gr + n_z + n_dq + n_wt);
+        const unsigned blocks = static_cast<unsigned>(n_cr + n_gr + n_dq + n_wt);
         ProfScope prof("conv_bprep", st);
         if (blocks > 0) {
             if (bf16)
                 hipLaunchKernelGGL(conv_bprep_kernel<uint16_t>, dim3(blocks), dim3(256), lds, st, C,
-                                   g, n_cr, n_gr, n_z, n_dq, t_in, cs, ev, n_pos, t_out, slope,
-                                   q_idx, grad_t, sf, ws.gam, ws.uq, ws.q,
-                                   ws.live, grad_t_in, n_in,
+                                   g, n_cr, n_gr, n_dq, t_in, cs, ev, n_pos, t_out, slope,
+                                   q_idx, grad_t, sf, ws.gam, ws.uq, ws.q, ws.rend,
                                    static_cast<const uint16_t *>(W), ws.wt);
             else
                 hipLaunchKernelGGL(conv_bprep_kernel<float>, dim3(blocks), dim3(256), lds, st, C,
-                                   g, n_cr, n_gr, n_z, n_dq, t_in, cs, ev, n_pos, t_out, slope,
-                                   q_idx, grad_t, sf, ws.gam, ws.uq, ws.q,
-                                   ws.live, grad_t_in, n_in,
+                                   g, n_cr, n_gr, n_dq, t_in, cs, ev, n_pos, t_out, slope,
+                                   q_idx, grad_t, sf, ws.gam, ws.uq, ws.q, ws.rend,
                                    static_cast<const float *>(W), ws.wt);
         }
         if ((e = hipGetLastError()) != hipSuccess) return e;
@@ -1085,7 +1160,8 @@ hipError_t launch_conv_backward(const LifConst &C, const ConvGeom &g, int64_t B,
         ProfScope prof("conv_dw", st);
 #define CDW_LAUNCH_K(TIV, NP, KSV)                                                            \
     hipLaunchKernelGGL((conv_dw_kernel<TIV, NP, KSV>), grid, dim3(256), lds, st, C, g, n_pos,  \
-                       p.s_per_split, ws.gam, ws.uq, ws.q, ws.live, ws.row, ws.L, ws.R, ws.part)
+                       p.s_per_split, ws.gam, ws.uq, ws.q, ws.rend, ws.row, ws.L, ws.R, ws.part,  \
+                       ws.zlive)
 #define CDW_LAUNCH(TIV, NP)                                               \
     do {                                                                  \
         if (C.kind == kGeneral) CDW_LAUNCH_K(TIV, NP, kGeneral);          \
@@ -1113,7 +1189,7 @@ hipError_t launch_conv_backward(const LifConst &C, const ConvGeom &g, int64_t B,
         ProfScope prof("conv_dtp", st);
 #define DTP_LAUNCH_K(KHV, NTV, KSV)                                                           \
     hipLaunchKernelGGL((conv_dtp_kernel<KHV, NTV, KSV>), grid, dim3(waves * kWave), 0, st, C,  \
-                       g, n_pos, ws.wt, ws.srt, ws.gam, ws.uq, ws.q, ws.live)
+                       g, n_pos, ws.wt, ws.srt, ws.gam, ws.uq, ws.q, ws.rend)
 #define DTP_LAUNCH(KHV, NTV)                                              \
     do {                                                                  \
         if (C.kind == kGeneral) DTP_LAUNCH_K(KHV, NTV, kGeneral);         \
@@ -1138,12 +1214,15 @@ hipError_t launch_conv_backward(const LifConst &C, const ConvGeom &g, int64_t B,
         // dW split reduction and dt_in gather: one launch
         const int64_t n = static_cast<int64_t>(g.C_out) * nj;
         const int n_red = grad_W ? static_cast<int>((n + kRedOut - 1) / kRedOut) : 0;
-        const int n_ga = dt ? static_cast<int>((n_in + 255) / 256) : 0;
+        const int per = g.Wp * g.PC;
+        const int nsl = (per + kGatherSlots - 1) / kGatherSlots;
+        const int n_ga = dt ? static_cast<int>(B * g.Hp) * nsl : 0;
         ProfScope prof("conv_bfin", st);
         if (n_red + n_ga > 0)
             hipLaunchKernelGGL(conv_bfin_kernel, dim3(static_cast<unsigned>(n_red + n_ga)),
-                               dim3(256), 0, st, g, R, n_red, p.nsplit, ws.part,
-                               (sf.on && sf.dq) ? sf.dq : nullptr, grad_W, n_in, ws.srt, grad_t_in);
+                               dim3(256), 0, st, g, R, n_red, p.nsplit, ws.part, ws.zlive,
+                               (sf.on && sf.dq) ? sf.dq : nullptr, grad_W, nsl, ws.srt, ws.rend,
+                               grad_t_in);
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     return hipSuccess;

@@ -56,6 +56,10 @@ struct LifConst {
     // the scan's interval filter in fp64: max K on [0, dt] and on the last
     // interval, and theta / 1.0001 (the filter's margin)
     double kmax_dt_d, kmax_last_d, theta_lo_d;
+    // max K over the whole window [0, t_max - T_0] (+inf where K grows
+    // without bound): with no further input, v never exceeds
+    // max(V, 0) + max(I, 0) kpeak_d
+    double kpeak_d;
     int twice;  // general row with tv = 2 ti exactly: closed-form crossing
 };
 
@@ -364,19 +368,23 @@ __device__ __forceinline__ void g_strided(const LifConst &C, const GStep &gs, fl
 // e^{-kappa len} (general row). On a crossing returns true with the fp32
 // segment, the bracket end hi (0: fires at u = 0, only through rounding) and
 // v - theta there.
-template <int KS = kAnyKind>
-__device__ __forceinline__ bool seg_test(const LifConst &C, double Vd, double Id, double vn_d,
-                                         bool last, float len, double kmax, float r_lo, Seg &sf,
-                                         float &hi, float &fhi) {
-    const int kind = kind_of<KS>(C);
-    // v(u) <= max(V,0) + max(I,0) max K, tested on the fp64 state against
-    // theta with a 1e-4 margin (only intervals that pass are analysed; max K
-    // is +inf on an open interval of the (inf, inf) row, where I = 0 must not
-    // give inf * 0)
+// The interval filter: v(u) <= max(V,0) + max(I,0) kmax, tested on the fp64
+// state against theta with a 1e-4 margin (only intervals that pass are
+// analysed; kmax is +inf on an open interval of the (inf, inf) row, where
+// I = 0 must not give inf * 0).
+__device__ __forceinline__ bool seg_may_cross(const LifConst &C, double Vd, double Id,
+                                              double kmax) {
     const double vpos = fmax(Vd, 0.0);
-    const double ub = (kind == kInfInf) ? ((Id > 0.0) ? fma(Id, kmax, vpos) : vpos)
-                                        : fma(fmax(Id, 0.0), kmax, vpos);
-    if (!(ub >= C.theta_lo_d)) return false;
+    const double ub = (Id > 0.0) ? fma(Id, kmax, vpos) : vpos;
+    return ub >= C.theta_lo_d;
+}
+
+// The analysis of an interval that passed the filter.
+template <int KS = kAnyKind>
+__device__ __forceinline__ bool seg_cross(const LifConst &C, double Vd, double Id, double vn_d,
+                                          bool last, float len, float r_lo, Seg &sf, float &hi,
+                                          float &fhi) {
+    const int kind = kind_of<KS>(C);
     const Seg s{static_cast<float>(Vd), static_cast<float>(Id)};
     const bool fin = !last || isfinite(len);
     float vend = -INFINITY;
@@ -424,6 +432,14 @@ __device__ __forceinline__ bool seg_test(const LifConst &C, double Vd, double Id
         }
     }
     return false;
+}
+
+template <int KS = kAnyKind>
+__device__ __forceinline__ bool seg_test(const LifConst &C, double Vd, double Id, double vn_d,
+                                         bool last, float len, double kmax, float r_lo, Seg &sf,
+                                         float &hi, float &fhi) {
+    return seg_may_cross(C, Vd, Id, kmax) &&
+           seg_cross<KS>(C, Vd, Id, vn_d, last, len, r_lo, sf, hi, fhi);
 }
 
 // Spike time inside the crossing interval found by seg_test: u with v(u) =
@@ -475,18 +491,31 @@ struct Scan {
     Seg sf{0.f, 0.f};
     float hi = 0.f, fhi = 0.f;  // bracket end of the crossing and v - theta there
 
-    __device__ __forceinline__ void step(const LifConst &C, int q, float w) {
+    // grid point q: w^_q enters the current, and the interval after T_q
+    // (kLast: the last one, [T_M, t_max)) is tested. The filter runs on every
+    // lane; one branch covers the lanes still searching that pass it.
+    template <bool kLast>
+    __device__ __forceinline__ void step_k(const LifConst &C, int q, float w) {
         Id += static_cast<double>(w);
         const double vn_d = fma(Vd, C.alpha_d, Id * C.k_dt_d);
-        if (qf < 0) {
-            const bool last = (q == C.M);
-            if (seg_test<KS>(C, Vd, Id, vn_d, last, last ? C.last_len : C.dt,
-                             last ? C.kmax_last_d : C.kmax_dt_d, last ? C.r_lo_last : C.r_lo_dt,
-                             sf, hi, fhi))
+        if (qf < 0 && seg_may_cross(C, Vd, Id, kLast ? C.kmax_last_d : C.kmax_dt_d)) {
+            if (seg_cross<KS>(C, Vd, Id, vn_d, kLast, kLast ? C.last_len : C.dt,
+                              kLast ? C.r_lo_last : C.r_lo_dt, sf, hi, fhi))
                 qf = q;
         }
         Vd = vn_d;
         Id *= C.beta_d;
+    }
+
+    __device__ __forceinline__ void step(const LifConst &C, int q, float w) {
+        if (q == C.M) step_k<true>(C, q, w);
+        else step_k<false>(C, q, w);
+    }
+
+    // With no further input, can this lane still cross? (v never exceeds
+    // max(V, 0) + max(I, 0) kpeak_d over the rest of the window.)
+    __device__ __forceinline__ bool may_still_fire(const LifConst &C) const {
+        return qf < 0 && seg_may_cross(C, Vd, Id, C.kpeak_d);
     }
 
     __device__ __forceinline__ bool found() const { return qf >= 0; }

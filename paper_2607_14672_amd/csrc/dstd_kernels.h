@@ -72,10 +72,14 @@ constexpr int kConvMaxK = 7;  // largest kernel height/width
 // Per cell row (b, py): records bucketed by (event row r, cell column px),
 // key = px * C_in + ci; off[(b*Hp + py) * (R*Wp + 1) + r*Wp + px] = bucket
 // start within the cell row's Wp * PC record slots.
-// The backward sort also writes the record's cell column (px) and its input
-// index in the cell row (src = px * PC + j'), stores the event derivatives
-// dL, dR in place of L, R, and zeroes the record's per-tap partial sums
-// P[record][KH*KW] (px, src and P are NULL in the forward).
+// The backward sort also writes the record's event row and cell column
+// (px = row << 16 | cell column) and its input index in the cell row
+// (src = px * PC + j'), and stores the event derivatives dL, dR in place of
+// L, R. P[record][KH*KW] holds the per-tap partial sums of dt_in: the entry
+// of tap k is written by the output position that reads the record through
+// k, and only where that position passes gradient up to the record's event
+// row (rend); the gather reads exactly those entries (px, src and P are NULL
+// in the forward).
 struct ConvSorted { int *key; float *L; float *R; int *off; int *px; int *src; float *P; };
 
 struct ConvBwdWs {
@@ -83,8 +87,11 @@ struct ConvBwdWs {
     float *L, *R;            // cell-major events (dW)
     float *gam, *uq;         // per output neuron, [B][Ho*Wo][C_out]: -g/slope, t - T_q
     int *q;                  //   and its interval (-1: no gradient flows)
-    int *live;               // [B][Ho*Wo]: any channel there passes gradient
+    int *rend;               // [B][Ho*Wo]: last event row whose records get gradient
+                             //   there (min(R-2, max q + 1) over channels; -1: none)
     float *part;             // dW partial sums [nsplit][C_out][KH*KW*C_in]
+    int *zlive;              // [nsplit]: 1 if the split has samples that pass
+                             //   gradient (its partials are written only then)
     float *wt;               // [KH*KW*C_in][C_out] weights / P (as the forward)
     ConvSorted srt;          // records sorted as in the forward, with dL, dR
 };

@@ -207,12 +207,14 @@ __global__ __launch_bounds__(256) void mfma_scan_kernel(LifConst C, int N_out,
     const float *col = wh + b * (C.M + 1) * static_cast<int64_t>(N_out) + (ok ? i : 0);
     Scan<KS> sc;
     float wn = col[0];
-    for (int m = 0; m <= C.M; ++m) {
+    bool done = false;
+    for (int m = 0; m < C.M && !done; ++m) {
         const float wc = wn;
-        if (m < C.M) wn = col[static_cast<int64_t>(m + 1) * N_out];
-        sc.step(C, m, wc);
-        if (__all(sc.found() || !ok)) break;
+        wn = col[static_cast<int64_t>(m + 1) * N_out];
+        sc.template step_k<false>(C, m, wc);
+        done = __all(sc.found() || !ok);
     }
+    if (!done) sc.template step_k<true>(C, C.M, wn);  // the last interval
     if (!ok) return;
     float to, sl;
     int q;

@@ -200,6 +200,10 @@ struct MsScan {
 
     __device__ __forceinline__ bool found() const { return nk >= F; }
 
+    // the walk's entry point (the last interval is told apart inside step)
+    template <bool kLast>
+    __device__ __forceinline__ void step_k(const LifConst &C, int m, float w) { step(C, m, w); }
+
     __device__ void step(const LifConst &C, int m, float w) {
         if (nk >= F) return;
         Id += static_cast<double>(w);

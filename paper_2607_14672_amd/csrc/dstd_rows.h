@@ -262,12 +262,14 @@ struct RowOutTtfs {
                                          const float *tp, int kPt) const {
         Scan<KS> sc;
         float wn = tp[0];  // next grid point's sum, read ahead
-        for (int m = 0; m <= C.M; ++m) {
+        bool done = false;
+        for (int m = 0; m < C.M && !done; ++m) {
             const float wc = wn;
-            if (m < C.M) wn = tp[(m + 1) * kPt];
-            sc.step(C, m, wc);
-            if (__all(sc.found() || !row_ok)) break;
+            wn = tp[(m + 1) * kPt];
+            sc.template step_k<false>(C, m, wc);
+            done = __all(sc.found() || !row_ok);
         }
+        if (!done) sc.template step_k<true>(C, C.M, wn);  // the last interval
         if (!row_ok) return;
         float to, sl;
         int q;

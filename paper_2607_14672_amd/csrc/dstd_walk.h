@@ -34,10 +34,12 @@ __device__ __forceinline__ void walk_sorted_rows(const LifConst &C, int N_in, in
     float aL = 0.f, aR = 0.f, carry = 0.f;
     bool done = false;
     // close rows cur .. target-1: grid point cur-1 gets this row's L sums
-    // plus the previous row's R sums
+    // plus the previous row's R sums. A record's row is at most M+1, so
+    // closing up to it stops before grid point M (the last interval, tested
+    // at the end only).
     auto close_to = [&](int target) {
         while (cur < target && !done) {
-            if (cur >= 1) sc.step(C, cur - 1, aL + carry);
+            if (cur >= 1) sc.template step_k<false>(C, cur - 1, aL + carry);
             carry = aR;
             aL = 0.f;
             aR = 0.f;
@@ -110,7 +112,8 @@ __device__ __forceinline__ void walk_sorted_rows(const LifConst &C, int N_in, in
             kk_start = stop;
         }
     }
-    close_to(C.M + 2);  // row M+2 has no records
+    close_to(C.M + 1);
+    if (!done) sc.template step_k<true>(C, C.M, aL + carry);  // row M+2 has no records
 }
 
 }  // namespace dstd

@@ -279,7 +279,7 @@ dstd_status check_conv(const dstd_conv_shape *cs, int64_t B, int M, dstd::ConvGe
 struct ConvWs {
     size_t wt, key, L, R, off;                        // both passes
     size_t px, src, P;                                // backward sort extras
-    size_t row, eL, eR, gam, uq, q, rend, part, zlive, dq;   // backward
+    size_t row, eL, eR, crlive, gam, uq, q, rend, part, zlive, dq;   // backward
     size_t total;
 };
 
@@ -306,6 +306,7 @@ ConvWs conv_ws_layout(int M, const dstd::ConvGeom &g, int64_t B, bool backward) 
         w.row = off; off += align_up(n * sizeof(int));
         w.eL = off; off += align_up(n * sizeof(float));
         w.eR = off; off += align_up(n * sizeof(float));
+        w.crlive = off; off += align_up((size_t)B * g.Hp * sizeof(int));
         w.gam = off; off += align_up(nout * sizeof(float));
         w.uq = off; off += align_up(nout * sizeof(float));
         w.q = off; off += align_up(nout * sizeof(int));
@@ -708,6 +709,7 @@ dstd_status conv_backward(const dstd_lif_params *p, const dstd_synfire_params *s
     bw.uq = at<float>(ws, L.uq);
     bw.q = at<int>(ws, L.q);
     bw.rend = at<int>(ws, L.rend);
+    bw.crlive = at<int>(ws, L.crlive);
     bw.part = at<float>(ws, L.part);
     bw.zlive = at<int>(ws, L.zlive);
     bw.wt = at<float>(ws, L.wt);

@@ -52,8 +52,9 @@ __device__ __forceinline__ int64_t nchw_index(const ConvGeom &g, int b, int ci, 
 }
 
 // Cell-major events of every input (row -1: no events) for the dW reduction
-// (NULL: not wanted).
-struct CellEv { int *row; float *L, *R; };
+// (NULL: not wanted), written only for cell rows where some input has events;
+// live[cr] says which (the dW kernel reads no others).
+struct CellEv { int *row; float *L, *R; int *live; };
 
 // The t-th raw input of cell row (b, py) in NCHW order (channel-major, so
 // consecutive t are mostly consecutive addresses): its NCHW index, and its
@@ -144,20 +145,12 @@ __device__ void sort_cell_row(const LifConst &C, const ConvGeom &g, const float 
             }
         }
     }
-    if (!__syncthreads_or(has)) {
-        // no input of this cell row has events: empty buckets, and (for dW)
-        // every input's event row -1
+    has = __syncthreads_or(has);
+    if (ev.row && threadIdx.x == 0) ev.live[cr] = has;
+    if (!has) {
+        // no input of this cell row has events: empty buckets
         int *off0 = cs.off + static_cast<int64_t>(cr) * (nb + 1);
         for (int f = threadIdx.x; f <= nb; f += blockDim.x) off0[f] = 0;
-        if (ev.row) {
-            const int per = g.Wp * g.PC;
-            const int64_t rb0 = static_cast<int64_t>(cr) * per;
-            for (int t = threadIdx.x; t < per; t += blockDim.x) {
-                ev.row[rb0 + t] = -1;
-                ev.L[rb0 + t] = 0.f;
-                ev.R[rb0 + t] = 0.f;
-            }
-        }
         return;
     }
     // exclusive prefix over the buckets in (r, px) order: per-thread chunk
@@ -255,6 +248,7 @@ __device__ void events_cell_row(const LifConst &C, const ConvGeom &g,
     const int b = cr / g.Hp, py = cr % g.Hp;
     const int per = g.Wp * g.PC;
     const int64_t rb = static_cast<int64_t>(cr) * per;
+    bool has = false;
     for (int t = threadIdx.x; t < per; t += blockDim.x) {
         int slot;
         const int64_t src = cell_row_input(g, b, py, t, slot);
@@ -262,7 +256,10 @@ __device__ void events_cell_row(const LifConst &C, const ConvGeom &g,
         ev.row[rb + slot] = e.row;
         ev.L[rb + slot] = e.L;
         ev.R[rb + slot] = e.R;
+        has = has || e.row >= 0;
     }
+    has = __syncthreads_or(has);
+    if (threadIdx.x == 0) ev.live[cr] = has;
 }
 
 // ------------------------------------------------------ weight layout ----
@@ -580,6 +577,26 @@ __device__ void grad_block(const LifConst &C, const ConvGeom &g, int64_t n_pos, 
     const int64_t s0 = blk * kGradPos;
     if (threadIdx.x < kGradPos) sl[threadIdx.x] = -1;
     __syncthreads();
+    // Only positions through which gradient passes are written (the dW and
+    // dt_in kernels read no others); with more than one channel tile their
+    // largest q is found first.
+    const bool tiles = g.C_out > kGradCh;
+    if (tiles) {
+        for (int e = threadIdx.x; e < g.C_out * kGradPos; e += blockDim.x) {
+            const int co = e / kGradPos, pl = e % kGradPos;
+            const int64_t sp = s0 + pl;
+            if (sp < n_pos) {
+                const int64_t o = ((sp / HoWo) * g.C_out + co) * HoWo + sp % HoWo;
+                const int q = q_idx[o];
+                if (q >= 0) {
+                    float gt = grad_t[o];
+                    if (sf.on) gt += synfire_dt(sf, t_out[o]);
+                    if (gt != 0.f) atomicMax(&sl[pl], q);
+                }
+            }
+        }
+        __syncthreads();
+    }
     for (int c0 = 0; c0 < g.C_out; c0 += kGradCh) {
         for (int e = threadIdx.x; e < kGradCh * kGradPos; e += blockDim.x) {
             const int cl = e / kGradPos, pl = e % kGradPos;
@@ -601,14 +618,14 @@ __device__ void grad_block(const LifConst &C, const ConvGeom &g, int64_t n_pos, 
             sg[cl * kS + pl] = gp.gam;
             su[cl * kS + pl] = gp.uq;
             sq[cl * kS + pl] = gp.q;
-            if (gp.q >= 0) atomicMax(&sl[pl], gp.q);
+            if (!tiles && gp.q >= 0) atomicMax(&sl[pl], gp.q);
         }
         __syncthreads();
         for (int e = threadIdx.x; e < kGradPos * kGradCh; e += blockDim.x) {
             const int pl = e / kGradCh, cl = e % kGradCh;
             const int co = c0 + cl;
             const int64_t sp = s0 + pl;
-            if (co < g.C_out && sp < n_pos) {
+            if (co < g.C_out && sp < n_pos && sl[pl] >= 0) {
                 const int64_t d = sp * g.C_out + co;
                 gam[d] = sg[cl * kS + pl];
                 uq[d] = su[cl * kS + pl];
@@ -808,6 +825,7 @@ __global__ __launch_bounds__(256) void conv_dw_kernel(LifConst C, ConvGeom g, in
                                                       const float *__restrict__ uq,
                                                       const int *__restrict__ qv,
                                                       const int *__restrict__ rend,
+                                                      const int *__restrict__ cr_live,
                                                       const int *__restrict__ ev_row,
                                                       const float *__restrict__ ev_L,
                                                       const float *__restrict__ ev_R,
@@ -898,7 +916,8 @@ __global__ __launch_bounds__(256) void conv_dw_kernel(LifConst C, ConvGeom g, in
             const int b = static_cast<int>(s / HoWo), p = static_cast<int>(s % HoWo);
             const int py = (p / g.Wo) * g.stride - g.pad + ky;
             const int px = (p % g.Wo) * g.stride - g.pad + kx;
-            if (j_ok && py >= 0 && py < g.Hp && px >= 0 && px < g.Wp) {
+            if (j_ok && py >= 0 && py < g.Hp && px >= 0 && px < g.Wp &&
+                cr_live[static_cast<int64_t>(b) * g.Hp + py]) {
                 const int64_t e0 = ((static_cast<int64_t>(b) * g.Hp + py) * g.Wp + px) * g.PC + ci;
                 for (int d = 0; d < g.P; ++d) {
                     const int64_t e = e0 + static_cast<int64_t>(d) * g.C_in;
@@ -971,7 +990,7 @@ __global__ __launch_bounds__(256) void conv_fprep_kernel(LifConst C, ConvGeom g,
     extern __shared__ int sh[];
     const int blk = static_cast<int>(blockIdx.x);
     if (blk < n_sort)
-        sort_cell_row(C, g, t_in, cs, CellEv{nullptr, nullptr, nullptr}, blk, sh);
+        sort_cell_row(C, g, t_in, cs, CellEv{nullptr, nullptr, nullptr, nullptr}, blk, sh);
     else
         weights_block<WT>(g, W, Wt, blk - n_sort);
 }
@@ -1127,7 +1146,7 @@ hipError_t launch_conv_backward(const LifConst &C, const ConvGeom &g, int64_t B,
         // dead-neuron terms only where dW is written
         const bool dead = sf.on && sf.dq && grad_W;
         const int n_dq = dead ? g.C_out : 0;
-        const CellEv ev{grad_W ? ws.row : nullptr, ws.L, ws.R};
+        const CellEv ev{grad_W ? ws.row : nullptr, ws.L, ws.R, ws.crlive};
         ConvSorted cs = ws.srt;
         if (!dt) cs.key = nullptr;
         int lds = std::max(kGradLdsBytes, 256 * static_cast<int>(sizeof(int)));
@@ -1160,8 +1179,8 @@ hipError_t launch_conv_backward(const LifConst &C, const ConvGeom &g, int64_t B,
         ProfScope prof("conv_dw", st);
 #define CDW_LAUNCH_K(TIV, NP, KSV)                                                            \
     hipLaunchKernelGGL((conv_dw_kernel<TIV, NP, KSV>), grid, dim3(256), lds, st, C, g, n_pos,  \
-                       p.s_per_split, ws.gam, ws.uq, ws.q, ws.rend, ws.row, ws.L, ws.R, ws.part,  \
-                       ws.zlive)
+                       p.s_per_split, ws.gam, ws.uq, ws.q, ws.rend, ws.crlive, ws.row, ws.L,  \
+                       ws.R, ws.part, ws.zlive)
 #define CDW_LAUNCH(TIV, NP)                                               \
     do {                                                                  \
         if (C.kind == kGeneral) CDW_LAUNCH_K(TIV, NP, kGeneral);          \

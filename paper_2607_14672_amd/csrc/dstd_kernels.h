@@ -84,7 +84,8 @@ struct ConvSorted { int *key; float *L; float *R; int *off; int *px; int *src; f
 
 struct ConvBwdWs {
     int *row;
-    float *L, *R;            // cell-major events (dW)
+    float *L, *R;            // cell-major events (dW), for cell rows with events
+    int *crlive;             // [B][Hp]: the cell row has an input with events
     float *gam, *uq;         // per output neuron, [B][Ho*Wo][C_out]: -g/slope, t - T_q
     int *q;                  //   and its interval (-1: no gradient flows)
     int *rend;               // [B][Ho*Wo]: last event row whose records get gradient

@@ -552,6 +552,205 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(6, 8))) voi
     q_idx[o_out] = q;
 }
 
+// Two output positions per wave, for layers with at most 32 output channels
+// and at most 33 event rows (R - 1 <= 32) whose receptive fields hold at most
+// kPairMaxRec raw inputs: lanes 0-31 take position 2w, lanes 32-63 position
+// 2w + 1, each lane one channel. Each half decodes its position's records --
+// in the order of the one-position walk: event row, kernel row, bucket
+// order -- into the wave's LDS list; then both halves sum the event rows in
+// lockstep, one row at a time (a half with fewer records in the row adds
+// zero-weight entries, which leave its sums unchanged), and close each row
+// into the interval scan together, so the scan runs on all 64 lanes. Every
+// neuron's sums and their order are those of the one-position kernel.
+constexpr int kPairMaxRec = 320;
+
+template <int KHT, int KS>
+__global__ __launch_bounds__(256) void conv_fwd_pair_kernel(LifConst C, ConvGeom g, int64_t n_pos,
+                                                            const float *__restrict__ Wt,
+                                                            ConvSorted cs,
+                                                            float *__restrict__ t_out,
+                                                            float *__restrict__ slope,
+                                                            int *__restrict__ q_idx) {
+    extern __shared__ int pair_lds[];  // per wave: wb[2][E], L[2][E], R[2][E]
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = uniform(threadIdx.x >> 6);
+    const int half = lane >> 5, li = lane & 31, hb = lane & 32;  // hb: the half's first lane
+    const int64_t p0 = (static_cast<int64_t>(blockIdx.x) * (blockDim.x >> 6) + wave) * 2;
+    if (p0 >= n_pos) return;  // wave-uniform; no block barrier below
+    const int64_t p = p0 + half;
+    const bool pos_ok = p < n_pos;
+    const int E = g.KH * g.KW * g.PC;
+    const int ebase = half * E;  // the half's part of the wave's list
+    int *ewb = pair_lds + wave * 6 * E;
+    float *eL = reinterpret_cast<float *>(ewb + 2 * E);
+    float *eR = eL + 2 * E;
+    const int co = li;
+    const bool row_ok = pos_ok && co < g.C_out;
+    const int HoWo = g.Ho * g.Wo;
+    const int R = rows_of(C);
+    const int64_t pp = pos_ok ? p : p0;
+    const int b = static_cast<int>(pp / HoWo), pos = static_cast<int>(pp % HoWo);
+    const int oy = pos / g.Wo, ox = pos % g.Wo;
+    const int x0 = ox * g.stride - g.pad;
+    const int xa = max(0, x0), xb = max(xa, min(g.Wp, x0 + g.KW));
+    const int nb1 = R * g.Wp + 1;
+    const int wlim = g.KH * g.KW * g.C_in - 1;
+    int64_t recb[KHT], offb[KHT];
+    int wofs[KHT];
+    bool vky[KHT];
+    int any = 0;
+#pragma unroll
+    for (int ky = 0; ky < KHT; ++ky) {
+        const int py = oy * g.stride - g.pad + ky;
+        vky[ky] = pos_ok && ky < g.KH && py >= 0 && py < g.Hp && xa < xb;
+        const int64_t cr = static_cast<int64_t>(b) * g.Hp + (vky[ky] ? py : 0);
+        recb[ky] = cr * g.Wp * g.PC;
+        offb[ky] = cr * nb1;
+        wofs[ky] = (ky * g.KW - x0) * g.C_in;
+        if (vky[ky]) any += cs.off[offb[ky] + nb1 - 1];
+    }
+    const int64_t o_out = (static_cast<int64_t>(b) * g.C_out + co) * HoWo + pos;
+    auto write_silent = [&]() {
+        if (row_ok) {
+            t_out[o_out] = INFINITY;
+            slope[o_out] = 0.f;
+            q_idx[o_out] = -1;
+        }
+    };
+    if (!__any(any > 0)) {  // neither receptive field's cell rows hold records
+        write_silent();
+        return;
+    }
+    // lane li of a half = event row li of its position: segment bounds and
+    // an exclusive prefix of the row counts within the half
+    const bool rvalid = li <= R - 2;
+    const int rr = min(li, R - 2);
+    int oa[KHT], n0[KHT];
+    int nr = 0;
+#pragma unroll
+    for (int ky = 0; ky < KHT; ++ky) {
+        const int *o = cs.off + offb[ky] + static_cast<int64_t>(rr) * g.Wp;
+        const int a = vky[ky] ? o[xa] : 0, e = vky[ky] ? o[xb] : 0;
+        oa[ky] = a;
+        n0[ky] = rvalid ? e - a : 0;
+        nr += n0[ky];
+    }
+    int inc = nr;
+#pragma unroll
+    for (int m = 1; m < 32; m <<= 1) {
+        const int o = __shfl_up(inc, m, 32);
+        if (li >= m) inc += o;
+    }
+    const int start = inc - nr;
+    const int start_eff = rvalid ? start : 0x7fffffff;
+    const int totA = uniform(__builtin_amdgcn_readlane(inc, 31));
+    const int totB = uniform(__builtin_amdgcn_readlane(inc, 63));
+    const int tot = half ? totB : totA;
+    // decode 32 records per half at a time into the LDS list
+    const int rstride = g.C_out * static_cast<int>(sizeof(float));
+    for (int c0 = 0; c0 < max(totA, totB); c0 += 32) {
+        const int v = c0 + li;
+        int lo = 0;  // the half's last row whose start is <= v
+#pragma unroll
+        for (int step = 16; step >= 1; step >>= 1) {
+            const int cand = lo + step;
+            const int sv = __shfl(start_eff, hb + (cand & 31));
+            if (cand < 32 && sv <= v) lo = cand;
+        }
+        int kk = v - __shfl(start, hb + lo);
+        int sel = -1, ridx = 0;
+#pragma unroll
+        for (int ky = 0; ky < KHT; ++ky) {
+            const int a = __shfl(oa[ky], hb + lo), nn = __shfl(n0[ky], hb + lo);
+            if (sel < 0) {
+                if (kk < nn) {
+                    sel = ky;
+                    ridx = a + kk;
+                } else {
+                    kk -= nn;
+                }
+            }
+        }
+        if (v < tot && sel >= 0) {
+            int64_t gi = 0;
+            int wof = 0;
+#pragma unroll
+            for (int ky = 0; ky < KHT; ++ky) {
+                if (sel == ky) {
+                    gi = recb[ky] + ridx;
+                    wof = wofs[ky];
+                }
+            }
+            ewb[ebase + v] = min(max(cs.key[gi] + wof, 0), wlim) * rstride;
+            eL[ebase + v] = cs.L[gi];
+            eR[ebase + v] = cs.R[gi];
+        }
+    }
+    __builtin_amdgcn_wave_barrier();
+    const uint64_t nzm = __ballot(nr > 0);
+    const uint32_t rows_any = static_cast<uint32_t>(nzm) | static_cast<uint32_t>(nzm >> 32);
+    if (rows_any == 0) {  // no records in either receptive field
+        write_silent();
+        return;
+    }
+    // rows before the first one with records add nothing to a zero state
+    const int r_first = __ffs(static_cast<int>(rows_any)) - 1;
+    const int r_last = 31 - __clz(static_cast<int>(rows_any));
+    const __amdgpu_buffer_rsrc_t wr = make_rsrc(
+        Wt, static_cast<uint32_t>(static_cast<int64_t>(wlim + 1) * g.C_out * sizeof(float)));
+    const int voff = (row_ok ? co : 0) * static_cast<int>(sizeof(float));
+    Scan<KS> sc;
+    float aL = 0.f, aR = 0.f, carry = 0.f;
+    for (int r = r_first; r <= R - 2; ++r) {
+        if (r <= r_last) {
+            const int nA = uniform(__builtin_amdgcn_readlane(nr, r));
+            const int nB = uniform(__builtin_amdgcn_readlane(nr, 32 + r));
+            const int sA = uniform(__builtin_amdgcn_readlane(start, r));
+            const int sB = uniform(__builtin_amdgcn_readlane(start, 32 + r));
+            const int n = max(nA, nB);
+            const int my_n = half ? nB : nA;
+            const int my_s = ebase + (half ? sB : sA);
+            for (int i0 = 0; i0 < n; i0 += kCBatch) {
+                int wb[kCBatch];
+                float Lq[kCBatch], Rq[kCBatch], w[kCBatch];
+#pragma unroll
+                for (int q = 0; q < kCBatch; ++q) {
+                    const bool ok = i0 + q < my_n;
+                    wb[q] = ok ? ewb[my_s + i0 + q] : 0;
+                    Lq[q] = ok ? eL[my_s + i0 + q] : 0.f;
+                    Rq[q] = ok ? eR[my_s + i0 + q] : 0.f;
+                }
+#pragma unroll
+                for (int q = 0; q < kCBatch; ++q) w[q] = BufLoad<float>::get(wr, voff + wb[q], 0);
+#pragma unroll
+                for (int q = 0; q < kCBatch; ++q) {
+                    if (i0 + q < n) {
+                        aL = fmaf(w[q], Lq[q], aL);
+                        aR = fmaf(w[q], Rq[q], aR);
+                    }
+                }
+            }
+        } else if (r == r_last + 2) {
+            // every record is in: stop once no lane still searching can
+            // reach the threshold without further input
+            if (!__any(row_ok && sc.may_still_fire(C))) break;
+        }
+        // grid point r-1: this row's L sums plus the previous row's R sums
+        if (r >= 1) sc.step(C, r - 1, aL + carry);
+        carry = aR;
+        aL = 0.f;
+        aR = 0.f;
+        if (__all(sc.found() || !row_ok)) break;
+    }
+    if (!row_ok) return;
+    float to, sl;
+    int q;
+    sc.finish(C, to, sl, q);
+    t_out[o_out] = to;
+    slope[o_out] = sl;
+    q_idx[o_out] = q;
+}
+
 // --------------------------------------------------------- backward ------
 // Gradient triples (gamma, t - T_q, q) of grad_prep for kGradPos output
 // positions s = b * Ho*Wo + p and every channel: read from the NCHW outputs
@@ -1050,6 +1249,12 @@ __global__ __launch_bounds__(256) void conv_bfin_kernel(ConvGeom g, int R, int n
 }
 
 // ------------------------------------------------------------ launchers --
+// the two-positions-per-wave forward applies (at most 32 channels, 32 event
+// rows and kPairMaxRec raw inputs per receptive field)
+bool conv_fwd_paired(int M, const ConvGeom &g) {
+    return g.C_out <= 32 && M + 2 <= 32 && g.KH * g.KW * g.PC <= kPairMaxRec;
+}
+
 int conv_sort_lds_bytes(int M, const ConvGeom &g) {
     return ((M + 3) * g.Wp + 256 + sort_stage_floats(M, g)) * static_cast<int>(sizeof(int));
 }
@@ -1074,9 +1279,27 @@ hipError_t launch_conv_forward(const LifConst &C, const ConvGeom &g, int64_t B, 
     }
     const int64_t n_pos = B * g.Ho * g.Wo;
     constexpr int waves = 4;
+    ProfScope prof("conv_fwd", st);
+    if (conv_fwd_paired(C.M, g)) {
+        const size_t lds = static_cast<size_t>(waves) * 6 * g.KH * g.KW * g.PC * sizeof(int);
+        dim3 pgrid(static_cast<unsigned>((n_pos + 2 * waves - 1) / (2 * waves)));
+#define CFP(KHV, KSV)                                                                            \
+    hipLaunchKernelGGL((conv_fwd_pair_kernel<KHV, KSV>), pgrid, dim3(waves * kWave), lds, st, C, \
+                       g, n_pos, Wt, cs, t_out, slope, q_idx)
+#define CFP_K(KHV)                                                        \
+    do {                                                                  \
+        if (C.kind == kGeneral) CFP(KHV, kGeneral);                       \
+        else CFP(KHV, kAnyKind);                                          \
+    } while (0)
+        if (g.KH == 1) CFP_K(1);
+        else if (g.KH <= 3) CFP_K(3);
+        else CFP_K(kConvMaxK);
+#undef CFP_K
+#undef CFP
+        return hipGetLastError();
+    }
     dim3 grid(static_cast<unsigned>((n_pos + waves - 1) / waves),
               static_cast<unsigned>((g.C_out + kWave - 1) / kWave));
-    ProfScope prof("conv_fwd", st);
 #define CFW(KHV, KSV)                                                                            \
     hipLaunchKernelGGL((conv_fwd_kernel<KHV, KSV>), grid, dim3(waves * kWave), 0, st, C, g, n_pos, \
                        Wt, cs, t_out, slope, q_idx)

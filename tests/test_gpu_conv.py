@@ -144,6 +144,13 @@ CASES = [
     ("200 channels (ragged tile)", 17, 2, _cs(20, 6, 8, 200, pool_in=2), 16, 1.0, 0.3, 7.0),
     ("300 channels", 18, 2, _cs(16, 4, 5, 300), 16, 1.5, 0.5, 7.0),
     ("3 input channels, 64 out", 19, 2, _cs(3, 12, 10, 64), 32, 1.0, 0.3, 7.0),
+    # two positions per wave (<= 32 channels, <= 32 event rows, <= 320 raw
+    # inputs per receptive field): pooled input at the row limit M = 30 with
+    # an odd number of positions (the last wave's second half is empty), and
+    # a 5x5 kernel with 31 channels; M = 31 is one row past the limit
+    ("paired: 2x2 pool, M 30, odd positions", 20, 1, _cs(8, 10, 14, 32, pool_in=2), 30, 1.0, 0.3, 7.0),
+    ("paired: 5x5, 31 channels", 21, 3, _cs(4, 7, 9, 31, K=5), 24, 1.5, 0.5, 7.0),
+    ("one position per wave at M 31", 22, 2, _cs(8, 6, 7, 32), 31, 1.0, 0.3, 7.0),
 ]
 
 

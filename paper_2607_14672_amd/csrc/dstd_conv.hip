@@ -552,39 +552,66 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(6, 8))) voi
     q_idx[o_out] = q;
 }
 
-// Two output positions per wave, for layers with at most 32 output channels
-// and at most 33 event rows (R - 1 <= 32) whose receptive fields hold at most
-// kPairMaxRec raw inputs: lanes 0-31 take position 2w, lanes 32-63 position
-// 2w + 1, each lane one channel. Each half decodes its position's records --
-// in the order of the one-position walk: event row, kernel row, bucket
-// order -- into the wave's LDS list; then both halves sum the event rows in
-// lockstep, one row at a time (a half with fewer records in the row adds
-// zero-weight entries, which leave its sums unchanged), and close each row
-// into the interval scan together, so the scan runs on all 64 lanes. Every
-// neuron's sums and their order are those of the one-position kernel.
-constexpr int kPairMaxRec = 320;
+// NP output positions per wave, LP = 64 / NP lanes each (one channel per
+// lane; with NP = 1 a grid row per 64-channel tile). Needs at most LP event
+// rows (R - 1 <= LP) and at most kListMaxRec raw inputs per receptive field
+// (E = KH * KW * PC). Each position's lanes decode its records -- in the
+// order of the chunked walk: event row, kernel row, bucket order -- into the
+// wave's LDS list; then the positions sum the event rows in lockstep, one row
+// at a time (a position with fewer records in the row adds zero-weight
+// entries, which leave its sums unchanged), and close each row into the
+// interval scan together, so the scan runs on all 64 lanes and the row
+// structure needs no per-record test. Every neuron's sums and their order
+// are those of the chunked walk.
+constexpr int kListMaxRec = 640;
 
-template <int KHT, int KS>
-__global__ __launch_bounds__(256) void conv_fwd_pair_kernel(LifConst C, ConvGeom g, int64_t n_pos,
+// K consecutive records of a row from the LDS list at idx, of which the lane's
+// position has `left` (entries past them add zero weight): weights loaded as
+// one batch, then summed in order.
+template <int K>
+__device__ __forceinline__ void list_batch(const int *ewb, const float *eL, const float *eR, int idx,
+                                           int left, __amdgpu_buffer_rsrc_t wr, int voff,
+                                           float &aL, float &aR) {
+    int wb[K];
+    float Lq[K], Rq[K], w[K];
+#pragma unroll
+    for (int q = 0; q < K; ++q) {
+        const bool ok = q < left;
+        wb[q] = ok ? ewb[idx + q] : 0;
+        Lq[q] = ok ? eL[idx + q] : 0.f;
+        Rq[q] = ok ? eR[idx + q] : 0.f;
+    }
+#pragma unroll
+    for (int q = 0; q < K; ++q) w[q] = BufLoad<float>::get(wr, voff + wb[q], 0);
+#pragma unroll
+    for (int q = 0; q < K; ++q) {
+        aL = fmaf(w[q], Lq[q], aL);
+        aR = fmaf(w[q], Rq[q], aR);
+    }
+}
+
+template <int KHT, int KS, int NP>
+__global__ __launch_bounds__(256) void conv_fwd_list_kernel(LifConst C, ConvGeom g, int64_t n_pos,
                                                             const float *__restrict__ Wt,
                                                             ConvSorted cs,
                                                             float *__restrict__ t_out,
                                                             float *__restrict__ slope,
                                                             int *__restrict__ q_idx) {
-    extern __shared__ int pair_lds[];  // per wave: wb[2][E], L[2][E], R[2][E]
+    constexpr int LP = kWave / NP;
+    extern __shared__ int list_lds[];  // per wave: wb[NP][E], L[NP][E], R[NP][E]
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = uniform(threadIdx.x >> 6);
-    const int half = lane >> 5, li = lane & 31, hb = lane & 32;  // hb: the half's first lane
-    const int64_t p0 = (static_cast<int64_t>(blockIdx.x) * (blockDim.x >> 6) + wave) * 2;
+    const int half = lane / LP, li = lane % LP, hb = half * LP;  // hb: the position's first lane
+    const int64_t p0 = (static_cast<int64_t>(blockIdx.x) * (blockDim.x >> 6) + wave) * NP;
     if (p0 >= n_pos) return;  // wave-uniform; no block barrier below
     const int64_t p = p0 + half;
     const bool pos_ok = p < n_pos;
     const int E = g.KH * g.KW * g.PC;
-    const int ebase = half * E;  // the half's part of the wave's list
-    int *ewb = pair_lds + wave * 6 * E;
-    float *eL = reinterpret_cast<float *>(ewb + 2 * E);
-    float *eR = eL + 2 * E;
-    const int co = li;
+    const int ebase = half * E;  // the position's part of the wave's list
+    int *ewb = list_lds + wave * 3 * NP * E;
+    float *eL = reinterpret_cast<float *>(ewb + NP * E);
+    float *eR = eL + NP * E;
+    const int co = blockIdx.y * LP + li;
     const bool row_ok = pos_ok && co < g.C_out;
     const int HoWo = g.Ho * g.Wo;
     const int R = rows_of(C);
@@ -617,12 +644,12 @@ __global__ __launch_bounds__(256) void conv_fwd_pair_kernel(LifConst C, ConvGeom
             q_idx[o_out] = -1;
         }
     };
-    if (!__any(any > 0)) {  // neither receptive field's cell rows hold records
+    if (!__any(any > 0)) {  // no receptive field's cell rows hold records
         write_silent();
         return;
     }
-    // lane li of a half = event row li of its position: segment bounds and
-    // an exclusive prefix of the row counts within the half
+    // lane li of a position = its event row li: segment bounds and an
+    // exclusive prefix of the row counts within the position's lanes
     const bool rvalid = li <= R - 2;
     const int rr = min(li, R - 2);
     int oa[KHT], n0[KHT];
@@ -637,25 +664,29 @@ __global__ __launch_bounds__(256) void conv_fwd_pair_kernel(LifConst C, ConvGeom
     }
     int inc = nr;
 #pragma unroll
-    for (int m = 1; m < 32; m <<= 1) {
-        const int o = __shfl_up(inc, m, 32);
+    for (int m = 1; m < LP; m <<= 1) {
+        const int o = __shfl_up(inc, m, LP);
         if (li >= m) inc += o;
     }
     const int start = inc - nr;
     const int start_eff = rvalid ? start : 0x7fffffff;
-    const int totA = uniform(__builtin_amdgcn_readlane(inc, 31));
-    const int totB = uniform(__builtin_amdgcn_readlane(inc, 63));
-    const int tot = half ? totB : totA;
-    // decode 32 records per half at a time into the LDS list
-    const int rstride = g.C_out * static_cast<int>(sizeof(float));
-    for (int c0 = 0; c0 < max(totA, totB); c0 += 32) {
-        const int v = c0 + li;
-        int lo = 0;  // the half's last row whose start is <= v
+    int tot = 0, tmax = 0;
 #pragma unroll
-        for (int step = 16; step >= 1; step >>= 1) {
+    for (int h = 0; h < NP; ++h) {
+        const int th = uniform(__builtin_amdgcn_readlane(inc, h * LP + LP - 1));
+        if (h == half) tot = th;
+        tmax = max(tmax, th);
+    }
+    // decode LP records per position at a time into the LDS list
+    const int rstride = g.C_out * static_cast<int>(sizeof(float));
+    for (int c0 = 0; c0 < tmax; c0 += LP) {
+        const int v = c0 + li;
+        int lo = 0;  // the position's last row whose start is <= v
+#pragma unroll
+        for (int step = LP / 2; step >= 1; step >>= 1) {
             const int cand = lo + step;
-            const int sv = __shfl(start_eff, hb + (cand & 31));
-            if (cand < 32 && sv <= v) lo = cand;
+            const int sv = __shfl(start_eff, hb + (cand & (LP - 1)));
+            if (cand < LP && sv <= v) lo = cand;
         }
         int kk = v - __shfl(start, hb + lo);
         int sel = -1, ridx = 0;
@@ -687,15 +718,17 @@ __global__ __launch_bounds__(256) void conv_fwd_pair_kernel(LifConst C, ConvGeom
         }
     }
     __builtin_amdgcn_wave_barrier();
-    const uint64_t nzm = __ballot(nr > 0);
-    const uint32_t rows_any = static_cast<uint32_t>(nzm) | static_cast<uint32_t>(nzm >> 32);
-    if (rows_any == 0) {  // no records in either receptive field
+    uint64_t rows_any = __ballot(nr > 0);
+#pragma unroll
+    for (int h = 1; h < NP; ++h) rows_any |= rows_any >> (h * LP);
+    if (NP > 1) rows_any &= (1ull << LP) - 1;
+    if (rows_any == 0) {  // no records in any receptive field
         write_silent();
         return;
     }
     // rows before the first one with records add nothing to a zero state
-    const int r_first = __ffs(static_cast<int>(rows_any)) - 1;
-    const int r_last = 31 - __clz(static_cast<int>(rows_any));
+    const int r_first = __ffsll(static_cast<unsigned long long>(rows_any)) - 1;
+    const int r_last = 63 - __clzll(static_cast<long long>(rows_any));
     const __amdgpu_buffer_rsrc_t wr = make_rsrc(
         Wt, static_cast<uint32_t>(static_cast<int64_t>(wlim + 1) * g.C_out * sizeof(float)));
     const int voff = (row_ok ? co : 0) * static_cast<int>(sizeof(float));
@@ -703,33 +736,27 @@ __global__ __launch_bounds__(256) void conv_fwd_pair_kernel(LifConst C, ConvGeom
     float aL = 0.f, aR = 0.f, carry = 0.f;
     for (int r = r_first; r <= R - 2; ++r) {
         if (r <= r_last) {
-            const int nA = uniform(__builtin_amdgcn_readlane(nr, r));
-            const int nB = uniform(__builtin_amdgcn_readlane(nr, 32 + r));
-            const int sA = uniform(__builtin_amdgcn_readlane(start, r));
-            const int sB = uniform(__builtin_amdgcn_readlane(start, 32 + r));
-            const int n = max(nA, nB);
-            const int my_n = half ? nB : nA;
-            const int my_s = ebase + (half ? sB : sA);
-            for (int i0 = 0; i0 < n; i0 += kCBatch) {
-                int wb[kCBatch];
-                float Lq[kCBatch], Rq[kCBatch], w[kCBatch];
+            int n = 0, my_n = 0, my_s = ebase;
 #pragma unroll
-                for (int q = 0; q < kCBatch; ++q) {
-                    const bool ok = i0 + q < my_n;
-                    wb[q] = ok ? ewb[my_s + i0 + q] : 0;
-                    Lq[q] = ok ? eL[my_s + i0 + q] : 0.f;
-                    Rq[q] = ok ? eR[my_s + i0 + q] : 0.f;
-                }
-#pragma unroll
-                for (int q = 0; q < kCBatch; ++q) w[q] = BufLoad<float>::get(wr, voff + wb[q], 0);
-#pragma unroll
-                for (int q = 0; q < kCBatch; ++q) {
-                    if (i0 + q < n) {
-                        aL = fmaf(w[q], Lq[q], aL);
-                        aR = fmaf(w[q], Rq[q], aR);
-                    }
+            for (int h = 0; h < NP; ++h) {
+                const int nh = uniform(__builtin_amdgcn_readlane(nr, h * LP + r));
+                const int sh = uniform(__builtin_amdgcn_readlane(start, h * LP + r));
+                n = max(n, nh);
+                if (h == half) {
+                    my_n = nh;
+                    my_s += sh;
                 }
             }
+            // batches of 8, then 4, then single records: no load or sum
+            // past the row's largest count
+            int i0 = 0;
+            for (; i0 + 8 <= n; i0 += 8)
+                list_batch<8>(ewb, eL, eR, my_s + i0, my_n - i0, wr, voff, aL, aR);
+            if (i0 + 4 <= n) {
+                list_batch<4>(ewb, eL, eR, my_s + i0, my_n - i0, wr, voff, aL, aR);
+                i0 += 4;
+            }
+            for (; i0 < n; ++i0) list_batch<1>(ewb, eL, eR, my_s + i0, my_n - i0, wr, voff, aL, aR);
         } else if (r == r_last + 2) {
             // every record is in: stop once no lane still searching can
             // reach the threshold without further input
@@ -1249,10 +1276,16 @@ __global__ __launch_bounds__(256) void conv_bfin_kernel(ConvGeom g, int R, int n
 }
 
 // ------------------------------------------------------------ launchers --
-// the two-positions-per-wave forward applies (at most 32 channels, 32 event
-// rows and kPairMaxRec raw inputs per receptive field)
-bool conv_fwd_paired(int M, const ConvGeom &g) {
-    return g.C_out <= 32 && M + 2 <= 32 && g.KH * g.KW * g.PC <= kPairMaxRec;
+// positions per wave of the list forward (its LDS list stays within 30 KB
+// per block): 2 for at most 32 channels, 32 event rows and kListMaxRec / 2
+// raw inputs per receptive field, else 0 (the chunked walk). One position
+// per wave (64-channel tiles) was measured slower than the chunked walk
+// (conv9's forward 0.81 against 0.68 ms): with few records per event row
+// the row-by-row batches stay short, where the chunked walk's batches run
+// across rows.
+int conv_fwd_list_np(int M, const ConvGeom &g) {
+    const int E = g.KH * g.KW * g.PC;
+    return (g.C_out <= 32 && M + 2 <= 32 && 2 * E <= kListMaxRec) ? 2 : 0;
 }
 
 int conv_sort_lds_bytes(int M, const ConvGeom &g) {
@@ -1280,22 +1313,23 @@ hipError_t launch_conv_forward(const LifConst &C, const ConvGeom &g, int64_t B, 
     const int64_t n_pos = B * g.Ho * g.Wo;
     constexpr int waves = 4;
     ProfScope prof("conv_fwd", st);
-    if (conv_fwd_paired(C.M, g)) {
-        const size_t lds = static_cast<size_t>(waves) * 6 * g.KH * g.KW * g.PC * sizeof(int);
-        dim3 pgrid(static_cast<unsigned>((n_pos + 2 * waves - 1) / (2 * waves)));
-#define CFP(KHV, KSV)                                                                            \
-    hipLaunchKernelGGL((conv_fwd_pair_kernel<KHV, KSV>), pgrid, dim3(waves * kWave), lds, st, C, \
-                       g, n_pos, Wt, cs, t_out, slope, q_idx)
-#define CFP_K(KHV)                                                        \
+    const int np = conv_fwd_list_np(C.M, g);
+    if (np > 0) {
+        const size_t lds = static_cast<size_t>(waves) * 3 * np * g.KH * g.KW * g.PC * sizeof(int);
+        dim3 lgrid(static_cast<unsigned>((n_pos + np * waves - 1) / (np * waves)));
+#define CFL(KHV, KSV, NPV)                                                                        \
+    hipLaunchKernelGGL((conv_fwd_list_kernel<KHV, KSV, NPV>), lgrid, dim3(waves * kWave), lds, st, \
+                       C, g, n_pos, Wt, cs, t_out, slope, q_idx)
+#define CFL_K(KHV)                                                        \
     do {                                                                  \
-        if (C.kind == kGeneral) CFP(KHV, kGeneral);                       \
-        else CFP(KHV, kAnyKind);                                          \
+        if (C.kind == kGeneral) CFL(KHV, kGeneral, 2);                    \
+        else CFL(KHV, kAnyKind, 2);                                       \
     } while (0)
-        if (g.KH == 1) CFP_K(1);
-        else if (g.KH <= 3) CFP_K(3);
-        else CFP_K(kConvMaxK);
-#undef CFP_K
-#undef CFP
+        if (g.KH == 1) CFL_K(1);
+        else if (g.KH <= 3) CFL_K(3);
+        else CFL_K(kConvMaxK);
+#undef CFL_K
+#undef CFL
         return hipGetLastError();
     }
     dim3 grid(static_cast<unsigned>((n_pos + waves - 1) / waves),

@@ -299,8 +299,9 @@ struct PosWalk {
     // geometry of position p (no memory reads)
     __device__ __forceinline__ void init(const LifConst &C, const ConvGeom &g, int64_t p) {
         const int HoWo = g.Ho * g.Wo;
-        b = uniform(static_cast<int>(p / HoWo));
-        pos = uniform(static_cast<int>(p % HoWo));
+        const int pi = static_cast<int>(p);  // B * Ho * Wo < 2^31 (checked at the boundary)
+        b = uniform(pi / HoWo);
+        pos = uniform(pi % HoWo);
         const int oy = pos / g.Wo, ox = pos % g.Wo;
         x0 = ox * g.stride - g.pad;
         xa = max(0, x0);
@@ -616,7 +617,7 @@ __global__ __launch_bounds__(256) void conv_fwd_list_kernel(LifConst C, ConvGeom
     const int HoWo = g.Ho * g.Wo;
     const int R = rows_of(C);
     const int64_t pp = pos_ok ? p : p0;
-    const int b = static_cast<int>(pp / HoWo), pos = static_cast<int>(pp % HoWo);
+    const int b = static_cast<int>(pp) / HoWo, pos = static_cast<int>(pp) % HoWo;
     const int oy = pos / g.Wo, ox = pos % g.Wo;
     const int x0 = ox * g.stride - g.pad;
     const int xa = max(0, x0), xb = max(xa, min(g.Wp, x0 + g.KW));
@@ -812,7 +813,8 @@ __device__ void grad_block(const LifConst &C, const ConvGeom &g, int64_t n_pos, 
             const int co = e / kGradPos, pl = e % kGradPos;
             const int64_t sp = s0 + pl;
             if (sp < n_pos) {
-                const int64_t o = ((sp / HoWo) * g.C_out + co) * HoWo + sp % HoWo;
+                const int si = static_cast<int>(sp);
+                const int64_t o = (static_cast<int64_t>(si / HoWo) * g.C_out + co) * HoWo + si % HoWo;
                 const int q = q_idx[o];
                 if (q >= 0) {
                     float gt = grad_t[o];
@@ -830,8 +832,8 @@ __device__ void grad_block(const LifConst &C, const ConvGeom &g, int64_t n_pos, 
             const int64_t sp = s0 + pl;
             GradPrep gp{0.f, 0.f, -1};
             if (co < g.C_out && sp < n_pos) {
-                const int64_t b = sp / HoWo;
-                const int p = static_cast<int>(sp % HoWo);
+                const int64_t b = static_cast<int>(sp) / HoWo;
+                const int p = static_cast<int>(sp) % HoWo;
                 const int64_t o = (b * g.C_out + co) * HoWo + p;
                 const int q = q_idx[o];
                 if (q >= 0) {  // silent neurons: no further loads
@@ -1139,7 +1141,7 @@ __global__ __launch_bounds__(256) void conv_dw_kernel(LifConst C, ConvGeom g, in
         bool live_next = false;
         if (more) live_next = fetch(s_lo + list[i + 1]);
         if (live) {
-            const int b = static_cast<int>(s / HoWo), p = static_cast<int>(s % HoWo);
+            const int b = static_cast<int>(s) / HoWo, p = static_cast<int>(s) % HoWo;
             const int py = (p / g.Wo) * g.stride - g.pad + ky;
             const int px = (p % g.Wo) * g.stride - g.pad + kx;
             if (j_ok && py >= 0 && py < g.Hp && px >= 0 && px < g.Wp &&

@@ -374,12 +374,20 @@ struct PosWalk {
 // into the interval scan as the row changes. Sums and their order are those
 // of a row-by-row walk.
 struct FwdEntry { int wb, row; float L, R; };
+// kDirect (receptive fields of at most 64 raw inputs, at most 64 event rows,
+// pooled or plain input): no cell-row sort; lane v takes raw input
+// v = ((ky * KW + kx) * P + d) * C_in + ci of the receptive field, bins its
+// spike time itself, and the lanes are ranked by event row (stable in v, so
+// within a row the order is kernel row, cell column, input slot: the sorted
+// walk's order) from ballots of the row's bits; the ranked entries go to the
+// same LDS list as one chunk of the walk.
 // (At most 80 VGPRs: six waves per SIMD, measured faster than five; eight
 // would spill.)
-template <int KHT, int KS>
+template <int KHT, int KS, bool kDirect>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(6, 8))) void conv_fwd_kernel(LifConst C, ConvGeom g, int64_t n_pos,
                                                        const float *__restrict__ Wt,
-                                                       ConvSorted cs, float *__restrict__ t_out,
+                                                       ConvSorted cs, const float *__restrict__ t_in,
+                                                       float *__restrict__ t_out,
                                                        float *__restrict__ slope,
                                                        int *__restrict__ q_idx) {
     __shared__ FwdEntry ent[4][kWave];
@@ -424,6 +432,77 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(6, 8))) voi
         }
     };
     bool done = false, started = false;
+    if constexpr (kDirect) {
+        const int F = g.KH * g.KW * g.PC;
+        bool has = false;
+        FwdEntry me{0, -1, 0.f, 0.f};
+        if (lane < F) {
+            const int ci = lane % g.C_in, t1 = lane / g.C_in;
+            const int d = t1 % g.P, k = t1 / g.P;
+            const int ky = k / g.KW, kx = k % g.KW;
+            const int oy = wk.pos / g.Wo;
+            const int py = oy * g.stride - g.pad + ky, px = wk.x0 + kx;
+            if (py >= 0 && py < g.Hp && px >= 0 && px < g.Wp) {
+                int y, x;
+                raw_pixel(g, py, px, d, y, x);
+                const Event e = bin_event<KS>(C, t_in[nchw_index(g, wk.b, ci, y, x)]);
+                if (e.row >= 0) {
+                    has = true;
+                    me = FwdEntry{(k * g.C_in + ci) * rstride, e.row, e.L, e.R};
+                }
+            }
+        }
+        const uint64_t hm = __ballot(has);
+        const int total = __popcll(hm);
+        if (total == 0) {  // no events in the receptive field: silent
+            if (row_ok) {
+                t_out[o_out] = INFINITY;
+                slope[o_out] = 0.f;
+                q_idx[o_out] = -1;
+            }
+            return;
+        }
+        // stable rank by event row: lanes with a smaller row, then lanes
+        // with the same row and a lower index
+        uint64_t lt = 0, eq = hm;
+        const int kbits = uniform(32 - __clz(max(R - 2, 1)));
+        for (int bit = kbits - 1; bit >= 0; --bit) {
+            const bool on = has && ((me.row >> bit) & 1);
+            const uint64_t bal = __ballot(on);
+            if (on) lt |= eq & ~bal;
+            eq &= on ? bal : (hm & ~bal);
+        }
+        const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+        if (has) my[__popcll(lt) + __popcll(eq & below)] = me;
+        __builtin_amdgcn_wave_barrier();
+        cur = uniform(my[0].row);  // the scan starts at the first row with records
+        started = true;
+        for (int s0 = 0; s0 < total; s0 += kCBatch) {
+            FwdEntry e[kCBatch];
+            float w[kCBatch];
+#pragma unroll
+            for (int q = 0; q < kCBatch; ++q) e[q] = my[s0 + q];  // LDS broadcasts
+#pragma unroll
+            for (int q = 0; q < kCBatch; ++q) w[q] = BufLoad<float>::get(wr, voff + e[q].wb, 0);
+            const int nk = min(kCBatch, total - s0);
+#pragma unroll
+            for (int q = 0; q < kCBatch; ++q) {
+                if (q < nk) {
+                    const int row = uniform(e[q].row);
+                    if (row != cur) {
+                        close_to_mid(row);
+                        if (__all(sc.found() || !row_ok)) {
+                            done = true;
+                            break;
+                        }
+                    }
+                    aL = fmaf(w[q], e[q].L, aL);
+                    aR = fmaf(w[q], e[q].R, aR);
+                }
+            }
+            if (done) break;
+        }
+    } else {
     // the KH cell rows' record counts (scalar loads) rule out most positions
     // without events in their receptive field before any vector load
     if (wk.cell_records(cs) == 0) {
@@ -529,6 +608,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(6, 8))) voi
             __builtin_amdgcn_wave_barrier();
         }
     }
+    }  // kDirect
     if (!started) {  // no events in the receptive field: silent
         if (row_ok) {
             t_out[o_out] = INFINITY;
@@ -1285,6 +1365,10 @@ __global__ __launch_bounds__(256) void conv_bfin_kernel(ConvGeom g, int R, int n
 // (conv9's forward 0.81 against 0.68 ms): with few records per event row
 // the row-by-row batches stay short, where the chunked walk's batches run
 // across rows.
+// the chunked walk bins its inputs itself (no sort) where a receptive field
+// holds at most 64 raw inputs
+bool conv_fwd_direct(const ConvGeom &g) { return g.KH * g.KW * g.PC <= kWave; }
+
 int conv_fwd_list_np(int M, const ConvGeom &g) {
     const int E = g.KH * g.KW * g.PC;
     return (g.C_out <= 32 && M + 2 <= 32 && 2 * E <= kListMaxRec) ? 2 : 0;
@@ -1298,7 +1382,10 @@ hipError_t launch_conv_forward(const LifConst &C, const ConvGeom &g, int64_t B, 
                                bool bf16, float *Wt, ConvSorted cs, const float *t_in,
                                float *t_out, float *slope, int *q_idx, hipStream_t st) {
     const int64_t nw = static_cast<int64_t>(g.KH) * g.KW * g.C_in * g.C_out;
-    const int n_sort = static_cast<int>(B * g.Hp);
+    const int np = conv_fwd_list_np(C.M, g);
+    const bool direct = np == 0 && conv_fwd_direct(g);
+    // the direct walk bins its inputs itself: no cell-row sort
+    const int n_sort = direct ? 0 : static_cast<int>(B * g.Hp);
     {
         ProfScope prof("conv_fprep", st);
         const unsigned blocks = static_cast<unsigned>(n_sort + (nw + 255) / 256);
@@ -1315,7 +1402,6 @@ hipError_t launch_conv_forward(const LifConst &C, const ConvGeom &g, int64_t B, 
     const int64_t n_pos = B * g.Ho * g.Wo;
     constexpr int waves = 4;
     ProfScope prof("conv_fwd", st);
-    const int np = conv_fwd_list_np(C.M, g);
     if (np > 0) {
         const size_t lds = static_cast<size_t>(waves) * 3 * np * g.KH * g.KW * g.PC * sizeof(int);
         dim3 lgrid(static_cast<unsigned>((n_pos + np * waves - 1) / (np * waves)));
@@ -1336,18 +1422,24 @@ hipError_t launch_conv_forward(const LifConst &C, const ConvGeom &g, int64_t B, 
     }
     dim3 grid(static_cast<unsigned>((n_pos + waves - 1) / waves),
               static_cast<unsigned>((g.C_out + kWave - 1) / kWave));
-#define CFW(KHV, KSV)                                                                            \
-    hipLaunchKernelGGL((conv_fwd_kernel<KHV, KSV>), grid, dim3(waves * kWave), 0, st, C, g, n_pos, \
-                       Wt, cs, t_out, slope, q_idx)
+#define CFW(KHV, KSV, DV)                                                                        \
+    hipLaunchKernelGGL((conv_fwd_kernel<KHV, KSV, DV>), grid, dim3(waves * kWave), 0, st, C, g,    \
+                       n_pos, Wt, cs, t_in, t_out, slope, q_idx)
+#define CFW_D(KHV, KSV)                                                   \
+    do {                                                                  \
+        if (direct) CFW(KHV, KSV, true);                                  \
+        else CFW(KHV, KSV, false);                                        \
+    } while (0)
 #define CFW_K(KHV)                                                        \
     do {                                                                  \
-        if (C.kind == kGeneral) CFW(KHV, kGeneral);                       \
-        else CFW(KHV, kAnyKind);                                          \
+        if (C.kind == kGeneral) CFW_D(KHV, kGeneral);                     \
+        else CFW_D(KHV, kAnyKind);                                        \
     } while (0)
     if (g.KH == 1) CFW_K(1);
     else if (g.KH <= 3) CFW_K(3);
     else CFW_K(kConvMaxK);
 #undef CFW_K
+#undef CFW_D
 #undef CFW
     return hipGetLastError();
 }

@@ -263,21 +263,37 @@ __device__ void events_cell_row(const LifConst &C, const ConvGeom &g,
 }
 
 // ------------------------------------------------------ weight layout ----
-// WT[(k * C_in + ci) * C_out + co] = W[co, ci, k] / P (k = ky*KW + kx); block
-// blk of 256 threads takes entries blk * 256 ...
+// WT[(k * C_in + ci) * C_out + co] = W[co, ci, k] / P (k = ky*KW + kx): W seen
+// as [C_out][C_in * KT] (u = ci * KT + k) is transposed in 32 x 32 tiles
+// through LDS (reads along u and writes along co coalesced); block blk takes
+// tile (co0, u0) = ((blk / ntu) * 32, (blk % ntu) * 32).
+constexpr int kWtLdsBytes = 32 * 33 * static_cast<int>(sizeof(float));
+
+__host__ __device__ __forceinline__ int64_t weight_tiles(const ConvGeom &g) {
+    const int64_t nu = static_cast<int64_t>(g.C_in) * g.KH * g.KW;
+    return ((nu + 31) / 32) * ((g.C_out + 31) / 32);
+}
+
 template <typename WT>
 __device__ void weights_block(const ConvGeom &g, const WT *__restrict__ W, float *__restrict__ out,
-                              int64_t blk) {
+                              int64_t blk, float (*buf)[33]) {
     const int KT = g.KH * g.KW;
-    const int64_t n = static_cast<int64_t>(KT) * g.C_in * g.C_out;
-    const int64_t t = blk * blockDim.x + threadIdx.x;
-    if (t >= n) return;
-    const int co = static_cast<int>(t % g.C_out);
-    const int64_t u = t / g.C_out;
-    const int ci = static_cast<int>(u % g.C_in);
-    const int k = static_cast<int>(u / g.C_in);
-    const float w = WLoad<WT>::get(W, (static_cast<int64_t>(co) * g.C_in + ci) * KT + k);
-    out[t] = w * g.inv_P;
+    const int NU = g.C_in * KT;
+    const int ntu = (NU + 31) / 32;
+    const int u0 = static_cast<int>(blk % ntu) * 32, c0 = static_cast<int>(blk / ntu) * 32;
+    const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
+    for (int r = ty; r < 32; r += blockDim.x >> 5) {
+        const int co = c0 + r, u = u0 + tx;
+        if (co < g.C_out && u < NU) buf[r][tx] = WLoad<WT>::get(W, static_cast<int64_t>(co) * NU + u);
+    }
+    __syncthreads();
+    for (int r = ty; r < 32; r += blockDim.x >> 5) {
+        const int u = u0 + r, co = c0 + tx;
+        if (u < NU && co < g.C_out) {
+            const int ci = u / KT, k = u % KT;
+            out[(static_cast<int64_t>(k) * g.C_in + ci) * g.C_out + co] = buf[tx][r] * g.inv_P;
+        }
+    }
 }
 
 // ------------------------------------------------------ position walk ----
@@ -1251,33 +1267,45 @@ __global__ __launch_bounds__(256) void conv_dw_kernel(LifConst C, ConvGeom g, in
 }
 
 // dW[co, ci, ky, kx] = (1/P) sum_z part[z][co][k * C_in + ci]. Threads follow
-// the partial-sum layout (coalesced reads); a block holds 32 consecutive
-// entries x 8 split groups: group h sums z = h, h + 8, ...; the 8 group sums
-// are added in group order (fixed order: deterministic) and written to the
-// [co][ci][ky][kx] slot. Splits without gradient-carrying samples wrote no
-// partials and are skipped (their sums would be +0, which leaves every
-// partial sum unchanged).
-constexpr int kRedOut = 32, kRedGrp = 8;
+// the partial-sum layout (coalesced reads); a block holds 256 / G consecutive
+// entries x G split groups (G from red_groups: more groups where there are
+// many splits): group h sums z = h, h + G, ...; the G group sums are added in
+// group order (fixed order: deterministic) and written to the [co][ci][ky][kx]
+// slot. Splits without gradient-carrying samples wrote no partials and are
+// skipped (their sums would be +0, which leaves every partial sum unchanged);
+// where no split has any, the block writes the dead-neuron term (or 0) at once.
+__host__ __device__ __forceinline__ int red_groups(int nsplit) {
+    int G = 8;
+    while (G < 64 && G * 16 < nsplit) G *= 2;
+    return G;
+}
 
 __device__ void dw_reduce_block(const ConvGeom &g, int nsplit, const float *__restrict__ part,
                                 const int *__restrict__ zlive, const float *__restrict__ dq,
-                                float *__restrict__ dW, int64_t blk, float (*red)[kRedOut]) {
+                                float *__restrict__ dW, int64_t blk, float *red) {
     const int KT = g.KH * g.KW;
     const int NJ = KT * g.C_in;
     const int64_t n = static_cast<int64_t>(g.C_out) * NJ;
-    const int lo = threadIdx.x % kRedOut, h = threadIdx.x / kRedOut;
-    const int64_t src = blk * kRedOut + lo;  // [co][k][ci]
-    float s = 0.f;
-    if (src < n) {
+    const int G = red_groups(nsplit), O = static_cast<int>(blockDim.x) / G;
+    const int lo = threadIdx.x % O, h = threadIdx.x / O;
+    const int64_t src = blk * O + lo;  // [co][k][ci]
+    bool any = false;
+    for (int z = threadIdx.x; z < nsplit; z += blockDim.x) any = any || zlive[z] != 0;
+    any = __syncthreads_or(any);
+    float tot = 0.f;
+    if (any) {
+        float s = 0.f;
+        if (src < n) {
 #pragma unroll 8
-        for (int z = h; z < nsplit; z += kRedGrp)
-            if (zlive[z]) s += part[static_cast<int64_t>(z) * n + src];
+            for (int z = h; z < nsplit; z += G)
+                if (zlive[z]) s += part[static_cast<int64_t>(z) * n + src];
+        }
+        red[h * O + lo] = s;
+        __syncthreads();
+        if (h == 0)
+            for (int q = 0; q < G; ++q) tot += red[q * O + lo];
     }
-    red[h][lo] = s;
-    __syncthreads();
     if (h == 0 && src < n) {
-        float tot = 0.f;
-        for (int q = 0; q < kRedGrp; ++q) tot += red[q][lo];
         const int co = static_cast<int>(src / NJ);
         const int rem = static_cast<int>(src % NJ);
         const int k = rem / g.C_in, ci = rem % g.C_in;
@@ -1300,7 +1328,7 @@ __global__ __launch_bounds__(256) void conv_fprep_kernel(LifConst C, ConvGeom g,
     if (blk < n_sort)
         sort_cell_row(C, g, t_in, cs, CellEv{nullptr, nullptr, nullptr, nullptr}, blk, sh);
     else
-        weights_block<WT>(g, W, Wt, blk - n_sort);
+        weights_block<WT>(g, W, Wt, blk - n_sort, reinterpret_cast<float (*)[33]>(sh));
 }
 
 // Backward set-up: [0, n_cr) cell rows (events for dW; with cs.key set also
@@ -1334,7 +1362,7 @@ __global__ __launch_bounds__(256) void conv_bprep_kernel(
         dead_channel_block(g, n_pos / (g.Ho * g.Wo), q_idx, sf, blk, sh);
         return;
     }
-    weights_block<WT>(g, W, Wt, blk - n_dq);
+    weights_block<WT>(g, W, Wt, blk - n_dq, reinterpret_cast<float (*)[33]>(sh));
 }
 
 // Backward finish: [0, n_red) dW split reduction, the rest gathers dt_in
@@ -1346,11 +1374,11 @@ __global__ __launch_bounds__(256) void conv_bfin_kernel(ConvGeom g, int R, int n
                                                         float *__restrict__ dW, int nsl,
                                                         ConvSorted cs, const int *__restrict__ rend,
                                                         float *__restrict__ dt_in) {
-    static_assert(kGatherSlots >= kRedGrp * kRedOut, "the reduction shares the gather's LDS");
+    static_assert(kGatherSlots >= 256, "the reduction shares the gather's LDS");
     __shared__ float lds[kGatherSlots];
     const int blk = static_cast<int>(blockIdx.x);
     if (blk < n_red) {
-        dw_reduce_block(g, nsplit, part, zlive, dq, dW, blk, reinterpret_cast<float (*)[kRedOut]>(lds));
+        dw_reduce_block(g, nsplit, part, zlive, dq, dW, blk, lds);
     } else {
         const int t = blk - n_red;
         dt_gather_block(g, R, cs, rend, dt_in, t / nsl, (t % nsl) * kGatherSlots, lds);
@@ -1381,15 +1409,14 @@ int conv_sort_lds_bytes(int M, const ConvGeom &g) {
 hipError_t launch_conv_forward(const LifConst &C, const ConvGeom &g, int64_t B, const void *W,
                                bool bf16, float *Wt, ConvSorted cs, const float *t_in,
                                float *t_out, float *slope, int *q_idx, hipStream_t st) {
-    const int64_t nw = static_cast<int64_t>(g.KH) * g.KW * g.C_in * g.C_out;
     const int np = conv_fwd_list_np(C.M, g);
     const bool direct = np == 0 && conv_fwd_direct(g);
     // the direct walk bins its inputs itself: no cell-row sort
     const int n_sort = direct ? 0 : static_cast<int>(B * g.Hp);
     {
         ProfScope prof("conv_fprep", st);
-        const unsigned blocks = static_cast<unsigned>(n_sort + (nw + 255) / 256);
-        const int lds = conv_sort_lds_bytes(C.M, g);
+        const unsigned blocks = static_cast<unsigned>(n_sort + weight_tiles(g));
+        const int lds = std::max(direct ? 0 : conv_sort_lds_bytes(C.M, g), kWtLdsBytes);
         if (bf16)
             hipLaunchKernelGGL(conv_fprep_kernel<uint16_t>, dim3(blocks), dim3(256), lds, st, C, g,
                                n_sort, t_in, cs, static_cast<const uint16_t *>(W), Wt);
@@ -1492,8 +1519,7 @@ hipError_t launch_conv_backward(const LifConst &C, const ConvGeom &g, int64_t B,
         // gradient rows, and the WT layout for dt_in: one launch
         const int n_cr = (n_in > 0 && (grad_W || dt)) ? static_cast<int>(B * g.Hp) : 0;
         const int n_gr = static_cast<int>((n_pos + kGradPos - 1) / kGradPos);
-        const int64_t nw = nj * g.C_out;
-        const int n_wt = dt ? static_cast<int>((nw + 255) / 256) : 0;
+        const int n_wt = dt ? static_cast<int>(weight_tiles(g)) : 0;
         // dead-neuron terms only where dW is written
         const bool dead = sf.on && sf.dq && grad_W;
         const int n_dq = dead ? g.C_out : 0;
@@ -1583,7 +1609,8 @@ hipError_t launch_conv_backward(const LifConst &C, const ConvGeom &g, int64_t B,
     {
         // dW split reduction and dt_in gather: one launch
         const int64_t n = static_cast<int64_t>(g.C_out) * nj;
-        const int n_red = grad_W ? static_cast<int>((n + kRedOut - 1) / kRedOut) : 0;
+        const int red_out = 256 / red_groups(p.nsplit);  // outputs per reduction block
+        const int n_red = grad_W ? static_cast<int>((n + red_out - 1) / red_out) : 0;
         const int per = g.Wp * g.PC;
         const int nsl = (per + kGatherSlots - 1) / kGatherSlots;
         const int n_ga = dt ? static_cast<int>(B * g.Hp) * nsl : 0;

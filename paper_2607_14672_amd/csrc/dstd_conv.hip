@@ -409,7 +409,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(6, 8))) voi
     __shared__ FwdEntry ent[4][kWave];
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = uniform(threadIdx.x >> 6);
-    const int64_t p = static_cast<int64_t>(blockIdx.x) * (blockDim.x >> 6) + wave;
+    const int64_t p = static_cast<int64_t>(xcd_block(blockIdx.x, gridDim.x)) * (blockDim.x >> 6) + wave;
     if (p >= n_pos) return;  // wave-uniform; no block barrier below
     FwdEntry *my = ent[wave];
     const int co = blockIdx.y * kWave + lane;
@@ -699,7 +699,8 @@ __global__ __launch_bounds__(256) void conv_fwd_list_kernel(LifConst C, ConvGeom
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = uniform(threadIdx.x >> 6);
     const int half = lane / LP, li = lane % LP, hb = half * LP;  // hb: the position's first lane
-    const int64_t p0 = (static_cast<int64_t>(blockIdx.x) * (blockDim.x >> 6) + wave) * NP;
+    const int64_t p0 =
+        (static_cast<int64_t>(xcd_block(blockIdx.x, gridDim.x)) * (blockDim.x >> 6) + wave) * NP;
     if (p0 >= n_pos) return;  // wave-uniform; no block barrier below
     const int64_t p = p0 + half;
     const bool pos_ok = p < n_pos;

@@ -555,6 +555,18 @@ __device__ void transpose_tile(int rows, int cols, const WT *__restrict__ in, WT
 
 __device__ __forceinline__ int uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }
 
+// The chip hands workgroup b to XCD b % 8 (eight XCDs, each with its own L2).
+// xcd_block maps the hardware block index to a logical one such that each
+// XCD takes one contiguous range of logical blocks: neighbouring output
+// positions then share an L2, and the partial cache lines their lanes write
+// (one channel each, NCHW) merge there instead of in HBM.
+constexpr int kXcds = 8;
+__device__ __forceinline__ int xcd_block(int bid, int nb) {
+    const int x = bid % kXcds, i = bid / kXcds;
+    const int per = nb / kXcds, rem = nb % kXcds;
+    return x * per + min(x, rem) + i;
+}
+
 // Eight per-lane values, each summed over the 64 lanes of the wave; the
 // totals come back scattered: every lane of the group 8k .. 8k+7 holds the
 // total of v[k]. Each halving step exchanges half of the values still held:

@@ -666,7 +666,7 @@ constexpr int kListMaxRec = 640;
 // position has `left` (entries past them add zero weight): weights loaded as
 // one batch, then summed in order.
 template <int K>
-__device__ __forceinline__ void list_batch(const int *ewb, const float *eL, const float *eR, int idx,
+__device__ __forceinline__ void list_batch(const int *ewb, const float2 *eLR, int idx,
                                            int left, __amdgpu_buffer_rsrc_t wr, int voff,
                                            float &aL, float &aR) {
     int wb[K];
@@ -675,8 +675,9 @@ __device__ __forceinline__ void list_batch(const int *ewb, const float *eL, cons
     for (int q = 0; q < K; ++q) {
         const bool ok = q < left;
         wb[q] = ok ? ewb[idx + q] : 0;
-        Lq[q] = ok ? eL[idx + q] : 0.f;
-        Rq[q] = ok ? eR[idx + q] : 0.f;
+        const float2 lr = ok ? eLR[idx + q] : make_float2(0.f, 0.f);
+        Lq[q] = lr.x;
+        Rq[q] = lr.y;
     }
 #pragma unroll
     for (int q = 0; q < K; ++q) w[q] = BufLoad<float>::get(wr, voff + wb[q], 0);
@@ -695,7 +696,7 @@ __global__ __launch_bounds__(256) void conv_fwd_list_kernel(LifConst C, ConvGeom
                                                             float *__restrict__ slope,
                                                             int *__restrict__ q_idx) {
     constexpr int LP = kWave / NP;
-    extern __shared__ int list_lds[];  // per wave: wb[NP][E], L[NP][E], R[NP][E]
+    extern __shared__ int list_lds[];  // per wave: wb[NP][E], then (L, R)[NP][E]
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = uniform(threadIdx.x >> 6);
     const int half = lane / LP, li = lane % LP, hb = half * LP;  // hb: the position's first lane
@@ -706,9 +707,9 @@ __global__ __launch_bounds__(256) void conv_fwd_list_kernel(LifConst C, ConvGeom
     const bool pos_ok = p < n_pos;
     const int E = g.KH * g.KW * g.PC;
     const int ebase = half * E;  // the position's part of the wave's list
-    int *ewb = list_lds + wave * 3 * NP * E;
-    float *eL = reinterpret_cast<float *>(ewb + NP * E);
-    float *eR = eL + NP * E;
+    const int EW = (NP * E + 1) & ~1;  // ints per list (even: the (L, R) pairs stay 8-byte aligned)
+    int *ewb = list_lds + wave * 3 * EW;
+    float2 *eLR = reinterpret_cast<float2 *>(ewb + EW);  // (L, R) of a record: one 8-byte read
     const int co = blockIdx.y * LP + li;
     const bool row_ok = pos_ok && co < g.C_out;
     const int HoWo = g.Ho * g.Wo;
@@ -811,8 +812,7 @@ __global__ __launch_bounds__(256) void conv_fwd_list_kernel(LifConst C, ConvGeom
                 }
             }
             ewb[ebase + v] = min(max(cs.key[gi] + wof, 0), wlim) * rstride;
-            eL[ebase + v] = cs.L[gi];
-            eR[ebase + v] = cs.R[gi];
+            eLR[ebase + v] = make_float2(cs.L[gi], cs.R[gi]);
         }
     }
     __builtin_amdgcn_wave_barrier();
@@ -849,12 +849,12 @@ __global__ __launch_bounds__(256) void conv_fwd_list_kernel(LifConst C, ConvGeom
             // past the row's largest count
             int i0 = 0;
             for (; i0 + 8 <= n; i0 += 8)
-                list_batch<8>(ewb, eL, eR, my_s + i0, my_n - i0, wr, voff, aL, aR);
+                list_batch<8>(ewb, eLR, my_s + i0, my_n - i0, wr, voff, aL, aR);
             if (i0 + 4 <= n) {
-                list_batch<4>(ewb, eL, eR, my_s + i0, my_n - i0, wr, voff, aL, aR);
+                list_batch<4>(ewb, eLR, my_s + i0, my_n - i0, wr, voff, aL, aR);
                 i0 += 4;
             }
-            for (; i0 < n; ++i0) list_batch<1>(ewb, eL, eR, my_s + i0, my_n - i0, wr, voff, aL, aR);
+            for (; i0 < n; ++i0) list_batch<1>(ewb, eLR, my_s + i0, my_n - i0, wr, voff, aL, aR);
         } else if (r == r_last + 2) {
             // every record is in: stop once no lane still searching can
             // reach the threshold without further input
@@ -1431,7 +1431,8 @@ hipError_t launch_conv_forward(const LifConst &C, const ConvGeom &g, int64_t B, 
     constexpr int waves = 4;
     ProfScope prof("conv_fwd", st);
     if (np > 0) {
-        const size_t lds = static_cast<size_t>(waves) * 3 * np * g.KH * g.KW * g.PC * sizeof(int);
+        const size_t lds =
+            static_cast<size_t>(waves) * 3 * ((np * g.KH * g.KW * g.PC + 1) & ~1) * sizeof(int);
         dim3 lgrid(static_cast<unsigned>((n_pos + np * waves - 1) / (np * waves)));
 #define CFL(KHV, KSV, NPV)                                                                        \
     hipLaunchKernelGGL((conv_fwd_list_kernel<KHV, KSV, NPV>), lgrid, dim3(waves * kWave), lds, st, \

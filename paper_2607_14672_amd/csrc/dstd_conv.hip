@@ -688,10 +688,15 @@ __device__ __forceinline__ void list_batch(const int *ewb, const float2 *eLR, in
     }
 }
 
-template <int KHT, int KS, int NP>
+// kDirect (E <= LP): as in the chunked walk, no cell-row sort: lane li of a
+// position takes raw input li of its receptive field and bins it; the row
+// counts come from LDS integer atomics, and each record's place in its row
+// from ballots of the row bits (stable in li: the sorted walk's order).
+template <int KHT, int KS, int NP, bool kDirect>
 __global__ __launch_bounds__(256) void conv_fwd_list_kernel(LifConst C, ConvGeom g, int64_t n_pos,
                                                             const float *__restrict__ Wt,
                                                             ConvSorted cs,
+                                                            const float *__restrict__ t_in,
                                                             float *__restrict__ t_out,
                                                             float *__restrict__ slope,
                                                             int *__restrict__ q_idx) {
@@ -724,17 +729,6 @@ __global__ __launch_bounds__(256) void conv_fwd_list_kernel(LifConst C, ConvGeom
     int64_t recb[KHT], offb[KHT];
     int wofs[KHT];
     bool vky[KHT];
-    int any = 0;
-#pragma unroll
-    for (int ky = 0; ky < KHT; ++ky) {
-        const int py = oy * g.stride - g.pad + ky;
-        vky[ky] = pos_ok && ky < g.KH && py >= 0 && py < g.Hp && xa < xb;
-        const int64_t cr = static_cast<int64_t>(b) * g.Hp + (vky[ky] ? py : 0);
-        recb[ky] = cr * g.Wp * g.PC;
-        offb[ky] = cr * nb1;
-        wofs[ky] = (ky * g.KW - x0) * g.C_in;
-        if (vky[ky]) any += cs.off[offb[ky] + nb1 - 1];
-    }
     const int64_t o_out = (static_cast<int64_t>(b) * g.C_out + co) * HoWo + pos;
     auto write_silent = [&]() {
         if (row_ok) {
@@ -743,23 +737,69 @@ __global__ __launch_bounds__(256) void conv_fwd_list_kernel(LifConst C, ConvGeom
             q_idx[o_out] = -1;
         }
     };
-    if (!__any(any > 0)) {  // no receptive field's cell rows hold records
-        write_silent();
-        return;
-    }
-    // lane li of a position = its event row li: segment bounds and an
-    // exclusive prefix of the row counts within the position's lanes
+    // lane li of a position = its event row li: the row's record count (and
+    // on the sorted path its segment bounds), then an exclusive prefix of
+    // the counts within the position's lanes
     const bool rvalid = li <= R - 2;
-    const int rr = min(li, R - 2);
     int oa[KHT], n0[KHT];
     int nr = 0;
+    // direct path: this lane's own record
+    bool dhas = false;
+    int drow = 0, dwb = 0;
+    float2 dlr = make_float2(0.f, 0.f);
+    if constexpr (kDirect) {
+        int *hist = list_lds + (blockDim.x >> 6) * 3 * EW + wave * kWave;  // [NP][LP] row counts
+        hist[lane] = 0;
+        __builtin_amdgcn_wave_barrier();
+        if (pos_ok && li < E) {
+            const int ci = li % g.C_in, t1 = li / g.C_in;
+            const int d = t1 % g.P, k = t1 / g.P;
+            const int ky = k / g.KW, kx = k % g.KW;
+            const int py = oy * g.stride - g.pad + ky, px = x0 + kx;
+            if (py >= 0 && py < g.Hp && px >= 0 && px < g.Wp) {
+                int y, x;
+                raw_pixel(g, py, px, d, y, x);
+                const Event e = bin_event<KS>(C, t_in[nchw_index(g, b, ci, y, x)]);
+                if (e.row >= 0) {
+                    dhas = true;
+                    drow = e.row;
+                    dwb = (k * g.C_in + ci) * g.C_out * static_cast<int>(sizeof(float));
+                    dlr = make_float2(e.L, e.R);
+                    atomicAdd(&hist[hb + e.row], 1);
+                }
+            }
+        }
+        __builtin_amdgcn_wave_barrier();
+        if (!__any(dhas)) {  // no events in any receptive field
+            write_silent();
+            return;
+        }
+        nr = rvalid ? hist[lane] : 0;
+    } else {
+        int any = 0;
 #pragma unroll
-    for (int ky = 0; ky < KHT; ++ky) {
-        const int *o = cs.off + offb[ky] + static_cast<int64_t>(rr) * g.Wp;
-        const int a = vky[ky] ? o[xa] : 0, e = vky[ky] ? o[xb] : 0;
-        oa[ky] = a;
-        n0[ky] = rvalid ? e - a : 0;
-        nr += n0[ky];
+        for (int ky = 0; ky < KHT; ++ky) {
+            const int py = oy * g.stride - g.pad + ky;
+            vky[ky] = pos_ok && ky < g.KH && py >= 0 && py < g.Hp && xa < xb;
+            const int64_t cr = static_cast<int64_t>(b) * g.Hp + (vky[ky] ? py : 0);
+            recb[ky] = cr * g.Wp * g.PC;
+            offb[ky] = cr * nb1;
+            wofs[ky] = (ky * g.KW - x0) * g.C_in;
+            if (vky[ky]) any += cs.off[offb[ky] + nb1 - 1];
+        }
+        if (!__any(any > 0)) {  // no receptive field's cell rows hold records
+            write_silent();
+            return;
+        }
+        const int rr = min(li, R - 2);
+#pragma unroll
+        for (int ky = 0; ky < KHT; ++ky) {
+            const int *o = cs.off + offb[ky] + static_cast<int64_t>(rr) * g.Wp;
+            const int a = vky[ky] ? o[xa] : 0, e = vky[ky] ? o[xb] : 0;
+            oa[ky] = a;
+            n0[ky] = rvalid ? e - a : 0;
+            nr += n0[ky];
+        }
     }
     int inc = nr;
 #pragma unroll
@@ -776,8 +816,27 @@ __global__ __launch_bounds__(256) void conv_fwd_list_kernel(LifConst C, ConvGeom
         if (h == half) tot = th;
         tmax = max(tmax, th);
     }
-    // decode LP records per position at a time into the LDS list
     const int rstride = g.C_out * static_cast<int>(sizeof(float));
+    if constexpr (kDirect) {
+        // place = the row's start + the records of the same row in lower lanes
+        const uint64_t half_mask = (((1ull << (LP - 1)) << 1) - 1) << hb;
+        const uint64_t hm = __ballot(dhas) & half_mask;
+        uint64_t eq = hm;
+        const int kbits = uniform(32 - __clz(max(R - 2, 1)));
+        for (int bit = 0; bit < kbits; ++bit) {
+            const bool on = dhas && ((drow >> bit) & 1);
+            const uint64_t bal = __ballot(on);
+            eq &= on ? bal : (hm & ~bal);
+        }
+        const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+        const int rs = __shfl(start, hb + (dhas ? drow : 0));
+        if (dhas) {
+            const int at = ebase + rs + __popcll(eq & below);
+            ewb[at] = dwb;
+            eLR[at] = dlr;
+        }
+    } else
+    // decode LP records per position at a time into the LDS list
     for (int c0 = 0; c0 < tmax; c0 += LP) {
         const int v = c0 + li;
         int lo = 0;  // the position's last row whose start is <= v
@@ -1394,9 +1453,12 @@ __global__ __launch_bounds__(256) void conv_bfin_kernel(ConvGeom g, int R, int n
 // (conv9's forward 0.81 against 0.68 ms): with few records per event row
 // the row-by-row batches stay short, where the chunked walk's batches run
 // across rows.
-// the chunked walk bins its inputs itself (no sort) where a receptive field
-// holds at most 64 raw inputs
-bool conv_fwd_direct(const ConvGeom &g) { return g.KH * g.KW * g.PC <= kWave; }
+// the forward bins its inputs itself (no sort) where a receptive field holds
+// at most as many raw inputs as a position has lanes (64; 32 with two
+// positions per wave)
+bool conv_fwd_direct(const ConvGeom &g, int np) {
+    return g.KH * g.KW * g.PC <= (np == 2 ? kWave / 2 : kWave);
+}
 
 int conv_fwd_list_np(int M, const ConvGeom &g) {
     const int E = g.KH * g.KW * g.PC;
@@ -1411,7 +1473,7 @@ hipError_t launch_conv_forward(const LifConst &C, const ConvGeom &g, int64_t B, 
                                bool bf16, float *Wt, ConvSorted cs, const float *t_in,
                                float *t_out, float *slope, int *q_idx, hipStream_t st) {
     const int np = conv_fwd_list_np(C.M, g);
-    const bool direct = np == 0 && conv_fwd_direct(g);
+    const bool direct = conv_fwd_direct(g, np);
     // the direct walk bins its inputs itself: no cell-row sort
     const int n_sort = direct ? 0 : static_cast<int>(B * g.Hp);
     {
@@ -1432,20 +1494,27 @@ hipError_t launch_conv_forward(const LifConst &C, const ConvGeom &g, int64_t B, 
     ProfScope prof("conv_fwd", st);
     if (np > 0) {
         const size_t lds =
-            static_cast<size_t>(waves) * 3 * ((np * g.KH * g.KW * g.PC + 1) & ~1) * sizeof(int);
+            static_cast<size_t>(waves) * (3 * ((np * g.KH * g.KW * g.PC + 1) & ~1) + (direct ? kWave : 0)) *
+            sizeof(int);
         dim3 lgrid(static_cast<unsigned>((n_pos + np * waves - 1) / (np * waves)));
-#define CFL(KHV, KSV, NPV)                                                                        \
-    hipLaunchKernelGGL((conv_fwd_list_kernel<KHV, KSV, NPV>), lgrid, dim3(waves * kWave), lds, st, \
-                       C, g, n_pos, Wt, cs, t_out, slope, q_idx)
+#define CFL(KHV, KSV, DV)                                                                         \
+    hipLaunchKernelGGL((conv_fwd_list_kernel<KHV, KSV, 2, DV>), lgrid, dim3(waves * kWave), lds,  \
+                       st, C, g, n_pos, Wt, cs, t_in, t_out, slope, q_idx)
+#define CFL_D(KHV, KSV)                                                   \
+    do {                                                                  \
+        if (direct) CFL(KHV, KSV, true);                                  \
+        else CFL(KHV, KSV, false);                                        \
+    } while (0)
 #define CFL_K(KHV)                                                        \
     do {                                                                  \
-        if (C.kind == kGeneral) CFL(KHV, kGeneral, 2);                    \
-        else CFL(KHV, kAnyKind, 2);                                       \
+        if (C.kind == kGeneral) CFL_D(KHV, kGeneral);                     \
+        else CFL_D(KHV, kAnyKind);                                        \
     } while (0)
         if (g.KH == 1) CFL_K(1);
         else if (g.KH <= 3) CFL_K(3);
         else CFL_K(kConvMaxK);
 #undef CFL_K
+#undef CFL_D
 #undef CFL
         return hipGetLastError();
     }

@@ -151,6 +151,11 @@ CASES = [
     ("paired: 2x2 pool, M 30, odd positions", 20, 1, _cs(8, 10, 14, 32, pool_in=2), 30, 1.0, 0.3, 7.0),
     ("paired: 5x5, 31 channels", 21, 3, _cs(4, 7, 9, 31, K=5), 24, 1.5, 0.5, 7.0),
     ("one position per wave at M 31", 22, 2, _cs(8, 6, 7, 32), 31, 1.0, 0.3, 7.0),
+    # receptive fields small enough that the forward bins its inputs itself
+    # (at most 32 raw inputs with two positions per wave, 64 with one), on
+    # pooled input
+    ("direct, paired: 1x1 on 2x2 pool", 23, 3, _cs(6, 8, 10, 20, K=1, pad=0, pool_in=2), 16, 1.0, 0.3, 6.0),
+    ("direct: 3x3 on 2x2 pool, 1 input channel", 24, 3, _cs(1, 12, 10, 40, pool_in=2), 20, 1.0, 0.3, 14.0),
 ]
 
 

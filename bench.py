@@ -78,6 +78,14 @@ class Net:
                          "mfma": dstd.DSTD_FLAG_CONTRACT_MFMA}[contract]
             p = dstd.make_params(lay.tau_m, lay.tau_s, lay.threshold, lay.M, lay.t0, lay.dt,
                                  lay.t_max, flags)
+            p_b = p
+            if lay.kind == "conv":
+                # the forward keeps its binned, sorted inputs in the backward's
+                # workspace, and the backward reuses them
+                p = dstd.make_params(lay.tau_m, lay.tau_s, lay.threshold, lay.M, lay.t0, lay.dt,
+                                     lay.t_max, dstd.DSTD_FLAG_CONV_KEEP)
+                p_b = dstd.make_params(lay.tau_m, lay.tau_s, lay.threshold, lay.M, lay.t0, lay.dt,
+                                       lay.t_max, dstd.DSTD_FLAG_CONV_REUSE)
             skip = None
             if lay.skip_back:
                 # SD block's third layer: t_in = cat(block input + delay, t_prev)
@@ -92,15 +100,15 @@ class Net:
                 cs = dstd.make_conv_shape(**lay.conv_shape())
                 out_shape = (B, lay.C_out) + dstd.conv_out_hw(cs)
                 t_in = t_prev.reshape(B, lay.C_in, lay.H, lay.W)
-                ws_f = dstd.dstd_lif_conv_forward_workspace_size(p, cs, B)
-                ws_b = dstd.dstd_lif_conv_backward_workspace_size(p, cs, B)
+                ws_f = 0  # the forward writes into the backward's workspace
+                ws_b = dstd.dstd_lif_conv_backward_workspace_size(p_b, cs, B)
             else:
                 cs = None
                 out_shape = (B, lay.n_out)
                 t_in = t_prev.reshape(B, lay.n_in)
                 ws_f = dstd.dstd_lif_forward_workspace_size(p, B, lay.n_in, lay.n_out)
                 ws_b = dstd.dstd_lif_backward_workspace_size(p, B, lay.n_in, lay.n_out)
-            e = dict(lay=lay, p=p, cs=cs, W=W,
+            e = dict(lay=lay, p=p, p_b=p_b, cs=cs, W=W,
                      wdt=dstd.DSTD_BF16 if lay.w_dtype == "bf16" else dstd.DSTD_F32,
                      t_in=t_in,
                      t_out=torch.empty(out_shape, dtype=torch.float32, device=dev),
@@ -108,8 +116,8 @@ class Net:
                      q=torch.empty(out_shape, dtype=torch.int32, device=dev),
                      g_out=torch.empty(out_shape, dtype=torch.float32, device=dev),
                      gW=torch.empty(tuple(W.shape), dtype=torch.float32, device=dev))
-            e["ws_f"] = dstd.workspace(ws_f, dev)
             e["ws_b"] = dstd.workspace(ws_b, dev)
+            e["ws_f"] = e["ws_b"] if cs is not None else dstd.workspace(ws_f, dev)
             e["skip"] = skip
             self.L.append(e)
             t_prev = e["t_out"]
@@ -191,7 +199,7 @@ class Net:
         g_in = e["g_in_buf"].data_ptr() if l > 0 else None
         if e["cs"] is not None:
             self._ck("dstd_lif_conv_backward", ds.dstd_lif_conv_backward(
-                e["p"], e["cs"], self.B, e["t_in"].data_ptr(), e["W"].data_ptr(), e["wdt"],
+                e["p_b"], e["cs"], self.B, e["t_in"].data_ptr(), e["W"].data_ptr(), e["wdt"],
                 e["t_out"].data_ptr(), e["slope"].data_ptr(), e["q"].data_ptr(),
                 e["g_out"].data_ptr(), e["gW"].data_ptr(), g_in, e["ws_b"].data_ptr(),
                 e["ws_b"].numel(), self.stream))

@@ -86,8 +86,15 @@ typedef enum { DSTD_F32 = 0, DSTD_BF16 = 1 } dstd_dtype;
  *                    multiply-adds (App. B.3).
  *                 With neither, the library picks by shape (the MFMA product
  *                 for bf16 weights, M <= 8 and large layers, where it was
- *                 measured faster). Both set: DSTD_ERR_PARAM. Other bits must
- *                 be 0.
+ *                 measured faster). Both set: DSTD_ERR_PARAM.
+ *                 Conv calls take instead (see dstd_lif_conv_forward /
+ *                 _backward):
+ *                  DSTD_FLAG_CONV_KEEP (forward): keep the binned, sorted
+ *                    inputs for the backward;
+ *                  DSTD_FLAG_CONV_REUSE (backward): use what a forward with
+ *                    DSTD_FLAG_CONV_KEEP kept.
+ *                 A flag a call does not take gives DSTD_ERR_UNSUPPORTED.
+ *                 Other bits must be 0.
  */
 typedef struct {
     float tau_m, tau_s;
@@ -101,6 +108,8 @@ typedef struct {
 #define DSTD_MAX_M 256
 #define DSTD_FLAG_CONTRACT_SPARSE 0x2
 #define DSTD_FLAG_CONTRACT_MFMA 0x4
+#define DSTD_FLAG_CONV_KEEP 0x8
+#define DSTD_FLAG_CONV_REUSE 0x10
 
 /* ---------------------------------------------------------------- dense -- */
 
@@ -200,7 +209,8 @@ typedef struct {
 } dstd_conv_shape;
 
 /* Workspace bytes of dstd_lif_conv_forward / _backward; 0 for invalid
-   arguments (the calls then report the precise error). */
+   arguments (the calls then report the precise error). With
+   DSTD_FLAG_CONV_KEEP the forward's size is the backward's. */
 size_t dstd_lif_conv_forward_workspace_size(const dstd_lif_params *p, const dstd_conv_shape *cs,
                                             int64_t B);
 size_t dstd_lif_conv_backward_workspace_size(const dstd_lif_params *p, const dstd_conv_shape *cs,
@@ -214,6 +224,14 @@ size_t dstd_lif_conv_backward_workspace_size(const dstd_lif_params *p, const dst
  *  t_in  [B][C_in][H][W]          input spike times (+inf = no spike)
  *  W     [C_out][C_in][KH][KW]    fp32 or bf16 (converted to fp32 inside)
  *  t_out, slope, q_idx [B][C_out][H_out][W_out]  as in dstd_lif_forward.
+ * With p->flags = DSTD_FLAG_CONV_KEEP the workspace must have
+ * dstd_lif_conv_backward_workspace_size bytes (else DSTD_ERR_WORKSPACE): the
+ * call also leaves there what the layer's backward would derive from t_in
+ * and W again -- the inputs binned to their events and sorted, with the
+ * event weights' derivatives (the events s_jm of Eq. (DSTD_kernel) and
+ * ds/dt depend on t_in alone), the cell-major events for dW and the
+ * weights' layout -- for a dstd_lif_conv_backward with
+ * DSTD_FLAG_CONV_REUSE on the same workspace.
  * B = 0 is a valid no-op.
  */
 dstd_status dstd_lif_conv_forward(const dstd_lif_params *p, const dstd_conv_shape *cs, int64_t B,
@@ -227,6 +245,14 @@ dstd_status dstd_lif_conv_forward(const dstd_lif_params *p, const dstd_conv_shap
  *            or NULL to skip.
  *  grad_t_in [B][C_in][H][W] out (overwritten), or NULL to skip; inputs
  *            without events get 0.
+ * With p->flags = DSTD_FLAG_CONV_REUSE the workspace must hold what a
+ * dstd_lif_conv_forward with DSTD_FLAG_CONV_KEEP wrote for the same t_in, W,
+ * shape, B and (apart from flags) parameters, unchanged since; the call then
+ * skips binning, sorting and the weight layout. The library cannot check
+ * this (the data are on the device): other contents give wrong gradients
+ * (indices read from the workspace are clamped, so accesses stay inside the
+ * workspace and the outputs). Results are bitwise those of the call without
+ * the flag.
  */
 dstd_status dstd_lif_conv_backward(const dstd_lif_params *p, const dstd_conv_shape *cs, int64_t B,
                                    const float *t_in, const void *W, dstd_dtype w_dtype,

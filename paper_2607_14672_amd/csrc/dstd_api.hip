@@ -57,8 +57,13 @@ dstd_status check_params(const dstd_lif_params *p, int32_t allowed_flags = 0) {
         return fail(DSTD_ERR_PARAM, "t_max must be > T_M = t0 + M*dt (got %g, T_M = %g)",
                     (double)p->t_max, TM);
     if ((p->flags & ~allowed_flags) != 0) {
-        if (p->flags & (DSTD_FLAG_CONTRACT_SPARSE | DSTD_FLAG_CONTRACT_MFMA))
+        const int32_t extra = p->flags & ~allowed_flags;
+        if (extra & (DSTD_FLAG_CONTRACT_SPARSE | DSTD_FLAG_CONTRACT_MFMA))
             return fail(DSTD_ERR_UNSUPPORTED, "the contraction flags apply to dense layers only");
+        if (extra & DSTD_FLAG_CONV_KEEP)
+            return fail(DSTD_ERR_UNSUPPORTED, "DSTD_FLAG_CONV_KEEP applies to the conv forward only");
+        if (extra & DSTD_FLAG_CONV_REUSE)
+            return fail(DSTD_ERR_UNSUPPORTED, "DSTD_FLAG_CONV_REUSE applies to the conv backward only");
         return fail(DSTD_ERR_PARAM, "unknown flags 0x%x", (unsigned)p->flags);
     }
     if ((p->flags & DSTD_FLAG_CONTRACT_SPARSE) && (p->flags & DSTD_FLAG_CONTRACT_MFMA))
@@ -278,7 +283,7 @@ dstd_status check_conv(const dstd_conv_shape *cs, int64_t B, int M, dstd::ConvGe
 
 struct ConvWs {
     size_t wt, key, L, R, off;                        // both passes
-    size_t px, src, P;                                // backward sort extras
+    size_t px, src, P, dL, dR;                        // backward sort extras
     size_t row, eL, eR, crlive, gam, uq, q, rend, part, zlive, dq;   // backward
     size_t total;
 };
@@ -303,6 +308,8 @@ ConvWs conv_ws_layout(int M, const dstd::ConvGeom &g, int64_t B, bool backward) 
         w.px = off; off += align_up(nr * sizeof(int));
         w.src = off; off += align_up(nr * sizeof(int));
         w.P = off; off += align_up(nr * (size_t)(g.KH * g.KW) * sizeof(float));
+        w.dL = off; off += align_up(nr * sizeof(float));
+        w.dR = off; off += align_up(nr * sizeof(float));
         w.row = off; off += align_up(n * sizeof(int));
         w.eL = off; off += align_up(n * sizeof(float));
         w.eR = off; off += align_up(n * sizeof(float));
@@ -588,14 +595,17 @@ dstd_status dstd_mse_grad(int64_t B, int64_t N, const float *t_out, const float 
 size_t dstd_lif_conv_forward_workspace_size(const dstd_lif_params *p, const dstd_conv_shape *cs,
                                             int64_t B) {
     dstd::ConvGeom g;
-    if (check_params(p) != DSTD_OK || check_conv(cs, B, p->M, &g) != DSTD_OK) return 0;
-    return conv_ws_layout(p->M, g, B, false).total;
+    if (check_params(p, DSTD_FLAG_CONV_KEEP) != DSTD_OK || check_conv(cs, B, p->M, &g) != DSTD_OK)
+        return 0;
+    // a forward that keeps its sort for the backward needs the backward's size
+    return conv_ws_layout(p->M, g, B, (p->flags & DSTD_FLAG_CONV_KEEP) != 0).total;
 }
 
 size_t dstd_lif_conv_backward_workspace_size(const dstd_lif_params *p, const dstd_conv_shape *cs,
                                              int64_t B) {
     dstd::ConvGeom g;
-    if (check_params(p) != DSTD_OK || check_conv(cs, B, p->M, &g) != DSTD_OK) return 0;
+    if (check_params(p, DSTD_FLAG_CONV_REUSE) != DSTD_OK || check_conv(cs, B, p->M, &g) != DSTD_OK)
+        return 0;
     return conv_ws_layout(p->M, g, B, true).total;
 }
 
@@ -603,7 +613,7 @@ dstd_status dstd_lif_conv_forward(const dstd_lif_params *p, const dstd_conv_shap
                                   const float *t_in, const void *W, dstd_dtype w_dtype,
                                   float *t_out, float *slope, int32_t *q_idx, void *ws,
                                   size_t ws_bytes, void *stream) {
-    dstd_status s = check_params(p);
+    dstd_status s = check_params(p, DSTD_FLAG_CONV_KEEP);
     if (s != DSTD_OK) return s;
     dstd::ConvGeom g;
     if ((s = check_conv(cs, B, p->M, &g)) != DSTD_OK) return s;
@@ -611,14 +621,25 @@ dstd_status dstd_lif_conv_forward(const dstd_lif_params *p, const dstd_conv_shap
         return fail(DSTD_ERR_PARAM, "unknown weight dtype %d", (int)w_dtype);
     if (B > 0 && (!t_in || !W || !t_out || !slope || !q_idx))
         return fail(DSTD_ERR_NULL, "t_in, W, t_out, slope and q_idx are required");
-    ConvWs L = conv_ws_layout(p->M, g, B, false);
+    // keeping the sort for the backward needs the backward's workspace
+    const bool keep = (p->flags & DSTD_FLAG_CONV_KEEP) != 0;
+    ConvWs L = conv_ws_layout(p->M, g, B, keep);
     if ((s = check_ws(ws, ws_bytes, L.total)) != DSTD_OK) return s;
     if (B == 0) return DSTD_OK;
     LifConst C = make_const(p);
     dstd::ConvSorted srt{at<int>(ws, L.key), at<float>(ws, L.L), at<float>(ws, L.R),
-                         at<int>(ws, L.off), nullptr, nullptr, nullptr};
+                         at<int>(ws, L.off), nullptr, nullptr, nullptr, nullptr, nullptr};
+    dstd::CellEv ev{nullptr, nullptr, nullptr, nullptr};
+    if (keep) {
+        srt.px = at<int>(ws, L.px);
+        srt.src = at<int>(ws, L.src);
+        srt.dL = at<float>(ws, L.dL);
+        srt.dR = at<float>(ws, L.dR);
+        ev = dstd::CellEv{at<int>(ws, L.row), at<float>(ws, L.eL), at<float>(ws, L.eR),
+                          at<int>(ws, L.crlive)};
+    }
     hipError_t e = dstd::launch_conv_forward(C, g, B, W, w_dtype == DSTD_BF16, at<float>(ws, L.wt),
-                                             srt, t_in, t_out, slope, q_idx,
+                                             srt, ev, t_in, t_out, slope, q_idx,
                                              static_cast<hipStream_t>(stream));
     return hip_status(e, "conv forward launch");
 }
@@ -685,7 +706,7 @@ dstd_status conv_backward(const dstd_lif_params *p, const dstd_synfire_params *s
                           dstd_dtype w_dtype, const float *t_out, const float *slope,
                           const int32_t *q_idx, const float *grad_t_out, float *grad_W,
                           float *grad_t_in, void *ws, size_t ws_bytes, void *stream) {
-    dstd_status s = check_params(p);
+    dstd_status s = check_params(p, DSTD_FLAG_CONV_REUSE);
     if (s != DSTD_OK) return s;
     if ((s = check_synfire(sp)) != DSTD_OK) return s;
     dstd::ConvGeom g;
@@ -715,11 +736,12 @@ dstd_status conv_backward(const dstd_lif_params *p, const dstd_synfire_params *s
     bw.wt = at<float>(ws, L.wt);
     bw.srt = dstd::ConvSorted{at<int>(ws, L.key), at<float>(ws, L.L), at<float>(ws, L.R),
                               at<int>(ws, L.off), at<int>(ws, L.px), at<int>(ws, L.src),
-                              at<float>(ws, L.P)};
+                              at<float>(ws, L.P), at<float>(ws, L.dL), at<float>(ws, L.dR)};
+    const bool reuse = (p->flags & DSTD_FLAG_CONV_REUSE) != 0;
     // With B == 0 the dW kernel still runs (one empty split) and writes zeros.
     hipError_t e = dstd::launch_conv_backward(C, g, B, W, w_dtype == DSTD_BF16, t_in, t_out, slope,
                                               q_idx, grad_t_out, bw, grad_W, grad_t_in,
-                                              make_synfire(sp, at<float>(ws, L.dq)),
+                                              make_synfire(sp, at<float>(ws, L.dq)), reuse,
                                               static_cast<hipStream_t>(stream));
     return hip_status(e, "conv backward launch");
 }

@@ -51,11 +51,6 @@ __device__ __forceinline__ int64_t nchw_index(const ConvGeom &g, int b, int ci, 
     return ((static_cast<int64_t>(b) * g.C_in + ci) * g.H + y) * g.W + x;
 }
 
-// Cell-major events of every input (row -1: no events) for the dW reduction
-// (NULL: not wanted), written only for cell rows where some input has events;
-// live[cr] says which (the dW kernel reads no others).
-struct CellEv { int *row; float *L, *R; int *live; };
-
 // The t-th raw input of cell row (b, py) in NCHW order (channel-major, so
 // consecutive t are mostly consecutive addresses): its NCHW index, and its
 // cell-major slot px * PC + j' in `slot`.
@@ -107,7 +102,7 @@ __device__ void sort_cell_row(const LifConst &C, const ConvGeom &g, const float 
     const int nw = blockDim.x >> 6;
     const int b = cr / g.Hp, py = cr % g.Hp;
     const int nb = R * g.Wp;  // buckets, flat f = r * Wp + px
-    const bool bwd = cs.P != nullptr;
+    const bool fwd = cs.L != nullptr, bwd = cs.dL != nullptr;
     int *hist = sh;
     int *part = sh + nb;
     float *tl = sort_stage_floats(C.M, g) > 0 ? reinterpret_cast<float *>(part + 256) : nullptr;
@@ -230,9 +225,13 @@ __device__ void sort_cell_row(const LifConst &C, const ConvGeom &g, const float 
             if (f >= 0) {
                 const int64_t o = rb + pos;
                 cs.key[o] = px * g.C_in + (j % g.C_in);
-                cs.L[o] = bwd ? e.dL : e.L;
-                cs.R[o] = bwd ? e.dR : e.R;
+                if (fwd) {
+                    cs.L[o] = e.L;
+                    cs.R[o] = e.R;
+                }
                 if (bwd) {
+                    cs.dL[o] = e.dL;
+                    cs.dR[o] = e.dR;
                     cs.px[o] = (e.row << 16) | px;
                     cs.src[o] = px * g.PC + j;
                 }
@@ -347,11 +346,14 @@ struct PosWalk {
     __device__ __forceinline__ void load_offs(const ConvGeom &g, const ConvSorted &cs, int R,
                                               int r0, int lane) {
         const int r = min(r0 + lane, R - 1);
+        // bucket starts are clamped to the cell row's slots (a backward that
+        // reuses a kept forward sort trusts workspace contents)
+        const int per = g.Wp * g.PC;
 #pragma unroll
         for (int ky = 0; ky < KHT; ++ky) {
             const int *o = cs.off + offb[ky] + static_cast<int64_t>(r) * g.Wp;
-            oa[ky] = vky[ky] ? o[xa] : 0;
-            ob[ky] = vky[ky] ? o[xb] : 0;
+            oa[ky] = vky[ky] ? min(max(o[xa], 0), per) : 0;
+            ob[ky] = vky[ky] ? min(max(o[xb], oa[ky]), per) : 0;
         }
     }
 
@@ -1101,7 +1103,7 @@ __global__ __launch_bounds__(256) void conv_dtp_kernel(LifConst C, ConvGeom g, i
 #pragma unroll
                     for (int kk = 0; kk < kCBatch; ++kk) {
                         const int wo = wk.wrow(as_const(cs.key + o)[kk], ky, rstride);
-                        const float dl = as_const(cs.L + o)[kk], dr = as_const(cs.R + o)[kk];
+                        const float dl = as_const(cs.dL + o)[kk], dr = as_const(cs.dR + o)[kk];
                         float acc = 0.f;
 #pragma unroll
                         for (int t = 0; t < NT; ++t) {
@@ -1116,8 +1118,8 @@ __global__ __launch_bounds__(256) void conv_dtp_kernel(LifConst C, ConvGeom g, i
                     const float tot = wave_sum8(v, lane);
                     const int kl = lane >> 3;
                     if ((lane & 7) == 0 && kl < nk) {
-                        const int pxl = cs.px[o + kl] & 0xffff;
-                        cs.P[(o + kl) * KT + ky * g.KW + (pxl - wk.x0)] = tot;
+                        const int kx = min(max((cs.px[o + kl] & 0xffff) - wk.x0, 0), g.KW - 1);
+                        cs.P[(o + kl) * KT + ky * g.KW + kx] = tot;
                     }
                 }
             }
@@ -1145,7 +1147,7 @@ __device__ void dt_gather_block(const ConvGeom &g, int R, const ConvSorted &cs,
     const int per = g.Wp * g.PC;
     const int ns = min(kGatherSlots, per - s0);
     const int nb1 = R * g.Wp + 1;
-    const int nrec = uniform(cs.off[static_cast<int64_t>(cr) * nb1 + nb1 - 1]);
+    const int nrec = uniform(min(max(cs.off[static_cast<int64_t>(cr) * nb1 + nb1 - 1], 0), per));
     const int b = cr / g.Hp, py = cr % g.Hp;
     if (nrec == 0) {  // no input of the cell row has events
         for (int t = threadIdx.x; t < per; t += blockDim.x) {
@@ -1305,7 +1307,7 @@ __global__ __launch_bounds__(256) void conv_dw_kernel(LifConst C, ConvGeom g, in
                 const int64_t e0 = ((static_cast<int64_t>(b) * g.Hp + py) * g.Wp + px) * g.PC + ci;
                 for (int d = 0; d < g.P; ++d) {
                     const int64_t e = e0 + static_cast<int64_t>(d) * g.C_in;
-                    const int r = ev_row[e];
+                    const int r = min(ev_row[e], R - 2);
                     if (r >= 0) {
                         const float L = ev_L[e], Rv = ev_R[e];
                         const float *q = cur + r * kStr;
@@ -1377,16 +1379,18 @@ __device__ void dw_reduce_block(const ConvGeom &g, int nsplit, const float *__re
 // --------------------------------------------------------- fused launches --
 // Independent per-call work shares one launch by block role (a launch costs
 // several microseconds even when its work is tiny).
-// Forward set-up: blocks [0, n_sort) sort cell rows, the rest lay out WT.
+// Forward set-up: blocks [0, n_sort) sort cell rows (with ev set, keeping
+// the cell-major events for the backward too), the rest lay out WT.
 template <typename WT>
 __global__ __launch_bounds__(256) void conv_fprep_kernel(LifConst C, ConvGeom g, int n_sort,
                                                          const float *__restrict__ t_in,
-                                                         ConvSorted cs, const WT *__restrict__ W,
+                                                         ConvSorted cs, CellEv ev,
+                                                         const WT *__restrict__ W,
                                                          float *__restrict__ Wt) {
     extern __shared__ int sh[];
     const int blk = static_cast<int>(blockIdx.x);
     if (blk < n_sort)
-        sort_cell_row(C, g, t_in, cs, CellEv{nullptr, nullptr, nullptr, nullptr}, blk, sh);
+        sort_cell_row(C, g, t_in, cs, ev, blk, sh);
     else
         weights_block<WT>(g, W, Wt, blk - n_sort, reinterpret_cast<float (*)[33]>(sh));
 }
@@ -1470,22 +1474,24 @@ int conv_sort_lds_bytes(int M, const ConvGeom &g) {
 }
 
 hipError_t launch_conv_forward(const LifConst &C, const ConvGeom &g, int64_t B, const void *W,
-                               bool bf16, float *Wt, ConvSorted cs, const float *t_in,
+                               bool bf16, float *Wt, ConvSorted cs, CellEv ev, const float *t_in,
                                float *t_out, float *slope, int *q_idx, hipStream_t st) {
     const int np = conv_fwd_list_np(C.M, g);
     const bool direct = conv_fwd_direct(g, np);
-    // the direct walk bins its inputs itself: no cell-row sort
-    const int n_sort = direct ? 0 : static_cast<int>(B * g.Hp);
+    const bool keep = cs.dL != nullptr;
+    // the direct walk bins its inputs itself: no cell-row sort, unless the
+    // sort is kept for the backward
+    const int n_sort = (direct && !keep) ? 0 : static_cast<int>(B * g.Hp);
     {
         ProfScope prof("conv_fprep", st);
         const unsigned blocks = static_cast<unsigned>(n_sort + weight_tiles(g));
-        const int lds = std::max(direct ? 0 : conv_sort_lds_bytes(C.M, g), kWtLdsBytes);
+        const int lds = std::max(n_sort > 0 ? conv_sort_lds_bytes(C.M, g) : 0, kWtLdsBytes);
         if (bf16)
             hipLaunchKernelGGL(conv_fprep_kernel<uint16_t>, dim3(blocks), dim3(256), lds, st, C, g,
-                               n_sort, t_in, cs, static_cast<const uint16_t *>(W), Wt);
+                               n_sort, t_in, cs, ev, static_cast<const uint16_t *>(W), Wt);
         else
             hipLaunchKernelGGL(conv_fprep_kernel<float>, dim3(blocks), dim3(256), lds, st, C, g,
-                               n_sort, t_in, cs, static_cast<const float *>(W), Wt);
+                               n_sort, t_in, cs, ev, static_cast<const float *>(W), Wt);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
@@ -1578,7 +1584,7 @@ hipError_t launch_conv_backward(const LifConst &C, const ConvGeom &g, int64_t B,
                                 bool bf16, const float *t_in, const float *t_out,
                                 const float *slope, const int *q_idx, const float *grad_t,
                                 ConvBwdWs ws, float *grad_W, float *grad_t_in, const Synfire &sf,
-                                hipStream_t st) {
+                                bool reuse, hipStream_t st) {
     const int R = C.M + 3;
     const int64_t n_in = B * g.Hp * g.Wp * g.PC;
     const int64_t n_pos = B * g.Ho * g.Wo;
@@ -1587,15 +1593,17 @@ hipError_t launch_conv_backward(const LifConst &C, const ConvGeom &g, int64_t B,
     hipError_t e;
     {
         // cell rows (events; with dt_in the sort), gradient triples +
-        // gradient rows, and the WT layout for dt_in: one launch
-        const int n_cr = (n_in > 0 && (grad_W || dt)) ? static_cast<int>(B * g.Hp) : 0;
+        // gradient rows, and the WT layout for dt_in: one launch (with a
+        // kept forward sort only the gradient roles)
+        const int n_cr = (!reuse && n_in > 0 && (grad_W || dt)) ? static_cast<int>(B * g.Hp) : 0;
         const int n_gr = static_cast<int>((n_pos + kGradPos - 1) / kGradPos);
-        const int n_wt = dt ? static_cast<int>(weight_tiles(g)) : 0;
+        const int n_wt = (dt && !reuse) ? static_cast<int>(weight_tiles(g)) : 0;
         // dead-neuron terms only where dW is written
         const bool dead = sf.on && sf.dq && grad_W;
         const int n_dq = dead ? g.C_out : 0;
         const CellEv ev{grad_W ? ws.row : nullptr, ws.L, ws.R, ws.crlive};
         ConvSorted cs = ws.srt;
+        cs.L = cs.R = nullptr;  // the backward sort writes derivatives only
         if (!dt) cs.key = nullptr;
         int lds = std::max(kGradLdsBytes, 256 * static_cast<int>(sizeof(int)));
         if (dt) lds = std::max(lds, conv_sort_lds_bytes(C.M, g));

@@ -72,15 +72,22 @@ constexpr int kConvMaxK = 7;  // largest kernel height/width
 // Per cell row (b, py): records bucketed by (event row r, cell column px),
 // key = px * C_in + ci; off[(b*Hp + py) * (R*Wp + 1) + r*Wp + px] = bucket
 // start within the cell row's Wp * PC record slots.
-// The backward sort also writes the record's event row and cell column
-// (px = row << 16 | cell column) and its input index in the cell row
-// (src = px * PC + j'), and stores the event derivatives dL, dR in place of
-// L, R. P[record][KH*KW] holds the per-tap partial sums of dt_in: the entry
-// of tap k is written by the output position that reads the record through
-// k, and only where that position passes gradient up to the record's event
-// row (rend); the gather reads exactly those entries (px, src and P are NULL
-// in the forward).
-struct ConvSorted { int *key; float *L; float *R; int *off; int *px; int *src; float *P; };
+// The forward sort writes the event weights L, R; the backward sort (or a
+// forward that keeps its sort for the backward) writes the record's event
+// row and cell column (px = row << 16 | cell column), its input index in the
+// cell row (src = px * PC + j') and the event derivatives dL, dR. Unused
+// arrays are NULL. P[record][KH*KW] holds the per-tap partial sums of dt_in:
+// the entry of tap k is written by the output position that reads the record
+// through k, and only where that position passes gradient up to the record's
+// event row (rend); the gather reads exactly those entries.
+struct ConvSorted {
+    int *key; float *L; float *R; int *off; int *px; int *src; float *P; float *dL; float *dR;
+};
+
+// Cell-major events of every input (row -1: no events) for the dW reduction,
+// written only for cell rows where some input has events; live[cr] says which
+// (the dW kernel reads no others). NULL row: not wanted.
+struct CellEv { int *row; float *L, *R; int *live; };
 
 struct ConvBwdWs {
     int *row;
@@ -109,14 +116,19 @@ constexpr int kDtStride = kWave + 1;
 
 ConvDwPlan plan_conv_dw(const ConvGeom &g, int64_t B, int M);
 int conv_sort_lds_bytes(int M, const ConvGeom &g);
+// keep (cs.dL and ev set): the sort also writes what the backward needs
+// (derivatives, px, src, cell-major events), even where the walk bins its
+// inputs itself.
 hipError_t launch_conv_forward(const LifConst &C, const ConvGeom &g, int64_t B, const void *W,
-                               bool bf16, float *Wt, ConvSorted cs, const float *t_in,
+                               bool bf16, float *Wt, ConvSorted cs, CellEv ev, const float *t_in,
                                float *t_out, float *slope, int *q_idx, hipStream_t st);
+// reuse: the workspace holds a kept forward sort (records, events, weight
+// layout) for these inputs and weights: no cell-row or weight-layout work.
 hipError_t launch_conv_backward(const LifConst &C, const ConvGeom &g, int64_t B, const void *W,
                                 bool bf16, const float *t_in, const float *t_out,
                                 const float *slope, const int *q_idx, const float *grad_t,
                                 ConvBwdWs ws, float *grad_W, float *grad_t_in,
-                                const Synfire &sf, hipStream_t st);
+                                const Synfire &sf, bool reuse, hipStream_t st);
 
 // Synfire term values (reporting): T and Q of one layer's outputs
 // t [B][rows][spatial] and weights [rows][row_len].

@@ -30,6 +30,8 @@ DSTD_MAX_M = 256
 DSTD_NOALLOC_SCRATCH_BYTES = 32 << 20
 DSTD_FLAG_CONTRACT_SPARSE = 0x2
 DSTD_FLAG_CONTRACT_MFMA = 0x4
+DSTD_FLAG_CONV_KEEP = 0x8
+DSTD_FLAG_CONV_REUSE = 0x10
 
 
 class dstd_lif_params(C.Structure):

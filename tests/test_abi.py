@@ -330,8 +330,11 @@ def test_contraction_flags():
     st = dstd.dstd_lif_forward(mf, 4, 10, 5, 1, 1, dstd.DSTD_F32, 1, 1, 1, 256, 1 << 20, None)
     assert st == dstd.DSTD_ERR_UNSUPPORTED and "bf16" in dstd.dstd_last_error()
     bad = _p()
-    bad.flags = 0x8
+    bad.flags = 0x20
     assert dstd.dstd_lif_forward(bad, 4, 10, 5, 1, 1, 0, 1, 1, 1, 256, 1 << 20, None) == dstd.DSTD_ERR_PARAM
+    bad.flags = dstd.DSTD_FLAG_CONV_KEEP  # a conv flag on a dense call
+    assert dstd.dstd_lif_forward(bad, 4, 10, 5, 1, 1, 0, 1, 1, 1, 256, 1 << 20, None) == \
+        dstd.DSTD_ERR_UNSUPPORTED
     cs = dstd.make_conv_shape(2, 5, 5, 3)
     assert dstd.dstd_lif_conv_forward_workspace_size(mf, cs, 2) == 0
     # MFMA room: events (16 B per input) + w^ (4 B per (b, m, i))
@@ -345,3 +348,32 @@ def test_contraction_flags():
     # the backward accepts the same parameters
     assert dstd.dstd_lif_backward_workspace_size(mf, B, N_in, N_out) == \
         dstd.dstd_lif_backward_workspace_size(_p(), B, N_in, N_out)
+
+
+def test_conv_keep_and_reuse_flags():
+    """A conv forward may keep its binned, sorted inputs for the backward
+    (DSTD_FLAG_CONV_KEEP, in a workspace of the backward's size), and the
+    backward may reuse them (DSTD_FLAG_CONV_REUSE); each flag belongs to one
+    call, and the forward's workspace query with KEEP is the backward's."""
+    cs = dstd.make_conv_shape(4, 6, 6, 5)
+    keep, reuse = _p(), _p()
+    keep.flags = dstd.DSTD_FLAG_CONV_KEEP
+    reuse.flags = dstd.DSTD_FLAG_CONV_REUSE
+    nf = dstd.dstd_lif_conv_forward_workspace_size(_p(), cs, 2)
+    nb = dstd.dstd_lif_conv_backward_workspace_size(_p(), cs, 2)
+    assert 0 < nf < nb
+    assert dstd.dstd_lif_conv_forward_workspace_size(keep, cs, 2) == nb
+    assert dstd.dstd_lif_conv_backward_workspace_size(reuse, cs, 2) == nb
+    # the flags on the other call
+    assert dstd.dstd_lif_conv_forward_workspace_size(reuse, cs, 2) == 0
+    assert dstd.dstd_lif_conv_backward_workspace_size(keep, cs, 2) == 0
+    assert dstd.dstd_lif_conv_forward(reuse, cs, 2, 1, 1, 0, 1, 1, 1, 256, nb, None) == \
+        dstd.DSTD_ERR_UNSUPPORTED
+    assert "DSTD_FLAG_CONV_REUSE" in dstd.dstd_last_error()
+    assert dstd.dstd_lif_conv_backward(keep, cs, 2, 1, 1, 0, 1, 1, 1, 1, 1, 1, 256, nb, None) == \
+        dstd.DSTD_ERR_UNSUPPORTED
+    # a keeping forward needs the backward's workspace
+    assert dstd.dstd_lif_conv_forward(keep, cs, 2, 1, 1, 0, 1, 1, 1, 256, nf, None) == \
+        dstd.DSTD_ERR_WORKSPACE
+    # the dense calls take neither
+    assert dstd.dstd_lif_backward_workspace_size(reuse, 4, 10, 5) == 0

@@ -168,6 +168,42 @@ def test_conv_geometry(dev, case):
     assert (orc["q"] >= 0).mean() > 0.1, "case should make neurons fire"
 
 
+_REUSE_CASES = [c for c in CASES if c[0] in (
+    "3x3 s1 ragged, 2 channel tiles", "3x3 stride 2", "2x2 event pool", "global event pool 1x1",
+    "256 channels", "paired: 2x2 pool, M 30, odd positions", "direct, paired: 1x1 on 2x2 pool",
+    "direct: 3x3 on 2x2 pool, 1 input channel", "pool + stride 2 + M 64")]
+
+
+@pytest.mark.parametrize("case", _REUSE_CASES, ids=[c[0] for c in _REUSE_CASES])
+def test_conv_backward_reuses_kept_forward_sort(dev, case):
+    """A forward with DSTD_FLAG_CONV_KEEP and a backward with
+    DSTD_FLAG_CONV_REUSE on the same workspace give the plain calls' results
+    bit for bit: forward outputs, dW and dt_in (the chunked, list and direct
+    forwards, pooled and strided geometry, several channel tiles)."""
+    import torch
+    from paper_2607_14672_amd import dstd
+    label, seed, B, cs, M, tm, ts, k = case
+    p, t, W = _conv_case(seed, B, cs, M, tm, ts, k=k)
+    t = _special_inputs(t, p, np.random.default_rng(seed))
+    plain, (prm, c, tt, Wt, to, sl, q) = _gpu_forward(dev, p, cs, t, W)
+    g = np.random.default_rng(seed + 5).standard_normal(plain["t_out"].shape).astype(np.float32)
+    gW0, gx0 = _gpu_backward(dev, (prm, c, tt, Wt, to, sl, q), g)
+    keep, reuse = _prm(p), _prm(p)
+    keep.flags = dstd.DSTD_FLAG_CONV_KEEP
+    reuse.flags = dstd.DSTD_FLAG_CONV_REUSE
+    ws = dstd.workspace(dstd.dstd_lif_conv_backward_workspace_size(reuse, c, B), dev)
+    ws.fill_(0x7f)  # stale contents must not matter
+    to2, sl2, q2 = dstd.conv_forward(keep, c, tt, Wt, ws=ws)
+    gt = torch.from_numpy(g).to(dev)
+    gW, gx = dstd.conv_backward(reuse, c, tt, Wt, to2, sl2, q2, gt, ws=ws)
+    torch.cuda.synchronize()
+    assert np.array_equal(to2.cpu().numpy(), plain["t_out"])
+    assert np.array_equal(sl2.cpu().numpy(), plain["slope"])
+    assert np.array_equal(q2.cpu().numpy(), plain["q"])
+    assert np.array_equal(gW.cpu().numpy(), gW0), label
+    assert np.array_equal(gx.cpu().numpy(), gx0), label
+
+
 def test_conv_rows_past_64(dev):
     """M = 100 and 256: the bucket tables are walked in chunks of 64 rows."""
     for M, seed in [(100, 11), (256, 12)]:

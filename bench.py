@@ -79,9 +79,10 @@ class Net:
             p = dstd.make_params(lay.tau_m, lay.tau_s, lay.threshold, lay.M, lay.t0, lay.dt,
                                  lay.t_max, flags)
             p_b = p
-            if lay.kind == "conv":
+            if lay.kind == "conv" and l > 0:
                 # the forward keeps its binned, sorted inputs in the backward's
-                # workspace, and the backward reuses them
+                # workspace, and the backward reuses them (the first layer's
+                # backward computes no dt_in, so it needs no sort)
                 p = dstd.make_params(lay.tau_m, lay.tau_s, lay.threshold, lay.M, lay.t0, lay.dt,
                                      lay.t_max, dstd.DSTD_FLAG_CONV_KEEP)
                 p_b = dstd.make_params(lay.tau_m, lay.tau_s, lay.threshold, lay.M, lay.t0, lay.dt,
@@ -100,7 +101,7 @@ class Net:
                 cs = dstd.make_conv_shape(**lay.conv_shape())
                 out_shape = (B, lay.C_out) + dstd.conv_out_hw(cs)
                 t_in = t_prev.reshape(B, lay.C_in, lay.H, lay.W)
-                ws_f = 0  # the forward writes into the backward's workspace
+                ws_f = dstd.dstd_lif_conv_forward_workspace_size(p, cs, B)
                 ws_b = dstd.dstd_lif_conv_backward_workspace_size(p_b, cs, B)
             else:
                 cs = None
@@ -117,7 +118,9 @@ class Net:
                      g_out=torch.empty(out_shape, dtype=torch.float32, device=dev),
                      gW=torch.empty(tuple(W.shape), dtype=torch.float32, device=dev))
             e["ws_b"] = dstd.workspace(ws_b, dev)
-            e["ws_f"] = e["ws_b"] if cs is not None else dstd.workspace(ws_f, dev)
+            # a keeping forward writes into the backward's workspace
+            keeps = cs is not None and (p.flags & dstd.DSTD_FLAG_CONV_KEEP) != 0
+            e["ws_f"] = e["ws_b"] if keeps else dstd.workspace(ws_f, dev)
             e["skip"] = skip
             self.L.append(e)
             t_prev = e["t_out"]

@@ -939,9 +939,10 @@ __global__ __launch_bounds__(256) void conv_fwd_list_kernel(LifConst C, ConvGeom
 
 // --------------------------------------------------------- backward ------
 // Gradient triples (gamma, t - T_q, q) of grad_prep for kGradPos output
-// positions s = b * Ho*Wo + p and every channel: read from the NCHW outputs
-// with positions along the lanes, staged in LDS kGradCh channels at a time
-// and written position-major [s][co] (each position's channels contiguous).
+// positions s = b * Ho*Wo + p and one tile of kGradCh channels (block blk =
+// position group * tiles + tile): read from the NCHW outputs with positions
+// along the lanes, staged in LDS and written position-major [s][co] (each
+// position's channels contiguous).
 // rend[s] = min(R-2, max q + 1) over the channels of s that pass gradient
 // (G[m] vanishes for m > q, and a record of event row r reads G[r-1] and
 // G[r]), -1 if none does.
@@ -959,13 +960,15 @@ __device__ void grad_block(const LifConst &C, const ConvGeom &g, int64_t n_pos, 
     int *sq = reinterpret_cast<int *>(su + kGradCh * kS);
     int *sl = sq + kGradCh * kS;
     const int HoWo = g.Ho * g.Wo;
-    const int64_t s0 = blk * kGradPos;
+    const int ntile = (g.C_out + kGradCh - 1) / kGradCh;
+    const int tile = static_cast<int>(blk % ntile);
+    const int64_t s0 = (blk / ntile) * kGradPos;
     if (threadIdx.x < kGradPos) sl[threadIdx.x] = -1;
     __syncthreads();
     // Only positions through which gradient passes are written (the dW and
     // dt_in kernels read no others); with more than one channel tile their
-    // largest q is found first.
-    const bool tiles = g.C_out > kGradCh;
+    // largest q over all channels is found first (by every tile's block).
+    const bool tiles = ntile > 1;
     if (tiles) {
         for (int e = threadIdx.x; e < g.C_out * kGradPos; e += blockDim.x) {
             const int co = e / kGradPos, pl = e % kGradPos;
@@ -983,7 +986,8 @@ __device__ void grad_block(const LifConst &C, const ConvGeom &g, int64_t n_pos, 
         }
         __syncthreads();
     }
-    for (int c0 = 0; c0 < g.C_out; c0 += kGradCh) {
+    {
+        const int c0 = tile * kGradCh;
         for (int e = threadIdx.x; e < kGradCh * kGradPos; e += blockDim.x) {
             const int cl = e / kGradPos, pl = e % kGradPos;
             const int co = c0 + cl;
@@ -1020,7 +1024,7 @@ __device__ void grad_block(const LifConst &C, const ConvGeom &g, int64_t n_pos, 
         }
         __syncthreads();
     }
-    if (rend && threadIdx.x < kGradPos && s0 + threadIdx.x < n_pos) {
+    if (rend && tile == 0 && threadIdx.x < kGradPos && s0 + threadIdx.x < n_pos) {
         const int qm = sl[threadIdx.x];
         rend[s0 + threadIdx.x] = qm < 0 ? -1 : min(rows_of(C) - 2, qm + 1);
     }
@@ -1354,8 +1358,16 @@ __device__ void dw_reduce_block(const ConvGeom &g, int nsplit, const float *__re
     bool any = false;
     for (int z = threadIdx.x; z < nsplit; z += blockDim.x) any = any || zlive[z] != 0;
     any = __syncthreads_or(any);
+    if (!any) {
+        // no split carries gradient (the same for every block of the layer):
+        // dW is the dead-neuron term or 0, written in dW's own order, one
+        // entry per thread, by the first n / blockDim blocks (coalesced)
+        const int64_t i = blk * blockDim.x + threadIdx.x;
+        if (i < n) dW[i] = dq ? 0.f + dq[i / NJ] : 0.f;
+        return;
+    }
     float tot = 0.f;
-    if (any) {
+    {
         float s = 0.f;
         if (src < n) {
 #pragma unroll 8
@@ -1596,7 +1608,8 @@ hipError_t launch_conv_backward(const LifConst &C, const ConvGeom &g, int64_t B,
         // gradient rows, and the WT layout for dt_in: one launch (with a
         // kept forward sort only the gradient roles)
         const int n_cr = (!reuse && n_in > 0 && (grad_W || dt)) ? static_cast<int>(B * g.Hp) : 0;
-        const int n_gr = static_cast<int>((n_pos + kGradPos - 1) / kGradPos);
+        const int n_gr = static_cast<int>((n_pos + kGradPos - 1) / kGradPos) *
+                         ((g.C_out + kGradCh - 1) / kGradCh);
         const int n_wt = (dt && !reuse) ? static_cast<int>(weight_tiles(g)) : 0;
         // dead-neuron terms only where dW is written
         const bool dead = sf.on && sf.dq && grad_W;

@@ -1420,7 +1420,9 @@ __global__ __launch_bounds__(256) void conv_bprep_kernel(
     float *__restrict__ uq, int *__restrict__ qv, int *__restrict__ rend,
     const WT *__restrict__ W, float *__restrict__ Wt) {
     extern __shared__ int sh[];
-    int blk = static_cast<int>(blockIdx.x);
+    // XCD-aware order: neighbouring gradient blocks read the two halves of
+    // the same cache lines of the NCHW outputs
+    int blk = xcd_block(blockIdx.x, gridDim.x);
     if (blk < n_cr) {
         if (cs.key)
             sort_cell_row(C, g, t_in, cs, ev, blk, sh);

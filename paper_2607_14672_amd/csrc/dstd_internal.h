@@ -498,7 +498,9 @@ struct Scan {
     __device__ __forceinline__ void step_k(const LifConst &C, int q, float w) {
         Id += static_cast<double>(w);
         const double vn_d = fma(Vd, C.alpha_d, Id * C.k_dt_d);
-        if (qf < 0 && seg_may_cross(C, Vd, Id, kLast ? C.kmax_last_d : C.kmax_dt_d)) {
+        // one branch: the filter is evaluated on every lane (no short circuit)
+        const bool go = (qf < 0) & seg_may_cross(C, Vd, Id, kLast ? C.kmax_last_d : C.kmax_dt_d);
+        if (go) {
             if (seg_cross<KS>(C, Vd, Id, vn_d, kLast, kLast ? C.last_len : C.dt,
                               kLast ? C.r_lo_last : C.r_lo_dt, sf, hi, fhi))
                 qf = q;

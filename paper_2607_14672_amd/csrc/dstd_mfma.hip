@@ -64,8 +64,7 @@ __global__ __launch_bounds__(256) void mfma_events_kernel(LifConst C, int64_t n,
     ev[k] = u32x4_t{static_cast<uint32_t>(e.row), l1 | (l2 << 16), l3 | (r1 << 16), r2 | (r3 << 16)};
 }
 
-constexpr int kMT = 128;   // rows (b, m) per block tile
-constexpr int kNT = 128;   // neurons per block tile
+constexpr int kNT = 128;   // neurons per block tile (rows (b, m) per tile: MT, 128 or 64)
 constexpr int kKT = 32;    // inputs per K tile
 constexpr int kFrag = 64;  // 16-byte fragments per (32-row block, 16-k step)
 
@@ -73,21 +72,26 @@ constexpr int kFrag = 64;  // 16-byte fragments per (32-row block, 16-k step)
 // fragment per lane, lanes consecutive (conflict-free 128-bit reads)
 __device__ __forceinline__ int frag_slot(int rb, int ks, int lane) { return (rb * 2 + ks) * kFrag + lane; }
 
+// MT rows per tile: each wave owns (MT / 2) x 64 of it, RA = MT / 64 row
+// blocks of 32 (64-row tiles give twice the blocks where the grid of 128-row
+// tiles would not fill the chip).
+template <int MT>
 __global__ __launch_bounds__(256) void mfma_contract_kernel(int M, int64_t rows, int N_in, int N_out,
                                                             const u32x4_t *__restrict__ ev,
                                                             const uint16_t *__restrict__ W,
                                                             float *__restrict__ wh) {
-    __shared__ u32x4_t As[3 * 4 * 2 * kFrag];  // [plane][row block][k step][lane]
-    __shared__ u32x4_t Bs[4 * 2 * kFrag];      // [col block][k step][lane]
+    constexpr int RB = MT / 32, RA = MT / 64;  // row blocks per tile and per wave
+    __shared__ u32x4_t As[3 * RB * 2 * kFrag];  // [plane][row block][k step][lane]
+    __shared__ u32x4_t Bs[4 * 2 * kFrag];       // [col block][k step][lane]
     const int tid = threadIdx.x;
     const int lane = tid & (kWave - 1);
     const int wave = tid >> 6;
-    const int64_t row0 = static_cast<int64_t>(blockIdx.y) * kMT;
+    const int64_t row0 = static_cast<int64_t>(blockIdx.y) * MT;
     const int col0 = blockIdx.x * kNT;
     const int M1 = M + 1;
-    f32x16_t acc[2][2];
+    f32x16_t acc[RA][2];
 #pragma unroll
-    for (int a = 0; a < 2; ++a)
+    for (int a = 0; a < RA; ++a)
 #pragma unroll
         for (int bb = 0; bb < 2; ++bb)
 #pragma unroll
@@ -95,15 +99,15 @@ __global__ __launch_bounds__(256) void mfma_contract_kernel(int M, int64_t rows,
     const int wr = wave >> 1, wc = wave & 1;
     // samples whose rows (b, m) fall in this tile
     const int64_t b_lo = row0 / M1;
-    const int64_t b_hi = min((row0 + kMT - 1) / M1, (rows - 1) / M1);
+    const int64_t b_hi = min((row0 + MT - 1) / M1, (rows - 1) / M1);
     const int ntask = static_cast<int>(b_hi - b_lo + 1) * kKT;  // (sample, input) events per K tile
     uint16_t *As16 = reinterpret_cast<uint16_t *>(As);
-    constexpr int kPlane = 4 * 2 * kFrag;  // fragments per plane
+    constexpr int kPlane = RB * 2 * kFrag;  // fragments per plane
     for (int k0 = 0; k0 < N_in; k0 += kKT) {
         __syncthreads();
         // ---- S tile: zeroed here, the events' nonzero rows written below
 #pragma unroll
-        for (int h = 0; h < 6; ++h) As[tid + h * 256] = u32x4_t{0u, 0u, 0u, 0u};
+        for (int h = 0; h < 3 * RB * 2 * kFrag / 256; ++h) As[tid + h * 256] = u32x4_t{0u, 0u, 0u, 0u};
         // ---- W tile: 16-byte runs of 8 inputs of one neuron
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
@@ -141,14 +145,14 @@ __global__ __launch_bounds__(256) void mfma_contract_kernel(int M, int64_t rows,
             const int fe = (((kk >> 3) & 1) * 32) * 8 + (kk & 7);
             const int fk = kk >> 4;
             const int64_t rL = b * M1 + (row - 1) - row0, rR = b * M1 + row - row0;
-            if (row >= 1 && rL >= 0 && rL < kMT) {
+            if (row >= 1 && rL >= 0 && rL < MT) {
                 const int r = static_cast<int>(rL);
                 const int o = frag_slot(r >> 5, fk, r & 31) * 8 + fe;
                 As16[o] = static_cast<uint16_t>(x.y & 0xFFFFu);
                 As16[kPlane * 8 + o] = static_cast<uint16_t>(x.y >> 16);
                 As16[2 * kPlane * 8 + o] = static_cast<uint16_t>(x.z & 0xFFFFu);
             }
-            if (row <= M && rR >= 0 && rR < kMT) {
+            if (row <= M && rR >= 0 && rR < MT) {
                 const int r = static_cast<int>(rR);
                 const int o = frag_slot(r >> 5, fk, r & 31) * 8 + fe;
                 As16[o] = static_cast<uint16_t>(x.z >> 16);
@@ -167,9 +171,9 @@ __global__ __launch_bounds__(256) void mfma_contract_kernel(int M, int64_t rows,
 #pragma unroll
             for (int p = 0; p < 3; ++p) {
 #pragma unroll
-                for (int a = 0; a < 2; ++a) {
+                for (int a = 0; a < RA; ++a) {
                     const bf16x8_t af =
-                        __builtin_bit_cast(bf16x8_t, As[p * 4 * 2 * kFrag + frag_slot(2 * wr + a, ks, lane)]);
+                        __builtin_bit_cast(bf16x8_t, As[p * kPlane + frag_slot(RA * wr + a, ks, lane)]);
 #pragma unroll
                     for (int bb = 0; bb < 2; ++bb)
                         acc[a][bb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af, bf[bb], acc[a][bb], 0, 0, 0);
@@ -180,14 +184,14 @@ __global__ __launch_bounds__(256) void mfma_contract_kernel(int M, int64_t rows,
     // ---- epilogue: accumulator r of lane l is row (r/4)*8 + (l/32)*4 + r%4,
     // column l%32 of its 32 x 32 tile
 #pragma unroll
-    for (int a = 0; a < 2; ++a)
+    for (int a = 0; a < RA; ++a)
 #pragma unroll
         for (int bb = 0; bb < 2; ++bb) {
             const int col = col0 + 32 * (2 * wc + bb) + (lane & 31);
             if (col >= N_out) continue;
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
-                const int64_t row = row0 + 32 * (2 * wr + a) + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
+                const int64_t row = row0 + 32 * (RA * wr + a) + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
                 if (row < rows) wh[row * N_out + col] = acc[a][bb][r];
             }
         }
@@ -247,9 +251,19 @@ hipError_t launch_forward_mfma(const LifConst &C, int64_t B, int64_t N_in, int64
     const int64_t rows = B * (C.M + 1);
     {
         ProfScope prof("fwd_mfma", st);
-        dim3 grid(static_cast<unsigned>((N_out + kNT - 1) / kNT), static_cast<unsigned>((rows + kMT - 1) / kMT));
-        hipLaunchKernelGGL(mfma_contract_kernel, grid, dim3(256), 0, st, C.M, rows, static_cast<int>(N_in),
-                           static_cast<int>(N_out), static_cast<const u32x4_t *>(ev), W, wh);
+        // 64-row tiles where 128-row tiles would give fewer than four blocks per CU
+        const int64_t nc = (N_out + kNT - 1) / kNT;
+        const bool small = nc * ((rows + 127) / 128) < 1024;
+        const int mt = small ? 64 : 128;
+        dim3 grid(static_cast<unsigned>(nc), static_cast<unsigned>((rows + mt - 1) / mt));
+        if (small)
+            hipLaunchKernelGGL(mfma_contract_kernel<64>, grid, dim3(256), 0, st, C.M, rows,
+                               static_cast<int>(N_in), static_cast<int>(N_out),
+                               static_cast<const u32x4_t *>(ev), W, wh);
+        else
+            hipLaunchKernelGGL(mfma_contract_kernel<128>, grid, dim3(256), 0, st, C.M, rows,
+                               static_cast<int>(N_in), static_cast<int>(N_out),
+                               static_cast<const u32x4_t *>(ev), W, wh);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }

@@ -637,10 +637,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(6, 8))) voi
     }
     if (!done) {
         // the last row's sums reach grid points cur-1 and cur; after them no
-        // input arrives, and the rest of the scan is skipped once no lane
-        // still searching can reach the threshold
+        // input arrives: the rest of the window is one free-decay segment
         close_to_end(min(cur + 2, R - 1));
-        if (cur < R - 1 && __any(row_ok && sc.may_still_fire(C))) close_to_end(R - 1);
+        if (cur < R - 1) sc.tail(C, cur - 1);
     }
     if (!row_ok) return;
     float to, sl;
@@ -917,9 +916,10 @@ __global__ __launch_bounds__(256) void conv_fwd_list_kernel(LifConst C, ConvGeom
             }
             for (; i0 < n; ++i0) list_batch<1>(ewb, eLR, my_s + i0, my_n - i0, wr, voff, aL, aR);
         } else if (r == r_last + 2) {
-            // every record is in: stop once no lane still searching can
-            // reach the threshold without further input
-            if (!__any(row_ok && sc.may_still_fire(C))) break;
+            // every record is in: grid points r-1 .. M see no input, the rest
+            // of the window is one free-decay segment
+            sc.tail(C, r - 1);
+            break;
         }
         // grid point r-1: this row's L sums plus the previous row's R sums
         if (r >= 1) sc.step(C, r - 1, aL + carry);

@@ -490,6 +490,7 @@ struct Scan {
     int qf = -1;
     Seg sf{0.f, 0.f};
     float hi = 0.f, fhi = 0.f;  // bracket end of the crossing and v - theta there
+    bool tl = false;            // the bracket is on the free-decay tail from T_qf
 
     // grid point q: w^_q enters the current, and the interval after T_q
     // (kLast: the last one, [T_M, t_max)) is tested. The filter runs on every
@@ -514,13 +515,24 @@ struct Scan {
         else step_k<false>(C, q, w);
     }
 
-    // With no further input, can this lane still cross? (v never exceeds
-    // max(V, 0) + max(I, 0) kpeak_d over the rest of the window.)
-    __device__ __forceinline__ bool may_still_fire(const LifConst &C) const {
-        return qf < 0 && seg_may_cross(C, Vd, Id, C.kpeak_d);
-    }
-
     __device__ __forceinline__ bool found() const { return qf >= 0; }
+
+    // No input arrives at grid points q0 .. M (the state is v at T_q0 and the
+    // current before the empty event there): from T_q0 to t_max v is one free
+    // decay, v(T_q0 + u) = V e^{-u/tv} + I K(u), the same function the
+    // remaining intervals would be tested on one by one. Its first crossing,
+    // if any, is bracketed once by the interval analysis applied to the whole
+    // segment; finish() then solves it there and names the interval that
+    // holds it. Lanes that have found their interval are unchanged.
+    __device__ __forceinline__ void tail(const LifConst &C, int q0) {
+        if (qf >= 0 || !seg_may_cross(C, Vd, Id, C.kpeak_d)) return;
+        const float len = fmaf(static_cast<float>(C.M - q0), C.dt, C.last_len);  // +inf stays
+        const float r_lo = (kind_of<KS>(C) == kGeneral && len < INFINITY) ? expf(-C.kappa * len) : 0.f;
+        if (seg_cross<KS>(C, Vd, Id, 0.0, true, len, r_lo, sf, hi, fhi)) {
+            qf = q0;
+            tl = true;
+        }
+    }
 
     __device__ __forceinline__ void finish(const LifConst &C, float &t_out, float &slope,
                                            int &q_out) const {
@@ -533,6 +545,7 @@ struct Scan {
         t_out = static_cast<float>(fma(static_cast<double>(qf), static_cast<double>(C.dt),
                                        static_cast<double>(C.t0)) + static_cast<double>(u));
         slope = sl;
+        if (tl) q_out = qf + min(static_cast<int>(u * C.inv_dt), C.M - qf);
     }
 };
 

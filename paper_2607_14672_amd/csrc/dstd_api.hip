@@ -145,6 +145,14 @@ LifConst make_const(const dstd_lif_params *p) {
     C.kmax_last_d = kern_d(kind, tv, ti, std::min(last, upk));
     C.theta_lo_d = (double)p->threshold / 1.0001;
     C.kpeak_d = kern_d(kind, tv, ti, std::min((double)p->M * dt + last, upk));
+    // max |K''| on [0, dt]: general row c |e^{-u/tv}/tv^2 - e^{-u/ti}/ti^2|
+    // <= c / ti^2; (tau, tau) e^{-u/tau} |u/tau^2 - 2/tau| <= 2/tau + dt/tau^2;
+    // (inf, tau) e^{-u/tau}/tau <= 1/tau; (inf, inf) 0
+    const double kpp = (kind == dstd::kGeneral) ? tv / (ti * (tv - ti))
+                       : (kind == dstd::kEqual) ? 2.0 / ti + dt / (ti * ti)
+                       : (kind == dstd::kInfTau) ? 1.0 / ti : 0.0;
+    C.curv_v_d = dt * dt / 8.0 * (isinf(tv) ? 0.0 : 1.0 / (tv * tv));
+    C.curv_i_d = dt * dt / 8.0 * kpp;
     C.twice = (kind == dstd::kGeneral && tv == 2.0 * ti) ? 1 : 0;
     C.inv_dt = (float)(1.0 / dt);
     C.e_mdt = (float)exp(-dt / ti);

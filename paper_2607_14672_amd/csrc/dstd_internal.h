@@ -60,6 +60,9 @@ struct LifConst {
     // without bound): with no further input, v never exceeds
     // max(V, 0) + max(I, 0) kpeak_d
     double kpeak_d;
+    // curvature bound of one interval of length dt: dt^2/8 times 1/tv^2 and
+    // times max |K''| on [0, dt] (the filter of the intervals before T_M)
+    double curv_v_d, curv_i_d;
     int twice;  // general row with tv = 2 ti exactly: closed-form crossing
 };
 
@@ -379,6 +382,17 @@ __device__ __forceinline__ bool seg_may_cross(const LifConst &C, double Vd, doub
     return ub >= C.theta_lo_d;
 }
 
+// The filter of an interval of length dt (before T_M) from its two ends: on
+// [0, dt] the linear interpolation of v(0) = V and v(dt) = vn lies below
+// max(V, vn), and v exceeds it by at most dt^2/8 max(-v''), where
+// |v''| <= |V| / tv^2 + |I| max |K''|. Every interval whose maximum reaches
+// theta_lo passes; the ones hovering below theta do not.
+__device__ __forceinline__ bool seg_may_cross_dt(const LifConst &C, double Vd, double Id,
+                                                 double vn_d) {
+    const double ub = fma(fabs(Id), C.curv_i_d, fma(fabs(Vd), C.curv_v_d, fmax(Vd, vn_d)));
+    return ub >= C.theta_lo_d;
+}
+
 // The analysis of an interval that passed the filter.
 template <int KS = kAnyKind>
 __device__ __forceinline__ bool seg_cross(const LifConst &C, double Vd, double Id, double vn_d,
@@ -500,7 +514,8 @@ struct Scan {
         Id += static_cast<double>(w);
         const double vn_d = fma(Vd, C.alpha_d, Id * C.k_dt_d);
         // one branch: the filter is evaluated on every lane (no short circuit)
-        const bool go = (qf < 0) & seg_may_cross(C, Vd, Id, kLast ? C.kmax_last_d : C.kmax_dt_d);
+        const bool go = (qf < 0) & (kLast ? seg_may_cross(C, Vd, Id, C.kmax_last_d)
+                                          : seg_may_cross_dt(C, Vd, Id, vn_d));
         if (go) {
             if (seg_cross<KS>(C, Vd, Id, vn_d, kLast, kLast ? C.last_len : C.dt,
                               kLast ? C.r_lo_last : C.r_lo_dt, sf, hi, fhi))

@@ -969,13 +969,21 @@ __device__ void grad_block(const LifConst &C, const ConvGeom &g, int64_t n_pos, 
     // dt_in kernels read no others); with more than one channel tile their
     // largest q over all channels is found first (by every tile's block).
     const bool tiles = ntile > 1;
+    // each thread keeps one position (blockDim is a multiple of kGradPos):
+    // its NCHW offset at channel 0, decoded once
+    const int pl = static_cast<int>(threadIdx.x) % kGradPos;
+    const int cstep = static_cast<int>(blockDim.x) / kGradPos;
+    const bool pos_ok = s0 + pl < n_pos;
+    int64_t obase = 0;
+    if (pos_ok) {
+        const int si = static_cast<int>(s0 + pl);  // B * Ho * Wo < 2^31 (checked at the boundary)
+        const int b = si / HoWo;
+        obase = static_cast<int64_t>(b) * g.C_out * HoWo + (si - b * HoWo);
+    }
     if (tiles) {
-        for (int e = threadIdx.x; e < g.C_out * kGradPos; e += blockDim.x) {
-            const int co = e / kGradPos, pl = e % kGradPos;
-            const int64_t sp = s0 + pl;
-            if (sp < n_pos) {
-                const int si = static_cast<int>(sp);
-                const int64_t o = (static_cast<int64_t>(si / HoWo) * g.C_out + co) * HoWo + si % HoWo;
+        if (pos_ok) {
+            for (int co = static_cast<int>(threadIdx.x) / kGradPos; co < g.C_out; co += cstep) {
+                const int64_t o = obase + static_cast<int64_t>(co) * HoWo;
                 const int q = q_idx[o];
                 if (q >= 0) {
                     float gt = grad_t[o];
@@ -988,15 +996,11 @@ __device__ void grad_block(const LifConst &C, const ConvGeom &g, int64_t n_pos, 
     }
     {
         const int c0 = tile * kGradCh;
-        for (int e = threadIdx.x; e < kGradCh * kGradPos; e += blockDim.x) {
-            const int cl = e / kGradPos, pl = e % kGradPos;
+        for (int cl = static_cast<int>(threadIdx.x) / kGradPos; cl < kGradCh; cl += cstep) {
             const int co = c0 + cl;
-            const int64_t sp = s0 + pl;
             GradPrep gp{0.f, 0.f, -1};
-            if (co < g.C_out && sp < n_pos) {
-                const int64_t b = static_cast<int>(sp) / HoWo;
-                const int p = static_cast<int>(sp) % HoWo;
-                const int64_t o = (b * g.C_out + co) * HoWo + p;
+            if (co < g.C_out && pos_ok) {
+                const int64_t o = obase + static_cast<int64_t>(co) * HoWo;
                 const int q = q_idx[o];
                 if (q >= 0) {  // silent neurons: no further loads
                     float gt = grad_t[o];
@@ -1012,14 +1016,14 @@ __device__ void grad_block(const LifConst &C, const ConvGeom &g, int64_t n_pos, 
         }
         __syncthreads();
         for (int e = threadIdx.x; e < kGradPos * kGradCh; e += blockDim.x) {
-            const int pl = e / kGradCh, cl = e % kGradCh;
+            const int pw = e / kGradCh, cl = e % kGradCh;
             const int co = c0 + cl;
-            const int64_t sp = s0 + pl;
-            if (co < g.C_out && sp < n_pos && sl[pl] >= 0) {
+            const int64_t sp = s0 + pw;
+            if (co < g.C_out && sp < n_pos && sl[pw] >= 0) {
                 const int64_t d = sp * g.C_out + co;
-                gam[d] = sg[cl * kS + pl];
-                uq[d] = su[cl * kS + pl];
-                qv[d] = sq[cl * kS + pl];
+                gam[d] = sg[cl * kS + pw];
+                uq[d] = su[cl * kS + pw];
+                qv[d] = sq[cl * kS + pw];
             }
         }
         __syncthreads();
@@ -1333,9 +1337,10 @@ __global__ __launch_bounds__(256) void conv_dw_kernel(LifConst C, ConvGeom g, in
 }
 
 // dW[co, ci, ky, kx] = (1/P) sum_z part[z][co][k * C_in + ci]. Threads follow
-// the partial-sum layout (coalesced reads); a block holds 256 / G consecutive
-// entries x G split groups (G from red_groups: more groups where there are
-// many splits): group h sums z = h, h + G, ...; the G group sums are added in
+// the partial-sum layout (coalesced reads); a block takes groups of 256 / G
+// consecutive entries x G split groups (G from red_groups: more groups where
+// there are many splits; at most 2048 blocks, each taking every nblk-th entry
+// group): group h sums z = h, h + G, ...; the G group sums are added in
 // group order (fixed order: deterministic) and written to the [co][ci][ky][kx]
 // slot. Splits without gradient-carrying samples wrote no partials and are
 // skipped (their sums would be +0, which leaves every partial sum unchanged);
@@ -1348,26 +1353,28 @@ __host__ __device__ __forceinline__ int red_groups(int nsplit) {
 
 __device__ void dw_reduce_block(const ConvGeom &g, int nsplit, const float *__restrict__ part,
                                 const int *__restrict__ zlive, const float *__restrict__ dq,
-                                float *__restrict__ dW, int64_t blk, float *red) {
+                                float *__restrict__ dW, int blk, int nblk, float *red) {
     const int KT = g.KH * g.KW;
     const int NJ = KT * g.C_in;
     const int64_t n = static_cast<int64_t>(g.C_out) * NJ;
     const int G = red_groups(nsplit), O = static_cast<int>(blockDim.x) / G;
     const int lo = threadIdx.x % O, h = threadIdx.x / O;
-    const int64_t src = blk * O + lo;  // [co][k][ci]
     bool any = false;
     for (int z = threadIdx.x; z < nsplit; z += blockDim.x) any = any || zlive[z] != 0;
     any = __syncthreads_or(any);
     if (!any) {
         // no split carries gradient (the same for every block of the layer):
-        // dW is the dead-neuron term or 0, written in dW's own order, one
-        // entry per thread, by the first n / blockDim blocks (coalesced)
-        const int64_t i = blk * blockDim.x + threadIdx.x;
-        if (i < n) dW[i] = dq ? 0.f + dq[i / NJ] : 0.f;
+        // dW is the dead-neuron term or 0, written in dW's own order
+        // (coalesced)
+        for (int64_t i = static_cast<int64_t>(blk) * blockDim.x + threadIdx.x; i < n;
+             i += static_cast<int64_t>(nblk) * blockDim.x)
+            dW[i] = dq ? 0.f + dq[i / NJ] : 0.f;
         return;
     }
-    float tot = 0.f;
-    {
+    // groups of O outputs, nblk blocks apart (block-uniform trip count)
+    const int64_t ngrp = (n + O - 1) / O;
+    for (int64_t grp = blk; grp < ngrp; grp += nblk) {
+        const int64_t src = grp * O + lo;  // [co][k][ci]
         float s = 0.f;
         if (src < n) {
 #pragma unroll 8
@@ -1376,15 +1383,17 @@ __device__ void dw_reduce_block(const ConvGeom &g, int nsplit, const float *__re
         }
         red[h * O + lo] = s;
         __syncthreads();
+        float tot = 0.f;
         if (h == 0)
             for (int q = 0; q < G; ++q) tot += red[q * O + lo];
-    }
-    if (h == 0 && src < n) {
-        const int co = static_cast<int>(src / NJ);
-        const int rem = static_cast<int>(src % NJ);
-        const int k = rem / g.C_in, ci = rem % g.C_in;
-        const float v = tot * g.inv_P;
-        dW[(static_cast<int64_t>(co) * g.C_in + ci) * KT + k] = dq ? v + dq[co] : v;
+        __syncthreads();  // red is rewritten by the next group
+        if (h == 0 && src < n) {
+            const int co = static_cast<int>(src / NJ);
+            const int rem = static_cast<int>(src % NJ);
+            const int k = rem / g.C_in, ci = rem % g.C_in;
+            const float v = tot * g.inv_P;
+            dW[(static_cast<int64_t>(co) * g.C_in + ci) * KT + k] = dq ? v + dq[co] : v;
+        }
     }
 }
 
@@ -1456,7 +1465,7 @@ __global__ __launch_bounds__(256) void conv_bfin_kernel(ConvGeom g, int R, int n
     __shared__ float lds[kGatherSlots];
     const int blk = static_cast<int>(blockIdx.x);
     if (blk < n_red) {
-        dw_reduce_block(g, nsplit, part, zlive, dq, dW, blk, lds);
+        dw_reduce_block(g, nsplit, part, zlive, dq, dW, blk, n_red, lds);
     } else {
         const int t = blk - n_red;
         dt_gather_block(g, R, cs, rend, dt_in, t / nsl, (t % nsl) * kGatherSlots, lds);
@@ -1703,8 +1712,10 @@ hipError_t launch_conv_backward(const LifConst &C, const ConvGeom &g, int64_t B,
     {
         // dW split reduction and dt_in gather: one launch
         const int64_t n = static_cast<int64_t>(g.C_out) * nj;
-        const int red_out = 256 / red_groups(p.nsplit);  // outputs per reduction block
-        const int n_red = grad_W ? static_cast<int>((n + red_out - 1) / red_out) : 0;
+        // reduction blocks: one per red_out outputs, at most 2048 (each then
+        // takes every 2048th group)
+        const int red_out = 256 / red_groups(p.nsplit);
+        const int n_red = grad_W ? static_cast<int>(std::min<int64_t>((n + red_out - 1) / red_out, 2048)) : 0;
         const int per = g.Wp * g.PC;
         const int nsl = (per + kGatherSlots - 1) / kGatherSlots;
         const int n_ga = dt ? static_cast<int>(B * g.Hp) * nsl : 0;

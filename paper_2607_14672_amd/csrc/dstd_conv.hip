@@ -449,6 +449,37 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(6, 8))) voi
             ++cur;
         }
     };
+    // the sums of a batch of nk <= kCBatch list entries in order; true once
+    // every lane has found its interval. A full batch inside one event row
+    // (rows never decrease along the list) is summed without per-entry tests.
+    auto sum_batch = [&](const FwdEntry (&e)[kCBatch], const float (&w)[kCBatch], int nk) {
+        const int ra = uniform(e[0].row);
+        if (nk == kCBatch && ra == uniform(e[kCBatch - 1].row)) {
+            if (ra != cur) {
+                close_to_mid(ra);
+                if (__all(sc.found() || !row_ok)) return true;
+            }
+#pragma unroll
+            for (int q = 0; q < kCBatch; ++q) {
+                aL = fmaf(w[q], e[q].L, aL);
+                aR = fmaf(w[q], e[q].R, aR);
+            }
+            return false;
+        }
+#pragma unroll
+        for (int q = 0; q < kCBatch; ++q) {
+            if (q < nk) {
+                const int row = uniform(e[q].row);
+                if (row != cur) {
+                    close_to_mid(row);
+                    if (__all(sc.found() || !row_ok)) return true;
+                }
+                aL = fmaf(w[q], e[q].L, aL);
+                aR = fmaf(w[q], e[q].R, aR);
+            }
+        }
+        return false;
+    };
     bool done = false, started = false;
     if constexpr (kDirect) {
         const int F = g.KH * g.KW * g.PC;
@@ -502,23 +533,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(6, 8))) voi
             for (int q = 0; q < kCBatch; ++q) e[q] = my[s0 + q];  // LDS broadcasts
 #pragma unroll
             for (int q = 0; q < kCBatch; ++q) w[q] = BufLoad<float>::get(wr, voff + e[q].wb, 0);
-            const int nk = min(kCBatch, total - s0);
-#pragma unroll
-            for (int q = 0; q < kCBatch; ++q) {
-                if (q < nk) {
-                    const int row = uniform(e[q].row);
-                    if (row != cur) {
-                        close_to_mid(row);
-                        if (__all(sc.found() || !row_ok)) {
-                            done = true;
-                            break;
-                        }
-                    }
-                    aL = fmaf(w[q], e[q].L, aL);
-                    aR = fmaf(w[q], e[q].R, aR);
-                }
+            if (sum_batch(e, w, min(kCBatch, total - s0))) {
+                done = true;
+                break;
             }
-            if (done) break;
         }
     } else {
     // the KH cell rows' record counts (scalar loads) rule out most positions
@@ -605,23 +623,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(6, 8))) voi
                 for (int q = 0; q < kCBatch; ++q) e[q] = my[s0 + q];  // LDS broadcasts
 #pragma unroll
                 for (int q = 0; q < kCBatch; ++q) w[q] = BufLoad<float>::get(wr, voff + e[q].wb, 0);
-                const int nk = min(kCBatch, nc - s0);
-#pragma unroll
-                for (int q = 0; q < kCBatch; ++q) {
-                    if (q < nk) {
-                        const int row = uniform(e[q].row);
-                        if (row != cur) {
-                            close_to_mid(row);
-                            if (__all(sc.found() || !row_ok)) {
-                                done = true;
-                                break;
-                            }
-                        }
-                        aL = fmaf(w[q], e[q].L, aL);
-                        aR = fmaf(w[q], e[q].R, aR);
-                    }
+                if (sum_batch(e, w, min(kCBatch, nc - s0))) {
+                    done = true;
+                    break;
                 }
-                if (done) break;
             }
             __builtin_amdgcn_wave_barrier();
         }

@@ -52,3 +52,29 @@ def test_conv_row(dev, tm, ts, k, tmax, geom):  # noqa: F811
     p, t, W = tc._conv_case(5, 3, cs, 16, tm, ts, k=k, t_max=tmax)
     t = tc._special_inputs(t, p, np.random.default_rng(9))
     tc._conv_parity(dev, p, cs, t, W, f"conv row ({tm},{ts}) {geom}", seed=2)
+
+
+# Kernels much faster than the grid (taus well below dt = 1/8): crossings
+# lie on bumps inside one interval, with v below threshold at both of its
+# ends (so for every fired neuron of the dense cases, checked on the oracle's
+# grid potentials for these seeds), where the scan's interval filter can only
+# pass them through its curvature term.
+FAST = [(0.05, 0.02), (0.03, 0.03), (0.02, 0.06)]
+FAST_IDS = ["general", "tau-tau", "tau-2tau"]
+
+
+@pytest.mark.parametrize("tm,ts", FAST, ids=FAST_IDS)
+def test_dense_fast_kernel_interior_crossings(dev, tm, ts):  # noqa: F811
+    p, t, W = _layer_case(11, 5, 120, 70, 8, tm, ts, k=60.0, spread=0.3)
+    gpu, orc = _fwd_bwd_parity(dev, p, t, W, f"fast kernel ({tm},{ts})", seed=5)
+    assert (orc["q"] >= 0).sum() > 50
+
+
+@pytest.mark.parametrize("tm,ts", FAST[:2], ids=FAST_IDS[:2])
+@pytest.mark.parametrize("geom", [dict(C_in=8, H=8, W=8, C_out=40), dict(C_in=4, H=9, W=9, C_out=24),
+                                  dict(C_in=2, H=10, W=10, C_out=70)],
+                         ids=["walk", "list", "direct"])
+def test_conv_fast_kernel_interior_crossings(dev, tm, ts, geom):  # noqa: F811
+    cs = tc._cs(**geom)
+    p, t, W = tc._conv_case(7, 3, cs, 8, tm, ts, k=60.0, spread=0.3)
+    tc._conv_parity(dev, p, cs, t, W, f"conv fast kernel ({tm},{ts}) {geom}", seed=6)

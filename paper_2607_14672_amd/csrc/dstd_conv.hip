@@ -399,24 +399,64 @@ struct FwdEntry { int wb, row; float L, R; };
 // within a row the order is kernel row, cell column, input slot: the sorted
 // walk's order) from ballots of the row's bits; the ranked entries go to the
 // same LDS list as one chunk of the walk.
+// A block takes kFwdWaves consecutive output positions of one 64-channel
+// tile, one per wave. Before its own position, every wave of the sorted walk
+// makes the same block-level test from scalar loads (no barrier): where the
+// block's positions lie in one image and the cell rows their receptive
+// fields span hold no records at all, the waves write the block's silent
+// outputs together, as runs of kFwdWaves consecutive positions per channel,
+// instead of 64 single floats 4 * Ho * Wo bytes apart per position (such
+// scattered stores bound the forward of layers without input events).
 // (At most 80 VGPRs: six waves per SIMD, measured faster than five; eight
 // would spill.)
+constexpr int kFwdWaves = 4;
 template <int KHT, int KS, bool kDirect>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(6, 8))) void conv_fwd_kernel(LifConst C, ConvGeom g, int64_t n_pos,
+__global__ __launch_bounds__(kFwdWaves * kWave) __attribute__((amdgpu_waves_per_eu(6, 8))) void conv_fwd_kernel(LifConst C, ConvGeom g, int64_t n_pos,
                                                        const float *__restrict__ Wt,
                                                        ConvSorted cs, const float *__restrict__ t_in,
                                                        float *__restrict__ t_out,
                                                        float *__restrict__ slope,
                                                        int *__restrict__ q_idx) {
-    __shared__ FwdEntry ent[4][kWave];
+    __shared__ FwdEntry ent[kFwdWaves][kWave];
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = uniform(threadIdx.x >> 6);
-    const int64_t p = static_cast<int64_t>(xcd_block(blockIdx.x, gridDim.x)) * (blockDim.x >> 6) + wave;
+    const int64_t p0 = static_cast<int64_t>(xcd_block(blockIdx.x, gridDim.x)) * kFwdWaves;
+    const int64_t p = p0 + wave;
+    const int HoWo = g.Ho * g.Wo;
+    if constexpr (!kDirect) {
+        // positions p0 .. pl (p0 < n_pos: the grid holds no empty block);
+        // B * Ho * Wo < 2^31 (checked at the boundary)
+        const int q0 = static_cast<int>(p0), ql = static_cast<int>(min(p0 + kFwdWaves, n_pos) - 1);
+        const int b0 = q0 / HoWo;
+        if (b0 == ql / HoWo) {
+            const int y_lo = max(0, (q0 - b0 * HoWo) / g.Wo * g.stride - g.pad);
+            const int y_hi = min(g.Hp - 1, (ql - b0 * HoWo) / g.Wo * g.stride - g.pad + g.KH - 1);
+            const int nb1 = rows_of(C) * g.Wp + 1;
+            int recs = 0;
+            for (int y = y_lo; y <= y_hi; ++y)
+                recs |= *as_const(cs.off + (static_cast<int64_t>(b0) * g.Hp + y) * nb1 + nb1 - 1);
+            if (recs == 0) {
+                // element e = wave * 64 + lane: channel e / kFwdWaves,
+                // position e % kFwdWaves
+                const int e = wave * kWave + lane;
+                const int64_t ps = p0 + e % kFwdWaves;
+                const int o = blockIdx.y * kWave + e / kFwdWaves;
+                if (ps < n_pos && o < g.C_out) {
+                    const int pi = static_cast<int>(ps);
+                    const int bb = pi / HoWo;
+                    const int64_t idx = (static_cast<int64_t>(bb) * g.C_out + o) * HoWo + (pi - bb * HoWo);
+                    t_out[idx] = INFINITY;
+                    slope[idx] = 0.f;
+                    q_idx[idx] = -1;
+                }
+                return;
+            }
+        }
+    }
     if (p >= n_pos) return;  // wave-uniform; no block barrier below
     FwdEntry *my = ent[wave];
     const int co = blockIdx.y * kWave + lane;
     const bool row_ok = co < g.C_out;
-    const int HoWo = g.Ho * g.Wo;
     const int R = rows_of(C);
     PosWalk<KHT> wk;
     wk.init(C, g, p);
@@ -1552,11 +1592,11 @@ hipError_t launch_conv_forward(const LifConst &C, const ConvGeom &g, int64_t B, 
 #undef CFL
         return hipGetLastError();
     }
-    dim3 grid(static_cast<unsigned>((n_pos + waves - 1) / waves),
+    dim3 grid(static_cast<unsigned>((n_pos + kFwdWaves - 1) / kFwdWaves),
               static_cast<unsigned>((g.C_out + kWave - 1) / kWave));
 #define CFW(KHV, KSV, DV)                                                                        \
-    hipLaunchKernelGGL((conv_fwd_kernel<KHV, KSV, DV>), grid, dim3(waves * kWave), 0, st, C, g,    \
-                       n_pos, Wt, cs, t_in, t_out, slope, q_idx)
+    hipLaunchKernelGGL((conv_fwd_kernel<KHV, KSV, DV>), grid, dim3(kFwdWaves * kWave), 0, st, C, \
+                       g, n_pos, Wt, cs, t_in, t_out, slope, q_idx)
 #define CFW_D(KHV, KSV)                                                   \
     do {                                                                  \
         if (direct) CFW(KHV, KSV, true);                                  \

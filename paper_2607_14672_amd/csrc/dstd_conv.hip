@@ -751,8 +751,43 @@ __global__ __launch_bounds__(256) void conv_fwd_list_kernel(LifConst C, ConvGeom
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = uniform(threadIdx.x >> 6);
     const int half = lane / LP, li = lane % LP, hb = half * LP;  // hb: the position's first lane
-    const int64_t p0 =
-        (static_cast<int64_t>(xcd_block(blockIdx.x, gridDim.x)) * (blockDim.x >> 6) + wave) * NP;
+    const int nwb = blockDim.x >> 6;
+    const int64_t pb = static_cast<int64_t>(xcd_block(blockIdx.x, gridDim.x)) * nwb * NP;
+    const int64_t p0 = pb + wave * NP;
+    if constexpr (!kDirect) {
+        // the block's positions pb .. (nwb * NP of them; pb < n_pos): where
+        // they lie in one image and the cell rows their receptive fields span
+        // hold no records, the waves write the block's silent outputs
+        // together, as runs of nwb * NP positions per channel (the same test
+        // in every wave, from scalar loads: no barrier)
+        const int HoWo = g.Ho * g.Wo, npb = nwb * NP;
+        const int q0 = static_cast<int>(pb), ql = static_cast<int>(min(pb + npb, n_pos) - 1);
+        const int b0 = q0 / HoWo;
+        if (b0 == ql / HoWo) {
+            const int y_lo = max(0, (q0 - b0 * HoWo) / g.Wo * g.stride - g.pad);
+            const int y_hi = min(g.Hp - 1, (ql - b0 * HoWo) / g.Wo * g.stride - g.pad + g.KH - 1);
+            const int nb1 = rows_of(C) * g.Wp + 1;
+            int recs = 0;
+            for (int y = y_lo; y <= y_hi; ++y)
+                recs |= *as_const(cs.off + (static_cast<int64_t>(b0) * g.Hp + y) * nb1 + nb1 - 1);
+            if (recs == 0) {
+                // element e = wave * 64 + lane: channel e / npb, position e % npb
+                for (int e = wave * kWave + lane; e < npb * LP; e += static_cast<int>(blockDim.x)) {
+                    const int64_t ps = pb + e % npb;
+                    const int o = blockIdx.y * LP + e / npb;
+                    if (ps < n_pos && o < g.C_out) {
+                        const int pi = static_cast<int>(ps);
+                        const int bb = pi / HoWo;
+                        const int64_t idx = (static_cast<int64_t>(bb) * g.C_out + o) * HoWo + (pi - bb * HoWo);
+                        t_out[idx] = INFINITY;
+                        slope[idx] = 0.f;
+                        q_idx[idx] = -1;
+                    }
+                }
+                return;
+            }
+        }
+    }
     if (p0 >= n_pos) return;  // wave-uniform; no block barrier below
     const int64_t p = p0 + half;
     const bool pos_ok = p < n_pos;

@@ -108,14 +108,32 @@ __device__ void sort_cell_row(const LifConst &C, const ConvGeom &g, const float 
     float *tl = sort_stage_floats(C.M, g) > 0 ? reinterpret_cast<float *>(part + 256) : nullptr;
     for (int k = threadIdx.x; k < nb; k += blockDim.x) hist[k] = 0;
     if (tl) {
+        // staged rows are checked for events as they are read: a row without
+        // any (the deep layers at random initialisation) skips the
+        // histogram pass. The test is a window 0.001 dt wider at both ends
+        // than the one bin_row keeps, [T_0 - dt, T_M + dt) (a superset:
+        // bin_row's rounding moves its bounds far less), so it costs two
+        // compares; NaN and +-inf fail it.
         const int per = g.Wp * g.PC;
+        const float w_lo = C.t0 - 1.001f * C.dt;
+        const float w_hi = fmaf(static_cast<float>(C.M) + 1.001f, C.dt, C.t0);
+        bool any = false;
         for (int t = threadIdx.x; t < per; t += blockDim.x) {
             int slot;
             const int64_t src = cell_row_input(g, b, py, t, slot);
-            tl[slot] = t_in[src];
+            const float v = t_in[src];
+            tl[slot] = v;
+            any = any || (v >= w_lo && v < w_hi);
         }
+        if (!__syncthreads_or(any)) {
+            if (ev.row && threadIdx.x == 0) ev.live[cr] = 0;
+            int *off0 = cs.off + static_cast<int64_t>(cr) * (nb + 1);
+            for (int f = threadIdx.x; f <= nb; f += blockDim.x) off0[f] = 0;
+            return;
+        }
+    } else {
+        __syncthreads();
     }
-    __syncthreads();
     auto t_at = [&](int px, int j) {
         if (tl) return tl[px * g.PC + j];
         int y, x;

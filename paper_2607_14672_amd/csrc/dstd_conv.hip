@@ -1102,7 +1102,8 @@ __device__ void grad_block(const LifConst &C, const ConvGeom &g, int64_t n_pos, 
                 const int q = q_idx[o];
                 if (q >= 0) {  // silent neurons: no further loads
                     float gt = grad_t[o];
-                    const float t = t_out[o];
+                    // the spike time only where it is used (no gradient: no load)
+                    const float t = (sf.on || gt != 0.f) ? t_out[o] : 0.f;
                     if (sf.on) gt += synfire_dt(sf, t);
                     if (gt != 0.f) gp = grad_prep(C, t, slope[o], q, gt);
                 }

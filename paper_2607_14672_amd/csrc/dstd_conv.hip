@@ -1256,7 +1256,19 @@ __device__ void dt_gather_block(const ConvGeom &g, int R, const ConvSorted &cs,
     const int nb1 = R * g.Wp + 1;
     const int nrec = uniform(min(max(cs.off[static_cast<int64_t>(cr) * nb1 + nb1 - 1], 0), per));
     const int b = cr / g.Hp, py = cr % g.Hp;
-    if (nrec == 0) {  // no input of the cell row has events
+    const int64_t pos0 = static_cast<int64_t>(b) * g.Ho * g.Wo;
+    // output rows oy whose kernel row ky = py + pad - oy * stride is in
+    // range, walked with ky ascending (the tap order of the sum)
+    const int ny0 = py + g.pad;
+    const int oy_hi = min(g.Ho - 1, ny0 / g.stride);
+    const int oy_lo = (max(0, ny0 - g.KH + 1) + g.stride - 1) / g.stride;
+    // no record, or no output position of those rows passes gradient: the
+    // cell row's dt_in is 0
+    bool live = false;
+    if (nrec > 0)
+        for (int k = threadIdx.x; k < (oy_hi - oy_lo + 1) * g.Wo; k += blockDim.x)
+            live = live || rend[pos0 + static_cast<int64_t>(oy_lo) * g.Wo + k] >= 0;
+    if (!__syncthreads_or(live)) {
         for (int t = threadIdx.x; t < per; t += blockDim.x) {
             int slot;
             const int64_t dst = cell_row_input(g, b, py, t, slot);
@@ -1268,12 +1280,6 @@ __device__ void dt_gather_block(const ConvGeom &g, int R, const ConvSorted &cs,
     __syncthreads();
     const int64_t rb = static_cast<int64_t>(cr) * per;
     const int KT = g.KH * g.KW;
-    const int64_t pos0 = static_cast<int64_t>(b) * g.Ho * g.Wo;
-    // output rows oy whose kernel row ky = py + pad - oy * stride is in
-    // range, walked with ky ascending (the tap order of the sum)
-    const int ny0 = py + g.pad;
-    const int oy_hi = min(g.Ho - 1, ny0 / g.stride);
-    const int oy_lo = (max(0, ny0 - g.KH + 1) + g.stride - 1) / g.stride;
     for (int k = threadIdx.x; k < nrec; k += blockDim.x) {
         const int src = cs.src[rb + k];
         if (src < s0 || src >= s0 + ns) continue;

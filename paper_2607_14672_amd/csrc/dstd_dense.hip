@@ -188,7 +188,8 @@ __global__ __launch_bounds__(kPrepThreads) void prep_kernel(LifConst C, int n_so
             GradPrep gp{0.f, 0.f, -1};
             if (q >= 0) {  // silent neurons: no further loads
                 float g = pg.grad_t[k];
-                const float t = pg.t_out[k];
+                // the spike time only where it is used (no gradient: no load)
+                const float t = (pg.sf.on || g != 0.f) ? pg.t_out[k] : 0.f;
                 if (pg.sf.on) g += synfire_dt(pg.sf, t);
                 if (g != 0.f) gp = grad_prep(C, t, pg.slope[k], q, g);
             }

@@ -311,7 +311,7 @@ ConvWs conv_ws_layout(int M, const dstd::ConvGeom &g, int64_t B, bool backward) 
     w.key = off; off += align_up(nr * sizeof(int));
     w.L = off; off += align_up(nr * sizeof(float));
     w.R = off; off += align_up(nr * sizeof(float));
-    w.off = off; off += align_up((size_t)B * g.Hp * ((size_t)R * g.Wp + 1) * sizeof(int));
+    w.off = off; off += align_up((size_t)B * g.Hp * (size_t)dstd::conv_off_stride(R, g) * sizeof(int));
     if (backward) {
         w.px = off; off += align_up(nr * sizeof(int));
         w.src = off; off += align_up(nr * sizeof(int));

@@ -102,6 +102,7 @@ __device__ void sort_cell_row(const LifConst &C, const ConvGeom &g, const float 
     const int nw = blockDim.x >> 6;
     const int b = cr / g.Hp, py = cr % g.Hp;
     const int nb = R * g.Wp;  // buckets, flat f = r * Wp + px
+    const int noff = conv_off_stride(R, g);
     const bool fwd = cs.L != nullptr, bwd = cs.dL != nullptr;
     int *hist = sh;
     int *part = sh + nb;
@@ -127,8 +128,8 @@ __device__ void sort_cell_row(const LifConst &C, const ConvGeom &g, const float 
         }
         if (!__syncthreads_or(any)) {
             if (ev.row && threadIdx.x == 0) ev.live[cr] = 0;
-            int *off0 = cs.off + static_cast<int64_t>(cr) * (nb + 1);
-            for (int f = threadIdx.x; f <= nb; f += blockDim.x) off0[f] = 0;
+            int *off0 = cs.off + static_cast<int64_t>(cr) * noff;
+            for (int f = threadIdx.x; f < noff; f += blockDim.x) off0[f] = 0;
             return;
         }
     } else {
@@ -162,8 +163,8 @@ __device__ void sort_cell_row(const LifConst &C, const ConvGeom &g, const float 
     if (ev.row && threadIdx.x == 0) ev.live[cr] = has;
     if (!has) {
         // no input of this cell row has events: empty buckets
-        int *off0 = cs.off + static_cast<int64_t>(cr) * (nb + 1);
-        for (int f = threadIdx.x; f <= nb; f += blockDim.x) off0[f] = 0;
+        int *off0 = cs.off + static_cast<int64_t>(cr) * noff;
+        for (int f = threadIdx.x; f < noff; f += blockDim.x) off0[f] = 0;
         return;
     }
     // exclusive prefix over the buckets in (r, px) order: per-thread chunk
@@ -189,16 +190,27 @@ __device__ void sort_cell_row(const LifConst &C, const ConvGeom &g, const float 
         part[4 * lane + 1] = ex + v0;
         part[4 * lane + 2] = ex + v0 + v1;
         part[4 * lane + 3] = ex + v0 + v1 + v2;
-        if (lane == kWave - 1) cs.off[static_cast<int64_t>(cr) * (nb + 1) + nb] = inc;
+        if (lane == kWave - 1) {
+            // the last row's end and the record count
+            int *off = cs.off + static_cast<int64_t>(cr) * noff;
+            off[g.Wp * R + R - 1] = inc;
+            off[noff - 1] = inc;
+        }
     }
     __syncthreads();
     int run = part[threadIdx.x];
-    int *off = cs.off + static_cast<int64_t>(cr) * (nb + 1);
+    int *off = cs.off + static_cast<int64_t>(cr) * noff;
+    int r = lo / g.Wp, px = lo - r * g.Wp;  // bucket f = r * Wp + px, advanced with f
     for (int f = lo; f < hi; ++f) {
         const int v = hist[f];
-        off[f] = run;
+        off[px * R + r] = run;
+        if (px == 0 && r > 0) off[g.Wp * R + r - 1] = run;  // the end of row r - 1
         hist[f] = run;
         run += v;
+        if (++px == g.Wp) {
+            px = 0;
+            ++r;
+        }
     }
     __syncthreads();
     // placement: lanes of one bucket are ranked by lane (j' ascending). The
@@ -339,7 +351,7 @@ struct PosWalk {
         x0 = ox * g.stride - g.pad;
         xa = max(0, x0);
         xb = max(xa, min(g.Wp, x0 + g.KW));
-        nb1 = rows_of(C) * g.Wp + 1;
+        nb1 = conv_off_stride(rows_of(C), g);
         wlim = g.KH * g.KW * g.C_in - 1;
 #pragma unroll
         for (int ky = 0; ky < KHT; ++ky) {
@@ -365,13 +377,14 @@ struct PosWalk {
                                               int r0, int lane) {
         const int r = min(r0 + lane, R - 1);
         // bucket starts are clamped to the cell row's slots (a backward that
-        // reuses a kept forward sort trusts workspace contents)
+        // reuses a kept forward sort trusts workspace contents); lanes read
+        // one column of the table each, contiguously
         const int per = g.Wp * g.PC;
 #pragma unroll
         for (int ky = 0; ky < KHT; ++ky) {
-            const int *o = cs.off + offb[ky] + static_cast<int64_t>(r) * g.Wp;
-            oa[ky] = vky[ky] ? min(max(o[xa], 0), per) : 0;
-            ob[ky] = vky[ky] ? min(max(o[xb], oa[ky]), per) : 0;
+            const int *o = cs.off + offb[ky] + r;
+            oa[ky] = vky[ky] ? min(max(o[xa * R], 0), per) : 0;
+            ob[ky] = vky[ky] ? min(max(o[xb * R], oa[ky]), per) : 0;
         }
     }
 
@@ -449,7 +462,7 @@ __global__ __launch_bounds__(kFwdWaves * kWave) __attribute__((amdgpu_waves_per_
         if (b0 == ql / HoWo) {
             const int y_lo = max(0, (q0 - b0 * HoWo) / g.Wo * g.stride - g.pad);
             const int y_hi = min(g.Hp - 1, (ql - b0 * HoWo) / g.Wo * g.stride - g.pad + g.KH - 1);
-            const int nb1 = rows_of(C) * g.Wp + 1;
+            const int nb1 = conv_off_stride(rows_of(C), g);
             int recs = 0;
             for (int y = y_lo; y <= y_hi; ++y)
                 recs |= *as_const(cs.off + (static_cast<int64_t>(b0) * g.Hp + y) * nb1 + nb1 - 1);
@@ -784,7 +797,7 @@ __global__ __launch_bounds__(256) void conv_fwd_list_kernel(LifConst C, ConvGeom
         if (b0 == ql / HoWo) {
             const int y_lo = max(0, (q0 - b0 * HoWo) / g.Wo * g.stride - g.pad);
             const int y_hi = min(g.Hp - 1, (ql - b0 * HoWo) / g.Wo * g.stride - g.pad + g.KH - 1);
-            const int nb1 = rows_of(C) * g.Wp + 1;
+            const int nb1 = conv_off_stride(rows_of(C), g);
             int recs = 0;
             for (int y = y_lo; y <= y_hi; ++y)
                 recs |= *as_const(cs.off + (static_cast<int64_t>(b0) * g.Hp + y) * nb1 + nb1 - 1);
@@ -823,7 +836,7 @@ __global__ __launch_bounds__(256) void conv_fwd_list_kernel(LifConst C, ConvGeom
     const int oy = pos / g.Wo, ox = pos % g.Wo;
     const int x0 = ox * g.stride - g.pad;
     const int xa = max(0, x0), xb = max(xa, min(g.Wp, x0 + g.KW));
-    const int nb1 = R * g.Wp + 1;
+    const int nb1 = conv_off_stride(R, g);
     const int wlim = g.KH * g.KW * g.C_in - 1;
     int64_t recb[KHT], offb[KHT];
     int wofs[KHT];
@@ -893,8 +906,8 @@ __global__ __launch_bounds__(256) void conv_fwd_list_kernel(LifConst C, ConvGeom
         const int rr = min(li, R - 2);
 #pragma unroll
         for (int ky = 0; ky < KHT; ++ky) {
-            const int *o = cs.off + offb[ky] + static_cast<int64_t>(rr) * g.Wp;
-            const int a = vky[ky] ? o[xa] : 0, e = vky[ky] ? o[xb] : 0;
+            const int *o = cs.off + offb[ky] + rr;
+            const int a = vky[ky] ? o[xa * R] : 0, e = vky[ky] ? o[xb * R] : 0;
             oa[ky] = a;
             n0[ky] = rvalid ? e - a : 0;
             nr += n0[ky];
@@ -1253,7 +1266,7 @@ __device__ void dt_gather_block(const ConvGeom &g, int R, const ConvSorted &cs,
                                 int s0, float *buf) {
     const int per = g.Wp * g.PC;
     const int ns = min(kGatherSlots, per - s0);
-    const int nb1 = R * g.Wp + 1;
+    const int nb1 = conv_off_stride(R, g);
     const int nrec = uniform(min(max(cs.off[static_cast<int64_t>(cr) * nb1 + nb1 - 1], 0), per));
     const int b = cr / g.Hp, py = cr % g.Hp;
     const int64_t pos0 = static_cast<int64_t>(b) * g.Ho * g.Wo;

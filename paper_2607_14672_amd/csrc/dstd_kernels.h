@@ -69,9 +69,17 @@ struct ConvGeom {
 
 constexpr int kConvMaxK = 7;  // largest kernel height/width
 
+// ints per cell row of the bucket-start table (R = M + 3 event rows)
+__host__ __device__ __forceinline__ int conv_off_stride(int R, const ConvGeom &g) {
+    return (g.Wp + 1) * R + 1;
+}
+
 // Per cell row (b, py): records bucketed by (event row r, cell column px),
-// key = px * C_in + ci; off[(b*Hp + py) * (R*Wp + 1) + r*Wp + px] = bucket
-// start within the cell row's Wp * PC record slots.
+// in (r, px) order, key = px * C_in + ci. The bucket starts within the cell
+// row's Wp * PC record slots are held column-major, off[cr * noff + px * R +
+// r] (cr = b*Hp + py, noff = conv_off_stride), so that lanes = event rows
+// read one column contiguously; column px = Wp holds the end of each row r
+// (the start of (r + 1, 0)), and the last entry the row's record count.
 // The forward sort writes the event weights L, R; the backward sort (or a
 // forward that keeps its sort for the backward) writes the record's event
 // row and cell column (px = row << 16 | cell column), its input index in the

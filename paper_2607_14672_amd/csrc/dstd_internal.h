@@ -371,10 +371,11 @@ __device__ __forceinline__ void g_strided(const LifConst &C, const GStep &gs, fl
 // e^{-kappa len} (general row). On a crossing returns true with the fp32
 // segment, the bracket end hi (0: fires at u = 0, only through rounding) and
 // v - theta there.
-// The interval filter: v(u) <= max(V,0) + max(I,0) kmax, tested on the fp64
-// state against theta with a 1e-4 margin (only intervals that pass are
-// analysed; kmax is +inf on an open interval of the (inf, inf) row, where
-// I = 0 must not give inf * 0).
+// The bound filter of a segment of any length (the last interval, the
+// free-decay tail, the exact and multi-spike walks): v(u) <= max(V,0) +
+// max(I,0) kmax, tested on the fp64 state against theta with a 1e-4 margin
+// (only segments that pass are analysed; kmax is +inf on an open interval
+// of the (inf, inf) row, where I = 0 must not give inf * 0).
 __device__ __forceinline__ bool seg_may_cross(const LifConst &C, double Vd, double Id,
                                               double kmax) {
     const double vpos = fmax(Vd, 0.0);

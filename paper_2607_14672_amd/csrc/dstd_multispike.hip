@@ -286,7 +286,7 @@ struct RowOutMs {
 
     template <int KS>
     __device__ __forceinline__ void scan(const LifConst &C, int N_out, int b, int i, bool row_ok,
-                                         const float *tp, int kPt) const {
+                                         const float *tp, int kPt, int /* m_end: resets need every point */) const {
         MsScan<KS> sc;
         sc.F = F;
         sc.ok = row_ok;

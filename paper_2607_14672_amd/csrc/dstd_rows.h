@@ -230,7 +230,10 @@ __global__ __launch_bounds__(kRowWaves * 64) void fwd_rows_kernel(LifConst C, in
             prev = w;
         }
     }
-    out.template scan<KS>(C, N_out, b, i, row_ok, tp, kPt);
+    // the last grid point that receives input: the last record's row r
+    // feeds points r - 1 and r (at most M)
+    const int m_end = (n > 0) ? min(uniform(*as_const(er + n - 1)), C.M) : -1;
+    out.template scan<KS>(C, N_out, b, i, row_ok, tp, kPt, m_end);
 }
 
 // Grid point sums needed by one block of NT tiles: P[R][NT][64] plus the
@@ -257,19 +260,26 @@ struct RowOutTtfs {
 
     __device__ __forceinline__ int wrow(int j) const { return j; }
 
+    // m_end: the last grid point with input (-1: none). Points after it
+    // add nothing: from there the rest of the window is one free-decay
+    // segment (Scan::tail).
     template <int KS>
     __device__ __forceinline__ void scan(const LifConst &C, int N_out, int b, int i, bool row_ok,
-                                         const float *tp, int kPt) const {
+                                         const float *tp, int kPt, int m_end) const {
         Scan<KS> sc;
         float wn = tp[0];  // next grid point's sum, read ahead
         bool done = false;
-        for (int m = 0; m < C.M && !done; ++m) {
+        const int m_stop = min(C.M, m_end + 1);
+        for (int m = 0; m < m_stop && !done; ++m) {
             const float wc = wn;
             wn = tp[(m + 1) * kPt];
             sc.template step_k<false>(C, m, wc);
             done = __all(sc.found() || !row_ok);
         }
-        if (!done) sc.template step_k<true>(C, C.M, wn);  // the last interval
+        if (!done) {
+            if (m_stop < C.M) sc.tail(C, m_stop);
+            else sc.template step_k<true>(C, C.M, wn);  // the last interval
+        }
         if (!row_ok) return;
         float to, sl;
         int q;

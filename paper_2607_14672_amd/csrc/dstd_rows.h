@@ -68,7 +68,15 @@ __global__ __launch_bounds__(kRowWaves * 64) void fwd_rows_kernel(LifConst C, in
     constexpr int kPt = NT * kWave;  // floats per point (all tiles)
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = uniform(threadIdx.x >> 6);
-    const int b = blockIdx.y;
+    // XCD-aware order: the hardware block maps to a logical (tile block bx,
+    // sample b) with the samples fastest, so each XCD takes one contiguous
+    // range and works through one weight tile, all samples, at a time: its
+    // W^T columns stay in that XCD's L2 instead of several tiles competing
+    const int nby = static_cast<int>(gridDim.y);
+    const int lin = xcd_block(static_cast<int>(blockIdx.x + blockIdx.y * gridDim.x),
+                              static_cast<int>(gridDim.x) * nby);
+    const int bx = lin / nby;
+    const int b = lin - bx * nby;
     const int R = rows_of(C);
     float *P = rsum;
     float *BL = rsum + R * kPt;
@@ -132,13 +140,13 @@ __global__ __launch_bounds__(kRowWaves * 64) void fwd_rows_kernel(LifConst C, in
     int voff[NT];
 #pragma unroll
     for (int t = 0; t < NT; ++t) {
-        const int i = (blockIdx.x * NT + t) * kWave + lane;
+        const int i = (bx * NT + t) * kWave + lane;
         voff[t] = min(i, N_out - 1) * static_cast<int>(sizeof(WT));
     }
     // VEC: one load of NT neurons; past N_out it reads the next row's first
     // weights or, after the last row, zeros (buffer range check): those sums
     // belong to lanes without a neuron and are never scanned into outputs
-    const int voffv = (blockIdx.x * NT * kWave + NT * lane) * static_cast<int>(sizeof(WT));
+    const int voffv = (bx * NT * kWave + NT * lane) * static_cast<int>(sizeof(WT));
     const int rstride = N_out * static_cast<int>(sizeof(WT));
     const int jmax = max(N_in - 1, 0);
     // Record fields come through the scalar cache, kRowSub records per load
@@ -211,7 +219,7 @@ __global__ __launch_bounds__(kRowWaves * 64) void fwd_rows_kernel(LifConst C, in
     // wave t scans tile t
     if (wave >= NT) return;
     const int tile = wave;
-    const int i = (blockIdx.x * NT + tile) * kWave + lane;
+    const int i = (bx * NT + tile) * kWave + lane;
     const bool row_ok = i < N_out;
     if (uniform(static_cast<int>(__any(row_ok))) == 0) return;
     // range boundaries: point lo(w) - 1 of each nonempty range w >= 1 (wave

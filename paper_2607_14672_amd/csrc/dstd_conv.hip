@@ -1093,34 +1093,57 @@ __device__ void grad_block(const LifConst &C, const ConvGeom &g, int64_t n_pos, 
     }
     if (tiles) {
         if (pos_ok) {
-            for (int co = static_cast<int>(threadIdx.x) / kGradPos; co < g.C_out; co += cstep) {
-                const int64_t o = obase + static_cast<int64_t>(co) * HoWo;
-                const int q = q_idx[o];
-                if (q >= 0) {
-                    float gt = grad_t[o];
-                    if (sf.on) gt += synfire_dt(sf, t_out[o]);
-                    if (gt != 0.f) atomicMax(&sl[pl], q);
+            // four channels per pass, their loads issued together
+            for (int c4 = static_cast<int>(threadIdx.x) / kGradPos; c4 < g.C_out; c4 += 4 * cstep) {
+                int q[4];
+#pragma unroll
+                for (int u = 0; u < 4; ++u) {
+                    const int co = c4 + u * cstep;
+                    q[u] = (co < g.C_out) ? q_idx[obase + static_cast<int64_t>(co) * HoWo] : -1;
+                }
+#pragma unroll
+                for (int u = 0; u < 4; ++u) {
+                    if (q[u] >= 0) {
+                        const int64_t o = obase + static_cast<int64_t>(c4 + u * cstep) * HoWo;
+                        float gt = grad_t[o];
+                        if (sf.on) gt += synfire_dt(sf, t_out[o]);
+                        if (gt != 0.f) atomicMax(&sl[pl], q[u]);
+                    }
                 }
             }
         }
         __syncthreads();
     }
     {
+        // a thread's kCh channels of its position (256 threads: 16 positions
+        // x 4 channel rows): each load stage is issued for all of them before
+        // the next, so the dependent loads (q, then the upstream gradient,
+        // then the spike time and slope) overlap across channels
+        constexpr int kCh = kGradCh * kGradPos / 256;
         const int c0 = tile * kGradCh;
-        for (int cl = static_cast<int>(threadIdx.x) / kGradPos; cl < kGradCh; cl += cstep) {
-            const int co = c0 + cl;
+        const int cl0 = static_cast<int>(threadIdx.x) / kGradPos;
+        int64_t o[kCh];
+        int q[kCh];
+        float gt[kCh];
+#pragma unroll
+        for (int u = 0; u < kCh; ++u) {
+            const int co = c0 + cl0 + u * cstep;
+            o[u] = obase + static_cast<int64_t>(co) * HoWo;
+            q[u] = (co < g.C_out && pos_ok) ? q_idx[o[u]] : -1;
+        }
+#pragma unroll
+        for (int u = 0; u < kCh; ++u) gt[u] = (q[u] >= 0) ? grad_t[o[u]] : 0.f;  // silent: no load
+#pragma unroll
+        for (int u = 0; u < kCh; ++u) {
             GradPrep gp{0.f, 0.f, -1};
-            if (co < g.C_out && pos_ok) {
-                const int64_t o = obase + static_cast<int64_t>(co) * HoWo;
-                const int q = q_idx[o];
-                if (q >= 0) {  // silent neurons: no further loads
-                    float gt = grad_t[o];
-                    // the spike time only where it is used (no gradient: no load)
-                    const float t = (sf.on || gt != 0.f) ? t_out[o] : 0.f;
-                    if (sf.on) gt += synfire_dt(sf, t);
-                    if (gt != 0.f) gp = grad_prep(C, t, slope[o], q, gt);
-                }
+            if (q[u] >= 0) {
+                // the spike time only where it is used (no gradient: no load)
+                const float t = (sf.on || gt[u] != 0.f) ? t_out[o[u]] : 0.f;
+                float gu = gt[u];
+                if (sf.on) gu += synfire_dt(sf, t);
+                if (gu != 0.f) gp = grad_prep(C, t, slope[o[u]], q[u], gu);
             }
+            const int cl = cl0 + u * cstep;
             sg[cl * kS + pl] = gp.gam;
             su[cl * kS + pl] = gp.uq;
             sq[cl * kS + pl] = gp.q;

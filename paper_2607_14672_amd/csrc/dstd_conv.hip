@@ -119,12 +119,23 @@ __device__ void sort_cell_row(const LifConst &C, const ConvGeom &g, const float 
         const float w_lo = C.t0 - 1.001f * C.dt;
         const float w_hi = fmaf(static_cast<float>(C.M) + 1.001f, C.dt, C.t0);
         bool any = false;
-        for (int t = threadIdx.x; t < per; t += blockDim.x) {
-            int slot;
-            const int64_t src = cell_row_input(g, b, py, t, slot);
-            const float v = t_in[src];
-            tl[slot] = v;
-            any = any || (v >= w_lo && v < w_hi);
+        // four inputs per pass, their loads issued together
+        for (int t4 = threadIdx.x; t4 < per; t4 += 4 * blockDim.x) {
+            int slot[4];
+            float v[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const int t = t4 + u * static_cast<int>(blockDim.x);
+                const int64_t src = cell_row_input(g, b, py, min(t, per - 1), slot[u]);
+                v[u] = (t < per) ? t_in[src] : 0.f;
+            }
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                if (t4 + u * static_cast<int>(blockDim.x) < per) {
+                    tl[slot[u]] = v[u];
+                    any = any || (v[u] >= w_lo && v[u] < w_hi);
+                }
+            }
         }
         if (!__syncthreads_or(any)) {
             if (ev.row && threadIdx.x == 0) ev.live[cr] = 0;

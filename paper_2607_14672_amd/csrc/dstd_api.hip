@@ -286,6 +286,8 @@ dstd_status check_conv(const dstd_conv_shape *cs, int64_t B, int M, dstd::ConvGe
                     "table (16128 buckets)", (long long)(M + 3) * G.Wp);
     G.PC = (int)pc;
     G.inv_P = (float)(1.0 / G.P);
+    G.dv_pch = dstd::fast_div((uint32_t)(G.Wp * G.P));
+    G.dv_w = dstd::fast_div((uint32_t)G.W);
     return DSTD_OK;
 }
 

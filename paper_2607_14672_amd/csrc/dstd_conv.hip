@@ -57,18 +57,18 @@ __device__ __forceinline__ int64_t nchw_index(const ConvGeom &g, int b, int ci, 
 __device__ __forceinline__ int64_t cell_row_input(const ConvGeom &g, int b, int py, int t,
                                                   int &slot) {
     const int per_ch = g.Wp * g.P;
-    const int ci = t / per_ch, rem = t % per_ch;
+    const int ci = fdiv(t, g.dv_pch), rem = t - ci * per_ch;  // t < 2^30
     int y, x, px, d;
     if (g.pool == 2) {
-        const int dy = rem / g.W;
-        x = rem % g.W;
+        const int dy = fdiv(rem, g.dv_w);
+        x = rem - dy * g.W;
         y = 2 * py + dy;
         px = x >> 1;
         d = dy * 2 + (x & 1);
     } else if (g.pool == 0) {
         d = rem;
-        y = d / g.W;
-        x = d % g.W;
+        y = fdiv(d, g.dv_w);
+        x = d - y * g.W;
         px = 0;
     } else {
         x = rem;

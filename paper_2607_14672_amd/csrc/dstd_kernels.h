@@ -61,11 +61,31 @@ hipError_t launch_mse(int64_t B, int64_t N, const float *t, const float *y, floa
 // ------------------------------------------------------------------ conv --
 // Geometry of a conv layer, derived on the host. The (pooled) input map has
 // Hp x Wp cells of P raw pixels; PC = P * C_in raw inputs per cell.
+// n / d for 0 <= n < 2^31 by a multiply and a shift (round-up magic number
+// of Granlund and Montgomery): s = ceil(log2 d), m = floor(2^32 (2^s - d) / d)
+// + 1, n / d = (mulhi(n, m) + n) >> s; set on the host by fast_div().
+struct FastDiv {
+    uint32_t m;
+    int s;
+};
+
 struct ConvGeom {
     int C_in, H, W, C_out, KH, KW, stride, pad, pool;
     int Hp, Wp, Ho, Wo, P, PC;
     float inv_P;
+    FastDiv dv_pch, dv_w;  // by Wp * P (raw inputs per channel of a cell row) and by W
 };
+
+inline FastDiv fast_div(uint32_t d) {
+    int s = 0;
+    while ((uint64_t(1) << s) < d) ++s;
+    return FastDiv{static_cast<uint32_t>(((uint64_t(1) << 32) * ((uint64_t(1) << s) - d)) / d + 1), s};
+}
+
+__device__ __forceinline__ int fdiv(int n, FastDiv f) {
+    const uint32_t u = static_cast<uint32_t>(n);
+    return static_cast<int>((__umulhi(u, f.m) + u) >> f.s);
+}
 
 constexpr int kConvMaxK = 7;  // largest kernel height/width
 

@@ -288,6 +288,7 @@ dstd_status check_conv(const dstd_conv_shape *cs, int64_t B, int M, dstd::ConvGe
     G.inv_P = (float)(1.0 / G.P);
     G.dv_pch = dstd::fast_div((uint32_t)(G.Wp * G.P));
     G.dv_w = dstd::fast_div((uint32_t)G.W);
+    G.dv_cin = dstd::fast_div((uint32_t)G.C_in);
     return DSTD_OK;
 }
 

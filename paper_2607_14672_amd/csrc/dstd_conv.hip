@@ -149,8 +149,9 @@ __device__ void sort_cell_row(const LifConst &C, const ConvGeom &g, const float 
     auto t_at = [&](int px, int j) {
         if (tl) return tl[px * g.PC + j];
         int y, x;
-        raw_pixel(g, py, px, j / g.C_in, y, x);
-        return t_in[nchw_index(g, b, j % g.C_in, y, x)];
+        const int d = fdiv(j, g.dv_cin);
+        raw_pixel(g, py, px, d, y, x);
+        return t_in[nchw_index(g, b, j - d * g.C_in, y, x)];
     };
     const int cpi = (g.PC < kWave) ? kWave / g.PC : 1;  // cells per pass
     const int lsub = (g.PC < kWave) ? lane / g.PC : 0;
@@ -265,7 +266,7 @@ __device__ void sort_cell_row(const LifConst &C, const ConvGeom &g, const float 
             __builtin_amdgcn_wave_barrier();
             if (f >= 0) {
                 const int64_t o = rb + pos;
-                cs.key[o] = px * g.C_in + (j % g.C_in);
+                cs.key[o] = px * g.C_in + (j - fdiv(j, g.dv_cin) * g.C_in);
                 if (fwd) {
                     cs.L[o] = e.L;
                     cs.R[o] = e.R;

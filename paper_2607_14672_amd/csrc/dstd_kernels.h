@@ -73,7 +73,7 @@ struct ConvGeom {
     int C_in, H, W, C_out, KH, KW, stride, pad, pool;
     int Hp, Wp, Ho, Wo, P, PC;
     float inv_P;
-    FastDiv dv_pch, dv_w;  // by Wp * P (raw inputs per channel of a cell row) and by W
+    FastDiv dv_pch, dv_w, dv_cin;  // by Wp * P (raw inputs per channel of a cell row), W, C_in
 };
 
 inline FastDiv fast_div(uint32_t d) {

@@ -430,10 +430,10 @@ struct PosWalk {
 // (binary search over the prefix with lane shuffles), its segment and its
 // record, and loads the record's fields with one vector load each; the
 // decoded entries (weight-row offset, row, L, R) go to a small LDS area of
-// the wave. The entries are then summed one by one, each read back as one
-// 16-byte LDS broadcast (weight rows loaded 8 at a time), and rows close
-// into the interval scan as the row changes. Sums and their order are those
-// of a row-by-row walk.
+// the wave. The entries are then summed in batches of up to 8 entries of one
+// event row (each entry read back as one 16-byte LDS broadcast, the batch's
+// weight rows loaded together), and rows close into the interval scan as the
+// row changes. Sums and their order are those of a row-by-row walk.
 struct FwdEntry { int wb, row; float L, R; };
 // kDirect (receptive fields of at most 64 raw inputs, at most 64 event rows,
 // pooled or plain input): no cell-row sort; lane v takes raw input
@@ -460,7 +460,8 @@ __global__ __launch_bounds__(kFwdWaves * kWave) __attribute__((amdgpu_waves_per_
                                                        float *__restrict__ t_out,
                                                        float *__restrict__ slope,
                                                        int *__restrict__ q_idx) {
-    __shared__ FwdEntry ent[kFwdWaves][kWave];
+    // a wave's list, padded so that a batch starting at any entry stays inside
+    __shared__ FwdEntry ent[kFwdWaves][kWave + kCBatch];
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = uniform(threadIdx.x >> 6);
     const int64_t p0 = static_cast<int64_t>(xcd_block(blockIdx.x, gridDim.x)) * kFwdWaves;
@@ -498,6 +499,7 @@ __global__ __launch_bounds__(kFwdWaves * kWave) __attribute__((amdgpu_waves_per_
     }
     if (p >= n_pos) return;  // wave-uniform; no block barrier below
     FwdEntry *my = ent[wave];
+    if (lane < kCBatch) my[kWave + lane] = FwdEntry{0, 0, 0.f, 0.f};
     const int co = blockIdx.y * kWave + lane;
     const bool row_ok = co < g.C_out;
     const int R = rows_of(C);
@@ -532,9 +534,10 @@ __global__ __launch_bounds__(kFwdWaves * kWave) __attribute__((amdgpu_waves_per_
             ++cur;
         }
     };
-    // the sums of a batch of nk <= kCBatch list entries in order; true once
-    // every lane has found its interval. A full batch inside one event row
-    // (rows never decrease along the list) is summed without per-entry tests.
+    // (direct path) the sums of a batch of nk <= kCBatch list entries in
+    // order; true once every lane has found its interval. A full batch inside
+    // one event row (rows never decrease along the list) is summed without
+    // per-entry tests.
     auto sum_batch = [&](const FwdEntry (&e)[kCBatch], const float (&w)[kCBatch], int nk) {
         const int ra = uniform(e[0].row);
         if (nk == kCBatch && ra == uniform(e[kCBatch - 1].row)) {
@@ -696,20 +699,49 @@ __global__ __launch_bounds__(kFwdWaves * kWave) __attribute__((amdgpu_waves_per_
             const float Lv = ok ? cs.L[gi] : 0.f;
             const float Rv = ok ? cs.R[gi] : 0.f;
             const int wb = min(max(key + wof, 0), wk.wlim) * rstride;
-            my[lane] = FwdEntry{wb, r0 + lo, Lv, Rv};
+            // the entry's row, and how many entries of that row the list holds
+            // from this one on (itself included): row | nrem << 16 (rows < 2^16)
+            const int nrem = min(__shfl(inc, lo) - v, kWave);
+            my[lane] = FwdEntry{wb, (r0 + lo) | (nrem << 16), Lv, Rv};
             __builtin_amdgcn_wave_barrier();
             const int nc = min(kWave, total - c0);
-            for (int s0 = 0; s0 < nc; s0 += kCBatch) {
+            // batches never cross a row: up to kCBatch entries of the head
+            // entry's row, summed without per-entry row tests; a batch's
+            // entries past its row are read (and their weights loaded) but
+            // not summed
+            for (int s0 = 0; s0 < nc;) {
                 FwdEntry e[kCBatch];
                 float w[kCBatch];
 #pragma unroll
                 for (int q = 0; q < kCBatch; ++q) e[q] = my[s0 + q];  // LDS broadcasts
 #pragma unroll
                 for (int q = 0; q < kCBatch; ++q) w[q] = BufLoad<float>::get(wr, voff + e[q].wb, 0);
-                if (sum_batch(e, w, min(kCBatch, nc - s0))) {
-                    done = true;
-                    break;
+                const int hd = uniform(e[0].row);
+                const int ra = hd & 0xffff;
+                const int nk = max(1, min(min(kCBatch, hd >> 16), nc - s0));  // always advances
+                if (ra != cur) {
+                    close_to_mid(ra);
+                    if (__all(sc.found() || !row_ok)) {
+                        done = true;
+                        break;
+                    }
                 }
+                if (nk == kCBatch) {
+#pragma unroll
+                    for (int q = 0; q < kCBatch; ++q) {
+                        aL = fmaf(w[q], e[q].L, aL);
+                        aR = fmaf(w[q], e[q].R, aR);
+                    }
+                } else {
+#pragma unroll
+                    for (int q = 0; q < kCBatch - 1; ++q) {
+                        if (q < nk) {
+                            aL = fmaf(w[q], e[q].L, aL);
+                            aR = fmaf(w[q], e[q].R, aR);
+                        }
+                    }
+                }
+                s0 += nk;
             }
             __builtin_amdgcn_wave_barrier();
         }

@@ -785,8 +785,9 @@ constexpr int kListMaxRec = 640;
 
 // K consecutive records of a row from the LDS list at idx, of which the lane's
 // position has `left` (entries past them add zero weight): weights loaded as
-// one batch, then summed in order.
-template <int K>
+// one batch, then summed in order. kFull: every position of the wave has all
+// K (no masking).
+template <int K, bool kFull = false>
 __device__ __forceinline__ void list_batch(const int *ewb, const float2 *eLR, int idx,
                                            int left, __amdgpu_buffer_rsrc_t wr, int voff,
                                            float &aL, float &aR) {
@@ -794,7 +795,7 @@ __device__ __forceinline__ void list_batch(const int *ewb, const float2 *eLR, in
     float Lq[K], Rq[K], w[K];
 #pragma unroll
     for (int q = 0; q < K; ++q) {
-        const bool ok = q < left;
+        const bool ok = kFull || q < left;
         wb[q] = ok ? ewb[idx + q] : 0;
         const float2 lr = ok ? eLR[idx + q] : make_float2(0.f, 0.f);
         Lq[q] = lr.x;
@@ -1049,20 +1050,24 @@ __global__ __launch_bounds__(256) void conv_fwd_list_kernel(LifConst C, ConvGeom
     float aL = 0.f, aR = 0.f, carry = 0.f;
     for (int r = r_first; r <= R - 2; ++r) {
         if (r <= r_last) {
-            int n = 0, my_n = 0, my_s = ebase;
+            int n = 0, nmin = 0x7fffffff, my_n = 0, my_s = ebase;
 #pragma unroll
             for (int h = 0; h < NP; ++h) {
                 const int nh = uniform(__builtin_amdgcn_readlane(nr, h * LP + r));
                 const int sh = uniform(__builtin_amdgcn_readlane(start, h * LP + r));
                 n = max(n, nh);
+                nmin = min(nmin, nh);
                 if (h == half) {
                     my_n = nh;
                     my_s += sh;
                 }
             }
-            // batches of 8, then 4, then single records: no load or sum
-            // past the row's largest count
+            // batches of 8 (unmasked while every position has them), then
+            // 4, then single records: no load or sum past the row's largest
+            // count
             int i0 = 0;
+            for (; i0 + 8 <= nmin; i0 += 8)
+                list_batch<8, true>(ewb, eLR, my_s + i0, my_n - i0, wr, voff, aL, aR);
             for (; i0 + 8 <= n; i0 += 8)
                 list_batch<8>(ewb, eLR, my_s + i0, my_n - i0, wr, voff, aL, aR);
             if (i0 + 4 <= n) {
@@ -1524,7 +1529,7 @@ __global__ __launch_bounds__(256) void conv_dw_kernel(LifConst C, ConvGeom g, in
 // dW[co, ci, ky, kx] = (1/P) sum_z part[z][co][k * C_in + ci]. Threads follow
 // the partial-sum layout (coalesced reads); a block takes groups of 256 / G
 // consecutive entries x G split groups (G from red_groups: more groups where
-// there are many splits; at most 2048 blocks, each taking every nblk-th entry
+// there are many splits; at most 512 blocks, each taking every nblk-th entry
 // group): group h sums z = h, h + G, ...; the G group sums are added in
 // group order (fixed order: deterministic) and written to the [co][ci][ky][kx]
 // slot. Splits without gradient-carrying samples wrote no partials and are
@@ -1897,10 +1902,10 @@ hipError_t launch_conv_backward(const LifConst &C, const ConvGeom &g, int64_t B,
     {
         // dW split reduction and dt_in gather: one launch
         const int64_t n = static_cast<int64_t>(g.C_out) * nj;
-        // reduction blocks: one per red_out outputs, at most 2048 (each then
-        // takes every 2048th group)
+        // reduction blocks: one per red_out outputs, at most 512 (each then
+        // takes every 512th group; two blocks per CU)
         const int red_out = 256 / red_groups(p.nsplit);
-        const int n_red = grad_W ? static_cast<int>(std::min<int64_t>((n + red_out - 1) / red_out, 2048)) : 0;
+        const int n_red = grad_W ? static_cast<int>(std::min<int64_t>((n + red_out - 1) / red_out, 512)) : 0;
         const int per = g.Wp * g.PC;
         const int nsl = (per + kGatherSlots - 1) / kGatherSlots;
         const int n_ga = dt ? static_cast<int>(B * g.Hp) * nsl : 0;

@@ -783,20 +783,28 @@ __global__ __launch_bounds__(kFwdWaves * kWave) __attribute__((amdgpu_waves_per_
 // are those of the chunked walk.
 constexpr int kListMaxRec = 640;
 
+// LDS ints of one wave's list of ne records: the weight rows as 16-bit
+// indices (a list layer's receptive field has at most kListMaxRec / 2 raw
+// inputs, so its weight rows fit), then the (L, R) pairs, 8-byte aligned
+__host__ __device__ __forceinline__ int list_wave_ints(int ne) {
+    const int ne4 = (ne + 3) & ~3;
+    return ne4 / 2 + 2 * ne4;
+}
+
 // K consecutive records of a row from the LDS list at idx, of which the lane's
 // position has `left` (entries past them add zero weight): weights loaded as
 // one batch, then summed in order. kFull: every position of the wave has all
 // K (no masking).
 template <int K, bool kFull = false>
-__device__ __forceinline__ void list_batch(const int *ewb, const float2 *eLR, int idx,
+__device__ __forceinline__ void list_batch(const uint16_t *erow, const float2 *eLR, int idx,
                                            int left, __amdgpu_buffer_rsrc_t wr, int voff,
-                                           float &aL, float &aR) {
+                                           int rstride, float &aL, float &aR) {
     int wb[K];
     float Lq[K], Rq[K], w[K];
 #pragma unroll
     for (int q = 0; q < K; ++q) {
         const bool ok = kFull || q < left;
-        wb[q] = ok ? ewb[idx + q] : 0;
+        wb[q] = ok ? static_cast<int>(__umul24(erow[idx + q], rstride)) : 0;  // both < 2^24
         const float2 lr = ok ? eLR[idx + q] : make_float2(0.f, 0.f);
         Lq[q] = lr.x;
         Rq[q] = lr.y;
@@ -823,7 +831,7 @@ __global__ __launch_bounds__(256) void conv_fwd_list_kernel(LifConst C, ConvGeom
                                                             float *__restrict__ slope,
                                                             int *__restrict__ q_idx) {
     constexpr int LP = kWave / NP;
-    extern __shared__ int list_lds[];  // per wave: wb[NP][E], then (L, R)[NP][E]
+    extern __shared__ int list_lds[];  // per wave: weight rows [NP][E] (16-bit), then (L, R)[NP][E]
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = uniform(threadIdx.x >> 6);
     const int half = lane / LP, li = lane % LP, hb = half * LP;  // hb: the position's first lane
@@ -869,9 +877,10 @@ __global__ __launch_bounds__(256) void conv_fwd_list_kernel(LifConst C, ConvGeom
     const bool pos_ok = p < n_pos;
     const int E = g.KH * g.KW * g.PC;
     const int ebase = half * E;  // the position's part of the wave's list
-    const int EW = (NP * E + 1) & ~1;  // ints per list (even: the (L, R) pairs stay 8-byte aligned)
-    int *ewb = list_lds + wave * 3 * EW;
-    float2 *eLR = reinterpret_cast<float2 *>(ewb + EW);  // (L, R) of a record: one 8-byte read
+    const int WI = list_wave_ints(NP * E);
+    uint16_t *erow = reinterpret_cast<uint16_t *>(list_lds + wave * WI);
+    // (L, R) of a record: one 8-byte read
+    float2 *eLR = reinterpret_cast<float2 *>(list_lds + wave * WI + ((NP * E + 3) & ~3) / 2);
     const int co = blockIdx.y * LP + li;
     const bool row_ok = pos_ok && co < g.C_out;
     const int HoWo = g.Ho * g.Wo;
@@ -905,7 +914,7 @@ __global__ __launch_bounds__(256) void conv_fwd_list_kernel(LifConst C, ConvGeom
     int drow = 0, dwb = 0;
     float2 dlr = make_float2(0.f, 0.f);
     if constexpr (kDirect) {
-        int *hist = list_lds + (blockDim.x >> 6) * 3 * EW + wave * kWave;  // [NP][LP] row counts
+        int *hist = list_lds + (blockDim.x >> 6) * WI + wave * kWave;  // [NP][LP] row counts
         hist[lane] = 0;
         __builtin_amdgcn_wave_barrier();
         if (pos_ok && li < E) {
@@ -920,7 +929,7 @@ __global__ __launch_bounds__(256) void conv_fwd_list_kernel(LifConst C, ConvGeom
                 if (e.row >= 0) {
                     dhas = true;
                     drow = e.row;
-                    dwb = (k * g.C_in + ci) * g.C_out * static_cast<int>(sizeof(float));
+                    dwb = k * g.C_in + ci;  // weight row
                     dlr = make_float2(e.L, e.R);
                     atomicAdd(&hist[hb + e.row], 1);
                 }
@@ -989,7 +998,7 @@ __global__ __launch_bounds__(256) void conv_fwd_list_kernel(LifConst C, ConvGeom
         const int rs = __shfl(start, hb + (dhas ? drow : 0));
         if (dhas) {
             const int at = ebase + rs + __popcll(eq & below);
-            ewb[at] = dwb;
+            erow[at] = static_cast<uint16_t>(dwb);
             eLR[at] = dlr;
         }
     } else
@@ -1027,7 +1036,7 @@ __global__ __launch_bounds__(256) void conv_fwd_list_kernel(LifConst C, ConvGeom
                     wof = wofs[ky];
                 }
             }
-            ewb[ebase + v] = min(max(cs.key[gi] + wof, 0), wlim) * rstride;
+            erow[ebase + v] = static_cast<uint16_t>(min(max(cs.key[gi] + wof, 0), wlim));
             eLR[ebase + v] = make_float2(cs.L[gi], cs.R[gi]);
         }
     }
@@ -1067,14 +1076,14 @@ __global__ __launch_bounds__(256) void conv_fwd_list_kernel(LifConst C, ConvGeom
             // count
             int i0 = 0;
             for (; i0 + 8 <= nmin; i0 += 8)
-                list_batch<8, true>(ewb, eLR, my_s + i0, my_n - i0, wr, voff, aL, aR);
+                list_batch<8, true>(erow, eLR, my_s + i0, my_n - i0, wr, voff, rstride, aL, aR);
             for (; i0 + 8 <= n; i0 += 8)
-                list_batch<8>(ewb, eLR, my_s + i0, my_n - i0, wr, voff, aL, aR);
+                list_batch<8>(erow, eLR, my_s + i0, my_n - i0, wr, voff, rstride, aL, aR);
             if (i0 + 4 <= n) {
-                list_batch<4>(ewb, eLR, my_s + i0, my_n - i0, wr, voff, aL, aR);
+                list_batch<4>(erow, eLR, my_s + i0, my_n - i0, wr, voff, rstride, aL, aR);
                 i0 += 4;
             }
-            for (; i0 < n; ++i0) list_batch<1>(ewb, eLR, my_s + i0, my_n - i0, wr, voff, aL, aR);
+            for (; i0 < n; ++i0) list_batch<1>(erow, eLR, my_s + i0, my_n - i0, wr, voff, rstride, aL, aR);
         } else if (r == r_last + 2) {
             // every record is in: grid points r-1 .. M see no input, the rest
             // of the window is one free-decay segment
@@ -1713,7 +1722,7 @@ hipError_t launch_conv_forward(const LifConst &C, const ConvGeom &g, int64_t B, 
     ProfScope prof("conv_fwd", st);
     if (np > 0) {
         const size_t lds =
-            static_cast<size_t>(waves) * (3 * ((np * g.KH * g.KW * g.PC + 1) & ~1) + (direct ? kWave : 0)) *
+            static_cast<size_t>(waves) * (list_wave_ints(np * g.KH * g.KW * g.PC) + (direct ? kWave : 0)) *
             sizeof(int);
         dim3 lgrid(static_cast<unsigned>((n_pos + np * waves - 1) / (np * waves)));
 #define CFL(KHV, KSV, DV)                                                                         \

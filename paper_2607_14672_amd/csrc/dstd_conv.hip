@@ -450,11 +450,15 @@ struct FwdEntry { int wb, row; float L, R; };
 // outputs together, as runs of kFwdWaves consecutive positions per channel,
 // instead of 64 single floats 4 * Ho * Wo bytes apart per position (such
 // scattered stores bound the forward of layers without input events).
-// (At most 80 VGPRs: six waves per SIMD, measured faster than five; eight
-// would spill.)
+// (At most 72 VGPRs, seven waves per SIMD, where that needs no spill: conv9
+// 0.819 -> 0.795 ms against six; else at most 80. Eight would spill.)
 constexpr int kFwdWaves = 4;
 template <int KHT, int KS, bool kDirect>
-__global__ __launch_bounds__(kFwdWaves * kWave) __attribute__((amdgpu_waves_per_eu(6, 8))) void conv_fwd_kernel(LifConst C, ConvGeom g, int64_t n_pos,
+constexpr int fwd_min_waves() {
+    return (KHT <= 3 && (kDirect || KS != kAnyKind)) ? 7 : 6;
+}
+template <int KHT, int KS, bool kDirect>
+__global__ __launch_bounds__(kFwdWaves * kWave) __attribute__((amdgpu_waves_per_eu(fwd_min_waves<KHT, KS, kDirect>(), 8))) void conv_fwd_kernel(LifConst C, ConvGeom g, int64_t n_pos,
                                                        const float *__restrict__ Wt,
                                                        ConvSorted cs, const float *__restrict__ t_in,
                                                        float *__restrict__ t_out,

@@ -309,17 +309,22 @@ def layer_desc(lay):
     return f"{lay.n_in}->{lay.n_out} M={lay.M}"
 
 
-def kernel_algorithmic_flops(net, act, with_scan=True):
+def kernel_algorithmic_flops(net, act, with_scan=True, fused_dwdt=False):
     """Algorithmic flops of one step, per kernel name (2-sparse events:
     FLOPS_PER_UPDATE per (sample, input with events, neuron)); the forward
     kernels, which run the interval scan of their neurons too, also count
-    FLOPS_PER_SCAN_STEP per (neuron, grid point) when with_scan."""
+    FLOPS_PER_SCAN_STEP per (neuron, grid point) when with_scan. With
+    fused_dwdt, the conv layers that compute dt_in ran dW and the dt_in
+    partials in one launch (conv_dwdt)."""
     fl = {k: 0.0 for k in ("fwd_dense", "dw_dense", "dtin_rows", "conv_fwd", "conv_dw",
-                           "conv_dtp", "fwd_mfma")}
+                           "conv_dtp", "conv_dwdt", "fwd_mfma")}
     for l, (e, a) in enumerate(zip(net.L, act)):
         upd = a["updates"]
-        fwd, dw, dt = (("conv_fwd", "conv_dw", "conv_dtp") if e["cs"] is not None else
+        conv = e["cs"] is not None
+        fwd, dw, dt = (("conv_fwd", "conv_dw", "conv_dtp") if conv else
                        ("fwd_dense", "dw_dense", "dtin_rows"))
+        if conv and fused_dwdt and l > 0:
+            dw = dt = "conv_dwdt"
         fl[fwd] += FLOPS_PER_UPDATE * upd
         if with_scan:
             fl[fwd] += FLOPS_PER_SCAN_STEP * e["t_out"].numel() * (e["lay"].M + 1)
@@ -745,8 +750,14 @@ def measure(torch, dstd, wl, dev, steps, warmup, profile_steps, eager, contract=
     prof = dstd.profile_table()
     per_step = {k: v[1] / profile_steps for k, v in prof.items()}
     launches = {k: v[0] / profile_steps for k, v in prof.items()}
-    flops = kernel_algorithmic_flops(net, act)
-    contraction = kernel_algorithmic_flops(net, act, with_scan=False)
+    # the library runs a conv layer's dW and dt_in partials in one launch
+    # where it has that launch for the layer's shapes (every bench layer)
+    fused = "conv_dwdt" in per_step
+    if fused and "conv_dtp" in per_step:
+        raise RuntimeError("conv layers ran both fused and separate dW / dt_in launches; "
+                           "the per-kernel flop attribution assumes one form")
+    flops = kernel_algorithmic_flops(net, act, fused_dwdt=fused)
+    contraction = kernel_algorithmic_flops(net, act, with_scan=False, fused_dwdt=fused)
     if "fwd_mfma" in per_step and "fwd_dense" not in per_step:
         # the MFMA kernel only contracts; its scan runs in mfma_scan
         flops["fwd_mfma"] = contraction.pop("fwd_dense")

@@ -1255,17 +1255,17 @@ __device__ void dead_channel_block(const ConvGeom &g, int64_t B, const int *__re
 
 // dt_in partials. Wave = output position; lane = output channel, NT tiles of
 // 64 per lane. Rows stop after the last grid point any channel's G reaches.
+// A block of 256 threads takes positions 4 * bx .. 4 * bx + 3.
 template <int KHT, int NT, int KS>
-__global__ __launch_bounds__(256) void conv_dtp_kernel(LifConst C, ConvGeom g, int64_t n_pos,
-                                                       const float *__restrict__ Wt,
-                                                       ConvSorted cs,
-                                                       const float *__restrict__ gam,
-                                                       const float *__restrict__ uq,
-                                                       const int *__restrict__ qv,
-                                                       const int *__restrict__ rend) {
+__device__ __forceinline__ void dtp_block(const LifConst &C, const ConvGeom &g, int64_t n_pos,
+                                          const float *__restrict__ Wt, const ConvSorted &cs,
+                                          const float *__restrict__ gam,
+                                          const float *__restrict__ uq,
+                                          const int *__restrict__ qv,
+                                          const int *__restrict__ rend, int64_t bx) {
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = uniform(threadIdx.x >> 6);
-    const int64_t p = static_cast<int64_t>(blockIdx.x) * (blockDim.x >> 6) + wave;
+    const int64_t p = bx * 4 + wave;
     if (p >= n_pos) return;  // wave-uniform; no block barrier below
     const int r_end = *as_const(rend + p);  // rows r <= r_end need G[r-1], G[r]
     if (r_end < 0) return;                  // no channel here passes gradient
@@ -1335,6 +1335,17 @@ __global__ __launch_bounds__(256) void conv_dtp_kernel(LifConst C, ConvGeom g, i
             gB[t] = g_at<KS>(C, gm[t], ua[t], qa[t], r + 1);
         }
     }
+}
+
+template <int KHT, int NT, int KS>
+__global__ __launch_bounds__(256) void conv_dtp_kernel(LifConst C, ConvGeom g, int64_t n_pos,
+                                                       const float *__restrict__ Wt,
+                                                       ConvSorted cs,
+                                                       const float *__restrict__ gam,
+                                                       const float *__restrict__ uq,
+                                                       const int *__restrict__ qv,
+                                                       const int *__restrict__ rend) {
+    dtp_block<KHT, NT, KS>(C, g, n_pos, Wt, cs, gam, uq, qv, rend, blockIdx.x);
 }
 
 // dt_in of the raw inputs of cell row cr, slots [s0, s0 + ns) of its
@@ -1415,29 +1426,40 @@ __device__ void dt_gather_block(const ConvGeom &g, int R, const ConvSorted &cs,
 // apart: one two-address LDS read; rows R-1 and R stay zero), the next
 // sample's values in registers (NPER per thread) during this one's sums. A
 // sample whose tile is all zero is skipped.
+// Block (bx, by, bz): inputs 256 bx .., channel tile by, batch split bz.
+// gs: the dynamic LDS ([2][R + 1][TI + 1], then the live sample list);
+// n_live_w: four ints of LDS.
+struct ConvDwArgs {
+    int64_t n_samp;
+    int s_per_split;
+    const float *gam, *uq;
+    const int *qv, *rend, *cr_live, *ev_row;
+    const float *ev_L, *ev_R;
+    float *part;
+    int *zlive;
+};
 template <int TI, int NPER, int KS>
-__global__ __launch_bounds__(256) void conv_dw_kernel(LifConst C, ConvGeom g, int64_t n_samp,
-                                                      int s_per_split,
-                                                      const float *__restrict__ gam,
-                                                      const float *__restrict__ uq,
-                                                      const int *__restrict__ qv,
-                                                      const int *__restrict__ rend,
-                                                      const int *__restrict__ cr_live,
-                                                      const int *__restrict__ ev_row,
-                                                      const float *__restrict__ ev_L,
-                                                      const float *__restrict__ ev_R,
-                                                      float *__restrict__ part,
-                                                      int *__restrict__ zlive) {
-    extern __shared__ float gs[];  // [2][R + 1][TI + 1], then the live sample list
-    __shared__ int n_live_w[4];
+__device__ __forceinline__ void dw_block(const LifConst &C, const ConvGeom &g,
+                                         const ConvDwArgs &a, int bx, int by, int bz,
+                                         float *gs, int *n_live_w) {
+    const int64_t n_samp = a.n_samp;
+    const int s_per_split = a.s_per_split;
+    const float *__restrict__ gam = a.gam;
+    const float *__restrict__ uq = a.uq;
+    const int *__restrict__ qv = a.qv;
+    const int *__restrict__ rend = a.rend;
+    const int *__restrict__ cr_live = a.cr_live;
+    const int *__restrict__ ev_row = a.ev_row;
+    const float *__restrict__ ev_L = a.ev_L;
+    const float *__restrict__ ev_R = a.ev_R;
     constexpr int kStr = TI + 1;
     const int R = rows_of(C);
     const int gbuf = (R + 1) * kStr;
     const int NJ = g.KH * g.KW * g.C_in;
-    const int jj = blockIdx.x * blockDim.x + threadIdx.x;
-    const int co0 = blockIdx.y * TI;
+    const int jj = bx * 256 + threadIdx.x;
+    const int co0 = by * TI;
     const int ni = min(TI, g.C_out - co0);
-    const int64_t s_lo = static_cast<int64_t>(blockIdx.z) * s_per_split;
+    const int64_t s_lo = static_cast<int64_t>(bz) * s_per_split;
     const int64_t s_hi = min(n_samp, s_lo + s_per_split);
     const bool j_ok = jj < NJ;
     const int k = (j_ok ? jj : 0) / g.C_in, ci = (j_ok ? jj : 0) % g.C_in;
@@ -1475,7 +1497,7 @@ __global__ __launch_bounds__(256) void conv_dw_kernel(LifConst C, ConvGeom g, in
             }
         }
     };
-    for (int t = threadIdx.x; t < 2 * 2 * kStr; t += blockDim.x)
+    for (int t = threadIdx.x; t < 2 * 2 * kStr; t += 256)
         gs[(t / (2 * kStr)) * gbuf + (R - 1) * kStr + t % (2 * kStr)] = 0.f;
     // the split's samples through which any gradient flows, in order
     int *list = reinterpret_cast<int *>(gs + 2 * gbuf);
@@ -1495,7 +1517,7 @@ __global__ __launch_bounds__(256) void conv_dw_kernel(LifConst C, ConvGeom g, in
         __syncthreads();
     }
     // a split without such samples writes no partials (the reduction skips it)
-    if (threadIdx.x == 0 && blockIdx.x == 0 && blockIdx.y == 0) zlive[blockIdx.z] = n_live > 0;
+    if (threadIdx.x == 0 && bx == 0 && by == 0) a.zlive[bz] = n_live > 0;
     if (n_live == 0) return;
     bool live = false;  // the staged sample's tile has a nonzero value
     {
@@ -1533,10 +1555,37 @@ __global__ __launch_bounds__(256) void conv_dw_kernel(LifConst C, ConvGeom g, in
         live = __syncthreads_or(live_next);
     }
     if (!j_ok) return;
-    float *out = part + (static_cast<int64_t>(blockIdx.z) * g.C_out + co0) * NJ + jj;
+    float *out = a.part + (static_cast<int64_t>(bz) * g.C_out + co0) * NJ + jj;
 #pragma unroll
     for (int ii = 0; ii < TI; ++ii)
         if (ii < ni) out[static_cast<int64_t>(ii) * NJ] = acc[ii];
+}
+
+template <int TI, int NPER, int KS>
+__global__ __launch_bounds__(256) void conv_dw_kernel(LifConst C, ConvGeom g, ConvDwArgs a) {
+    extern __shared__ float gs[];
+    __shared__ int n_live_w[4];
+    dw_block<TI, NPER, KS>(C, g, a, blockIdx.x, blockIdx.y, blockIdx.z, gs, n_live_w);
+}
+
+// dW blocks (nbx * nby * nbz of them, x fastest) and then the dt_in partial
+// blocks of the same layer in one launch: the two read the same gradient
+// triples and write disjoint buffers, so they need no order between them.
+template <int TI, int NPER, int KHT, int NT, int KS>
+__global__ __launch_bounds__(256) void conv_dwdt_kernel(LifConst C, ConvGeom g, ConvDwArgs a,
+                                                        int nbx, int nby, int n_dw,
+                                                        int64_t n_pos,
+                                                        const float *__restrict__ Wt,
+                                                        ConvSorted cs) {
+    extern __shared__ float gs[];
+    __shared__ int n_live_w[4];
+    const int id = blockIdx.x;
+    if (id < n_dw) {
+        const int bx = id % nbx, t = id / nbx;
+        dw_block<TI, NPER, KS>(C, g, a, bx, t % nby, t / nby, gs, n_live_w);
+    } else {
+        dtp_block<KHT, NT, KS>(C, g, n_pos, Wt, cs, a.gam, a.uq, a.qv, a.rend, id - n_dw);
+    }
 }
 
 // dW[co, ci, ky, kx] = (1/P) sum_z part[z][co][k * C_in + ci]. Threads follow
@@ -1851,19 +1900,56 @@ hipError_t launch_conv_backward(const LifConst &C, const ConvGeom &g, int64_t B,
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     ConvDwPlan p{};
+    ConvDwArgs da{n_pos, 0, ws.gam, ws.uq, ws.q, ws.rend, ws.crlive, ws.row, ws.L, ws.R,
+                  ws.part, ws.zlive};
+    dim3 dw_grid(1, 1, 1);
+    size_t dw_lds = 0;
+    int nper = 0;
     if (grad_W) {
         p = plan_conv_dw(g, B, C.M);
-        dim3 grid(static_cast<unsigned>((nj + 255) / 256),
-                  static_cast<unsigned>((g.C_out + p.ti - 1) / p.ti),
-                  static_cast<unsigned>(p.nsplit));
-        const size_t lds = 2 * static_cast<size_t>(R + 1) * (p.ti + 1) * sizeof(float) +
-                           static_cast<size_t>(p.s_per_split) * sizeof(int);
-        const int nper = conv_dw_nper(C.M, p.ti);
+        da.s_per_split = p.s_per_split;
+        dw_grid = dim3(static_cast<unsigned>((nj + 255) / 256),
+                       static_cast<unsigned>((g.C_out + p.ti - 1) / p.ti),
+                       static_cast<unsigned>(p.nsplit));
+        dw_lds = 2 * static_cast<size_t>(R + 1) * (p.ti + 1) * sizeof(float) +
+                 static_cast<size_t>(p.s_per_split) * sizeof(int);
+        nper = conv_dw_nper(C.M, p.ti);
+    }
+    const bool dtl = dt && n_pos > 0;
+    constexpr int kDtWaves = 4;  // dt_in partial blocks: four positions each
+    const int64_t n_dtp = dtl ? (n_pos + kDtWaves - 1) / kDtWaves : 0;
+    const int nt = (g.C_out + kWave - 1) / kWave;
+    const int nt_k = nt == 1 ? 1 : nt == 2 ? 2 : nt <= 4 ? 4 : 8;
+    const int kh_k = g.KH == 1 ? 1 : g.KH <= 3 ? 3 : kConvMaxK;
+    // dW and the dt_in partials in one launch where both run (general
+    // kernel row, the tile shapes instantiated below); else one launch each
+    bool fused = false;
+    if (grad_W && dtl && C.kind == kGeneral) {
+        const int64_t n_dw = static_cast<int64_t>(dw_grid.x) * dw_grid.y * dw_grid.z;
+        if (n_dw + n_dtp < (int64_t{1} << 31)) {
+            const dim3 grid(static_cast<unsigned>(n_dw + n_dtp));
+            const int nbx = static_cast<int>(dw_grid.x), nby = static_cast<int>(dw_grid.y);
+            ProfScope prof("conv_dwdt", st);
+#define DWDT(TIV, NPV, KHV, NTV)                                                                \
+    if (!fused && p.ti == TIV && nper == NPV && kh_k == KHV && nt_k == NTV) {                   \
+        hipLaunchKernelGGL((conv_dwdt_kernel<TIV, NPV, KHV, NTV, kGeneral>), grid, dim3(256),   \
+                           dw_lds, st, C, g, da, nbx, nby, static_cast<int>(n_dw), n_pos, ws.wt, \
+                           ws.srt);                                                             \
+        fused = true;                                                                           \
+    }
+            DWDT(32, 5, 1, 1) DWDT(32, 5, 3, 1)
+            DWDT(64, 5, 1, 1) DWDT(64, 5, 1, 2) DWDT(64, 5, 1, 4)
+            DWDT(64, 5, 3, 1) DWDT(64, 5, 3, 2) DWDT(64, 5, 3, 4)
+            DWDT(64, 9, 1, 1) DWDT(64, 9, 1, 2) DWDT(64, 9, 1, 4)
+            DWDT(64, 9, 3, 1) DWDT(64, 9, 3, 2) DWDT(64, 9, 3, 4)
+#undef DWDT
+            if ((e = hipGetLastError()) != hipSuccess) return e;
+        }
+    }
+    if (grad_W && !fused) {
         ProfScope prof("conv_dw", st);
-#define CDW_LAUNCH_K(TIV, NP, KSV)                                                            \
-    hipLaunchKernelGGL((conv_dw_kernel<TIV, NP, KSV>), grid, dim3(256), lds, st, C, g, n_pos,  \
-                       p.s_per_split, ws.gam, ws.uq, ws.q, ws.rend, ws.crlive, ws.row, ws.L,  \
-                       ws.R, ws.part, ws.zlive)
+#define CDW_LAUNCH_K(TIV, NP, KSV) \
+    hipLaunchKernelGGL((conv_dw_kernel<TIV, NP, KSV>), dw_grid, dim3(256), dw_lds, st, C, g, da)
 #define CDW_LAUNCH(TIV, NP)                                               \
     do {                                                                  \
         if (C.kind == kGeneral) CDW_LAUNCH_K(TIV, NP, kGeneral);          \
@@ -1884,14 +1970,12 @@ hipError_t launch_conv_backward(const LifConst &C, const ConvGeom &g, int64_t B,
 #undef CDW_LAUNCH_K
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
-    if (dt && n_pos > 0) {
-        constexpr int waves = 4;
-        dim3 grid(static_cast<unsigned>((n_pos + waves - 1) / waves));
-        const int nt = (g.C_out + kWave - 1) / kWave;
+    if (dtl && !fused) {
+        dim3 grid(static_cast<unsigned>(n_dtp));
         ProfScope prof("conv_dtp", st);
 #define DTP_LAUNCH_K(KHV, NTV, KSV)                                                           \
-    hipLaunchKernelGGL((conv_dtp_kernel<KHV, NTV, KSV>), grid, dim3(waves * kWave), 0, st, C,  \
-                       g, n_pos, ws.wt, ws.srt, ws.gam, ws.uq, ws.q, ws.rend)
+    hipLaunchKernelGGL((conv_dtp_kernel<KHV, NTV, KSV>), grid, dim3(kDtWaves * kWave), 0, st,  \
+                       C, g, n_pos, ws.wt, ws.srt, ws.gam, ws.uq, ws.q, ws.rend)
 #define DTP_LAUNCH(KHV, NTV)                                              \
     do {                                                                  \
         if (C.kind == kGeneral) DTP_LAUNCH_K(KHV, NTV, kGeneral);         \
@@ -1899,13 +1983,13 @@ hipError_t launch_conv_backward(const LifConst &C, const ConvGeom &g, int64_t B,
     } while (0)
 #define DTP_NT(KHV)                               \
     do {                                          \
-        if (nt == 1) DTP_LAUNCH(KHV, 1);          \
-        else if (nt == 2) DTP_LAUNCH(KHV, 2);     \
-        else if (nt <= 4) DTP_LAUNCH(KHV, 4);     \
+        if (nt_k == 1) DTP_LAUNCH(KHV, 1);        \
+        else if (nt_k == 2) DTP_LAUNCH(KHV, 2);   \
+        else if (nt_k == 4) DTP_LAUNCH(KHV, 4);   \
         else DTP_LAUNCH(KHV, 8);                  \
     } while (0)
-        if (g.KH == 1) DTP_NT(1);
-        else if (g.KH <= 3) DTP_NT(3);
+        if (kh_k == 1) DTP_NT(1);
+        else if (kh_k == 3) DTP_NT(3);
         else DTP_NT(kConvMaxK);
 #undef DTP_NT
 #undef DTP_LAUNCH

@@ -244,9 +244,12 @@ __device__ void sort_cell_row(const LifConst &C, const ConvGeom &g, const float 
                 e = bin_event(C, t_at(px, j));
                 const int64_t k = rb + static_cast<int64_t>(px) * g.PC + j;
                 if (ev.row) {
+                    // (L, R) are read only where the row is >= 0
                     ev.row[k] = e.row;
-                    ev.L[k] = e.L;
-                    ev.R[k] = e.R;
+                    if (e.row >= 0) {
+                        ev.L[k] = e.L;
+                        ev.R[k] = e.R;
+                    }
                 }
                 if (e.row >= 0) f = e.row * g.Wp + px;
             }
@@ -295,8 +298,10 @@ __device__ void events_cell_row(const LifConst &C, const ConvGeom &g,
         const int64_t src = cell_row_input(g, b, py, t, slot);
         const Event e = bin_event(C, t_in[src]);
         ev.row[rb + slot] = e.row;
-        ev.L[rb + slot] = e.L;
-        ev.R[rb + slot] = e.R;
+        if (e.row >= 0) {  // (L, R) are read only where the row is >= 0
+            ev.L[rb + slot] = e.L;
+            ev.R[rb + slot] = e.R;
+        }
         has = has || e.row >= 0;
     }
     has = __syncthreads_or(has);

@@ -119,7 +119,8 @@ struct CellEv { int *row; float *L, *R; int *live; };
 
 struct ConvBwdWs {
     int *row;
-    float *L, *R;            // cell-major events (dW), for cell rows with events
+    float *L, *R;            // cell-major events (dW), for cell rows with events; L, R
+                             //   hold values only where row >= 0
     int *crlive;             // [B][Hp]: the cell row has an input with events
     float *gam, *uq;         // per output neuron, [B][Ho*Wo][C_out]: -g/slope, t - T_q
     int *q;                  //   and its interval (-1: no gradient flows)

@@ -289,6 +289,8 @@ dstd_status check_conv(const dstd_conv_shape *cs, int64_t B, int M, dstd::ConvGe
     G.dv_pch = dstd::fast_div((uint32_t)(G.Wp * G.P));
     G.dv_w = dstd::fast_div((uint32_t)G.W);
     G.dv_cin = dstd::fast_div((uint32_t)G.C_in);
+    G.dv_p = dstd::fast_div((uint32_t)G.P);
+    G.dv_kw = dstd::fast_div((uint32_t)G.KW);
     return DSTD_OK;
 }
 

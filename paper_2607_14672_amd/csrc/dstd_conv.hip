@@ -51,6 +51,51 @@ __device__ __forceinline__ int64_t nchw_index(const ConvGeom &g, int b, int ci, 
     return ((static_cast<int64_t>(b) * g.C_in + ci) * g.H + y) * g.W + x;
 }
 
+// Raw input v = ((ky * KW + kx) * P + d) * C_in + ci (v < 64) of the
+// receptive field of an output position of image b whose window starts at
+// cell row py0 = oy * stride - pad and cell column x0: its NCHW index, or -1
+// where the cell lies in the padding; wrow = its weight row k * C_in + ci.
+__device__ __forceinline__ int64_t rf_input(const ConvGeom &g, int b, int py0, int x0, int v,
+                                            int &wrow) {
+    const int t1 = fdiv(v, g.dv_cin), ci = v - t1 * g.C_in;
+    const int k = fdiv(t1, g.dv_p), d = t1 - k * g.P;
+    const int ky = fdiv(k, g.dv_kw), kx = k - ky * g.KW;
+    const int py = py0 + ky, px = x0 + kx;
+    wrow = k * g.C_in + ci;
+    if (py < 0 || py >= g.Hp || px < 0 || px >= g.Wp) return -1;
+    int y, x;
+    raw_pixel(g, py, px, d, y, x);
+    return nchw_index(g, b, ci, y, x);
+}
+
+// Events of the raw inputs [1024 blk, 1024 blk + 1024) in NCHW order (layers
+// whose forward bins its receptive fields directly, plain input): key = event
+// row (-1: none), L, R where the row is >= 0. Every position that reads an
+// input then loads its event instead of binning it again.
+constexpr int kBinPerBlock = 1024;
+__device__ void bin_block(const LifConst &C, int64_t n_in, const float *__restrict__ t_in,
+                          const ConvSorted &cs, int blk) {
+    const int64_t i0 = static_cast<int64_t>(blk) * kBinPerBlock + threadIdx.x;
+    float v[kBinPerBlock / 256];
+#pragma unroll
+    for (int u = 0; u < kBinPerBlock / 256; ++u) {
+        const int64_t i = i0 + u * 256;
+        v[u] = (i < n_in) ? t_in[i] : INFINITY;
+    }
+#pragma unroll
+    for (int u = 0; u < kBinPerBlock / 256; ++u) {
+        const int64_t i = i0 + u * 256;
+        if (i < n_in) {
+            const Event e = bin_event(C, v[u]);
+            cs.key[i] = e.row;
+            if (e.row >= 0) {
+                cs.L[i] = e.L;
+                cs.R[i] = e.R;
+            }
+        }
+    }
+}
+
 // The t-th raw input of cell row (b, py) in NCHW order (channel-major, so
 // consecutive t are mostly consecutive addresses): its NCHW index, and its
 // cell-major slot px * PC + j' in `slot`.
@@ -468,7 +513,7 @@ __global__ __launch_bounds__(kFwdWaves * kWave) __attribute__((amdgpu_waves_per_
                                                        ConvSorted cs, const float *__restrict__ t_in,
                                                        float *__restrict__ t_out,
                                                        float *__restrict__ slope,
-                                                       int *__restrict__ q_idx) {
+                                                       int *__restrict__ q_idx, int pre) {
     // a wave's list, padded so that a batch starting at any entry stays inside
     __shared__ FwdEntry ent[kFwdWaves][kWave + kCBatch];
     const int lane = threadIdx.x & (kWave - 1);
@@ -581,18 +626,23 @@ __global__ __launch_bounds__(kFwdWaves * kWave) __attribute__((amdgpu_waves_per_
         bool has = false;
         FwdEntry me{0, -1, 0.f, 0.f};
         if (lane < F) {
-            const int ci = lane % g.C_in, t1 = lane / g.C_in;
-            const int d = t1 % g.P, k = t1 / g.P;
-            const int ky = k / g.KW, kx = k % g.KW;
-            const int oy = wk.pos / g.Wo;
-            const int py = oy * g.stride - g.pad + ky, px = wk.x0 + kx;
-            if (py >= 0 && py < g.Hp && px >= 0 && px < g.Wp) {
-                int y, x;
-                raw_pixel(g, py, px, d, y, x);
-                const Event e = bin_event<KS>(C, t_in[nchw_index(g, wk.b, ci, y, x)]);
-                if (e.row >= 0) {
-                    has = true;
-                    me = FwdEntry{(k * g.C_in + ci) * rstride, e.row, e.L, e.R};
+            int wrow;
+            const int64_t src = rf_input(g, wk.b, (wk.pos / g.Wo) * g.stride - g.pad, wk.x0,
+                                         lane, wrow);
+            if (src >= 0) {
+                if (pre) {  // binned once per input by the set-up launch
+                    const int r = cs.key[src];
+                    const float Lv = cs.L[src], Rv = cs.R[src];
+                    if (r >= 0) {
+                        has = true;
+                        me = FwdEntry{wrow * rstride, r, Lv, Rv};
+                    }
+                } else {
+                    const Event e = bin_event<KS>(C, t_in[src]);
+                    if (e.row >= 0) {
+                        has = true;
+                        me = FwdEntry{wrow * rstride, e.row, e.L, e.R};
+                    }
                 }
             }
         }
@@ -838,7 +888,7 @@ __global__ __launch_bounds__(256) void conv_fwd_list_kernel(LifConst C, ConvGeom
                                                             const float *__restrict__ t_in,
                                                             float *__restrict__ t_out,
                                                             float *__restrict__ slope,
-                                                            int *__restrict__ q_idx) {
+                                                            int *__restrict__ q_idx, int pre) {
     constexpr int LP = kWave / NP;
     extern __shared__ int list_lds[];  // per wave: weight rows [NP][E] (16-bit), then (L, R)[NP][E]
     const int lane = threadIdx.x & (kWave - 1);
@@ -927,20 +977,27 @@ __global__ __launch_bounds__(256) void conv_fwd_list_kernel(LifConst C, ConvGeom
         hist[lane] = 0;
         __builtin_amdgcn_wave_barrier();
         if (pos_ok && li < E) {
-            const int ci = li % g.C_in, t1 = li / g.C_in;
-            const int d = t1 % g.P, k = t1 / g.P;
-            const int ky = k / g.KW, kx = k % g.KW;
-            const int py = oy * g.stride - g.pad + ky, px = x0 + kx;
-            if (py >= 0 && py < g.Hp && px >= 0 && px < g.Wp) {
-                int y, x;
-                raw_pixel(g, py, px, d, y, x);
-                const Event e = bin_event<KS>(C, t_in[nchw_index(g, b, ci, y, x)]);
-                if (e.row >= 0) {
+            int wrow;
+            const int64_t src = rf_input(g, b, oy * g.stride - g.pad, x0, li, wrow);
+            if (src >= 0) {
+                int r;
+                float Lv, Rv;
+                if (pre) {  // binned once per input by the set-up launch
+                    r = cs.key[src];
+                    Lv = cs.L[src];
+                    Rv = cs.R[src];
+                } else {
+                    const Event e = bin_event<KS>(C, t_in[src]);
+                    r = e.row;
+                    Lv = e.L;
+                    Rv = e.R;
+                }
+                if (r >= 0) {
                     dhas = true;
-                    drow = e.row;
-                    dwb = k * g.C_in + ci;  // weight row
-                    dlr = make_float2(e.L, e.R);
-                    atomicAdd(&hist[hb + e.row], 1);
+                    drow = r;
+                    dwb = wrow;  // weight row
+                    dlr = make_float2(Lv, Rv);
+                    atomicAdd(&hist[hb + r], 1);
                 }
             }
         }
@@ -1661,6 +1718,7 @@ __device__ void dw_reduce_block(const ConvGeom &g, int nsplit, const float *__re
 // the cell-major events for the backward too), the rest lay out WT.
 template <typename WT>
 __global__ __launch_bounds__(256) void conv_fprep_kernel(LifConst C, ConvGeom g, int n_sort,
+                                                         int n_bin, int64_t n_in,
                                                          const float *__restrict__ t_in,
                                                          ConvSorted cs, CellEv ev,
                                                          const WT *__restrict__ W,
@@ -1669,8 +1727,10 @@ __global__ __launch_bounds__(256) void conv_fprep_kernel(LifConst C, ConvGeom g,
     const int blk = static_cast<int>(blockIdx.x);
     if (blk < n_sort)
         sort_cell_row(C, g, t_in, cs, ev, blk, sh);
+    else if (blk < n_sort + n_bin)
+        bin_block(C, n_in, t_in, cs, blk - n_sort);
     else
-        weights_block<WT>(g, W, Wt, blk - n_sort, reinterpret_cast<float (*)[33]>(sh));
+        weights_block<WT>(g, W, Wt, blk - n_sort - n_bin, reinterpret_cast<float (*)[33]>(sh));
 }
 
 // Backward set-up: [0, n_cr) cell rows (events for dW; with cs.key set also
@@ -1762,16 +1822,22 @@ hipError_t launch_conv_forward(const LifConst &C, const ConvGeom &g, int64_t B, 
     // the direct walk bins its inputs itself: no cell-row sort, unless the
     // sort is kept for the backward
     const int n_sort = (direct && !keep) ? 0 : static_cast<int>(B * g.Hp);
+    // without the sort, a direct layer on plain input has its raw inputs
+    // binned once here, in NCHW order, in the sort's key/L/R arrays (as many
+    // slots as raw inputs), and its positions load those events
+    const int64_t n_in = B * g.C_in * g.H * g.W;
+    const int pre = (direct && !keep && g.pool == 1) ? 1 : 0;
+    const int n_bin = pre ? static_cast<int>((n_in + kBinPerBlock - 1) / kBinPerBlock) : 0;
     {
         ProfScope prof("conv_fprep", st);
-        const unsigned blocks = static_cast<unsigned>(n_sort + weight_tiles(g));
+        const unsigned blocks = static_cast<unsigned>(n_sort + n_bin + weight_tiles(g));
         const int lds = std::max(n_sort > 0 ? conv_sort_lds_bytes(C.M, g) : 0, kWtLdsBytes);
         if (bf16)
             hipLaunchKernelGGL(conv_fprep_kernel<uint16_t>, dim3(blocks), dim3(256), lds, st, C, g,
-                               n_sort, t_in, cs, ev, static_cast<const uint16_t *>(W), Wt);
+                               n_sort, n_bin, n_in, t_in, cs, ev, static_cast<const uint16_t *>(W), Wt);
         else
             hipLaunchKernelGGL(conv_fprep_kernel<float>, dim3(blocks), dim3(256), lds, st, C, g,
-                               n_sort, t_in, cs, ev, static_cast<const float *>(W), Wt);
+                               n_sort, n_bin, n_in, t_in, cs, ev, static_cast<const float *>(W), Wt);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
@@ -1785,7 +1851,7 @@ hipError_t launch_conv_forward(const LifConst &C, const ConvGeom &g, int64_t B, 
         dim3 lgrid(static_cast<unsigned>((n_pos + np * waves - 1) / (np * waves)));
 #define CFL(KHV, KSV, DV)                                                                         \
     hipLaunchKernelGGL((conv_fwd_list_kernel<KHV, KSV, 2, DV>), lgrid, dim3(waves * kWave), lds,  \
-                       st, C, g, n_pos, Wt, cs, t_in, t_out, slope, q_idx)
+                       st, C, g, n_pos, Wt, cs, t_in, t_out, slope, q_idx, pre)
 #define CFL_D(KHV, KSV)                                                   \
     do {                                                                  \
         if (direct) CFL(KHV, KSV, true);                                  \
@@ -1808,7 +1874,7 @@ hipError_t launch_conv_forward(const LifConst &C, const ConvGeom &g, int64_t B, 
               static_cast<unsigned>((g.C_out + kWave - 1) / kWave));
 #define CFW(KHV, KSV, DV)                                                                        \
     hipLaunchKernelGGL((conv_fwd_kernel<KHV, KSV, DV>), grid, dim3(kFwdWaves * kWave), 0, st, C, \
-                       g, n_pos, Wt, cs, t_in, t_out, slope, q_idx)
+                       g, n_pos, Wt, cs, t_in, t_out, slope, q_idx, pre)
 #define CFW_D(KHV, KSV)                                                   \
     do {                                                                  \
         if (direct) CFW(KHV, KSV, true);                                  \

@@ -291,6 +291,7 @@ dstd_status check_conv(const dstd_conv_shape *cs, int64_t B, int M, dstd::ConvGe
     G.dv_cin = dstd::fast_div((uint32_t)G.C_in);
     G.dv_p = dstd::fast_div((uint32_t)G.P);
     G.dv_kw = dstd::fast_div((uint32_t)G.KW);
+    G.dv_pc = dstd::fast_div((uint32_t)G.PC);
     return DSTD_OK;
 }
 

@@ -139,6 +139,16 @@ __host__ __device__ __forceinline__ int sort_stage_floats(int M, const ConvGeom 
     return ((M + 3) * g.Wp + 256 + per) * 4 <= 64 * 1024 ? per : 0;
 }
 
+// With the row staged: ints of the four waves' lists of event inputs (each
+// wave owns the cell columns px = wave mod 4, at most ceil(Wp / 4) * PC
+// inputs), or 0 where they do not fit beside the staging in 64 KB.
+constexpr int kSortWaves = 4;  // the sort runs in blocks of 256 threads
+__host__ __device__ __forceinline__ int sort_list_ints(int M, const ConvGeom &g) {
+    const int stage = sort_stage_floats(M, g);
+    const int cap = (g.Wp + kSortWaves - 1) / kSortWaves * g.PC * kSortWaves;
+    return (stage > 0 && ((M + 3) * g.Wp + 256 + stage + cap) * 4 <= 64 * 1024) ? cap : 0;
+}
+
 __device__ void sort_cell_row(const LifConst &C, const ConvGeom &g, const float *__restrict__ t_in,
                               const ConvSorted &cs, const CellEv &ev, int cr, int *sh) {
     const int R = rows_of(C);
@@ -201,18 +211,36 @@ __device__ void sort_cell_row(const LifConst &C, const ConvGeom &g, const float 
     const int cpi = (g.PC < kWave) ? kWave / g.PC : 1;  // cells per pass
     const int lsub = (g.PC < kWave) ? lane / g.PC : 0;
     const int lj = (g.PC < kWave) ? lane % g.PC : lane;
+    const int64_t rb = static_cast<int64_t>(cr) * g.Wp * g.PC;
+    const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+    // List form (the row staged and the lists fitting): the histogram pass
+    // also appends each event input (slot px * PC + j, row r) to its wave's
+    // list in pass order and writes every input's event row; the placement
+    // then visits only the listed inputs. A wave's buckets (r, px) hold only
+    // its own cell columns, so list order is the pass order within each.
+    const int lcap = (tl && nw == kSortWaves) ? sort_list_ints(C.M, g) / kSortWaves : 0;
+    int *lst = lcap > 0 ? reinterpret_cast<int *>(tl + sort_stage_floats(C.M, g)) + wave * lcap
+                        : nullptr;
+    int nq = 0;
     bool has = false;
     for (int i0 = 0; wave + nw * i0 < g.Wp; i0 += cpi) {
         const int px = wave + nw * (i0 + lsub);
         const bool cell_ok = lsub < cpi && px < g.Wp;
         for (int j0 = 0; j0 < g.PC; j0 += kWave) {
             const int j = j0 + lj;
+            int r = -1;
             if (cell_ok && j < g.PC) {
-                const int r = bin_row(C, t_at(px, j));
+                r = bin_row(C, t_at(px, j));
+                if (lst && ev.row) ev.row[rb + px * g.PC + j] = r;
                 if (r >= 0) {
                     atomicAdd(&hist[r * g.Wp + px], 1);
                     has = true;
                 }
+            }
+            if (lst) {
+                const uint64_t m = __ballot(r >= 0);
+                if (r >= 0) lst[nq + __popcll(m & below)] = ((px * g.PC + j) << 9) | r;
+                nq += __popcll(m);
             }
         }
     }
@@ -275,8 +303,55 @@ __device__ void sort_cell_row(const LifConst &C, const ConvGeom &g, const float 
     // a per-pass bucket key k = row * cpi + lsub (one ballot per bit, a cost
     // independent of how many buckets the pass touches); the highest lane of
     // each group then moves the bucket's next free slot.
-    const int64_t rb = static_cast<int64_t>(cr) * g.Wp * g.PC;
-    const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+    if (lst) {
+        // list form: 64 listed inputs per pass, key row * ncw + px / 4
+        // (ncw = the wave's cell columns); entries are in pass order, so each
+        // bucket's records keep the input order
+        const int ncw = (g.Wp + kSortWaves - 1) / kSortWaves;
+        const int kb2 = uniform(R * ncw > 1 ? 32 - __clz(R * ncw - 1) : 0);
+        for (int c0 = 0; c0 < nq; c0 += kWave) {
+            const bool ok = c0 + lane < nq;
+            const int en = ok ? lst[c0 + lane] : 0;
+            const int slot = en >> 9, r = en & 511;
+            const int px = fdiv(slot, g.dv_pc), j = slot - px * g.PC;
+            Event e{-1, 0.f, 0.f, 0.f, 0.f};
+            if (ok) e = bin_event(C, tl[slot]);  // its row is r
+            const int kb = ok ? r * ncw + px / kSortWaves : 0;
+            uint64_t same = __ballot(ok);
+            for (int bit = 0; bit < kb2; ++bit) {
+                const bool on = (kb >> bit) & 1;
+                const uint64_t bal = __ballot(on);
+                same &= on ? bal : ~bal;
+            }
+            const int f = r * g.Wp + px;
+            int pos = 0;
+            if (ok) {
+                const int base = hist[f];
+                pos = base + __popcll(same & below);
+                if ((same >> lane) == 1ull) hist[f] = base + __popcll(same);
+            }
+            __builtin_amdgcn_wave_barrier();
+            if (ok) {
+                if (ev.row) {
+                    ev.L[rb + slot] = e.L;
+                    ev.R[rb + slot] = e.R;
+                }
+                const int64_t o = rb + pos;
+                cs.key[o] = px * g.C_in + (j - fdiv(j, g.dv_cin) * g.C_in);
+                if (fwd) {
+                    cs.L[o] = e.L;
+                    cs.R[o] = e.R;
+                }
+                if (bwd) {
+                    cs.dL[o] = e.dL;
+                    cs.dR[o] = e.dR;
+                    cs.px[o] = (r << 16) | px;
+                    cs.src[o] = slot;
+                }
+            }
+        }
+        return;
+    }
     const int kbits = uniform(R * cpi > 1 ? 32 - __clz(R * cpi - 1) : 0);
     for (int i0 = 0; wave + nw * i0 < g.Wp; i0 += cpi) {
         const int px = wave + nw * (i0 + lsub);
@@ -1810,7 +1885,8 @@ int conv_fwd_list_np(int M, const ConvGeom &g) {
 }
 
 int conv_sort_lds_bytes(int M, const ConvGeom &g) {
-    return ((M + 3) * g.Wp + 256 + sort_stage_floats(M, g)) * static_cast<int>(sizeof(int));
+    return ((M + 3) * g.Wp + 256 + sort_stage_floats(M, g) + sort_list_ints(M, g)) *
+           static_cast<int>(sizeof(int));
 }
 
 hipError_t launch_conv_forward(const LifConst &C, const ConvGeom &g, int64_t B, const void *W,

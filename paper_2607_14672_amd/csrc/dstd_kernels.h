@@ -74,7 +74,7 @@ struct ConvGeom {
     int Hp, Wp, Ho, Wo, P, PC;
     float inv_P;
     FastDiv dv_pch, dv_w, dv_cin;  // by Wp * P (raw inputs per channel of a cell row), W, C_in
-    FastDiv dv_p, dv_kw;           // by P and KW (receptive-field decode)
+    FastDiv dv_p, dv_kw, dv_pc;    // by P, KW (receptive-field decode) and PC
 };
 
 inline FastDiv fast_div(uint32_t d) {

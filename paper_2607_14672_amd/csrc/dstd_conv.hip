@@ -1324,11 +1324,14 @@ __device__ void grad_block(const LifConst &C, const ConvGeom &g, int64_t n_pos, 
         int64_t o[kCh];
         int q[kCh];
         float gt[kCh];
+        // with channel tiles the pass above found whether any channel of the
+        // position passes gradient; a position without writes nothing
+        const bool live = pos_ok && (!tiles || sl[pl] >= 0);
 #pragma unroll
         for (int u = 0; u < kCh; ++u) {
             const int co = c0 + cl0 + u * cstep;
             o[u] = obase + static_cast<int64_t>(co) * HoWo;
-            q[u] = (co < g.C_out && pos_ok) ? q_idx[o[u]] : -1;
+            q[u] = (co < g.C_out && live) ? q_idx[o[u]] : -1;
         }
 #pragma unroll
         for (int u = 0; u < kCh; ++u) gt[u] = (q[u] >= 0) ? grad_t[o[u]] : 0.f;  // silent: no load

@@ -129,11 +129,13 @@ __device__ __forceinline__ int64_t cell_row_input(const ConvGeom &g, int b, int 
 // One block of 256 threads per cell row (b, py).
 // LDS: hist[r][px] (later the next free slot of bucket (r, px)), the 256
 // per-thread partial sums of the prefix scan, then (when they fit) the cell
-// row's input spike times in cell-major order, read once in NCHW order.
+// row's input spike times in cell-major order, read once in NCHW order, and
+// (when they fit too) the four waves' lists of inputs with events.
 // Wave w owns cells px = w, w + 4, ... (each bucket is ranked by one wave
 // only); where a cell has fewer than 64 inputs a wave takes several of its
 // cells per pass. Records of a bucket keep the input order (j' ascending).
-// The placement pass also writes the cell row's events (ev).
+// The cell row's events (ev) are written too: every input's row, and L, R
+// where the row is >= 0.
 __host__ __device__ __forceinline__ int sort_stage_floats(int M, const ConvGeom &g) {
     const int per = g.Wp * g.PC;
     return ((M + 3) * g.Wp + 256 + per) * 4 <= 64 * 1024 ? per : 0;
@@ -1793,7 +1795,8 @@ __device__ void dw_reduce_block(const ConvGeom &g, int nsplit, const float *__re
 // Independent per-call work shares one launch by block role (a launch costs
 // several microseconds even when its work is tiny).
 // Forward set-up: blocks [0, n_sort) sort cell rows (with ev set, keeping
-// the cell-major events for the backward too), the rest lay out WT.
+// the cell-major events for the backward too), the next n_bin bin the raw
+// inputs of a direct layer once (bin_block), the rest lay out WT.
 template <typename WT>
 __global__ __launch_bounds__(256) void conv_fprep_kernel(LifConst C, ConvGeom g, int n_sort,
                                                          int n_bin, int64_t n_in,
